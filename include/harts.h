@@ -1,0 +1,277 @@
+/*
+ * harts.h -- C ABI of libharts: tree-packed chunkwise linear attention with
+ * per-head scalar decay over prefix-compressed rollout trees, for one
+ * MI355X (gfx950) GPU.
+ *
+ * Method: HARTS (arXiv 2608.28158).  The planner is the paper's Algorithm
+ * "minimum-call" (Sec. 3.3); the device calls implement the selective
+ * chunk-state contract of eq. chunkla-interface (Sec. 3.4): one packed call
+ * per execution round, each sequence starting from its own initial state,
+ * replaying the bounded interval between its resume anchor (eq.
+ * resume-anchor) and its fork, writing outputs only for its own rows,
+ * returning its final state and the chunk-boundary states later rounds
+ * request; the backward carries gradients through those handoffs.
+ *
+ * Recurrence (per head, state S of shape [dk, dv]):
+ *     S_t = exp(g_t) S_{t-1} + k_t v_t^T,      o_t = scale * S_t^T q_t.
+ *
+ * Conventions shared by every call
+ *   - Return value: HARTS_OK (0) or a negative HARTS_E* code; the message of
+ *     the last failure on the calling thread is returned by harts_last_error().
+ *     Arguments are validated on the host before anything is enqueued: on a
+ *     validation error nothing touches the device.
+ *   - Device calls are asynchronous on the given stream (a hipStream_t passed
+ *     as void*, NULL = the default stream) and never synchronise the host.
+ *     Round-to-round dependencies are carried by stream order.
+ *   - The library never allocates device memory.  The caller owns every
+ *     device buffer; scratch space is passed as (ws, ws_bytes) sized by the
+ *     *_workspace_size queries.  Plans are library-owned host objects.
+ *   - Row layout: token-major [rows, H, d] in the plan's physical row order
+ *     (sequences in id order, each sequence's own segments contiguous).
+ *     q, k: [C, H, dk]; v, o: [C, H, dv]; g, dg: float32 [C, H].
+ *     States: float32 [., H, dk, dv], dv fastest.  Pointers 16-byte aligned.
+ *   - dtype: HARTS_F32 (q, k, v, o, dO and gradients float32) or HARTS_BF16
+ *     (those tensors bfloat16; g, states and their gradients always float32).
+ *   - Supported head shapes: dk = dv in {64, 128} for bf16, 64 for float32;
+ *     chunk size 64.  Anything else returns HARTS_EUNSUPPORTED.
+ */
+#ifndef HARTS_H_
+#define HARTS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  HARTS_OK = 0,
+  HARTS_EINVAL = -1,       /* malformed argument (forest, sizes, pointers) */
+  HARTS_EUNSUPPORTED = -2, /* valid but not implemented (dtype, head dims)  */
+  HARTS_EHIP = -3,         /* a HIP runtime call or launch failed           */
+  HARTS_ENOMEM = -4        /* host allocation failed, or a buffer too small */
+};
+
+enum { HARTS_F32 = 0, HARTS_BF16 = 1 };
+
+/* Opaque plan (host memory, owned by the library). */
+typedef struct harts_plan_s harts_plan_t;
+
+/* Thread-local message describing the last failure ("" if none). */
+const char* harts_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * harts_plan -- minimum-call planning and plan recovery (Sec. 3.3,
+ * Algorithm "minimum-call"; eqs. leaf-calls, tin, tpre, early-start,
+ * mandatory-replay).
+ *
+ *   n_seg    number of segments (fork-free token runs), >= 1.
+ *   parent   [n_seg] parent segment id, -1 for a root.  Several roots make a
+ *            forest (one microbatch); trees are ordered by root id and each
+ *            tree has its own chunk grid starting at position 0.  Children
+ *            are ordered by ascending id (the "fixed child order").
+ *   seg_len  [n_seg] tokens per segment, each > 0.
+ *   chunk    execution chunk size B >= 1 (the device calls require 64).
+ *   out      receives the plan; release it with harts_plan_free.
+ *
+ * Linear time and space in n_seg + replay length.  Errors: HARTS_EINVAL for
+ * a null pointer, n_seg < 1, chunk < 1, a parent id out of range or equal to
+ * the segment, a cycle, a length <= 0, or totals beyond int32 row indexing.
+ *
+ * Ordering conventions (the paper leaves them open): sequences are created
+ * in Recover's order -- the direct continuation is recursed into before the
+ * side children are launched, side children in child order, trees in root
+ * order -- and numbered by a stable sort of that order on the round.  A side
+ * branch that starts in the same round reuses its parent sequence's
+ * initial-state source; one that starts a round later consumes the state
+ * S_{b_v} requested from the parent's sequence.  Requested states are
+ * deduplicated and numbered by (producer sequence, boundary position).  The
+ * state bank holds the n_trees tree initial states first, then the slots.
+ * ---------------------------------------------------------------------- */
+int harts_plan(int32_t n_seg, const int32_t* parent, const int64_t* seg_len,
+               int32_t chunk, harts_plan_t** out);
+
+void harts_plan_free(harts_plan_t* plan);
+
+typedef struct harts_plan_info {
+  int32_t n_seg, n_trees, n_leaves;
+  int32_t n_rounds;   /* K: minimum number of sequential packed calls      */
+  int32_t n_seq;      /* input sequences over all rounds (= n_leaves)      */
+  int32_t n_slots;    /* requested chunk-boundary states                   */
+  int32_t n_bank;     /* n_trees + n_slots                                 */
+  int32_t chunk;
+  int64_t C;          /* compact rows (unique, non-replay)                 */
+  int64_t S;          /* semantic positions (sum of trajectory lengths)    */
+  int64_t R;          /* replay rows, eq. mandatory-replay                 */
+  int64_t n_req;      /* (sequence, boundary) requests, = n_slots          */
+  int64_t n_chunks;   /* chunks over all sequences (replay included)       */
+  int64_t blob_bytes; /* size of the device descriptor image               */
+} harts_plan_info;
+
+int harts_plan_get_info(const harts_plan_t* plan, harts_plan_info* info);
+
+/* Host arrays filled by harts_plan_export; any member may be NULL (skipped).
+ * Sizes in brackets come from harts_plan_info. */
+typedef struct harts_plan_arrays {
+  /* per segment [n_seg] */
+  int64_t* seg_start;    /* s_v: trajectory position of the first token     */
+  int64_t* seg_end;      /* e_v = s_v + len_v                                */
+  int64_t* seg_row;      /* physical row of the first token                 */
+  int32_t* seg_seq;      /* sequence that outputs the segment               */
+  int64_t* seg_mult;     /* q_v: leaves under v (eq. multiplicity)          */
+  int32_t* seg_tpre;     /* T_pre(v), eq. tpre                               */
+  int32_t* seg_tin;      /* T_in(v), eq. tin                                 */
+  int32_t* seg_tree;     /* tree (root order) of the segment                */
+  int32_t* leaf_seg;     /* [n_leaves] leaf segments by ascending id         */
+  int32_t* tree_calls;   /* [n_trees] T_pre(root) of every tree              */
+  int32_t* round_seq_off;/* [n_rounds+1] sequences of round r (0-based):
+                            [off[r], off[r+1])                              */
+  /* per sequence [n_seq] */
+  int32_t* seq_round;    /* 1-based round                                   */
+  int32_t* seq_tree;
+  int32_t* seq_first_seg;
+  int32_t* seq_final_leaf; /* index into leaf_seg / S_final                 */
+  int32_t* seq_init_bank;  /* bank entry holding the initial state          */
+  int64_t* seq_anchor;   /* start position A (a multiple of chunk)          */
+  int64_t* seq_n_replay; /* replay rows before the first own row (< chunk)  */
+  int64_t* seq_replay_off; /* [n_seq+1] offsets into replay_row             */
+  int64_t* seq_row;      /* physical row of the first own token             */
+  int64_t* seq_n_own;    /* own rows                                        */
+  int32_t* seq_chain_off;/* [n_seq+1] offsets into chain_seg                */
+  int32_t* chain_seg;    /* [n_seg] segments of every sequence, in order    */
+  int32_t* seq_req_off;  /* [n_seq+1] offsets into req_chunk / req_bank     */
+  /* requests [n_req] */
+  int32_t* req_chunk;    /* boundary c: state at the start of chunk c       */
+  int32_t* req_bank;     /* bank entry the boundary state is written to     */
+  /* slots [n_slots] */
+  int32_t* slot_seq;     /* producer sequence                               */
+  int64_t* slot_pos;     /* boundary position b_v                            */
+  /* replay [R] */
+  int64_t* replay_row;   /* physical row replayed, per sequence in order    */
+} harts_plan_arrays;
+
+int harts_plan_export(const harts_plan_t* plan, const harts_plan_arrays* dst);
+
+/* Per-round launch facts (round is 0-based, < n_rounds). */
+typedef struct harts_round_info {
+  int32_t n_seq;         /* sequences in the round                          */
+  int32_t seq_begin;     /* first sequence id of the round                  */
+  int64_t n_chunks;      /* chunks over the round's sequences               */
+  int64_t n_rows;        /* packed rows: own + replay                       */
+  int64_t n_own;         /* own rows (outputs)                              */
+  int64_t n_replay;      /* replay rows                                     */
+  int64_t own_row_begin; /* own rows of the round are contiguous from here  */
+  int64_t init_idx_off;  /* byte offset in the blob of the round's int32
+                            [n_seq] initial-state bank indices (the idx
+                            argument of harts_state_gather)                 */
+} harts_round_info;
+
+int harts_plan_round_info(const harts_plan_t* plan, int32_t round,
+                          harts_round_info* info);
+
+/* Device descriptor image (int32, blob_bytes bytes, 256-byte sections).
+ * The caller copies it to device memory once per plan (step "round
+ * descriptors to the device") and passes that copy as d_blob to the device
+ * calls below.  Errors: HARTS_ENOMEM if bytes < blob_bytes. */
+int harts_plan_blob(const harts_plan_t* plan, void* host_dst, size_t bytes);
+
+/* ------------------------------------------------------------------------
+ * harts_la_fwd -- one execution round of the packed forward (Sec. 3.4,
+ * eq. chunkla-interface; chunkwise form of Sec. 2.2).
+ *
+ * For every sequence i of the round (rows: its replay rows, gathered by
+ * index from earlier rows, then its own rows):
+ *   reads   q (own rows only), k, v, g; S0[i] = its initial state;
+ *   writes  o for its own rows only (o may be NULL: state pass only, the
+ *           recompute-forward of the backward -- states, no outputs);
+ *           bank[req] = S_c for each requested chunk boundary c;
+ *           S_final[final_leaf] = the state after its last token;
+ *           saved (if non-NULL): what harts_la_bwd needs to skip the
+ *           recompute (sized by harts_la_saved_size).
+ *   S0       [n_seq_round, H, dk, dv] float32 (harts_state_gather output).
+ *   scale    output scale (1/sqrt(dk) is the usual choice).
+ * Errors: HARTS_EINVAL (null required pointer, bad round, ws too small),
+ * HARTS_EUNSUPPORTED (dtype / dims / chunk), HARTS_EHIP (launch failed).
+ * ---------------------------------------------------------------------- */
+int harts_la_fwd(const harts_plan_t* plan, int32_t round, const void* d_blob,
+                 int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                 const void* q, const void* k, const void* v, const float* g,
+                 const float* S0, void* o, float* S_final, float* bank,
+                 void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * harts_la_bwd -- backward of one round (Sec. 3.4 "Differentiable boundary
+ * states"; "Full-layer activation recomputation").  Rounds are run in
+ * reverse: a requested state's gradient (dbank[req]) is complete once every
+ * later round that consumed it has run and scattered its dS0 (harts_state_gather
+ * mode 1).
+ *
+ *   dO        [C, H, dv] upstream gradient of o (own rows of the round read).
+ *   dS_final  [n_leaves, H, dk, dv] upstream gradient of the final states.
+ *   dbank     [n_bank, H, dk, dv] accumulated gradients of requested states.
+ *   saved     from harts_la_fwd, or NULL: the forward states are then
+ *             recomputed from S0 inside this call (recompute-forward).
+ *   dq, dk_, dv_  [C, H, d] written for the round's own rows (not added).
+ *   dg        float32 [C, H] written for own rows.
+ *   replay_grad float32 [R, H, dk + dv + 1]: per replay row (global replay
+ *             index) its dk, dv and dg contributions; reduced into the
+ *             compact rows by harts_replay_reduce after the last round.
+ *   dS0       float32 [n_seq_round, H, dk, dv]: gradient at every sequence's
+ *             initial state.
+ * Deterministic: no floating-point atomics; reruns are bitwise identical.
+ * ---------------------------------------------------------------------- */
+int harts_la_bwd(const harts_plan_t* plan, int32_t round, const void* d_blob,
+                 int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                 const void* q, const void* k, const void* v, const float* g,
+                 const float* S0, const void* dO, const float* dS_final,
+                 const float* dbank, const void* saved, void* dq, void* dk_,
+                 void* dv_, float* dg, float* replay_grad, float* dS0,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/* Bytes of device scratch for a round's forward (pass 0) or backward
+ * (pass 1; has_saved = 0 means the recompute path). */
+int harts_la_workspace_size(const harts_plan_t* plan, int32_t round,
+                            int32_t pass, int32_t dtype, int32_t H, int32_t dk,
+                            int32_t dv, int32_t has_saved, size_t* bytes);
+
+/* Bytes of the optional per-round forward save buffer. */
+int harts_la_saved_size(const harts_plan_t* plan, int32_t round,
+                        int32_t dtype, int32_t H, int32_t dk, int32_t dv,
+                        size_t* bytes);
+
+/* ------------------------------------------------------------------------
+ * harts_state_gather -- state handoff between rounds (Sec. 3.4: a later
+ * sequence starts from a boundary state returned by an earlier round; if
+ * several consumers share one boundary tensor, their gradients are summed).
+ *
+ *   mode 0 (gather):      dst[i] = idx[i] < 0 ? 0 : src[idx[i]],  i < n.
+ *   mode 1 (scatter-add): dst[idx[i]] += src[i] for i = 0..n-1 in order
+ *                         (idx[i] < 0 skipped).  The adjoint of mode 0;
+ *                         deterministic, no atomics.
+ *   src, dst  float32 device arrays of states, elems_per_state floats each
+ *             (H*dk*dv); idx is an int32 device array.
+ * Errors: HARTS_EINVAL (null pointer, n < 0, elems_per_state not a positive
+ * multiple of 4, bad mode), HARTS_EHIP.
+ * ---------------------------------------------------------------------- */
+int harts_state_gather(const float* src, const int32_t* idx, int32_t n,
+                       int64_t elems_per_state, float* dst, int32_t mode,
+                       void* stream);
+
+/* ------------------------------------------------------------------------
+ * harts_replay_reduce -- gradients of replayed rows (Sec. 4.2: replay reads
+ * existing compact activations, and the indexed-gather backward accumulates
+ * every consumer's gradient at the unique producer).  For every compact row
+ * that some sequence replays, adds the replay_grad entries of that row (in
+ * ascending replay index) to dk_, dv_ and dg.  Run once, after the backward
+ * of the last (first) round.  Deterministic.
+ * ---------------------------------------------------------------------- */
+int harts_replay_reduce(const harts_plan_t* plan, const void* d_blob,
+                        int32_t dtype, int32_t H, int32_t dk, int32_t dv,
+                        const float* replay_grad, void* dk_, void* dv_,
+                        float* dg, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HARTS_H_ */

@@ -1,0 +1,144 @@
+"""ctypes binding of libharts (declarations in include/harts.h).
+
+Argument marshalling only: every step of the path runs in the library.  The
+library is built in-tree by ``paper_2608_28158_amd.build`` and loaded from
+this package directory; a missing library is an error, never a fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("HARTS_LIB", os.path.join(HERE, "libharts.so"))
+
+HARTS_OK, HARTS_EINVAL, HARTS_EUNSUPPORTED, HARTS_EHIP, HARTS_ENOMEM = 0, -1, -2, -3, -4
+HARTS_F32, HARTS_BF16 = 0, 1
+
+# Every symbol include/harts.h declares.
+EXPORTS = (
+    "harts_last_error", "harts_plan", "harts_plan_free", "harts_plan_get_info",
+    "harts_plan_export", "harts_plan_round_info", "harts_plan_blob",
+    "harts_la_fwd", "harts_la_bwd", "harts_la_workspace_size",
+    "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
+)
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "n_seg", "n_trees", "n_leaves", "n_rounds", "n_seq", "n_slots",
+        "n_bank", "chunk")] + [(n, C.c_int64) for n in (
+        "C", "S", "R", "n_req", "n_chunks", "blob_bytes")]
+
+
+_I64, _I32 = C.POINTER(C.c_int64), C.POINTER(C.c_int32)
+# (name, ctype pointer, numpy dtype, size key) -- order as in the header
+PLAN_ARRAY_FIELDS = (
+    ("seg_start", _I64, np.int64, "n_seg"),
+    ("seg_end", _I64, np.int64, "n_seg"),
+    ("seg_row", _I64, np.int64, "n_seg"),
+    ("seg_seq", _I32, np.int32, "n_seg"),
+    ("seg_mult", _I64, np.int64, "n_seg"),
+    ("seg_tpre", _I32, np.int32, "n_seg"),
+    ("seg_tin", _I32, np.int32, "n_seg"),
+    ("seg_tree", _I32, np.int32, "n_seg"),
+    ("leaf_seg", _I32, np.int32, "n_leaves"),
+    ("tree_calls", _I32, np.int32, "n_trees"),
+    ("round_seq_off", _I32, np.int32, "n_rounds+1"),
+    ("seq_round", _I32, np.int32, "n_seq"),
+    ("seq_tree", _I32, np.int32, "n_seq"),
+    ("seq_first_seg", _I32, np.int32, "n_seq"),
+    ("seq_final_leaf", _I32, np.int32, "n_seq"),
+    ("seq_init_bank", _I32, np.int32, "n_seq"),
+    ("seq_anchor", _I64, np.int64, "n_seq"),
+    ("seq_n_replay", _I64, np.int64, "n_seq"),
+    ("seq_replay_off", _I64, np.int64, "n_seq+1"),
+    ("seq_row", _I64, np.int64, "n_seq"),
+    ("seq_n_own", _I64, np.int64, "n_seq"),
+    ("seq_chain_off", _I32, np.int32, "n_seq+1"),
+    ("chain_seg", _I32, np.int32, "n_seg"),
+    ("seq_req_off", _I32, np.int32, "n_seq+1"),
+    ("req_chunk", _I32, np.int32, "n_req"),
+    ("req_bank", _I32, np.int32, "n_req"),
+    ("slot_seq", _I32, np.int32, "n_slots"),
+    ("slot_pos", _I64, np.int64, "n_slots"),
+    ("replay_row", _I64, np.int64, "R"),
+)
+
+
+class PlanArrays(C.Structure):
+    _fields_ = [(n, t) for n, t, _, _ in PLAN_ARRAY_FIELDS]
+
+
+class RoundInfo(C.Structure):
+    _fields_ = [("n_seq", C.c_int32), ("seq_begin", C.c_int32)] + [
+        (n, C.c_int64) for n in ("n_chunks", "n_rows", "n_own", "n_replay",
+                                 "own_row_begin", "init_idx_off")]
+
+
+class HartsError(RuntimeError):
+    def __init__(self, code, where, msg):
+        super().__init__(f"{where} failed ({code}): {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """Load libharts.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"libharts.so not found at {LIB_PATH}; build it with "
+            "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = C.CDLL(LIB_PATH)
+    vp, sz, i32, i64, f32 = C.c_void_p, C.c_size_t, C.c_int32, C.c_int64, C.c_float
+    fp = C.POINTER(C.c_float)
+    L.harts_last_error.restype = C.c_char_p
+    L.harts_last_error.argtypes = []
+    L.harts_plan.restype = C.c_int
+    L.harts_plan.argtypes = [i32, _I32, _I64, i32, C.POINTER(vp)]
+    L.harts_plan_free.restype = None
+    L.harts_plan_free.argtypes = [vp]
+    L.harts_plan_get_info.restype = C.c_int
+    L.harts_plan_get_info.argtypes = [vp, C.POINTER(PlanInfo)]
+    L.harts_plan_export.restype = C.c_int
+    L.harts_plan_export.argtypes = [vp, C.POINTER(PlanArrays)]
+    L.harts_plan_round_info.restype = C.c_int
+    L.harts_plan_round_info.argtypes = [vp, i32, C.POINTER(RoundInfo)]
+    L.harts_plan_blob.restype = C.c_int
+    L.harts_plan_blob.argtypes = [vp, vp, sz]
+    L.harts_la_fwd.restype = C.c_int
+    L.harts_la_fwd.argtypes = [vp, i32, vp, i32, i32, i32, i32, f32,
+                               vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.harts_la_bwd.restype = C.c_int
+    L.harts_la_bwd.argtypes = [vp, i32, vp, i32, i32, i32, i32, f32,
+                               vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                               vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.harts_la_workspace_size.restype = C.c_int
+    L.harts_la_workspace_size.argtypes = [vp, i32, i32, i32, i32, i32, i32, i32,
+                                          C.POINTER(sz)]
+    L.harts_la_saved_size.restype = C.c_int
+    L.harts_la_saved_size.argtypes = [vp, i32, i32, i32, i32, i32, C.POINTER(sz)]
+    L.harts_state_gather.restype = C.c_int
+    L.harts_state_gather.argtypes = [vp, vp, i32, i64, vp, i32, vp]
+    L.harts_replay_reduce.restype = C.c_int
+    L.harts_replay_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp,
+                                      vp, vp]
+    _lib = L
+    return L
+
+
+def check(code, where):
+    if code != HARTS_OK:
+        msg = lib().harts_last_error().decode(errors="replace")
+        raise HartsError(code, where, msg)
+
+
+def last_error() -> str:
+    return lib().harts_last_error().decode(errors="replace")

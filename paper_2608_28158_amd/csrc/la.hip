@@ -1,0 +1,902 @@
+// Packed chunkwise linear attention with per-head scalar decay, one
+// execution round per call (HARTS, Sec. 3.4, eq. chunkla-interface), for
+// gfx950.  Recurrence per head (state S: [dk, dv]):
+//     S_t = exp(g_t) S_{t-1} + k_t v_t^T,    o_t = scale * S_t^T q_t.
+// Chunkwise form (Sec. 2.2): for chunk c with start state S_c and in-chunk
+// prefix sums G (G_i = g_0 + ... + g_i),
+//     O        = scale * ((Q K^T) * exp(G_i - G_j) [j <= i]) V
+//              + scale * diag(exp(G)) Q S_c
+//     S_{c+1}  = exp(G_last) S_c + (K * exp(G_last - G))^T V.
+//
+// Kernels (per round):
+//   k_fwd_state  sequential over the chunks of a sequence, 32 state columns
+//                per workgroup: writes the start state of every chunk (and
+//                the final state) to a chunk-state buffer, the requested
+//                boundary states to the bank and the final state to S_final.
+//   k_fwd_out    one workgroup per (chunk, head): outputs of the own rows.
+//   k_bwd_state  reverse scan of the state adjoint
+//                dS_c = exp(G_last) dS_{c+1} + scale (Q * exp(G))^T dO
+//                (+ the bank gradient injected at requested boundaries),
+//                writes the adjoint at every chunk end, the per-chunk
+//                <S_{c+1}, dS_{c+1}> partial sums and dS0.
+//   k_bwd_grad   one workgroup per (chunk, head): dq, dk, dv, dg.
+//   k_gather / k_scatter_add      state handoff and its adjoint.
+//   k_replay_reduce               replay-row gradients into compact rows.
+// All products run on MFMA (bf16 16x16x32 or f32 16x16x4) with operands
+// staged in LDS; accumulation and states are float32.  No float atomics.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "la_common.hpp"
+#include "plan.hpp"
+
+namespace harts {
+
+// ---------------------------------------------------------------------------
+// small helpers
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ inline void load_vec16(T* dst, const T* src) {
+  *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
+}
+
+// State tiles owned by one wave in the scan kernels: the [D x DVT] slice is
+// cut into (D/16) x 2 tiles of 16x16; wave w owns tiles w*TPW .. w*TPW+TPW-1,
+// tile q at rows 16*(q/2), columns 16*(q%2) of the slice.
+template <int D>
+struct ScanTiles {
+  static constexpr int TPW = (D / 16) * (DVT / 16) / NWAVES;
+  __device__ static inline int mt(int w, int i) { return (w * TPW + i) >> 1; }
+  __device__ static inline int nt(int w, int i) { return (w * TPW + i) & 1; }
+};
+
+template <int D>
+__device__ inline void load_state_slice(f32x4* S, const float* src, int tile, int w, int lane) {
+  using ST = ScanTiles<D>;
+#pragma unroll
+  for (int i = 0; i < ST::TPW; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      S[i][r] = src[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT + ST::nt(w, i) * 16 +
+                    acc_col(lane)];
+}
+
+template <int D>
+__device__ inline void store_state_slice(float* dst, const f32x4* S, int tile, int w, int lane) {
+  using ST = ScanTiles<D>;
+#pragma unroll
+  for (int i = 0; i < ST::TPW; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      dst[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT + ST::nt(w, i) * 16 +
+          acc_col(lane)] = S[i][r];
+}
+
+template <int D>
+__device__ inline void add_state_slice(f32x4* S, const float* src, int tile, int w, int lane) {
+  using ST = ScanTiles<D>;
+#pragma unroll
+  for (int i = 0; i < ST::TPW; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      S[i][r] += src[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT +
+                     ST::nt(w, i) * 16 + acc_col(lane)];
+}
+
+// ---------------------------------------------------------------------------
+// forward: state scan
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(NTHREADS) void k_fwd_state(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ replay_row,
+    const int32_t* __restrict__ req_chunk, const int32_t* __restrict__ req_bank, int H,
+    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
+    const float* __restrict__ S0, float* __restrict__ hbuf, float* __restrict__ bank,
+    float* __restrict__ S_final) {
+  constexpr int NTILE = D / DVT;
+  constexpr int LD = CB + Elem<T>::PAD;
+  constexpr int VE = 16 / sizeof(T);
+  using ST = ScanTiles<D>;
+  const int li = blockIdx.x / NTILE, tile = blockIdx.x % NTILE, h = blockIdx.y;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int nc = seq[SEQ_N_CHUNKS];
+  const int64_t hb0 = static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + li;
+  const int64_t SS = static_cast<int64_t>(D) * D;
+
+  __shared__ T Kt[D * LD];    // (K * exp(G_last - G))^T : [dk][j]
+  __shared__ T Vt[DVT * LD];  // V slice transposed      : [dv][j]
+  __shared__ ChunkRows cr;
+  __shared__ float G[CB];
+
+  f32x4 S[ST::TPW];
+  load_state_slice<D>(S, S0 + (static_cast<int64_t>(li) * H + h) * SS, tile, w, lane);
+  int rq = seq[SEQ_REQ_OFF];
+  const int rq_end = rq + seq[SEQ_N_REQ];
+
+  for (int c = 0; c < nc; ++c) {
+    if (hbuf) store_state_slice<D>(hbuf + ((hb0 + c) * H + h) * SS, S, tile, w, lane);
+    if (rq < rq_end && req_chunk[rq] == c) {
+      if (bank) store_state_slice<D>(bank + (static_cast<int64_t>(req_bank[rq]) * H + h) * SS, S,
+                                     tile, w, lane);
+      ++rq;
+    }
+    resolve_rows(cr, seq, c, replay_row, t);
+    __syncthreads();
+    chunk_cumsum(G, cr, g, H, h, t);
+    __syncthreads();
+    const float GL = G[CB - 1];
+    for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
+      const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
+      alignas(16) T vals[VE];
+      if (cr.kind[row] != ROW_PAD) {
+        load_vec16(vals, k + (static_cast<int64_t>(cr.row[row]) * H + h) * D + d0);
+        const float sc = __expf(GL - G[row]);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) Kt[(d0 + e) * LD + row] = Elem<T>::from_f(Elem<T>::to_f(vals[e]) * sc);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) Kt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
+      }
+    }
+    for (int idx = t; idx < CB * (DVT / VE); idx += NTHREADS) {
+      const int row = idx / (DVT / VE), d0 = (idx % (DVT / VE)) * VE;
+      alignas(16) T vals[VE];
+      if (cr.kind[row] != ROW_PAD) {
+        load_vec16(vals, v + (static_cast<int64_t>(cr.row[row]) * H + h) * D + tile * DVT + d0);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) Vt[(d0 + e) * LD + row] = vals[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) Vt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
+      }
+    }
+    __syncthreads();
+    const float dec = __expf(GL);
+#pragma unroll
+    for (int i = 0; i < ST::TPW; ++i) {
+      S[i] *= dec;
+      Mma<T>::tile(S[i], Kt + ST::mt(w, i) * 16 * LD, LD, Vt + ST::nt(w, i) * 16 * LD, LD, CB, lane);
+    }
+    __syncthreads();
+  }
+  if (hbuf) store_state_slice<D>(hbuf + ((hb0 + nc) * H + h) * SS, S, tile, w, lane);
+  if (S_final)
+    store_state_slice<D>(S_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS, S,
+                         tile, w, lane);
+}
+
+// ---------------------------------------------------------------------------
+// forward: outputs of one chunk
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct FwdOutSmem {
+  static constexpr int LDQ = D + Elem<T>::PAD;
+  static constexpr int LDV = CB + Elem<T>::PAD;
+  static constexpr int LDH = D + Elem<T>::PAD;
+  static constexpr int LDA = CB + Elem<T>::PAD;
+  T Qs[CB * LDQ];
+  T Ks[CB * LDQ];
+  T Vt[D * LDV];   // [dv][j]
+  T hT[D * LDH];   // S_c^T : [dv][dk]
+  T As[CB * LDA];  // masked Q K^T : [i][j]
+  ChunkRows cr;
+  float G[CB];
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(NTHREADS) void k_fwd_out(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ chunk_tab,
+    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
+    const float* __restrict__ hbuf, T* __restrict__ o) {
+  using SM = FwdOutSmem<T, D>;
+  constexpr int VE = 16 / sizeof(T);
+  __shared__ SM sm;
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int li = chunk_tab[2 * ci], c = chunk_tab[2 * ci + 1];
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int64_t SS = static_cast<int64_t>(D) * D;
+  resolve_rows(sm.cr, seq, c, replay_row, t);
+  __syncthreads();
+  chunk_cumsum(sm.G, sm.cr, g, H, h, t);
+  for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
+    const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
+    const int kind = sm.cr.kind[row];
+    const int64_t off = (static_cast<int64_t>(sm.cr.row[row]) * H + h) * D + d0;
+    alignas(16) T vals[VE];
+    if (kind == ROW_OWN) load_vec16(vals, q + off);
+    else for (int e = 0; e < VE; ++e) vals[e] = Elem<T>::from_f(0.f);
+    load_vec16(&sm.Qs[row * SM::LDQ + d0], vals);
+    if (kind != ROW_PAD) load_vec16(vals, k + off);
+    else for (int e = 0; e < VE; ++e) vals[e] = Elem<T>::from_f(0.f);
+    load_vec16(&sm.Ks[row * SM::LDQ + d0], vals);
+    if (kind != ROW_PAD) load_vec16(vals, v + off);
+    else for (int e = 0; e < VE; ++e) vals[e] = Elem<T>::from_f(0.f);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) sm.Vt[(d0 + e) * SM::LDV + row] = vals[e];
+  }
+  const float* hc = hbuf + ((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + li + c) * H + h) * SS;
+  for (int idx = t; idx < D * D / 4; idx += NTHREADS) {
+    const int dk = idx / (D / 4), dv0 = (idx % (D / 4)) * 4;
+    const float4 x = *reinterpret_cast<const float4*>(hc + dk * D + dv0);
+    sm.hT[(dv0 + 0) * SM::LDH + dk] = Elem<T>::from_f(x.x);
+    sm.hT[(dv0 + 1) * SM::LDH + dk] = Elem<T>::from_f(x.y);
+    sm.hT[(dv0 + 2) * SM::LDH + dk] = Elem<T>::from_f(x.z);
+    sm.hT[(dv0 + 3) * SM::LDH + dk] = Elem<T>::from_f(x.w);
+  }
+  __syncthreads();
+  // masked attention matrix: wave w owns rows 16w .. 16w+15
+#pragma unroll
+  for (int nt = 0; nt < CB / 16; ++nt) {
+    f32x4 a = {0.f, 0.f, 0.f, 0.f};
+    Mma<T>::tile(a, sm.Qs + 16 * w * SM::LDQ, SM::LDQ, sm.Ks + nt * 16 * SM::LDQ, SM::LDQ, D, lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+      const float val = n <= m ? a[r] * __expf(sm.G[m] - sm.G[n]) : 0.f;
+      sm.As[m * SM::LDA + n] = Elem<T>::from_f(val);
+    }
+  }
+  __syncthreads();
+#pragma unroll 2
+  for (int nt = 0; nt < D / 16; ++nt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    Mma<T>::tile(acc, sm.Qs + 16 * w * SM::LDQ, SM::LDQ, sm.hT + nt * 16 * SM::LDH, SM::LDH, D,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] *= __expf(sm.G[16 * w + acc_row(lane, r)]);
+    Mma<T>::tile(acc, sm.As + 16 * w * SM::LDA, SM::LDA, sm.Vt + nt * 16 * SM::LDV, SM::LDV, CB,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * w + acc_row(lane, r);
+      if (sm.cr.kind[m] == ROW_OWN)
+        o[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + nt * 16 + acc_col(lane)] =
+            Elem<T>::from_f(acc[r] * scale);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward: reverse scan of the state adjoint
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(NTHREADS) void k_bwd_state(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ replay_row,
+    const int32_t* __restrict__ req_chunk, const int32_t* __restrict__ req_bank, int H,
+    float scale, const T* __restrict__ q, const float* __restrict__ g, const T* __restrict__ dO,
+    const float* __restrict__ hbuf, const float* __restrict__ dS_final,
+    const float* __restrict__ dbank, float* __restrict__ dhbuf, float* __restrict__ ipbuf,
+    float* __restrict__ dS0) {
+  constexpr int NTILE = D / DVT;
+  constexpr int LD = CB + Elem<T>::PAD;
+  constexpr int VE = 16 / sizeof(T);
+  using ST = ScanTiles<D>;
+  const int li = blockIdx.x / NTILE, tile = blockIdx.x % NTILE, h = blockIdx.y;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int nc = seq[SEQ_N_CHUNKS];
+  const int64_t c0 = seq[SEQ_CHUNK_OFF];
+  const int64_t hb0 = c0 + li;
+  const int64_t SS = static_cast<int64_t>(D) * D;
+
+  __shared__ T Qt[D * LD];    // (Q * exp(G) * scale)^T : [dk][i]
+  __shared__ T dOt[DVT * LD]; // dO slice transposed     : [dv][i]
+  __shared__ ChunkRows cr;
+  __shared__ float G[CB];
+  __shared__ float red[NWAVES];
+
+  f32x4 dS[ST::TPW];
+  load_state_slice<D>(dS, dS_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS,
+                      tile, w, lane);
+  const int rq_begin = seq[SEQ_REQ_OFF];
+  int rq = rq_begin + seq[SEQ_N_REQ] - 1;
+
+  for (int c = nc - 1; c >= 0; --c) {
+    // adjoint at the end of chunk c and its inner product with S_{c+1}
+    store_state_slice<D>(dhbuf + ((c0 + c) * H + h) * SS, dS, tile, w, lane);
+    {
+      const float* hn = hbuf + ((hb0 + c + 1) * H + h) * SS;
+      float part = 0.f;
+#pragma unroll
+      for (int i = 0; i < ST::TPW; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          part += dS[i][r] * hn[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT +
+                                ST::nt(w, i) * 16 + acc_col(lane)];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off, 64);
+      if (lane == 0) red[w] = part;
+    }
+    resolve_rows(cr, seq, c, replay_row, t);
+    __syncthreads();
+    if (t == 0) {
+      float s = 0.f;
+      for (int i = 0; i < NWAVES; ++i) s += red[i];
+      ipbuf[((c0 + c) * H + h) * NTILE + tile] = s;
+    }
+    chunk_cumsum(G, cr, g, H, h, t);
+    __syncthreads();
+    for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
+      const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
+      alignas(16) T vals[VE];
+      if (cr.kind[row] == ROW_OWN) {
+        load_vec16(vals, q + (static_cast<int64_t>(cr.row[row]) * H + h) * D + d0);
+        const float sc = __expf(G[row]) * scale;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) Qt[(d0 + e) * LD + row] = Elem<T>::from_f(Elem<T>::to_f(vals[e]) * sc);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) Qt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
+      }
+    }
+    for (int idx = t; idx < CB * (DVT / VE); idx += NTHREADS) {
+      const int row = idx / (DVT / VE), d0 = (idx % (DVT / VE)) * VE;
+      alignas(16) T vals[VE];
+      if (cr.kind[row] == ROW_OWN) {
+        load_vec16(vals, dO + (static_cast<int64_t>(cr.row[row]) * H + h) * D + tile * DVT + d0);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) dOt[(d0 + e) * LD + row] = vals[e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) dOt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
+      }
+    }
+    __syncthreads();
+    const float dec = __expf(G[CB - 1]);
+#pragma unroll
+    for (int i = 0; i < ST::TPW; ++i) {
+      dS[i] *= dec;
+      Mma<T>::tile(dS[i], Qt + ST::mt(w, i) * 16 * LD, LD, dOt + ST::nt(w, i) * 16 * LD, LD, CB,
+                   lane);
+    }
+    if (c >= 1 && rq >= rq_begin && req_chunk[rq] == c) {
+      add_state_slice<D>(dS, dbank + (static_cast<int64_t>(req_bank[rq]) * H + h) * SS, tile, w,
+                         lane);
+      --rq;
+    }
+    __syncthreads();
+  }
+  store_state_slice<D>(dS0 + (static_cast<int64_t>(li) * H + h) * SS, dS, tile, w, lane);
+}
+
+// ---------------------------------------------------------------------------
+// backward: gradients of one chunk
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct BwdSmem {
+  static constexpr int LDQ = D + Elem<T>::PAD;
+  static constexpr int LDA = CB + Elem<T>::PAD;
+  static constexpr int LDT = CB + Elem<T>::PAD;
+  static constexpr int LDS = D + Elem<T>::PAD;
+  T Qs[CB * LDQ];
+  T Ks[CB * LDQ];
+  T Vs[CB * LDQ];
+  T dOs[CB * LDQ];
+  T At[CB * LDA];   // A^T   : [j][i]
+  T dAs[CB * LDA];  // dA    : [i][j]
+  T dAt[CB * LDA];  // dA^T  : [j][i]
+  T TR[D * LDT];    // K^T, then Q^T, then dO^T : [d][row]
+  T SR[D * LDS];    // S_c, then dS_{c+1}, then dS_{c+1}^T
+  ChunkRows cr;
+  float G[CB];
+  float dgb[CB];
+};
+
+template <typename T, int D>
+__device__ inline void transpose_rows(T* dst, int ldd, const T* src, int lds, int t) {
+  for (int idx = t; idx < CB * D; idx += NTHREADS) {
+    const int d = idx % D, row = idx / D;
+    dst[d * ldd + row] = src[row * lds + d];
+  }
+}
+
+template <typename T, int D>
+__device__ inline void load_state_lds(T* dst, int ldd, const float* src, bool transpose, int t) {
+  for (int idx = t; idx < D * D / 4; idx += NTHREADS) {
+    const int a = idx / (D / 4), b0 = (idx % (D / 4)) * 4;
+    const float4 x = *reinterpret_cast<const float4*>(src + a * D + b0);
+    if (!transpose) {
+      dst[a * ldd + b0 + 0] = Elem<T>::from_f(x.x);
+      dst[a * ldd + b0 + 1] = Elem<T>::from_f(x.y);
+      dst[a * ldd + b0 + 2] = Elem<T>::from_f(x.z);
+      dst[a * ldd + b0 + 3] = Elem<T>::from_f(x.w);
+    } else {
+      dst[(b0 + 0) * ldd + a] = Elem<T>::from_f(x.x);
+      dst[(b0 + 1) * ldd + a] = Elem<T>::from_f(x.y);
+      dst[(b0 + 2) * ldd + a] = Elem<T>::from_f(x.z);
+      dst[(b0 + 3) * ldd + a] = Elem<T>::from_f(x.w);
+    }
+  }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(NTHREADS) void k_bwd_grad(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ chunk_tab,
+    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
+    const T* __restrict__ dO, const float* __restrict__ hbuf, const float* __restrict__ dhbuf,
+    const float* __restrict__ ipbuf, T* __restrict__ dq, T* __restrict__ dk,
+    T* __restrict__ dv, float* __restrict__ dg, float* __restrict__ rep_grad) {
+  using SM = BwdSmem<T, D>;
+  constexpr int VE = 16 / sizeof(T);
+  constexpr int NTILE = D / DVT;
+  constexpr int RG = 2 * D + 1;  // replay_grad row: dk | dv | dg
+  __shared__ SM sm;
+  const int ci = blockIdx.x, h = blockIdx.y;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int li = chunk_tab[2 * ci], c = chunk_tab[2 * ci + 1];
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int64_t c0 = seq[SEQ_CHUNK_OFF];
+  const int64_t SS = static_cast<int64_t>(D) * D;
+
+  resolve_rows(sm.cr, seq, c, replay_row, t);
+  __syncthreads();
+  chunk_cumsum(sm.G, sm.cr, g, H, h, t);
+  for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
+    const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
+    const int kind = sm.cr.kind[row];
+    const int64_t off = (static_cast<int64_t>(sm.cr.row[row]) * H + h) * D + d0;
+    alignas(16) T zero[VE];
+    alignas(16) T vals[VE];
+    for (int e = 0; e < VE; ++e) zero[e] = Elem<T>::from_f(0.f);
+    if (kind == ROW_OWN) { load_vec16(vals, q + off); load_vec16(&sm.Qs[row * SM::LDQ + d0], vals); }
+    else load_vec16(&sm.Qs[row * SM::LDQ + d0], zero);
+    if (kind == ROW_OWN) { load_vec16(vals, dO + off); load_vec16(&sm.dOs[row * SM::LDQ + d0], vals); }
+    else load_vec16(&sm.dOs[row * SM::LDQ + d0], zero);
+    if (kind != ROW_PAD) { load_vec16(vals, k + off); load_vec16(&sm.Ks[row * SM::LDQ + d0], vals); }
+    else load_vec16(&sm.Ks[row * SM::LDQ + d0], zero);
+    if (kind != ROW_PAD) { load_vec16(vals, v + off); load_vec16(&sm.Vs[row * SM::LDQ + d0], vals); }
+    else load_vec16(&sm.Vs[row * SM::LDQ + d0], zero);
+  }
+  __syncthreads();
+  const float GL = sm.G[CB - 1];
+  // A (unscaled) and dA = scale * (dO V^T), both masked; wave w owns rows i in 16w..16w+15
+#pragma unroll
+  for (int nt = 0; nt < CB / 16; ++nt) {
+    f32x4 a = {0.f, 0.f, 0.f, 0.f}, da = {0.f, 0.f, 0.f, 0.f};
+    Mma<T>::tile(a, sm.Qs + 16 * w * SM::LDQ, SM::LDQ, sm.Ks + nt * 16 * SM::LDQ, SM::LDQ, D, lane);
+    Mma<T>::tile(da, sm.dOs + 16 * w * SM::LDQ, SM::LDQ, sm.Vs + nt * 16 * SM::LDQ, SM::LDQ, D,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+      const float dm = n <= m ? __expf(sm.G[m] - sm.G[n]) : 0.f;
+      const T av = Elem<T>::from_f(a[r] * dm);
+      const T dav = Elem<T>::from_f(da[r] * dm * scale);
+      sm.At[n * SM::LDA + m] = av;
+      sm.dAs[m * SM::LDA + n] = dav;
+      sm.dAt[n * SM::LDA + m] = dav;
+    }
+  }
+  transpose_rows<T, D>(sm.TR, SM::LDT, sm.Ks, SM::LDQ, t);
+  load_state_lds<T, D>(sm.SR, SM::LDS, hbuf + ((c0 + li + c) * H + h) * SS, false, t);
+  __syncthreads();
+
+  // dq = dA K + scale * diag(exp(G)) dO S_c^T
+  float dgp[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int nt = 0; nt < D / 16; ++nt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    Mma<T>::tile(acc, sm.dOs + 16 * w * SM::LDQ, SM::LDQ, sm.SR + nt * 16 * SM::LDS, SM::LDS, D,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] *= __expf(sm.G[16 * w + acc_row(lane, r)]) * scale;
+    Mma<T>::tile(acc, sm.dAs + 16 * w * SM::LDA, SM::LDA, sm.TR + nt * 16 * SM::LDT, SM::LDT, CB,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+      dgp[r] += Elem<T>::to_f(sm.Qs[m * SM::LDQ + n]) * acc[r];
+      if (sm.cr.kind[m] == ROW_OWN)
+        dq[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float s = sum16(dgp[r]);
+    if ((lane & 15) == 0) sm.dgb[16 * w + acc_row(lane, r)] = s;
+    dgp[r] = 0.f;
+  }
+  __syncthreads();
+  transpose_rows<T, D>(sm.TR, SM::LDT, sm.Qs, SM::LDQ, t);
+  load_state_lds<T, D>(sm.SR, SM::LDS, dhbuf + ((c0 + c) * H + h) * SS, false, t);
+  __syncthreads();
+
+  // dk = dA^T Q + diag(exp(G_last - G)) V dS_{c+1}^T
+  for (int nt = 0; nt < D / 16; ++nt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    Mma<T>::tile(acc, sm.Vs + 16 * w * SM::LDQ, SM::LDQ, sm.SR + nt * 16 * SM::LDS, SM::LDS, D,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] *= __expf(GL - sm.G[16 * w + acc_row(lane, r)]);
+    Mma<T>::tile(acc, sm.dAt + 16 * w * SM::LDA, SM::LDA, sm.TR + nt * 16 * SM::LDT, SM::LDT, CB,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+      dgp[r] += Elem<T>::to_f(sm.Ks[m * SM::LDQ + n]) * acc[r];
+      const int kind = sm.cr.kind[m];
+      if (kind == ROW_OWN)
+        dk[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+      else if (kind == ROW_REPLAY)
+        rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + n] = acc[r];
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float s = sum16(dgp[r]);
+    if ((lane & 15) == 0) sm.dgb[16 * w + acc_row(lane, r)] -= s;
+  }
+  __syncthreads();
+  transpose_rows<T, D>(sm.TR, SM::LDT, sm.dOs, SM::LDQ, t);
+  load_state_lds<T, D>(sm.SR, SM::LDS, dhbuf + ((c0 + c) * H + h) * SS, true, t);
+  __syncthreads();
+
+  // dv = scale * A^T dO + diag(exp(G_last - G)) K dS_{c+1}
+  const float inv_scale = 1.f / scale;
+  for (int nt = 0; nt < D / 16; ++nt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    Mma<T>::tile(acc, sm.Ks + 16 * w * SM::LDQ, SM::LDQ, sm.SR + nt * 16 * SM::LDS, SM::LDS, D,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] *= __expf(GL - sm.G[16 * w + acc_row(lane, r)]) * inv_scale;
+    Mma<T>::tile(acc, sm.At + 16 * w * SM::LDA, SM::LDA, sm.TR + nt * 16 * SM::LDT, SM::LDT, CB,
+                 lane);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+      const float val = acc[r] * scale;
+      const int kind = sm.cr.kind[m];
+      if (kind == ROW_OWN)
+        dv[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(val);
+      else if (kind == ROW_REPLAY)
+        rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + D + n] = val;
+    }
+  }
+  // dg_t = sum_{u >= t in chunk} (q_u.dq_u - k_u.dk_u) + <S_{c+1}, dS_{c+1}>
+  if (t < CB) {
+    float x = sm.dgb[t];
+#pragma unroll
+    for (int off = 1; off < CB; off <<= 1) {
+      const float y = __shfl_down(x, off, CB);
+      if (t + off < CB) x += y;
+    }
+    float ip = 0.f;
+#pragma unroll
+    for (int i = 0; i < NTILE; ++i) ip += ipbuf[((c0 + c) * H + h) * NTILE + i];
+    const int kind = sm.cr.kind[t];
+    if (kind == ROW_OWN) dg[static_cast<int64_t>(sm.cr.row[t]) * H + h] = x + ip;
+    else if (kind == ROW_REPLAY)
+      rep_grad[(static_cast<int64_t>(sm.cr.rep[t]) * H + h) * RG + 2 * D] = x + ip;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// state handoff and replay reduction
+// ---------------------------------------------------------------------------
+__global__ void k_gather(const float4* __restrict__ src, const int32_t* __restrict__ idx,
+                         int64_t e4, float4* __restrict__ dst) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int i = blockIdx.y;
+  if (e >= e4) return;
+  const int s = idx[i];
+  dst[static_cast<int64_t>(i) * e4 + e] =
+      s < 0 ? make_float4(0.f, 0.f, 0.f, 0.f) : src[static_cast<int64_t>(s) * e4 + e];
+}
+
+__global__ void k_scatter_add(const float4* __restrict__ src, const int32_t* __restrict__ idx,
+                              int n, int64_t e4, float4* __restrict__ dst) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= e4) return;
+  for (int i = 0; i < n; ++i) {  // one thread per element: sources in order
+    const int s = idx[i];
+    if (s < 0) continue;
+    float4 a = dst[static_cast<int64_t>(s) * e4 + e];
+    const float4 b = src[static_cast<int64_t>(i) * e4 + e];
+    a.x += b.x;
+    a.y += b.y;
+    a.z += b.z;
+    a.w += b.w;
+    dst[static_cast<int64_t>(s) * e4 + e] = a;
+  }
+}
+
+template <typename T, int D>
+__global__ void k_replay_reduce(const int32_t* __restrict__ red_rows,
+                                const int32_t* __restrict__ red_off,
+                                const int32_t* __restrict__ red_idx, int H,
+                                const float* __restrict__ rep_grad, T* __restrict__ dk,
+                                T* __restrict__ dv, float* __restrict__ dg) {
+  constexpr int RG = 2 * D + 1;
+  const int u = blockIdx.x, h = blockIdx.y;
+  const int64_t row = red_rows[u];
+  const int b = red_off[u], e = red_off[u + 1];
+  for (int x = threadIdx.x; x < RG; x += blockDim.x) {
+    float s = 0.f;
+    for (int j = b; j < e; ++j) s += rep_grad[(static_cast<int64_t>(red_idx[j]) * H + h) * RG + x];
+    if (x < D) {
+      T* p = dk + (row * H + h) * D + x;
+      *p = Elem<T>::from_f(Elem<T>::to_f(*p) + s);
+    } else if (x < 2 * D) {
+      T* p = dv + (row * H + h) * D + (x - D);
+      *p = Elem<T>::from_f(Elem<T>::to_f(*p) + s);
+    } else {
+      dg[row * H + h] += s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+namespace {
+
+int hip_check(const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error(std::string(where) + ": " + hipGetErrorString(e));
+    return HARTS_EHIP;
+  }
+  return HARTS_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_shape(const harts_plan_t* p, int32_t round, int32_t dtype, int32_t H, int32_t dk,
+                int32_t dv, const char* where) {
+  if (!p) { set_error(std::string(where) + ": plan is NULL"); return HARTS_EINVAL; }
+  if (round < 0 || round >= p->K) { set_error(std::string(where) + ": round out of range"); return HARTS_EINVAL; }
+  if (H < 1) { set_error(std::string(where) + ": H must be >= 1"); return HARTS_EINVAL; }
+  if (p->chunk != CB) { set_error(std::string(where) + ": device calls need chunk size 64"); return HARTS_EUNSUPPORTED; }
+  if (dtype != HARTS_F32 && dtype != HARTS_BF16) { set_error(std::string(where) + ": unknown dtype"); return HARTS_EUNSUPPORTED; }
+  if (dk != dv || (dk != 64 && dk != 128)) { set_error(std::string(where) + ": need dk == dv in {64, 128}"); return HARTS_EUNSUPPORTED; }
+  if (dtype == HARTS_F32 && dk != 64) { set_error(std::string(where) + ": float32 path supports d = 64"); return HARTS_EUNSUPPORTED; }
+  return HARTS_OK;
+}
+
+size_t hbuf_bytes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
+  const RoundLayout& L = p->rounds[round];
+  return static_cast<size_t>(L.n_chunks + L.n_seq) * H * D * D * sizeof(float);
+}
+size_t dhbuf_bytes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
+  const RoundLayout& L = p->rounds[round];
+  return static_cast<size_t>(L.n_chunks) * H * D * D * sizeof(float);
+}
+size_t ipbuf_bytes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
+  const RoundLayout& L = p->rounds[round];
+  return (static_cast<size_t>(L.n_chunks) * H * (D / DVT) * sizeof(float) + 255) / 256 * 256;
+}
+
+struct Blob {
+  const int32_t* seq_tab;
+  const int32_t* chunk_tab;
+  const int32_t* replay_row;
+  const int32_t* req_chunk;
+  const int32_t* req_bank;
+};
+
+Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
+  const int32_t* b = static_cast<const int32_t*>(d_blob);
+  const RoundLayout& L = p->rounds[round];
+  return Blob{b + L.seq_tab, b + L.chunk_tab, b + p->off_replay_row, b + p->off_req_chunk,
+              b + p->off_req_bank};
+}
+
+template <typename T, int D>
+void launch_fwd_state(const harts_plan_t* p, int32_t round, const Blob& B, int H, const void* k,
+                      const void* v, const float* g, const float* S0, float* hbuf, float* bank,
+                      float* S_final, hipStream_t s) {
+  const RoundLayout& L = p->rounds[round];
+  hipLaunchKernelGGL((k_fwd_state<T, D>), dim3(L.n_seq * (D / DVT), H), dim3(NTHREADS), 0, s,
+                     B.seq_tab, B.replay_row, B.req_chunk, B.req_bank, H,
+                     static_cast<const T*>(k), static_cast<const T*>(v), g, S0, hbuf, bank,
+                     S_final);
+}
+
+template <typename T, int D>
+int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, float scale,
+            const void* q, const void* k, const void* v, const float* g, const float* S0, void* o,
+            float* S_final, float* bank, float* hbuf, hipStream_t s) {
+  const RoundLayout& L = p->rounds[round];
+  const Blob B = blob_ptrs(p, round, d_blob);
+  launch_fwd_state<T, D>(p, round, B, H, k, v, g, S0, hbuf, bank, S_final, s);
+  if (int rc = hip_check("harts_la_fwd(state)")) return rc;
+  if (!o) return HARTS_OK;  // state pass only (recompute-forward)
+  hipLaunchKernelGGL((k_fwd_out<T, D>), dim3(static_cast<unsigned>(L.n_chunks), H),
+                     dim3(NTHREADS), 0, s, B.seq_tab, B.chunk_tab, B.replay_row, H, scale,
+                     static_cast<const T*>(q), static_cast<const T*>(k),
+                     static_cast<const T*>(v), g, hbuf, static_cast<T*>(o));
+  return hip_check("harts_la_fwd(out)");
+}
+
+template <typename T, int D>
+int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, float scale,
+            const void* q, const void* k, const void* v, const float* g, const float* S0,
+            const void* dO, const float* dS_final, const float* dbank, float* hbuf, bool recompute,
+            float* dhbuf, float* ipbuf, void* dq, void* dk, void* dv, float* dg,
+            float* rep_grad, float* dS0, hipStream_t s) {
+  const RoundLayout& L = p->rounds[round];
+  const Blob B = blob_ptrs(p, round, d_blob);
+  if (recompute) {
+    launch_fwd_state<T, D>(p, round, B, H, k, v, g, S0, hbuf, nullptr, nullptr, s);
+    if (int rc = hip_check("harts_la_bwd(recompute)")) return rc;
+  }
+  hipLaunchKernelGGL((k_bwd_state<T, D>), dim3(L.n_seq * (D / DVT), H), dim3(NTHREADS), 0, s,
+                     B.seq_tab, B.replay_row, B.req_chunk, B.req_bank, H, scale,
+                     static_cast<const T*>(q), g, static_cast<const T*>(dO), hbuf, dS_final,
+                     dbank, dhbuf, ipbuf, dS0);
+  if (int rc = hip_check("harts_la_bwd(state)")) return rc;
+  hipLaunchKernelGGL((k_bwd_grad<T, D>), dim3(static_cast<unsigned>(L.n_chunks), H),
+                     dim3(NTHREADS), 0, s, B.seq_tab, B.chunk_tab, B.replay_row, H, scale,
+                     static_cast<const T*>(q), static_cast<const T*>(k),
+                     static_cast<const T*>(v), g, static_cast<const T*>(dO), hbuf, dhbuf, ipbuf,
+                     static_cast<T*>(dq), static_cast<T*>(dk), static_cast<T*>(dv), dg, rep_grad);
+  return hip_check("harts_la_bwd(grad)");
+}
+
+}  // namespace
+}  // namespace harts
+
+using namespace harts;
+
+extern "C" int harts_la_saved_size(const harts_plan_t* p, int32_t round, int32_t dtype, int32_t H,
+                                   int32_t dk, int32_t dv, size_t* bytes) {
+  if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_saved_size")) return rc;
+  if (!bytes) { set_error("harts_la_saved_size: bytes is NULL"); return HARTS_EINVAL; }
+  *bytes = hbuf_bytes(p, round, H, dk);
+  return HARTS_OK;
+}
+
+extern "C" int harts_la_workspace_size(const harts_plan_t* p, int32_t round, int32_t pass,
+                                       int32_t dtype, int32_t H, int32_t dk, int32_t dv,
+                                       int32_t has_saved, size_t* bytes) {
+  if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_workspace_size")) return rc;
+  if (!bytes || (pass != 0 && pass != 1)) {
+    set_error("harts_la_workspace_size: bad pass or NULL bytes");
+    return HARTS_EINVAL;
+  }
+  if (pass == 0) *bytes = hbuf_bytes(p, round, H, dk);
+  else
+    *bytes = dhbuf_bytes(p, round, H, dk) + ipbuf_bytes(p, round, H, dk) +
+             (has_saved ? 0 : hbuf_bytes(p, round, H, dk));
+  return HARTS_OK;
+}
+
+extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_blob,
+                            int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                            const void* q, const void* k, const void* v, const float* g,
+                            const float* S0, void* o, float* S_final, float* bank, void* saved,
+                            void* ws, size_t ws_bytes, void* stream) {
+  if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_fwd")) return rc;
+  if (!d_blob || !q || !k || !v || !g || !S0 || !S_final || (!bank && p->n_slots > 0)) {
+    set_error("harts_la_fwd: NULL required pointer");
+    return HARTS_EINVAL;
+  }
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(S0) || !aligned16(o) ||
+      !aligned16(S_final) || !aligned16(saved) || !aligned16(ws)) {
+    set_error("harts_la_fwd: pointers must be 16-byte aligned");
+    return HARTS_EINVAL;
+  }
+  float* hbuf = static_cast<float*>(saved);
+  if (!hbuf) {
+    if (!ws || ws_bytes < hbuf_bytes(p, round, H, dk)) {
+      set_error("harts_la_fwd: workspace too small (see harts_la_workspace_size)");
+      return HARTS_EINVAL;
+    }
+    hbuf = static_cast<float*>(ws);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == HARTS_BF16) {
+    if (dk == 128) return run_fwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, hbuf, s);
+    return run_fwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, hbuf, s);
+  }
+  return run_fwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, hbuf, s);
+}
+
+extern "C" int harts_la_bwd(const harts_plan_t* p, int32_t round, const void* d_blob,
+                            int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                            const void* q, const void* k, const void* v, const float* g,
+                            const float* S0, const void* dO, const float* dS_final,
+                            const float* dbank, const void* saved, void* dq, void* dk_, void* dv_,
+                            float* dg, float* replay_grad, float* dS0, void* ws, size_t ws_bytes,
+                            void* stream) {
+  if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_bwd")) return rc;
+  if (!d_blob || !q || !k || !v || !g || !S0 || !dO || !dS_final || !dq || !dk_ || !dv_ || !dg ||
+      !dS0 || (!dbank && p->n_slots > 0) || (!replay_grad && p->R > 0) || !ws) {
+    set_error("harts_la_bwd: NULL required pointer");
+    return HARTS_EINVAL;
+  }
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) || !aligned16(dq) ||
+      !aligned16(dk_) || !aligned16(dv_) || !aligned16(saved) || !aligned16(ws) ||
+      !aligned16(dS0) || !aligned16(dS_final)) {
+    set_error("harts_la_bwd: pointers must be 16-byte aligned");
+    return HARTS_EINVAL;
+  }
+  const bool recompute = saved == nullptr;
+  const size_t need = dhbuf_bytes(p, round, H, dk) + ipbuf_bytes(p, round, H, dk) +
+                      (recompute ? hbuf_bytes(p, round, H, dk) : 0);
+  if (ws_bytes < need) {
+    set_error("harts_la_bwd: workspace too small (see harts_la_workspace_size)");
+    return HARTS_EINVAL;
+  }
+  char* w = static_cast<char*>(ws);
+  float* dhbuf = reinterpret_cast<float*>(w);
+  float* ipbuf = reinterpret_cast<float*>(w + dhbuf_bytes(p, round, H, dk));
+  float* hbuf = recompute ? reinterpret_cast<float*>(w + dhbuf_bytes(p, round, H, dk) +
+                                                      ipbuf_bytes(p, round, H, dk))
+                          : static_cast<float*>(const_cast<void*>(saved));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == HARTS_BF16) {
+    if (dk == 128)
+      return run_bwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank,
+                                hbuf, recompute, dhbuf, ipbuf, dq, dk_, dv_, dg, replay_grad, dS0,
+                                s);
+    return run_bwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank,
+                             hbuf, recompute, dhbuf, ipbuf, dq, dk_, dv_, dg, replay_grad, dS0, s);
+  }
+  return run_bwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank, hbuf,
+                            recompute, dhbuf, ipbuf, dq, dk_, dv_, dg, replay_grad, dS0, s);
+}
+
+extern "C" int harts_state_gather(const float* src, const int32_t* idx, int32_t n,
+                                  int64_t elems_per_state, float* dst, int32_t mode,
+                                  void* stream) {
+  if (n < 0 || elems_per_state <= 0 || elems_per_state % 4 != 0 || (mode != 0 && mode != 1)) {
+    set_error("harts_state_gather: bad n, elems_per_state or mode");
+    return HARTS_EINVAL;
+  }
+  if (n == 0) return HARTS_OK;
+  if (!src || !idx || !dst || !aligned16(src) || !aligned16(dst)) {
+    set_error("harts_state_gather: NULL or misaligned pointer");
+    return HARTS_EINVAL;
+  }
+  if (mode == 0 && n > 65535) {
+    set_error("harts_state_gather: at most 65535 states per gather");
+    return HARTS_EINVAL;
+  }
+  const int64_t e4 = elems_per_state / 4;
+  const unsigned blocks = static_cast<unsigned>((e4 + 255) / 256);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (mode == 0)
+    hipLaunchKernelGGL(k_gather, dim3(blocks, n), dim3(256), 0, s,
+                       reinterpret_cast<const float4*>(src), idx, e4,
+                       reinterpret_cast<float4*>(dst));
+  else
+    hipLaunchKernelGGL(k_scatter_add, dim3(blocks), dim3(256), 0, s,
+                       reinterpret_cast<const float4*>(src), idx, n, e4,
+                       reinterpret_cast<float4*>(dst));
+  return hip_check("harts_state_gather");
+}
+
+extern "C" int harts_replay_reduce(const harts_plan_t* p, const void* d_blob, int32_t dtype,
+                                   int32_t H, int32_t dk, int32_t dv, const float* replay_grad,
+                                   void* dk_, void* dv_, float* dg, void* stream) {
+  if (int rc = check_shape(p, 0, dtype, H, dk, dv, "harts_replay_reduce")) return rc;
+  if (p->n_red == 0) return HARTS_OK;
+  if (!d_blob || !replay_grad || !dk_ || !dv_ || !dg) {
+    set_error("harts_replay_reduce: NULL required pointer");
+    return HARTS_EINVAL;
+  }
+  const int32_t* b = static_cast<const int32_t*>(d_blob);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 grid(static_cast<unsigned>(p->n_red), H);
+  if (dtype == HARTS_BF16) {
+    if (dk == 128)
+      hipLaunchKernelGGL((k_replay_reduce<bf16, 128>), grid, dim3(256), 0, s, b + p->off_red_rows,
+                         b + p->off_red_off, b + p->off_red_idx, H, replay_grad,
+                         static_cast<bf16*>(dk_), static_cast<bf16*>(dv_), dg);
+    else
+      hipLaunchKernelGGL((k_replay_reduce<bf16, 64>), grid, dim3(256), 0, s, b + p->off_red_rows,
+                         b + p->off_red_off, b + p->off_red_idx, H, replay_grad,
+                         static_cast<bf16*>(dk_), static_cast<bf16*>(dv_), dg);
+  } else {
+    hipLaunchKernelGGL((k_replay_reduce<float, 64>), grid, dim3(256), 0, s, b + p->off_red_rows,
+                       b + p->off_red_off, b + p->off_red_idx, H, replay_grad,
+                       static_cast<float*>(dk_), static_cast<float*>(dv_), dg);
+  }
+  return hip_check("harts_replay_reduce");
+}

@@ -1,0 +1,62 @@
+// Internal definition of the plan object and of the device descriptor image.
+// Shared by the host planner (plan.cpp) and the device-call layer (la.hip).
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "harts.h"
+
+namespace harts {
+
+// Fields of one sequence entry in a round's sequence table (int32 words).
+enum SeqField : int {
+  SEQ_CHUNK_OFF = 0,  // first chunk of the sequence within the round
+  SEQ_N_TOK = 1,      // replay + own rows
+  SEQ_N_REPLAY = 2,   // replay rows (< chunk)
+  SEQ_REPLAY_OFF = 3, // global replay index of the first replay row
+  SEQ_OWN_ROW = 4,    // physical row of the first own row
+  SEQ_INIT_BANK = 5,  // bank entry of the initial state
+  SEQ_FINAL_LEAF = 6, // leaf index receiving the final state
+  SEQ_REQ_OFF = 7,    // first request (global index)
+  SEQ_N_REQ = 8,      // requests of the sequence
+  SEQ_N_CHUNKS = 9,   // chunks of the sequence
+  SEQ_WORDS = 16
+};
+
+struct RoundLayout {
+  int32_t n_seq = 0, seq_begin = 0, max_seq_chunks = 0;
+  int64_t n_chunks = 0, n_rows = 0, n_own = 0, n_replay = 0, own_row_begin = 0;
+  int64_t seq_tab = 0;    // int32 offset of the sequence table
+  int64_t init_idx = 0;   // int32 offset of the [n_seq] init bank indices
+  int64_t chunk_tab = 0;  // int32 offset of the [n_chunks][2] chunk table
+};
+
+}  // namespace harts
+
+struct harts_plan_s {
+  int32_t n_seg = 0, n_trees = 0, n_leaves = 0, K = 0, n_seq = 0, n_slots = 0;
+  int32_t n_bank = 0, chunk = 0;
+  int64_t C = 0, S = 0, R = 0, n_chunks = 0;
+
+  std::vector<int64_t> seg_start, seg_end, seg_row, seg_mult;
+  std::vector<int32_t> seg_seq, seg_tpre, seg_tin, seg_tree, leaf_seg;
+  std::vector<int32_t> tree_calls, round_seq_off;
+  std::vector<int32_t> seq_round, seq_tree, seq_first_seg, seq_final_leaf;
+  std::vector<int32_t> seq_init_bank, seq_chain_off, chain_seg, seq_req_off;
+  std::vector<int64_t> seq_anchor, seq_n_replay, seq_replay_off, seq_row;
+  std::vector<int64_t> seq_n_own;
+  std::vector<int32_t> req_chunk, req_bank, slot_seq;
+  std::vector<int64_t> slot_pos, replay_row;
+
+  // device descriptor image (int32 words) and its layout
+  std::vector<int32_t> blob;
+  std::vector<harts::RoundLayout> rounds;
+  int64_t off_replay_row = 0, off_req_chunk = 0, off_req_bank = 0;
+  int64_t off_red_rows = 0, off_red_off = 0, off_red_idx = 0, n_red = 0;
+};
+
+namespace harts {
+void set_error(const std::string& msg);
+}
