@@ -1,0 +1,353 @@
+#!/usr/bin/env python
+"""Benchmark of tree-packed chunkwise linear attention on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic microbatch with
+inputs resident in HBM: for every execution round the state gather, the
+packed forward (outputs, requested and final states); then, with full-layer
+activation recomputation as in every performance run of the paper, the
+backward re-runs the state pass of every round from the fixed plan and walks
+the rounds in reverse (gradients, handoff scatter-add), ending with the
+replay-gradient reduction.  The host planner runs once per microbatch and is
+timed separately (the paper's F/B/Grad vs Core split).
+
+Workload (default): 8 agentic rollout trees, ~64k compact tokens, 16 heads,
+d = 128, chunk 64, bf16 q/k/v, float32 decay and states.
+
+Prints one JSON line.  ``--gpus`` above 1 is not supported: this build runs
+one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0      # dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3
+
+WORKLOADS = {
+    2: "8 agentic rollout trees, ~64k compact tokens, H=16, d=128, chunk 64, bf16; "
+       "forward + backward with full-layer recompute",
+    3: "32 agentic rollout trees (depth <= 6), ~128k compact tokens, H=32, d=128, chunk 64, "
+       "bf16; forward + backward with full-layer recompute",
+    1: "4 spine trees, ~16k compact tokens, H=16, d=128, chunk 64, bf16; "
+       "forward + backward with full-layer recompute",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def la_source_sha():
+    h = hashlib.sha256()
+    for name in ("la.hip", "la_common.hpp"):
+        with open(os.path.join(ROOT, "paper_2608_28158_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def to_device(x, phys, dt):
+    import torch
+    out = np.empty_like(x)
+    out[phys] = x
+    return torch.from_numpy(out).to("cuda").to(dt).contiguous()
+
+
+def phys_index(seg_len, seg_row):
+    seg_len = np.asarray(seg_len, np.int64)
+    row0 = np.concatenate([[0], np.cumsum(seg_len)[:-1]])
+    phys = np.empty(int(seg_len.sum()), np.int64)
+    for v in range(len(seg_len)):
+        phys[row0[v]:row0[v] + seg_len[v]] = seg_row[v] + np.arange(seg_len[v])
+    return phys
+
+
+def algorithmic_bytes(plan, H, d, el):
+    """Bytes each kernel must move for its job, per launch set of one step.
+
+    Rows are packed rows (own + replay); q, o, dO and dq only exist on own
+    rows.  State terms: initial states, requested boundary states, final
+    states and their gradients (float32 H*d*d each).  Per-chunk state
+    materialisation is not counted."""
+    st = H * d * d * 4
+    out = {}
+    fs = fo = bs = bg = ga = sa = 0
+    for r in plan.rounds:
+        rows, own, rep, nseq = r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"]
+        nreq_r = 0
+        for i in range(r["seq_begin"], r["seq_begin"] + nseq):
+            nreq_r += int(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i])
+        fs += rows * H * (2 * d * el + 4) + nseq * st * 2 + nreq_r * st
+        fo += own * H * d * el * 2 + rows * H * (2 * d * el + 4)
+        bs += own * H * 2 * d * el + rows * H * 4 + nseq * st * 2 + nreq_r * st
+        bg += (own * H * (2 * d * el + 3 * d * el + 4) + rows * H * (2 * d * el + 4)
+               + rep * H * (2 * d + 1) * 4)
+        ga += nseq * st * 2
+        sa += nseq * st * 3
+    out["k_fwd_state"] = fs * 2          # forward and recompute pass
+    out["k_fwd_out"] = fo
+    out["k_bwd_state"] = bs
+    out["k_bwd_grad"] = bg
+    out["k_gather"] = ga * 2
+    out["k_scatter_add"] = sa
+    R = plan.info["R"]
+    out["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
+    return out
+
+
+def launches_per_step(plan):
+    K = plan.info["n_rounds"]
+    return {"k_fwd_state": 2 * K, "k_fwd_out": K, "k_bwd_state": K, "k_bwd_grad": K,
+            "k_gather": 2 * K, "k_scatter_add": K, "k_replay_reduce": 1 if plan.info["R"] else 0}
+
+
+def read_traffic(kernel, workload_key):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_key}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("source_sha") != la_source_sha():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(forest, x, cfg, heads=(0,)):
+    """The fp64 oracle (compact chunkwise execution + reverse-mode gradients)
+    on a bounded sample: the listed heads of the same microbatch."""
+    import torch
+    from oracle.compact import compact_fwd_bwd
+    hs = list(heads)
+    sl = lambda a: a[:, hs]
+    t0 = time.perf_counter()
+    compact_fwd_bwd(forest.parent, forest.seg_len, 64, sl(x["q"]), sl(x["k"]), sl(x["v"]),
+                    sl(x["g"]), cfg["d"] ** -0.5, sl(x["dO"]), sl(x["dS_final"]), sl(x["S0"]))
+    dt = time.perf_counter() - t0
+    H = cfg["H"]
+    return {"value": forest.n_rows / (dt * H / len(hs)), "unit": "compact tokens/s",
+            "cores": torch.get_num_threads(), "kind": "oracle",
+            "sample": f"{len(hs)} of {H} heads of the same microbatch, forward + backward, "
+                      f"float64 compact chunkwise oracle; {dt:.1f} s, scaled by {H // len(hs)} "
+                      f"(heads are independent)"}
+
+
+def run_step(runner, t):
+    fwd = runner.forward(t["q"], t["k"], t["v"], t["g"], t["S0"], outputs=True,
+                         keep_states=False)
+    runner.backward(t["q"], t["k"], t["v"], t["g"], t["dO"], t["dS_final"], fwd=None,
+                    S0_tree=t["S0"], recompute=True)
+    return fwd
+
+
+def time_steps(runner, t, steps, warmup, profile):
+    import torch
+    from paper_2608_28158_amd import _lib
+    for _ in range(warmup):
+        run_step(runner, t)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if profile:
+        _lib.profile_begin()
+    start.record(stream)
+    for _ in range(steps):
+        run_step(runner, t)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    kern = _lib.profile_end() if profile else {}
+    return ms, kern
+
+
+def setup(idx):
+    import torch
+    from paper_2608_28158_amd.plan import HartsPlan
+    from paper_2608_28158_amd.tree_la import TreeLARunner
+    from workloads import config_inputs
+    forest, cfg, x = config_inputs(idx)
+    plan_times = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        plan = HartsPlan(forest.parent, forest.seg_len, 64)
+        plan_times.append(time.perf_counter() - t0)
+    phys = phys_index(forest.seg_len, plan["seg_row"])
+    dt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+    t = dict(q=to_device(x["q"], phys, dt), k=to_device(x["k"], phys, dt),
+             v=to_device(x["v"], phys, dt), g=to_device(x["g"], phys, torch.float32),
+             dO=to_device(x["dO"], phys, dt),
+             dS_final=torch.from_numpy(x["dS_final"]).cuda(),
+             S0=torch.from_numpy(x["S0"]).cuda())
+    runner = TreeLARunner(plan, cfg["H"], cfg["d"], dt, "cuda")
+    return forest, cfg, x, plan, t, runner, float(np.median(plan_times))
+
+
+def expanded_comparison(steps, warmup):
+    """Config 4: the same inputs run tree-packed and trajectory-wise (every
+    root-to-leaf path its own zero-initialised sequence, inputs expanded on
+    the device beforehand, one packed call)."""
+    import torch
+    from paper_2608_28158_amd.plan import HartsPlan
+    from paper_2608_28158_amd.tree_la import TreeLARunner
+    forest, cfg, x, plan, t, runner, _ = setup(4)
+    ms_tree, _ = time_steps(runner, t, steps, warmup, profile=False)
+    # expanded forest: one single-segment tree per trajectory, canonical rows
+    kids = forest.children()
+    parent = forest.parent
+    row0 = np.concatenate([[0], np.cumsum(forest.seg_len)[:-1]])
+    trajs = []
+    for leaf in forest.leaves():
+        path = []
+        v = leaf
+        while v >= 0:
+            path.append(v)
+            v = parent[v]
+        rows = np.concatenate([row0[w] + np.arange(forest.seg_len[w]) for w in reversed(path)])
+        trajs.append(rows)
+    lens = np.array([len(r) for r in trajs], np.int64)
+    eplan = HartsPlan(np.full(len(trajs), -1, np.int32), lens, 64)
+    assert eplan.info["n_rounds"] == 1
+    erows = np.concatenate(trajs)                       # canonical row of each expanded row
+    ephys = phys_index(lens, eplan["seg_row"])          # expanded canonical -> physical
+    dt = t["q"].dtype
+    te = {}
+    for name in ("q", "k", "v", "g", "dO"):
+        src = x[name][erows]
+        te[name] = to_device(src, ephys, torch.float32 if name == "g" else dt)
+    te["dS_final"] = torch.from_numpy(x["dS_final"]).cuda()
+    te["S0"] = torch.zeros((len(trajs), cfg["H"], cfg["d"], cfg["d"]), dtype=torch.float32,
+                           device="cuda")
+    erunner = TreeLARunner(eplan, cfg["H"], cfg["d"], dt, "cuda")
+    ms_exp, _ = time_steps(erunner, te, steps, warmup, profile=False)
+    # metamorphic check: identical outputs on every trajectory row (same
+    # chunk grid, same floating-point path)
+    fo = run_step(runner, t)["o"].float().cpu().numpy()
+    eo = run_step(erunner, te)["o"].float().cpu().numpy()
+    phys = phys_index(forest.seg_len, plan["seg_row"])
+    same = bool(np.array_equal(fo[phys][erows], eo[ephys]))
+    C = forest.n_rows
+    S = int(lens.sum())
+    return {"workload": "4 agentic trees, ~32k compact tokens, H=16, d=128, bf16, fwd+bwd "
+                        "with recompute",
+            "C": C, "S": S, "tree_packed_ms": ms_tree, "expanded_ms": ms_exp,
+            "tree_packed_compact_tok_s": C / (ms_tree * 1e-3),
+            "expanded_compact_tok_s": C / (ms_exp * 1e-3),
+            "speedup": ms_exp / ms_tree, "outputs_bitwise_equal": same,
+            "paper_context": "4.81-4.87x F/B/Grad end-to-end speedup, 8x H20-3e, BF16, "
+                             "Ling-3.0-tiny (whole model, not this operator)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, choices=(1, 2, 3))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-expanded", action="store_true")
+    ap.add_argument("--steps-only", action="store_true",
+                    help="run the timed steps only (for profiler runs)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run a plain device copy of this many MiB (counter scale)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"copy probe: {args.copy_probe_mib} MiB read + written, 5 launches")
+        return
+    log(f"[bench] config {args.config}: building workload")
+    forest, cfg, x, plan, t, runner, plan_s = setup(args.config)
+    log(f"[bench] C={plan.info['C']} S={plan.info['S']} R={plan.info['R']} "
+        f"K={plan.info['n_rounds']} seqs={plan.info['n_seq']}")
+    ms, kern = time_steps(runner, t, args.steps, args.warmup, profile=not args.steps_only)
+    log(f"[bench] {ms:.3f} ms/step")
+    if args.steps_only:
+        return
+    H, d = cfg["H"], cfg["d"]
+    el = 2 if cfg["dtype"] == "bf16" else 4
+    C = plan.info["C"]
+    value = C / (ms * 1e-3)
+    alg = algorithmic_bytes(plan, H, d, el)
+    per_step = launches_per_step(plan)
+    kstats = {}
+    for name, (n, tot) in kern.items():
+        steps_seen = max(1, n // max(1, per_step.get(name, 1)))
+        b = alg.get(name, 0) / max(1, per_step.get(name, 1))   # per launch
+        avg_ms = tot / n
+        kstats[name] = {"launches": n, "avg_ms": avg_ms, "share": tot / (ms * args.steps),
+                        "alg_bytes_per_launch": b,
+                        "achieved_GBs": b / (avg_ms * 1e-3) / 1e9}
+    dom = max(kstats, key=lambda k: kstats[k]["avg_ms"] * kstats[k]["launches"])
+    ds = kstats[dom]
+    traffic = read_traffic(dom, f"config{args.config}")
+    flop_tok = H * (98304 + 245760 + 32768) * (d / 128) ** 2  # fwd + bwd + recompute state pass
+    achieved_tflops = C * flop_tok / (ms * 1e-3) / 1e12
+    peak_tf = PEAK_BF16_TFLOPS if el == 2 else PEAK_F32_TFLOPS
+    step_bytes = sum(alg.values())
+    out = {
+        "metric": "compact tokens/s, tree-packed linear-attn fwd+bwd; MFMA util % of peak",
+        "value": value,
+        "unit": "compact tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.config], "C": C, "S": plan.info["S"],
+                   "R": plan.info["R"], "rounds": plan.info["n_rounds"],
+                   "sequences": plan.info["n_seq"], "H": H, "d": d, "chunk": 64},
+        "roofline": {"bound": "hbm", "kernel": dom,
+                     "achieved": ds["achieved_GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ds["achieved_GBs"] / PEAK_HBM_GBS,
+                     "traffic": traffic},
+        "mfma_util_pct": 100.0 * achieved_tflops / peak_tf,
+        "step_alg_GBs": step_bytes / (ms * 1e-3) / 1e9,
+        "plan_ms": plan_s * 1e3,
+        "value_with_plan": C / ((ms + plan_s * 1e3) * 1e-3),
+        "kernels": kstats,
+        "kernel_source_sha": la_source_sha(),
+    }
+    if not args.no_expanded:
+        log("[bench] compact vs expanded (4 trees, ~32k compact tokens)")
+        out["compact_vs_expanded"] = expanded_comparison(max(3, args.steps // 2), 2)
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle, one head)")
+        out["cpu_baseline"] = cpu_baseline(forest, x, cfg)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

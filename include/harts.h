@@ -271,6 +271,24 @@ int harts_replay_reduce(const harts_plan_t* plan, const void* d_blob,
                         const float* replay_grad, void* dk_, void* dv_,
                         float* dg, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Kernel timing (measurement support; not part of the method).  Between
+ * harts_profile_begin and harts_profile_end every kernel the library
+ * launches is bracketed by a pair of HIP events recorded on its own launch
+ * stream.  harts_profile_end waits for those events, sums the elapsed time
+ * per kernel name and fills up to cap entries of out (n_out receives the
+ * number of distinct kernels).  Host-side only; not thread-safe against
+ * concurrent profiling sessions.
+ * ---------------------------------------------------------------------- */
+typedef struct harts_kernel_time {
+  char name[48];
+  int32_t launches;
+  double total_ms;
+} harts_kernel_time;
+
+int harts_profile_begin(void);
+int harts_profile_end(harts_kernel_time* out, int32_t cap, int32_t* n_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,6 +23,7 @@ EXPORTS = (
     "harts_plan_export", "harts_plan_round_info", "harts_plan_blob",
     "harts_la_fwd", "harts_la_bwd", "harts_la_workspace_size",
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
+    "harts_profile_begin", "harts_profile_end",
 )
 
 
@@ -78,6 +79,10 @@ class RoundInfo(C.Structure):
                                  "own_row_begin", "init_idx_off")]
 
 
+class KernelTime(C.Structure):
+    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int32), ("total_ms", C.c_double)]
+
+
 class HartsError(RuntimeError):
     def __init__(self, code, where, msg):
         super().__init__(f"{where} failed ({code}): {msg}")
@@ -130,8 +135,26 @@ def lib():
     L.harts_replay_reduce.restype = C.c_int
     L.harts_replay_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp,
                                       vp, vp]
+    L.harts_profile_begin.restype = C.c_int
+    L.harts_profile_begin.argtypes = []
+    L.harts_profile_end.restype = C.c_int
+    L.harts_profile_end.argtypes = [C.POINTER(KernelTime), i32, C.POINTER(i32)]
     _lib = L
     return L
+
+
+def profile_begin():
+    check(lib().harts_profile_begin(), "harts_profile_begin")
+
+
+def profile_end():
+    """Per-kernel (launches, total ms) since profile_begin, from HIP events."""
+    L = lib()
+    n = C.c_int32()
+    arr = (KernelTime * 64)()
+    check(L.harts_profile_end(arr, 64, C.byref(n)), "harts_profile_end")
+    return {arr[i].name.decode(): (arr[i].launches, arr[i].total_ms)
+            for i in range(min(n.value, 64))}
 
 
 def check(code, where):

@@ -27,7 +27,10 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstring>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "la_common.hpp"
 #include "plan.hpp"
@@ -635,6 +638,47 @@ __global__ void k_replay_reduce(const int32_t* __restrict__ red_rows,
 // ---------------------------------------------------------------------------
 namespace {
 
+// Optional per-launch timing: a pair of events recorded on the launch stream
+// around every kernel while profiling is on (harts_profile_begin/end).
+struct ProfRecord {
+  const char* name;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRecord> g_prof;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t pooled_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct ProfScope {
+  ProfRecord rec{nullptr, nullptr, nullptr};
+  hipStream_t stream;
+  ProfScope(const char* name, hipStream_t s) : stream(s) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof_on) return;
+    rec.name = name;
+    rec.start = pooled_event();
+    rec.stop = pooled_event();
+    if (rec.start) (void)hipEventRecord(rec.start, stream);
+  }
+  ~ProfScope() {
+    if (!rec.name) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (rec.stop) (void)hipEventRecord(rec.stop, stream);
+    if (rec.start && rec.stop) g_prof.push_back(rec);
+  }
+};
+
 int hip_check(const char* where) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
@@ -691,6 +735,7 @@ void launch_fwd_state(const harts_plan_t* p, int32_t round, const Blob& B, int H
                       const void* v, const float* g, const float* S0, float* hbuf, float* bank,
                       float* S_final, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
+  ProfScope ps("k_fwd_state", s);
   hipLaunchKernelGGL((k_fwd_state<T, D>), dim3(L.n_seq * (D / DVT), H), dim3(NTHREADS), 0, s,
                      B.seq_tab, B.replay_row, B.req_chunk, B.req_bank, H,
                      static_cast<const T*>(k), static_cast<const T*>(v), g, S0, hbuf, bank,
@@ -706,6 +751,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   launch_fwd_state<T, D>(p, round, B, H, k, v, g, S0, hbuf, bank, S_final, s);
   if (int rc = hip_check("harts_la_fwd(state)")) return rc;
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
+  ProfScope ps("k_fwd_out", s);
   hipLaunchKernelGGL((k_fwd_out<T, D>), dim3(static_cast<unsigned>(L.n_chunks), H),
                      dim3(NTHREADS), 0, s, B.seq_tab, B.chunk_tab, B.replay_row, H, scale,
                      static_cast<const T*>(q), static_cast<const T*>(k),
@@ -725,11 +771,15 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     launch_fwd_state<T, D>(p, round, B, H, k, v, g, S0, hbuf, nullptr, nullptr, s);
     if (int rc = hip_check("harts_la_bwd(recompute)")) return rc;
   }
+  {
+  ProfScope ps("k_bwd_state", s);
   hipLaunchKernelGGL((k_bwd_state<T, D>), dim3(L.n_seq * (D / DVT), H), dim3(NTHREADS), 0, s,
                      B.seq_tab, B.replay_row, B.req_chunk, B.req_bank, H, scale,
                      static_cast<const T*>(q), g, static_cast<const T*>(dO), hbuf, dS_final,
                      dbank, dhbuf, ipbuf, dS0);
+  }
   if (int rc = hip_check("harts_la_bwd(state)")) return rc;
+  ProfScope ps("k_bwd_grad", s);
   hipLaunchKernelGGL((k_bwd_grad<T, D>), dim3(static_cast<unsigned>(L.n_chunks), H),
                      dim3(NTHREADS), 0, s, B.seq_tab, B.chunk_tab, B.replay_row, H, scale,
                      static_cast<const T*>(q), static_cast<const T*>(k),
@@ -861,6 +911,7 @@ extern "C" int harts_state_gather(const float* src, const int32_t* idx, int32_t 
   const int64_t e4 = elems_per_state / 4;
   const unsigned blocks = static_cast<unsigned>((e4 + 255) / 256);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  ProfScope ps(mode == 0 ? "k_gather" : "k_scatter_add", s);
   if (mode == 0)
     hipLaunchKernelGGL(k_gather, dim3(blocks, n), dim3(256), 0, s,
                        reinterpret_cast<const float4*>(src), idx, e4,
@@ -884,6 +935,7 @@ extern "C" int harts_replay_reduce(const harts_plan_t* p, const void* d_blob, in
   const int32_t* b = static_cast<const int32_t*>(d_blob);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const dim3 grid(static_cast<unsigned>(p->n_red), H);
+  ProfScope ps("k_replay_reduce", s);
   if (dtype == HARTS_BF16) {
     if (dk == 128)
       hipLaunchKernelGGL((k_replay_reduce<bf16, 128>), grid, dim3(256), 0, s, b + p->off_red_rows,
@@ -899,4 +951,49 @@ extern "C" int harts_replay_reduce(const harts_plan_t* p, const void* d_blob, in
                        static_cast<float*>(dk_), static_cast<float*>(dv_), dg);
   }
   return hip_check("harts_replay_reduce");
+}
+
+extern "C" int harts_profile_begin(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = true;
+  return HARTS_OK;
+}
+
+extern "C" int harts_profile_end(harts_kernel_time* out, int32_t cap, int32_t* n_out) {
+  std::vector<ProfRecord> recs;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_on = false;
+    recs.swap(g_prof);
+  }
+  std::vector<harts_kernel_time> agg;
+  int rc = HARTS_OK;
+  for (const ProfRecord& r : recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.stop) != hipSuccess || hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+      set_error("harts_profile_end: event query failed");
+      rc = HARTS_EHIP;
+    }
+    size_t j = 0;
+    while (j < agg.size() && std::strcmp(agg[j].name, r.name) != 0) ++j;
+    if (j == agg.size()) {
+      harts_kernel_time k{};
+      std::strncpy(k.name, r.name, sizeof(k.name) - 1);
+      agg.push_back(k);
+    }
+    agg[j].launches += 1;
+    agg[j].total_ms += ms;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    for (const ProfRecord& r : recs) {
+      g_event_pool.push_back(r.start);
+      g_event_pool.push_back(r.stop);
+    }
+  }
+  const int32_t n = static_cast<int32_t>(agg.size());
+  if (n_out) *n_out = n;
+  if (out)
+    for (int32_t i = 0; i < n && i < cap; ++i) out[i] = agg[i];
+  return rc;
 }

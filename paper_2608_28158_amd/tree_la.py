@@ -46,6 +46,8 @@ class TreeLARunner:
         self.device = torch.device(device)
         if self.device.type != "cuda":
             raise RuntimeError("tree-packed linear attention runs on the GPU only")
+        if self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
         self.scale = float(d ** -0.5 if scale is None else scale)
         self.L = _lib.lib()
         self.blob = plan.blob(self.device)

@@ -5,7 +5,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from workloads import draw_inputs, forest_for_config
+from workloads import config_inputs  # noqa: F401
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
@@ -27,10 +27,3 @@ def phys_index(seg_len, seg_row):
     return phys
 
 
-def config_inputs(idx, s0_scale=0.0):
-    forest, rng, cfg = forest_for_config(idx)
-    n_leaves = len(forest.leaves())
-    n_trees = int(np.sum(forest.parent < 0))
-    x = draw_inputs(forest.n_rows, n_leaves, cfg["H"], cfg["d"], cfg["d"], rng,
-                    dtype=cfg["dtype"], n_trees=n_trees, s0_scale=s0_scale)
-    return forest, cfg, x

@@ -12,4 +12,4 @@ from .trees import (  # noqa: F401
     forest_for_config,
     CONFIGS,
 )
-from .tensors import draw_inputs, to_bf16_roundtrip  # noqa: F401
+from .tensors import config_inputs, draw_inputs, to_bf16_roundtrip  # noqa: F401

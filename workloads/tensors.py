@@ -46,3 +46,14 @@ def draw_inputs(n_rows: int, n_leaves: int, H: int, dk: int, dv: int, rng,
     elif dtype != "f32":
         raise ValueError(dtype)
     return dict(q=q, k=k, v=v, g=g, dO=dO, dS_final=dS_final, S0=S0)
+
+
+def config_inputs(idx, s0_scale=0.0):
+    """Forest, workload table entry and inputs of configuration ``idx``."""
+    from .trees import forest_for_config
+    forest, rng, cfg = forest_for_config(idx)
+    n_leaves = len(forest.leaves())
+    n_trees = int(np.sum(forest.parent < 0))
+    x = draw_inputs(forest.n_rows, n_leaves, cfg["H"], cfg["d"], cfg["d"], rng,
+                    dtype=cfg["dtype"], n_trees=n_trees, s0_scale=s0_scale)
+    return forest, cfg, x
