@@ -3,27 +3,41 @@
 // gfx950.  Recurrence per head (state S: [dk, dv]):
 //     S_t = exp(g_t) S_{t-1} + k_t v_t^T,    o_t = scale * S_t^T q_t.
 // Chunkwise form (Sec. 2.2): for chunk c with start state S_c and in-chunk
-// prefix sums G (G_i = g_0 + ... + g_i),
+// inclusive prefix sums G (G_i = g_0 + ... + g_i, local to the chunk),
 //     O        = scale * ((Q K^T) * exp(G_i - G_j) [j <= i]) V
 //              + scale * diag(exp(G)) Q S_c
 //     S_{c+1}  = exp(G_last) S_c + (K * exp(G_last - G))^T V.
 //
-// Kernels (per round):
-//   k_fwd_state  sequential over the chunks of a sequence, 32 state columns
-//                per workgroup: writes the start state of every chunk (and
-//                the final state) to a chunk-state buffer, the requested
-//                boundary states to the bank and the final state to S_final.
-//   k_fwd_out    one workgroup per (chunk, head): outputs of the own rows.
-//   k_bwd_state  reverse scan of the state adjoint
-//                dS_c = exp(G_last) dS_{c+1} + scale (Q * exp(G))^T dO
-//                (+ the bank gradient injected at requested boundaries),
-//                writes the adjoint at every chunk end, the per-chunk
-//                <S_{c+1}, dS_{c+1}> partial sums and dS0.
-//   k_bwd_grad   one workgroup per (chunk, head): dq, dk, dv, dg.
-//   k_gather / k_scatter_add      state handoff and its adjoint.
-//   k_replay_reduce               replay-row gradients into compact rows.
-// All products run on MFMA (bf16 16x16x32 or f32 16x16x4) with operands
-// staged in LDS; accumulation and states are float32.  No float atomics.
+// Work decomposition.  Every sequence of a round is cut into blocks of
+// consecutive chunks (the planner ends a block at every requested boundary
+// and at most every block_chunks chunks).  One workgroup owns one
+// (block, head) and keeps the whole [d x d] float32 state in MFMA
+// accumulators while it walks the block's chunks; per-chunk states are never
+// written to memory.  Blocks of one sequence are chained by small
+// element-parallel scans over block summaries:
+//
+//   forward   k_fwd_blocksum  state of each block started from zero, and
+//                             its total log-decay Gamma_b;
+//             k_fwd_blockscan S_end[b] = exp(Gamma_b) S_end[b-1] + dS_b,
+//                             which also yields every requested boundary
+//                             state and every final state;
+//             k_fwd_block     outputs of the own rows of each block.
+//   backward  k_bwd_fwdorder  dq (needs S_c, so it walks chunks forward),
+//                             q.dq per row and the block's local adjoint
+//                             U_b = sum_t exp(G_t^blk) scale q_t dO_t^T;
+//             k_bwd_blockscan dS_end[b] by the reverse recurrence
+//                             dS_start[b] = exp(Gamma_b) dS_end[b] + U_b,
+//                             bank gradients injected at requested block
+//                             ends, dS0 per sequence, boundary terms;
+//             k_bwd_revorder  dk, dv (need dS_{c+1}: chunks backward),
+//                             k.dk per row, local suffix sums of dg;
+//             k_dg_carry      adds to dg the contributions of later blocks.
+// dg uses dg_t = sum_{u >= t} (q_u.dq_u - k_u.dk_u) + <dS_final, S_final>
+//              + sum_{requested P > t} <dbank_P, S_P>   (per sequence),
+// which follows from rescaling q and k (adding e to g_t scales q_u by e^e and
+// k_u by e^-e for u >= t).
+// All products run on MFMA (bf16 16x16x32 / 16x16x16 or f32 16x16x4); states
+// and accumulation are float32; no floating-point atomics.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -38,547 +52,712 @@
 namespace harts {
 
 // ---------------------------------------------------------------------------
-// small helpers
-// ---------------------------------------------------------------------------
-template <typename T>
-__device__ inline void load_vec16(T* dst, const T* src) {
-  *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(src);
-}
-
-// State tiles owned by one wave in the scan kernels: the [D x DVT] slice is
-// cut into (D/16) x 2 tiles of 16x16; wave w owns tiles w*TPW .. w*TPW+TPW-1,
-// tile q at rows 16*(q/2), columns 16*(q%2) of the slice.
-template <int D>
-struct ScanTiles {
-  static constexpr int TPW = (D / 16) * (DVT / 16) / NWAVES;
-  __device__ static inline int mt(int w, int i) { return (w * TPW + i) >> 1; }
-  __device__ static inline int nt(int w, int i) { return (w * TPW + i) & 1; }
-};
-
-template <int D>
-__device__ inline void load_state_slice(f32x4* S, const float* src, int tile, int w, int lane) {
-  using ST = ScanTiles<D>;
-#pragma unroll
-  for (int i = 0; i < ST::TPW; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      S[i][r] = src[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT + ST::nt(w, i) * 16 +
-                    acc_col(lane)];
-}
-
-template <int D>
-__device__ inline void store_state_slice(float* dst, const f32x4* S, int tile, int w, int lane) {
-  using ST = ScanTiles<D>;
-#pragma unroll
-  for (int i = 0; i < ST::TPW; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      dst[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT + ST::nt(w, i) * 16 +
-          acc_col(lane)] = S[i][r];
-}
-
-template <int D>
-__device__ inline void add_state_slice(f32x4* S, const float* src, int tile, int w, int lane) {
-  using ST = ScanTiles<D>;
-#pragma unroll
-  for (int i = 0; i < ST::TPW; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      S[i][r] += src[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT +
-                     ST::nt(w, i) * 16 + acc_col(lane)];
-}
-
-// ---------------------------------------------------------------------------
-// forward: state scan
+// chunk staging: global rows -> registers -> LDS tiles
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_fwd_state(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ replay_row,
-    const int32_t* __restrict__ req_chunk, const int32_t* __restrict__ req_bank, int H,
-    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ S0, float* __restrict__ hbuf, float* __restrict__ bank,
-    float* __restrict__ S_final) {
-  constexpr int NTILE = D / DVT;
-  constexpr int LD = CB + Elem<T>::PAD;
-  constexpr int VE = 16 / sizeof(T);
-  using ST = ScanTiles<D>;
-  const int li = blockIdx.x / NTILE, tile = blockIdx.x % NTILE, h = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int nc = seq[SEQ_N_CHUNKS];
-  const int64_t hb0 = static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + li;
-  const int64_t SS = static_cast<int64_t>(D) * D;
+struct Stage {
+  static constexpr int VE = 16 / sizeof(T);          // elements per 16-byte vector
+  static constexpr int VPR = D / VE;                 // vectors per row
+  static constexpr int NV = CB * VPR / NTHREADS;     // vectors per thread per tensor
+  static constexpr int NT = D / 16;                  // 16-wide tiles along d
+  static constexpr int CPW = NT / NWAVES;            // state column tiles per wave
+  static constexpr int LDR = D + Elem<T>::PAD;       // row-major tile [64][D]
+  static constexpr int LDT = CB + Elem<T>::PAD;      // transposed tile [D][64]
+  static constexpr int LDA = CB + Elem<T>::PAD;      // [64][64] tiles
+};
 
-  __shared__ T Kt[D * LD];    // (K * exp(G_last - G))^T : [dk][j]
-  __shared__ T Vt[DVT * LD];  // V slice transposed      : [dv][j]
+union Vec16 {
+  uint4 u;
+  float f[4];
+  bf16 b[8];
+};
+
+template <typename T>
+__device__ inline T vget(const Vec16& v, int e);
+template <>
+__device__ inline float vget<float>(const Vec16& v, int e) { return v.f[e]; }
+template <>
+__device__ inline bf16 vget<bf16>(const Vec16& v, int e) { return v.b[e]; }
+
+// Load this thread's vectors of one tensor for the chunk's rows; rows whose
+// kind is below min_kind (padding; replay rows for q and dO) read as zero.
+template <typename T, int D>
+__device__ inline void load_chunk(Vec16* r, const T* __restrict__ src,
+                                  const ChunkRows& cr, int H, int h, int t, int min_kind) {
+  using S = Stage<T, D>;
+#pragma unroll
+  for (int i = 0; i < S::NV; ++i) {
+    const int idx = t + i * NTHREADS;
+    const int row = idx / S::VPR, d0 = (idx % S::VPR) * S::VE;
+    if (cr.kind[row] >= min_kind)
+      r[i].u = *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(cr.row[row]) * H + h) * D + d0);
+    else
+      r[i].u = make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+template <typename T, int D>
+__device__ inline void store_rowmajor(T* dst, const Vec16* r, int t) {
+  using S = Stage<T, D>;
+#pragma unroll
+  for (int i = 0; i < S::NV; ++i) {
+    const int idx = t + i * NTHREADS;
+    const int row = idx / S::VPR, d0 = (idx % S::VPR) * S::VE;
+    *reinterpret_cast<uint4*>(dst + row * S::LDR + d0) = r[i].u;
+  }
+}
+
+// dst[d][row] = src[row][d] * scale[row] (scale == nullptr: no scaling)
+template <typename T, int D>
+__device__ inline void store_transposed(T* dst, const Vec16* r,
+                                        const float* scale, int t) {
+  using S = Stage<T, D>;
+#pragma unroll
+  for (int i = 0; i < S::NV; ++i) {
+    const int idx = t + i * NTHREADS;
+    const int row = idx / S::VPR, d0 = (idx % S::VPR) * S::VE;
+    if (scale) {
+      const float sc = scale[row];
+#pragma unroll
+      for (int e = 0; e < S::VE; ++e)
+        dst[(d0 + e) * S::LDT + row] = Elem<T>::from_f(Elem<T>::to_f(vget<T>(r[i], e)) * sc);
+    } else {
+#pragma unroll
+      for (int e = 0; e < S::VE; ++e) dst[(d0 + e) * S::LDT + row] = vget<T>(r[i], e);
+    }
+  }
+}
+
+// Row table of chunk c of a sequence plus the in-chunk prefix sums of g.
+__device__ inline void chunk_setup(ChunkRows& cr, float* G, const int32_t* seq, int c,
+                                   const int32_t* replay_row, const float* g, int H, int h,
+                                   int t) {
+  resolve_rows(cr, seq, c, replay_row, t);
+  chunk_cumsum(G, cr, g, H, h, t);  // same threads (wave 0) that resolved the rows
+}
+
+// A state held as tiles: tile (mt, nt) is rows 16*mt.., cols 16*nt.. of a
+// [D x D] matrix; wave w owns column tiles [w*CPW, (w+1)*CPW) of every row.
+template <int D>
+struct StateTiles {
+  static constexpr int NT = D / 16;
+  static constexpr int CPW = NT / NWAVES;
+  static constexpr int N = NT * CPW;  // tiles per wave
+  __device__ static inline int mt(int i) { return i / CPW; }
+  __device__ static inline int nt(int w, int i) { return w * CPW + i % CPW; }
+};
+
+// Load a [D x D] row-major float32 state into tiles; transpose: tile holds
+// src^T.
+template <int D>
+__device__ inline void state_load(f32x4* S, const float* src, bool transpose, int w, int lane) {
+  using ST = StateTiles<D>;
+#pragma unroll
+  for (int i = 0; i < ST::N; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int a = ST::mt(i) * 16 + acc_row(lane, r), b = ST::nt(w, i) * 16 + acc_col(lane);
+      S[i][r] = src ? (transpose ? src[b * D + a] : src[a * D + b]) : 0.f;
+    }
+}
+
+template <int D>
+__device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) {
+  using ST = StateTiles<D>;
+#pragma unroll
+  for (int i = 0; i < ST::N; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      dst[(ST::mt(i) * 16 + acc_row(lane, r)) * D + ST::nt(w, i) * 16 + acc_col(lane)] = S[i][r];
+}
+
+// ---------------------------------------------------------------------------
+// forward: block summaries (state of the block started from zero)
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(NTHREADS) void k_fwd_blocksum(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ replay_row, int H, const T* __restrict__ k,
+    const T* __restrict__ v, const float* __restrict__ g, float* __restrict__ dSb,
+    float* __restrict__ gam) {
+  using SG = Stage<T, D>;
+  using ST = StateTiles<D>;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int32_t* seq = seq_tab + bk[BLK_SEQ] * SEQ_WORDS;
+  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  __shared__ T Kt[D * SG::LDT];  // (K * exp(G_last - G))^T : [dk][j]
+  __shared__ T Vt[D * SG::LDT];  // V^T                     : [dv][j]
   __shared__ ChunkRows cr;
   __shared__ float G[CB];
-
-  f32x4 S[ST::TPW];
-  load_state_slice<D>(S, S0 + (static_cast<int64_t>(li) * H + h) * SS, tile, w, lane);
-  int rq = seq[SEQ_REQ_OFF];
-  const int rq_end = rq + seq[SEQ_N_REQ];
-
-  for (int c = 0; c < nc; ++c) {
-    if (hbuf) store_state_slice<D>(hbuf + ((hb0 + c) * H + h) * SS, S, tile, w, lane);
-    if (rq < rq_end && req_chunk[rq] == c) {
-      if (bank) store_state_slice<D>(bank + (static_cast<int64_t>(req_bank[rq]) * H + h) * SS, S,
-                                     tile, w, lane);
-      ++rq;
-    }
-    resolve_rows(cr, seq, c, replay_row, t);
-    __syncthreads();
-    chunk_cumsum(G, cr, g, H, h, t);
+  __shared__ float sk[CB];
+  f32x4 S[ST::N];
+#pragma unroll
+  for (int i = 0; i < ST::N; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float gsum = 0.f;
+  for (int c = c0; c < c0 + nc; ++c) {
+    chunk_setup(cr, G, seq, c, replay_row, g, H, h, t);
     __syncthreads();
     const float GL = G[CB - 1];
-    for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
-      const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
-      alignas(16) T vals[VE];
-      if (cr.kind[row] != ROW_PAD) {
-        load_vec16(vals, k + (static_cast<int64_t>(cr.row[row]) * H + h) * D + d0);
-        const float sc = __expf(GL - G[row]);
-#pragma unroll
-        for (int e = 0; e < VE; ++e) Kt[(d0 + e) * LD + row] = Elem<T>::from_f(Elem<T>::to_f(vals[e]) * sc);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) Kt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
-      }
-    }
-    for (int idx = t; idx < CB * (DVT / VE); idx += NTHREADS) {
-      const int row = idx / (DVT / VE), d0 = (idx % (DVT / VE)) * VE;
-      alignas(16) T vals[VE];
-      if (cr.kind[row] != ROW_PAD) {
-        load_vec16(vals, v + (static_cast<int64_t>(cr.row[row]) * H + h) * D + tile * DVT + d0);
-#pragma unroll
-        for (int e = 0; e < VE; ++e) Vt[(d0 + e) * LD + row] = vals[e];
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) Vt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
-      }
-    }
+    if (t < CB) sk[t] = __expf(GL - G[t]);
+    Vec16 lk[SG::NV], lv[SG::NV];
+    load_chunk<T, D>(lk, k, cr, H, h, t, ROW_REPLAY);
+    load_chunk<T, D>(lv, v, cr, H, h, t, ROW_REPLAY);
+    __syncthreads();
+    store_transposed<T, D>(Kt, lk, sk, t);
+    store_transposed<T, D>(Vt, lv, nullptr, t);
     __syncthreads();
     const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < ST::TPW; ++i) {
+    for (int i = 0; i < ST::N; ++i) {
       S[i] *= dec;
-      Mma<T>::tile(S[i], Kt + ST::mt(w, i) * 16 * LD, LD, Vt + ST::nt(w, i) * 16 * LD, LD, CB, lane);
+      Mma<T>::tile(S[i], Kt + ST::mt(i) * 16 * SG::LDT, SG::LDT, Vt + ST::nt(w, i) * 16 * SG::LDT,
+                   SG::LDT, CB, lane);
     }
+    gsum += GL;
     __syncthreads();
   }
-  if (hbuf) store_state_slice<D>(hbuf + ((hb0 + nc) * H + h) * SS, S, tile, w, lane);
+  state_store<D>(dSb + (static_cast<int64_t>(b) * H + h) * D * D, S, w, lane);
+  if (t == 0) gam[static_cast<int64_t>(b) * H + h] = gsum;
+}
+
+// ---------------------------------------------------------------------------
+// forward: chain the blocks of every sequence (element-parallel)
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(NTHREADS) void k_fwd_blockscan(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
+    const float* __restrict__ S0, const float* __restrict__ dSb, const float* __restrict__ gam,
+    float* __restrict__ S_end, float* __restrict__ bank, float* __restrict__ S_final) {
+  constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
+  constexpr int NSW = static_cast<int>(SS4 / NTHREADS);
+  const int li = blockIdx.x / NSW, part = blockIdx.x % NSW, h = blockIdx.y;
+  const int64_t e4 = static_cast<int64_t>(part) * NTHREADS + threadIdx.x;
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
+  float4 s = reinterpret_cast<const float4*>(S0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4];
+  for (int b = b0; b < b0 + nb; ++b) {
+    const int64_t bi = (static_cast<int64_t>(b) * H + h);
+    const float dec = __expf(gam[bi]);
+    const float4 x = reinterpret_cast<const float4*>(dSb)[bi * SS4 + e4];
+    s.x = dec * s.x + x.x;
+    s.y = dec * s.y + x.y;
+    s.z = dec * s.z + x.z;
+    s.w = dec * s.w + x.w;
+    reinterpret_cast<float4*>(S_end)[bi * SS4 + e4] = s;
+    const int eb = blk_tab[b * BLK_WORDS + BLK_END_BANK];
+    if (eb >= 0 && bank)
+      reinterpret_cast<float4*>(bank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4] = s;
+  }
   if (S_final)
-    store_state_slice<D>(S_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS, S,
-                         tile, w, lane);
+    reinterpret_cast<float4*>(S_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4] = s;
 }
 
 // ---------------------------------------------------------------------------
-// forward: outputs of one chunk
+// forward: outputs of the own rows of a block
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-struct FwdOutSmem {
-  static constexpr int LDQ = D + Elem<T>::PAD;
-  static constexpr int LDV = CB + Elem<T>::PAD;
-  static constexpr int LDH = D + Elem<T>::PAD;
-  static constexpr int LDA = CB + Elem<T>::PAD;
-  T Qs[CB * LDQ];
-  T Ks[CB * LDQ];
-  T Vt[D * LDV];   // [dv][j]
-  T hT[D * LDH];   // S_c^T : [dv][dk]
-  T As[CB * LDA];  // masked Q K^T : [i][j]
+struct FwdSmem {
+  using SG = Stage<T, D>;
+  T Q[CB * SG::LDR];
+  T K[CB * SG::LDR];
+  T Kt[D * SG::LDT];  // (K * exp(G_last - G))^T
+  T Vt[D * SG::LDT];  // V^T
+  T A[CB * SG::LDA];  // masked Q K^T
   ChunkRows cr;
   float G[CB];
+  float sk[CB];  // exp(G_last - G)
+  float eg[CB];  // exp(G)
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_fwd_out(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ chunk_tab,
+__global__ __launch_bounds__(NTHREADS) void k_fwd_block(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ hbuf, T* __restrict__ o) {
-  using SM = FwdOutSmem<T, D>;
-  constexpr int VE = 16 / sizeof(T);
-  __shared__ SM sm;
-  const int ci = blockIdx.x, h = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int li = chunk_tab[2 * ci], c = chunk_tab[2 * ci + 1];
+    const float* __restrict__ S0, const float* __restrict__ S_end, T* __restrict__ o) {
+  using SG = Stage<T, D>;
+  using ST = StateTiles<D>;
+  __shared__ FwdSmem<T, D> sm;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int64_t SS = static_cast<int64_t>(D) * D;
-  resolve_rows(sm.cr, seq, c, replay_row, t);
-  __syncthreads();
-  chunk_cumsum(sm.G, sm.cr, g, H, h, t);
-  for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
-    const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
-    const int kind = sm.cr.kind[row];
-    const int64_t off = (static_cast<int64_t>(sm.cr.row[row]) * H + h) * D + d0;
-    alignas(16) T vals[VE];
-    if (kind == ROW_OWN) load_vec16(vals, q + off);
-    else for (int e = 0; e < VE; ++e) vals[e] = Elem<T>::from_f(0.f);
-    load_vec16(&sm.Qs[row * SM::LDQ + d0], vals);
-    if (kind != ROW_PAD) load_vec16(vals, k + off);
-    else for (int e = 0; e < VE; ++e) vals[e] = Elem<T>::from_f(0.f);
-    load_vec16(&sm.Ks[row * SM::LDQ + d0], vals);
-    if (kind != ROW_PAD) load_vec16(vals, v + off);
-    else for (int e = 0; e < VE; ++e) vals[e] = Elem<T>::from_f(0.f);
-#pragma unroll
-    for (int e = 0; e < VE; ++e) sm.Vt[(d0 + e) * SM::LDV + row] = vals[e];
-  }
-  const float* hc = hbuf + ((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + li + c) * H + h) * SS;
-  for (int idx = t; idx < D * D / 4; idx += NTHREADS) {
-    const int dk = idx / (D / 4), dv0 = (idx % (D / 4)) * 4;
-    const float4 x = *reinterpret_cast<const float4*>(hc + dk * D + dv0);
-    sm.hT[(dv0 + 0) * SM::LDH + dk] = Elem<T>::from_f(x.x);
-    sm.hT[(dv0 + 1) * SM::LDH + dk] = Elem<T>::from_f(x.y);
-    sm.hT[(dv0 + 2) * SM::LDH + dk] = Elem<T>::from_f(x.z);
-    sm.hT[(dv0 + 3) * SM::LDH + dk] = Elem<T>::from_f(x.w);
-  }
-  __syncthreads();
-  // masked attention matrix: wave w owns rows 16w .. 16w+15
-#pragma unroll
-  for (int nt = 0; nt < CB / 16; ++nt) {
-    f32x4 a = {0.f, 0.f, 0.f, 0.f};
-    Mma<T>::tile(a, sm.Qs + 16 * w * SM::LDQ, SM::LDQ, sm.Ks + nt * 16 * SM::LDQ, SM::LDQ, D, lane);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-      const float val = n <= m ? a[r] * __expf(sm.G[m] - sm.G[n]) : 0.f;
-      sm.As[m * SM::LDA + n] = Elem<T>::from_f(val);
+  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  const int64_t DD = static_cast<int64_t>(D) * D;
+  f32x4 S[ST::N];  // S : tile (dk, dv), wave owns dv column tiles
+  state_load<D>(S, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                    : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                false, w, lane);
+  for (int c = c0; c < c0 + nc; ++c) {
+    chunk_setup(sm.cr, sm.G, seq, c, replay_row, g, H, h, t);
+    __syncthreads();
+    const float GL = sm.G[CB - 1];
+    if (t < CB) {
+      sm.sk[t] = __expf(GL - sm.G[t]);
+      sm.eg[t] = __expf(sm.G[t]);
     }
-  }
-  __syncthreads();
-#pragma unroll 2
-  for (int nt = 0; nt < D / 16; ++nt) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    Mma<T>::tile(acc, sm.Qs + 16 * w * SM::LDQ, SM::LDQ, sm.hT + nt * 16 * SM::LDH, SM::LDH, D,
-                 lane);
+    Vec16 lq[SG::NV], lk[SG::NV], lv[SG::NV];
+    load_chunk<T, D>(lq, q, sm.cr, H, h, t, ROW_OWN);
+    load_chunk<T, D>(lk, k, sm.cr, H, h, t, ROW_REPLAY);
+    load_chunk<T, D>(lv, v, sm.cr, H, h, t, ROW_REPLAY);
+    __syncthreads();
+    store_rowmajor<T, D>(sm.Q, lq, t);
+    store_rowmajor<T, D>(sm.K, lk, t);
+    store_transposed<T, D>(sm.Kt, lk, sm.sk, t);
+    store_transposed<T, D>(sm.Vt, lv, nullptr, t);
+    __syncthreads();
+    // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w owns rows 16w..16w+15
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] *= __expf(sm.G[16 * w + acc_row(lane, r)]);
-    Mma<T>::tile(acc, sm.As + 16 * w * SM::LDA, SM::LDA, sm.Vt + nt * 16 * SM::LDV, SM::LDV, CB,
-                 lane);
+    for (int jt = 0; jt < CB / 16; ++jt) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      Mma<T>::tile(a, sm.Q + 16 * w * SG::LDR, SG::LDR, sm.K + jt * 16 * SG::LDR, SG::LDR, D, lane);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * w + acc_row(lane, r);
-      if (sm.cr.kind[m] == ROW_OWN)
-        o[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + nt * 16 + acc_col(lane)] =
-            Elem<T>::from_f(acc[r] * scale);
+      for (int r = 0; r < 4; ++r) {
+        const int m = 16 * w + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+        sm.A[m * SG::LDA + n] = Elem<T>::from_f(n <= m ? a[r] * __expf(sm.G[m] - sm.G[n]) : 0.f);
+      }
     }
+    __syncthreads();
+    // O[:, wave's dv columns] = scale * (diag(exp(G)) Q S_c + A V)
+    for (int it = 0; it < CB / 16; ++it) {
+#pragma unroll
+      for (int cc = 0; cc < ST::CPW; ++cc) {
+        const int nt = w * ST::CPW + cc;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < ST::NT; ++kt)
+          MmaRegB<T>::step(acc, sm.Q + it * 16 * SG::LDR + kt * 16, SG::LDR, S[kt * ST::CPW + cc], lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
+        Mma<T>::tile(acc, sm.A + it * 16 * SG::LDA, SG::LDA, sm.Vt + nt * 16 * SG::LDT, SG::LDT, CB,
+                     lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = it * 16 + acc_row(lane, r);
+          if (sm.cr.kind[m] == ROW_OWN)
+            o[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + nt * 16 + acc_col(lane)] =
+                Elem<T>::from_f(acc[r] * scale);
+        }
+      }
+    }
+    // S_{c+1} = exp(G_last) S_c + (K * exp(G_last - G))^T V
+    const float dec = __expf(GL);
+#pragma unroll
+    for (int i = 0; i < ST::N; ++i) {
+      S[i] *= dec;
+      Mma<T>::tile(S[i], sm.Kt + ST::mt(i) * 16 * SG::LDT, SG::LDT,
+                   sm.Vt + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+    }
+    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// backward: reverse scan of the state adjoint
+// backward, forward order: dq, q.dq per row and the block's local adjoint
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_bwd_state(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ replay_row,
-    const int32_t* __restrict__ req_chunk, const int32_t* __restrict__ req_bank, int H,
-    float scale, const T* __restrict__ q, const float* __restrict__ g, const T* __restrict__ dO,
-    const float* __restrict__ hbuf, const float* __restrict__ dS_final,
-    const float* __restrict__ dbank, float* __restrict__ dhbuf, float* __restrict__ ipbuf,
-    float* __restrict__ dS0) {
-  constexpr int NTILE = D / DVT;
-  constexpr int LD = CB + Elem<T>::PAD;
-  constexpr int VE = 16 / sizeof(T);
-  using ST = ScanTiles<D>;
-  const int li = blockIdx.x / NTILE, tile = blockIdx.x % NTILE, h = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+struct BfSmem {
+  using SG = Stage<T, D>;
+  T dO[CB * SG::LDR];
+  T V[CB * SG::LDR];
+  T Kt[D * SG::LDT];   // K^T
+  T Vs[D * SG::LDT];   // (V * exp(G_last - G))^T
+  T Qt[D * SG::LDT];   // Q^T (own rows)
+  T dOs[D * SG::LDT];  // (dO * exp(G_blk) * scale)^T, G_blk counted from the block start
+  T dA[CB * SG::LDA];
+  ChunkRows cr;
+  float G[CB];
+  float sv[CB];  // exp(G_last - G)
+  float eg[CB];  // exp(G) * scale
+  float su[CB];  // exp(G_blk) * scale
+  float rq[NWAVES][CB];
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(NTHREADS) void k_bwd_fwdorder(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
+    const T* __restrict__ dO, const float* __restrict__ S0, const float* __restrict__ S_end,
+    T* __restrict__ dq, float* __restrict__ rq_out, float* __restrict__ U_out) {
+  using SG = Stage<T, D>;
+  using ST = StateTiles<D>;
+  __shared__ BfSmem<T, D> sm;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int nc = seq[SEQ_N_CHUNKS];
-  const int64_t c0 = seq[SEQ_CHUNK_OFF];
-  const int64_t hb0 = c0 + li;
-  const int64_t SS = static_cast<int64_t>(D) * D;
-
-  __shared__ T Qt[D * LD];    // (Q * exp(G) * scale)^T : [dk][i]
-  __shared__ T dOt[DVT * LD]; // dO slice transposed     : [dv][i]
-  __shared__ ChunkRows cr;
-  __shared__ float G[CB];
-  __shared__ float red[NWAVES];
-
-  f32x4 dS[ST::TPW];
-  load_state_slice<D>(dS, dS_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS,
-                      tile, w, lane);
-  const int rq_begin = seq[SEQ_REQ_OFF];
-  int rq = rq_begin + seq[SEQ_N_REQ] - 1;
-
-  for (int c = nc - 1; c >= 0; --c) {
-    // adjoint at the end of chunk c and its inner product with S_{c+1}
-    store_state_slice<D>(dhbuf + ((c0 + c) * H + h) * SS, dS, tile, w, lane);
-    {
-      const float* hn = hbuf + ((hb0 + c + 1) * H + h) * SS;
-      float part = 0.f;
+  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  const int64_t DD = static_cast<int64_t>(D) * D;
+  f32x4 St[ST::N];  // S^T : tile (dv, dk), wave owns dk column tiles
+  f32x4 U[ST::N];   // U   : tile (dk, dv), wave owns dv column tiles
+  state_load<D>(St, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                     : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                true, w, lane);
 #pragma unroll
-      for (int i = 0; i < ST::TPW; ++i)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          part += dS[i][r] * hn[(ST::mt(w, i) * 16 + acc_row(lane, r)) * D + tile * DVT +
-                                ST::nt(w, i) * 16 + acc_col(lane)];
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) part += __shfl_xor(part, off, 64);
-      if (lane == 0) red[w] = part;
-    }
-    resolve_rows(cr, seq, c, replay_row, t);
+  for (int i = 0; i < ST::N; ++i) U[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float Gs = 0.f;  // log-decay from the block start to the current chunk start
+  for (int c = c0; c < c0 + nc; ++c) {
+    chunk_setup(sm.cr, sm.G, seq, c, replay_row, g, H, h, t);
     __syncthreads();
-    if (t == 0) {
+    const float GL = sm.G[CB - 1];
+    if (t < CB) {
+      sm.sv[t] = __expf(GL - sm.G[t]);
+      sm.eg[t] = __expf(sm.G[t]) * scale;
+      sm.su[t] = __expf(Gs + sm.G[t]) * scale;
+    }
+    Vec16 lq[SG::NV], lk[SG::NV], lv[SG::NV], ld[SG::NV];
+    load_chunk<T, D>(lq, q, sm.cr, H, h, t, ROW_OWN);
+    load_chunk<T, D>(lk, k, sm.cr, H, h, t, ROW_REPLAY);
+    load_chunk<T, D>(lv, v, sm.cr, H, h, t, ROW_REPLAY);
+    load_chunk<T, D>(ld, dO, sm.cr, H, h, t, ROW_OWN);
+    __syncthreads();
+    store_rowmajor<T, D>(sm.dO, ld, t);
+    store_rowmajor<T, D>(sm.V, lv, t);
+    store_transposed<T, D>(sm.Kt, lk, nullptr, t);
+    store_transposed<T, D>(sm.Vs, lv, sm.sv, t);
+    store_transposed<T, D>(sm.Qt, lq, nullptr, t);
+    store_transposed<T, D>(sm.dOs, ld, sm.su, t);
+    __syncthreads();
+    // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w owns rows 16w..
+#pragma unroll
+    for (int jt = 0; jt < CB / 16; ++jt) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      Mma<T>::tile(a, sm.dO + 16 * w * SG::LDR, SG::LDR, sm.V + jt * 16 * SG::LDR, SG::LDR, D, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = 16 * w + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+        sm.dA[m * SG::LDA + n] =
+            Elem<T>::from_f(n <= m ? a[r] * __expf(sm.G[m] - sm.G[n]) * scale : 0.f);
+      }
+    }
+    __syncthreads();
+    // dq[:, wave's dk columns] = scale diag(exp(G)) dO S_c^T + dA K
+    for (int it = 0; it < CB / 16; ++it) {
+      float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cc = 0; cc < ST::CPW; ++cc) {
+        const int nt = w * ST::CPW + cc;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < ST::NT; ++kt)
+          MmaRegB<T>::step(acc, sm.dO + it * 16 * SG::LDR + kt * 16, SG::LDR, St[kt * ST::CPW + cc], lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
+        Mma<T>::tile(acc, sm.dA + it * 16 * SG::LDA, SG::LDA, sm.Kt + nt * 16 * SG::LDT, SG::LDT, CB,
+                     lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = it * 16 + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+          part[r] += Elem<T>::to_f(sm.Qt[n * SG::LDT + m]) * acc[r];
+          if (sm.cr.kind[m] == ROW_OWN)
+            dq[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float s = sum16(part[r]);
+        if ((lane & 15) == 0) sm.rq[w][it * 16 + acc_row(lane, r)] = s;
+      }
+    }
+    // U += (Q * exp(G_blk) * scale)^T dO ; S^T <- exp(G_last) S^T + (V * exp(G_last - G))^T K
+    const float dec = __expf(GL);
+#pragma unroll
+    for (int i = 0; i < ST::N; ++i) {
+      Mma<T>::tile(U[i], sm.Qt + ST::mt(i) * 16 * SG::LDT, SG::LDT,
+                   sm.dOs + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+      St[i] *= dec;
+      Mma<T>::tile(St[i], sm.Vs + ST::mt(i) * 16 * SG::LDT, SG::LDT,
+                   sm.Kt + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+    }
+    __syncthreads();
+    if (t < CB) {
       float s = 0.f;
-      for (int i = 0; i < NWAVES; ++i) s += red[i];
-      ipbuf[((c0 + c) * H + h) * NTILE + tile] = s;
-    }
-    chunk_cumsum(G, cr, g, H, h, t);
-    __syncthreads();
-    for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
-      const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
-      alignas(16) T vals[VE];
-      if (cr.kind[row] == ROW_OWN) {
-        load_vec16(vals, q + (static_cast<int64_t>(cr.row[row]) * H + h) * D + d0);
-        const float sc = __expf(G[row]) * scale;
 #pragma unroll
-        for (int e = 0; e < VE; ++e) Qt[(d0 + e) * LD + row] = Elem<T>::from_f(Elem<T>::to_f(vals[e]) * sc);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) Qt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
-      }
+      for (int i = 0; i < NWAVES; ++i) s += sm.rq[i][t];
+      rq_out[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] = s;
     }
-    for (int idx = t; idx < CB * (DVT / VE); idx += NTHREADS) {
-      const int row = idx / (DVT / VE), d0 = (idx % (DVT / VE)) * VE;
-      alignas(16) T vals[VE];
-      if (cr.kind[row] == ROW_OWN) {
-        load_vec16(vals, dO + (static_cast<int64_t>(cr.row[row]) * H + h) * D + tile * DVT + d0);
-#pragma unroll
-        for (int e = 0; e < VE; ++e) dOt[(d0 + e) * LD + row] = vals[e];
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) dOt[(d0 + e) * LD + row] = Elem<T>::from_f(0.f);
-      }
-    }
-    __syncthreads();
-    const float dec = __expf(G[CB - 1]);
-#pragma unroll
-    for (int i = 0; i < ST::TPW; ++i) {
-      dS[i] *= dec;
-      Mma<T>::tile(dS[i], Qt + ST::mt(w, i) * 16 * LD, LD, dOt + ST::nt(w, i) * 16 * LD, LD, CB,
-                   lane);
-    }
-    if (c >= 1 && rq >= rq_begin && req_chunk[rq] == c) {
-      add_state_slice<D>(dS, dbank + (static_cast<int64_t>(req_bank[rq]) * H + h) * SS, tile, w,
-                         lane);
-      --rq;
-    }
-    __syncthreads();
+    Gs += GL;
   }
-  store_state_slice<D>(dS0 + (static_cast<int64_t>(li) * H + h) * SS, dS, tile, w, lane);
+  state_store<D>(U_out + (static_cast<int64_t>(b) * H + h) * DD, U, w, lane);
 }
 
 // ---------------------------------------------------------------------------
-// backward: gradients of one chunk
+// backward: reverse chain over the blocks of every sequence (element-parallel)
+// ---------------------------------------------------------------------------
+__device__ inline float block_sum(float x, float* red, int t) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  __syncthreads();
+  if ((t & 63) == 0) red[t >> 6] = x;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NWAVES; ++i) s += red[i];
+  return s;
+}
+
+template <int D>
+__global__ __launch_bounds__(NTHREADS) void k_bwd_blockscan(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
+    const float* __restrict__ dS_final, const float* __restrict__ dbank,
+    const float* __restrict__ S_end, const float* __restrict__ U, const float* __restrict__ gam,
+    float* __restrict__ dS_end, float* __restrict__ dS0, float* __restrict__ betap) {
+  constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
+  constexpr int NSW = static_cast<int>(SS4 / NTHREADS);
+  __shared__ float red[NWAVES];
+  const int li = blockIdx.x / NSW, part = blockIdx.x % NSW, h = blockIdx.y, t = threadIdx.x;
+  const int64_t e4 = static_cast<int64_t>(part) * NTHREADS + t;
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
+  const float4* S4 = reinterpret_cast<const float4*>(S_end);
+  float4 ds = reinterpret_cast<const float4*>(dS_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4];
+  {
+    const int bl = b0 + nb - 1;
+    const float4 s = S4[(static_cast<int64_t>(bl) * H + h) * SS4 + e4];
+    const float bsum = block_sum(ds.x * s.x + ds.y * s.y + ds.z * s.z + ds.w * s.w, red, t);
+    if (t == 0) betap[(static_cast<int64_t>(bl) * H + h) * NSW + part] = bsum;
+  }
+  for (int b = b0 + nb - 1; b >= b0; --b) {
+    const int64_t bi = static_cast<int64_t>(b) * H + h;
+    reinterpret_cast<float4*>(dS_end)[bi * SS4 + e4] = ds;
+    const float dec = __expf(gam[bi]);
+    const float4 u = reinterpret_cast<const float4*>(U)[bi * SS4 + e4];
+    ds.x = dec * ds.x + u.x;
+    ds.y = dec * ds.y + u.y;
+    ds.z = dec * ds.z + u.z;
+    ds.w = dec * ds.w + u.w;
+    if (b > b0) {
+      const int64_t pi = static_cast<int64_t>(b - 1) * H + h;
+      const int eb = blk_tab[(b - 1) * BLK_WORDS + BLK_END_BANK];
+      float dot = 0.f;
+      if (eb >= 0) {
+        const float4 inj = reinterpret_cast<const float4*>(dbank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4];
+        const float4 s = S4[pi * SS4 + e4];
+        dot = inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w;
+        ds.x += inj.x;
+        ds.y += inj.y;
+        ds.z += inj.z;
+        ds.w += inj.w;
+      }
+      const float bsum = eb >= 0 ? block_sum(dot, red, t) : 0.f;
+      if (t == 0) betap[pi * NSW + part] = bsum;
+    }
+  }
+  reinterpret_cast<float4*>(dS0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4] = ds;
+}
+
+// ---------------------------------------------------------------------------
+// backward, reverse order: dk, dv, k.dk and local suffix sums of dg
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-struct BwdSmem {
-  static constexpr int LDQ = D + Elem<T>::PAD;
-  static constexpr int LDA = CB + Elem<T>::PAD;
-  static constexpr int LDT = CB + Elem<T>::PAD;
-  static constexpr int LDS = D + Elem<T>::PAD;
-  T Qs[CB * LDQ];
-  T Ks[CB * LDQ];
-  T Vs[CB * LDQ];
-  T dOs[CB * LDQ];
-  T At[CB * LDA];   // A^T   : [j][i]
-  T dAs[CB * LDA];  // dA    : [i][j]
-  T dAt[CB * LDA];  // dA^T  : [j][i]
-  T TR[D * LDT];    // K^T, then Q^T, then dO^T : [d][row]
-  T SR[D * LDS];    // S_c, then dS_{c+1}, then dS_{c+1}^T
+struct BrSmem {
+  using SG = Stage<T, D>;
+  T Q[CB * SG::LDR];
+  T K[CB * SG::LDR];
+  T V[CB * SG::LDR];
+  T dO[CB * SG::LDR];
+  T Qt[D * SG::LDT];   // Q^T (own rows)
+  T Qs[D * SG::LDT];   // (Q * exp(G) * scale)^T
+  T dOt[D * SG::LDT];  // dO^T
+  T At[CB * SG::LDA];  // A^T
+  T dAt[CB * SG::LDA]; // dA^T
   ChunkRows cr;
   float G[CB];
-  float dgb[CB];
+  float sk[CB];  // exp(G_last - G)
+  float eg[CB];  // exp(G) * scale
+  float rk[NWAVES][CB];
 };
 
 template <typename T, int D>
-__device__ inline void transpose_rows(T* dst, int ldd, const T* src, int lds, int t) {
-  for (int idx = t; idx < CB * D; idx += NTHREADS) {
-    const int d = idx % D, row = idx / D;
-    dst[d * ldd + row] = src[row * lds + d];
-  }
-}
-
-template <typename T, int D>
-__device__ inline void load_state_lds(T* dst, int ldd, const float* src, bool transpose, int t) {
-  for (int idx = t; idx < D * D / 4; idx += NTHREADS) {
-    const int a = idx / (D / 4), b0 = (idx % (D / 4)) * 4;
-    const float4 x = *reinterpret_cast<const float4*>(src + a * D + b0);
-    if (!transpose) {
-      dst[a * ldd + b0 + 0] = Elem<T>::from_f(x.x);
-      dst[a * ldd + b0 + 1] = Elem<T>::from_f(x.y);
-      dst[a * ldd + b0 + 2] = Elem<T>::from_f(x.z);
-      dst[a * ldd + b0 + 3] = Elem<T>::from_f(x.w);
-    } else {
-      dst[(b0 + 0) * ldd + a] = Elem<T>::from_f(x.x);
-      dst[(b0 + 1) * ldd + a] = Elem<T>::from_f(x.y);
-      dst[(b0 + 2) * ldd + a] = Elem<T>::from_f(x.z);
-      dst[(b0 + 3) * ldd + a] = Elem<T>::from_f(x.w);
-    }
-  }
-}
-
-template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_bwd_grad(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ chunk_tab,
+__global__ __launch_bounds__(NTHREADS) void k_bwd_revorder(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const T* __restrict__ dO, const float* __restrict__ hbuf, const float* __restrict__ dhbuf,
-    const float* __restrict__ ipbuf, T* __restrict__ dq, T* __restrict__ dk,
-    T* __restrict__ dv, float* __restrict__ dg, float* __restrict__ rep_grad) {
-  using SM = BwdSmem<T, D>;
-  constexpr int VE = 16 / sizeof(T);
-  constexpr int NTILE = D / DVT;
-  constexpr int RG = 2 * D + 1;  // replay_grad row: dk | dv | dg
-  __shared__ SM sm;
-  const int ci = blockIdx.x, h = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int li = chunk_tab[2 * ci], c = chunk_tab[2 * ci + 1];
+    const T* __restrict__ dO, const float* __restrict__ dS_end, const float* __restrict__ rq,
+    T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dg, float* __restrict__ rep_grad,
+    float* __restrict__ Rb) {
+  using SG = Stage<T, D>;
+  using ST = StateTiles<D>;
+  constexpr int RG = 2 * D + 1;
+  __shared__ BrSmem<T, D> sm;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int64_t c0 = seq[SEQ_CHUNK_OFF];
-  const int64_t SS = static_cast<int64_t>(D) * D;
-
-  resolve_rows(sm.cr, seq, c, replay_row, t);
-  __syncthreads();
-  chunk_cumsum(sm.G, sm.cr, g, H, h, t);
-  for (int idx = t; idx < CB * (D / VE); idx += NTHREADS) {
-    const int row = idx / (D / VE), d0 = (idx % (D / VE)) * VE;
-    const int kind = sm.cr.kind[row];
-    const int64_t off = (static_cast<int64_t>(sm.cr.row[row]) * H + h) * D + d0;
-    alignas(16) T zero[VE];
-    alignas(16) T vals[VE];
-    for (int e = 0; e < VE; ++e) zero[e] = Elem<T>::from_f(0.f);
-    if (kind == ROW_OWN) { load_vec16(vals, q + off); load_vec16(&sm.Qs[row * SM::LDQ + d0], vals); }
-    else load_vec16(&sm.Qs[row * SM::LDQ + d0], zero);
-    if (kind == ROW_OWN) { load_vec16(vals, dO + off); load_vec16(&sm.dOs[row * SM::LDQ + d0], vals); }
-    else load_vec16(&sm.dOs[row * SM::LDQ + d0], zero);
-    if (kind != ROW_PAD) { load_vec16(vals, k + off); load_vec16(&sm.Ks[row * SM::LDQ + d0], vals); }
-    else load_vec16(&sm.Ks[row * SM::LDQ + d0], zero);
-    if (kind != ROW_PAD) { load_vec16(vals, v + off); load_vec16(&sm.Vs[row * SM::LDQ + d0], vals); }
-    else load_vec16(&sm.Vs[row * SM::LDQ + d0], zero);
-  }
-  __syncthreads();
-  const float GL = sm.G[CB - 1];
-  // A (unscaled) and dA = scale * (dO V^T), both masked; wave w owns rows i in 16w..16w+15
-#pragma unroll
-  for (int nt = 0; nt < CB / 16; ++nt) {
-    f32x4 a = {0.f, 0.f, 0.f, 0.f}, da = {0.f, 0.f, 0.f, 0.f};
-    Mma<T>::tile(a, sm.Qs + 16 * w * SM::LDQ, SM::LDQ, sm.Ks + nt * 16 * SM::LDQ, SM::LDQ, D, lane);
-    Mma<T>::tile(da, sm.dOs + 16 * w * SM::LDQ, SM::LDQ, sm.Vs + nt * 16 * SM::LDQ, SM::LDQ, D,
-                 lane);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-      const float dm = n <= m ? __expf(sm.G[m] - sm.G[n]) : 0.f;
-      const T av = Elem<T>::from_f(a[r] * dm);
-      const T dav = Elem<T>::from_f(da[r] * dm * scale);
-      sm.At[n * SM::LDA + m] = av;
-      sm.dAs[m * SM::LDA + n] = dav;
-      sm.dAt[n * SM::LDA + m] = dav;
-    }
-  }
-  transpose_rows<T, D>(sm.TR, SM::LDT, sm.Ks, SM::LDQ, t);
-  load_state_lds<T, D>(sm.SR, SM::LDS, hbuf + ((c0 + li + c) * H + h) * SS, false, t);
-  __syncthreads();
-
-  // dq = dA K + scale * diag(exp(G)) dO S_c^T
-  float dgp[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int nt = 0; nt < D / 16; ++nt) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    Mma<T>::tile(acc, sm.dOs + 16 * w * SM::LDQ, SM::LDQ, sm.SR + nt * 16 * SM::LDS, SM::LDS, D,
-                 lane);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] *= __expf(sm.G[16 * w + acc_row(lane, r)]) * scale;
-    Mma<T>::tile(acc, sm.dAs + 16 * w * SM::LDA, SM::LDA, sm.TR + nt * 16 * SM::LDT, SM::LDT, CB,
-                 lane);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-      dgp[r] += Elem<T>::to_f(sm.Qs[m * SM::LDQ + n]) * acc[r];
-      if (sm.cr.kind[m] == ROW_OWN)
-        dq[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float s = sum16(dgp[r]);
-    if ((lane & 15) == 0) sm.dgb[16 * w + acc_row(lane, r)] = s;
-    dgp[r] = 0.f;
-  }
-  __syncthreads();
-  transpose_rows<T, D>(sm.TR, SM::LDT, sm.Qs, SM::LDQ, t);
-  load_state_lds<T, D>(sm.SR, SM::LDS, dhbuf + ((c0 + c) * H + h) * SS, false, t);
-  __syncthreads();
-
-  // dk = dA^T Q + diag(exp(G_last - G)) V dS_{c+1}^T
-  for (int nt = 0; nt < D / 16; ++nt) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    Mma<T>::tile(acc, sm.Vs + 16 * w * SM::LDQ, SM::LDQ, sm.SR + nt * 16 * SM::LDS, SM::LDS, D,
-                 lane);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] *= __expf(GL - sm.G[16 * w + acc_row(lane, r)]);
-    Mma<T>::tile(acc, sm.dAt + 16 * w * SM::LDA, SM::LDA, sm.TR + nt * 16 * SM::LDT, SM::LDT, CB,
-                 lane);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-      dgp[r] += Elem<T>::to_f(sm.Ks[m * SM::LDQ + n]) * acc[r];
-      const int kind = sm.cr.kind[m];
-      if (kind == ROW_OWN)
-        dk[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
-      else if (kind == ROW_REPLAY)
-        rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + n] = acc[r];
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float s = sum16(dgp[r]);
-    if ((lane & 15) == 0) sm.dgb[16 * w + acc_row(lane, r)] -= s;
-  }
-  __syncthreads();
-  transpose_rows<T, D>(sm.TR, SM::LDT, sm.dOs, SM::LDQ, t);
-  load_state_lds<T, D>(sm.SR, SM::LDS, dhbuf + ((c0 + c) * H + h) * SS, true, t);
-  __syncthreads();
-
-  // dv = scale * A^T dO + diag(exp(G_last - G)) K dS_{c+1}
+  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  const int64_t DD = static_cast<int64_t>(D) * D;
+  const float* dse = dS_end + (static_cast<int64_t>(b) * H + h) * DD;
+  f32x4 dSt[ST::N];  // dS^T : tile (dv, dk), wave owns dk column tiles
+  f32x4 dSn[ST::N];  // dS   : tile (dk, dv), wave owns dv column tiles
+  state_load<D>(dSt, dse, true, w, lane);
+  state_load<D>(dSn, dse, false, w, lane);
   const float inv_scale = 1.f / scale;
-  for (int nt = 0; nt < D / 16; ++nt) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    Mma<T>::tile(acc, sm.Ks + 16 * w * SM::LDQ, SM::LDQ, sm.SR + nt * 16 * SM::LDS, SM::LDS, D,
-                 lane);
+  float carry = 0.f;  // sum of (q.dq - k.dk) over the later chunks of the block
+  for (int c = c0 + nc - 1; c >= c0; --c) {
+    chunk_setup(sm.cr, sm.G, seq, c, replay_row, g, H, h, t);
+    __syncthreads();
+    const float GL = sm.G[CB - 1];
+    if (t < CB) {
+      sm.sk[t] = __expf(GL - sm.G[t]);
+      sm.eg[t] = __expf(sm.G[t]) * scale;
+    }
+    Vec16 lq[SG::NV], lk[SG::NV], lv[SG::NV], ld[SG::NV];
+    load_chunk<T, D>(lq, q, sm.cr, H, h, t, ROW_OWN);
+    load_chunk<T, D>(lk, k, sm.cr, H, h, t, ROW_REPLAY);
+    load_chunk<T, D>(lv, v, sm.cr, H, h, t, ROW_REPLAY);
+    load_chunk<T, D>(ld, dO, sm.cr, H, h, t, ROW_OWN);
+    __syncthreads();
+    store_rowmajor<T, D>(sm.Q, lq, t);
+    store_rowmajor<T, D>(sm.K, lk, t);
+    store_rowmajor<T, D>(sm.V, lv, t);
+    store_rowmajor<T, D>(sm.dO, ld, t);
+    store_transposed<T, D>(sm.Qt, lq, nullptr, t);
+    store_transposed<T, D>(sm.Qs, lq, sm.eg, t);
+    store_transposed<T, D>(sm.dOt, ld, nullptr, t);
+    __syncthreads();
+    // A and dA (masked), stored transposed; wave w owns rows i in 16w..
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] *= __expf(GL - sm.G[16 * w + acc_row(lane, r)]) * inv_scale;
-    Mma<T>::tile(acc, sm.At + 16 * w * SM::LDA, SM::LDA, sm.TR + nt * 16 * SM::LDT, SM::LDT, CB,
-                 lane);
+    for (int jt = 0; jt < CB / 16; ++jt) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f}, da = {0.f, 0.f, 0.f, 0.f};
+      Mma<T>::tile(a, sm.Q + 16 * w * SG::LDR, SG::LDR, sm.K + jt * 16 * SG::LDR, SG::LDR, D, lane);
+      Mma<T>::tile(da, sm.dO + 16 * w * SG::LDR, SG::LDR, sm.V + jt * 16 * SG::LDR, SG::LDR, D, lane);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * w + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-      const float val = acc[r] * scale;
-      const int kind = sm.cr.kind[m];
-      if (kind == ROW_OWN)
-        dv[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(val);
+      for (int r = 0; r < 4; ++r) {
+        const int m = 16 * w + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+        const float dm = n <= m ? __expf(sm.G[m] - sm.G[n]) : 0.f;
+        sm.At[n * SG::LDA + m] = Elem<T>::from_f(a[r] * dm);
+        sm.dAt[n * SG::LDA + m] = Elem<T>::from_f(da[r] * dm * scale);
+      }
+    }
+    __syncthreads();
+    // dk[:, wave's dk columns] = diag(exp(G_last - G)) V dS^T + dA^T Q
+    for (int jt = 0; jt < CB / 16; ++jt) {
+      float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cc = 0; cc < ST::CPW; ++cc) {
+        const int nt = w * ST::CPW + cc;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < ST::NT; ++kt)
+          MmaRegB<T>::step(acc, sm.V + jt * 16 * SG::LDR + kt * 16, SG::LDR, dSt[kt * ST::CPW + cc], lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)];
+        Mma<T>::tile(acc, sm.dAt + jt * 16 * SG::LDA, SG::LDA, sm.Qt + nt * 16 * SG::LDT, SG::LDT, CB,
+                     lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = jt * 16 + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+          part[r] += Elem<T>::to_f(sm.K[m * SG::LDR + n]) * acc[r];
+          const int kind = sm.cr.kind[m];
+          if (kind == ROW_OWN)
+            dk[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+          else if (kind == ROW_REPLAY)
+            rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + n] = acc[r];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float s = sum16(part[r]);
+        if ((lane & 15) == 0) sm.rk[w][jt * 16 + acc_row(lane, r)] = s;
+      }
+    }
+    // dv[:, wave's dv columns] = diag(exp(G_last - G)) K dS + scale A^T dO
+    for (int jt = 0; jt < CB / 16; ++jt) {
+#pragma unroll
+      for (int cc = 0; cc < ST::CPW; ++cc) {
+        const int nt = w * ST::CPW + cc;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < ST::NT; ++kt)
+          MmaRegB<T>::step(acc, sm.K + jt * 16 * SG::LDR + kt * 16, SG::LDR, dSn[kt * ST::CPW + cc], lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)] * inv_scale;
+        Mma<T>::tile(acc, sm.At + jt * 16 * SG::LDA, SG::LDA, sm.dOt + nt * 16 * SG::LDT, SG::LDT, CB,
+                     lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = jt * 16 + acc_row(lane, r), n = nt * 16 + acc_col(lane);
+          const float val = acc[r] * scale;
+          const int kind = sm.cr.kind[m];
+          if (kind == ROW_OWN)
+            dv[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(val);
+          else if (kind == ROW_REPLAY)
+            rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + D + n] = val;
+        }
+      }
+    }
+    // dS_c = exp(G_last) dS_{c+1} + (Q * exp(G) * scale)^T dO, in both layouts
+    const float dec = __expf(GL);
+#pragma unroll
+    for (int i = 0; i < ST::N; ++i) {
+      dSn[i] *= dec;
+      Mma<T>::tile(dSn[i], sm.Qs + ST::mt(i) * 16 * SG::LDT, SG::LDT,
+                   sm.dOt + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+      dSt[i] *= dec;
+      Mma<T>::tile(dSt[i], sm.dOt + ST::mt(i) * 16 * SG::LDT, SG::LDT,
+                   sm.Qs + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+    }
+    __syncthreads();
+    // local suffix sums of q.dq - k.dk (wave 0, one row per lane)
+    if (t < CB) {
+      const int kind = sm.cr.kind[t];
+      float x = 0.f;
+      if (kind != ROW_PAD) {
+        float rks = 0.f;
+#pragma unroll
+        for (int i = 0; i < NWAVES; ++i) rks += sm.rk[i][t];
+        x = rq[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] - rks;
+      }
+#pragma unroll
+      for (int off = 1; off < CB; off <<= 1) {
+        const float y = __shfl_down(x, off, CB);
+        if (t + off < CB) x += y;
+      }
+      const float val = x + carry;
+      if (kind == ROW_OWN) dg[static_cast<int64_t>(sm.cr.row[t]) * H + h] = val;
       else if (kind == ROW_REPLAY)
-        rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + D + n] = val;
+        rep_grad[(static_cast<int64_t>(sm.cr.rep[t]) * H + h) * RG + 2 * D] = val;
+      carry += __shfl(x, 0, CB);
     }
   }
-  // dg_t = sum_{u >= t in chunk} (q_u.dq_u - k_u.dk_u) + <S_{c+1}, dS_{c+1}>
-  if (t < CB) {
-    float x = sm.dgb[t];
-#pragma unroll
-    for (int off = 1; off < CB; off <<= 1) {
-      const float y = __shfl_down(x, off, CB);
-      if (t + off < CB) x += y;
-    }
-    float ip = 0.f;
-#pragma unroll
-    for (int i = 0; i < NTILE; ++i) ip += ipbuf[((c0 + c) * H + h) * NTILE + i];
-    const int kind = sm.cr.kind[t];
-    if (kind == ROW_OWN) dg[static_cast<int64_t>(sm.cr.row[t]) * H + h] = x + ip;
-    else if (kind == ROW_REPLAY)
-      rep_grad[(static_cast<int64_t>(sm.cr.rep[t]) * H + h) * RG + 2 * D] = x + ip;
-  }
+  if (t == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
 }
 
 // ---------------------------------------------------------------------------
+// dg: add the contributions of later blocks and of the boundary terms
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(NTHREADS) void k_dg_carry(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ replay_row, int H, const float* __restrict__ betap,
+    const float* __restrict__ Rb, float* __restrict__ dg, float* __restrict__ rep_grad) {
+  constexpr int NSW = D * D / 4 / NTHREADS;
+  constexpr int RG = 2 * D + 1;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int32_t* seq = seq_tab + bk[BLK_SEQ] * SEQ_WORDS;
+  const int b_end = seq[SEQ_BLK_OFF] + seq[SEQ_N_BLK];
+  float carry = 0.f;
+  for (int bb = b; bb < b_end; ++bb) {
+    const int64_t bi = static_cast<int64_t>(bb) * H + h;
+    for (int p = 0; p < NSW; ++p) carry += betap[bi * NSW + p];
+    if (bb > b) carry += Rb[bi];
+  }
+  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  const int n_rep = seq[SEQ_N_REPLAY], n_tok = seq[SEQ_N_TOK];
+  for (int idx = t; idx < nc * CB; idx += NTHREADS) {
+    const int p = c0 * CB + idx;
+    if (p < n_rep) {
+      const int j = seq[SEQ_REPLAY_OFF] + p;
+      rep_grad[(static_cast<int64_t>(j) * H + h) * RG + 2 * D] += carry;
+    } else if (p < n_tok) {
+      dg[(static_cast<int64_t>(seq[SEQ_OWN_ROW]) + (p - n_rep)) * H + h] += carry;
+    }
+  }
+}
+
 // state handoff and replay reduction
 // ---------------------------------------------------------------------------
 __global__ void k_gather(const float4* __restrict__ src, const int32_t* __restrict__ idx,
@@ -692,100 +871,168 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int check_shape(const harts_plan_t* p, int32_t round, int32_t dtype, int32_t H, int32_t dk,
                 int32_t dv, const char* where) {
-  if (!p) { set_error(std::string(where) + ": plan is NULL"); return HARTS_EINVAL; }
-  if (round < 0 || round >= p->K) { set_error(std::string(where) + ": round out of range"); return HARTS_EINVAL; }
-  if (H < 1) { set_error(std::string(where) + ": H must be >= 1"); return HARTS_EINVAL; }
-  if (p->chunk != CB) { set_error(std::string(where) + ": device calls need chunk size 64"); return HARTS_EUNSUPPORTED; }
-  if (dtype != HARTS_F32 && dtype != HARTS_BF16) { set_error(std::string(where) + ": unknown dtype"); return HARTS_EUNSUPPORTED; }
-  if (dk != dv || (dk != 64 && dk != 128)) { set_error(std::string(where) + ": need dk == dv in {64, 128}"); return HARTS_EUNSUPPORTED; }
-  if (dtype == HARTS_F32 && dk != 64) { set_error(std::string(where) + ": float32 path supports d = 64"); return HARTS_EUNSUPPORTED; }
+  const std::string w(where);
+  if (!p) { set_error(w + ": plan is NULL"); return HARTS_EINVAL; }
+  if (round < 0 || round >= p->K) { set_error(w + ": round out of range"); return HARTS_EINVAL; }
+  if (H < 1 || H > 65535) { set_error(w + ": H must be in [1, 65535]"); return HARTS_EINVAL; }
+  if (p->chunk != CB) { set_error(w + ": device calls need chunk size 64"); return HARTS_EUNSUPPORTED; }
+  if (dtype != HARTS_F32 && dtype != HARTS_BF16) { set_error(w + ": unknown dtype"); return HARTS_EUNSUPPORTED; }
+  if (dk != dv || (dk != 64 && dk != 128)) { set_error(w + ": need dk == dv in {64, 128}"); return HARTS_EUNSUPPORTED; }
+  if (dtype == HARTS_F32 && dk != 64) { set_error(w + ": float32 path supports d = 64"); return HARTS_EUNSUPPORTED; }
   return HARTS_OK;
 }
 
-size_t hbuf_bytes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Buffer sizes of one round.
+struct Sizes {
+  size_t blk_state;  // [n_blk, H, D, D] float32
+  size_t gam;        // [n_blk, H] float32
+  size_t rq;         // [n_chunks * 64, H] float32
+  size_t rb;         // [n_blk, H] float32
+  size_t betap;      // [n_blk, H, NSW] float32
+  size_t saved;      // S_end + Gamma
+  size_t ws_fwd;     // block summaries
+  size_t ws_bwd;     // U + dS_end + rq + Rb + betap
+  size_t ws_rec;     // extra for the recompute path: summaries + saved
+};
+
+Sizes sizes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
   const RoundLayout& L = p->rounds[round];
-  return static_cast<size_t>(L.n_chunks + L.n_seq) * H * D * D * sizeof(float);
-}
-size_t dhbuf_bytes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
-  const RoundLayout& L = p->rounds[round];
-  return static_cast<size_t>(L.n_chunks) * H * D * D * sizeof(float);
-}
-size_t ipbuf_bytes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
-  const RoundLayout& L = p->rounds[round];
-  return (static_cast<size_t>(L.n_chunks) * H * (D / DVT) * sizeof(float) + 255) / 256 * 256;
+  Sizes s{};
+  const size_t nsw = static_cast<size_t>(D) * D / 4 / NTHREADS;
+  s.blk_state = align256(static_cast<size_t>(L.n_blk) * H * D * D * sizeof(float));
+  s.gam = align256(static_cast<size_t>(L.n_blk) * H * sizeof(float));
+  s.rq = align256(static_cast<size_t>(L.n_chunks) * CB * H * sizeof(float));
+  s.rb = align256(static_cast<size_t>(L.n_blk) * H * sizeof(float));
+  s.betap = align256(static_cast<size_t>(L.n_blk) * H * nsw * sizeof(float));
+  s.saved = s.blk_state + s.gam;
+  s.ws_fwd = s.blk_state;
+  s.ws_bwd = 2 * s.blk_state + s.rq + s.rb + s.betap;
+  s.ws_rec = s.blk_state + s.saved;
+  return s;
 }
 
 struct Blob {
   const int32_t* seq_tab;
-  const int32_t* chunk_tab;
+  const int32_t* blk_tab;
   const int32_t* replay_row;
-  const int32_t* req_chunk;
-  const int32_t* req_bank;
 };
 
 Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   const int32_t* b = static_cast<const int32_t*>(d_blob);
   const RoundLayout& L = p->rounds[round];
-  return Blob{b + L.seq_tab, b + L.chunk_tab, b + p->off_replay_row, b + p->off_req_chunk,
-              b + p->off_req_bank};
+  return Blob{b + L.seq_tab, b + L.blk_tab, b + p->off_replay_row};
 }
 
+// forward state pass: block summaries then the block chain
 template <typename T, int D>
-void launch_fwd_state(const harts_plan_t* p, int32_t round, const Blob& B, int H, const void* k,
-                      const void* v, const float* g, const float* S0, float* hbuf, float* bank,
-                      float* S_final, hipStream_t s) {
+int launch_state_pass(const harts_plan_t* p, int32_t round, const Blob& B, int H, const void* k,
+                      const void* v, const float* g, const float* S0, float* dSb, float* gam,
+                      float* S_end, float* bank, float* S_final, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
-  ProfScope ps("k_fwd_state", s);
-  hipLaunchKernelGGL((k_fwd_state<T, D>), dim3(L.n_seq * (D / DVT), H), dim3(NTHREADS), 0, s,
-                     B.seq_tab, B.replay_row, B.req_chunk, B.req_bank, H,
-                     static_cast<const T*>(k), static_cast<const T*>(v), g, S0, hbuf, bank,
-                     S_final);
+  {
+    ProfScope ps("k_fwd_blocksum", s);
+    hipLaunchKernelGGL((k_fwd_blocksum<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+                       B.blk_tab, B.replay_row, H, static_cast<const T*>(k),
+                       static_cast<const T*>(v), g, dSb, gam);
+  }
+  if (int rc = hip_check("k_fwd_blocksum")) return rc;
+  {
+    constexpr int NSW = D * D / 4 / NTHREADS;
+    ProfScope ps("k_fwd_blockscan", s);
+    hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(NTHREADS), 0, s,
+                       B.seq_tab, B.blk_tab, H, S0, dSb, gam, S_end, bank, S_final);
+  }
+  return hip_check("k_fwd_blockscan");
 }
 
 template <typename T, int D>
 int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, float scale,
             const void* q, const void* k, const void* v, const float* g, const float* S0, void* o,
-            float* S_final, float* bank, float* hbuf, hipStream_t s) {
+            float* S_final, float* bank, char* saved, char* ws, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
+  const Sizes z = sizes(p, round, H, D);
   const Blob B = blob_ptrs(p, round, d_blob);
-  launch_fwd_state<T, D>(p, round, B, H, k, v, g, S0, hbuf, bank, S_final, s);
-  if (int rc = hip_check("harts_la_fwd(state)")) return rc;
+  float* dSb = reinterpret_cast<float*>(ws);
+  float* S_end = reinterpret_cast<float*>(saved);
+  float* gam = reinterpret_cast<float*>(saved + z.blk_state);
+  if (int rc = launch_state_pass<T, D>(p, round, B, H, k, v, g, S0, dSb, gam, S_end, bank,
+                                        S_final, s))
+    return rc;
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
-  ProfScope ps("k_fwd_out", s);
-  hipLaunchKernelGGL((k_fwd_out<T, D>), dim3(static_cast<unsigned>(L.n_chunks), H),
-                     dim3(NTHREADS), 0, s, B.seq_tab, B.chunk_tab, B.replay_row, H, scale,
-                     static_cast<const T*>(q), static_cast<const T*>(k),
-                     static_cast<const T*>(v), g, hbuf, static_cast<T*>(o));
-  return hip_check("harts_la_fwd(out)");
+  {
+    ProfScope ps("k_fwd_block", s);
+    hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+                       B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                       static_cast<const T*>(k), static_cast<const T*>(v), g, S0, S_end,
+                       static_cast<T*>(o));
+  }
+  return hip_check("k_fwd_block");
 }
 
 template <typename T, int D>
 int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, float scale,
             const void* q, const void* k, const void* v, const float* g, const float* S0,
-            const void* dO, const float* dS_final, const float* dbank, float* hbuf, bool recompute,
-            float* dhbuf, float* ipbuf, void* dq, void* dk, void* dv, float* dg,
-            float* rep_grad, float* dS0, hipStream_t s) {
+            const void* dO, const float* dS_final, const float* dbank, const char* saved,
+            char* ws, void* dq, void* dk, void* dv, float* dg, float* rep_grad, float* dS0,
+            hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
+  const Sizes z = sizes(p, round, H, D);
   const Blob B = blob_ptrs(p, round, d_blob);
-  if (recompute) {
-    launch_fwd_state<T, D>(p, round, B, H, k, v, g, S0, hbuf, nullptr, nullptr, s);
-    if (int rc = hip_check("harts_la_bwd(recompute)")) return rc;
+  char* w = ws;
+  float* U = reinterpret_cast<float*>(w);
+  w += z.blk_state;
+  float* dS_end = reinterpret_cast<float*>(w);
+  w += z.blk_state;
+  float* rq = reinterpret_cast<float*>(w);
+  w += z.rq;
+  float* Rb = reinterpret_cast<float*>(w);
+  w += z.rb;
+  float* betap = reinterpret_cast<float*>(w);
+  w += z.betap;
+  if (!saved) {  // recompute-forward: block summaries and chain from S0
+    float* dSb = reinterpret_cast<float*>(w);
+    char* sv = w + z.blk_state;
+    if (int rc = launch_state_pass<T, D>(p, round, B, H, k, v, g, S0, dSb,
+                                          reinterpret_cast<float*>(sv + z.blk_state),
+                                          reinterpret_cast<float*>(sv), nullptr, nullptr, s))
+      return rc;
+    saved = sv;
   }
+  const float* S_end = reinterpret_cast<const float*>(saved);
+  const float* gam = reinterpret_cast<const float*>(saved + z.blk_state);
   {
-  ProfScope ps("k_bwd_state", s);
-  hipLaunchKernelGGL((k_bwd_state<T, D>), dim3(L.n_seq * (D / DVT), H), dim3(NTHREADS), 0, s,
-                     B.seq_tab, B.replay_row, B.req_chunk, B.req_bank, H, scale,
-                     static_cast<const T*>(q), g, static_cast<const T*>(dO), hbuf, dS_final,
-                     dbank, dhbuf, ipbuf, dS0);
+    ProfScope ps("k_bwd_fwdorder", s);
+    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+                       B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                       static_cast<const T*>(k), static_cast<const T*>(v), g,
+                       static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq, U);
   }
-  if (int rc = hip_check("harts_la_bwd(state)")) return rc;
-  ProfScope ps("k_bwd_grad", s);
-  hipLaunchKernelGGL((k_bwd_grad<T, D>), dim3(static_cast<unsigned>(L.n_chunks), H),
-                     dim3(NTHREADS), 0, s, B.seq_tab, B.chunk_tab, B.replay_row, H, scale,
-                     static_cast<const T*>(q), static_cast<const T*>(k),
-                     static_cast<const T*>(v), g, static_cast<const T*>(dO), hbuf, dhbuf, ipbuf,
-                     static_cast<T*>(dq), static_cast<T*>(dk), static_cast<T*>(dv), dg, rep_grad);
-  return hip_check("harts_la_bwd(grad)");
+  if (int rc = hip_check("k_bwd_fwdorder")) return rc;
+  {
+    constexpr int NSW = D * D / 4 / NTHREADS;
+    ProfScope ps("k_bwd_blockscan", s);
+    hipLaunchKernelGGL((k_bwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(NTHREADS), 0, s,
+                       B.seq_tab, B.blk_tab, H, dS_final, dbank, S_end, U, gam, dS_end, dS0,
+                       betap);
+  }
+  if (int rc = hip_check("k_bwd_blockscan")) return rc;
+  {
+    ProfScope ps("k_bwd_revorder", s);
+    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+                       B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                       static_cast<const T*>(k), static_cast<const T*>(v), g,
+                       static_cast<const T*>(dO), dS_end, rq, static_cast<T*>(dk),
+                       static_cast<T*>(dv), dg, rep_grad, Rb);
+  }
+  if (int rc = hip_check("k_bwd_revorder")) return rc;
+  {
+    ProfScope ps("k_dg_carry", s);
+    hipLaunchKernelGGL((k_dg_carry<D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+                       B.blk_tab, B.replay_row, H, betap, Rb, dg, rep_grad);
+  }
+  return hip_check("k_dg_carry");
 }
 
 }  // namespace
@@ -797,7 +1044,7 @@ extern "C" int harts_la_saved_size(const harts_plan_t* p, int32_t round, int32_t
                                    int32_t dk, int32_t dv, size_t* bytes) {
   if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_saved_size")) return rc;
   if (!bytes) { set_error("harts_la_saved_size: bytes is NULL"); return HARTS_EINVAL; }
-  *bytes = hbuf_bytes(p, round, H, dk);
+  *bytes = sizes(p, round, H, dk).saved;
   return HARTS_OK;
 }
 
@@ -809,10 +1056,9 @@ extern "C" int harts_la_workspace_size(const harts_plan_t* p, int32_t round, int
     set_error("harts_la_workspace_size: bad pass or NULL bytes");
     return HARTS_EINVAL;
   }
-  if (pass == 0) *bytes = hbuf_bytes(p, round, H, dk);
-  else
-    *bytes = dhbuf_bytes(p, round, H, dk) + ipbuf_bytes(p, round, H, dk) +
-             (has_saved ? 0 : hbuf_bytes(p, round, H, dk));
+  const Sizes z = sizes(p, round, H, dk);
+  if (pass == 0) *bytes = z.ws_fwd + (has_saved ? 0 : z.saved);
+  else *bytes = z.ws_bwd + (has_saved ? 0 : z.ws_rec);
   return HARTS_OK;
 }
 
@@ -822,29 +1068,29 @@ extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_
                             const float* S0, void* o, float* S_final, float* bank, void* saved,
                             void* ws, size_t ws_bytes, void* stream) {
   if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_fwd")) return rc;
-  if (!d_blob || !q || !k || !v || !g || !S0 || !S_final || (!bank && p->n_slots > 0)) {
+  if (!d_blob || !q || !k || !v || !g || !S0 || !S_final || !ws || (!bank && p->n_slots > 0)) {
     set_error("harts_la_fwd: NULL required pointer");
     return HARTS_EINVAL;
   }
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(S0) || !aligned16(o) ||
-      !aligned16(S_final) || !aligned16(saved) || !aligned16(ws)) {
+      !aligned16(S_final) || !aligned16(bank) || !aligned16(saved) || !aligned16(ws)) {
     set_error("harts_la_fwd: pointers must be 16-byte aligned");
     return HARTS_EINVAL;
   }
-  float* hbuf = static_cast<float*>(saved);
-  if (!hbuf) {
-    if (!ws || ws_bytes < hbuf_bytes(p, round, H, dk)) {
-      set_error("harts_la_fwd: workspace too small (see harts_la_workspace_size)");
-      return HARTS_EINVAL;
-    }
-    hbuf = static_cast<float*>(ws);
+  const Sizes z = sizes(p, round, H, dk);
+  if (ws_bytes < z.ws_fwd + (saved ? 0 : z.saved)) {
+    set_error("harts_la_fwd: workspace too small (see harts_la_workspace_size)");
+    return HARTS_EINVAL;
   }
+  char* w = static_cast<char*>(ws);
+  char* sv = saved ? static_cast<char*>(saved) : w + z.ws_fwd;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == HARTS_BF16) {
-    if (dk == 128) return run_fwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, hbuf, s);
-    return run_fwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, hbuf, s);
+    if (dk == 128)
+      return run_fwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, sv, w, s);
+    return run_fwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, sv, w, s);
   }
-  return run_fwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, hbuf, s);
+  return run_fwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, sv, w, s);
 }
 
 extern "C" int harts_la_bwd(const harts_plan_t* p, int32_t round, const void* d_blob,
@@ -862,36 +1108,28 @@ extern "C" int harts_la_bwd(const harts_plan_t* p, int32_t round, const void* d_
   }
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) || !aligned16(dq) ||
       !aligned16(dk_) || !aligned16(dv_) || !aligned16(saved) || !aligned16(ws) ||
-      !aligned16(dS0) || !aligned16(dS_final)) {
+      !aligned16(dS0) || !aligned16(dS_final) || !aligned16(S0) || !aligned16(dbank)) {
     set_error("harts_la_bwd: pointers must be 16-byte aligned");
     return HARTS_EINVAL;
   }
-  const bool recompute = saved == nullptr;
-  const size_t need = dhbuf_bytes(p, round, H, dk) + ipbuf_bytes(p, round, H, dk) +
-                      (recompute ? hbuf_bytes(p, round, H, dk) : 0);
-  if (ws_bytes < need) {
+  const Sizes z = sizes(p, round, H, dk);
+  if (ws_bytes < z.ws_bwd + (saved ? 0 : z.ws_rec)) {
     set_error("harts_la_bwd: workspace too small (see harts_la_workspace_size)");
     return HARTS_EINVAL;
   }
+  const char* sv = static_cast<const char*>(saved);
   char* w = static_cast<char*>(ws);
-  float* dhbuf = reinterpret_cast<float*>(w);
-  float* ipbuf = reinterpret_cast<float*>(w + dhbuf_bytes(p, round, H, dk));
-  float* hbuf = recompute ? reinterpret_cast<float*>(w + dhbuf_bytes(p, round, H, dk) +
-                                                      ipbuf_bytes(p, round, H, dk))
-                          : static_cast<float*>(const_cast<void*>(saved));
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == HARTS_BF16) {
     if (dk == 128)
       return run_bwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank,
-                                hbuf, recompute, dhbuf, ipbuf, dq, dk_, dv_, dg, replay_grad, dS0,
-                                s);
-    return run_bwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank,
-                             hbuf, recompute, dhbuf, ipbuf, dq, dk_, dv_, dg, replay_grad, dS0, s);
+                                sv, w, dq, dk_, dv_, dg, replay_grad, dS0, s);
+    return run_bwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank, sv,
+                             w, dq, dk_, dv_, dg, replay_grad, dS0, s);
   }
-  return run_bwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank, hbuf,
-                            recompute, dhbuf, ipbuf, dq, dk_, dv_, dg, replay_grad, dS0, s);
+  return run_bwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank, sv,
+                            w, dq, dk_, dv_, dg, replay_grad, dS0, s);
 }
-
 extern "C" int harts_state_gather(const float* src, const int32_t* idx, int32_t n,
                                   int64_t elems_per_state, float* dst, int32_t mode,
                                   void* stream) {

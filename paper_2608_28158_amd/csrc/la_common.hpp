@@ -63,6 +63,33 @@ template <> struct Mma<float> {
   }
 };
 
+// acc += A[16 x 16] * B[16 x 16] where A is read from LDS (A points at the
+// tile's first row and column, row stride lda) and B is a 16x16 float32
+// accumulator tile held in registers (C layout: lane l, element r holds
+// B[4*(l/16) + r][l % 16]).  The C layout of a tile is exactly the B-operand
+// layout of the 16x16x16 bf16 instruction; the float32 path issues four
+// 16x16x4 instructions over the k indices {4g + j}, g = lane / 16.
+template <typename T> struct MmaRegB;
+template <> struct MmaRegB<bf16> {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  __device__ static inline void step(f32x4& c, const bf16* A, int lda, const f32x4& B, int lane) {
+    const bf16x4 a = *reinterpret_cast<const bf16x4*>(A + (lane & 15) * lda + (lane >> 4) * 4);
+    bf16x4 b;
+    b[0] = static_cast<bf16>(B[0]);
+    b[1] = static_cast<bf16>(B[1]);
+    b[2] = static_cast<bf16>(B[2]);
+    b[3] = static_cast<bf16>(B[3]);
+    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct MmaRegB<float> {
+  __device__ static inline void step(f32x4& c, const float* A, int lda, const f32x4& B, int lane) {
+    const float* a = A + (lane & 15) * lda + (lane >> 4) * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], B[j], c, 0, 0, 0);
+  }
+};
+
 // Accumulator element r of lane l in a 16x16 tile sits at
 // row 4*(l/16) + r, column l % 16.
 __device__ inline int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }

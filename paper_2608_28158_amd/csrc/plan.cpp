@@ -347,6 +347,27 @@ struct Builder {
     return true;
   }
 
+  // Blocks of a round for a given block size: cuts every L chunks and at
+  // every requested boundary.
+  int32_t count_blocks(const RoundLayout& L, int32_t bc) const {
+    const harts_plan_s& p = *P;
+    int64_t total = 0;
+    for (int32_t i = L.seq_begin; i < L.seq_begin + L.n_seq; ++i) {
+      const int64_t tok = p.seq_n_replay[i] + p.seq_n_own[i];
+      const int32_t nc = static_cast<int32_t>((tok + B - 1) / B);
+      int32_t c0 = 0, rq = p.seq_req_off[i];
+      const int32_t rq_end = p.seq_req_off[i + 1];
+      while (c0 < nc) {
+        int32_t c1 = std::min(nc, c0 + bc);
+        while (rq < rq_end && p.req_chunk[rq] <= c0) ++rq;
+        if (rq < rq_end && p.req_chunk[rq] <= c1) c1 = p.req_chunk[rq];
+        ++total;
+        c0 = c1;
+      }
+    }
+    return static_cast<int32_t>(total);
+  }
+
   void build_blob() {
     harts_plan_s& p = *P;
     const int32_t K = p.K;
@@ -368,12 +389,21 @@ struct Builder {
         L.max_seq_chunks = std::max<int32_t>(L.max_seq_chunks, static_cast<int32_t>(nc));
       }
       p.n_chunks += L.n_chunks;
+      // block size: the largest of 64, 32, 16, 8 chunks that still cuts the
+      // round into >= 48 blocks (so that (block, head) work units fill the GPU)
+      L.block_chunks = 8;
+      for (int32_t cand = 64; cand >= 8; cand /= 2) {
+        if (count_blocks(L, cand) >= 48) { L.block_chunks = cand; break; }
+      }
+      L.n_blk = count_blocks(L, L.block_chunks);
       L.seq_tab = off;
       off = align_up(off + int64_t(L.n_seq) * SEQ_WORDS);
       L.init_idx = off;
       off = align_up(off + L.n_seq);
       L.chunk_tab = off;
       off = align_up(off + 2 * L.n_chunks);
+      L.blk_tab = off;
+      off = align_up(off + int64_t(L.n_blk) * BLK_WORDS);
     }
     p.off_replay_row = off;
     off = align_up(off + p.R);
@@ -403,8 +433,10 @@ struct Builder {
     p.blob.assign(std::max<int64_t>(off, kAlignWords), 0);
     int32_t* b = p.blob.data();
     for (int32_t r = 0; r < K; ++r) {
-      const RoundLayout& L = p.rounds[r];
+      RoundLayout& L = p.rounds[r];
       int64_t chunk_off = 0;
+      int64_t blk_next = 0;
+      int32_t max_seq_blocks = 0;
       for (int32_t li = 0; li < L.n_seq; ++li) {
         const int32_t i = L.seq_begin + li;
         const int64_t tok = p.seq_n_replay[i] + p.seq_n_own[i];
@@ -421,12 +453,39 @@ struct Builder {
         e[SEQ_N_REQ] = p.seq_req_off[i + 1] - p.seq_req_off[i];
         e[SEQ_N_CHUNKS] = static_cast<int32_t>(nc);
         b[L.init_idx + li] = p.seq_init_bank[i];
+        // blocks of this sequence
+        e[SEQ_BLK_OFF] = static_cast<int32_t>(blk_next);
+        int32_t nb = 0;
+        int32_t c0 = 0;
+        int32_t rq = p.seq_req_off[i];
+        const int32_t rq_end = p.seq_req_off[i + 1];
+        while (c0 < nc) {
+          int32_t c1 = std::min<int32_t>(static_cast<int32_t>(nc), c0 + L.block_chunks);
+          while (rq < rq_end && p.req_chunk[rq] <= c0) ++rq;
+          int32_t end_bank = -1;
+          if (rq < rq_end && p.req_chunk[rq] <= c1) {
+            c1 = p.req_chunk[rq];
+            end_bank = p.req_bank[rq];
+          }
+          int32_t* bk = b + L.blk_tab + blk_next * BLK_WORDS;
+          bk[BLK_SEQ] = li;
+          bk[BLK_C0] = c0;
+          bk[BLK_NC] = c1 - c0;
+          bk[BLK_IDX] = nb;
+          bk[BLK_END_BANK] = end_bank;
+          ++blk_next;
+          ++nb;
+          c0 = c1;
+        }
+        e[SEQ_N_BLK] = nb;
+        max_seq_blocks = std::max(max_seq_blocks, nb);
         for (int64_t c = 0; c < nc; ++c) {
           b[L.chunk_tab + 2 * (chunk_off + c)] = li;
           b[L.chunk_tab + 2 * (chunk_off + c) + 1] = static_cast<int32_t>(c);
         }
         chunk_off += nc;
       }
+      L.max_seq_blocks = max_seq_blocks;
     }
     for (int64_t j = 0; j < p.R; ++j) b[p.off_replay_row + j] = static_cast<int32_t>(p.replay_row[j]);
     for (size_t j = 0; j < p.req_chunk.size(); ++j) {

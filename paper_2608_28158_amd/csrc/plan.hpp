@@ -22,11 +22,27 @@ enum SeqField : int {
   SEQ_REQ_OFF = 7,    // first request (global index)
   SEQ_N_REQ = 8,      // requests of the sequence
   SEQ_N_CHUNKS = 9,   // chunks of the sequence
+  SEQ_BLK_OFF = 10,   // first block of the sequence within the round
+  SEQ_N_BLK = 11,     // blocks of the sequence
   SEQ_WORDS = 16
+};
+
+// Fields of one block entry (a run of consecutive chunks of one sequence;
+// blocks end at every requested boundary and at most every `block_chunks`
+// chunks).
+enum BlkField : int {
+  BLK_SEQ = 0,      // sequence (local index within the round)
+  BLK_C0 = 1,       // first chunk (within the sequence)
+  BLK_NC = 2,       // chunks in the block
+  BLK_IDX = 3,      // block index within the sequence
+  BLK_END_BANK = 4, // bank entry requested at the block's end, or -1
+  BLK_WORDS = 8
 };
 
 struct RoundLayout {
   int32_t n_seq = 0, seq_begin = 0, max_seq_chunks = 0;
+  int32_t n_blk = 0, block_chunks = 0, max_seq_blocks = 0;
+  int64_t blk_tab = 0;    // int32 offset of the [n_blk][BLK_WORDS] block table
   int64_t n_chunks = 0, n_rows = 0, n_own = 0, n_replay = 0, own_row_begin = 0;
   int64_t seq_tab = 0;    // int32 offset of the sequence table
   int64_t init_idx = 0;   // int32 offset of the [n_seq] init bank indices

@@ -53,7 +53,8 @@ class TreeLARunner:
         self.blob = plan.blob(self.device)
         self.elems = H * d * d
         sz = C.c_size_t()
-        self.saved_bytes, self.ws_fwd, self.ws_bwd_saved, self.ws_bwd_rec = [], [], [], []
+        self.saved_bytes, self.ws_fwd, self.ws_fwd_nosave = [], [], []
+        self.ws_bwd_saved, self.ws_bwd_rec = [], []
         for r in range(plan.info["n_rounds"]):
             _lib.check(self.L.harts_la_saved_size(plan.handle, r, self.code, H, d, d,
                                                   C.byref(sz)), "harts_la_saved_size")
@@ -61,6 +62,9 @@ class TreeLARunner:
             _lib.check(self.L.harts_la_workspace_size(plan.handle, r, 0, self.code, H, d, d, 1,
                                                       C.byref(sz)), "harts_la_workspace_size")
             self.ws_fwd.append(sz.value)
+            _lib.check(self.L.harts_la_workspace_size(plan.handle, r, 0, self.code, H, d, d, 0,
+                                                      C.byref(sz)), "harts_la_workspace_size")
+            self.ws_fwd_nosave.append(sz.value)
             _lib.check(self.L.harts_la_workspace_size(plan.handle, r, 1, self.code, H, d, d, 1,
                                                       C.byref(sz)), "harts_la_workspace_size")
             self.ws_bwd_saved.append(sz.value)
@@ -118,12 +122,11 @@ class TreeLARunner:
         for r in range(P.info["n_rounds"]):
             S0 = self.gather(bank, r)
             sv = self._bytes(self.saved_bytes[r]) if keep_states else None
-            ws = None if keep_states else self._bytes(self.ws_fwd[r])
+            ws = self._bytes(self.ws_fwd[r] if keep_states else self.ws_fwd_nosave[r])
             _lib.check(self.L.harts_la_fwd(
                 P.handle, r, _ptr(self.blob), self.code, H, d, d, self.scale,
                 _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S0), _ptr(o), _ptr(S_final),
-                _ptr(bank), _ptr(sv), _ptr(ws), ws.numel() if ws is not None else 0,
-                self._stream()), "harts_la_fwd")
+                _ptr(bank), _ptr(sv), _ptr(ws), ws.numel(), self._stream()), "harts_la_fwd")
             saved.append(sv)
         return dict(o=o, S_final=S_final, bank=bank, saved=saved)
 
