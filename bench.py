@@ -73,42 +73,41 @@ def phys_index(seg_len, seg_row):
 
 
 def algorithmic_bytes(plan, H, d, el):
-    """Bytes each kernel must move for its job, per launch set of one step.
+    """Bytes each kernel must move for its job over one step, by kernel.
 
-    Rows are packed rows (own + replay); q, o, dO and dq only exist on own
-    rows.  State terms: initial states, requested boundary states, final
-    states and their gradients (float32 H*d*d each).  Per-chunk state
-    materialisation is not counted."""
+    Rows are packed rows (own + replay); q, o, dO and dq exist on own rows
+    only.  Block-level states (summaries, chained block-end states, local
+    adjoints) are float32 H*d*d each and are counted for the kernels whose
+    job is to produce or consume them; per-chunk states are never
+    materialised.  Returns (bytes per step, launches per step) per kernel."""
     st = H * d * d * 4
-    out = {}
-    fs = fo = bs = bg = ga = sa = 0
-    for r in plan.rounds:
-        rows, own, rep, nseq = r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"]
-        nreq_r = 0
-        for i in range(r["seq_begin"], r["seq_begin"] + nseq):
-            nreq_r += int(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i])
-        fs += rows * H * (2 * d * el + 4) + nseq * st * 2 + nreq_r * st
-        fo += own * H * d * el * 2 + rows * H * (2 * d * el + 4)
-        bs += own * H * 2 * d * el + rows * H * 4 + nseq * st * 2 + nreq_r * st
-        bg += (own * H * (2 * d * el + 3 * d * el + 4) + rows * H * (2 * d * el + 4)
-               + rep * H * (2 * d + 1) * 4)
-        ga += nseq * st * 2
-        sa += nseq * st * 3
-    out["k_fwd_state"] = fs * 2          # forward and recompute pass
-    out["k_fwd_out"] = fo
-    out["k_bwd_state"] = bs
-    out["k_bwd_grad"] = bg
-    out["k_gather"] = ga * 2
-    out["k_scatter_add"] = sa
-    R = plan.info["R"]
-    out["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
-    return out
-
-
-def launches_per_step(plan):
     K = plan.info["n_rounds"]
-    return {"k_fwd_state": 2 * K, "k_fwd_out": K, "k_bwd_state": K, "k_bwd_grad": K,
-            "k_gather": 2 * K, "k_scatter_add": K, "k_replay_reduce": 1 if plan.info["R"] else 0}
+    b = dict.fromkeys(["k_fwd_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder",
+                       "k_bwd_blockscan", "k_bwd_revorder", "k_dg_carry", "k_gather",
+                       "k_scatter_add"], 0)
+    for r in plan.rounds:
+        rows, own, rep, nseq, nblk = (r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"],
+                                      r["n_blk"])
+        nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i]
+                       for i in range(r["seq_begin"], r["seq_begin"] + nseq)))
+        kv = rows * H * (2 * d * el + 4)                       # k, v, g of every packed row
+        b["k_fwd_blocksum"] += 2 * (kv + nblk * st)            # forward + recompute pass
+        b["k_fwd_blockscan"] += 2 * (nseq * st + 2 * nblk * st + nreq * st + nseq * st)
+        b["k_fwd_block"] += kv + own * H * 2 * d * el + nblk * st
+        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + 2 * nblk * st
+        b["k_bwd_blockscan"] += 4 * nblk * st + nseq * st + nreq * st + nseq * st
+        b["k_bwd_revorder"] += (kv + own * H * (2 * d * el + 2 * d * el + 4)
+                                + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st)
+        b["k_dg_carry"] += rows * H * 8
+        b["k_gather"] += 2 * 2 * nseq * st                     # forward + recompute
+        b["k_scatter_add"] += 3 * nseq * st
+    R = plan.info["R"]
+    b["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
+    launches = {"k_fwd_blocksum": 2 * K, "k_fwd_blockscan": 2 * K, "k_fwd_block": K,
+                "k_bwd_fwdorder": K, "k_bwd_blockscan": K, "k_bwd_revorder": K,
+                "k_dg_carry": K, "k_gather": 2 * K, "k_scatter_add": K,
+                "k_replay_reduce": 1 if R else 0}
+    return b, launches
 
 
 def read_traffic(kernel, workload_key):
@@ -242,7 +241,7 @@ def expanded_comparison(steps, warmup):
     fo = run_step(runner, t)["o"].float().cpu().numpy()
     eo = run_step(erunner, te)["o"].float().cpu().numpy()
     phys = phys_index(forest.seg_len, plan["seg_row"])
-    same = bool(np.array_equal(fo[phys][erows], eo[ephys]))
+    diff = float(np.max(np.abs(fo[phys][erows] - eo[ephys])) / np.max(np.abs(eo)))
     C = forest.n_rows
     S = int(lens.sum())
     return {"workload": "4 agentic trees, ~32k compact tokens, H=16, d=128, bf16, fwd+bwd "
@@ -250,7 +249,7 @@ def expanded_comparison(steps, warmup):
             "C": C, "S": S, "tree_packed_ms": ms_tree, "expanded_ms": ms_exp,
             "tree_packed_compact_tok_s": C / (ms_tree * 1e-3),
             "expanded_compact_tok_s": C / (ms_exp * 1e-3),
-            "speedup": ms_exp / ms_tree, "outputs_bitwise_equal": same,
+            "speedup": ms_exp / ms_tree, "outputs_max_rel_diff": diff,
             "paper_context": "4.81-4.87x F/B/Grad end-to-end speedup, 8x H20-3e, BF16, "
                              "Ling-3.0-tiny (whole model, not this operator)"}
 
@@ -296,8 +295,7 @@ def main():
     el = 2 if cfg["dtype"] == "bf16" else 4
     C = plan.info["C"]
     value = C / (ms * 1e-3)
-    alg = algorithmic_bytes(plan, H, d, el)
-    per_step = launches_per_step(plan)
+    alg, per_step = algorithmic_bytes(plan, H, d, el)
     kstats = {}
     for name, (n, tot) in kern.items():
         steps_seen = max(1, n // max(1, per_step.get(name, 1)))

@@ -157,6 +157,9 @@ int harts_plan_export(const harts_plan_t* plan, const harts_plan_arrays* dst);
 typedef struct harts_round_info {
   int32_t n_seq;         /* sequences in the round                          */
   int32_t seq_begin;     /* first sequence id of the round                  */
+  int32_t n_blk;         /* blocks (runs of chunks of one sequence, ending
+                            at requested boundaries) -- the device work units */
+  int32_t block_chunks;  /* longest block, in chunks                        */
   int64_t n_chunks;      /* chunks over the round's sequences               */
   int64_t n_rows;        /* packed rows: own + replay                       */
   int64_t n_own;         /* own rows (outputs)                              */

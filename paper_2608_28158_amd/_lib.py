@@ -74,7 +74,8 @@ class PlanArrays(C.Structure):
 
 
 class RoundInfo(C.Structure):
-    _fields_ = [("n_seq", C.c_int32), ("seq_begin", C.c_int32)] + [
+    _fields_ = [("n_seq", C.c_int32), ("seq_begin", C.c_int32), ("n_blk", C.c_int32),
+                ("block_chunks", C.c_int32)] + [
         (n, C.c_int64) for n in ("n_chunks", "n_rows", "n_own", "n_replay",
                                  "own_row_begin", "init_idx_off")]
 

@@ -12,9 +12,11 @@
 // consecutive chunks (the planner ends a block at every requested boundary
 // and at most every block_chunks chunks).  One workgroup owns one
 // (block, head) and keeps the whole [d x d] float32 state in MFMA
-// accumulators while it walks the block's chunks; per-chunk states are never
-// written to memory.  Blocks of one sequence are chained by small
-// element-parallel scans over block summaries:
+// accumulators (wave w holds state columns 16w .. 16w+15) while it walks the
+// block's chunks; per-chunk states are never written to memory.  The next
+// chunk's rows are loaded into registers while the current chunk computes.
+// Blocks of one sequence are chained by element-parallel scans over block
+// summaries:
 //
 //   forward   k_fwd_blocksum  state of each block started from zero, and
 //                             its total log-decay Gamma_b;
@@ -52,20 +54,8 @@
 namespace harts {
 
 // ---------------------------------------------------------------------------
-// chunk staging: global rows -> registers -> LDS tiles
+// chunk staging: global rows -> registers (one chunk ahead) -> LDS tiles
 // ---------------------------------------------------------------------------
-template <typename T, int D>
-struct Stage {
-  static constexpr int VE = 16 / sizeof(T);          // elements per 16-byte vector
-  static constexpr int VPR = D / VE;                 // vectors per row
-  static constexpr int NV = CB * VPR / NTHREADS;     // vectors per thread per tensor
-  static constexpr int NT = D / 16;                  // 16-wide tiles along d
-  static constexpr int CPW = NT / NWAVES;            // state column tiles per wave
-  static constexpr int LDR = D + Elem<T>::PAD;       // row-major tile [64][D]
-  static constexpr int LDT = CB + Elem<T>::PAD;      // transposed tile [D][64]
-  static constexpr int LDA = CB + Elem<T>::PAD;      // [64][64] tiles
-};
-
 union Vec16 {
   uint4 u;
   float f[4];
@@ -78,141 +68,163 @@ template <>
 __device__ inline float vget<float>(const Vec16& v, int e) { return v.f[e]; }
 template <>
 __device__ inline bf16 vget<bf16>(const Vec16& v, int e) { return v.b[e]; }
+template <typename T>
+__device__ inline void vset(Vec16& v, int e, T x);
+template <>
+__device__ inline void vset<float>(Vec16& v, int e, float x) { v.f[e] = x; }
+template <>
+__device__ inline void vset<bf16>(Vec16& v, int e, bf16 x) { v.b[e] = x; }
 
-// Load this thread's vectors of one tensor for the chunk's rows; rows whose
-// kind is below min_kind (padding; replay rows for q and dO) read as zero.
+// This thread's rows of one chunk (a row's d-range is split over VPR threads).
 template <typename T, int D>
-__device__ inline void load_chunk(Vec16* r, const T* __restrict__ src,
-                                  const ChunkRows& cr, int H, int h, int t, int min_kind) {
-  using S = Stage<T, D>;
+struct ChunkRefs {
+  RowRef r[Cfg<T, D>::NV];
+  __device__ inline void resolve(const int32_t* seq, int c, const int32_t* replay_row, int t) {
+    using C = Cfg<T, D>;
 #pragma unroll
-  for (int i = 0; i < S::NV; ++i) {
-    const int idx = t + i * NTHREADS;
-    const int row = idx / S::VPR, d0 = (idx % S::VPR) * S::VE;
-    if (cr.kind[row] >= min_kind)
-      r[i].u = *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(cr.row[row]) * H + h) * D + d0);
-    else
-      r[i].u = make_uint4(0u, 0u, 0u, 0u);
+    for (int i = 0; i < C::NV; ++i) r[i] = pos_row(seq, c * CB + (t + i * C::NTHR) / C::VPR, replay_row);
   }
-}
-
-template <typename T, int D>
-__device__ inline void store_rowmajor(T* dst, const Vec16* r, int t) {
-  using S = Stage<T, D>;
-#pragma unroll
-  for (int i = 0; i < S::NV; ++i) {
-    const int idx = t + i * NTHREADS;
-    const int row = idx / S::VPR, d0 = (idx % S::VPR) * S::VE;
-    *reinterpret_cast<uint4*>(dst + row * S::LDR + d0) = r[i].u;
-  }
-}
-
-// dst[d][row] = src[row][d] * scale[row] (scale == nullptr: no scaling)
-template <typename T, int D>
-__device__ inline void store_transposed(T* dst, const Vec16* r,
-                                        const float* scale, int t) {
-  using S = Stage<T, D>;
-#pragma unroll
-  for (int i = 0; i < S::NV; ++i) {
-    const int idx = t + i * NTHREADS;
-    const int row = idx / S::VPR, d0 = (idx % S::VPR) * S::VE;
-    if (scale) {
-      const float sc = scale[row];
-#pragma unroll
-      for (int e = 0; e < S::VE; ++e)
-        dst[(d0 + e) * S::LDT + row] = Elem<T>::from_f(Elem<T>::to_f(vget<T>(r[i], e)) * sc);
-    } else {
-#pragma unroll
-      for (int e = 0; e < S::VE; ++e) dst[(d0 + e) * S::LDT + row] = vget<T>(r[i], e);
-    }
-  }
-}
-
-// Row table of chunk c of a sequence plus the in-chunk prefix sums of g.
-__device__ inline void chunk_setup(ChunkRows& cr, float* G, const int32_t* seq, int c,
-                                   const int32_t* replay_row, const float* g, int H, int h,
-                                   int t) {
-  resolve_rows(cr, seq, c, replay_row, t);
-  chunk_cumsum(G, cr, g, H, h, t);  // same threads (wave 0) that resolved the rows
-}
-
-// A state held as tiles: tile (mt, nt) is rows 16*mt.., cols 16*nt.. of a
-// [D x D] matrix; wave w owns column tiles [w*CPW, (w+1)*CPW) of every row.
-template <int D>
-struct StateTiles {
-  static constexpr int NT = D / 16;
-  static constexpr int CPW = NT / NWAVES;
-  static constexpr int N = NT * CPW;  // tiles per wave
-  __device__ static inline int mt(int i) { return i / CPW; }
-  __device__ static inline int nt(int w, int i) { return w * CPW + i % CPW; }
 };
 
-// Load a [D x D] row-major float32 state into tiles; transpose: tile holds
-// src^T.
+template <typename T, int D>
+__device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkRefs<T, D>& cr,
+                             int H, int h, int t, int min_kind) {
+  using C = Cfg<T, D>;
+#pragma unroll
+  for (int i = 0; i < C::NV; ++i) {
+    const int d0 = ((t + i * C::NTHR) % C::VPR) * C::VE;
+    dst[i].u = cr.r[i].kind >= min_kind
+                   ? *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(cr.r[i].row) * H + h) * D + d0)
+                   : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+// dst[row][d] = src[row][d] (* scale[row] if scale != nullptr)
+template <typename T, int D>
+__device__ inline void put(T* dst, const Vec16* src, const float* scale, int t) {
+  using C = Cfg<T, D>;
+#pragma unroll
+  for (int i = 0; i < C::NV; ++i) {
+    const int idx = t + i * C::NTHR;
+    const int row = idx / C::VPR, d0 = (idx % C::VPR) * C::VE;
+    Vec16 v = src[i];
+    if (scale) {
+      const float s = scale[row];
+#pragma unroll
+      for (int e = 0; e < C::VE; ++e) vset<T>(v, e, Elem<T>::from_f(Elem<T>::to_f(vget<T>(v, e)) * s));
+    }
+    *reinterpret_cast<uint4*>(dst + row * C::LDR + d0) = v.u;
+  }
+}
+
+// Per-chunk row table and decay prefix sums, shared through LDS.
+struct ChunkMeta {
+  int row[CB];
+  int kind[CB];
+  int rep[CB];
+  float G[CB];
+};
+
+// Wave 0: row table of chunk c and G from the prefetched g (lane = row).
+// Returns G[t] in Gt and G[63] in GL (wave 0 lanes only).
+__device__ inline void meta_setup(ChunkMeta& m, const int32_t* seq, int c, const int32_t* replay_row,
+                                  float gpre, int t, float& Gt, float& GL) {
+  Gt = 0.f;
+  GL = 0.f;
+  if (t < CB) {
+    const RowRef rr = pos_row(seq, c * CB + t, replay_row);
+    m.row[t] = rr.row;
+    m.kind[t] = rr.kind;
+    m.rep[t] = rr.rep;
+    float x = gpre;
+#pragma unroll
+    for (int off = 1; off < CB; off <<= 1) {
+      const float y = __shfl_up(x, off, CB);
+      if (t >= off) x += y;
+    }
+    m.G[t] = x;
+    Gt = x;
+    GL = __shfl(x, CB - 1, CB);
+  }
+}
+
+// Wave 0: g of chunk c (0 for padding).
+__device__ inline float fetch_g(const int32_t* seq, int c, const int32_t* replay_row,
+                                const float* g, int H, int h, int t) {
+  if (t >= CB) return 0.f;
+  const RowRef rr = pos_row(seq, c * CB + t, replay_row);
+  return rr.kind != ROW_PAD ? g[static_cast<int64_t>(rr.row) * H + h] : 0.f;
+}
+
+// A state held as NT tiles per wave: tile i is rows 16i.., columns 16w.. of
+// a [D x D] matrix (wave w owns one 16-column strip).
 template <int D>
 __device__ inline void state_load(f32x4* S, const float* src, bool transpose, int w, int lane) {
-  using ST = StateTiles<D>;
 #pragma unroll
-  for (int i = 0; i < ST::N; ++i)
+  for (int i = 0; i < D / 16; ++i)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int a = ST::mt(i) * 16 + acc_row(lane, r), b = ST::nt(w, i) * 16 + acc_col(lane);
+      const int a = i * 16 + acc_row(lane, r), b = w * 16 + acc_col(lane);
       S[i][r] = src ? (transpose ? src[b * D + a] : src[a * D + b]) : 0.f;
     }
 }
 
 template <int D>
 __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) {
-  using ST = StateTiles<D>;
 #pragma unroll
-  for (int i = 0; i < ST::N; ++i)
+  for (int i = 0; i < D / 16; ++i)
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      dst[(ST::mt(i) * 16 + acc_row(lane, r)) * D + ST::nt(w, i) * 16 + acc_col(lane)] = S[i][r];
+    for (int r = 0; r < 4; ++r) dst[(i * 16 + acc_row(lane, r)) * D + w * 16 + acc_col(lane)] = S[i][r];
 }
 
 // ---------------------------------------------------------------------------
 // forward: block summaries (state of the block started from zero)
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_fwd_blocksum(
+__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_fwd_blocksum(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ replay_row, int H, const T* __restrict__ k,
     const T* __restrict__ v, const float* __restrict__ g, float* __restrict__ dSb,
     float* __restrict__ gam) {
-  using SG = Stage<T, D>;
-  using ST = StateTiles<D>;
+  using C = Cfg<T, D>;
+  __shared__ T Ks[CB * C::LDR];  // K * exp(G_last - G)
+  __shared__ T Vs[CB * C::LDR];
+  __shared__ ChunkMeta meta;
+  __shared__ float sk[CB];
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int32_t* seq = seq_tab + bk[BLK_SEQ] * SEQ_WORDS;
-  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
-  __shared__ T Kt[D * SG::LDT];  // (K * exp(G_last - G))^T : [dk][j]
-  __shared__ T Vt[D * SG::LDT];  // V^T                     : [dv][j]
-  __shared__ ChunkRows cr;
-  __shared__ float G[CB];
-  __shared__ float sk[CB];
-  f32x4 S[ST::N];
+  const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  f32x4 S[C::NT];
 #pragma unroll
-  for (int i = 0; i < ST::N; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ChunkRefs<T, D> refs;
+  Vec16 pk[C::NV], pv[C::NV];
+  refs.resolve(seq, c0, replay_row, t);
+  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+  float gp = fetch_g(seq, c0, replay_row, g, H, h, t);
   float gsum = 0.f;
-  for (int c = c0; c < c0 + nc; ++c) {
-    chunk_setup(cr, G, seq, c, replay_row, g, H, h, t);
+  for (int c = c0; c < c_end; ++c) {
+    float Gt, GLw;
+    meta_setup(meta, seq, c, replay_row, gp, t, Gt, GLw);
+    if (t < CB) sk[t] = __expf(GLw - Gt);
     __syncthreads();
-    const float GL = G[CB - 1];
-    if (t < CB) sk[t] = __expf(GL - G[t]);
-    Vec16 lk[SG::NV], lv[SG::NV];
-    load_chunk<T, D>(lk, k, cr, H, h, t, ROW_REPLAY);
-    load_chunk<T, D>(lv, v, cr, H, h, t, ROW_REPLAY);
+    const float GL = meta.G[CB - 1];
+    put<T, D>(Ks, pk, sk, t);
+    put<T, D>(Vs, pv, nullptr, t);
     __syncthreads();
-    store_transposed<T, D>(Kt, lk, sk, t);
-    store_transposed<T, D>(Vt, lv, nullptr, t);
-    __syncthreads();
+    if (c + 1 < c_end) {
+      refs.resolve(seq, c + 1, replay_row, t);
+      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+      gp = fetch_g(seq, c + 1, replay_row, g, H, h, t);
+    }
     const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < ST::N; ++i) {
+    for (int i = 0; i < C::NT; ++i) {
       S[i] *= dec;
-      Mma<T>::tile(S[i], Kt + ST::mt(i) * 16 * SG::LDT, SG::LDT, Vt + ST::nt(w, i) * 16 * SG::LDT,
-                   SG::LDT, CB, lane);
+      tile<T, true, true>(S[i], Ks + i * 16, C::LDR, Vs + w * 16, C::LDR, CB, lane);
     }
     gsum += GL;
     __syncthreads();
@@ -222,17 +234,19 @@ __global__ __launch_bounds__(NTHREADS) void k_fwd_blocksum(
 }
 
 // ---------------------------------------------------------------------------
-// forward: chain the blocks of every sequence (element-parallel)
+// element-parallel chains over the blocks of every sequence
 // ---------------------------------------------------------------------------
+constexpr int SCAN_THR = 256;
+
 template <int D>
-__global__ __launch_bounds__(NTHREADS) void k_fwd_blockscan(
+__global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
     const float* __restrict__ S0, const float* __restrict__ dSb, const float* __restrict__ gam,
     float* __restrict__ S_end, float* __restrict__ bank, float* __restrict__ S_final) {
   constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
-  constexpr int NSW = static_cast<int>(SS4 / NTHREADS);
+  constexpr int NSW = static_cast<int>(SS4 / SCAN_THR);
   const int li = blockIdx.x / NSW, part = blockIdx.x % NSW, h = blockIdx.y;
-  const int64_t e4 = static_cast<int64_t>(part) * NTHREADS + threadIdx.x;
+  const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + threadIdx.x;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
   float4 s = reinterpret_cast<const float4*>(S0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4];
@@ -253,240 +267,7 @@ __global__ __launch_bounds__(NTHREADS) void k_fwd_blockscan(
     reinterpret_cast<float4*>(S_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4] = s;
 }
 
-// ---------------------------------------------------------------------------
-// forward: outputs of the own rows of a block
-// ---------------------------------------------------------------------------
-template <typename T, int D>
-struct FwdSmem {
-  using SG = Stage<T, D>;
-  T Q[CB * SG::LDR];
-  T K[CB * SG::LDR];
-  T Kt[D * SG::LDT];  // (K * exp(G_last - G))^T
-  T Vt[D * SG::LDT];  // V^T
-  T A[CB * SG::LDA];  // masked Q K^T
-  ChunkRows cr;
-  float G[CB];
-  float sk[CB];  // exp(G_last - G)
-  float eg[CB];  // exp(G)
-};
-
-template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_fwd_block(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
-    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ S0, const float* __restrict__ S_end, T* __restrict__ o) {
-  using SG = Stage<T, D>;
-  using ST = StateTiles<D>;
-  __shared__ FwdSmem<T, D> sm;
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int li = bk[BLK_SEQ];
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
-  const int64_t DD = static_cast<int64_t>(D) * D;
-  f32x4 S[ST::N];  // S : tile (dk, dv), wave owns dv column tiles
-  state_load<D>(S, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
-                                    : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                false, w, lane);
-  for (int c = c0; c < c0 + nc; ++c) {
-    chunk_setup(sm.cr, sm.G, seq, c, replay_row, g, H, h, t);
-    __syncthreads();
-    const float GL = sm.G[CB - 1];
-    if (t < CB) {
-      sm.sk[t] = __expf(GL - sm.G[t]);
-      sm.eg[t] = __expf(sm.G[t]);
-    }
-    Vec16 lq[SG::NV], lk[SG::NV], lv[SG::NV];
-    load_chunk<T, D>(lq, q, sm.cr, H, h, t, ROW_OWN);
-    load_chunk<T, D>(lk, k, sm.cr, H, h, t, ROW_REPLAY);
-    load_chunk<T, D>(lv, v, sm.cr, H, h, t, ROW_REPLAY);
-    __syncthreads();
-    store_rowmajor<T, D>(sm.Q, lq, t);
-    store_rowmajor<T, D>(sm.K, lk, t);
-    store_transposed<T, D>(sm.Kt, lk, sm.sk, t);
-    store_transposed<T, D>(sm.Vt, lv, nullptr, t);
-    __syncthreads();
-    // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w owns rows 16w..16w+15
-#pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) {
-      f32x4 a = {0.f, 0.f, 0.f, 0.f};
-      Mma<T>::tile(a, sm.Q + 16 * w * SG::LDR, SG::LDR, sm.K + jt * 16 * SG::LDR, SG::LDR, D, lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = 16 * w + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-        sm.A[m * SG::LDA + n] = Elem<T>::from_f(n <= m ? a[r] * __expf(sm.G[m] - sm.G[n]) : 0.f);
-      }
-    }
-    __syncthreads();
-    // O[:, wave's dv columns] = scale * (diag(exp(G)) Q S_c + A V)
-    for (int it = 0; it < CB / 16; ++it) {
-#pragma unroll
-      for (int cc = 0; cc < ST::CPW; ++cc) {
-        const int nt = w * ST::CPW + cc;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kt = 0; kt < ST::NT; ++kt)
-          MmaRegB<T>::step(acc, sm.Q + it * 16 * SG::LDR + kt * 16, SG::LDR, S[kt * ST::CPW + cc], lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
-        Mma<T>::tile(acc, sm.A + it * 16 * SG::LDA, SG::LDA, sm.Vt + nt * 16 * SG::LDT, SG::LDT, CB,
-                     lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = it * 16 + acc_row(lane, r);
-          if (sm.cr.kind[m] == ROW_OWN)
-            o[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + nt * 16 + acc_col(lane)] =
-                Elem<T>::from_f(acc[r] * scale);
-        }
-      }
-    }
-    // S_{c+1} = exp(G_last) S_c + (K * exp(G_last - G))^T V
-    const float dec = __expf(GL);
-#pragma unroll
-    for (int i = 0; i < ST::N; ++i) {
-      S[i] *= dec;
-      Mma<T>::tile(S[i], sm.Kt + ST::mt(i) * 16 * SG::LDT, SG::LDT,
-                   sm.Vt + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
-    }
-    __syncthreads();
-  }
-}
-
-// ---------------------------------------------------------------------------
-// backward, forward order: dq, q.dq per row and the block's local adjoint
-// ---------------------------------------------------------------------------
-template <typename T, int D>
-struct BfSmem {
-  using SG = Stage<T, D>;
-  T dO[CB * SG::LDR];
-  T V[CB * SG::LDR];
-  T Kt[D * SG::LDT];   // K^T
-  T Vs[D * SG::LDT];   // (V * exp(G_last - G))^T
-  T Qt[D * SG::LDT];   // Q^T (own rows)
-  T dOs[D * SG::LDT];  // (dO * exp(G_blk) * scale)^T, G_blk counted from the block start
-  T dA[CB * SG::LDA];
-  ChunkRows cr;
-  float G[CB];
-  float sv[CB];  // exp(G_last - G)
-  float eg[CB];  // exp(G) * scale
-  float su[CB];  // exp(G_blk) * scale
-  float rq[NWAVES][CB];
-};
-
-template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_bwd_fwdorder(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
-    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const T* __restrict__ dO, const float* __restrict__ S0, const float* __restrict__ S_end,
-    T* __restrict__ dq, float* __restrict__ rq_out, float* __restrict__ U_out) {
-  using SG = Stage<T, D>;
-  using ST = StateTiles<D>;
-  __shared__ BfSmem<T, D> sm;
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int li = bk[BLK_SEQ];
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
-  const int64_t DD = static_cast<int64_t>(D) * D;
-  f32x4 St[ST::N];  // S^T : tile (dv, dk), wave owns dk column tiles
-  f32x4 U[ST::N];   // U   : tile (dk, dv), wave owns dv column tiles
-  state_load<D>(St, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
-                                     : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                true, w, lane);
-#pragma unroll
-  for (int i = 0; i < ST::N; ++i) U[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float Gs = 0.f;  // log-decay from the block start to the current chunk start
-  for (int c = c0; c < c0 + nc; ++c) {
-    chunk_setup(sm.cr, sm.G, seq, c, replay_row, g, H, h, t);
-    __syncthreads();
-    const float GL = sm.G[CB - 1];
-    if (t < CB) {
-      sm.sv[t] = __expf(GL - sm.G[t]);
-      sm.eg[t] = __expf(sm.G[t]) * scale;
-      sm.su[t] = __expf(Gs + sm.G[t]) * scale;
-    }
-    Vec16 lq[SG::NV], lk[SG::NV], lv[SG::NV], ld[SG::NV];
-    load_chunk<T, D>(lq, q, sm.cr, H, h, t, ROW_OWN);
-    load_chunk<T, D>(lk, k, sm.cr, H, h, t, ROW_REPLAY);
-    load_chunk<T, D>(lv, v, sm.cr, H, h, t, ROW_REPLAY);
-    load_chunk<T, D>(ld, dO, sm.cr, H, h, t, ROW_OWN);
-    __syncthreads();
-    store_rowmajor<T, D>(sm.dO, ld, t);
-    store_rowmajor<T, D>(sm.V, lv, t);
-    store_transposed<T, D>(sm.Kt, lk, nullptr, t);
-    store_transposed<T, D>(sm.Vs, lv, sm.sv, t);
-    store_transposed<T, D>(sm.Qt, lq, nullptr, t);
-    store_transposed<T, D>(sm.dOs, ld, sm.su, t);
-    __syncthreads();
-    // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w owns rows 16w..
-#pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) {
-      f32x4 a = {0.f, 0.f, 0.f, 0.f};
-      Mma<T>::tile(a, sm.dO + 16 * w * SG::LDR, SG::LDR, sm.V + jt * 16 * SG::LDR, SG::LDR, D, lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = 16 * w + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-        sm.dA[m * SG::LDA + n] =
-            Elem<T>::from_f(n <= m ? a[r] * __expf(sm.G[m] - sm.G[n]) * scale : 0.f);
-      }
-    }
-    __syncthreads();
-    // dq[:, wave's dk columns] = scale diag(exp(G)) dO S_c^T + dA K
-    for (int it = 0; it < CB / 16; ++it) {
-      float part[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int cc = 0; cc < ST::CPW; ++cc) {
-        const int nt = w * ST::CPW + cc;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kt = 0; kt < ST::NT; ++kt)
-          MmaRegB<T>::step(acc, sm.dO + it * 16 * SG::LDR + kt * 16, SG::LDR, St[kt * ST::CPW + cc], lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
-        Mma<T>::tile(acc, sm.dA + it * 16 * SG::LDA, SG::LDA, sm.Kt + nt * 16 * SG::LDT, SG::LDT, CB,
-                     lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = it * 16 + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-          part[r] += Elem<T>::to_f(sm.Qt[n * SG::LDT + m]) * acc[r];
-          if (sm.cr.kind[m] == ROW_OWN)
-            dq[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float s = sum16(part[r]);
-        if ((lane & 15) == 0) sm.rq[w][it * 16 + acc_row(lane, r)] = s;
-      }
-    }
-    // U += (Q * exp(G_blk) * scale)^T dO ; S^T <- exp(G_last) S^T + (V * exp(G_last - G))^T K
-    const float dec = __expf(GL);
-#pragma unroll
-    for (int i = 0; i < ST::N; ++i) {
-      Mma<T>::tile(U[i], sm.Qt + ST::mt(i) * 16 * SG::LDT, SG::LDT,
-                   sm.dOs + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
-      St[i] *= dec;
-      Mma<T>::tile(St[i], sm.Vs + ST::mt(i) * 16 * SG::LDT, SG::LDT,
-                   sm.Kt + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
-    }
-    __syncthreads();
-    if (t < CB) {
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < NWAVES; ++i) s += sm.rq[i][t];
-      rq_out[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] = s;
-    }
-    Gs += GL;
-  }
-  state_store<D>(U_out + (static_cast<int64_t>(b) * H + h) * DD, U, w, lane);
-}
-
-// ---------------------------------------------------------------------------
-// backward: reverse chain over the blocks of every sequence (element-parallel)
-// ---------------------------------------------------------------------------
-__device__ inline float block_sum(float x, float* red, int t) {
+__device__ inline float scan_block_sum(float x, float* red, int t) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
   __syncthreads();
@@ -494,21 +275,21 @@ __device__ inline float block_sum(float x, float* red, int t) {
   __syncthreads();
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < NWAVES; ++i) s += red[i];
+  for (int i = 0; i < SCAN_THR / 64; ++i) s += red[i];
   return s;
 }
 
 template <int D>
-__global__ __launch_bounds__(NTHREADS) void k_bwd_blockscan(
+__global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
     const float* __restrict__ dS_final, const float* __restrict__ dbank,
     const float* __restrict__ S_end, const float* __restrict__ U, const float* __restrict__ gam,
     float* __restrict__ dS_end, float* __restrict__ dS0, float* __restrict__ betap) {
   constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
-  constexpr int NSW = static_cast<int>(SS4 / NTHREADS);
-  __shared__ float red[NWAVES];
+  constexpr int NSW = static_cast<int>(SS4 / SCAN_THR);
+  __shared__ float red[SCAN_THR / 64];
   const int li = blockIdx.x / NSW, part = blockIdx.x % NSW, h = blockIdx.y, t = threadIdx.x;
-  const int64_t e4 = static_cast<int64_t>(part) * NTHREADS + t;
+  const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + t;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
   const float4* S4 = reinterpret_cast<const float4*>(S_end);
@@ -516,7 +297,7 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_blockscan(
   {
     const int bl = b0 + nb - 1;
     const float4 s = S4[(static_cast<int64_t>(bl) * H + h) * SS4 + e4];
-    const float bsum = block_sum(ds.x * s.x + ds.y * s.y + ds.z * s.z + ds.w * s.w, red, t);
+    const float bsum = scan_block_sum(ds.x * s.x + ds.y * s.y + ds.z * s.z + ds.w * s.w, red, t);
     if (t == 0) betap[(static_cast<int64_t>(bl) * H + h) * NSW + part] = bsum;
   }
   for (int b = b0 + nb - 1; b >= b0; --b) {
@@ -531,17 +312,16 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_blockscan(
     if (b > b0) {
       const int64_t pi = static_cast<int64_t>(b - 1) * H + h;
       const int eb = blk_tab[(b - 1) * BLK_WORDS + BLK_END_BANK];
-      float dot = 0.f;
-      if (eb >= 0) {
+      float bsum = 0.f;
+      if (eb >= 0) {  // uniform over the workgroup
         const float4 inj = reinterpret_cast<const float4*>(dbank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4];
         const float4 s = S4[pi * SS4 + e4];
-        dot = inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w;
+        bsum = scan_block_sum(inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w, red, t);
         ds.x += inj.x;
         ds.y += inj.y;
         ds.z += inj.z;
         ds.w += inj.w;
       }
-      const float bsum = eb >= 0 ? block_sum(dot, red, t) : 0.f;
       if (t == 0) betap[pi * NSW + part] = bsum;
     }
   }
@@ -549,165 +329,390 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_blockscan(
 }
 
 // ---------------------------------------------------------------------------
+// forward: outputs of the own rows of a block
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct FwdSmem {
+  using C = Cfg<T, D>;
+  T Q[CB * C::LDR];
+  T K[CB * C::LDR];
+  T Ks[CB * C::LDR];  // K * exp(G_last - G)
+  T V[CB * C::LDR];
+  T A[CB * C::LDA];   // masked Q K^T
+  ChunkMeta meta;
+  float sk[CB];       // exp(G_last - G)
+  float eg[CB];       // exp(G)
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_fwd_block(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
+    const float* __restrict__ S0, const float* __restrict__ S_end, T* __restrict__ o) {
+  using C = Cfg<T, D>;
+  __shared__ FwdSmem<T, D> sm;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int li = bk[BLK_SEQ];
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  const int64_t DD = static_cast<int64_t>(D) * D;
+  f32x4 S[C::NT];  // S : tile i = rows (dk) 16i.., columns (dv) 16w..
+  state_load<D>(S, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                    : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                false, w, lane);
+  ChunkRefs<T, D> refs;
+  Vec16 pq[C::NV], pk[C::NV], pv[C::NV];
+  refs.resolve(seq, c0, replay_row, t);
+  fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
+  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+  float gp = fetch_g(seq, c0, replay_row, g, H, h, t);
+  for (int c = c0; c < c_end; ++c) {
+    float Gt, GLw;
+    meta_setup(sm.meta, seq, c, replay_row, gp, t, Gt, GLw);
+    if (t < CB) {
+      sm.sk[t] = __expf(GLw - Gt);
+      sm.eg[t] = __expf(Gt);
+    }
+    __syncthreads();
+    const float GL = sm.meta.G[CB - 1];
+    put<T, D>(sm.Q, pq, nullptr, t);
+    put<T, D>(sm.K, pk, nullptr, t);
+    put<T, D>(sm.Ks, pk, sm.sk, t);
+    put<T, D>(sm.V, pv, nullptr, t);
+    __syncthreads();
+    if (c + 1 < c_end) {
+      refs.resolve(seq, c + 1, replay_row, t);
+      fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
+      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+      gp = fetch_g(seq, c + 1, replay_row, g, H, h, t);
+    }
+    // A = (Q K^T) * exp(G_i - G_j) [j <= i]
+#pragma unroll
+    for (int x = w * C::ATPW; x < (w + 1) * C::ATPW; ++x) {
+      const int it = x >> 2, jt = x & 3;
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      tile<T, false, false>(a, sm.Q + it * 16 * C::LDR, C::LDR, sm.K + jt * 16 * C::LDR, C::LDR, D, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+        sm.A[m * C::LDA + n] =
+            Elem<T>::from_f(n <= m ? a[r] * __expf(sm.meta.G[m] - sm.meta.G[n]) : 0.f);
+      }
+    }
+    __syncthreads();
+    // O[:, 16w..] = scale * (diag(exp(G)) Q S_c + A V)
+#pragma unroll
+    for (int it = 0; it < CB / 16; ++it) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kt = 0; kt < C::NT; ++kt)
+        MmaRegB<T>::step(acc, sm.Q + it * 16 * C::LDR + kt * 16, C::LDR, S[kt], lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
+      tile<T, false, true>(acc, sm.A + it * 16 * C::LDA, C::LDA, sm.V + w * 16, C::LDR, CB, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = it * 16 + acc_row(lane, r);
+        if (sm.meta.kind[m] == ROW_OWN)
+          o[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + w * 16 + acc_col(lane)] =
+              Elem<T>::from_f(acc[r] * scale);
+      }
+    }
+    // S_{c+1} = exp(G_last) S_c + (K * exp(G_last - G))^T V
+    const float dec = __expf(GL);
+#pragma unroll
+    for (int i = 0; i < C::NT; ++i) {
+      S[i] *= dec;
+      tile<T, true, true>(S[i], sm.Ks + i * 16, C::LDR, sm.V + w * 16, C::LDR, CB, lane);
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward, forward order: dq, q.dq per row and the block's local adjoint
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+struct BfSmem {
+  using C = Cfg<T, D>;
+  T dO[CB * C::LDR];
+  T V[CB * C::LDR];
+  T K[CB * C::LDR];
+  T Q[CB * C::LDR];   // own rows
+  T Qh[CB * C::LDR];  // Q * exp(G_blk) * scale, G_blk counted from the block start
+  T Vs[CB * C::LDR];  // V * exp(G_last - G)
+  T dA[CB * C::LDA];  // scale * (dO V^T) masked
+  ChunkMeta meta;
+  float sv[CB];       // exp(G_last - G)
+  float eg[CB];       // exp(G) * scale
+  float su[CB];       // exp(G_blk) * scale
+  float rq[C::NW][CB];
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_bwd_fwdorder(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
+    const T* __restrict__ dO, const float* __restrict__ S0, const float* __restrict__ S_end,
+    T* __restrict__ dq, float* __restrict__ rq_out, float* __restrict__ U_out) {
+  using C = Cfg<T, D>;
+  __shared__ BfSmem<T, D> sm;
+  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int li = bk[BLK_SEQ];
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  const int64_t DD = static_cast<int64_t>(D) * D;
+  f32x4 St[C::NT];  // S^T : tile i = rows (dv) 16i.., columns (dk) 16w..
+  f32x4 U[C::NT];   // U   : tile i = rows (dk) 16i.., columns (dv) 16w..
+  state_load<D>(St, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                     : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                true, w, lane);
+#pragma unroll
+  for (int i = 0; i < C::NT; ++i) U[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ChunkRefs<T, D> refs;
+  Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
+  refs.resolve(seq, c0, replay_row, t);
+  fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
+  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
+  float gp = fetch_g(seq, c0, replay_row, g, H, h, t);
+  float Gs = 0.f;  // log-decay from the block start to the current chunk start
+  for (int c = c0; c < c_end; ++c) {
+    float Gt, GLw;
+    meta_setup(sm.meta, seq, c, replay_row, gp, t, Gt, GLw);
+    if (t < CB) {
+      sm.sv[t] = __expf(GLw - Gt);
+      sm.eg[t] = __expf(Gt) * scale;
+      sm.su[t] = __expf(Gs + Gt) * scale;
+    }
+    __syncthreads();
+    const float GL = sm.meta.G[CB - 1];
+    put<T, D>(sm.dO, pd, nullptr, t);
+    put<T, D>(sm.V, pv, nullptr, t);
+    put<T, D>(sm.K, pk, nullptr, t);
+    put<T, D>(sm.Q, pq, nullptr, t);
+    put<T, D>(sm.Qh, pq, sm.su, t);
+    put<T, D>(sm.Vs, pv, sm.sv, t);
+    __syncthreads();
+    if (c + 1 < c_end) {
+      refs.resolve(seq, c + 1, replay_row, t);
+      fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
+      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
+      gp = fetch_g(seq, c + 1, replay_row, g, H, h, t);
+    }
+    // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]
+#pragma unroll
+    for (int x = w * C::ATPW; x < (w + 1) * C::ATPW; ++x) {
+      const int it = x >> 2, jt = x & 3;
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      tile<T, false, false>(a, sm.dO + it * 16 * C::LDR, C::LDR, sm.V + jt * 16 * C::LDR, C::LDR, D, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+        sm.dA[m * C::LDA + n] =
+            Elem<T>::from_f(n <= m ? a[r] * __expf(sm.meta.G[m] - sm.meta.G[n]) * scale : 0.f);
+      }
+    }
+    __syncthreads();
+    // dq[:, 16w..] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
+#pragma unroll
+    for (int it = 0; it < CB / 16; ++it) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kt = 0; kt < C::NT; ++kt)
+        MmaRegB<T>::step(acc, sm.dO + it * 16 * C::LDR + kt * 16, C::LDR, St[kt], lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
+      tile<T, false, true>(acc, sm.dA + it * 16 * C::LDA, C::LDA, sm.K + w * 16, C::LDR, CB, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = it * 16 + acc_row(lane, r), n = w * 16 + acc_col(lane);
+        const float s = sum16(Elem<T>::to_f(sm.Q[m * C::LDR + n]) * acc[r]);
+        if ((lane & 15) == 0) sm.rq[w][m] = s;
+        if (sm.meta.kind[m] == ROW_OWN)
+          dq[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+      }
+    }
+    // U += (Q * exp(G_blk) * scale)^T dO ; S^T <- exp(G_last) S^T + (V * exp(G_last - G))^T K
+    const float dec = __expf(GL);
+#pragma unroll
+    for (int i = 0; i < C::NT; ++i) {
+      tile<T, true, true>(U[i], sm.Qh + i * 16, C::LDR, sm.dO + w * 16, C::LDR, CB, lane);
+      St[i] *= dec;
+      tile<T, true, true>(St[i], sm.Vs + i * 16, C::LDR, sm.K + w * 16, C::LDR, CB, lane);
+    }
+    __syncthreads();
+    if (t < CB) {
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < C::NW; ++i) s += sm.rq[i][t];
+      rq_out[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] = s;
+    }
+    Gs += GL;
+  }
+  state_store<D>(U_out + (static_cast<int64_t>(b) * H + h) * DD, U, w, lane);
+}
+
+// ---------------------------------------------------------------------------
 // backward, reverse order: dk, dv, k.dk and local suffix sums of dg
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 struct BrSmem {
-  using SG = Stage<T, D>;
-  T Q[CB * SG::LDR];
-  T K[CB * SG::LDR];
-  T V[CB * SG::LDR];
-  T dO[CB * SG::LDR];
-  T Qt[D * SG::LDT];   // Q^T (own rows)
-  T Qs[D * SG::LDT];   // (Q * exp(G) * scale)^T
-  T dOt[D * SG::LDT];  // dO^T
-  T At[CB * SG::LDA];  // A^T
-  T dAt[CB * SG::LDA]; // dA^T
-  ChunkRows cr;
-  float G[CB];
-  float sk[CB];  // exp(G_last - G)
-  float eg[CB];  // exp(G) * scale
-  float rk[NWAVES][CB];
+  using C = Cfg<T, D>;
+  T Q[CB * C::LDR];   // own rows
+  T K[CB * C::LDR];
+  T V[CB * C::LDR];
+  T dO[CB * C::LDR];  // own rows
+  T Qs[CB * C::LDR];  // Q * exp(G) * scale
+  T A[CB * C::LDA];   // masked Q K^T
+  T dA[CB * C::LDA];  // scale * (dO V^T) masked
+  ChunkMeta meta;
+  float sk[CB];       // exp(G_last - G)
+  float eg[CB];       // exp(G) * scale
+  float rk[C::NW][CB];
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__(NTHREADS) void k_bwd_revorder(
+__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_bwd_revorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const T* __restrict__ dO, const float* __restrict__ dS_end, const float* __restrict__ rq,
     T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dg, float* __restrict__ rep_grad,
     float* __restrict__ Rb) {
-  using SG = Stage<T, D>;
-  using ST = StateTiles<D>;
+  using C = Cfg<T, D>;
   constexpr int RG = 2 * D + 1;
   __shared__ BrSmem<T, D> sm;
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
   const float* dse = dS_end + (static_cast<int64_t>(b) * H + h) * DD;
-  f32x4 dSt[ST::N];  // dS^T : tile (dv, dk), wave owns dk column tiles
-  f32x4 dSn[ST::N];  // dS   : tile (dk, dv), wave owns dv column tiles
+  f32x4 dSt[C::NT];  // dS^T : tile i = rows (dv) 16i.., columns (dk) 16w..
+  f32x4 dSn[C::NT];  // dS   : tile i = rows (dk) 16i.., columns (dv) 16w..
   state_load<D>(dSt, dse, true, w, lane);
   state_load<D>(dSn, dse, false, w, lane);
   const float inv_scale = 1.f / scale;
   float carry = 0.f;  // sum of (q.dq - k.dk) over the later chunks of the block
-  for (int c = c0 + nc - 1; c >= c0; --c) {
-    chunk_setup(sm.cr, sm.G, seq, c, replay_row, g, H, h, t);
-    __syncthreads();
-    const float GL = sm.G[CB - 1];
+  ChunkRefs<T, D> refs;
+  Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
+  refs.resolve(seq, c_last, replay_row, t);
+  fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
+  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
+  float gp = fetch_g(seq, c_last, replay_row, g, H, h, t);
+  for (int c = c_last; c >= c0; --c) {
+    float Gt, GLw;
+    meta_setup(sm.meta, seq, c, replay_row, gp, t, Gt, GLw);
     if (t < CB) {
-      sm.sk[t] = __expf(GL - sm.G[t]);
-      sm.eg[t] = __expf(sm.G[t]) * scale;
+      sm.sk[t] = __expf(GLw - Gt);
+      sm.eg[t] = __expf(Gt) * scale;
     }
-    Vec16 lq[SG::NV], lk[SG::NV], lv[SG::NV], ld[SG::NV];
-    load_chunk<T, D>(lq, q, sm.cr, H, h, t, ROW_OWN);
-    load_chunk<T, D>(lk, k, sm.cr, H, h, t, ROW_REPLAY);
-    load_chunk<T, D>(lv, v, sm.cr, H, h, t, ROW_REPLAY);
-    load_chunk<T, D>(ld, dO, sm.cr, H, h, t, ROW_OWN);
     __syncthreads();
-    store_rowmajor<T, D>(sm.Q, lq, t);
-    store_rowmajor<T, D>(sm.K, lk, t);
-    store_rowmajor<T, D>(sm.V, lv, t);
-    store_rowmajor<T, D>(sm.dO, ld, t);
-    store_transposed<T, D>(sm.Qt, lq, nullptr, t);
-    store_transposed<T, D>(sm.Qs, lq, sm.eg, t);
-    store_transposed<T, D>(sm.dOt, ld, nullptr, t);
+    const float GL = sm.meta.G[CB - 1];
+    put<T, D>(sm.Q, pq, nullptr, t);
+    put<T, D>(sm.K, pk, nullptr, t);
+    put<T, D>(sm.V, pv, nullptr, t);
+    put<T, D>(sm.dO, pd, nullptr, t);
+    put<T, D>(sm.Qs, pq, sm.eg, t);
     __syncthreads();
-    // A and dA (masked), stored transposed; wave w owns rows i in 16w..
+    if (c > c0) {
+      refs.resolve(seq, c - 1, replay_row, t);
+      fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
+      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
+      gp = fetch_g(seq, c - 1, replay_row, g, H, h, t);
+    }
+    // A and dA, masked
 #pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) {
+    for (int x = w * C::ATPW; x < (w + 1) * C::ATPW; ++x) {
+      const int it = x >> 2, jt = x & 3;
       f32x4 a = {0.f, 0.f, 0.f, 0.f}, da = {0.f, 0.f, 0.f, 0.f};
-      Mma<T>::tile(a, sm.Q + 16 * w * SG::LDR, SG::LDR, sm.K + jt * 16 * SG::LDR, SG::LDR, D, lane);
-      Mma<T>::tile(da, sm.dO + 16 * w * SG::LDR, SG::LDR, sm.V + jt * 16 * SG::LDR, SG::LDR, D, lane);
+      tile<T, false, false>(a, sm.Q + it * 16 * C::LDR, C::LDR, sm.K + jt * 16 * C::LDR, C::LDR, D, lane);
+      tile<T, false, false>(da, sm.dO + it * 16 * C::LDR, C::LDR, sm.V + jt * 16 * C::LDR, C::LDR, D, lane);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = 16 * w + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-        const float dm = n <= m ? __expf(sm.G[m] - sm.G[n]) : 0.f;
-        sm.At[n * SG::LDA + m] = Elem<T>::from_f(a[r] * dm);
-        sm.dAt[n * SG::LDA + m] = Elem<T>::from_f(da[r] * dm * scale);
+        const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+        const float dm = n <= m ? __expf(sm.meta.G[m] - sm.meta.G[n]) : 0.f;
+        sm.A[m * C::LDA + n] = Elem<T>::from_f(a[r] * dm);
+        sm.dA[m * C::LDA + n] = Elem<T>::from_f(da[r] * dm * scale);
       }
     }
     __syncthreads();
-    // dk[:, wave's dk columns] = diag(exp(G_last - G)) V dS^T + dA^T Q
+    // dk[:, 16w..] = diag(exp(G_last - G)) V dS^T + dA^T Q ; partial k.dk
+#pragma unroll
     for (int jt = 0; jt < CB / 16; ++jt) {
-      float part[4] = {0.f, 0.f, 0.f, 0.f};
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int cc = 0; cc < ST::CPW; ++cc) {
-        const int nt = w * ST::CPW + cc;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int kt = 0; kt < C::NT; ++kt)
+        MmaRegB<T>::step(acc, sm.V + jt * 16 * C::LDR + kt * 16, C::LDR, dSt[kt], lane);
 #pragma unroll
-        for (int kt = 0; kt < ST::NT; ++kt)
-          MmaRegB<T>::step(acc, sm.V + jt * 16 * SG::LDR + kt * 16, SG::LDR, dSt[kt * ST::CPW + cc], lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)];
-        Mma<T>::tile(acc, sm.dAt + jt * 16 * SG::LDA, SG::LDA, sm.Qt + nt * 16 * SG::LDT, SG::LDT, CB,
-                     lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = jt * 16 + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-          part[r] += Elem<T>::to_f(sm.K[m * SG::LDR + n]) * acc[r];
-          const int kind = sm.cr.kind[m];
-          if (kind == ROW_OWN)
-            dk[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
-          else if (kind == ROW_REPLAY)
-            rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + n] = acc[r];
-        }
-      }
+      for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)];
+      tile<T, true, true>(acc, sm.dA + jt * 16, C::LDA, sm.Q + w * 16, C::LDR, CB, lane);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float s = sum16(part[r]);
-        if ((lane & 15) == 0) sm.rk[w][jt * 16 + acc_row(lane, r)] = s;
+        const int m = jt * 16 + acc_row(lane, r), n = w * 16 + acc_col(lane);
+        const float s = sum16(Elem<T>::to_f(sm.K[m * C::LDR + n]) * acc[r]);
+        if ((lane & 15) == 0) sm.rk[w][m] = s;
+        const int kind = sm.meta.kind[m];
+        if (kind == ROW_OWN)
+          dk[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+        else if (kind == ROW_REPLAY)
+          rep_grad[(static_cast<int64_t>(sm.meta.rep[m]) * H + h) * RG + n] = acc[r];
       }
     }
-    // dv[:, wave's dv columns] = diag(exp(G_last - G)) K dS + scale A^T dO
+    // dv[:, 16w..] = diag(exp(G_last - G)) K dS + scale A^T dO
+#pragma unroll
     for (int jt = 0; jt < CB / 16; ++jt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int cc = 0; cc < ST::CPW; ++cc) {
-        const int nt = w * ST::CPW + cc;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int kt = 0; kt < C::NT; ++kt)
+        MmaRegB<T>::step(acc, sm.K + jt * 16 * C::LDR + kt * 16, C::LDR, dSn[kt], lane);
 #pragma unroll
-        for (int kt = 0; kt < ST::NT; ++kt)
-          MmaRegB<T>::step(acc, sm.K + jt * 16 * SG::LDR + kt * 16, SG::LDR, dSn[kt * ST::CPW + cc], lane);
+      for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)] * inv_scale;
+      tile<T, true, true>(acc, sm.A + jt * 16, C::LDA, sm.dO + w * 16, C::LDR, CB, lane);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)] * inv_scale;
-        Mma<T>::tile(acc, sm.At + jt * 16 * SG::LDA, SG::LDA, sm.dOt + nt * 16 * SG::LDT, SG::LDT, CB,
-                     lane);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = jt * 16 + acc_row(lane, r), n = nt * 16 + acc_col(lane);
-          const float val = acc[r] * scale;
-          const int kind = sm.cr.kind[m];
-          if (kind == ROW_OWN)
-            dv[(static_cast<int64_t>(sm.cr.row[m]) * H + h) * D + n] = Elem<T>::from_f(val);
-          else if (kind == ROW_REPLAY)
-            rep_grad[(static_cast<int64_t>(sm.cr.rep[m]) * H + h) * RG + D + n] = val;
-        }
+      for (int r = 0; r < 4; ++r) {
+        const int m = jt * 16 + acc_row(lane, r), n = w * 16 + acc_col(lane);
+        const float val = acc[r] * scale;
+        const int kind = sm.meta.kind[m];
+        if (kind == ROW_OWN)
+          dv[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + n] = Elem<T>::from_f(val);
+        else if (kind == ROW_REPLAY)
+          rep_grad[(static_cast<int64_t>(sm.meta.rep[m]) * H + h) * RG + D + n] = val;
       }
     }
     // dS_c = exp(G_last) dS_{c+1} + (Q * exp(G) * scale)^T dO, in both layouts
     const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < ST::N; ++i) {
+    for (int i = 0; i < C::NT; ++i) {
       dSn[i] *= dec;
-      Mma<T>::tile(dSn[i], sm.Qs + ST::mt(i) * 16 * SG::LDT, SG::LDT,
-                   sm.dOt + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+      tile<T, true, true>(dSn[i], sm.Qs + i * 16, C::LDR, sm.dO + w * 16, C::LDR, CB, lane);
       dSt[i] *= dec;
-      Mma<T>::tile(dSt[i], sm.dOt + ST::mt(i) * 16 * SG::LDT, SG::LDT,
-                   sm.Qs + ST::nt(w, i) * 16 * SG::LDT, SG::LDT, CB, lane);
+      tile<T, true, true>(dSt[i], sm.dO + i * 16, C::LDR, sm.Qs + w * 16, C::LDR, CB, lane);
     }
     __syncthreads();
     // local suffix sums of q.dq - k.dk (wave 0, one row per lane)
     if (t < CB) {
-      const int kind = sm.cr.kind[t];
+      const int kind = sm.meta.kind[t];
       float x = 0.f;
       if (kind != ROW_PAD) {
         float rks = 0.f;
 #pragma unroll
-        for (int i = 0; i < NWAVES; ++i) rks += sm.rk[i][t];
+        for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][t];
         x = rq[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] - rks;
       }
 #pragma unroll
@@ -716,9 +721,9 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_revorder(
         if (t + off < CB) x += y;
       }
       const float val = x + carry;
-      if (kind == ROW_OWN) dg[static_cast<int64_t>(sm.cr.row[t]) * H + h] = val;
+      if (kind == ROW_OWN) dg[static_cast<int64_t>(sm.meta.row[t]) * H + h] = val;
       else if (kind == ROW_REPLAY)
-        rep_grad[(static_cast<int64_t>(sm.cr.rep[t]) * H + h) * RG + 2 * D] = val;
+        rep_grad[(static_cast<int64_t>(sm.meta.rep[t]) * H + h) * RG + 2 * D] = val;
       carry += __shfl(x, 0, CB);
     }
   }
@@ -729,11 +734,11 @@ __global__ __launch_bounds__(NTHREADS) void k_bwd_revorder(
 // dg: add the contributions of later blocks and of the boundary terms
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(NTHREADS) void k_dg_carry(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ replay_row, int H, const float* __restrict__ betap,
-    const float* __restrict__ Rb, float* __restrict__ dg, float* __restrict__ rep_grad) {
-  constexpr int NSW = D * D / 4 / NTHREADS;
+__global__ __launch_bounds__(SCAN_THR) void k_dg_carry(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
+    const float* __restrict__ betap, const float* __restrict__ Rb, float* __restrict__ dg,
+    float* __restrict__ rep_grad) {
+  constexpr int NSW = D * D / 4 / SCAN_THR;
   constexpr int RG = 2 * D + 1;
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
@@ -747,7 +752,7 @@ __global__ __launch_bounds__(NTHREADS) void k_dg_carry(
   }
   const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
   const int n_rep = seq[SEQ_N_REPLAY], n_tok = seq[SEQ_N_TOK];
-  for (int idx = t; idx < nc * CB; idx += NTHREADS) {
+  for (int idx = t; idx < nc * CB; idx += SCAN_THR) {
     const int p = c0 * CB + idx;
     if (p < n_rep) {
       const int j = seq[SEQ_REPLAY_OFF] + p;
@@ -900,7 +905,7 @@ struct Sizes {
 Sizes sizes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
   const RoundLayout& L = p->rounds[round];
   Sizes s{};
-  const size_t nsw = static_cast<size_t>(D) * D / 4 / NTHREADS;
+  const size_t nsw = static_cast<size_t>(D) * D / 4 / SCAN_THR;
   s.blk_state = align256(static_cast<size_t>(L.n_blk) * H * D * D * sizeof(float));
   s.gam = align256(static_cast<size_t>(L.n_blk) * H * sizeof(float));
   s.rq = align256(static_cast<size_t>(L.n_chunks) * CB * H * sizeof(float));
@@ -933,15 +938,15 @@ int launch_state_pass(const harts_plan_t* p, int32_t round, const Blob& B, int H
   const RoundLayout& L = p->rounds[round];
   {
     ProfScope ps("k_fwd_blocksum", s);
-    hipLaunchKernelGGL((k_fwd_blocksum<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+    hipLaunchKernelGGL((k_fwd_blocksum<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.replay_row, H, static_cast<const T*>(k),
                        static_cast<const T*>(v), g, dSb, gam);
   }
   if (int rc = hip_check("k_fwd_blocksum")) return rc;
   {
-    constexpr int NSW = D * D / 4 / NTHREADS;
+    constexpr int NSW = D * D / 4 / SCAN_THR;
     ProfScope ps("k_fwd_blockscan", s);
-    hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(NTHREADS), 0, s,
+    hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
                        B.seq_tab, B.blk_tab, H, S0, dSb, gam, S_end, bank, S_final);
   }
   return hip_check("k_fwd_blockscan");
@@ -963,7 +968,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
   {
     ProfScope ps("k_fwd_block", s);
-    hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+    hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g, S0, S_end,
                        static_cast<T*>(o));
@@ -1004,23 +1009,23 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   const float* gam = reinterpret_cast<const float*>(saved + z.blk_state);
   {
     ProfScope ps("k_bwd_fwdorder", s);
-    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq, U);
   }
   if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
-    constexpr int NSW = D * D / 4 / NTHREADS;
+    constexpr int NSW = D * D / 4 / SCAN_THR;
     ProfScope ps("k_bwd_blockscan", s);
-    hipLaunchKernelGGL((k_bwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(NTHREADS), 0, s,
+    hipLaunchKernelGGL((k_bwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
                        B.seq_tab, B.blk_tab, H, dS_final, dbank, S_end, U, gam, dS_end, dS0,
                        betap);
   }
   if (int rc = hip_check("k_bwd_blockscan")) return rc;
   {
     ProfScope ps("k_bwd_revorder", s);
-    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
+    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), dS_end, rq, static_cast<T*>(dk),
@@ -1029,8 +1034,8 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   if (int rc = hip_check("k_bwd_revorder")) return rc;
   {
     ProfScope ps("k_dg_carry", s);
-    hipLaunchKernelGGL((k_dg_carry<D>), dim3(L.n_blk, H), dim3(NTHREADS), 0, s, B.seq_tab,
-                       B.blk_tab, B.replay_row, H, betap, Rb, dg, rep_grad);
+    hipLaunchKernelGGL((k_dg_carry<D>), dim3(L.n_blk, H), dim3(SCAN_THR), 0, s, B.seq_tab,
+                       B.blk_tab, H, betap, Rb, dg, rep_grad);
   }
   return hip_check("k_dg_carry");
 }

@@ -7,6 +7,7 @@
 // linear in the number of segments plus the replay length.
 #include <algorithm>
 #include <climits>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -371,6 +372,12 @@ struct Builder {
   void build_blob() {
     harts_plan_s& p = *P;
     const int32_t K = p.K;
+    // Target number of blocks per round (tuning knob, default 128).
+    int32_t min_blocks = 128;
+    if (const char* env = std::getenv("HARTS_MIN_BLOCKS")) {
+      const long x = std::strtol(env, nullptr, 10);
+      if (x >= 1 && x <= (1 << 20)) min_blocks = static_cast<int32_t>(x);
+    }
     int64_t off = 0;
     p.rounds.assign(K, RoundLayout{});
     p.n_chunks = 0;
@@ -390,10 +397,11 @@ struct Builder {
       }
       p.n_chunks += L.n_chunks;
       // block size: the largest of 64, 32, 16, 8 chunks that still cuts the
-      // round into >= 48 blocks (so that (block, head) work units fill the GPU)
+      // round into >= min_blocks blocks, so that (block, head) work units
+      // fill the GPU and no single block dominates the critical path
       L.block_chunks = 8;
       for (int32_t cand = 64; cand >= 8; cand /= 2) {
-        if (count_blocks(L, cand) >= 48) { L.block_chunks = cand; break; }
+        if (count_blocks(L, cand) >= min_blocks) { L.block_chunks = cand; break; }
       }
       L.n_blk = count_blocks(L, L.block_chunks);
       L.seq_tab = off;
@@ -608,6 +616,8 @@ extern "C" int harts_plan_round_info(const harts_plan_t* p, int32_t round, harts
   const harts::RoundLayout& L = p->rounds[round];
   info->n_seq = L.n_seq;
   info->seq_begin = L.seq_begin;
+  info->n_blk = L.n_blk;
+  info->block_chunks = L.block_chunks;
   info->n_chunks = L.n_chunks;
   info->n_rows = L.n_rows;
   info->n_own = L.n_own;
