@@ -82,7 +82,7 @@ def algorithmic_bytes(plan, H, d, el):
     materialised.  Returns (bytes per step, launches per step) per kernel."""
     st = H * d * d * 4
     K = plan.info["n_rounds"]
-    b = dict.fromkeys(["k_fwd_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder",
+    b = dict.fromkeys(["k_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder",
                        "k_bwd_blockscan", "k_bwd_revorder", "k_dg_carry", "k_gather",
                        "k_scatter_add"], 0)
     for r in plan.rounds:
@@ -91,10 +91,12 @@ def algorithmic_bytes(plan, H, d, el):
         nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i]
                        for i in range(r["seq_begin"], r["seq_begin"] + nseq)))
         kv = rows * H * (2 * d * el + 4)                       # k, v, g of every packed row
-        b["k_fwd_blocksum"] += 2 * (kv + nblk * st)            # forward + recompute pass
+        qdo = own * H * 2 * d * el + rows * H * 4                # q, dO of own rows, g
+        # side 0 (k, v) in the forward and the recompute pass, side 1 (q, dO) in backward
+        b["k_blocksum"] += 2 * (kv + nblk * st) + qdo + nblk * st
         b["k_fwd_blockscan"] += 2 * (nseq * st + 2 * nblk * st + nreq * st + nseq * st)
         b["k_fwd_block"] += kv + own * H * 2 * d * el + nblk * st
-        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + 2 * nblk * st
+        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + nblk * st
         b["k_bwd_blockscan"] += 4 * nblk * st + nseq * st + nreq * st + nseq * st
         b["k_bwd_revorder"] += (kv + own * H * (2 * d * el + 2 * d * el + 4)
                                 + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st)
@@ -103,7 +105,7 @@ def algorithmic_bytes(plan, H, d, el):
         b["k_scatter_add"] += 3 * nseq * st
     R = plan.info["R"]
     b["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
-    launches = {"k_fwd_blocksum": 2 * K, "k_fwd_blockscan": 2 * K, "k_fwd_block": K,
+    launches = {"k_blocksum": 2 * K, "k_fwd_blockscan": 2 * K, "k_fwd_block": K,
                 "k_bwd_fwdorder": K, "k_bwd_blockscan": K, "k_bwd_revorder": K,
                 "k_dg_carry": K, "k_gather": 2 * K, "k_scatter_add": K,
                 "k_replay_reduce": 1 if R else 0}

@@ -11,28 +11,32 @@
 // Work decomposition.  Every sequence of a round is cut into blocks of
 // consecutive chunks (the planner ends a block at every requested boundary
 // and at most every block_chunks chunks).  One workgroup owns one
-// (block, head) and keeps the whole [d x d] float32 state in MFMA
-// accumulators (wave w holds state columns 16w .. 16w+15) while it walks the
-// block's chunks; per-chunk states are never written to memory.  The next
-// chunk's rows are loaded into registers while the current chunk computes.
-// Blocks of one sequence are chained by element-parallel scans over block
-// summaries:
+// (block, head) and keeps a [d x d] float32 state in MFMA accumulators
+// (wave w holds state columns 16w .. 16w+15) while it walks the block's
+// chunks; per-chunk states are never written to memory.  The next chunk's
+// rows are loaded into registers while the current chunk computes.  Decay
+// factors that weight the rows of a state-update operand are applied to its
+// fragments in registers, so LDS holds only unscaled chunk tiles.  Blocks of
+// one sequence are chained by element-parallel scans over block summaries:
 //
-//   forward   k_fwd_blocksum  state of each block started from zero, and
-//                             its total log-decay Gamma_b;
+//   forward   k_blocksum      side 0: state of each block started from zero
+//                             and its total log-decay Gamma_b;
 //             k_fwd_blockscan S_end[b] = exp(Gamma_b) S_end[b-1] + dS_b,
 //                             which also yields every requested boundary
 //                             state and every final state;
 //             k_fwd_block     outputs of the own rows of each block.
-//   backward  k_bwd_fwdorder  dq (needs S_c, so it walks chunks forward),
-//                             q.dq per row and the block's local adjoint
-//                             U_b = sum_t exp(G_t^blk) scale q_t dO_t^T;
+//   backward  k_blocksum      side 1: the block's local adjoint
+//                             U_b = sum_t exp(G_t^blk) scale q_t dO_t^T
+//                             (with side 0 as well when recomputing);
 //             k_bwd_blockscan dS_end[b] by the reverse recurrence
 //                             dS_start[b] = exp(Gamma_b) dS_end[b] + U_b,
 //                             bank gradients injected at requested block
 //                             ends, dS0 per sequence, boundary terms;
-//             k_bwd_revorder  dk, dv (need dS_{c+1}: chunks backward),
-//                             k.dk per row, local suffix sums of dg;
+//             k_bwd_fwdorder  dq and q.dq per row (needs S_c, so it walks
+//                             chunks forward);
+//             k_bwd_revorder  dv (side 0) and dk, k.dk, local suffix sums of
+//                             dg (side 1); both need dS_{c+1} and walk
+//                             chunks backward;
 //             k_dg_carry      adds to dg the contributions of later blocks.
 // dg uses dg_t = sum_{u >= t} (q_u.dq_u - k_u.dk_u) + <dS_final, S_final>
 //              + sum_{requested P > t} <dbank_P, S_P>   (per sequence),
@@ -75,29 +79,35 @@ __device__ inline void vset<float>(Vec16& v, int e, float x) { v.f[e] = x; }
 template <>
 __device__ inline void vset<bf16>(Vec16& v, int e, bf16 x) { v.b[e] = x; }
 
-// This thread's rows of one chunk (a row's d-range is split over VPR threads).
+// Rows of one chunk: a contiguous run of 64 own rows (fast: physical rows
+// row0 .. row0 + 63, every interior chunk of a sequence) or rows resolved one
+// by one (chunks holding replay rows or padding).  Uniform per workgroup.
+struct ChunkRows {
+  int fast;
+  int row0;
+};
+__device__ inline ChunkRows chunk_rows(const int32_t* seq, int c) {
+  const int p0 = c * CB, n_rep = seq[SEQ_N_REPLAY];
+  ChunkRows cr;
+  cr.fast = p0 >= n_rep && p0 + CB <= seq[SEQ_N_TOK];
+  cr.row0 = seq[SEQ_OWN_ROW] + p0 - n_rep;
+  return cr;
+}
+
+// This thread's rows of one chunk (a row's d-range is split over VPR
+// threads), each as row * 4 + kind; resolved for chunks that are not fast.
 template <typename T, int D>
 struct ChunkRefs {
-  RowRef r[Cfg<T, D>::NV];
+  int rk[Cfg<T, D>::NV];
   __device__ inline void resolve(const int32_t* seq, int c, const int32_t* replay_row, int t) {
     using C = Cfg<T, D>;
 #pragma unroll
-    for (int i = 0; i < C::NV; ++i) r[i] = pos_row(seq, c * CB + (t + i * C::NTHR) / C::VPR, replay_row);
+    for (int i = 0; i < C::NV; ++i) {
+      const RowRef rr = pos_row(seq, c * CB + (t + i * C::NTHR) / C::VPR, replay_row);
+      rk[i] = rr.row * 4 + rr.kind;
+    }
   }
 };
-
-template <typename T, int D>
-__device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkRefs<T, D>& cr,
-                             int H, int h, int t, int min_kind) {
-  using C = Cfg<T, D>;
-#pragma unroll
-  for (int i = 0; i < C::NV; ++i) {
-    const int d0 = ((t + i * C::NTHR) % C::VPR) * C::VE;
-    dst[i].u = cr.r[i].kind >= min_kind
-                   ? *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(cr.r[i].row) * H + h) * D + d0)
-                   : make_uint4(0u, 0u, 0u, 0u);
-  }
-}
 
 // dst[row][d] = src[row][d] (* scale[row] if scale != nullptr)
 template <typename T, int D>
@@ -113,124 +123,190 @@ __device__ inline void put(T* dst, const Vec16* src, const float* scale, int t) 
 #pragma unroll
       for (int e = 0; e < C::VE; ++e) vset<T>(v, e, Elem<T>::from_f(Elem<T>::to_f(vget<T>(v, e)) * s));
     }
-    *reinterpret_cast<uint4*>(dst + row * C::LDR + d0) = v.u;
+    *reinterpret_cast<uint4*>(dst + C::TD::at(row, d0)) = v.u;
   }
 }
 
-// Per-chunk row table and decay prefix sums, shared through LDS.
+// Per-chunk row table, decay prefix sums and two per-row factors, shared
+// through LDS.
 struct ChunkMeta {
+  alignas(16) float G[CB];  // G_t = g_0 + ... + g_t within the chunk
+  alignas(16) float x[CB];  // kernel-specific per-row factors
+  alignas(16) float y[CB];
   int row[CB];
   int kind[CB];
   int rep[CB];
-  float G[CB];
 };
 
-// Wave 0: row table of chunk c and G from the prefetched g (lane = row).
-// Returns G[t] in Gt and G[63] in GL (wave 0 lanes only).
-__device__ inline void meta_setup(ChunkMeta& m, const int32_t* seq, int c, const int32_t* replay_row,
-                                  float gpre, int t, float& Gt, float& GL) {
-  Gt = 0.f;
-  GL = 0.f;
-  if (t < CB) {
-    const RowRef rr = pos_row(seq, c * CB + t, replay_row);
-    m.row[t] = rr.row;
-    m.kind[t] = rr.kind;
-    m.rep[t] = rr.rep;
-    float x = gpre;
-#pragma unroll
-    for (int off = 1; off < CB; off <<= 1) {
-      const float y = __shfl_up(x, off, CB);
-      if (t >= off) x += y;
+// Where this thread's rows of one chunk live, resolved one chunk ahead: the
+// rows it stages (all threads) and, for wave 0, row t of the chunk with its g.
+template <typename T, int D>
+struct ChunkSrc {
+  ChunkRows cr;
+  ChunkRefs<T, D> refs;
+  RowRef mr;
+  float gv;
+  __device__ inline void resolve(const int32_t* seq, int c, const int32_t* replay_row,
+                                 const float* g, int H, int h, int t) {
+    cr = chunk_rows(seq, c);
+    if (!cr.fast) refs.resolve(seq, c, replay_row, t);
+    if (t < CB) {
+      mr = cr.fast ? RowRef{cr.row0 + t, ROW_OWN, -1} : pos_row(seq, c * CB + t, replay_row);
+      gv = mr.kind != ROW_PAD ? g[static_cast<int64_t>(mr.row) * H + h] : 0.f;
     }
-    m.G[t] = x;
-    Gt = x;
-    GL = __shfl(x, CB - 1, CB);
+  }
+};
+
+// This thread's 16-byte pieces of one chunk tile of src (rows of kind below
+// min_kind read as zero).
+template <typename T, int D>
+__device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkSrc<T, D>& cs,
+                             int H, int h, int t, int min_kind) {
+  using C = Cfg<T, D>;
+  if (cs.cr.fast) {
+    const T* base = src + (static_cast<int64_t>(cs.cr.row0) * H + h) * D;
+#pragma unroll
+    for (int i = 0; i < C::NV; ++i) {
+      const int idx = t + i * C::NTHR;
+      dst[i].u = *reinterpret_cast<const uint4*>(base + (idx / C::VPR) * H * D + (idx % C::VPR) * C::VE);
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < C::NV; ++i) {
+    const int d0 = ((t + i * C::NTHR) % C::VPR) * C::VE;
+    const int row = cs.refs.rk[i] >> 2;
+    dst[i].u = (cs.refs.rk[i] & 3) >= min_kind
+                   ? *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(row) * H + h) * D + d0)
+                   : make_uint4(0u, 0u, 0u, 0u);
   }
 }
 
-// Wave 0: g of chunk c (0 for padding).
-__device__ inline float fetch_g(const int32_t* seq, int c, const int32_t* replay_row,
-                                const float* g, int H, int h, int t) {
-  if (t >= CB) return 0.f;
-  const RowRef rr = pos_row(seq, c * CB + t, replay_row);
-  return rr.kind != ROW_PAD ? g[static_cast<int64_t>(rr.row) * H + h] : 0.f;
+// Wave 0 (lane t = row t): publishes the row table and G of the chunk whose
+// sources are in cs; returns G_t and G_last.
+template <typename T, int D>
+__device__ inline void meta_publish(ChunkMeta& m, const ChunkSrc<T, D>& cs, int t, float& Gt,
+                                    float& GL) {
+  m.row[t] = cs.mr.row;
+  m.kind[t] = cs.mr.kind;
+  m.rep[t] = cs.mr.rep;
+  float x = cs.gv;
+#pragma unroll
+  for (int off = 1; off < CB; off <<= 1) {
+    const float y = __shfl_up(x, off, CB);
+    if (t >= off) x += y;
+  }
+  m.G[t] = x;
+  Gt = x;
+  GL = __shfl(x, CB - 1, CB);
 }
 
-// A state held as NT tiles per wave: tile i is rows 16i.., columns 16w.. of
-// a [D x D] matrix (wave w owns one 16-column strip).
-template <int D>
+// A wave's part of a [D x D] state: tile j * NT + i is rows 16 i.., columns
+// 16 (CPW w + j).. of the matrix (or of its transpose).
+template <int D, int CPW>
 __device__ inline void state_load(f32x4* S, const float* src, bool transpose, int w, int lane) {
+  constexpr int NT = D / 16;
 #pragma unroll
-  for (int i = 0; i < D / 16; ++i)
+  for (int j = 0; j < CPW; ++j)
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
+        S[j * NT + i][r] = src ? (transpose ? src[b * D + a] : src[a * D + b]) : 0.f;
+      }
+}
+
+template <int D, int CPW>
+__device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) {
+  constexpr int NT = D / 16;
+#pragma unroll
+  for (int j = 0; j < CPW; ++j)
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        dst[(i * 16 + acc_row(lane, r)) * D + (CPW * w + j) * 16 + acc_col(lane)] = S[j * NT + i][r];
+}
+
+// Masked score tiles of row block it: P[it][jt] = c[jt] * exp(G_m - G_n) * f
+// for n <= m, 0 above the diagonal.
+template <typename T>
+__device__ inline void put_scores(T* P, const f32x4* c, const float* G, float f, int it, int lane) {
+  using TA = Tile<T, CB>;
+#pragma unroll
+  for (int jt = 0; jt < CB / 16; ++jt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int a = i * 16 + acc_row(lane, r), b = w * 16 + acc_col(lane);
-      S[i][r] = src ? (transpose ? src[b * D + a] : src[a * D + b]) : 0.f;
+      const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
+      P[TA::at(m, n)] = Elem<T>::from_f(jt <= it && n <= m ? c[jt][r] * __expf(G[m] - G[n]) * f : 0.f);
     }
 }
 
-template <int D>
-__device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) {
-#pragma unroll
-  for (int i = 0; i < D / 16; ++i)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) dst[(i * 16 + acc_row(lane, r)) * D + w * 16 + acc_col(lane)] = S[i][r];
-}
-
 // ---------------------------------------------------------------------------
-// forward: block summaries (state of the block started from zero)
+// block summaries: one pass over a block's chunks, state started from zero
 // ---------------------------------------------------------------------------
+// side 0 (forward):  dS_b = sum over the block of the chunk recurrence
+//                    S <- exp(G_last) S + K^T diag(exp(G_last - G)) V, and
+//                    Gamma_b = total log-decay of the block;
+// side 1 (adjoint):  U_b = sum_t exp(G_t^blk) scale q_t dO_t^T, G_t^blk the
+//                    inclusive log-decay from the block start to row t.
+// blockIdx.z selects the side (side0 + z).
 template <typename T, int D>
-__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_fwd_blocksum(
+__global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksum(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ replay_row, int H, const T* __restrict__ k,
-    const T* __restrict__ v, const float* __restrict__ g, float* __restrict__ dSb,
-    float* __restrict__ gam) {
+    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dO,
+    const float* __restrict__ g, float* __restrict__ dSb, float* __restrict__ U,
+    float* __restrict__ gam, int side0) {
   using C = Cfg<T, D>;
-  __shared__ T Ks[CB * C::LDR];  // K * exp(G_last - G)
-  __shared__ T Vs[CB * C::LDR];
+  __shared__ T Xs[Tile<T, D>::SIZE];
+  __shared__ T Ys[Tile<T, D>::SIZE];
   __shared__ ChunkMeta meta;
-  __shared__ float sk[CB];
+  const int side = side0 + static_cast<int>(blockIdx.z);
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int32_t* seq = seq_tab + bk[BLK_SEQ] * SEQ_WORDS;
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
-  f32x4 S[C::NT];
+  const T* X = side ? q : k;
+  const T* Y = side ? dO : v;
+  const int min_kind = side ? ROW_OWN : ROW_REPLAY;
+  f32x4 S[C::CPW * C::NT];
 #pragma unroll
-  for (int i = 0; i < C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  ChunkRefs<T, D> refs;
-  Vec16 pk[C::NV], pv[C::NV];
-  refs.resolve(seq, c0, replay_row, t);
-  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-  float gp = fetch_g(seq, c0, replay_row, g, H, h, t);
-  float gsum = 0.f;
+  for (int i = 0; i < C::CPW * C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ChunkSrc<T, D> cs;
+  Vec16 px[C::NV], py[C::NV];
+  cs.resolve(seq, c0, replay_row, g, H, h, t);
+  fetch<T, D>(px, X, cs, H, h, t, min_kind);
+  fetch<T, D>(py, Y, cs, H, h, t, min_kind);
+  float Gs = 0.f;  // log-decay from the block start to the current chunk start
   for (int c = c0; c < c_end; ++c) {
-    float Gt, GLw;
-    meta_setup(meta, seq, c, replay_row, gp, t, Gt, GLw);
-    if (t < CB) sk[t] = __expf(GLw - Gt);
+    if (t < CB) {
+      float Gt, GLw;
+      meta_publish(meta, cs, t, Gt, GLw);
+      meta.x[t] = side ? __expf(Gs + Gt) * scale : __expf(GLw - Gt);
+    }
+    put<T, D>(Xs, px, nullptr, t);
+    put<T, D>(Ys, py, nullptr, t);
     __syncthreads();
     const float GL = meta.G[CB - 1];
-    put<T, D>(Ks, pk, sk, t);
-    put<T, D>(Vs, pv, nullptr, t);
-    __syncthreads();
     if (c + 1 < c_end) {
-      refs.resolve(seq, c + 1, replay_row, t);
-      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-      gp = fetch_g(seq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(seq, c + 1, replay_row, g, H, h, t);
+      fetch<T, D>(px, X, cs, H, h, t, min_kind);
+      fetch<T, D>(py, Y, cs, H, h, t, min_kind);
     }
-    const float dec = __expf(GL);
+    if (!side) {
+      const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < C::NT; ++i) {
-      S[i] *= dec;
-      tile<T, true, true>(S[i], Ks + i * 16, C::LDR, Vs + w * 16, C::LDR, CB, lane);
+      for (int i = 0; i < C::CPW * C::NT; ++i) S[i] *= dec;
     }
-    gsum += GL;
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, Xs, Ys, C::CPW * w * 16, meta.x, lane);
+    Gs += GL;
     __syncthreads();
   }
-  state_store<D>(dSb + (static_cast<int64_t>(b) * H + h) * D * D, S, w, lane);
-  if (t == 0) gam[static_cast<int64_t>(b) * H + h] = gsum;
+  const int64_t bi = static_cast<int64_t>(b) * H + h;
+  state_store<D, C::CPW>((side ? U : dSb) + bi * D * D, S, w, lane);
+  if (!side && t == 0) gam[bi] = Gs;
 }
 
 // ---------------------------------------------------------------------------
@@ -333,223 +409,224 @@ __global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 struct FwdSmem {
-  using C = Cfg<T, D>;
-  T Q[CB * C::LDR];
-  T K[CB * C::LDR];
-  T Ks[CB * C::LDR];  // K * exp(G_last - G)
-  T V[CB * C::LDR];
-  T A[CB * C::LDA];   // masked Q K^T
-  ChunkMeta meta;
-  float sk[CB];       // exp(G_last - G)
-  float eg[CB];       // exp(G)
+  T Q[Tile<T, D>::SIZE];
+  T K[Tile<T, D>::SIZE];
+  T V[Tile<T, D>::SIZE];
+  T A[Tile<T, CB>::SIZE];    // masked Q K^T
+  ChunkMeta meta;  // x = exp(G_last - G), y = exp(G)
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_fwd_block(
+__global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_block(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ S0, const float* __restrict__ S_end, T* __restrict__ o) {
   using C = Cfg<T, D>;
+  using RB = RegB<T>;
+  constexpr int NS = C::CPW * C::NT;
   __shared__ FwdSmem<T, D> sm;
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const int64_t DD = static_cast<int64_t>(D) * D;
-  f32x4 S[C::NT];  // S : tile i = rows (dk) 16i.., columns (dv) 16w..
-  state_load<D>(S, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
-                                    : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                false, w, lane);
-  ChunkRefs<T, D> refs;
+  f32x4 S[NS];  // S : rows (dk), columns (dv) of the wave's strips
+  state_load<D, C::CPW>(S, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                            : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                        false, w, lane);
+  ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV];
-  refs.resolve(seq, c0, replay_row, t);
-  fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
-  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-  float gp = fetch_g(seq, c0, replay_row, g, H, h, t);
+  cs.resolve(seq, c0, replay_row, g, H, h, t);
+  fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
+  fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
   for (int c = c0; c < c_end; ++c) {
-    float Gt, GLw;
-    meta_setup(sm.meta, seq, c, replay_row, gp, t, Gt, GLw);
     if (t < CB) {
-      sm.sk[t] = __expf(GLw - Gt);
-      sm.eg[t] = __expf(Gt);
+      float Gt, GLw;
+      meta_publish(sm.meta, cs, t, Gt, GLw);
+      sm.meta.x[t] = __expf(GLw - Gt);
+      sm.meta.y[t] = __expf(Gt);
     }
-    __syncthreads();
-    const float GL = sm.meta.G[CB - 1];
+    const ChunkRows cur = cs.cr;
     put<T, D>(sm.Q, pq, nullptr, t);
     put<T, D>(sm.K, pk, nullptr, t);
-    put<T, D>(sm.Ks, pk, sm.sk, t);
     put<T, D>(sm.V, pv, nullptr, t);
     __syncthreads();
+    const float GL = sm.meta.G[CB - 1];
     if (c + 1 < c_end) {
-      refs.resolve(seq, c + 1, replay_row, t);
-      fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
-      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-      gp = fetch_g(seq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(seq, c + 1, replay_row, g, H, h, t);
+      fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
+      fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     }
-    // A = (Q K^T) * exp(G_i - G_j) [j <= i]
+    // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
+    {
+      f32x4 a[CB / 16];
 #pragma unroll
-    for (int x = w * C::ATPW; x < (w + 1) * C::ATPW; ++x) {
-      const int it = x >> 2, jt = x & 3;
-      f32x4 a = {0.f, 0.f, 0.f, 0.f};
-      tile<T, false, false>(a, sm.Q + it * 16 * C::LDR, C::LDR, sm.K + jt * 16 * C::LDR, C::LDR, D, lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-        sm.A[m * C::LDA + n] =
-            Elem<T>::from_f(n <= m ? a[r] * __expf(sm.meta.G[m] - sm.meta.G[n]) : 0.f);
-      }
+      for (int jt = 0; jt < CB / 16; ++jt) a[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      score_row<T, typename C::TD, typename C::TD>(a, sm.Q, sm.K, w, D, lane);
+      put_scores<T>(sm.A, a, sm.meta.G, 1.f, w, lane);
     }
     __syncthreads();
-    // O[:, 16w..] = scale * (diag(exp(G)) Q S_c + A V)
-#pragma unroll
+    // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V)
+#pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      f32x4 acc[C::CPW];
 #pragma unroll
-      for (int kt = 0; kt < C::NT; ++kt)
-        MmaRegB<T>::step(acc, sm.Q + it * 16 * C::LDR + kt * 16, C::LDR, S[kt], lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
-      tile<T, false, true>(acc, sm.A + it * 16 * C::LDA, C::LDA, sm.V + w * 16, C::LDR, CB, lane);
+      for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      opaque_state<NS>(S);
+      regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, sm.Q, it * 16, S, lane);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = it * 16 + acc_row(lane, r);
-        if (sm.meta.kind[m] == ROW_OWN)
-          o[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + w * 16 + acc_col(lane)] =
-              Elem<T>::from_f(acc[r] * scale);
+        const float e = sm.meta.y[it * 16 + acc_row(lane, r)];
+#pragma unroll
+        for (int j = 0; j < C::CPW; ++j) acc[j][r] *= e;
+      }
+      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW>(acc, sm.A, it * 16, sm.V, col0, 0,
+                                                                 (it + 1) * 16, lane);
+      if (cur.fast) {
+        T* dst = o + (static_cast<int64_t>(cur.row0) * H + h) * D + col0 + acc_col(lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j)
+            dst[(it * 16 + acc_row(lane, r)) * H * D + 16 * j] = Elem<T>::from_f(acc[j][r] * scale);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = it * 16 + acc_row(lane, r);
+          if (sm.meta.kind[m] == ROW_OWN) {
+            T* dst = o + (static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + col0 + acc_col(lane);
+#pragma unroll
+            for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r] * scale);
+          }
+        }
       }
     }
-    // S_{c+1} = exp(G_last) S_c + (K * exp(G_last - G))^T V
+    // S_{c+1} = exp(G_last) S_c + K^T diag(exp(G_last - G)) V
     const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < C::NT; ++i) {
-      S[i] *= dec;
-      tile<T, true, true>(S[i], sm.Ks + i * 16, C::LDR, sm.V + w * 16, C::LDR, CB, lane);
-    }
+    for (int i = 0; i < NS; ++i) S[i] *= dec;
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, sm.K, sm.V, col0, sm.meta.x, lane);
     __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// backward, forward order: dq, q.dq per row and the block's local adjoint
+// backward, forward order: dq and q.dq per row (needs S_c: chunks forward)
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 struct BfSmem {
   using C = Cfg<T, D>;
-  T dO[CB * C::LDR];
-  T V[CB * C::LDR];
-  T K[CB * C::LDR];
-  T Q[CB * C::LDR];   // own rows
-  T Qh[CB * C::LDR];  // Q * exp(G_blk) * scale, G_blk counted from the block start
-  T Vs[CB * C::LDR];  // V * exp(G_last - G)
-  T dA[CB * C::LDA];  // scale * (dO V^T) masked
-  ChunkMeta meta;
-  float sv[CB];       // exp(G_last - G)
-  float eg[CB];       // exp(G) * scale
-  float su[CB];       // exp(G_blk) * scale
+  T dO[Tile<T, D>::SIZE];
+  T V[Tile<T, D>::SIZE];
+  T K[Tile<T, D>::SIZE];
+  T Q[Tile<T, D>::SIZE];     // own rows
+  T dA[Tile<T, CB>::SIZE];   // scale * (dO V^T) masked
+  ChunkMeta meta;  // x = exp(G_last - G), y = exp(G) * scale
   float rq[C::NW][CB];
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_bwd_fwdorder(
+__global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwdorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const T* __restrict__ dO, const float* __restrict__ S0, const float* __restrict__ S_end,
-    T* __restrict__ dq, float* __restrict__ rq_out, float* __restrict__ U_out) {
+    T* __restrict__ dq, float* __restrict__ rq_out) {
   using C = Cfg<T, D>;
+  using RB = RegB<T>;
+  constexpr int NS = C::CPW * C::NT;
   __shared__ BfSmem<T, D> sm;
   const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const int64_t DD = static_cast<int64_t>(D) * D;
-  f32x4 St[C::NT];  // S^T : tile i = rows (dv) 16i.., columns (dk) 16w..
-  f32x4 U[C::NT];   // U   : tile i = rows (dk) 16i.., columns (dv) 16w..
-  state_load<D>(St, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
-                                     : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                true, w, lane);
-#pragma unroll
-  for (int i = 0; i < C::NT; ++i) U[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  ChunkRefs<T, D> refs;
+  f32x4 St[NS];  // S^T : rows (dv), columns (dk) of the wave's strips
+  state_load<D, C::CPW>(St, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                             : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                        true, w, lane);
+  ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  refs.resolve(seq, c0, replay_row, t);
-  fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
-  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
-  float gp = fetch_g(seq, c0, replay_row, g, H, h, t);
-  float Gs = 0.f;  // log-decay from the block start to the current chunk start
+  cs.resolve(seq, c0, replay_row, g, H, h, t);
+  fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
+  fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
   for (int c = c0; c < c_end; ++c) {
-    float Gt, GLw;
-    meta_setup(sm.meta, seq, c, replay_row, gp, t, Gt, GLw);
     if (t < CB) {
-      sm.sv[t] = __expf(GLw - Gt);
-      sm.eg[t] = __expf(Gt) * scale;
-      sm.su[t] = __expf(Gs + Gt) * scale;
+      float Gt, GLw;
+      meta_publish(sm.meta, cs, t, Gt, GLw);
+      sm.meta.x[t] = __expf(GLw - Gt);
+      sm.meta.y[t] = __expf(Gt) * scale;
     }
-    __syncthreads();
-    const float GL = sm.meta.G[CB - 1];
+    const ChunkRows cur = cs.cr;
     put<T, D>(sm.dO, pd, nullptr, t);
     put<T, D>(sm.V, pv, nullptr, t);
     put<T, D>(sm.K, pk, nullptr, t);
     put<T, D>(sm.Q, pq, nullptr, t);
-    put<T, D>(sm.Qh, pq, sm.su, t);
-    put<T, D>(sm.Vs, pv, sm.sv, t);
     __syncthreads();
+    const float GL = sm.meta.G[CB - 1];
     if (c + 1 < c_end) {
-      refs.resolve(seq, c + 1, replay_row, t);
-      fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
-      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
-      gp = fetch_g(seq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(seq, c + 1, replay_row, g, H, h, t);
+      fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
+      fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
     }
-    // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]
+    // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
+    {
+      f32x4 a[CB / 16];
 #pragma unroll
-    for (int x = w * C::ATPW; x < (w + 1) * C::ATPW; ++x) {
-      const int it = x >> 2, jt = x & 3;
-      f32x4 a = {0.f, 0.f, 0.f, 0.f};
-      tile<T, false, false>(a, sm.dO + it * 16 * C::LDR, C::LDR, sm.V + jt * 16 * C::LDR, C::LDR, D, lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-        sm.dA[m * C::LDA + n] =
-            Elem<T>::from_f(n <= m ? a[r] * __expf(sm.meta.G[m] - sm.meta.G[n]) * scale : 0.f);
-      }
+      for (int jt = 0; jt < CB / 16; ++jt) a[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      score_row<T, typename C::TD, typename C::TD>(a, sm.dO, sm.V, w, D, lane);
+      put_scores<T>(sm.dA, a, sm.meta.G, scale, w, lane);
     }
     __syncthreads();
-    // dq[:, 16w..] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
-#pragma unroll
+    // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
+#pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      f32x4 acc[C::CPW];
 #pragma unroll
-      for (int kt = 0; kt < C::NT; ++kt)
-        MmaRegB<T>::step(acc, sm.dO + it * 16 * C::LDR + kt * 16, C::LDR, St[kt], lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] *= sm.eg[it * 16 + acc_row(lane, r)];
-      tile<T, false, true>(acc, sm.dA + it * 16 * C::LDA, C::LDA, sm.K + w * 16, C::LDR, CB, lane);
+      for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      opaque_state<NS>(St);
+      regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, sm.dO, it * 16, St, lane);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = it * 16 + acc_row(lane, r), n = w * 16 + acc_col(lane);
-        const float s = sum16(Elem<T>::to_f(sm.Q[m * C::LDR + n]) * acc[r]);
+        const float e = sm.meta.y[it * 16 + acc_row(lane, r)];
+#pragma unroll
+        for (int j = 0; j < C::CPW; ++j) acc[j][r] *= e;
+      }
+      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW>(acc, sm.dA, it * 16, sm.K, col0, 0,
+                                                                 (it + 1) * 16, lane);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = it * 16 + acc_row(lane, r);
+        float x = 0.f;
+#pragma unroll
+        for (int j = 0; j < C::CPW; ++j)
+          x += Elem<T>::to_f(sm.Q[C::TD::at(m, col0 + 16 * j + acc_col(lane))]) * acc[j][r];
+        const float s = sum16(x);
         if ((lane & 15) == 0) sm.rq[w][m] = s;
-        if (sm.meta.kind[m] == ROW_OWN)
-          dq[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
+        if (cur.fast || sm.meta.kind[m] == ROW_OWN) {
+          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : sm.meta.row[m];
+          T* dst = dq + (row * H + h) * D + col0 + acc_col(lane);
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r]);
+        }
       }
     }
-    // U += (Q * exp(G_blk) * scale)^T dO ; S^T <- exp(G_last) S^T + (V * exp(G_last - G))^T K
+    // S^T <- exp(G_last) S^T + V^T diag(exp(G_last - G)) K
     const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < C::NT; ++i) {
-      tile<T, true, true>(U[i], sm.Qh + i * 16, C::LDR, sm.dO + w * 16, C::LDR, CB, lane);
-      St[i] *= dec;
-      tile<T, true, true>(St[i], sm.Vs + i * 16, C::LDR, sm.K + w * 16, C::LDR, CB, lane);
-    }
+    for (int i = 0; i < NS; ++i) St[i] *= dec;
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(St, sm.V, sm.K, col0, sm.meta.x, lane);
     __syncthreads();
     if (t < CB) {
       float s = 0.f;
@@ -557,163 +634,168 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_bwd_fwdorder(
       for (int i = 0; i < C::NW; ++i) s += sm.rq[i][t];
       rq_out[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] = s;
     }
-    Gs += GL;
   }
-  state_store<D>(U_out + (static_cast<int64_t>(b) * H + h) * DD, U, w, lane);
 }
 
 // ---------------------------------------------------------------------------
-// backward, reverse order: dk, dv, k.dk and local suffix sums of dg
+// backward, reverse order (needs dS_{c+1}: chunks backward).  Each (block,
+// head) runs as two workgroups that share the chunk rows through the caches:
+//   side 0: dv = diag(exp(G_last - G)) K dS + scale A^T dO, holding dS;
+//   side 1: dk = diag(exp(G_last - G)) V dS^T + dA^T Q, holding dS^T, plus
+//           k.dk per row and the local suffix sums of dg.
+// Both sides run the adjoint recurrence
+//   dS_c = exp(G_last) dS_{c+1} + Q^T diag(exp(G) scale) dO
+// in their own layout.  Workgroup ids are grouped by 16: ids 16j..16j+7 are
+// side 0 of pairs 8j..8j+7 and ids 16j+8..16j+15 their side 1, so the two
+// sides of a pair are dispatched together (and land on the same XCD when
+// dispatch is round-robin over eight XCDs).
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 struct BrSmem {
   using C = Cfg<T, D>;
-  T Q[CB * C::LDR];   // own rows
-  T K[CB * C::LDR];
-  T V[CB * C::LDR];
-  T dO[CB * C::LDR];  // own rows
-  T Qs[CB * C::LDR];  // Q * exp(G) * scale
-  T A[CB * C::LDA];   // masked Q K^T
-  T dA[CB * C::LDA];  // scale * (dO V^T) masked
-  ChunkMeta meta;
-  float sk[CB];       // exp(G_last - G)
-  float eg[CB];       // exp(G) * scale
+  T Q[Tile<T, D>::SIZE];     // own rows
+  T K[Tile<T, D>::SIZE];
+  T V[Tile<T, D>::SIZE];     // side 1 only
+  T dO[Tile<T, D>::SIZE];    // own rows
+  T P[Tile<T, CB>::SIZE];    // side 0: A = Q K^T masked; side 1: dA = scale (dO V^T) masked
+  ChunkMeta meta;  // x = exp(G_last - G), y = exp(G) * scale
   float rk[C::NW][CB];
 };
 
-template <typename T, int D>
-__global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_bwd_revorder(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
-    const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const T* __restrict__ dO, const float* __restrict__ dS_end, const float* __restrict__ rq,
-    T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dg, float* __restrict__ rep_grad,
-    float* __restrict__ Rb) {
+template <typename T, int D, int SIDE>
+__device__ __forceinline__ void bwd_revorder_side(
+    BrSmem<T, D>& sm, int pair, const int32_t* __restrict__ seq_tab,
+    const int32_t* __restrict__ blk_tab, const int32_t* __restrict__ replay_row, int H, float scale,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
+    const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
+    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb) {
   using C = Cfg<T, D>;
+  constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
-  __shared__ BrSmem<T, D> sm;
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  constexpr bool side = SIDE == 1;
+  const int b = pair / H, h = pair % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
-  const float* dse = dS_end + (static_cast<int64_t>(b) * H + h) * DD;
-  f32x4 dSt[C::NT];  // dS^T : tile i = rows (dv) 16i.., columns (dk) 16w..
-  f32x4 dSn[C::NT];  // dS   : tile i = rows (dk) 16i.., columns (dv) 16w..
-  state_load<D>(dSt, dse, true, w, lane);
-  state_load<D>(dSn, dse, false, w, lane);
-  const float inv_scale = 1.f / scale;
-  float carry = 0.f;  // sum of (q.dq - k.dk) over the later chunks of the block
-  ChunkRefs<T, D> refs;
+  // side 0: dS   rows (dk), columns (dv) of the wave's strips
+  // side 1: dS^T rows (dv), columns (dk) of the wave's strips
+  f32x4 dS[NS];
+  state_load<D, C::CPW>(dS, dS_end + (static_cast<int64_t>(b) * H + h) * DD, side == 1, w, lane);
+  float carry = 0.f;  // side 1: sum of (q.dq - k.dk) over the later chunks of the block
+  ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  refs.resolve(seq, c_last, replay_row, t);
-  fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
-  fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
-  float gp = fetch_g(seq, c_last, replay_row, g, H, h, t);
+  cs.resolve(seq, c_last, replay_row, g, H, h, t);
+  fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
+  fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+  if (side) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
+  // side 1, wave 0: q.dq of row t of the chunk, one chunk ahead
+  const float* rq_h = rq + (static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) * CB + t) * H + h;
+  float rq_next = side && t < CB ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
   for (int c = c_last; c >= c0; --c) {
-    float Gt, GLw;
-    meta_setup(sm.meta, seq, c, replay_row, gp, t, Gt, GLw);
     if (t < CB) {
-      sm.sk[t] = __expf(GLw - Gt);
-      sm.eg[t] = __expf(Gt) * scale;
+      float Gt, GLw;
+      meta_publish(sm.meta, cs, t, Gt, GLw);
+      sm.meta.x[t] = __expf(GLw - Gt);
+      sm.meta.y[t] = __expf(Gt) * scale;
     }
-    __syncthreads();
-    const float GL = sm.meta.G[CB - 1];
+    const ChunkRows cur = cs.cr;
+    const float rq_cur = rq_next;
     put<T, D>(sm.Q, pq, nullptr, t);
     put<T, D>(sm.K, pk, nullptr, t);
-    put<T, D>(sm.V, pv, nullptr, t);
+    if (side) put<T, D>(sm.V, pv, nullptr, t);
     put<T, D>(sm.dO, pd, nullptr, t);
-    put<T, D>(sm.Qs, pq, sm.eg, t);
     __syncthreads();
+    const float GL = sm.meta.G[CB - 1];
     if (c > c0) {
-      refs.resolve(seq, c - 1, replay_row, t);
-      fetch<T, D>(pq, q, refs, H, h, t, ROW_OWN);
-      fetch<T, D>(pk, k, refs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pv, v, refs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pd, dO, refs, H, h, t, ROW_OWN);
-      gp = fetch_g(seq, c - 1, replay_row, g, H, h, t);
+      cs.resolve(seq, c - 1, replay_row, g, H, h, t);
+      fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
+      fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+      if (side) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
+      if (side && t < CB) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
     }
-    // A and dA, masked
+    // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
+    // M = exp(G_i - G_j) [j <= i]; wave w computes row block w
+    {
+      f32x4 a[CB / 16];
 #pragma unroll
-    for (int x = w * C::ATPW; x < (w + 1) * C::ATPW; ++x) {
-      const int it = x >> 2, jt = x & 3;
-      f32x4 a = {0.f, 0.f, 0.f, 0.f}, da = {0.f, 0.f, 0.f, 0.f};
-      tile<T, false, false>(a, sm.Q + it * 16 * C::LDR, C::LDR, sm.K + jt * 16 * C::LDR, C::LDR, D, lane);
-      tile<T, false, false>(da, sm.dO + it * 16 * C::LDR, C::LDR, sm.V + jt * 16 * C::LDR, C::LDR, D, lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-        const float dm = n <= m ? __expf(sm.meta.G[m] - sm.meta.G[n]) : 0.f;
-        sm.A[m * C::LDA + n] = Elem<T>::from_f(a[r] * dm);
-        sm.dA[m * C::LDA + n] = Elem<T>::from_f(da[r] * dm * scale);
-      }
+      for (int jt = 0; jt < CB / 16; ++jt) a[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (side) score_row<T, typename C::TD, typename C::TD>(a, sm.dO, sm.V, w, D, lane);
+      else score_row<T, typename C::TD, typename C::TD>(a, sm.Q, sm.K, w, D, lane);
+      put_scores<T>(sm.P, a, sm.meta.G, side ? scale : 1.f, w, lane);
     }
     __syncthreads();
-    // dk[:, 16w..] = diag(exp(G_last - G)) V dS^T + dA^T Q ; partial k.dk
-#pragma unroll
+#pragma unroll 1
     for (int jt = 0; jt < CB / 16; ++jt) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      // side 0: acc = diag(x) K dS + scale A^T dO ; side 1: acc = diag(x) V dS^T + dA^T Q
+      // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
+      f32x4 acc[C::CPW], ad[C::CPW];
 #pragma unroll
-      for (int kt = 0; kt < C::NT; ++kt)
-        MmaRegB<T>::step(acc, sm.V + jt * 16 * C::LDR + kt * 16, C::LDR, dSt[kt], lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)];
-      tile<T, true, true>(acc, sm.dA + jt * 16, C::LDA, sm.Q + w * 16, C::LDR, CB, lane);
+      for (int j = 0; j < C::CPW; ++j) {
+        acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+      opaque_state<NS>(dS);
+      regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, side ? sm.V : sm.K, jt * 16, dS, lane);
+      const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
+      tile_cols<T, typename C::TA, true, typename C::TD, C::CPW>(ad, sm.P, jt * 16, side ? sm.Q : sm.dO,
+                                                                col0, k0, CB, lane);
+      const float f = side ? 1.f : scale;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = jt * 16 + acc_row(lane, r), n = w * 16 + acc_col(lane);
-        const float s = sum16(Elem<T>::to_f(sm.K[m * C::LDR + n]) * acc[r]);
-        if ((lane & 15) == 0) sm.rk[w][m] = s;
-        const int kind = sm.meta.kind[m];
-        if (kind == ROW_OWN)
-          dk[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + n] = Elem<T>::from_f(acc[r]);
-        else if (kind == ROW_REPLAY)
-          rep_grad[(static_cast<int64_t>(sm.meta.rep[m]) * H + h) * RG + n] = acc[r];
+        const float e = sm.meta.x[jt * 16 + acc_row(lane, r)];
+#pragma unroll
+        for (int j = 0; j < C::CPW; ++j) acc[j][r] = acc[j][r] * e + f * ad[j][r];
       }
-    }
-    // dv[:, 16w..] = diag(exp(G_last - G)) K dS + scale A^T dO
-#pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kt = 0; kt < C::NT; ++kt)
-        MmaRegB<T>::step(acc, sm.K + jt * 16 * C::LDR + kt * 16, C::LDR, dSn[kt], lane);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[r] *= sm.sk[jt * 16 + acc_row(lane, r)] * inv_scale;
-      tile<T, true, true>(acc, sm.A + jt * 16, C::LDA, sm.dO + w * 16, C::LDR, CB, lane);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = jt * 16 + acc_row(lane, r), n = w * 16 + acc_col(lane);
-        const float val = acc[r] * scale;
-        const int kind = sm.meta.kind[m];
-        if (kind == ROW_OWN)
-          dv[(static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + n] = Elem<T>::from_f(val);
-        else if (kind == ROW_REPLAY)
-          rep_grad[(static_cast<int64_t>(sm.meta.rep[m]) * H + h) * RG + D + n] = val;
+        const int m = jt * 16 + acc_row(lane, r);
+        const int kind = cur.fast ? static_cast<int>(ROW_OWN) : sm.meta.kind[m];
+        if (side) {
+          float x = 0.f;
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j)
+            x += Elem<T>::to_f(sm.K[C::TD::at(m, col0 + 16 * j + acc_col(lane))]) * acc[j][r];
+          const float s = sum16(x);
+          if ((lane & 15) == 0) sm.rk[w][m] = s;
+        }
+        if (cur.fast || kind == ROW_OWN) {
+          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : sm.meta.row[m];
+          T* dst = (side ? dk : dv) + (row * H + h) * D + col0 + acc_col(lane);
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r]);
+        } else if (kind == ROW_REPLAY) {
+          float* dst = rep_grad + (static_cast<int64_t>(sm.meta.rep[m]) * H + h) * RG + (side ? 0 : D) +
+                       col0 + acc_col(lane);
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j) dst[16 * j] = acc[j][r];
+        }
       }
     }
-    // dS_c = exp(G_last) dS_{c+1} + (Q * exp(G) * scale)^T dO, in both layouts
+    // side 0: dS   <- exp(G_last) dS   + Q^T  diag(exp(G) scale) dO
+    // side 1: dS^T <- exp(G_last) dS^T + dO^T diag(exp(G) scale) Q
     const float dec = __expf(GL);
 #pragma unroll
-    for (int i = 0; i < C::NT; ++i) {
-      dSn[i] *= dec;
-      tile<T, true, true>(dSn[i], sm.Qs + i * 16, C::LDR, sm.dO + w * 16, C::LDR, CB, lane);
-      dSt[i] *= dec;
-      tile<T, true, true>(dSt[i], sm.dO + i * 16, C::LDR, sm.Qs + w * 16, C::LDR, CB, lane);
-    }
+    for (int i = 0; i < NS; ++i) dS[i] *= dec;
+    if (!side)
+      state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(dS, sm.Q, sm.dO, col0, sm.meta.y, lane);
+    else
+      state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(dS, sm.dO, sm.Q, col0, sm.meta.y, lane);
     __syncthreads();
-    // local suffix sums of q.dq - k.dk (wave 0, one row per lane)
-    if (t < CB) {
+    // side 1, wave 0: local suffix sums of q.dq - k.dk, one row per lane
+    if (side && t < CB) {
       const int kind = sm.meta.kind[t];
       float x = 0.f;
       if (kind != ROW_PAD) {
         float rks = 0.f;
 #pragma unroll
         for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][t];
-        x = rq[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] - rks;
+        x = rq_cur - rks;
       }
 #pragma unroll
       for (int off = 1; off < CB; off <<= 1) {
@@ -727,7 +809,28 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR)) void k_bwd_revorder(
       carry += __shfl(x, 0, CB);
     }
   }
-  if (t == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
+  if (side && t == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
+}
+
+
+template <typename T, int D>
+__global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_revorder(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ replay_row, int H, int n_pairs, float scale,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
+    const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
+    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb) {
+  __shared__ BrSmem<T, D> sm;
+  const int id = blockIdx.x;
+  const int pair = (id >> 4) * 8 + (id & 7);
+  if (pair >= n_pairs) return;  // whole workgroup, before any barrier
+  if ((id >> 3) & 1)
+    bwd_revorder_side<T, D, 1>(sm, pair, seq_tab, blk_tab, replay_row, H, scale, q, k, v, g, dO,
+                               dS_end, rq, dk, dv, dg, rep_grad, Rb);
+  else
+    bwd_revorder_side<T, D, 0>(sm, pair, seq_tab, blk_tab, replay_row, H, scale, q, k, v, g, dO,
+                               dS_end, rq, dk, dv, dg, rep_grad, Rb);
 }
 
 // ---------------------------------------------------------------------------
@@ -930,25 +1033,30 @@ Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   return Blob{b + L.seq_tab, b + L.blk_tab, b + p->off_replay_row};
 }
 
-// forward state pass: block summaries then the block chain
+// Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b).
 template <typename T, int D>
-int launch_state_pass(const harts_plan_t* p, int32_t round, const Blob& B, int H, const void* k,
-                      const void* v, const float* g, const float* S0, float* dSb, float* gam,
-                      float* S_end, float* bank, float* S_final, hipStream_t s) {
+int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, float scale,
+                    const void* q, const void* k, const void* v, const void* dO, const float* g,
+                    float* dSb, float* U, float* gam, int side0, int n_sides, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
-  {
-    ProfScope ps("k_fwd_blocksum", s);
-    hipLaunchKernelGGL((k_fwd_blocksum<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.replay_row, H, static_cast<const T*>(k),
-                       static_cast<const T*>(v), g, dSb, gam);
-  }
-  if (int rc = hip_check("k_fwd_blocksum")) return rc;
-  {
-    constexpr int NSW = D * D / 4 / SCAN_THR;
-    ProfScope ps("k_fwd_blockscan", s);
-    hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
-                       B.seq_tab, B.blk_tab, H, S0, dSb, gam, S_end, bank, S_final);
-  }
+  ProfScope ps("k_blocksum", s);
+  hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk, H, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
+                     B.seq_tab, B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                     static_cast<const T*>(k), static_cast<const T*>(v),
+                     static_cast<const T*>(dO), g, dSb, U, gam, side0);
+  return hip_check("k_blocksum");
+}
+
+// Chain of block summaries: S_end per block, requested boundary states, final states.
+template <int D>
+int launch_fwd_scan(const harts_plan_t* p, int32_t round, const Blob& B, int H, const float* S0,
+                    const float* dSb, const float* gam, float* S_end, float* bank, float* S_final,
+                    hipStream_t s) {
+  const RoundLayout& L = p->rounds[round];
+  constexpr int NSW = D * D / 4 / SCAN_THR;
+  ProfScope ps("k_fwd_blockscan", s);
+  hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
+                     B.seq_tab, B.blk_tab, H, S0, dSb, gam, S_end, bank, S_final);
   return hip_check("k_fwd_blockscan");
 }
 
@@ -962,9 +1070,10 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   float* dSb = reinterpret_cast<float*>(ws);
   float* S_end = reinterpret_cast<float*>(saved);
   float* gam = reinterpret_cast<float*>(saved + z.blk_state);
-  if (int rc = launch_state_pass<T, D>(p, round, B, H, k, v, g, S0, dSb, gam, S_end, bank,
-                                        S_final, s))
+  if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, nullptr, g, dSb, nullptr,
+                                      gam, 0, 1, s))
     return rc;
+  if (int rc = launch_fwd_scan<D>(p, round, B, H, S0, dSb, gam, S_end, bank, S_final, s)) return rc;
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
   {
     ProfScope ps("k_fwd_block", s);
@@ -996,25 +1105,24 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   w += z.rb;
   float* betap = reinterpret_cast<float*>(w);
   w += z.betap;
-  if (!saved) {  // recompute-forward: block summaries and chain from S0
+  if (!saved) {
+    // recompute-forward: forward summaries (chained from S0 below) and the
+    // adjoint summaries in one launch
     float* dSb = reinterpret_cast<float*>(w);
     char* sv = w + z.blk_state;
-    if (int rc = launch_state_pass<T, D>(p, round, B, H, k, v, g, S0, dSb,
-                                          reinterpret_cast<float*>(sv + z.blk_state),
-                                          reinterpret_cast<float*>(sv), nullptr, nullptr, s))
+    float* S_end_w = reinterpret_cast<float*>(sv);
+    float* gam_w = reinterpret_cast<float*>(sv + z.blk_state);
+    if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, dSb, U, gam_w, 0, 2, s))
+      return rc;
+    if (int rc = launch_fwd_scan<D>(p, round, B, H, S0, dSb, gam_w, S_end_w, nullptr, nullptr, s))
       return rc;
     saved = sv;
+  } else if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, nullptr, U,
+                                             nullptr, 1, 1, s)) {
+    return rc;
   }
   const float* S_end = reinterpret_cast<const float*>(saved);
   const float* gam = reinterpret_cast<const float*>(saved + z.blk_state);
-  {
-    ProfScope ps("k_bwd_fwdorder", s);
-    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
-                       static_cast<const T*>(k), static_cast<const T*>(v), g,
-                       static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq, U);
-  }
-  if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
     constexpr int NSW = D * D / 4 / SCAN_THR;
     ProfScope ps("k_bwd_blockscan", s);
@@ -1024,9 +1132,19 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   }
   if (int rc = hip_check("k_bwd_blockscan")) return rc;
   {
-    ProfScope ps("k_bwd_revorder", s);
-    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
+    ProfScope ps("k_bwd_fwdorder", s);
+    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                       static_cast<const T*>(k), static_cast<const T*>(v), g,
+                       static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq);
+  }
+  if (int rc = hip_check("k_bwd_fwdorder")) return rc;
+  {
+    const int n_pairs = L.n_blk * H;
+    const unsigned n_wg = static_cast<unsigned>((n_pairs + 7) / 8) * 16u;
+    ProfScope ps("k_bwd_revorder", s);
+    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(n_wg), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
+                       B.blk_tab, B.replay_row, H, n_pairs, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), dS_end, rq, static_cast<T*>(dk),
                        static_cast<T*>(dv), dg, rep_grad, Rb);

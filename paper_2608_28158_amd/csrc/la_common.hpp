@@ -7,9 +7,9 @@
 // token index are read "k-major" with the gfx950 LDS transpose read
 // (ds_read_b64_tr_b16): within each group of 16 lanes, lane i, slot j
 // receives element i % 4 of the 4-element read issued by lane 4j + i / 4, so
-// lane L of group g reading &X[4g + L/4][4*(L%4)] obtains X[4g + e][L],
-// e = 0..3 -- the 16x16x16 operand layout; two such reads form the 16x16x32
-// one.  The float32 path reads single elements and needs no transpose.
+// lane L of group g reading &X[R + L/4][C + 4*(L%4)] obtains X[R + e][C + L],
+// e = 0..3; with R = 4g this is the 16x16x16 operand layout.  The float32
+// path reads single elements and needs no transpose.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -33,52 +33,96 @@ enum : int { ROW_PAD = 0, ROW_REPLAY = 1, ROW_OWN = 2 };
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
-  static constexpr int PAD = 4;  // 16 bytes of row padding in LDS
   __device__ static inline float to_f(float x) { return x; }
   __device__ static inline float from_f(float x) { return x; }
 };
 template <> struct Elem<bf16> {
-  static constexpr int PAD = 8;
   __device__ static inline float to_f(bf16 x) { return static_cast<float>(x); }
   __device__ static inline bf16 from_f(float x) { return static_cast<bf16>(x); }  // RNE
 };
 
-// Launch shape and LDS strides for element type T and head dimension D.
+// LDS tile layout: 64 rows of COLS elements, row-major, each row padded by
+// 16 bytes.  Addresses are affine in (r, c), so every fragment read is a
+// per-lane base plus an immediate offset.  With the padding, 16-byte row
+// writes and 2-byte accumulator-layout writes are free of bank conflicts and
+// the 8-byte fragment reads below (k-contiguous and transposed) lose at most
+// a few cycles per instruction to them.
+template <typename T, int COLS>
+struct Tile {
+  static constexpr int LD = COLS + 16 / static_cast<int>(sizeof(T));  // row stride (elements)
+  static constexpr int SIZE = CB * LD;
+  __device__ static inline int at(int r, int c) { return r * LD + c; }
+};
+
+// Launch shape for element type T and head dimension D.  Four waves per
+// workgroup; wave w owns the state columns 16 CPW w .. 16 CPW (w + 1) - 1 (CPW
+// 16-column strips) and all NT 16-row tiles of them.  Chunk kernels are built
+// for two resident workgroups per CU (two waves per SIMD).
 template <typename T, int D>
 struct Cfg {
-  static constexpr int NW = D == 128 ? 8 : 4;          // waves per workgroup
+  static constexpr int NW = 4;                         // waves per workgroup
   static constexpr int NTHR = 64 * NW;
   static constexpr int VE = 16 / sizeof(T);            // elements per 16-byte vector
   static constexpr int VPR = D / VE;                   // vectors per row
   static constexpr int NV = CB * VPR / NTHR;           // vectors per thread per tile
-  static constexpr int NT = D / 16;                    // 16-wide tiles along d
-  static constexpr int LDR = D + Elem<T>::PAD;         // [64][D] tiles
-  static constexpr int LDA = CB + Elem<T>::PAD;        // [64][64] tiles
-  static constexpr int ATPW = 16 / NW;                 // score tiles per wave
-  static_assert(NT == NW, "one 16-column state tile per wave");
+  static constexpr int NT = D / 16;                    // 16-row tiles of a state
+  static constexpr int CPW = D / 16 / NW;              // 16-column strips per wave
+  static constexpr int WPE = 2;                        // waves per SIMD
+  using TD = Tile<T, D>;                               // [64][D] tiles
+  using TA = Tile<T, CB>;                              // [64][64] tiles
+  static_assert(CPW >= 1 && NT == NW * CPW, "state split into column strips");
+  static_assert(NW == CB / 16, "one score row block per wave");
 };
 
 // 16x16 MFMA tile products.  C[m][n] += sum_k A[m][k] B[k][n] with each
-// operand either k-contiguous ("kc": A stored [m][k], B stored [n][k]) or
-// k-major ("km": A stored [k][m], B stored [k][n]).  Pointers address the
-// tile origin (row m0 / n0 for kc, column m0 / n0 for km) at k = 0.
+// operand either k-contiguous ("kc": A stored as rows m, B stored as rows n)
+// or k-major ("km": A stored as rows k with m along the row, B as rows k with
+// n along the row).  An operand is (tile base, tile layout, origin): for kc
+// the origin is (row m0 or n0, column k = 0); for km it is (row k = 0,
+// column m0 or n0).
 template <typename T> struct Frag;
+// bf16: one 16x16x32 instruction per 32-deep k step.  Lane (g, i), g = lane /
+// 16, holds k in {4g..4g+3} u {16+4g..16+4g+3} for both operands (the same
+// permutation of k on both sides leaves the product unchanged), so every
+// fragment is two non-adjacent 8-byte LDS reads.
 template <> struct Frag<bf16> {
   static constexpr int KSTEP = 32;
   typedef bf16x8 V;
-  __device__ static inline V kc(const bf16* p, int ld, int lane) {
-    return *reinterpret_cast<const bf16x8*>(p + (lane & 15) * ld + (lane >> 4) * 8);
+  __device__ static inline V join(const bf16x4& a, const bf16x4& b) {
+    V v;
+    v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+    v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
+    return v;
   }
-  __device__ static inline V km(const bf16* p, int ld, int lane) {
-    const bf16* base = p + ((lane >> 4) * 8 + ((lane & 15) >> 2)) * ld + 4 * (lane & 3);
+  template <typename L>
+  __device__ static inline V kc(const bf16* t, int r0, int c0, int lane) {
+    const int r = r0 + (lane & 15), c = c0 + (lane >> 4) * 4;
+    return join(*reinterpret_cast<const bf16x4*>(t + L::at(r, c)),
+                *reinterpret_cast<const bf16x4*>(t + L::at(r, c + 16)));
+  }
+  template <typename L>
+  __device__ static inline V km(const bf16* t, int r0, int c0, int lane) {
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 4 * ld));
-    V r;
-    const bf16x4 a = __builtin_bit_cast(bf16x4, lo), b = __builtin_bit_cast(bf16x4, hi);
-    r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
-    r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
-    return r;
+    const int r = r0 + (lane >> 4) * 4 + ((lane & 15) >> 2), c = c0 + 4 * (lane & 3);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(t + L::at(r, c)));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(t + L::at(r + 16, c)));
+    return join(__builtin_bit_cast(bf16x4, lo), __builtin_bit_cast(bf16x4, hi));
+  }
+  // km fragment with row k of the tile (the contraction index) scaled by
+  // s[k]: slot e holds k = r0 + 4g + e, slot 4 + e holds k = r0 + 16 + 4g + e.
+  template <typename L>
+  __device__ static inline V km_scaled(const bf16* t, int r0, int c0, const float* s, int lane) {
+    const V x = km<L>(t, r0, c0, lane);
+    const int k4 = r0 + (lane >> 4) * 4;
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(s + k4);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(s + k4 + 16);
+    V y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      y[e] = static_cast<bf16>(static_cast<float>(x[e]) * lo[e]);
+      y[4 + e] = static_cast<bf16>(static_cast<float>(x[4 + e]) * hi[e]);
+    }
+    return y;
   }
   __device__ static inline void mma(f32x4& c, const V& a, const V& b) {
     c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -87,53 +131,151 @@ template <> struct Frag<bf16> {
 template <> struct Frag<float> {
   static constexpr int KSTEP = 4;
   typedef float V;
-  __device__ static inline V kc(const float* p, int ld, int lane) {
-    return p[(lane & 15) * ld + (lane >> 4)];
+  template <typename L>
+  __device__ static inline V kc(const float* t, int r0, int c0, int lane) {
+    return t[L::at(r0 + (lane & 15), c0 + (lane >> 4))];
   }
-  __device__ static inline V km(const float* p, int ld, int lane) {
-    return p[(lane >> 4) * ld + (lane & 15)];
+  template <typename L>
+  __device__ static inline V km(const float* t, int r0, int c0, int lane) {
+    return t[L::at(r0 + (lane >> 4), c0 + (lane & 15))];
+  }
+  template <typename L>
+  __device__ static inline V km_scaled(const float* t, int r0, int c0, const float* s, int lane) {
+    return km<L>(t, r0, c0, lane) * s[r0 + (lane >> 4)];
   }
   __device__ static inline void mma(f32x4& c, const V& a, const V& b) {
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
   }
 };
 
-template <typename T, bool A_KM, bool B_KM>
-__device__ inline void tile(f32x4& c, const T* A, int lda, const T* B, int ldb, int K, int lane) {
+// c += A * B over K; A, B described as (tile, layout, kc/km, origin).
+template <typename T, typename LA, bool A_KM, typename LB, bool B_KM>
+__device__ inline void tile(f32x4& c, const T* A, int am, const T* B, int bn, int K, int lane) {
   using F = Frag<T>;
 #pragma unroll
   for (int k = 0; k < K; k += F::KSTEP) {
-    const typename F::V a = A_KM ? F::km(A + k * lda, lda, lane) : F::kc(A + k, lda, lane);
-    const typename F::V b = B_KM ? F::km(B + k * ldb, ldb, lane) : F::kc(B + k, ldb, lane);
+    const typename F::V a = A_KM ? F::template km<LA>(A, k, am, lane) : F::template kc<LA>(A, am, k, lane);
+    const typename F::V b = B_KM ? F::template km<LB>(B, k, bn, lane) : F::template kc<LB>(B, bn, k, lane);
     F::mma(c, a, b);
   }
 }
 
-// acc += A[16 x 16] * B where A is k-contiguous in LDS (A points at the tile
-// origin, row stride lda) and B is a 16x16 float32 accumulator tile held in
-// registers (C layout: lane l, element r holds B[4*(l/16) + r][l % 16]).
-// The C layout is exactly the B-operand layout of the 16x16x16 bf16
-// instruction; the float32 path issues four 16x16x4 instructions over the k
-// indices {4g + j}, g = lane / 16.
-template <typename T> struct MmaRegB;
-template <> struct MmaRegB<bf16> {
-  __device__ static inline void step(f32x4& c, const bf16* A, int lda, const f32x4& B, int lane) {
-    const bf16x4 a = *reinterpret_cast<const bf16x4*>(A + (lane & 15) * lda + (lane >> 4) * 4);
-    bf16x4 b;
-    b[0] = static_cast<bf16>(B[0]);
-    b[1] = static_cast<bf16>(B[1]);
-    b[2] = static_cast<bf16>(B[2]);
-    b[3] = static_cast<bf16>(B[3]);
-    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
-  }
-};
-template <> struct MmaRegB<float> {
-  __device__ static inline void step(f32x4& c, const float* A, int lda, const f32x4& B, int lane) {
-    const float* a = A + (lane & 15) * lda + (lane >> 4) * 4;
+// c[j] += A * B_j for the NJ output tiles of one row block (origins bn + 16 j),
+// the A fragment shared; B is k-major.  k runs over [k0, K).
+template <typename T, typename LA, bool A_KM, typename LB, int NJ>
+__device__ inline void tile_cols(f32x4* c, const T* A, int am, const T* B, int bn, int k0, int K,
+                                 int lane) {
+  using F = Frag<T>;
+#pragma unroll 1
+  for (int k = k0; k < K; k += F::KSTEP) {
+    const typename F::V a = A_KM ? F::template km<LA>(A, k, am, lane) : F::template kc<LA>(A, am, k, lane);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], B[j], c, 0, 0, 0);
+    for (int j = 0; j < NJ; ++j) F::mma(c[j], a, F::template km<LB>(B, k, bn + 16 * j, lane));
+  }
+}
+
+// Masked score row block: c[jt] += L[m0.., :] R[16 jt.., :]^T for jt <= it
+// (both operands k-contiguous over the head dimension, K = D), the L
+// fragment shared across the tiles of the row.
+template <typename T, typename LL, typename LR>
+__device__ inline void score_row(f32x4* c, const T* Lt, const T* Rt, int it, int K, int lane) {
+  using F = Frag<T>;
+#pragma unroll 1
+  for (int k = 0; k < K; k += F::KSTEP) {
+    const typename F::V a = F::template kc<LL>(Lt, it * 16, k, lane);
+#pragma unroll
+    for (int jt = 0; jt < CB / 16; ++jt)
+      if (jt <= it) F::mma(c[jt], a, F::template kc<LR>(Rt, jt * 16, k, lane));
+  }
+}
+
+// S[j NT + i] += A_i * diag(s) * B_j for the state tiles of a wave: A_i is
+// k-major with origin column 16 i, B_j k-major with origin column bn + 16 j
+// and its row k scaled by s[k]; each fragment is loaded once per k step.
+template <typename T, typename LA, typename LB, int NT, int CPW>
+__device__ inline void state_update(f32x4* S, const T* A, const T* B, int bn, const float* s, int lane) {
+  using F = Frag<T>;
+#pragma unroll 1
+  for (int k = 0; k < CB; k += F::KSTEP) {
+    typename F::V b[CPW];
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) b[j] = F::template km_scaled<LB>(B, k, bn + 16 * j, s, lane);
+#pragma unroll
+    for (int i = 0; i < NT; ++i) {
+      const typename F::V a = F::template km<LA>(A, k, i * 16, lane);
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) F::mma(S[j * NT + i], a, b[j]);
+    }
+  }
+}
+
+// acc[j] += A * B_j where A is k-contiguous in LDS (rows m0.., columns k of a
+// tile with layout L) and B_j is the wave's state strip j held in registers
+// in the accumulator layout (lane l, element r of state tile kt holds
+// B[16 kt + 4 (l / 16) + r][l % 16]), pre-converted by RegB<T>::pack.  For
+// bf16 two state tiles kt, kt + 1 form the B operand of one 16x16x32
+// instruction: lane group g then holds k = 16 kt + {4g..4g+3} and
+// 16 (kt + 1) + {4g..4g+3}, which is exactly the k set of the k-contiguous A
+// fragment read at column 16 kt.  The float32 path issues four 16x16x4
+// instructions per state tile over k = 16 kt + 4g + e.
+template <typename T> struct RegB;
+template <> struct RegB<bf16> {
+  static constexpr int KT = 2;  // state tiles per B operand
+  typedef bf16x8 P;
+  typedef bf16x8 A;
+  __device__ static inline P pack(const f32x4* B) {
+    P b;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      b[r] = static_cast<bf16>(B[0][r]);
+      b[4 + r] = static_cast<bf16>(B[1][r]);
+    }
+    return b;
+  }
+  template <typename L>
+  __device__ static inline A load(const bf16* t, int m0, int k0, int lane) {
+    return Frag<bf16>::kc<L>(t, m0, k0, lane);
+  }
+  __device__ static inline void mma(f32x4& c, const A& a, const P& b) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
 };
+template <> struct RegB<float> {
+  static constexpr int KT = 1;
+  typedef f32x4 P;
+  typedef f32x4 A;
+  __device__ static inline P pack(const f32x4* B) { return B[0]; }
+  template <typename L>
+  __device__ static inline A load(const float* t, int m0, int k0, int lane) {
+    const int r = m0 + (lane & 15), c4 = k0 + (lane >> 4) * 4;
+    return f32x4{t[L::at(r, c4)], t[L::at(r, c4 + 1)], t[L::at(r, c4 + 2)], t[L::at(r, c4 + 3)]};
+  }
+  __device__ static inline void mma(f32x4& c, const A& a, const P& b) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[e], b[e], c, 0, 0, 0);
+  }
+};
+
+// acc[j] += A[m0.., :] * B_j over the whole state dimension, B_j being the
+// wave's float32 state strip j (tiles S[j NT + kt]), converted per use.
+template <typename T, typename L, int NT, int CPW>
+__device__ inline void regb_rows(f32x4* acc, const T* A, int m0, const f32x4* S, int lane) {
+  using R = RegB<T>;
+#pragma unroll
+  for (int kt = 0; kt < NT; kt += R::KT) {
+    const typename R::A a = R::template load<L>(A, m0, kt * 16, lane);
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) R::mma(acc[j], a, R::pack(S + j * NT + kt));
+  }
+}
+
+// Hides the values of a state from the optimiser (no instructions): values
+// derived from it inside a loop stay inside the loop.
+template <int N>
+__device__ inline void opaque_state(f32x4* S) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(S[i]));
+}
 
 // Accumulator element r of lane l in a 16x16 tile sits at row 4*(l/16) + r,
 // column l % 16.
