@@ -48,6 +48,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# short workload names used by the committed profile summaries
+WORKLOAD_KEY = {1: "spine16k", 2: "agentic64k", 3: "agentic128k"}
+
+
 def la_source_sha():
     h = hashlib.sha256()
     for name in ("la.hip", "la_common.hpp"):
@@ -308,7 +312,7 @@ def main():
                         "achieved_GBs": b / (avg_ms * 1e-3) / 1e9}
     dom = max(kstats, key=lambda k: kstats[k]["avg_ms"] * kstats[k]["launches"])
     ds = kstats[dom]
-    traffic = read_traffic(dom, f"config{args.config}")
+    traffic = read_traffic(dom, WORKLOAD_KEY[args.config])
     flop_tok = H * (98304 + 245760 + 32768) * (d / 128) ** 2  # fwd + bwd + recompute state pass
     achieved_tflops = C * flop_tok / (ms * 1e-3) / 1e12
     peak_tf = PEAK_BF16_TFLOPS if el == 2 else PEAK_F32_TFLOPS

@@ -1,0 +1,89 @@
+"""Turns rocprofv3 output of ``bench.py --steps-only`` into the short text
+summaries kept under ``profiles/``.
+
+    python -m paper_2608_28158_amd.profile_summary stats <kernel_stats.csv> <out.md> <command...>
+    python -m paper_2608_28158_amd.profile_summary traffic <fetch.csv> <write.csv> \\
+        <copy_fetch.csv> <copy_write.csv> <copy_mib> <kernel> <out.txt> <command...>
+
+The traffic summary scales FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by
+what the same counters read for a plain device copy of known size, and
+records the hash of the kernel sources it was taken on.
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import hashlib
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def source_sha():
+    h = hashlib.sha256()
+    for name in ("la.hip", "la_common.hpp"):
+        with open(os.path.join(ROOT, "paper_2608_28158_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def short(name):
+    n = name.split("(")[0]
+    for key in ("k_bwd_revorder", "k_bwd_fwdorder", "k_blocksum", "k_fwd_blockscan",
+                "k_fwd_block", "k_bwd_blockscan", "k_dg_carry", "k_gather", "k_scatter_add",
+                "k_replay_reduce"):
+        if key in n:
+            return key
+    return n.replace("void ", "")[:48]
+
+
+def stats(src, out, cmd):
+    rows = list(csv.DictReader(open(src)))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    lines = ["# rocprofv3 kernel statistics", "", "Command:", "", "    " + " ".join(cmd), "",
+             f"Kernel source hash: {source_sha()}", "",
+             "| kernel | calls | total ms | avg us | min us | max us | share |",
+             "|---|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append("| %s | %s | %.3f | %.1f | %.1f | %.1f | %.1f%% |" % (
+            short(r["Name"]), r["Calls"], float(r["TotalDurationNs"]) / 1e6,
+            float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+            100 * float(r["TotalDurationNs"]) / tot))
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
+def per_kernel(path, counter):
+    agg, disp = collections.defaultdict(float), collections.defaultdict(set)
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        k = short(r["Kernel_Name"])
+        agg[k] += float(r["Counter_Value"])
+        disp[k].add(r["Dispatch_Id"])
+    return {k: agg[k] / len(disp[k]) for k in agg}
+
+
+def traffic(fetch, write, cfetch, cwrite, copy_mib, kernel, out, cmd):
+    f, w = per_kernel(fetch, "FETCH_SIZE"), per_kernel(write, "WRITE_SIZE")
+    cf = max(v for k, v in per_kernel(cfetch, "FETCH_SIZE").items() if "copy" in k.lower())
+    cw = max(v for k, v in per_kernel(cwrite, "WRITE_SIZE").items() if "copy" in k.lower())
+    kib = float(copy_mib) * 1024
+    sf, sw = kib / cf, kib / cw
+    hbm = (f[kernel] * sf + w[kernel] * sw) * 1024
+    lines = [f"# HBM traffic of {kernel} (rocprofv3 --pmc, per dispatch)",
+             "command: " + " ".join(cmd),
+             f"copy probe: {copy_mib} MiB read and written; FETCH_SIZE reads {cf:.0f} KiB "
+             f"(scale {sf:.3f}), WRITE_SIZE reads {cw:.0f} KiB (scale {sw:.3f})",
+             f"fetch_kib_per_launch: {f[kernel]:.0f}",
+             f"write_kib_per_launch: {w[kernel]:.0f}",
+             f"hbm_bytes_per_launch: {hbm:.0f}",
+             f"source_sha: {source_sha()}"]
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "stats":
+        stats(sys.argv[2], sys.argv[3], sys.argv[4:])
+    else:
+        traffic(*sys.argv[2:9], sys.argv[9:])
