@@ -86,11 +86,11 @@ struct ChunkRows {
   int fast;
   int row0;
 };
-__device__ inline ChunkRows chunk_rows(const int32_t* seq, int c) {
-  const int p0 = c * CB, n_rep = seq[SEQ_N_REPLAY];
+__device__ inline ChunkRows chunk_rows(const SeqInfo& sq, int c) {
+  const int p0 = c * CB;
   ChunkRows cr;
-  cr.fast = p0 >= n_rep && p0 + CB <= seq[SEQ_N_TOK];
-  cr.row0 = seq[SEQ_OWN_ROW] + p0 - n_rep;
+  cr.fast = p0 >= sq.n_rep && p0 + CB <= sq.n_tok;
+  cr.row0 = sq.own_row + p0 - sq.n_rep;
   return cr;
 }
 
@@ -99,7 +99,7 @@ __device__ inline ChunkRows chunk_rows(const int32_t* seq, int c) {
 template <typename T, int D>
 struct ChunkRefs {
   int rk[Cfg<T, D>::NV];
-  __device__ inline void resolve(const int32_t* seq, int c, const int32_t* replay_row, int t) {
+  __device__ inline void resolve(const SeqInfo& seq, int c, const int32_t* replay_row, int t) {
     using C = Cfg<T, D>;
 #pragma unroll
     for (int i = 0; i < C::NV; ++i) {
@@ -146,7 +146,7 @@ struct ChunkSrc {
   ChunkRefs<T, D> refs;
   RowRef mr;
   float gv;
-  __device__ inline void resolve(const int32_t* seq, int c, const int32_t* replay_row,
+  __device__ inline void resolve(const SeqInfo& seq, int c, const int32_t* replay_row,
                                  const float* g, int H, int h, int t) {
     cr = chunk_rows(seq, c);
     if (!cr.fast) refs.resolve(seq, c, replay_row, t);
@@ -229,18 +229,44 @@ __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) 
         dst[(i * 16 + acc_row(lane, r)) * D + (CPW * w + j) * 16 + acc_col(lane)] = S[j * NT + i][r];
 }
 
-// Masked score tiles of row block it: P[it][jt] = c[jt] * exp(G_m - G_n) * f
-// for n <= m, 0 above the diagonal.
-template <typename T>
-__device__ inline void put_scores(T* P, const f32x4* c, const float* G, float f, int it, int lane) {
+// Row block IT of a masked score tile, computed by one wave:
+// P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for n <= m, 0 above the
+// diagonal (tiles left of the diagonal need no mask).
+template <typename T, int D, int IT>
+__device__ inline void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f, int lane) {
   using TA = Tile<T, CB>;
+  using TD = Tile<T, D>;
+  f32x4 c[IT + 1];
 #pragma unroll
-  for (int jt = 0; jt < CB / 16; ++jt)
+  for (int jt = 0; jt <= IT; ++jt) c[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  score_row<T, TD, TD, IT, D>(c, Lt, Rt, lane);
+  float Gm[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) Gm[r] = G[IT * 16 + acc_row(lane, r)];
+#pragma unroll
+  for (int jt = 0; jt < CB / 16; ++jt) {
+    const int n = jt * 16 + acc_col(lane);
+    const float Gn = jt <= IT ? G[n] : 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = it * 16 + acc_row(lane, r), n = jt * 16 + acc_col(lane);
-      P[TA::at(m, n)] = Elem<T>::from_f(jt <= it && n <= m ? c[jt][r] * __expf(G[m] - G[n]) * f : 0.f);
+      const int m = IT * 16 + acc_row(lane, r);
+      float x = 0.f;
+      if (jt < IT) x = c[jt][r] * __expf(Gm[r] - Gn) * f;
+      else if (jt == IT) x = n <= m ? c[jt][r] * __expf(Gm[r] - Gn) * f : 0.f;
+      P[TA::at(m, n)] = Elem<T>::from_f(x);
     }
+  }
+}
+
+// Wave w computes row block w of the masked score tile.
+template <typename T, int D>
+__device__ inline void score_tile(T* P, const T* Lt, const T* Rt, const float* G, float f, int w, int lane) {
+  switch (w) {
+    case 0: score_block<T, D, 0>(P, Lt, Rt, G, f, lane); break;
+    case 1: score_block<T, D, 1>(P, Lt, Rt, G, f, lane); break;
+    case 2: score_block<T, D, 2>(P, Lt, Rt, G, f, lane); break;
+    default: score_block<T, D, 3>(P, Lt, Rt, G, f, lane); break;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -255,6 +281,7 @@ __device__ inline void put_scores(T* P, const f32x4* c, const float* G, float f,
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksum(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dO,
     const float* __restrict__ g, float* __restrict__ dSb, float* __restrict__ U,
@@ -264,9 +291,9 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   __shared__ T Ys[Tile<T, D>::SIZE];
   __shared__ ChunkMeta meta;
   const int side = side0 + static_cast<int>(blockIdx.z);
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x], h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int32_t* seq = seq_tab + bk[BLK_SEQ] * SEQ_WORDS;
+  const SeqInfo sq = seq_info(seq_tab + bk[BLK_SEQ] * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const T* X = side ? q : k;
   const T* Y = side ? dO : v;
@@ -276,7 +303,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   for (int i = 0; i < C::CPW * C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   ChunkSrc<T, D> cs;
   Vec16 px[C::NV], py[C::NV];
-  cs.resolve(seq, c0, replay_row, g, H, h, t);
+  cs.resolve(sq, c0, replay_row, g, H, h, t);
   fetch<T, D>(px, X, cs, H, h, t, min_kind);
   fetch<T, D>(py, Y, cs, H, h, t, min_kind);
   float Gs = 0.f;  // log-decay from the block start to the current chunk start
@@ -291,7 +318,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
     __syncthreads();
     const float GL = meta.G[CB - 1];
     if (c + 1 < c_end) {
-      cs.resolve(seq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c + 1, replay_row, g, H, h, t);
       fetch<T, D>(px, X, cs, H, h, t, min_kind);
       fetch<T, D>(py, Y, cs, H, h, t, min_kind);
     }
@@ -419,6 +446,7 @@ struct FwdSmem {
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_block(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ S0, const float* __restrict__ S_end, T* __restrict__ o) {
@@ -426,11 +454,11 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ FwdSmem<T, D> sm;
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x], h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const int64_t DD = static_cast<int64_t>(D) * D;
   f32x4 S[NS];  // S : rows (dk), columns (dv) of the wave's strips
@@ -439,7 +467,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
                         false, w, lane);
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV];
-  cs.resolve(seq, c0, replay_row, g, H, h, t);
+  cs.resolve(sq, c0, replay_row, g, H, h, t);
   fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
@@ -457,19 +485,13 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     __syncthreads();
     const float GL = sm.meta.G[CB - 1];
     if (c + 1 < c_end) {
-      cs.resolve(seq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c + 1, replay_row, g, H, h, t);
       fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
       fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
       fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     }
     // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    {
-      f32x4 a[CB / 16];
-#pragma unroll
-      for (int jt = 0; jt < CB / 16; ++jt) a[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      score_row<T, typename C::TD, typename C::TD>(a, sm.Q, sm.K, w, D, lane);
-      put_scores<T>(sm.A, a, sm.meta.G, 1.f, w, lane);
-    }
+    score_tile<T, D>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     __syncthreads();
     // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V)
 #pragma unroll 1
@@ -533,6 +555,7 @@ struct BfSmem {
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwdorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const T* __restrict__ dO, const float* __restrict__ S0, const float* __restrict__ S_end,
@@ -541,11 +564,11 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ BfSmem<T, D> sm;
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x], h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const int64_t DD = static_cast<int64_t>(D) * D;
   f32x4 St[NS];  // S^T : rows (dv), columns (dk) of the wave's strips
@@ -554,7 +577,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
                         true, w, lane);
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  cs.resolve(seq, c0, replay_row, g, H, h, t);
+  cs.resolve(sq, c0, replay_row, g, H, h, t);
   fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
@@ -574,20 +597,14 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
     __syncthreads();
     const float GL = sm.meta.G[CB - 1];
     if (c + 1 < c_end) {
-      cs.resolve(seq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c + 1, replay_row, g, H, h, t);
       fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
       fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
       fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
       fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
     }
     // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    {
-      f32x4 a[CB / 16];
-#pragma unroll
-      for (int jt = 0; jt < CB / 16; ++jt) a[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      score_row<T, typename C::TD, typename C::TD>(a, sm.dO, sm.V, w, D, lane);
-      put_scores<T>(sm.dA, a, sm.meta.G, scale, w, lane);
-    }
+    score_tile<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
     __syncthreads();
     // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
 #pragma unroll 1
@@ -632,7 +649,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < C::NW; ++i) s += sm.rq[i][t];
-      rq_out[((static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) + c) * CB + t) * H + h] = s;
+      rq_out[((static_cast<int64_t>(sq.chunk_off) + c) * CB + t) * H + h] = s;
     }
   }
 }
@@ -665,7 +682,8 @@ struct BrSmem {
 template <typename T, int D, int SIDE>
 __device__ __forceinline__ void bwd_revorder_side(
     BrSmem<T, D>& sm, int pair, const int32_t* __restrict__ seq_tab,
-    const int32_t* __restrict__ blk_tab, const int32_t* __restrict__ replay_row, int H, float scale,
+    const int32_t* __restrict__ blk_tab, const int32_t* __restrict__ blk_order,
+    const int32_t* __restrict__ replay_row, int H, float scale,
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
     const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
@@ -674,11 +692,11 @@ __device__ __forceinline__ void bwd_revorder_side(
   constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
   constexpr bool side = SIDE == 1;
-  const int b = pair / H, h = pair % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[pair / H], h = pair % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
   // side 0: dS   rows (dk), columns (dv) of the wave's strips
@@ -688,13 +706,13 @@ __device__ __forceinline__ void bwd_revorder_side(
   float carry = 0.f;  // side 1: sum of (q.dq - k.dk) over the later chunks of the block
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  cs.resolve(seq, c_last, replay_row, g, H, h, t);
+  cs.resolve(sq, c_last, replay_row, g, H, h, t);
   fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   if (side) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
   // side 1, wave 0: q.dq of row t of the chunk, one chunk ahead
-  const float* rq_h = rq + (static_cast<int64_t>(seq[SEQ_CHUNK_OFF]) * CB + t) * H + h;
+  const float* rq_h = rq + (static_cast<int64_t>(sq.chunk_off) * CB + t) * H + h;
   float rq_next = side && t < CB ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
   for (int c = c_last; c >= c0; --c) {
     if (t < CB) {
@@ -712,7 +730,7 @@ __device__ __forceinline__ void bwd_revorder_side(
     __syncthreads();
     const float GL = sm.meta.G[CB - 1];
     if (c > c0) {
-      cs.resolve(seq, c - 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c - 1, replay_row, g, H, h, t);
       fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
       fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
       if (side) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
@@ -721,14 +739,8 @@ __device__ __forceinline__ void bwd_revorder_side(
     }
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i]; wave w computes row block w
-    {
-      f32x4 a[CB / 16];
-#pragma unroll
-      for (int jt = 0; jt < CB / 16; ++jt) a[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (side) score_row<T, typename C::TD, typename C::TD>(a, sm.dO, sm.V, w, D, lane);
-      else score_row<T, typename C::TD, typename C::TD>(a, sm.Q, sm.K, w, D, lane);
-      put_scores<T>(sm.P, a, sm.meta.G, side ? scale : 1.f, w, lane);
-    }
+    if (side) score_tile<T, D>(sm.P, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    else score_tile<T, D>(sm.P, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     __syncthreads();
 #pragma unroll 1
     for (int jt = 0; jt < CB / 16; ++jt) {
@@ -816,6 +828,7 @@ __device__ __forceinline__ void bwd_revorder_side(
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_revorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, int n_pairs, float scale,
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
@@ -826,10 +839,10 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_rev
   const int pair = (id >> 4) * 8 + (id & 7);
   if (pair >= n_pairs) return;  // whole workgroup, before any barrier
   if ((id >> 3) & 1)
-    bwd_revorder_side<T, D, 1>(sm, pair, seq_tab, blk_tab, replay_row, H, scale, q, k, v, g, dO,
+    bwd_revorder_side<T, D, 1>(sm, pair, seq_tab, blk_tab, blk_order, replay_row, H, scale, q, k, v, g, dO,
                                dS_end, rq, dk, dv, dg, rep_grad, Rb);
   else
-    bwd_revorder_side<T, D, 0>(sm, pair, seq_tab, blk_tab, replay_row, H, scale, q, k, v, g, dO,
+    bwd_revorder_side<T, D, 0>(sm, pair, seq_tab, blk_tab, blk_order, replay_row, H, scale, q, k, v, g, dO,
                                dS_end, rq, dk, dv, dg, rep_grad, Rb);
 }
 
@@ -1024,13 +1037,14 @@ Sizes sizes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
 struct Blob {
   const int32_t* seq_tab;
   const int32_t* blk_tab;
+  const int32_t* blk_order;
   const int32_t* replay_row;
 };
 
 Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   const int32_t* b = static_cast<const int32_t*>(d_blob);
   const RoundLayout& L = p->rounds[round];
-  return Blob{b + L.seq_tab, b + L.blk_tab, b + p->off_replay_row};
+  return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_order, b + p->off_replay_row};
 }
 
 // Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b).
@@ -1041,7 +1055,7 @@ int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, 
   const RoundLayout& L = p->rounds[round];
   ProfScope ps("k_blocksum", s);
   hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk, H, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
-                     B.seq_tab, B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                     B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                      static_cast<const T*>(k), static_cast<const T*>(v),
                      static_cast<const T*>(dO), g, dSb, U, gam, side0);
   return hip_check("k_blocksum");
@@ -1078,7 +1092,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   {
     ProfScope ps("k_fwd_block", s);
     hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                       B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g, S0, S_end,
                        static_cast<T*>(o));
   }
@@ -1134,7 +1148,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   {
     ProfScope ps("k_bwd_fwdorder", s);
     hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.replay_row, H, scale, static_cast<const T*>(q),
+                       B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq);
   }
@@ -1144,7 +1158,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     const unsigned n_wg = static_cast<unsigned>((n_pairs + 7) / 8) * 16u;
     ProfScope ps("k_bwd_revorder", s);
     hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(n_wg), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.replay_row, H, n_pairs, scale, static_cast<const T*>(q),
+                       B.blk_tab, B.blk_order, B.replay_row, H, n_pairs, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), dS_end, rq, static_cast<T*>(dk),
                        static_cast<T*>(dv), dg, rep_grad, Rb);

@@ -174,18 +174,17 @@ __device__ inline void tile_cols(f32x4* c, const T* A, int am, const T* B, int b
   }
 }
 
-// Masked score row block: c[jt] += L[m0.., :] R[16 jt.., :]^T for jt <= it
-// (both operands k-contiguous over the head dimension, K = D), the L
+// Masked score row block IT: c[jt] += L[16 IT.., :] R[16 jt.., :]^T for
+// jt <= IT (both operands k-contiguous over the head dimension, K = D), the L
 // fragment shared across the tiles of the row.
-template <typename T, typename LL, typename LR>
-__device__ inline void score_row(f32x4* c, const T* Lt, const T* Rt, int it, int K, int lane) {
+template <typename T, typename LL, typename LR, int IT, int K>
+__device__ inline void score_row(f32x4* c, const T* Lt, const T* Rt, int lane) {
   using F = Frag<T>;
-#pragma unroll 1
-  for (int k = 0; k < K; k += F::KSTEP) {
-    const typename F::V a = F::template kc<LL>(Lt, it * 16, k, lane);
 #pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt)
-      if (jt <= it) F::mma(c[jt], a, F::template kc<LR>(Rt, jt * 16, k, lane));
+  for (int k = 0; k < K; k += F::KSTEP) {
+    const typename F::V a = F::template kc<LL>(Lt, IT * 16, k, lane);
+#pragma unroll
+    for (int jt = 0; jt <= IT; ++jt) F::mma(c[jt], a, F::template kc<LR>(Rt, jt * 16, k, lane));
   }
 }
 
@@ -282,17 +281,30 @@ __device__ inline void opaque_state(f32x4* S) {
 __device__ inline int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }
 __device__ inline int acc_col(int lane) { return lane & 15; }
 
+// The sequence-table fields the chunk kernels use, read once per workgroup
+// (uniform, kept in scalar registers).
+struct SeqInfo {
+  int n_rep;       // replay rows (< chunk)
+  int n_tok;       // replay + own rows
+  int replay_off;  // global replay index of the first replay row
+  int own_row;     // physical row of the first own row
+  int chunk_off;   // first chunk of the sequence within the round
+};
+__device__ inline SeqInfo seq_info(const int32_t* seq) {
+  return SeqInfo{seq[SEQ_N_REPLAY], seq[SEQ_N_TOK], seq[SEQ_REPLAY_OFF], seq[SEQ_OWN_ROW],
+                 seq[SEQ_CHUNK_OFF]};
+}
+
 // Packed position p of a sequence -> (global row, kind, replay index).
 struct RowRef {
   int row, kind, rep;
 };
-__device__ inline RowRef pos_row(const int32_t* seq, int p, const int32_t* replay_row) {
-  const int n_rep = seq[SEQ_N_REPLAY];
-  if (p < n_rep) {
-    const int j = seq[SEQ_REPLAY_OFF] + p;
+__device__ inline RowRef pos_row(const SeqInfo& sq, int p, const int32_t* replay_row) {
+  if (p < sq.n_rep) {
+    const int j = sq.replay_off + p;
     return RowRef{replay_row[j], ROW_REPLAY, j};
   }
-  if (p < seq[SEQ_N_TOK]) return RowRef{seq[SEQ_OWN_ROW] + (p - n_rep), ROW_OWN, -1};
+  if (p < sq.n_tok) return RowRef{sq.own_row + (p - sq.n_rep), ROW_OWN, -1};
   return RowRef{0, ROW_PAD, -1};
 }
 

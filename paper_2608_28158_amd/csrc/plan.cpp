@@ -412,6 +412,8 @@ struct Builder {
       off = align_up(off + 2 * L.n_chunks);
       L.blk_tab = off;
       off = align_up(off + int64_t(L.n_blk) * BLK_WORDS);
+      L.blk_order = off;
+      off = align_up(off + L.n_blk);
     }
     p.off_replay_row = off;
     off = align_up(off + p.R);
@@ -494,6 +496,15 @@ struct Builder {
         chunk_off += nc;
       }
       L.max_seq_blocks = max_seq_blocks;
+      // launch order of the block kernels: longest block first (stable), so
+      // that the last workgroups to start are the shortest ones
+      std::vector<int32_t> order(L.n_blk);
+      for (int32_t j = 0; j < L.n_blk; ++j) order[j] = j;
+      const int32_t* bt = b + L.blk_tab;
+      std::stable_sort(order.begin(), order.end(), [bt](int32_t x, int32_t y) {
+        return bt[x * BLK_WORDS + BLK_NC] > bt[y * BLK_WORDS + BLK_NC];
+      });
+      std::copy(order.begin(), order.end(), b + L.blk_order);
     }
     for (int64_t j = 0; j < p.R; ++j) b[p.off_replay_row + j] = static_cast<int32_t>(p.replay_row[j]);
     for (size_t j = 0; j < p.req_chunk.size(); ++j) {

@@ -43,6 +43,7 @@ struct RoundLayout {
   int32_t n_seq = 0, seq_begin = 0, max_seq_chunks = 0;
   int32_t n_blk = 0, block_chunks = 0, max_seq_blocks = 0;
   int64_t blk_tab = 0;    // int32 offset of the [n_blk][BLK_WORDS] block table
+  int64_t blk_order = 0;  // int32 offset of [n_blk] block ids, longest block first
   int64_t n_chunks = 0, n_rows = 0, n_own = 0, n_replay = 0, own_row_begin = 0;
   int64_t seq_tab = 0;    // int32 offset of the sequence table
   int64_t init_idx = 0;   // int32 offset of the [n_seq] init bank indices
