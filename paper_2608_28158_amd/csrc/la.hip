@@ -133,9 +133,7 @@ struct ChunkMeta {
   alignas(16) float G[CB];  // G_t = g_0 + ... + g_t within the chunk
   alignas(16) float x[CB];  // kernel-specific per-row factors
   alignas(16) float y[CB];
-  int row[CB];
-  int kind[CB];
-  int rep[CB];
+  int rowk[CB];  // physical row * 4 + kind (replay index = replay_off + position)
 };
 
 // Where this thread's rows of one chunk live, resolved one chunk ahead: the
@@ -187,18 +185,11 @@ __device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkS
 template <typename T, int D>
 __device__ inline void meta_publish(ChunkMeta& m, const ChunkSrc<T, D>& cs, int t, float& Gt,
                                     float& GL) {
-  m.row[t] = cs.mr.row;
-  m.kind[t] = cs.mr.kind;
-  m.rep[t] = cs.mr.rep;
-  float x = cs.gv;
-#pragma unroll
-  for (int off = 1; off < CB; off <<= 1) {
-    const float y = __shfl_up(x, off, CB);
-    if (t >= off) x += y;
-  }
+  m.rowk[t] = cs.mr.row * 4 + cs.mr.kind;
+  const float x = wave_prefix_sum(cs.gv, t);
   m.G[t] = x;
   Gt = x;
-  GL = __shfl(x, CB - 1, CB);
+  GL = lane_value(x, CB - 1);
 }
 
 // A wave's part of a [D x D] state: tile j * NT + i is rows 16 i.., columns
@@ -229,43 +220,57 @@ __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) 
         dst[(i * 16 + acc_row(lane, r)) * D + (CPW * w + j) * 16 + acc_col(lane)] = S[j * NT + i][r];
 }
 
-// Row block IT of a masked score tile, computed by one wave:
-// P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for n <= m, 0 above the
-// diagonal (tiles left of the diagonal need no mask).
-template <typename T, int D, int IT>
+// Part of row block IT of a masked score tile, computed by one wave: column
+// tiles jt = J0, J0 + JS, ...  P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for
+// n <= m, 0 above the diagonal (tiles left of the diagonal need no mask).
+template <typename T, int D, int IT, int J0, int JS>
 __device__ inline void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f, int lane) {
   using TA = Tile<T, CB>;
   using TD = Tile<T, D>;
-  f32x4 c[IT + 1];
+  constexpr int NJ = (CB / 16 - J0 + JS - 1) / JS;
+  f32x4 c[NJ];
 #pragma unroll
-  for (int jt = 0; jt <= IT; ++jt) c[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  score_row<T, TD, TD, IT, D>(c, Lt, Rt, lane);
-  float Gm[4];
+  for (int q = 0; q < NJ; ++q) c[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  score_row<T, TD, TD, IT, J0, JS, D>(c, Lt, Rt, lane);
+  const f32x4 Gm = row_vec(G, IT * 16, lane);
 #pragma unroll
-  for (int r = 0; r < 4; ++r) Gm[r] = G[IT * 16 + acc_row(lane, r)];
-#pragma unroll
-  for (int jt = 0; jt < CB / 16; ++jt) {
+  for (int q = 0; q < NJ; ++q) {
+    const int jt = J0 + q * JS;
     const int n = jt * 16 + acc_col(lane);
     const float Gn = jt <= IT ? G[n] : 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = IT * 16 + acc_row(lane, r);
       float x = 0.f;
-      if (jt < IT) x = c[jt][r] * __expf(Gm[r] - Gn) * f;
-      else if (jt == IT) x = n <= m ? c[jt][r] * __expf(Gm[r] - Gn) * f : 0.f;
+      if (jt < IT) x = c[q][r] * __expf(Gm[r] - Gn) * f;
+      else if (jt == IT) x = n <= m ? c[q][r] * __expf(Gm[r] - Gn) * f : 0.f;
       P[TA::at(m, n)] = Elem<T>::from_f(x);
     }
   }
 }
 
-// Wave w computes row block w of the masked score tile.
-template <typename T, int D>
+// The NW waves of a workgroup split the masked score tile: row block w % 4,
+// and with eight waves every other column tile (parity w / 4).
+template <typename T, int D, int NW>
 __device__ inline void score_tile(T* P, const T* Lt, const T* Rt, const float* G, float f, int w, int lane) {
-  switch (w) {
-    case 0: score_block<T, D, 0>(P, Lt, Rt, G, f, lane); break;
-    case 1: score_block<T, D, 1>(P, Lt, Rt, G, f, lane); break;
-    case 2: score_block<T, D, 2>(P, Lt, Rt, G, f, lane); break;
-    default: score_block<T, D, 3>(P, Lt, Rt, G, f, lane); break;
+  if constexpr (NW == 4) {
+    switch (w) {
+      case 0: score_block<T, D, 0, 0, 1>(P, Lt, Rt, G, f, lane); break;
+      case 1: score_block<T, D, 1, 0, 1>(P, Lt, Rt, G, f, lane); break;
+      case 2: score_block<T, D, 2, 0, 1>(P, Lt, Rt, G, f, lane); break;
+      default: score_block<T, D, 3, 0, 1>(P, Lt, Rt, G, f, lane); break;
+    }
+  } else {
+    switch (w) {
+      case 0: score_block<T, D, 0, 0, 2>(P, Lt, Rt, G, f, lane); break;
+      case 1: score_block<T, D, 1, 0, 2>(P, Lt, Rt, G, f, lane); break;
+      case 2: score_block<T, D, 2, 0, 2>(P, Lt, Rt, G, f, lane); break;
+      case 3: score_block<T, D, 3, 0, 2>(P, Lt, Rt, G, f, lane); break;
+      case 4: score_block<T, D, 0, 1, 2>(P, Lt, Rt, G, f, lane); break;
+      case 5: score_block<T, D, 1, 1, 2>(P, Lt, Rt, G, f, lane); break;
+      case 6: score_block<T, D, 2, 1, 2>(P, Lt, Rt, G, f, lane); break;
+      default: score_block<T, D, 3, 1, 2>(P, Lt, Rt, G, f, lane); break;
+    }
   }
 }
 
@@ -491,21 +496,20 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
       fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     }
     // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    score_tile<T, D>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+    score_tile<T, D, C::NW>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     __syncthreads();
     // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V)
-#pragma unroll 1
+#pragma unroll 2
     for (int it = 0; it < CB / 16; ++it) {
       f32x4 acc[C::CPW];
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       opaque_state<NS>(S);
       regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, sm.Q, it * 16, S, lane);
+{
+        const f32x4 e = row_vec(sm.meta.y, it * 16, lane);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = sm.meta.y[it * 16 + acc_row(lane, r)];
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j) acc[j][r] *= e;
+        for (int j = 0; j < C::CPW; ++j) acc[j] *= e;
       }
       tile_cols<T, typename C::TA, false, typename C::TD, C::CPW>(acc, sm.A, it * 16, sm.V, col0, 0,
                                                                  (it + 1) * 16, lane);
@@ -520,8 +524,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = it * 16 + acc_row(lane, r);
-          if (sm.meta.kind[m] == ROW_OWN) {
-            T* dst = o + (static_cast<int64_t>(sm.meta.row[m]) * H + h) * D + col0 + acc_col(lane);
+          if ((sm.meta.rowk[m] & 3) == ROW_OWN) {
+            T* dst = o + (static_cast<int64_t>((sm.meta.rowk[m] >> 2)) * H + h) * D + col0 + acc_col(lane);
 #pragma unroll
             for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r] * scale);
           }
@@ -604,35 +608,33 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
       fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
     }
     // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    score_tile<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    score_tile<T, D, C::NW>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
     __syncthreads();
     // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
-#pragma unroll 1
+#pragma unroll 2
     for (int it = 0; it < CB / 16; ++it) {
       f32x4 acc[C::CPW];
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       opaque_state<NS>(St);
       regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, sm.dO, it * 16, St, lane);
+{
+        const f32x4 e = row_vec(sm.meta.y, it * 16, lane);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = sm.meta.y[it * 16 + acc_row(lane, r)];
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j) acc[j][r] *= e;
+        for (int j = 0; j < C::CPW; ++j) acc[j] *= e;
       }
       tile_cols<T, typename C::TA, false, typename C::TD, C::CPW>(acc, sm.dA, it * 16, sm.K, col0, 0,
                                                                  (it + 1) * 16, lane);
+      f32x4 qd = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < C::CPW; ++j) qd += ColRead<T>::template get<typename C::TD>(sm.Q, it * 16, col0 + 16 * j, lane) * acc[j];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = it * 16 + acc_row(lane, r);
-        float x = 0.f;
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j)
-          x += Elem<T>::to_f(sm.Q[C::TD::at(m, col0 + 16 * j + acc_col(lane))]) * acc[j][r];
-        const float s = sum16(x);
+        const float s = sum16(qd[r]);
         if ((lane & 15) == 0) sm.rq[w][m] = s;
-        if (cur.fast || sm.meta.kind[m] == ROW_OWN) {
-          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : sm.meta.row[m];
+        if (cur.fast || (sm.meta.rowk[m] & 3) == ROW_OWN) {
+          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (sm.meta.rowk[m] >> 2);
           T* dst = dq + (row * H + h) * D + col0 + acc_col(lane);
 #pragma unroll
           for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r]);
@@ -739,10 +741,10 @@ __device__ __forceinline__ void bwd_revorder_side(
     }
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i]; wave w computes row block w
-    if (side) score_tile<T, D>(sm.P, sm.dO, sm.V, sm.meta.G, scale, w, lane);
-    else score_tile<T, D>(sm.P, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+    if (side) score_tile<T, D, C::NW>(sm.P, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    else score_tile<T, D, C::NW>(sm.P, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     __syncthreads();
-#pragma unroll 1
+#pragma unroll 2
     for (int jt = 0; jt < CB / 16; ++jt) {
       // side 0: acc = diag(x) K dS + scale A^T dO ; side 1: acc = diag(x) V dS^T + dA^T Q
       // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
@@ -758,31 +760,31 @@ __device__ __forceinline__ void bwd_revorder_side(
       tile_cols<T, typename C::TA, true, typename C::TD, C::CPW>(ad, sm.P, jt * 16, side ? sm.Q : sm.dO,
                                                                 col0, k0, CB, lane);
       const float f = side ? 1.f : scale;
+      {
+        const f32x4 e = row_vec(sm.meta.x, jt * 16, lane);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = sm.meta.x[jt * 16 + acc_row(lane, r)];
+        for (int j = 0; j < C::CPW; ++j) acc[j] = acc[j] * e + f * ad[j];
+      }
+      f32x4 kd = {0.f, 0.f, 0.f, 0.f};
+      if (side) {
 #pragma unroll
-        for (int j = 0; j < C::CPW; ++j) acc[j][r] = acc[j][r] * e + f * ad[j][r];
+        for (int j = 0; j < C::CPW; ++j) kd += ColRead<T>::template get<typename C::TD>(sm.K, jt * 16, col0 + 16 * j, lane) * acc[j];
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = jt * 16 + acc_row(lane, r);
-        const int kind = cur.fast ? static_cast<int>(ROW_OWN) : sm.meta.kind[m];
+        const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (sm.meta.rowk[m] & 3);
         if (side) {
-          float x = 0.f;
-#pragma unroll
-          for (int j = 0; j < C::CPW; ++j)
-            x += Elem<T>::to_f(sm.K[C::TD::at(m, col0 + 16 * j + acc_col(lane))]) * acc[j][r];
-          const float s = sum16(x);
+          const float s = sum16(kd[r]);
           if ((lane & 15) == 0) sm.rk[w][m] = s;
         }
         if (cur.fast || kind == ROW_OWN) {
-          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : sm.meta.row[m];
+          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (sm.meta.rowk[m] >> 2);
           T* dst = (side ? dk : dv) + (row * H + h) * D + col0 + acc_col(lane);
 #pragma unroll
           for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r]);
         } else if (kind == ROW_REPLAY) {
-          float* dst = rep_grad + (static_cast<int64_t>(sm.meta.rep[m]) * H + h) * RG + (side ? 0 : D) +
+          float* dst = rep_grad + ((static_cast<int64_t>(sq.replay_off) + c * CB + m) * H + h) * RG + (side ? 0 : D) +
                        col0 + acc_col(lane);
 #pragma unroll
           for (int j = 0; j < C::CPW; ++j) dst[16 * j] = acc[j][r];
@@ -801,7 +803,7 @@ __device__ __forceinline__ void bwd_revorder_side(
     __syncthreads();
     // side 1, wave 0: local suffix sums of q.dq - k.dk, one row per lane
     if (side && t < CB) {
-      const int kind = sm.meta.kind[t];
+      const int kind = (sm.meta.rowk[t] & 3);
       float x = 0.f;
       if (kind != ROW_PAD) {
         float rks = 0.f;
@@ -809,16 +811,12 @@ __device__ __forceinline__ void bwd_revorder_side(
         for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][t];
         x = rq_cur - rks;
       }
-#pragma unroll
-      for (int off = 1; off < CB; off <<= 1) {
-        const float y = __shfl_down(x, off, CB);
-        if (t + off < CB) x += y;
-      }
+      x = wave_suffix_sum(x, t);
       const float val = x + carry;
-      if (kind == ROW_OWN) dg[static_cast<int64_t>(sm.meta.row[t]) * H + h] = val;
+      if (kind == ROW_OWN) dg[static_cast<int64_t>((sm.meta.rowk[t] >> 2)) * H + h] = val;
       else if (kind == ROW_REPLAY)
-        rep_grad[(static_cast<int64_t>(sm.meta.rep[t]) * H + h) * RG + 2 * D] = val;
-      carry += __shfl(x, 0, CB);
+        rep_grad[((static_cast<int64_t>(sq.replay_off) + c * CB + t) * H + h) * RG + 2 * D] = val;
+      carry += lane_value(x, 0);
     }
   }
   if (side && t == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;

@@ -71,7 +71,6 @@ struct Cfg {
   using TD = Tile<T, D>;                               // [64][D] tiles
   using TA = Tile<T, CB>;                              // [64][64] tiles
   static_assert(CPW >= 1 && NT == NW * CPW, "state split into column strips");
-  static_assert(NW == CB / 16, "one score row block per wave");
 };
 
 // 16x16 MFMA tile products.  C[m][n] += sum_k A[m][k] B[k][n] with each
@@ -174,17 +173,17 @@ __device__ inline void tile_cols(f32x4* c, const T* A, int am, const T* B, int b
   }
 }
 
-// Masked score row block IT: c[jt] += L[16 IT.., :] R[16 jt.., :]^T for
-// jt <= IT (both operands k-contiguous over the head dimension, K = D), the L
-// fragment shared across the tiles of the row.
-template <typename T, typename LL, typename LR, int IT, int K>
+// Masked score row block IT: c[q] += L[16 IT.., :] R[16 jt.., :]^T for the
+// column tiles jt = J0 + q JS <= IT (both operands k-contiguous over the head
+// dimension, K = D), the L fragment shared across the tiles.
+template <typename T, typename LL, typename LR, int IT, int J0, int JS, int K>
 __device__ inline void score_row(f32x4* c, const T* Lt, const T* Rt, int lane) {
   using F = Frag<T>;
 #pragma unroll
   for (int k = 0; k < K; k += F::KSTEP) {
     const typename F::V a = F::template kc<LL>(Lt, IT * 16, k, lane);
 #pragma unroll
-    for (int jt = 0; jt <= IT; ++jt) F::mma(c[jt], a, F::template kc<LR>(Rt, jt * 16, k, lane));
+    for (int jt = J0, q = 0; jt <= IT; jt += JS, ++q) F::mma(c[q], a, F::template kc<LR>(Rt, jt * 16, k, lane));
   }
 }
 
@@ -276,6 +275,32 @@ __device__ inline void opaque_state(f32x4* S) {
   for (int i = 0; i < N; ++i) asm volatile("" : "+v"(S[i]));
 }
 
+// Reads in the accumulator layout of a 16x16 tile: lane (g, i), g = lane / 16,
+// receives rows r0 + 4g + e (e = 0..3) of column c0 + i.  For bf16 this is one
+// transpose read (lane i of group g points at row r0 + 4g + i/4, column
+// c0 + 4 (i % 4)); per-row float vectors are one 16-byte read.
+template <typename T> struct ColRead;
+template <> struct ColRead<bf16> {
+  template <typename L>
+  __device__ static inline f32x4 get(const bf16* t, int r0, int c0, int lane) {
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    const int r = r0 + (lane >> 4) * 4 + ((lane & 15) >> 2), c = c0 + 4 * (lane & 3);
+    const bf16x4 b = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(t + L::at(r, c))));
+    return f32x4{static_cast<float>(b[0]), static_cast<float>(b[1]), static_cast<float>(b[2]),
+                 static_cast<float>(b[3])};
+  }
+};
+template <> struct ColRead<float> {
+  template <typename L>
+  __device__ static inline f32x4 get(const float* t, int r0, int c0, int lane) {
+    const int r = r0 + (lane >> 4) * 4, c = c0 + (lane & 15);
+    return f32x4{t[L::at(r, c)], t[L::at(r + 1, c)], t[L::at(r + 2, c)], t[L::at(r + 3, c)]};
+  }
+};
+__device__ inline f32x4 row_vec(const float* v, int r0, int lane) {
+  return *reinterpret_cast<const f32x4*>(v + r0 + (lane >> 4) * 4);
+}
+
 // Accumulator element r of lane l in a 16x16 tile sits at row 4*(l/16) + r,
 // column l % 16.
 __device__ inline int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }
@@ -308,13 +333,59 @@ __device__ inline RowRef pos_row(const SeqInfo& sq, int p, const int32_t* replay
   return RowRef{0, ROW_PAD, -1};
 }
 
-// Sum over the 16 lanes that share the same accumulator rows.
+// Cross-lane steps on DPP (data-parallel primitives: a VALU operand modifier
+// moving data between lanes of a 16-lane row), so that no step goes through
+// the LDS queue.  Lanes without a source read 0.
+template <int CTRL>
+__device__ inline float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                               0xF, 0xF, true));
+}
+constexpr int DPP_QUAD_XOR1 = 0xB1;      // quad_perm [1, 0, 3, 2]
+constexpr int DPP_QUAD_XOR2 = 0x4E;      // quad_perm [2, 3, 0, 1]
+constexpr int DPP_ROW_SHL = 0x100;       // + n: lane i reads lane i + n of its row
+constexpr int DPP_ROW_SHR = 0x110;       // + n: lane i reads lane i - n of its row
+constexpr int DPP_ROW_MIRROR = 0x140;    // lane i reads lane 15 - i
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane i reads lane 7 - i of its half row
+
+// Sum over the 16 lanes of a row (the lanes that share accumulator rows).
 __device__ inline float sum16(float x) {
-  x += __shfl_xor(x, 1, 64);
-  x += __shfl_xor(x, 2, 64);
-  x += __shfl_xor(x, 4, 64);
-  x += __shfl_xor(x, 8, 64);
+  x += dpp<DPP_QUAD_XOR1>(x);
+  x += dpp<DPP_QUAD_XOR2>(x);
+  x += dpp<DPP_ROW_HALF_MIRROR>(x);
+  x += dpp<DPP_ROW_MIRROR>(x);
   return x;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (lane order).
+__device__ inline float wave_prefix_sum(float x, int lane) {
+  x += dpp<DPP_ROW_SHR + 1>(x);
+  x += dpp<DPP_ROW_SHR + 2>(x);
+  x += dpp<DPP_ROW_SHR + 4>(x);
+  x += dpp<DPP_ROW_SHR + 8>(x);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 15));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 31));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 47));
+  const int row = lane >> 4;
+  return x + (row >= 1 ? r0 : 0.f) + (row >= 2 ? r1 : 0.f) + (row >= 3 ? r2 : 0.f);
+}
+
+// Inclusive suffix sum over the 64 lanes of a wave (lane order).
+__device__ inline float wave_suffix_sum(float x, int lane) {
+  x += dpp<DPP_ROW_SHL + 1>(x);
+  x += dpp<DPP_ROW_SHL + 2>(x);
+  x += dpp<DPP_ROW_SHL + 4>(x);
+  x += dpp<DPP_ROW_SHL + 8>(x);
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
+  const int row = lane >> 4;
+  return x + (row <= 0 ? r1 : 0.f) + (row <= 1 ? r2 : 0.f) + (row <= 2 ? r3 : 0.f);
+}
+
+// Value of lane l (uniform).
+__device__ inline float lane_value(float x, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
 }
 
 }  // namespace harts
