@@ -136,7 +136,7 @@ def read_traffic(kernel, workload_key):
         return None
 
 
-def cpu_baseline(forest, x, cfg, heads=(0,)):
+def cpu_baseline(forest, x, cfg, heads=(0, 5, 10, 15)):
     """The fp64 oracle (compact chunkwise execution + reverse-mode gradients)
     on a bounded sample: the listed heads of the same microbatch."""
     import torch
@@ -163,24 +163,52 @@ def run_step(runner, t):
     return fwd
 
 
-def time_steps(runner, t, steps, warmup, profile):
+def time_steps(runner, t, steps, warmup, profile, fn=None):
+    """Times `steps` calls of fn (default: one full step) after `warmup`
+    untimed ones, bracketed by synchronisations.  Returns (mean ms, kernel
+    profile, per-step ms) -- per-step times from events between the steps."""
     import torch
     from paper_2608_28158_amd import _lib
+    fn = fn or (lambda: run_step(runner, t))
     for _ in range(warmup):
-        run_step(runner, t)
+        fn()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     if profile:
         _lib.profile_begin()
-    start.record(stream)
-    for _ in range(steps):
-        run_step(runner, t)
-    stop.record(stream)
+    ev[0].record(stream)
+    for i in range(steps):
+        fn()
+        ev[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / steps
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    ms = ev[0].elapsed_time(ev[steps]) / steps
     kern = _lib.profile_end() if profile else {}
-    return ms, kern
+    return ms, kern, per
+
+
+def pass_times(runner, t, steps, warmup):
+    """Median ms of the separate passes: forward, backward from saved states,
+    forward + backward (states saved), forward + backward with
+    recompute-forward."""
+    q, k, v, g, dO, dSf, S0 = (t[n] for n in ("q", "k", "v", "g", "dO", "dS_final", "S0"))
+    saved = runner.forward(q, k, v, g, S0, outputs=True, keep_states=True)
+    fns = {
+        "fwd": lambda: runner.forward(q, k, v, g, S0, outputs=True, keep_states=False),
+        "bwd": lambda: runner.backward(q, k, v, g, dO, dSf, fwd=saved, S0_tree=S0,
+                                       recompute=False),
+        "fwd_bwd": lambda: runner.backward(q, k, v, g, dO, dSf,
+                                           fwd=runner.forward(q, k, v, g, S0, outputs=True,
+                                                              keep_states=True),
+                                           S0_tree=S0, recompute=False),
+        "recompute_fwd_bwd": lambda: run_step(runner, t),
+    }
+    out = {}
+    for name, fn in fns.items():
+        _, _, per = time_steps(runner, t, steps, warmup, False, fn)
+        out[name] = float(np.median(per))
+    return out
 
 
 def setup(idx):
@@ -213,7 +241,7 @@ def expanded_comparison(steps, warmup):
     from paper_2608_28158_amd.plan import HartsPlan
     from paper_2608_28158_amd.tree_la import TreeLARunner
     forest, cfg, x, plan, t, runner, _ = setup(4)
-    ms_tree, _ = time_steps(runner, t, steps, warmup, profile=False)
+    ms_tree, _, _ = time_steps(runner, t, steps, warmup, profile=False)
     # expanded forest: one single-segment tree per trajectory, canonical rows
     kids = forest.children()
     parent = forest.parent
@@ -241,7 +269,7 @@ def expanded_comparison(steps, warmup):
     te["S0"] = torch.zeros((len(trajs), cfg["H"], cfg["d"], cfg["d"]), dtype=torch.float32,
                            device="cuda")
     erunner = TreeLARunner(eplan, cfg["H"], cfg["d"], dt, "cuda")
-    ms_exp, _ = time_steps(erunner, te, steps, warmup, profile=False)
+    ms_exp, _, _ = time_steps(erunner, te, steps, warmup, profile=False)
     # metamorphic check: identical outputs on every trajectory row (same
     # chunk grid, same floating-point path)
     fo = run_step(runner, t)["o"].float().cpu().numpy()
@@ -293,10 +321,13 @@ def main():
     forest, cfg, x, plan, t, runner, plan_s = setup(args.config)
     log(f"[bench] C={plan.info['C']} S={plan.info['S']} R={plan.info['R']} "
         f"K={plan.info['n_rounds']} seqs={plan.info['n_seq']}")
-    ms, kern = time_steps(runner, t, args.steps, args.warmup, profile=not args.steps_only)
+    ms, _, step_ms = time_steps(runner, t, args.steps, args.warmup, profile=False)
     log(f"[bench] {ms:.3f} ms/step")
     if args.steps_only:
         return
+    # per-kernel times come from a separate run: the events recorded around
+    # every launch add host and queue work to the step
+    _, kern, _ = time_steps(runner, t, args.steps, 1, profile=True)
     H, d = cfg["H"], cfg["d"]
     el = 2 if cfg["dtype"] == "bf16" else 4
     C = plan.info["C"]
@@ -307,7 +338,8 @@ def main():
         steps_seen = max(1, n // max(1, per_step.get(name, 1)))
         b = alg.get(name, 0) / max(1, per_step.get(name, 1))   # per launch
         avg_ms = tot / n
-        kstats[name] = {"launches": n, "avg_ms": avg_ms, "share": tot / (ms * args.steps),
+        kstats[name] = {"launches": n, "avg_ms": avg_ms,
+                        "share": tot / sum(v[1] for v in kern.values()),
                         "alg_bytes_per_launch": b,
                         "achieved_GBs": b / (avg_ms * 1e-3) / 1e9}
     dom = max(kstats, key=lambda k: kstats[k]["avg_ms"] * kstats[k]["launches"])
@@ -339,16 +371,22 @@ def main():
                      "traffic": traffic},
         "mfma_util_pct": 100.0 * achieved_tflops / peak_tf,
         "step_alg_GBs": step_bytes / (ms * 1e-3) / 1e9,
+        "ms_median": float(np.median(step_ms)),
+        "ms_p10": float(np.percentile(step_ms, 10)),
+        "ms_p90": float(np.percentile(step_ms, 90)),
         "plan_ms": plan_s * 1e3,
         "value_with_plan": C / ((ms + plan_s * 1e3) * 1e-3),
         "kernels": kstats,
         "kernel_source_sha": la_source_sha(),
     }
+    log("[bench] separate passes")
+    passes = pass_times(runner, t, args.steps, args.warmup)
+    out["passes"] = {k: {"ms": v, "compact_tok_s": C / (v * 1e-3)} for k, v in passes.items()}
     if not args.no_expanded:
         log("[bench] compact vs expanded (4 trees, ~32k compact tokens)")
         out["compact_vs_expanded"] = expanded_comparison(max(3, args.steps // 2), 2)
     if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle, one head)")
+        log("[bench] cpu baseline (oracle, four heads)")
         out["cpu_baseline"] = cpu_baseline(forest, x, cfg)
     print(json.dumps(out), flush=True)
 

@@ -220,58 +220,46 @@ __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) 
         dst[(i * 16 + acc_row(lane, r)) * D + (CPW * w + j) * 16 + acc_col(lane)] = S[j * NT + i][r];
 }
 
-// Part of row block IT of a masked score tile, computed by one wave: column
-// tiles jt = J0, J0 + JS, ...  P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for
-// n <= m, 0 above the diagonal (tiles left of the diagonal need no mask).
-template <typename T, int D, int IT, int J0, int JS>
-__device__ inline void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f, int lane) {
+// Row block it (the wave index) of a masked score tile, all four column
+// tiles: P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for n <= m, 0 above the
+// diagonal.  Tiles above the diagonal are computed and discarded: the wave
+// owning the last row block has four tiles to compute in any case, and the
+// code stays free of branches.
+template <typename T, int D>
+__device__ __forceinline__ void score_tile(T* P, const T* Lt, const T* Rt, const float* G, float f,
+                                           int it, int lane) {
   using TA = Tile<T, CB>;
   using TD = Tile<T, D>;
-  constexpr int NJ = (CB / 16 - J0 + JS - 1) / JS;
-  f32x4 c[NJ];
+  using F = Frag<T>;
+  f32x4 c[CB / 16];
 #pragma unroll
-  for (int q = 0; q < NJ; ++q) c[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  score_row<T, TD, TD, IT, J0, JS, D>(c, Lt, Rt, lane);
-  const f32x4 Gm = row_vec(G, IT * 16, lane);
+  for (int jt = 0; jt < CB / 16; ++jt) c[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+  for (int k = 0; k < D; k += F::KSTEP) {
+    const typename F::V a = F::template kc<TD>(Lt, it * 16, k, lane);
 #pragma unroll
-  for (int q = 0; q < NJ; ++q) {
-    const int jt = J0 + q * JS;
+    for (int jt = 0; jt < CB / 16; ++jt) F::mma(c[jt], a, F::template kc<TD>(Rt, jt * 16, k, lane));
+  }
+  const f32x4 Gm = row_vec(G, it * 16, lane);
+#pragma unroll
+  for (int jt = 0; jt < CB / 16; ++jt) {
     const int n = jt * 16 + acc_col(lane);
-    const float Gn = jt <= IT ? G[n] : 0.f;
+    const float Gn = G[n];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int m = IT * 16 + acc_row(lane, r);
-      float x = 0.f;
-      if (jt < IT) x = c[q][r] * __expf(Gm[r] - Gn) * f;
-      else if (jt == IT) x = n <= m ? c[q][r] * __expf(Gm[r] - Gn) * f : 0.f;
-      P[TA::at(m, n)] = Elem<T>::from_f(x);
+      const int m = it * 16 + acc_row(lane, r);
+      P[TA::at(m, n)] = Elem<T>::from_f(n <= m ? c[jt][r] * __expf(Gm[r] - Gn) * f : 0.f);
     }
   }
 }
 
-// The NW waves of a workgroup split the masked score tile: row block w % 4,
-// and with eight waves every other column tile (parity w / 4).
-template <typename T, int D, int NW>
-__device__ inline void score_tile(T* P, const T* Lt, const T* Rt, const float* G, float f, int w, int lane) {
-  if constexpr (NW == 4) {
-    switch (w) {
-      case 0: score_block<T, D, 0, 0, 1>(P, Lt, Rt, G, f, lane); break;
-      case 1: score_block<T, D, 1, 0, 1>(P, Lt, Rt, G, f, lane); break;
-      case 2: score_block<T, D, 2, 0, 1>(P, Lt, Rt, G, f, lane); break;
-      default: score_block<T, D, 3, 0, 1>(P, Lt, Rt, G, f, lane); break;
-    }
-  } else {
-    switch (w) {
-      case 0: score_block<T, D, 0, 0, 2>(P, Lt, Rt, G, f, lane); break;
-      case 1: score_block<T, D, 1, 0, 2>(P, Lt, Rt, G, f, lane); break;
-      case 2: score_block<T, D, 2, 0, 2>(P, Lt, Rt, G, f, lane); break;
-      case 3: score_block<T, D, 3, 0, 2>(P, Lt, Rt, G, f, lane); break;
-      case 4: score_block<T, D, 0, 1, 2>(P, Lt, Rt, G, f, lane); break;
-      case 5: score_block<T, D, 1, 1, 2>(P, Lt, Rt, G, f, lane); break;
-      case 6: score_block<T, D, 2, 1, 2>(P, Lt, Rt, G, f, lane); break;
-      default: score_block<T, D, 3, 1, 2>(P, Lt, Rt, G, f, lane); break;
-    }
-  }
+// The same as an out-of-line call: the reverse-order kernel keeps its score
+// phase in a separate register allocation (its chunk loop holds two states'
+// worth of registers).
+template <typename T, int D>
+__device__ __attribute__((noinline)) void score_tile_call(T* P, const T* Lt, const T* Rt,
+                                                          const float* G, float f, int it, int lane) {
+  score_tile<T, D>(P, Lt, Rt, G, f, it, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -489,18 +477,21 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     put<T, D>(sm.V, pv, nullptr, t);
     __syncthreads();
     const float GL = sm.meta.G[CB - 1];
-    if (c + 1 < c_end) {
+    // the next chunk's rows are loaded one tile at a time between the phases
+    // of this chunk, so that the loads do not queue up behind each other
+    const bool more = c + 1 < c_end;
+    if (more) {
       cs.resolve(sq, c + 1, replay_row, g, H, h, t);
       fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
-      fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     }
     // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    score_tile<T, D, C::NW>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+    score_tile<T, D>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+    if (more) fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
     __syncthreads();
     // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V)
-#pragma unroll 2
+#pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
+      if (it == 1 && more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
       f32x4 acc[C::CPW];
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -600,19 +591,21 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
     put<T, D>(sm.Q, pq, nullptr, t);
     __syncthreads();
     const float GL = sm.meta.G[CB - 1];
-    if (c + 1 < c_end) {
+    // the next chunk's rows, one tile at a time between the phases
+    const bool more = c + 1 < c_end;
+    if (more) {
       cs.resolve(sq, c + 1, replay_row, g, H, h, t);
-      fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
-      fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
       fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
     }
     // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    score_tile<T, D, C::NW>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    score_tile<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    if (more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     __syncthreads();
     // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
-#pragma unroll 2
+#pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
+      if (it == 1 && more) fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
+      if (it == 2 && more) fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
       f32x4 acc[C::CPW];
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -741,10 +734,10 @@ __device__ __forceinline__ void bwd_revorder_side(
     }
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i]; wave w computes row block w
-    if (side) score_tile<T, D, C::NW>(sm.P, sm.dO, sm.V, sm.meta.G, scale, w, lane);
-    else score_tile<T, D, C::NW>(sm.P, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+    if (side) score_tile_call<T, D>(sm.P, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    else score_tile_call<T, D>(sm.P, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     __syncthreads();
-#pragma unroll 2
+#pragma unroll 1
     for (int jt = 0; jt < CB / 16; ++jt) {
       // side 0: acc = diag(x) K dS + scale A^T dO ; side 1: acc = diag(x) V dS^T + dA^T Q
       // (A and dA vanish above the diagonal, so the transposed products start at row block jt)

@@ -173,20 +173,6 @@ __device__ inline void tile_cols(f32x4* c, const T* A, int am, const T* B, int b
   }
 }
 
-// Masked score row block IT: c[q] += L[16 IT.., :] R[16 jt.., :]^T for the
-// column tiles jt = J0 + q JS <= IT (both operands k-contiguous over the head
-// dimension, K = D), the L fragment shared across the tiles.
-template <typename T, typename LL, typename LR, int IT, int J0, int JS, int K>
-__device__ inline void score_row(f32x4* c, const T* Lt, const T* Rt, int lane) {
-  using F = Frag<T>;
-#pragma unroll
-  for (int k = 0; k < K; k += F::KSTEP) {
-    const typename F::V a = F::template kc<LL>(Lt, IT * 16, k, lane);
-#pragma unroll
-    for (int jt = J0, q = 0; jt <= IT; jt += JS, ++q) F::mma(c[q], a, F::template kc<LR>(Rt, jt * 16, k, lane));
-  }
-}
-
 // S[j NT + i] += A_i * diag(s) * B_j for the state tiles of a wave: A_i is
 // k-major with origin column 16 i, B_j k-major with origin column bn + 16 j
 // and its row k scaled by s[k]; each fragment is loaded once per k step.
