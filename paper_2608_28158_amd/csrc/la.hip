@@ -94,13 +94,23 @@ __device__ inline ChunkRows chunk_rows(const SeqInfo& sq, int c) {
   return cr;
 }
 
+// How NTH threads split the 16-byte pieces of a [64][D] chunk tile.
+template <typename T, int D, int NTH>
+struct Stg {
+  static constexpr int NTHR = NTH;
+  static constexpr int VE = 16 / sizeof(T);   // elements per 16-byte vector
+  static constexpr int VPR = D / VE;          // vectors per row
+  static constexpr int NV = CB * VPR / NTH;   // vectors per thread per tile
+  using TD = Tile<T, D>;
+};
+
 // This thread's rows of one chunk (a row's d-range is split over VPR
 // threads), each as row * 4 + kind; resolved for chunks that are not fast.
-template <typename T, int D>
+template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
 struct ChunkRefs {
-  int rk[Cfg<T, D>::NV];
+  int rk[Stg<T, D, NTH>::NV];
   __device__ inline void resolve(const SeqInfo& seq, int c, const int32_t* replay_row, int t) {
-    using C = Cfg<T, D>;
+    using C = Stg<T, D, NTH>;
 #pragma unroll
     for (int i = 0; i < C::NV; ++i) {
       const RowRef rr = pos_row(seq, c * CB + (t + i * C::NTHR) / C::VPR, replay_row);
@@ -110,9 +120,9 @@ struct ChunkRefs {
 };
 
 // dst[row][d] = src[row][d] (* scale[row] if scale != nullptr)
-template <typename T, int D>
+template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
 __device__ inline void put(T* dst, const Vec16* src, const float* scale, int t) {
-  using C = Cfg<T, D>;
+  using C = Stg<T, D, NTH>;
 #pragma unroll
   for (int i = 0; i < C::NV; ++i) {
     const int idx = t + i * C::NTHR;
@@ -138,10 +148,10 @@ struct ChunkMeta {
 
 // Where this thread's rows of one chunk live, resolved one chunk ahead: the
 // rows it stages (all threads) and, for wave 0, row t of the chunk with its g.
-template <typename T, int D>
+template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
 struct ChunkSrc {
   ChunkRows cr;
-  ChunkRefs<T, D> refs;
+  ChunkRefs<T, D, NTH> refs;
   RowRef mr;
   float gv;
   __device__ inline void resolve(const SeqInfo& seq, int c, const int32_t* replay_row,
@@ -157,10 +167,10 @@ struct ChunkSrc {
 
 // This thread's 16-byte pieces of one chunk tile of src (rows of kind below
 // min_kind read as zero).
-template <typename T, int D>
-__device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkSrc<T, D>& cs,
+template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
+__device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkSrc<T, D, NTH>& cs,
                              int H, int h, int t, int min_kind) {
-  using C = Cfg<T, D>;
+  using C = Stg<T, D, NTH>;
   if (cs.cr.fast) {
     const T* base = src + (static_cast<int64_t>(cs.cr.row0) * H + h) * D;
 #pragma unroll
@@ -182,8 +192,8 @@ __device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkS
 
 // Wave 0 (lane t = row t): publishes the row table and G of the chunk whose
 // sources are in cs; returns G_t and G_last.
-template <typename T, int D>
-__device__ inline void meta_publish(ChunkMeta& m, const ChunkSrc<T, D>& cs, int t, float& Gt,
+template <typename T, int D, int NTH>
+__device__ inline void meta_publish(ChunkMeta& m, const ChunkSrc<T, D, NTH>& cs, int t, float& Gt,
                                     float& GL) {
   m.rowk[t] = cs.mr.row * 4 + cs.mr.kind;
   const float x = wave_prefix_sum(cs.gv, t);
@@ -284,7 +294,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   __shared__ T Ys[Tile<T, D>::SIZE];
   __shared__ ChunkMeta meta;
   const int side = side0 + static_cast<int>(blockIdx.z);
-  const int b = blk_order[blockIdx.x], h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const SeqInfo sq = seq_info(seq_tab + bk[BLK_SEQ] * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
@@ -447,7 +457,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ FwdSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x], h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
@@ -559,7 +569,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ BfSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x], h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
@@ -650,93 +660,44 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
 }
 
 // ---------------------------------------------------------------------------
-// backward, reverse order (needs dS_{c+1}: chunks backward).  Each (block,
-// head) runs as two workgroups that share the chunk rows through the caches:
-//   side 0: dv = diag(exp(G_last - G)) K dS + scale A^T dO, holding dS;
-//   side 1: dk = diag(exp(G_last - G)) V dS^T + dA^T Q, holding dS^T, plus
-//           k.dk per row and the local suffix sums of dg.
-// Both sides run the adjoint recurrence
+// backward, reverse order (needs dS_{c+1}: chunks backward).  One workgroup of
+// two halves per (block, head), sharing the chunk tiles in LDS:
+//   waves 0..3 (side 0): dv = diag(exp(G_last - G)) K dS + scale A^T dO,
+//                        holding dS;
+//   waves 4..7 (side 1): dk = diag(exp(G_last - G)) V dS^T + dA^T Q, holding
+//                        dS^T, plus k.dk per row and the local suffix sums of
+//                        dg.
+// Each half runs the adjoint recurrence
 //   dS_c = exp(G_last) dS_{c+1} + Q^T diag(exp(G) scale) dO
-// in their own layout.  Workgroup ids are grouped by 16: ids 16j..16j+7 are
-// side 0 of pairs 8j..8j+7 and ids 16j+8..16j+15 their side 1, so the two
-// sides of a pair are dispatched together (and land on the same XCD when
-// dispatch is round-robin over eight XCDs).
+// in its own layout.
 // ---------------------------------------------------------------------------
+// Two score tiles fit the LDS of a CU in bf16 only; in fp32 the halves take
+// turns with one tile (score A, dv rows, score dA, dk rows).
 template <typename T, int D>
 struct BrSmem {
   using C = Cfg<T, D>;
-  T Q[Tile<T, D>::SIZE];     // own rows
+  static constexpr int NP = sizeof(T) == 2 ? 2 : 1;
+  T Q[Tile<T, D>::SIZE];       // own rows
   T K[Tile<T, D>::SIZE];
-  T V[Tile<T, D>::SIZE];     // side 1 only
-  T dO[Tile<T, D>::SIZE];    // own rows
-  T P[Tile<T, CB>::SIZE];    // side 0: A = Q K^T masked; side 1: dA = scale (dO V^T) masked
-  ChunkMeta meta;  // x = exp(G_last - G), y = exp(G) * scale
+  T V[Tile<T, D>::SIZE];
+  T dO[Tile<T, D>::SIZE];      // own rows
+  T P[NP][Tile<T, CB>::SIZE];  // A = Q K^T masked; dA = scale (dO V^T) masked
+  ChunkMeta meta;             // x = exp(G_last - G), y = exp(G) * scale
   float rk[C::NW][CB];
 };
 
+// Output rows and adjoint update of one chunk for one half of the workgroup.
 template <typename T, int D, int SIDE>
-__device__ __forceinline__ void bwd_revorder_side(
-    BrSmem<T, D>& sm, int pair, const int32_t* __restrict__ seq_tab,
-    const int32_t* __restrict__ blk_tab, const int32_t* __restrict__ blk_order,
-    const int32_t* __restrict__ replay_row, int H, float scale,
-    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-    const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
-    const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
-    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb) {
+__device__ __forceinline__ void bwd_revorder_rows(
+    BrSmem<T, D>& sm, f32x4* dS, const ChunkRows& cur, const SeqInfo& sq, int c, int H, int h,
+    float scale, float GL, int w, int lane, T* __restrict__ dk, T* __restrict__ dv,
+    float* __restrict__ rep_grad) {
   using C = Cfg<T, D>;
   constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
   constexpr bool side = SIDE == 1;
-  const int b = blk_order[pair / H], h = pair % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int col0 = C::CPW * w * 16;
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int li = bk[BLK_SEQ];
-  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
-  const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
-  const int64_t DD = static_cast<int64_t>(D) * D;
-  // side 0: dS   rows (dk), columns (dv) of the wave's strips
-  // side 1: dS^T rows (dv), columns (dk) of the wave's strips
-  f32x4 dS[NS];
-  state_load<D, C::CPW>(dS, dS_end + (static_cast<int64_t>(b) * H + h) * DD, side == 1, w, lane);
-  float carry = 0.f;  // side 1: sum of (q.dq - k.dk) over the later chunks of the block
-  ChunkSrc<T, D> cs;
-  Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  cs.resolve(sq, c_last, replay_row, g, H, h, t);
-  fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
-  fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
-  if (side) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
-  // side 1, wave 0: q.dq of row t of the chunk, one chunk ahead
-  const float* rq_h = rq + (static_cast<int64_t>(sq.chunk_off) * CB + t) * H + h;
-  float rq_next = side && t < CB ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
-  for (int c = c_last; c >= c0; --c) {
-    if (t < CB) {
-      float Gt, GLw;
-      meta_publish(sm.meta, cs, t, Gt, GLw);
-      sm.meta.x[t] = __expf(GLw - Gt);
-      sm.meta.y[t] = __expf(Gt) * scale;
-    }
-    const ChunkRows cur = cs.cr;
-    const float rq_cur = rq_next;
-    put<T, D>(sm.Q, pq, nullptr, t);
-    put<T, D>(sm.K, pk, nullptr, t);
-    if (side) put<T, D>(sm.V, pv, nullptr, t);
-    put<T, D>(sm.dO, pd, nullptr, t);
-    __syncthreads();
-    const float GL = sm.meta.G[CB - 1];
-    if (c > c0) {
-      cs.resolve(sq, c - 1, replay_row, g, H, h, t);
-      fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
-      fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
-      if (side) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
-      if (side && t < CB) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
-    }
-    // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
-    // M = exp(G_i - G_j) [j <= i]; wave w computes row block w
-    if (side) score_tile_call<T, D>(sm.P, sm.dO, sm.V, sm.meta.G, scale, w, lane);
-    else score_tile_call<T, D>(sm.P, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
-    __syncthreads();
+  const T* P = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];
 #pragma unroll 1
     for (int jt = 0; jt < CB / 16; ++jt) {
       // side 0: acc = diag(x) K dS + scale A^T dO ; side 1: acc = diag(x) V dS^T + dA^T Q
@@ -750,7 +711,7 @@ __device__ __forceinline__ void bwd_revorder_side(
       opaque_state<NS>(dS);
       regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, side ? sm.V : sm.K, jt * 16, dS, lane);
       const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
-      tile_cols<T, typename C::TA, true, typename C::TD, C::CPW>(ad, sm.P, jt * 16, side ? sm.Q : sm.dO,
+      tile_cols<T, typename C::TA, true, typename C::TD, C::CPW>(ad, P, jt * 16, side ? sm.Q : sm.dO,
                                                                 col0, k0, CB, lane);
       const float f = side ? 1.f : scale;
       {
@@ -793,9 +754,89 @@ __device__ __forceinline__ void bwd_revorder_side(
       state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(dS, sm.Q, sm.dO, col0, sm.meta.y, lane);
     else
       state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(dS, sm.dO, sm.Q, col0, sm.meta.y, lane);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_revorder(
+    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
+    const int32_t* __restrict__ blk_order, const int32_t* __restrict__ replay_row, int H,
+    float scale, const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
+    const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
+    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb) {
+  using C = Cfg<T, D>;
+  constexpr int NTH = 2 * C::NTHR;
+  using SG = Stg<T, D, NTH>;
+  constexpr int NS = C::CPW * C::NT;
+  constexpr int RG = 2 * D + 1;
+  __shared__ BrSmem<T, D> sm;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, tid = threadIdx.x;
+  const int side = tid >= C::NTHR ? 1 : 0;  // uniform over a wave
+  const int t = tid - side * C::NTHR, lane = tid & 63, w = t >> 6;
+  const int32_t* bk = blk_tab + b * BLK_WORDS;
+  const int li = bk[BLK_SEQ];
+  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
+  const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
+  const int64_t DD = static_cast<int64_t>(D) * D;
+  // side 0: dS   rows (dk), columns (dv) of the wave's strips
+  // side 1: dS^T rows (dv), columns (dk) of the wave's strips
+  f32x4 dS[NS];
+  state_load<D, C::CPW>(dS, dS_end + (static_cast<int64_t>(b) * H + h) * DD, side == 1, w, lane);
+  float carry = 0.f;  // side 1: sum of (q.dq - k.dk) over the later chunks of the block
+  ChunkSrc<T, D, NTH> cs;
+  Vec16 pq[SG::NV], pk[SG::NV], pv[SG::NV], pd[SG::NV];
+  cs.resolve(sq, c_last, replay_row, g, H, h, tid);
+  fetch<T, D, NTH>(pq, q, cs, H, h, tid, ROW_OWN);
+  fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
+  fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
+  fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
+  // side 1, first wave: q.dq of row t of the chunk, one chunk ahead
+  const bool sw0 = side == 1 && t < CB;
+  const float* rq_h = rq + (static_cast<int64_t>(sq.chunk_off) * CB + t) * H + h;
+  float rq_next = sw0 ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
+  for (int c = c_last; c >= c0; --c) {
+    if (tid < CB) {
+      float Gt, GLw;
+      meta_publish(sm.meta, cs, tid, Gt, GLw);
+      sm.meta.x[tid] = __expf(GLw - Gt);
+      sm.meta.y[tid] = __expf(Gt) * scale;
+    }
+    const ChunkRows cur = cs.cr;
+    const float rq_cur = rq_next;
+    put<T, D, NTH>(sm.Q, pq, nullptr, tid);
+    put<T, D, NTH>(sm.K, pk, nullptr, tid);
+    put<T, D, NTH>(sm.V, pv, nullptr, tid);
+    put<T, D, NTH>(sm.dO, pd, nullptr, tid);
     __syncthreads();
-    // side 1, wave 0: local suffix sums of q.dq - k.dk, one row per lane
-    if (side && t < CB) {
+    const float GL = sm.meta.G[CB - 1];
+    if (c > c0) {
+      cs.resolve(sq, c - 1, replay_row, g, H, h, tid);
+      fetch<T, D, NTH>(pq, q, cs, H, h, tid, ROW_OWN);
+      fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
+      fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
+      fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
+      if (sw0) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
+    }
+    // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
+    // M = exp(G_i - G_j) [j <= i]; wave w of each half computes row block w
+    if constexpr (BrSmem<T, D>::NP == 2) {
+      if (side) score_tile<T, D>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      else score_tile<T, D>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      __syncthreads();
+      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      else bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+    } else {
+      if (!side) score_tile<T, D>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      __syncthreads();
+      if (!side) bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      __syncthreads();
+      if (side) score_tile<T, D>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      __syncthreads();
+      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+    }
+    __syncthreads();
+    // side 1, first wave: local suffix sums of q.dq - k.dk, one row per lane
+    if (sw0) {
       const int kind = (sm.meta.rowk[t] & 3);
       float x = 0.f;
       if (kind != ROW_PAD) {
@@ -813,28 +854,6 @@ __device__ __forceinline__ void bwd_revorder_side(
     }
   }
   if (side && t == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
-}
-
-
-template <typename T, int D>
-__global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_revorder(
-    const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ blk_order,
-    const int32_t* __restrict__ replay_row, int H, int n_pairs, float scale,
-    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-    const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
-    const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
-    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb) {
-  __shared__ BrSmem<T, D> sm;
-  const int id = blockIdx.x;
-  const int pair = (id >> 4) * 8 + (id & 7);
-  if (pair >= n_pairs) return;  // whole workgroup, before any barrier
-  if ((id >> 3) & 1)
-    bwd_revorder_side<T, D, 1>(sm, pair, seq_tab, blk_tab, blk_order, replay_row, H, scale, q, k, v, g, dO,
-                               dS_end, rq, dk, dv, dg, rep_grad, Rb);
-  else
-    bwd_revorder_side<T, D, 0>(sm, pair, seq_tab, blk_tab, blk_order, replay_row, H, scale, q, k, v, g, dO,
-                               dS_end, rq, dk, dv, dg, rep_grad, Rb);
 }
 
 // ---------------------------------------------------------------------------
@@ -1045,7 +1064,7 @@ int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, 
                     float* dSb, float* U, float* gam, int side0, int n_sides, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   ProfScope ps("k_blocksum", s);
-  hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk, H, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
+  hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk * H, 1, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
                      B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                      static_cast<const T*>(k), static_cast<const T*>(v),
                      static_cast<const T*>(dO), g, dSb, U, gam, side0);
@@ -1082,7 +1101,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
   {
     ProfScope ps("k_fwd_block", s);
-    hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
+    hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g, S0, S_end,
                        static_cast<T*>(o));
@@ -1138,21 +1157,19 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   if (int rc = hip_check("k_bwd_blockscan")) return rc;
   {
     ProfScope ps("k_bwd_fwdorder", s);
-    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk, H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
+    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq);
   }
   if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
-    const int n_pairs = L.n_blk * H;
-    const unsigned n_wg = static_cast<unsigned>((n_pairs + 7) / 8) * 16u;
     ProfScope ps("k_bwd_revorder", s);
-    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(n_wg), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.blk_order, B.replay_row, H, n_pairs, scale, static_cast<const T*>(q),
-                       static_cast<const T*>(k), static_cast<const T*>(v), g,
-                       static_cast<const T*>(dO), dS_end, rq, static_cast<T*>(dk),
-                       static_cast<T*>(dv), dg, rep_grad, Rb);
+    hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk * H), dim3(2 * Cfg<T, D>::NTHR), 0, s,
+                       B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale,
+                       static_cast<const T*>(q), static_cast<const T*>(k),
+                       static_cast<const T*>(v), g, static_cast<const T*>(dO), dS_end, rq,
+                       static_cast<T*>(dk), static_cast<T*>(dv), dg, rep_grad, Rb);
   }
   if (int rc = hip_check("k_bwd_revorder")) return rc;
   {
