@@ -234,8 +234,9 @@ __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) 
 // tiles: P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for n <= m, 0 above the
 // diagonal.  Tiles above the diagonal are computed and discarded: the wave
 // owning the last row block has four tiles to compute in any case, and the
-// code stays free of branches.
-template <typename T, int D>
+// code stays free of branches.  With PT the tile is stored transposed
+// (P[n][m] holds the value of row m, column n).
+template <typename T, int D, bool PT = false>
 __device__ __forceinline__ void score_tile(T* P, const T* Lt, const T* Rt, const float* G, float f,
                                            int it, int lane) {
   using TA = Tile<T, CB>;
@@ -246,20 +247,29 @@ __device__ __forceinline__ void score_tile(T* P, const T* Lt, const T* Rt, const
   for (int jt = 0; jt < CB / 16; ++jt) c[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
   for (int k = 0; k < D; k += F::KSTEP) {
+    // all five reads of the step are issued before its first product
     const typename F::V a = F::template kc<TD>(Lt, it * 16, k, lane);
+    typename F::V b[CB / 16];
 #pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) F::mma(c[jt], a, F::template kc<TD>(Rt, jt * 16, k, lane));
+    for (int jt = 0; jt < CB / 16; ++jt) b[jt] = F::template kc<TD>(Rt, jt * 16, k, lane);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int jt = 0; jt < CB / 16; ++jt) F::mma(c[jt], a, b[jt]);
   }
   const f32x4 Gm = row_vec(G, it * 16, lane);
 #pragma unroll
   for (int jt = 0; jt < CB / 16; ++jt) {
     const int n = jt * 16 + acc_col(lane);
     const float Gn = G[n];
+    f32x4 v;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = it * 16 + acc_row(lane, r);
-      P[TA::at(m, n)] = Elem<T>::from_f(n <= m ? c[jt][r] * __expf(Gm[r] - Gn) * f : 0.f);
+      v[r] = n <= m ? c[jt][r] * __expf(Gm[r] - Gn) * f : 0.f;
+      if (!PT) P[TA::at(m, n)] = Elem<T>::from_f(v[r]);
     }
+    // transposed: the lane's four rows m are contiguous in row n of P^T
+    if (PT) Vec4<T>::store(P + TA::at(n, it * 16 + acc_row(lane, 0)), v);
   }
 }
 
@@ -683,10 +693,13 @@ struct BrSmem {
   T dO[Tile<T, D>::SIZE];      // own rows
   T P[NP][Tile<T, CB>::SIZE];  // A = Q K^T masked; dA = scale (dO V^T) masked
   ChunkMeta meta;             // x = exp(G_last - G), y = exp(G) * scale
-  float rk[C::NW][CB];
+  float rk[4 * C::NW][CB];    // partial k.dk of each row, per wave and lane group
 };
 
 // Output rows and adjoint update of one chunk for one half of the workgroup.
+// The products run with their operands swapped, so that lane (g, i) of a wave
+// holds row 16 jt + i of the output at columns col0 + 16 j + 4g .. + 3: one
+// 8-byte (bf16) or 16-byte (float) store per strip, one row per lane.
 template <typename T, int D, int SIDE>
 __device__ __forceinline__ void bwd_revorder_rows(
     BrSmem<T, D>& sm, f32x4* dS, const ChunkRows& cur, const SeqInfo& sq, int c, int H, int h,
@@ -697,63 +710,65 @@ __device__ __forceinline__ void bwd_revorder_rows(
   constexpr int RG = 2 * D + 1;
   constexpr bool side = SIDE == 1;
   const int col0 = C::CPW * w * 16;
-  const T* P = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];
+  const T* PT = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];  // transposed score tile
+  const int g4 = 4 * (lane >> 4);
 #pragma unroll 1
-    for (int jt = 0; jt < CB / 16; ++jt) {
-      // side 0: acc = diag(x) K dS + scale A^T dO ; side 1: acc = diag(x) V dS^T + dA^T Q
-      // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
-      f32x4 acc[C::CPW], ad[C::CPW];
+  for (int jt = 0; jt < CB / 16; ++jt) {
+    // side 0: dv = diag(x) K dS + scale A^T dO ; side 1: dk = diag(x) V dS^T + dA^T Q
+    // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
+    f32x4 acc[C::CPW], ad[C::CPW];
+#pragma unroll
+    for (int j = 0; j < C::CPW; ++j) {
+      acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    opaque_state<NS>(dS);
+    regb_rows<T, typename C::TD, C::NT, C::CPW, true, true>(acc, side ? sm.V : sm.K, jt * 16, dS, lane);
+    const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
+    tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true, true>(
+        ad, PT, jt * 16, side ? sm.Q : sm.dO, col0, k0, CB, lane);
+    const int m = jt * 16 + (lane & 15);
+    const float e = sm.meta.x[m];
+    const float f = side ? 1.f : scale;
+#pragma unroll
+    for (int j = 0; j < C::CPW; ++j) acc[j] = acc[j] * e + f * ad[j];
+    if (side) {
+      // k.dk of row m over this lane's columns; the partial sums of a row
+      // (one per wave and lane group) are added by the suffix step
+      float kd = 0.f;
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) {
-        acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const f32x4 kv = Vec4<T>::load(sm.K + C::TD::at(m, col0 + 16 * j + g4));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) kd += kv[r] * acc[j][r];
       }
-      opaque_state<NS>(dS);
-      regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, side ? sm.V : sm.K, jt * 16, dS, lane);
-      const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
-      tile_cols<T, typename C::TA, true, typename C::TD, C::CPW>(ad, P, jt * 16, side ? sm.Q : sm.dO,
-                                                                col0, k0, CB, lane);
-      const float f = side ? 1.f : scale;
-      {
-        const f32x4 e = row_vec(sm.meta.x, jt * 16, lane);
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j) acc[j] = acc[j] * e + f * ad[j];
-      }
-      f32x4 kd = {0.f, 0.f, 0.f, 0.f};
-      if (side) {
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j) kd += ColRead<T>::template get<typename C::TD>(sm.K, jt * 16, col0 + 16 * j, lane) * acc[j];
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = jt * 16 + acc_row(lane, r);
-        const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (sm.meta.rowk[m] & 3);
-        if (side) {
-          const float s = sum16(kd[r]);
-          if ((lane & 15) == 0) sm.rk[w][m] = s;
-        }
-        if (cur.fast || kind == ROW_OWN) {
-          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (sm.meta.rowk[m] >> 2);
-          T* dst = (side ? dk : dv) + (row * H + h) * D + col0 + acc_col(lane);
-#pragma unroll
-          for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r]);
-        } else if (kind == ROW_REPLAY) {
-          float* dst = rep_grad + ((static_cast<int64_t>(sq.replay_off) + c * CB + m) * H + h) * RG + (side ? 0 : D) +
-                       col0 + acc_col(lane);
-#pragma unroll
-          for (int j = 0; j < C::CPW; ++j) dst[16 * j] = acc[j][r];
-        }
-      }
+      sm.rk[w * 4 + (lane >> 4)][m] = kd;
     }
-    // side 0: dS   <- exp(G_last) dS   + Q^T  diag(exp(G) scale) dO
-    // side 1: dS^T <- exp(G_last) dS^T + dO^T diag(exp(G) scale) Q
-    const float dec = __expf(GL);
+    const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (sm.meta.rowk[m] & 3);
+    if (kind == ROW_OWN) {
+      const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (sm.meta.rowk[m] >> 2);
+      T* dst = (side ? dk : dv) + (row * H + h) * D + col0 + g4;
 #pragma unroll
-    for (int i = 0; i < NS; ++i) dS[i] *= dec;
-    if (!side)
-      state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(dS, sm.Q, sm.dO, col0, sm.meta.y, lane);
-    else
-      state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(dS, sm.dO, sm.Q, col0, sm.meta.y, lane);
+      for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j]);
+    } else if (kind == ROW_REPLAY) {
+      // rows of 2D + 1 floats: no vector alignment
+      float* dst = rep_grad + ((static_cast<int64_t>(sq.replay_off) + c * CB + m) * H + h) * RG +
+                   (side ? 0 : D) + col0 + g4;
+#pragma unroll
+      for (int j = 0; j < C::CPW; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[16 * j + r] = acc[j][r];
+    }
+  }
+  // side 0: dS   <- exp(G_last) dS   + Q^T  diag(exp(G) scale) dO
+  // side 1: dS^T <- exp(G_last) dS^T + dO^T diag(exp(G) scale) Q
+  const float dec = __expf(GL);
+#pragma unroll
+  for (int i = 0; i < NS; ++i) dS[i] *= dec;
+  if (!side)
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, sm.Q, sm.dO, col0, sm.meta.y, lane);
+  else
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, sm.dO, sm.Q, col0, sm.meta.y, lane);
 }
 
 template <typename T, int D>
@@ -820,17 +835,17 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i]; wave w of each half computes row block w
     if constexpr (BrSmem<T, D>::NP == 2) {
-      if (side) score_tile<T, D>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
-      else score_tile<T, D>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      if (side) score_tile<T, D, true>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      else score_tile<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
       else bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
     } else {
-      if (!side) score_tile<T, D>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      if (!side) score_tile<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
       __syncthreads();
       if (!side) bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
       __syncthreads();
-      if (side) score_tile<T, D>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      if (side) score_tile<T, D, true>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
     }
@@ -842,7 +857,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       if (kind != ROW_PAD) {
         float rks = 0.f;
 #pragma unroll
-        for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][t];
+        for (int i = 0; i < 4 * C::NW; ++i) rks += sm.rk[i][t];
         x = rq_cur - rks;
       }
       x = wave_suffix_sum(x, t);

@@ -41,6 +41,27 @@ template <> struct Elem<bf16> {
   __device__ static inline bf16 from_f(float x) { return static_cast<bf16>(x); }  // RNE
 };
 
+// Four consecutive elements as one float32x4 (one 8-byte bf16 or 16-byte
+// float access; the address must be aligned to that size).
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  __device__ static inline f32x4 load(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  __device__ static inline void store(float* p, const f32x4& v) { *reinterpret_cast<f32x4*>(p) = v; }
+};
+template <> struct Vec4<bf16> {
+  __device__ static inline f32x4 load(const bf16* p) {
+    const bf16x4 b = *reinterpret_cast<const bf16x4*>(p);
+    return f32x4{static_cast<float>(b[0]), static_cast<float>(b[1]), static_cast<float>(b[2]),
+                 static_cast<float>(b[3])};
+  }
+  __device__ static inline void store(bf16* p, const f32x4& v) {
+    bf16x4 b;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) b[e] = static_cast<bf16>(v[e]);
+    *reinterpret_cast<bf16x4*>(p) = b;
+  }
+};
+
 // LDS tile layout: 64 rows of COLS elements, row-major, each row padded by
 // 16 bytes.  Addresses are affine in (r, c), so every fragment read is a
 // per-lane base plus an immediate offset.  With the padding, 16-byte row
@@ -161,34 +182,68 @@ __device__ inline void tile(f32x4& c, const T* A, int am, const T* B, int bn, in
 
 // c[j] += A * B_j for the NJ output tiles of one row block (origins bn + 16 j),
 // the A fragment shared; B is k-major.  k runs over [k0, K).
-template <typename T, typename LA, bool A_KM, typename LB, int NJ>
+// With SWAP the operands of each product trade places, which leaves the
+// transposed tile (B_j^T A^T) in c[j]: lane (g, i) then holds row i, columns
+// 4g..4g+3 of A B_j.  With EAGER all fragments of a step are requested before
+// its first product (more registers live, no wait per product).
+template <typename T, typename LA, bool A_KM, typename LB, int NJ, bool SWAP = false, bool EAGER = false>
 __device__ inline void tile_cols(f32x4* c, const T* A, int am, const T* B, int bn, int k0, int K,
                                  int lane) {
   using F = Frag<T>;
 #pragma unroll 1
   for (int k = k0; k < K; k += F::KSTEP) {
     const typename F::V a = A_KM ? F::template km<LA>(A, k, am, lane) : F::template kc<LA>(A, am, k, lane);
+    if constexpr (EAGER) {
+      typename F::V b[NJ];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) F::mma(c[j], a, F::template km<LB>(B, k, bn + 16 * j, lane));
+      for (int j = 0; j < NJ; ++j) b[j] = F::template km<LB>(B, k, bn + 16 * j, lane);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        if (SWAP) F::mma(c[j], b[j], a);
+        else F::mma(c[j], a, b[j]);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const typename F::V b = F::template km<LB>(B, k, bn + 16 * j, lane);
+        if (SWAP) F::mma(c[j], b, a);
+        else F::mma(c[j], a, b);
+      }
+    }
   }
 }
 
 // S[j NT + i] += A_i * diag(s) * B_j for the state tiles of a wave: A_i is
 // k-major with origin column 16 i, B_j k-major with origin column bn + 16 j
 // and its row k scaled by s[k]; each fragment is loaded once per k step.
-template <typename T, typename LA, typename LB, int NT, int CPW>
+template <typename T, typename LA, typename LB, int NT, int CPW, bool EAGER = false>
 __device__ inline void state_update(f32x4* S, const T* A, const T* B, int bn, const float* s, int lane) {
   using F = Frag<T>;
 #pragma unroll 1
   for (int k = 0; k < CB; k += F::KSTEP) {
     typename F::V b[CPW];
+    if constexpr (EAGER) {
+      // all fragments of the step are requested before its first product
+      typename F::V a[NT];
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) b[j] = F::template km_scaled<LB>(B, k, bn + 16 * j, s, lane);
+      for (int i = 0; i < NT; ++i) a[i] = F::template km<LA>(A, k, i * 16, lane);
 #pragma unroll
-    for (int i = 0; i < NT; ++i) {
-      const typename F::V a = F::template km<LA>(A, k, i * 16, lane);
+      for (int j = 0; j < CPW; ++j) b[j] = F::template km_scaled<LB>(B, k, bn + 16 * j, s, lane);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int j = 0; j < CPW; ++j) F::mma(S[j * NT + i], a, b[j]);
+      for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int j = 0; j < CPW; ++j) F::mma(S[j * NT + i], a[i], b[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) b[j] = F::template km_scaled<LB>(B, k, bn + 16 * j, s, lane);
+#pragma unroll
+      for (int i = 0; i < NT; ++i) {
+        const typename F::V a = F::template km<LA>(A, k, i * 16, lane);
+#pragma unroll
+        for (int j = 0; j < CPW; ++j) F::mma(S[j * NT + i], a, b[j]);
+      }
     }
   }
 }
@@ -242,14 +297,33 @@ template <> struct RegB<float> {
 
 // acc[j] += A[m0.., :] * B_j over the whole state dimension, B_j being the
 // wave's float32 state strip j (tiles S[j NT + kt]), converted per use.
-template <typename T, typename L, int NT, int CPW>
+// With SWAP the products leave the transposed tiles in acc, EAGER as in
+// tile_cols.
+template <typename T, typename L, int NT, int CPW, bool SWAP = false, bool EAGER = false>
 __device__ inline void regb_rows(f32x4* acc, const T* A, int m0, const f32x4* S, int lane) {
   using R = RegB<T>;
+  if constexpr (EAGER) {
+    typename R::A a[NT / R::KT];
 #pragma unroll
-  for (int kt = 0; kt < NT; kt += R::KT) {
-    const typename R::A a = R::template load<L>(A, m0, kt * 16, lane);
+    for (int kt = 0; kt < NT; kt += R::KT) a[kt / R::KT] = R::template load<L>(A, m0, kt * 16, lane);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int j = 0; j < CPW; ++j) R::mma(acc[j], a, R::pack(S + j * NT + kt));
+    for (int kt = 0; kt < NT; kt += R::KT)
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) {
+        if (SWAP) R::mma(acc[j], R::pack(S + j * NT + kt), a[kt / R::KT]);
+        else R::mma(acc[j], a[kt / R::KT], R::pack(S + j * NT + kt));
+      }
+  } else {
+#pragma unroll
+    for (int kt = 0; kt < NT; kt += R::KT) {
+      const typename R::A a = R::template load<L>(A, m0, kt * 16, lane);
+#pragma unroll
+      for (int j = 0; j < CPW; ++j) {
+        if (SWAP) R::mma(acc[j], R::pack(S + j * NT + kt), a);
+        else R::mma(acc[j], a, R::pack(S + j * NT + kt));
+      }
+    }
   }
 }
 
