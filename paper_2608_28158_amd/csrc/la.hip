@@ -508,7 +508,9 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     score_tile<T, D>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     if (more) fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
     __syncthreads();
-    // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V)
+    // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V), products with
+    // swapped operands: lane (g, i) holds row 16 it + i, columns
+    // col0 + 16 j + 4g .. + 3
 #pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
       if (it == 1 && more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
@@ -516,31 +518,21 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       opaque_state<NS>(S);
-      regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, sm.Q, it * 16, S, lane);
-{
-        const f32x4 e = row_vec(sm.meta.y, it * 16, lane);
+      regb_rows<T, typename C::TD, C::NT, C::CPW, true, true>(acc, sm.Q, it * 16, S, lane);
+      const int m = it * 16 + (lane & 15);
+      {
+        const float e = sm.meta.y[m];
 #pragma unroll
         for (int j = 0; j < C::CPW; ++j) acc[j] *= e;
       }
-      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW>(acc, sm.A, it * 16, sm.V, col0, 0,
-                                                                 (it + 1) * 16, lane);
-      if (cur.fast) {
-        T* dst = o + (static_cast<int64_t>(cur.row0) * H + h) * D + col0 + acc_col(lane);
+      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true, true>(
+          acc, sm.A, it * 16, sm.V, col0, 0, (it + 1) * 16, lane);
+      const int rk = cur.fast ? 0 : sm.meta.rowk[m];
+      if (cur.fast || (rk & 3) == ROW_OWN) {
+        const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (rk >> 2);
+        T* dst = o + (row * H + h) * D + col0 + 4 * (lane >> 4);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int j = 0; j < C::CPW; ++j)
-            dst[(it * 16 + acc_row(lane, r)) * H * D + 16 * j] = Elem<T>::from_f(acc[j][r] * scale);
-      } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = it * 16 + acc_row(lane, r);
-          if ((sm.meta.rowk[m] & 3) == ROW_OWN) {
-            T* dst = o + (static_cast<int64_t>((sm.meta.rowk[m] >> 2)) * H + h) * D + col0 + acc_col(lane);
-#pragma unroll
-            for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r] * scale);
-          }
-        }
+        for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j] * scale);
       }
     }
     // S_{c+1} = exp(G_last) S_c + K^T diag(exp(G_last - G)) V
@@ -621,7 +613,9 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
     score_tile<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
     if (more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     __syncthreads();
-    // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq
+    // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq.
+    // Products with swapped operands: lane (g, i) holds row 16 it + i,
+    // columns col0 + 16 j + 4g .. + 3
 #pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
       if (it == 1 && more) fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
@@ -630,28 +624,31 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       opaque_state<NS>(St);
-      regb_rows<T, typename C::TD, C::NT, C::CPW>(acc, sm.dO, it * 16, St, lane);
-{
-        const f32x4 e = row_vec(sm.meta.y, it * 16, lane);
+      regb_rows<T, typename C::TD, C::NT, C::CPW, true>(acc, sm.dO, it * 16, St, lane);
+      const int m = it * 16 + (lane & 15);
+      {
+        const float e = sm.meta.y[m];
 #pragma unroll
         for (int j = 0; j < C::CPW; ++j) acc[j] *= e;
       }
-      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW>(acc, sm.dA, it * 16, sm.K, col0, 0,
-                                                                 (it + 1) * 16, lane);
-      f32x4 qd = {0.f, 0.f, 0.f, 0.f};
+      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true>(acc, sm.dA, it * 16, sm.K, col0,
+                                                                       0, (it + 1) * 16, lane);
+      const int g4 = 4 * (lane >> 4);
+      float qd = 0.f;
 #pragma unroll
-      for (int j = 0; j < C::CPW; ++j) qd += ColRead<T>::template get<typename C::TD>(sm.Q, it * 16, col0 + 16 * j, lane) * acc[j];
+      for (int j = 0; j < C::CPW; ++j) {
+        const f32x4 qv = Vec4<T>::load(sm.Q + C::TD::at(m, col0 + 16 * j + g4));
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = it * 16 + acc_row(lane, r);
-        const float s = sum16(qd[r]);
-        if ((lane & 15) == 0) sm.rq[w][m] = s;
-        if (cur.fast || (sm.meta.rowk[m] & 3) == ROW_OWN) {
-          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (sm.meta.rowk[m] >> 2);
-          T* dst = dq + (row * H + h) * D + col0 + acc_col(lane);
+        for (int r = 0; r < 4; ++r) qd += qv[r] * acc[j][r];
+      }
+      qd = group_sum4(qd);
+      if (lane < 16) sm.rq[w][m] = qd;
+      const int rk = cur.fast ? 0 : sm.meta.rowk[m];
+      if (cur.fast || (rk & 3) == ROW_OWN) {
+        const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (rk >> 2);
+        T* dst = dq + (row * H + h) * D + col0 + g4;
 #pragma unroll
-          for (int j = 0; j < C::CPW; ++j) dst[16 * j] = Elem<T>::from_f(acc[j][r]);
-        }
+        for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j]);
       }
     }
     // S^T <- exp(G_last) S^T + V^T diag(exp(G_last - G)) K

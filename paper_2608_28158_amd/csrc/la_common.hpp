@@ -448,4 +448,20 @@ __device__ inline float lane_value(float x, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
 }
 
+// Sum over the four 16-lane groups of a wave (lanes i, i + 16, i + 32,
+// i + 48), returned to every lane.  v_permlane32_swap exchanges the upper
+// half of its first operand with the lower half of its second; applied to two
+// copies of x, the pair then holds x[l] and x[l ^ 32] in every lane (and
+// likewise for v_permlane16_swap with rows of 16).  Both results of the swap
+// are needed, hence inline asm with two tied operands; the nops keep the
+// swap clear of any VALU read/write hazard.
+__device__ inline float group_sum4(float x) {
+  float a = x, b = x;
+  asm volatile("s_nop 4\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 4" : "+v"(a), "+v"(b));
+  const float y = a + b;
+  float c = y, d = y;
+  asm volatile("s_nop 4\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 4" : "+v"(c), "+v"(d));
+  return c + d;
+}
+
 }  // namespace harts
