@@ -697,11 +697,11 @@ struct BrSmem {
 // The products run with their operands swapped, so that lane (g, i) of a wave
 // holds row 16 jt + i of the output at columns col0 + 16 j + 4g .. + 3: one
 // 8-byte (bf16) or 16-byte (float) store per strip, one row per lane.
-template <typename T, int D, int SIDE>
+template <typename T, int D, int SIDE, typename Hook>
 __device__ __forceinline__ void bwd_revorder_rows(
     BrSmem<T, D>& sm, f32x4* dS, const ChunkRows& cur, const SeqInfo& sq, int c, int H, int h,
     float scale, float GL, int w, int lane, T* __restrict__ dk, T* __restrict__ dv,
-    float* __restrict__ rep_grad) {
+    float* __restrict__ rep_grad, const Hook& hook) {
   using C = Cfg<T, D>;
   constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
@@ -711,6 +711,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
   const int g4 = 4 * (lane >> 4);
 #pragma unroll 1
   for (int jt = 0; jt < CB / 16; ++jt) {
+    hook(jt);
     // side 0: dv = diag(x) K dS + scale A^T dO ; side 1: dk = diag(x) V dS^T + dA^T Q
     // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
     f32x4 acc[C::CPW], ad[C::CPW];
@@ -821,30 +822,36 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     put<T, D, NTH>(sm.dO, pd, nullptr, tid);
     __syncthreads();
     const float GL = sm.meta.G[CB - 1];
-    if (c > c0) {
+    // the next chunk's rows are loaded one tile at a time between the phases
+    // of this chunk, so that the loads overlap the products
+    const bool more = c > c0;
+    if (more) {
       cs.resolve(sq, c - 1, replay_row, g, H, h, tid);
       fetch<T, D, NTH>(pq, q, cs, H, h, tid, ROW_OWN);
-      fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
-      fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
-      fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
       if (sw0) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
     }
+    const auto hook = [&](int jt) {
+      if (more && jt == 1) fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
+      if (more && jt == 3) fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
+    };
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i]; wave w of each half computes row block w
     if constexpr (BrSmem<T, D>::NP == 2) {
       if (side) score_tile<T, D, true>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
       else score_tile<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      if (more) fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
       __syncthreads();
-      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
-      else bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
+      else bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
     } else {
       if (!side) score_tile<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      if (more) fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
       __syncthreads();
-      if (!side) bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      if (!side) bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
       __syncthreads();
       if (side) score_tile<T, D, true>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
       __syncthreads();
-      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
     }
     __syncthreads();
     // side 1, first wave: local suffix sums of q.dq - k.dk, one row per lane
