@@ -709,6 +709,8 @@ __device__ __forceinline__ void bwd_revorder_rows(
   const int col0 = C::CPW * w * 16;
   const T* PT = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];  // transposed score tile
   const int g4 = 4 * (lane >> 4);
+  PackedState<T, C::NT, C::CPW> ps;
+  ps.pack(dS);
 #pragma unroll 1
   for (int jt = 0; jt < CB / 16; ++jt) {
     hook(jt);
@@ -720,8 +722,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
       acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    opaque_state<NS>(dS);
-    regb_rows<T, typename C::TD, C::NT, C::CPW, true, true>(acc, side ? sm.V : sm.K, jt * 16, dS, lane);
+    regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, false>(acc, side ? sm.V : sm.K, jt * 16, ps, lane);
     const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
     tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true, true>(
         ad, PT, jt * 16, side ? sm.Q : sm.dO, col0, k0, CB, lane);

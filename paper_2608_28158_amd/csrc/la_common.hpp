@@ -327,6 +327,43 @@ __device__ inline void regb_rows(f32x4* acc, const T* A, int m0, const f32x4* S,
   }
 }
 
+// A wave's state strips converted once to B operands (for bf16 two state
+// tiles per operand), for several regb_rows_packed calls on an unchanged
+// state.  The converted values are hidden from the optimiser, so that the
+// conversion is not repeated at each use.
+template <typename T, int NT, int CPW>
+struct PackedState {
+  typename RegB<T>::P p[CPW][NT / RegB<T>::KT];
+  __device__ inline void pack(const f32x4* S) {
+    using R = RegB<T>;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+#pragma unroll
+      for (int kt = 0; kt < NT; kt += R::KT) {
+        p[j][kt / R::KT] = R::pack(S + j * NT + kt);
+        asm volatile("" : "+v"(p[j][kt / R::KT]));
+      }
+  }
+};
+
+// regb_rows on a packed state (SWAP, EAGER as there).
+template <typename T, typename L, int NT, int CPW, bool SWAP = false, bool EAGER = false>
+__device__ inline void regb_rows_packed(f32x4* acc, const T* A, int m0, const PackedState<T, NT, CPW>& ps,
+                                        int lane) {
+  using R = RegB<T>;
+  typename R::A a[NT / R::KT];
+#pragma unroll
+  for (int kt = 0; kt < NT; kt += R::KT) a[kt / R::KT] = R::template load<L>(A, m0, kt * 16, lane);
+  if (EAGER) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int kt = 0; kt < NT; kt += R::KT)
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      if (SWAP) R::mma(acc[j], ps.p[j][kt / R::KT], a[kt / R::KT]);
+      else R::mma(acc[j], a[kt / R::KT], ps.p[j][kt / R::KT]);
+    }
+}
+
 // Hides the values of a state from the optimiser (no instructions): values
 // derived from it inside a loop stay inside the loop.
 template <int N>
