@@ -511,14 +511,15 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V), products with
     // swapped operands: lane (g, i) holds row 16 it + i, columns
     // col0 + 16 j + 4g .. + 3
+    PackedState<T, C::NT, C::CPW> ps;
+    ps.pack(S);
 #pragma unroll 1
     for (int it = 0; it < CB / 16; ++it) {
       if (it == 1 && more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
       f32x4 acc[C::CPW];
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      opaque_state<NS>(S);
-      regb_rows<T, typename C::TD, C::NT, C::CPW, true, true>(acc, sm.Q, it * 16, S, lane);
+      regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, true>(acc, sm.Q, it * 16, ps, lane);
       const int m = it * 16 + (lane & 15);
       {
         const float e = sm.meta.y[m];
@@ -690,7 +691,7 @@ struct BrSmem {
   T dO[Tile<T, D>::SIZE];      // own rows
   T P[NP][Tile<T, CB>::SIZE];  // A = Q K^T masked; dA = scale (dO V^T) masked
   ChunkMeta meta;             // x = exp(G_last - G), y = exp(G) * scale
-  float rk[4 * C::NW][CB];    // partial k.dk of each row, per wave and lane group
+  float rk[C::NW][CB];        // partial k.dk of each row, per wave
 };
 
 // Output rows and adjoint update of one chunk for one half of the workgroup.
@@ -732,8 +733,8 @@ __device__ __forceinline__ void bwd_revorder_rows(
 #pragma unroll
     for (int j = 0; j < C::CPW; ++j) acc[j] = acc[j] * e + f * ad[j];
     if (side) {
-      // k.dk of row m over this lane's columns; the partial sums of a row
-      // (one per wave and lane group) are added by the suffix step
+      // k.dk of row m over the wave's columns (the waves' partial sums are
+      // added by the suffix step)
       float kd = 0.f;
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) {
@@ -741,7 +742,8 @@ __device__ __forceinline__ void bwd_revorder_rows(
 #pragma unroll
         for (int r = 0; r < 4; ++r) kd += kv[r] * acc[j][r];
       }
-      sm.rk[w * 4 + (lane >> 4)][m] = kd;
+      kd = group_sum4(kd);
+      if (lane < 16) sm.rk[w][m] = kd;
     }
     const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (sm.meta.rowk[m] & 3);
     if (kind == ROW_OWN) {
@@ -862,7 +864,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       if (kind != ROW_PAD) {
         float rks = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4 * C::NW; ++i) rks += sm.rk[i][t];
+        for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][t];
         x = rq_cur - rks;
       }
       x = wave_suffix_sum(x, t);
