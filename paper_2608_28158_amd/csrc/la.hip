@@ -273,14 +273,63 @@ __device__ __forceinline__ void score_tile(T* P, const T* Lt, const T* Rt, const
   }
 }
 
+// The masked score tile in three 32 x 32 blocks, (row half, column half) =
+// (0, 0), (1, 0), (1, 1) for waves 0, 1, 2; the block above the diagonal is
+// never read by the consumers and wave 3 does nothing here.  Each block is
+// 2 x 2 tiles of 16 and reads 32 rows of each operand (the four row blocks
+// of score_tile read all of R four times).  Inside the diagonal blocks the
+// tile above the diagonal is skipped and stored as zeros: the consumers'
+// 32-deep steps read it.  P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for
+// n <= m; with PT the tile is stored transposed.
+template <typename T, int D, bool PT = false>
+__device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f,
+                                            int w, int lane) {
+  using TA = Tile<T, CB>;
+  using TD = Tile<T, D>;
+  using F = Frag<T>;
+  const int rb = w == 0 ? 0 : 32, cb = w == 2 ? 32 : 0;
+  const bool diag = rb == cb;
+  f32x4 c[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+  for (int k = 0; k < D; k += F::KSTEP) {
+    const typename F::V a0 = F::template kc<TD>(Lt, rb, k, lane);
+    const typename F::V a1 = F::template kc<TD>(Lt, rb + 16, k, lane);
+    const typename F::V b0 = F::template kc<TD>(Rt, cb, k, lane);
+    const typename F::V b1 = F::template kc<TD>(Rt, cb + 16, k, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    F::mma(c[0][0], a0, b0);
+    F::mma(c[1][0], a1, b0);
+    F::mma(c[1][1], a1, b1);
+    if (!diag) F::mma(c[0][1], a0, b1);
+  }
+#pragma unroll
+  for (int ti = 0; ti < 2; ++ti) {
+    const int m0 = rb + 16 * ti;
+    const f32x4 Gm = row_vec(G, m0, lane);
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj) {
+      const int n = cb + 16 * tj + acc_col(lane);
+      const float Gn = G[n];
+      const bool zero = diag && ti == 0 && tj == 1;
+      f32x4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + acc_row(lane, r);
+        v[r] = !zero && n <= m ? c[ti][tj][r] * __expf(Gm[r] - Gn) * f : 0.f;
+        if (!PT) P[TA::at(m, n)] = Elem<T>::from_f(v[r]);
+      }
+      if (PT) Vec4<T>::store(P + TA::at(n, m0 + acc_row(lane, 0)), v);
+    }
+  }
+}
+
 // The same as an out-of-line call: the reverse-order kernel keeps its score
 // phase in a separate register allocation (its chunk loop holds two states'
 // worth of registers).
-template <typename T, int D>
-__device__ __attribute__((noinline)) void score_tile_call(T* P, const T* Lt, const T* Rt,
-                                                          const float* G, float f, int it, int lane) {
-  score_tile<T, D>(P, Lt, Rt, G, f, it, lane);
-}
 
 // ---------------------------------------------------------------------------
 // block summaries: one pass over a block's chunks, state started from zero
@@ -505,7 +554,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
       fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
     }
     // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    score_tile<T, D>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+    if (w < 3) score_block<T, D>(sm.A, sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
     if (more) fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
     __syncthreads();
     // O[:, wave columns] = scale * (diag(exp(G)) Q S_c + A V), products with
@@ -611,7 +660,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
       fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
     }
     // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    score_tile<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
+    if (w < 3) score_block<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
     if (more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
     __syncthreads();
     // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq.
@@ -798,7 +847,6 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   // side 1: dS^T rows (dv), columns (dk) of the wave's strips
   f32x4 dS[NS];
   state_load<D, C::CPW>(dS, dS_end + (static_cast<int64_t>(b) * H + h) * DD, side == 1, w, lane);
-  float carry = 0.f;  // side 1: sum of (q.dq - k.dk) over the later chunks of the block
   ChunkSrc<T, D, NTH> cs;
   Vec16 pq[SG::NV], pk[SG::NV], pv[SG::NV], pd[SG::NV];
   cs.resolve(sq, c_last, replay_row, g, H, h, tid);
@@ -806,10 +854,31 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
   fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
   fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
-  // side 1, first wave: q.dq of row t of the chunk, one chunk ahead
-  const bool sw0 = side == 1 && t < CB;
-  const float* rq_h = rq + (static_cast<int64_t>(sq.chunk_off) * CB + t) * H + h;
-  float rq_next = sw0 ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
+  // Side 1, wave 3 (lane = row of the chunk) loads q.dq one chunk ahead and
+  // takes the local suffix sums of q.dq - k.dk of each chunk during the next
+  // chunk's score phase, in which it computes no score block.
+  const bool sw = side == 1 && w == 3;
+  const float* rq_h = rq + (static_cast<int64_t>(sq.chunk_off) * CB + lane) * H + h;
+  float rq_next = sw ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
+  float rq_prev = 0.f;  // chunk cp, the one after the current chunk
+  int rowk_prev = 0;
+  float carry = 0.f;    // sum of (q.dq - k.dk) over the later chunks of the block
+  const auto suffix = [&](int cp) {
+    const int kind = rowk_prev & 3;
+    float x = 0.f;
+    if (kind != ROW_PAD) {
+      float rks = 0.f;
+#pragma unroll
+      for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][lane];
+      x = rq_prev - rks;
+    }
+    x = wave_suffix_sum(x, lane);
+    const float val = x + carry;
+    if (kind == ROW_OWN) dg[static_cast<int64_t>(rowk_prev >> 2) * H + h] = val;
+    else if (kind == ROW_REPLAY)
+      rep_grad[((static_cast<int64_t>(sq.replay_off) + cp * CB + lane) * H + h) * RG + 2 * D] = val;
+    carry += lane_value(x, 0);
+  };
   for (int c = c_last; c >= c0; --c) {
     if (tid < CB) {
       float Gt, GLw;
@@ -831,51 +900,46 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     if (more) {
       cs.resolve(sq, c - 1, replay_row, g, H, h, tid);
       fetch<T, D, NTH>(pq, q, cs, H, h, tid, ROW_OWN);
-      if (sw0) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
+      if (sw) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
     }
     const auto hook = [&](int jt) {
       if (more && jt == 1) fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
       if (more && jt == 3) fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
     };
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
-    // M = exp(G_i - G_j) [j <= i]; wave w of each half computes row block w
+    // M = exp(G_i - G_j) [j <= i], in three 32 x 32 blocks per half
     if constexpr (BrSmem<T, D>::NP == 2) {
-      if (side) score_tile<T, D, true>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
-      else score_tile<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      if (w < 3) {
+        if (side) score_block<T, D, true>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+        else score_block<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      } else if (sw && c < c_last) {
+        suffix(c + 1);
+      }
       if (more) fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
       else bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
     } else {
-      if (!side) score_tile<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+      if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
       if (more) fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
       __syncthreads();
       if (!side) bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
       __syncthreads();
-      if (side) score_tile<T, D, true>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      if (side && w < 3) score_block<T, D, true>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      else if (sw && c < c_last) suffix(c + 1);
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
     }
-    __syncthreads();
-    // side 1, first wave: local suffix sums of q.dq - k.dk, one row per lane
-    if (sw0) {
-      const int kind = (sm.meta.rowk[t] & 3);
-      float x = 0.f;
-      if (kind != ROW_PAD) {
-        float rks = 0.f;
-#pragma unroll
-        for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][t];
-        x = rq_cur - rks;
-      }
-      x = wave_suffix_sum(x, t);
-      const float val = x + carry;
-      if (kind == ROW_OWN) dg[static_cast<int64_t>((sm.meta.rowk[t] >> 2)) * H + h] = val;
-      else if (kind == ROW_REPLAY)
-        rep_grad[((static_cast<int64_t>(sq.replay_off) + c * CB + t) * H + h) * RG + 2 * D] = val;
-      carry += lane_value(x, 0);
+    if (sw) {
+      rowk_prev = sm.meta.rowk[lane];
+      rq_prev = rq_cur;
     }
+    __syncthreads();
   }
-  if (side && t == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
+  if (sw) {
+    suffix(c0);
+    if (lane == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
+  }
 }
 
 // ---------------------------------------------------------------------------
