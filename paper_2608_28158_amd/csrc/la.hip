@@ -728,42 +728,48 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
 //   dS_c = exp(G_last) dS_{c+1} + Q^T diag(exp(G) scale) dO
 // in its own layout.
 // ---------------------------------------------------------------------------
-// Two score tiles fit the LDS of a CU in bf16 only; in fp32 the halves take
-// turns with one tile (score A, dv rows, score dA, dk rows).
+// The chunk tiles are double-buffered: while a chunk is computed from one
+// buffer, the next chunk's tiles are written into the other, two tiles at a
+// time, from registers loaded one phase earlier.  Two score tiles fit next to
+// that in bf16 only; in fp32 the halves take turns with one tile (score A,
+// dv rows, score dA, dk rows).
+enum { TQ = 0, TK = 1, TV = 2, TDO = 3 };
 template <typename T, int D>
 struct BrSmem {
   using C = Cfg<T, D>;
   static constexpr int NP = sizeof(T) == 2 ? 2 : 1;
-  T Q[Tile<T, D>::SIZE];       // own rows
-  T K[Tile<T, D>::SIZE];
-  T V[Tile<T, D>::SIZE];
-  T dO[Tile<T, D>::SIZE];      // own rows
-  T P[NP][Tile<T, CB>::SIZE];  // A = Q K^T masked; dA = scale (dO V^T) masked
-  ChunkMeta meta;             // x = exp(G_last - G), y = exp(G) * scale
-  float rk[C::NW][CB];        // partial k.dk of each row, per wave
+  T tile[2][4][Tile<T, D>::SIZE];  // [buffer][Q (own rows), K, V, dO (own rows)]
+  T P[NP][Tile<T, CB>::SIZE];      // A = Q K^T masked; dA = scale (dO V^T) masked
+  ChunkMeta meta[2];               // x = exp(G_last - G), y = exp(G) * scale
+  float rk[C::NW][CB];             // partial k.dk of each row, per wave
 };
 
-// Output rows and adjoint update of one chunk for one half of the workgroup.
-// The products run with their operands swapped, so that lane (g, i) of a wave
-// holds row 16 jt + i of the output at columns col0 + 16 j + 4g .. + 3: one
-// 8-byte (bf16) or 16-byte (float) store per strip, one row per lane.
-template <typename T, int D, int SIDE, typename Hook>
+// Output rows and adjoint update of one chunk (tiles of buffer bf) for one
+// half of the workgroup.  The products run with their operands swapped, so
+// that lane (g, i) of a wave holds row 16 jt + i of the output at columns
+// col0 + 16 j + 4g .. + 3: one 8-byte (bf16) or 16-byte (float) store per
+// strip, one row per lane.
+template <typename T, int D, int SIDE>
 __device__ __forceinline__ void bwd_revorder_rows(
-    BrSmem<T, D>& sm, f32x4* dS, const ChunkRows& cur, const SeqInfo& sq, int c, int H, int h,
-    float scale, float GL, int w, int lane, T* __restrict__ dk, T* __restrict__ dv,
-    float* __restrict__ rep_grad, const Hook& hook) {
+    BrSmem<T, D>& sm, int bf, f32x4* dS, const ChunkRows& cur, const SeqInfo& sq, int c, int H,
+    int h, float scale, float GL, int w, int lane, T* __restrict__ dk, T* __restrict__ dv,
+    float* __restrict__ rep_grad) {
   using C = Cfg<T, D>;
   constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
   constexpr bool side = SIDE == 1;
   const int col0 = C::CPW * w * 16;
   const T* PT = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];  // transposed score tile
+  const T* Q = sm.tile[bf][TQ];
+  const T* K = sm.tile[bf][TK];
+  const T* V = sm.tile[bf][TV];
+  const T* dOt = sm.tile[bf][TDO];
+  const ChunkMeta& mt = sm.meta[bf];
   const int g4 = 4 * (lane >> 4);
   PackedState<T, C::NT, C::CPW> ps;
   ps.pack(dS);
 #pragma unroll 1
   for (int jt = 0; jt < CB / 16; ++jt) {
-    hook(jt);
     // side 0: dv = diag(x) K dS + scale A^T dO ; side 1: dk = diag(x) V dS^T + dA^T Q
     // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
     f32x4 acc[C::CPW], ad[C::CPW];
@@ -772,12 +778,12 @@ __device__ __forceinline__ void bwd_revorder_rows(
       acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, false>(acc, side ? sm.V : sm.K, jt * 16, ps, lane);
+    regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, false>(acc, side ? V : K, jt * 16, ps, lane);
     const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
     tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true, true>(
-        ad, PT, jt * 16, side ? sm.Q : sm.dO, col0, k0, CB, lane);
+        ad, PT, jt * 16, side ? Q : dOt, col0, k0, CB, lane);
     const int m = jt * 16 + (lane & 15);
-    const float e = sm.meta.x[m];
+    const float e = mt.x[m];
     const float f = side ? 1.f : scale;
 #pragma unroll
     for (int j = 0; j < C::CPW; ++j) acc[j] = acc[j] * e + f * ad[j];
@@ -787,16 +793,16 @@ __device__ __forceinline__ void bwd_revorder_rows(
       float kd = 0.f;
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) {
-        const f32x4 kv = Vec4<T>::load(sm.K + C::TD::at(m, col0 + 16 * j + g4));
+        const f32x4 kv = Vec4<T>::load(K + C::TD::at(m, col0 + 16 * j + g4));
 #pragma unroll
         for (int r = 0; r < 4; ++r) kd += kv[r] * acc[j][r];
       }
       kd = group_sum4(kd);
       if (lane < 16) sm.rk[w][m] = kd;
     }
-    const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (sm.meta.rowk[m] & 3);
+    const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (mt.rowk[m] & 3);
     if (kind == ROW_OWN) {
-      const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (sm.meta.rowk[m] >> 2);
+      const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (mt.rowk[m] >> 2);
       T* dst = (side ? dk : dv) + (row * H + h) * D + col0 + g4;
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j]);
@@ -816,9 +822,9 @@ __device__ __forceinline__ void bwd_revorder_rows(
 #pragma unroll
   for (int i = 0; i < NS; ++i) dS[i] *= dec;
   if (!side)
-    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, sm.Q, sm.dO, col0, sm.meta.y, lane);
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, Q, dOt, col0, mt.y, lane);
   else
-    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, sm.dO, sm.Q, col0, sm.meta.y, lane);
+    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, dOt, Q, col0, mt.y, lane);
 }
 
 template <typename T, int D>
@@ -832,7 +838,6 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   using C = Cfg<T, D>;
   constexpr int NTH = 2 * C::NTHR;
   using SG = Stg<T, D, NTH>;
-  constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
   __shared__ BrSmem<T, D> sm;
   const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, tid = threadIdx.x;
@@ -845,15 +850,38 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   const int64_t DD = static_cast<int64_t>(D) * D;
   // side 0: dS   rows (dk), columns (dv) of the wave's strips
   // side 1: dS^T rows (dv), columns (dk) of the wave's strips
-  f32x4 dS[NS];
+  f32x4 dS[C::CPW * C::NT];
   state_load<D, C::CPW>(dS, dS_end + (static_cast<int64_t>(b) * H + h) * DD, side == 1, w, lane);
+  // Publishes the row table and decay factors of the chunk resolved in cs
+  // into meta[bf] (first wave).
+  const auto publish = [&](const ChunkSrc<T, D, NTH>& src, int bf) {
+    if (tid < CB) {
+      float Gt, GLw;
+      meta_publish(sm.meta[bf], src, tid, Gt, GLw);
+      sm.meta[bf].x[tid] = __expf(GLw - Gt);
+      sm.meta[bf].y[tid] = __expf(Gt) * scale;
+    }
+  };
+  // The last chunk of the block goes into buffer 0, two tiles at a time.
   ChunkSrc<T, D, NTH> cs;
-  Vec16 pq[SG::NV], pk[SG::NV], pv[SG::NV], pd[SG::NV];
+  Vec16 pa[SG::NV], pb[SG::NV];
   cs.resolve(sq, c_last, replay_row, g, H, h, tid);
-  fetch<T, D, NTH>(pq, q, cs, H, h, tid, ROW_OWN);
-  fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
-  fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
-  fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
+  fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
+  fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
+  put<T, D, NTH>(sm.tile[0][TQ], pa, nullptr, tid);
+  put<T, D, NTH>(sm.tile[0][TK], pb, nullptr, tid);
+  fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
+  fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
+  put<T, D, NTH>(sm.tile[0][TV], pa, nullptr, tid);
+  put<T, D, NTH>(sm.tile[0][TDO], pb, nullptr, tid);
+  publish(cs, 0);
+  ChunkRows cur_next = cs.cr;
+  // the first two tiles of the chunk before it
+  if (c_last > c0) {
+    cs.resolve(sq, c_last - 1, replay_row, g, H, h, tid);
+    fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
+    fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
+  }
   // Side 1, wave 3 (lane = row of the chunk) loads q.dq one chunk ahead and
   // takes the local suffix sums of q.dq - k.dk of each chunk during the next
   // chunk's score phase, in which it computes no score block.
@@ -879,59 +907,60 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       rep_grad[((static_cast<int64_t>(sq.replay_off) + cp * CB + lane) * H + h) * RG + 2 * D] = val;
     carry += lane_value(x, 0);
   };
+  __syncthreads();
   for (int c = c_last; c >= c0; --c) {
-    if (tid < CB) {
-      float Gt, GLw;
-      meta_publish(sm.meta, cs, tid, Gt, GLw);
-      sm.meta.x[tid] = __expf(GLw - Gt);
-      sm.meta.y[tid] = __expf(Gt) * scale;
-    }
-    const ChunkRows cur = cs.cr;
-    const float rq_cur = rq_next;
-    put<T, D, NTH>(sm.Q, pq, nullptr, tid);
-    put<T, D, NTH>(sm.K, pk, nullptr, tid);
-    put<T, D, NTH>(sm.V, pv, nullptr, tid);
-    put<T, D, NTH>(sm.dO, pd, nullptr, tid);
-    __syncthreads();
-    const float GL = sm.meta.G[CB - 1];
-    // the next chunk's rows are loaded one tile at a time between the phases
-    // of this chunk, so that the loads overlap the products
+    const int bf = (c_last - c) & 1, nb = bf ^ 1;
     const bool more = c > c0;
-    if (more) {
-      cs.resolve(sq, c - 1, replay_row, g, H, h, tid);
-      fetch<T, D, NTH>(pq, q, cs, H, h, tid, ROW_OWN);
-      if (sw) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
-    }
-    const auto hook = [&](int jt) {
-      if (more && jt == 1) fetch<T, D, NTH>(pv, v, cs, H, h, tid, ROW_REPLAY);
-      if (more && jt == 3) fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
-    };
+    const ChunkRows cur = cur_next;
+    const float rq_cur = rq_next;
+    if (sw && more) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
+    const float GL = sm.meta[bf].G[CB - 1];
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i], in three 32 x 32 blocks per half
     if constexpr (BrSmem<T, D>::NP == 2) {
       if (w < 3) {
-        if (side) score_block<T, D, true>(sm.P[1], sm.dO, sm.V, sm.meta.G, scale, w, lane);
-        else score_block<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
+        if (side) score_block<T, D, true>(sm.P[1], sm.tile[bf][TDO], sm.tile[bf][TV], sm.meta[bf].G, scale, w, lane);
+        else score_block<T, D, true>(sm.P[0], sm.tile[bf][TQ], sm.tile[bf][TK], sm.meta[bf].G, 1.f, w, lane);
       } else if (sw && c < c_last) {
         suffix(c + 1);
       }
-      if (more) fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
-      __syncthreads();
-      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
-      else bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
     } else {
-      if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.Q, sm.K, sm.meta.G, 1.f, w, lane);
-      if (more) fetch<T, D, NTH>(pk, k, cs, H, h, tid, ROW_REPLAY);
+      if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.tile[bf][TQ], sm.tile[bf][TK], sm.meta[bf].G, 1.f, w, lane);
+    }
+    // next chunk: Q, K into the other buffer; V, dO requested
+    if (more) {
+      put<T, D, NTH>(sm.tile[nb][TQ], pa, nullptr, tid);
+      put<T, D, NTH>(sm.tile[nb][TK], pb, nullptr, tid);
+      fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
+      fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
+    }
+    __syncthreads();
+    if constexpr (BrSmem<T, D>::NP == 2) {
+      if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      else bwd_revorder_rows<T, D, 0>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+    } else {
+      if (!side) bwd_revorder_rows<T, D, 0>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
       __syncthreads();
-      if (!side) bwd_revorder_rows<T, D, 0>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
-      __syncthreads();
-      if (side && w < 3) score_block<T, D, true>(sm.P[0], sm.dO, sm.V, sm.meta.G, scale, w, lane);
+      if (side && w < 3) score_block<T, D, true>(sm.P[0], sm.tile[bf][TDO], sm.tile[bf][TV], sm.meta[bf].G, scale, w, lane);
       else if (sw && c < c_last) suffix(c + 1);
       __syncthreads();
-      if (side) bwd_revorder_rows<T, D, 1>(sm, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad, hook);
+      if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+    }
+    // next chunk: V, dO and the row table into the other buffer; the
+    // chunk after it resolved and its Q, K requested
+    if (more) {
+      put<T, D, NTH>(sm.tile[nb][TV], pa, nullptr, tid);
+      put<T, D, NTH>(sm.tile[nb][TDO], pb, nullptr, tid);
+      publish(cs, nb);
+      cur_next = cs.cr;
+      if (c - 1 > c0) {
+        cs.resolve(sq, c - 2, replay_row, g, H, h, tid);
+        fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
+        fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
+      }
     }
     if (sw) {
-      rowk_prev = sm.meta.rowk[lane];
+      rowk_prev = sm.meta[bf].rowk[lane];
       rq_prev = rq_cur;
     }
     __syncthreads();
