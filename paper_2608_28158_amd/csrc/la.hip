@@ -230,6 +230,42 @@ __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) 
         dst[(i * 16 + acc_row(lane, r)) * D + (CPW * w + j) * 16 + acc_col(lane)] = S[j * NT + i][r];
 }
 
+// A [D x D] float state staged through LDS: read once with 16-byte loads by
+// all NTH threads (row pitch D + 4 floats), then handed out to the waves in
+// the accumulator layout of state_load.  The pitch makes the reads of the
+// plain layout free of bank conflicts; the transposed ones conflict up to
+// four ways, once per block.
+template <int D>
+struct StateStage {
+  static constexpr int PITCH = D + 4;
+  static constexpr int BYTES = D * PITCH * 4;
+};
+template <int D, int NTH>
+__device__ inline void state_to_lds(float* stg, const float* __restrict__ src, int tid) {
+  constexpr int N4 = D * D / 4;
+  static_assert(N4 % NTH == 0, "state split");
+#pragma unroll
+  for (int i = 0; i < N4 / NTH; ++i) {
+    const int e4 = tid + i * NTH;
+    const int r = e4 / (D / 4), c = (e4 % (D / 4)) * 4;
+    *reinterpret_cast<float4*>(stg + r * StateStage<D>::PITCH + c) =
+        *reinterpret_cast<const float4*>(src + static_cast<int64_t>(e4) * 4);
+  }
+}
+template <int D, int CPW>
+__device__ inline void state_from_lds(f32x4* S, const float* stg, bool transpose, int w, int lane) {
+  constexpr int NT = D / 16, P = StateStage<D>::PITCH;
+#pragma unroll
+  for (int j = 0; j < CPW; ++j)
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
+        S[j * NT + i][r] = transpose ? stg[b * P + a] : stg[a * P + b];
+      }
+}
+
 // Row block it (the wave index) of a masked score tile, all four column
 // tiles: P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for n <= m, 0 above the
 // diagonal.  Tiles above the diagonal are computed and discarded: the wave
@@ -768,8 +804,19 @@ __device__ __forceinline__ void bwd_revorder_rows(
   const int g4 = 4 * (lane >> 4);
   PackedState<T, C::NT, C::CPW> ps;
   ps.pack(dS);
+  // the row factors of the lane's four rows, read before the loop
+  float xr[CB / 16];
+#pragma unroll
+  for (int jt = 0; jt < CB / 16; ++jt) xr[jt] = mt.x[jt * 16 + (lane & 15)];
 #pragma unroll 1
   for (int jt = 0; jt < CB / 16; ++jt) {
+    const int m = jt * 16 + (lane & 15);
+    // side 1: the K values of the lane's row and columns, requested first
+    typename Vec4Raw<T>::V kraw[C::CPW];
+    if (side) {
+#pragma unroll
+      for (int j = 0; j < C::CPW; ++j) kraw[j] = Vec4Raw<T>::load(K + C::TD::at(m, col0 + 16 * j + g4));
+    }
     // side 0: dv = diag(x) K dS + scale A^T dO ; side 1: dk = diag(x) V dS^T + dA^T Q
     // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
     f32x4 acc[C::CPW], ad[C::CPW];
@@ -778,12 +825,13 @@ __device__ __forceinline__ void bwd_revorder_rows(
       acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, false>(acc, side ? V : K, jt * 16, ps, lane);
+    regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, true>(acc, side ? V : K, jt * 16, ps, lane);
     const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
     tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true, true>(
         ad, PT, jt * 16, side ? Q : dOt, col0, k0, CB, lane);
-    const int m = jt * 16 + (lane & 15);
-    const float e = mt.x[m];
+    float e = xr[0];
+#pragma unroll
+    for (int i = 1; i < CB / 16; ++i) e = jt == i ? xr[i] : e;
     const float f = side ? 1.f : scale;
 #pragma unroll
     for (int j = 0; j < C::CPW; ++j) acc[j] = acc[j] * e + f * ad[j];
@@ -793,7 +841,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
       float kd = 0.f;
 #pragma unroll
       for (int j = 0; j < C::CPW; ++j) {
-        const f32x4 kv = Vec4<T>::load(K + C::TD::at(m, col0 + 16 * j + g4));
+        const f32x4 kv = Vec4Raw<T>::widen(kraw[j]);
 #pragma unroll
         for (int r = 0; r < 4; ++r) kd += kv[r] * acc[j][r];
       }
@@ -848,10 +896,9 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
-  // side 0: dS   rows (dk), columns (dv) of the wave's strips
-  // side 1: dS^T rows (dv), columns (dk) of the wave's strips
-  f32x4 dS[C::CPW * C::NT];
-  state_load<D, C::CPW>(dS, dS_end + (static_cast<int64_t>(b) * H + h) * DD, side == 1, w, lane);
+  static_assert(StateStage<D>::BYTES <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)),
+                "state staging fits the second tile buffer");
+  float* stg = reinterpret_cast<float*>(&sm.tile[1][0][0]);
   // Publishes the row table and decay factors of the chunk resolved in cs
   // into meta[bf] (first wave).
   const auto publish = [&](const ChunkSrc<T, D, NTH>& src, int bf) {
@@ -865,9 +912,12 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   // The last chunk of the block goes into buffer 0, two tiles at a time.
   ChunkSrc<T, D, NTH> cs;
   Vec16 pa[SG::NV], pb[SG::NV];
+  // dS_end is read once into the second buffer (free until the first
+  // chunk's score), next to the first chunk's tiles
   cs.resolve(sq, c_last, replay_row, g, H, h, tid);
   fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
   fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
+  state_to_lds<D, NTH>(stg, dS_end + (static_cast<int64_t>(b) * H + h) * DD, tid);
   put<T, D, NTH>(sm.tile[0][TQ], pa, nullptr, tid);
   put<T, D, NTH>(sm.tile[0][TK], pb, nullptr, tid);
   fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
@@ -876,6 +926,11 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   put<T, D, NTH>(sm.tile[0][TDO], pb, nullptr, tid);
   publish(cs, 0);
   ChunkRows cur_next = cs.cr;
+  __syncthreads();
+  // side 0: dS   rows (dk), columns (dv) of the wave's strips
+  // side 1: dS^T rows (dv), columns (dk) of the wave's strips
+  f32x4 dS[C::CPW * C::NT];
+  state_from_lds<D, C::CPW>(dS, stg, side == 1, w, lane);
   // the first two tiles of the chunk before it
   if (c_last > c0) {
     cs.resolve(sq, c_last - 1, replay_row, g, H, h, tid);

@@ -62,6 +62,23 @@ template <> struct Vec4<bf16> {
   }
 };
 
+// Four consecutive elements read in their storage type, widened later (so
+// that the read can be issued well before the value is needed).
+template <typename T> struct Vec4Raw;
+template <> struct Vec4Raw<float> {
+  typedef f32x4 V;
+  __device__ static inline V load(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
+  __device__ static inline f32x4 widen(const V& v) { return v; }
+};
+template <> struct Vec4Raw<bf16> {
+  typedef bf16x4 V;
+  __device__ static inline V load(const bf16* p) { return *reinterpret_cast<const bf16x4*>(p); }
+  __device__ static inline f32x4 widen(const V& b) {
+    return f32x4{static_cast<float>(b[0]), static_cast<float>(b[1]), static_cast<float>(b[2]),
+                 static_cast<float>(b[3])};
+  }
+};
+
 // LDS tile layout: 64 rows of COLS elements, row-major, each row padded by
 // 16 bytes.  Addresses are affine in (r, c), so every fragment read is a
 // per-lane base plus an immediate offset.  With the padding, 16-byte row
