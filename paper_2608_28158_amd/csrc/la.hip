@@ -252,6 +252,38 @@ __device__ inline void state_to_lds(float* stg, const float* __restrict__ src, i
         *reinterpret_cast<const float4*>(src + static_cast<int64_t>(e4) * 4);
   }
 }
+// The whole staged load, in NPASS passes of D / NPASS stored rows each (for
+// LDS that holds only part of a state); every thread of the workgroup calls
+// it (it synchronises the workgroup).
+template <int D, int CPW, int NTH, int NPASS>
+__device__ inline void state_via_lds(f32x4* S, float* stg, const float* __restrict__ src,
+                                     bool transpose, int w, int lane, int tid) {
+  constexpr int NT = D / 16, P = D + 4, RP = D / NPASS, N4 = RP * D / 4;
+  static_assert(N4 % NTH == 0, "state split");
+#pragma unroll
+  for (int pass = 0; pass < NPASS; ++pass) {
+#pragma unroll
+    for (int i = 0; i < N4 / NTH; ++i) {
+      const int e4 = tid + i * NTH;
+      const int r = e4 / (D / 4), c = (e4 % (D / 4)) * 4;
+      *reinterpret_cast<float4*>(stg + r * P + c) =
+          *reinterpret_cast<const float4*>(src + (static_cast<int64_t>(pass) * RP * D + e4 * 4));
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+#pragma unroll
+      for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
+          const int row = transpose ? b : a, col = transpose ? a : b;
+          if (row / RP == pass) S[j * NT + i][r] = stg[(row - pass * RP) * P + col];
+        }
+    __syncthreads();
+  }
+}
+
 template <int D, int CPW>
 __device__ inline void state_from_lds(f32x4* S, const float* stg, bool transpose, int w, int lane) {
   constexpr int NT = D / 16, P = StateStage<D>::PITCH;
@@ -559,16 +591,21 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const int64_t DD = static_cast<int64_t>(D) * D;
-  f32x4 S[NS];  // S : rows (dk), columns (dv) of the wave's strips
-  state_load<D, C::CPW>(S, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
-                                            : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                        false, w, lane);
+  // the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV];
   cs.resolve(sq, c0, replay_row, g, H, h, t);
   fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
+  f32x4 S[NS];  // S : rows (dk), columns (dv) of the wave's strips
+  // the start state, staged through the (still unused) tiles in two halves
+  static_assert(D / 2 * (D + 4) * 4 <= static_cast<int>(sizeof(FwdSmem<T, D>) - sizeof(ChunkMeta)),
+                "half a state fits the tiles");
+  state_via_lds<D, C::CPW, C::NTHR, 2>(S, reinterpret_cast<float*>(&sm.Q[0]),
+                                       bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                                        : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                                       false, w, lane, t);
   for (int c = c0; c < c_end; ++c) {
     if (t < CB) {
       float Gt, GLw;
@@ -664,10 +701,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const int64_t DD = static_cast<int64_t>(D) * D;
-  f32x4 St[NS];  // S^T : rows (dv), columns (dk) of the wave's strips
-  state_load<D, C::CPW>(St, bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
-                                             : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                        true, w, lane);
+  // the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
   cs.resolve(sq, c0, replay_row, g, H, h, t);
@@ -675,6 +709,13 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
+  f32x4 St[NS];  // S^T : rows (dv), columns (dk) of the wave's strips
+  // the start state, staged through the (still unused) tiles
+  static_assert(D * (D + 4) * 4 <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)), "state fits the tiles");
+  state_via_lds<D, C::CPW, C::NTHR, 1>(St, reinterpret_cast<float*>(&sm.dO[0]),
+                                       bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                                        : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                                       true, w, lane, t);
   for (int c = c0; c < c_end; ++c) {
     if (t < CB) {
       float Gt, GLw;
