@@ -470,6 +470,9 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
 // element-parallel chains over the blocks of every sequence
 // ---------------------------------------------------------------------------
 constexpr int SCAN_THR = 256;
+// Blocks whose summaries a scan requests together: the chain is serial in
+// the blocks, its loads are not.
+constexpr int SCAN_PF = 8;
 
 template <int D>
 __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
@@ -483,18 +486,33 @@ __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
   float4 s = reinterpret_cast<const float4*>(S0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4];
-  for (int b = b0; b < b0 + nb; ++b) {
-    const int64_t bi = (static_cast<int64_t>(b) * H + h);
-    const float dec = __expf(gam[bi]);
-    const float4 x = reinterpret_cast<const float4*>(dSb)[bi * SS4 + e4];
-    s.x = dec * s.x + x.x;
-    s.y = dec * s.y + x.y;
-    s.z = dec * s.z + x.z;
-    s.w = dec * s.w + x.w;
-    reinterpret_cast<float4*>(S_end)[bi * SS4 + e4] = s;
-    const int eb = blk_tab[b * BLK_WORDS + BLK_END_BANK];
-    if (eb >= 0 && bank)
-      reinterpret_cast<float4*>(bank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4] = s;
+  for (int bg = b0; bg < b0 + nb; bg += SCAN_PF) {
+    float4 x[SCAN_PF];
+    float gm[SCAN_PF];
+#pragma unroll
+    for (int i = 0; i < SCAN_PF; ++i) {
+      if (bg + i < b0 + nb) {
+        const int64_t bi = static_cast<int64_t>(bg + i) * H + h;
+        gm[i] = gam[bi];
+        x[i] = reinterpret_cast<const float4*>(dSb)[bi * SS4 + e4];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < SCAN_PF; ++i) {
+      const int b = bg + i;
+      if (b < b0 + nb) {
+        const int64_t bi = static_cast<int64_t>(b) * H + h;
+        const float dec = __expf(gm[i]);
+        s.x = dec * s.x + x[i].x;
+        s.y = dec * s.y + x[i].y;
+        s.z = dec * s.z + x[i].z;
+        s.w = dec * s.w + x[i].w;
+        reinterpret_cast<float4*>(S_end)[bi * SS4 + e4] = s;
+        const int eb = blk_tab[b * BLK_WORDS + BLK_END_BANK];
+        if (eb >= 0 && bank)
+          reinterpret_cast<float4*>(bank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4] = s;
+      }
+    }
   }
   if (S_final)
     reinterpret_cast<float4*>(S_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4] = s;
@@ -533,29 +551,43 @@ __global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
     const float bsum = scan_block_sum(ds.x * s.x + ds.y * s.y + ds.z * s.z + ds.w * s.w, red, t);
     if (t == 0) betap[(static_cast<int64_t>(bl) * H + h) * NSW + part] = bsum;
   }
-  for (int b = b0 + nb - 1; b >= b0; --b) {
-    const int64_t bi = static_cast<int64_t>(b) * H + h;
-    reinterpret_cast<float4*>(dS_end)[bi * SS4 + e4] = ds;
-    const float dec = __expf(gam[bi]);
-    const float4 u = reinterpret_cast<const float4*>(U)[bi * SS4 + e4];
-    ds.x = dec * ds.x + u.x;
-    ds.y = dec * ds.y + u.y;
-    ds.z = dec * ds.z + u.z;
-    ds.w = dec * ds.w + u.w;
-    if (b > b0) {
-      const int64_t pi = static_cast<int64_t>(b - 1) * H + h;
-      const int eb = blk_tab[(b - 1) * BLK_WORDS + BLK_END_BANK];
-      float bsum = 0.f;
-      if (eb >= 0) {  // uniform over the workgroup
-        const float4 inj = reinterpret_cast<const float4*>(dbank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4];
-        const float4 s = S4[pi * SS4 + e4];
-        bsum = scan_block_sum(inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w, red, t);
-        ds.x += inj.x;
-        ds.y += inj.y;
-        ds.z += inj.z;
-        ds.w += inj.w;
+  for (int bg = b0 + nb - 1; bg >= b0; bg -= SCAN_PF) {
+    float4 u[SCAN_PF];
+    float gm[SCAN_PF];
+#pragma unroll
+    for (int i = 0; i < SCAN_PF; ++i) {
+      if (bg - i >= b0) {
+        const int64_t bi = static_cast<int64_t>(bg - i) * H + h;
+        gm[i] = gam[bi];
+        u[i] = reinterpret_cast<const float4*>(U)[bi * SS4 + e4];
       }
-      if (t == 0) betap[pi * NSW + part] = bsum;
+    }
+#pragma unroll
+    for (int i = 0; i < SCAN_PF; ++i) {
+      const int b = bg - i;
+      if (b < b0) break;
+      const int64_t bi = static_cast<int64_t>(b) * H + h;
+      reinterpret_cast<float4*>(dS_end)[bi * SS4 + e4] = ds;
+      const float dec = __expf(gm[i]);
+      ds.x = dec * ds.x + u[i].x;
+      ds.y = dec * ds.y + u[i].y;
+      ds.z = dec * ds.z + u[i].z;
+      ds.w = dec * ds.w + u[i].w;
+      if (b > b0) {
+        const int64_t pi = static_cast<int64_t>(b - 1) * H + h;
+        const int eb = blk_tab[(b - 1) * BLK_WORDS + BLK_END_BANK];
+        float bsum = 0.f;
+        if (eb >= 0) {  // uniform over the workgroup
+          const float4 inj = reinterpret_cast<const float4*>(dbank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4];
+          const float4 s = S4[pi * SS4 + e4];
+          bsum = scan_block_sum(inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w, red, t);
+          ds.x += inj.x;
+          ds.y += inj.y;
+          ds.z += inj.z;
+          ds.w += inj.w;
+        }
+        if (t == 0) betap[pi * NSW + part] = bsum;
+      }
     }
   }
   reinterpret_cast<float4*>(dS0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4] = ds;
