@@ -147,7 +147,8 @@ struct ChunkMeta {
 };
 
 // Where this thread's rows of one chunk live, resolved one chunk ahead: the
-// rows it stages (all threads) and, for wave 0, row t of the chunk with its g.
+// rows it stages (all threads) and, for the wave that publishes the chunk's
+// row table (mrow = its lane, -1 elsewhere), row mrow of the chunk with its g.
 template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
 struct ChunkSrc {
   ChunkRows cr;
@@ -155,12 +156,20 @@ struct ChunkSrc {
   RowRef mr;
   float gv;
   __device__ inline void resolve(const SeqInfo& seq, int c, const int32_t* replay_row,
-                                 const float* g, int H, int h, int t) {
+                                 const float* g, int H, int h, int t, int mrow) {
     cr = chunk_rows(seq, c);
-    if (!cr.fast) refs.resolve(seq, c, replay_row, t);
-    if (t < CB) {
-      mr = cr.fast ? RowRef{cr.row0 + t, ROW_OWN, -1} : pos_row(seq, c * CB + t, replay_row);
-      gv = mr.kind != ROW_PAD ? g[static_cast<int64_t>(mr.row) * H + h] : 0.f;
+    // the two cases apart, so that the fast case's g address waits on no load
+    if (cr.fast) {
+      if (mrow >= 0) {
+        mr = RowRef{cr.row0 + mrow, ROW_OWN, -1};
+        gv = g[static_cast<int64_t>(mr.row) * H + h];
+      }
+    } else {
+      refs.resolve(seq, c, replay_row, t);
+      if (mrow >= 0) {
+        mr = pos_row(seq, c * CB + mrow, replay_row);
+        gv = mr.kind != ROW_PAD ? g[static_cast<int64_t>(mr.row) * H + h] : 0.f;
+      }
     }
   }
 };
@@ -190,8 +199,8 @@ __device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkS
   }
 }
 
-// Wave 0 (lane t = row t): publishes the row table and G of the chunk whose
-// sources are in cs; returns G_t and G_last.
+// The publishing wave (lane t = row t): publishes the row table and G of the
+// chunk whose sources are in cs; returns G_t and G_last.
 template <typename T, int D, int NTH>
 __device__ inline void meta_publish(ChunkMeta& m, const ChunkSrc<T, D, NTH>& cs, int t, float& Gt,
                                     float& GL) {
@@ -433,7 +442,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   for (int i = 0; i < C::CPW * C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   ChunkSrc<T, D> cs;
   Vec16 px[C::NV], py[C::NV];
-  cs.resolve(sq, c0, replay_row, g, H, h, t);
+  cs.resolve(sq, c0, replay_row, g, H, h, t, t < CB ? t : -1);
   fetch<T, D>(px, X, cs, H, h, t, min_kind);
   fetch<T, D>(py, Y, cs, H, h, t, min_kind);
   float Gs = 0.f;  // log-decay from the block start to the current chunk start
@@ -448,7 +457,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
     __syncthreads();
     const float GL = meta.G[CB - 1];
     if (c + 1 < c_end) {
-      cs.resolve(sq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c + 1, replay_row, g, H, h, t, t < CB ? t : -1);
       fetch<T, D>(px, X, cs, H, h, t, min_kind);
       fetch<T, D>(py, Y, cs, H, h, t, min_kind);
     }
@@ -626,7 +635,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   // the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV];
-  cs.resolve(sq, c0, replay_row, g, H, h, t);
+  cs.resolve(sq, c0, replay_row, g, H, h, t, t < CB ? t : -1);
   fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
@@ -655,7 +664,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     // of this chunk, so that the loads do not queue up behind each other
     const bool more = c + 1 < c_end;
     if (more) {
-      cs.resolve(sq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c + 1, replay_row, g, H, h, t, t < CB ? t : -1);
       fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
     }
     // A = (Q K^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
@@ -736,7 +745,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   // the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  cs.resolve(sq, c0, replay_row, g, H, h, t);
+  cs.resolve(sq, c0, replay_row, g, H, h, t, t < CB ? t : -1);
   fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
   fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
   fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
@@ -765,7 +774,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
     // the next chunk's rows, one tile at a time between the phases
     const bool more = c + 1 < c_end;
     if (more) {
-      cs.resolve(sq, c + 1, replay_row, g, H, h, t);
+      cs.resolve(sq, c + 1, replay_row, g, H, h, t, t < CB ? t : -1);
       fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
     }
     // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
@@ -875,6 +884,11 @@ __device__ __forceinline__ void bwd_revorder_rows(
   const T* dOt = sm.tile[bf][TDO];
   const ChunkMeta& mt = sm.meta[bf];
   const int g4 = 4 * (lane >> 4);
+  // the chunk's 64 rows of the output (row0 may precede the sequence's own
+  // rows when the chunk starts with replay rows; only own rows are stored)
+  const __amdgpu_buffer_rsrc_t out_rsrc =
+      buffer_rsrc((side ? dk : dv) + static_cast<int64_t>(cur.row0) * H * D,
+                  static_cast<uint32_t>(CB * H * D * sizeof(T)));
   PackedState<T, C::NT, C::CPW> ps;
   ps.pack(dS);
   // the row factors of the lane's four rows, read before the loop
@@ -921,13 +935,21 @@ __device__ __forceinline__ void bwd_revorder_rows(
       kd = group_sum4(kd);
       if (lane < 16) sm.rk[w][m] = kd;
     }
+    // Own rows: an own row at position m of the chunk is physical row
+    // row0 + m, so every lane stores at its offset from row0 (through a
+    // resource over the chunk's 64 rows) and a lane whose row is not own
+    // stores nothing.  The stores are thus the same on every path, which lets
+    // the wait for the next chunk's loads skip them.
     const int kind = cur.fast ? static_cast<int>(ROW_OWN) : (mt.rowk[m] & 3);
-    if (kind == ROW_OWN) {
-      const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (mt.rowk[m] >> 2);
-      T* dst = (side ? dk : dv) + (row * H + h) * D + col0 + g4;
+    {
+      const uint32_t off = kind == ROW_OWN
+                               ? static_cast<uint32_t>(((m * H + h) * D + col0 + g4) * static_cast<int>(sizeof(T)))
+                               : BUF_DROP;
 #pragma unroll
-      for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j]);
-    } else if (kind == ROW_REPLAY) {
+      for (int j = 0; j < C::CPW; ++j)
+        BufVec4<T>::store(out_rsrc, off + static_cast<uint32_t>(16 * j * sizeof(T)), acc[j]);
+    }
+    if (kind == ROW_REPLAY) {
       // rows of 2D + 1 floats: no vector alignment
       float* dst = rep_grad + ((static_cast<int64_t>(sq.replay_off) + c * CB + m) * H + h) * RG +
                    (side ? 0 : D) + col0 + g4;
@@ -972,22 +994,23 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   static_assert(StateStage<D>::BYTES <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)),
                 "state staging fits the second tile buffer");
   float* stg = reinterpret_cast<float*>(&sm.tile[1][0][0]);
-  // Publishes the row table and decay factors of the chunk resolved in cs
-  // into meta[bf] (first wave).
+  // Side 0, wave 3 (lane = row of the chunk) publishes each chunk's row table
+  // and decay factors during the score phase of the chunk before it, in which
+  // it computes no score block.
+  const bool pw = side == 0 && w == 3;
+  const int mrow = pw ? lane : -1;
   const auto publish = [&](const ChunkSrc<T, D, NTH>& src, int bf) {
-    if (tid < CB) {
-      float Gt, GLw;
-      meta_publish(sm.meta[bf], src, tid, Gt, GLw);
-      sm.meta[bf].x[tid] = __expf(GLw - Gt);
-      sm.meta[bf].y[tid] = __expf(Gt) * scale;
-    }
+    float Gt, GLw;
+    meta_publish(sm.meta[bf], src, lane, Gt, GLw);
+    sm.meta[bf].x[lane] = __expf(GLw - Gt);
+    sm.meta[bf].y[lane] = __expf(Gt) * scale;
   };
   // The last chunk of the block goes into buffer 0, two tiles at a time.
   ChunkSrc<T, D, NTH> cs;
   Vec16 pa[SG::NV], pb[SG::NV];
   // dS_end is read once into the second buffer (free until the first
   // chunk's score), next to the first chunk's tiles
-  cs.resolve(sq, c_last, replay_row, g, H, h, tid);
+  cs.resolve(sq, c_last, replay_row, g, H, h, tid, mrow);
   fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
   fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
   state_to_lds<D, NTH>(stg, dS_end + (static_cast<int64_t>(b) * H + h) * DD, tid);
@@ -997,7 +1020,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
   put<T, D, NTH>(sm.tile[0][TV], pa, nullptr, tid);
   put<T, D, NTH>(sm.tile[0][TDO], pb, nullptr, tid);
-  publish(cs, 0);
+  if (pw) publish(cs, 0);
   ChunkRows cur_next = cs.cr;
   __syncthreads();
   // side 0: dS   rows (dk), columns (dv) of the wave's strips
@@ -1006,7 +1029,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   state_from_lds<D, C::CPW>(dS, stg, side == 1, w, lane);
   // the first two tiles of the chunk before it
   if (c_last > c0) {
-    cs.resolve(sq, c_last - 1, replay_row, g, H, h, tid);
+    cs.resolve(sq, c_last - 1, replay_row, g, H, h, tid, mrow);
     fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
     fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
   }
@@ -1051,8 +1074,11 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
         else score_block<T, D, true>(sm.P[0], sm.tile[bf][TQ], sm.tile[bf][TK], sm.meta[bf].G, 1.f, w, lane);
       } else if (sw && c < c_last) {
         suffix(c + 1);
+      } else if (pw && more) {
+        publish(cs, nb);
       }
     } else {
+      if (pw && more) publish(cs, nb);
       if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.tile[bf][TQ], sm.tile[bf][TK], sm.meta[bf].G, 1.f, w, lane);
     }
     // next chunk: Q, K into the other buffer; V, dO requested
@@ -1074,15 +1100,14 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
     }
-    // next chunk: V, dO and the row table into the other buffer; the
-    // chunk after it resolved and its Q, K requested
+    // next chunk: V, dO into the other buffer; the chunk after it resolved
+    // and its Q, K requested
     if (more) {
       put<T, D, NTH>(sm.tile[nb][TV], pa, nullptr, tid);
       put<T, D, NTH>(sm.tile[nb][TDO], pb, nullptr, tid);
-      publish(cs, nb);
       cur_next = cs.cr;
       if (c - 1 > c0) {
-        cs.resolve(sq, c - 2, replay_row, g, H, h, tid);
+        cs.resolve(sq, c - 2, replay_row, g, H, h, tid, mrow);
         fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
         fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
       }

@@ -79,6 +79,30 @@ template <> struct Vec4Raw<bf16> {
   }
 };
 
+// Stores through a buffer resource (raw, byte offsets): a lane whose offset
+// lies at or past the resource's size stores nothing, so a store can be
+// issued by every lane instead of inside a branch.
+constexpr uint32_t BUF_DROP = 0x80000000u;  // an offset past any resource here
+__device__ inline __amdgpu_buffer_rsrc_t buffer_rsrc(void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, static_cast<short>(0), static_cast<int>(bytes), 0x00020000);
+}
+template <typename T> struct BufVec4;
+template <> struct BufVec4<bf16> {
+  __device__ static inline void store(__amdgpu_buffer_rsrc_t r, uint32_t off, const f32x4& v) {
+    bf16x4 b;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) b[e] = static_cast<bf16>(v[e]);
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, b), r, static_cast<int>(off), 0, 0);
+  }
+};
+template <> struct BufVec4<float> {
+  __device__ static inline void store(__amdgpu_buffer_rsrc_t r, uint32_t off, const f32x4& v) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, static_cast<int>(off), 0, 0);
+  }
+};
+
 // LDS tile layout: 64 rows of COLS elements, row-major, each row padded by
 // 16 bytes.  Addresses are affine in (r, c), so every fragment read is a
 // per-lane base plus an immediate offset.  With the padding, 16-byte row
