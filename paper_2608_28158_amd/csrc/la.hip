@@ -430,7 +430,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   __shared__ T Ys[Tile<T, D>::SIZE];
   __shared__ ChunkMeta meta;
   const int side = side0 + static_cast<int>(blockIdx.z);
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
+  const int w = wave_id(t);
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const SeqInfo sq = seq_info(seq_tab + bk[BLK_SEQ] * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
@@ -625,7 +626,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ FwdSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
+  const int w = wave_id(t);
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
@@ -735,7 +737,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ BfSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
+  const int w = wave_id(t);
   const int col0 = C::CPW * w * 16;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
@@ -985,7 +988,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   __shared__ BrSmem<T, D> sm;
   const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, tid = threadIdx.x;
   const int side = tid >= C::NTHR ? 1 : 0;  // uniform over a wave
-  const int t = tid - side * C::NTHR, lane = tid & 63, w = t >> 6;
+  const int t = tid - side * C::NTHR, lane = tid & 63, w = wave_id(t);
   const int32_t* bk = blk_tab + b * BLK_WORDS;
   const int li = bk[BLK_SEQ];
   const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);

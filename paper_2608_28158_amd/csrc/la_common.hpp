@@ -471,6 +471,11 @@ __device__ inline RowRef pos_row(const SeqInfo& sq, int p, const int32_t* replay
   return RowRef{0, ROW_PAD, -1};
 }
 
+// The wave index of thread t, as a value the compiler knows to be uniform
+// over the wave (so that branches on it are scalar branches and values
+// derived from it live in scalar registers).
+__device__ inline int wave_id(int t) { return __builtin_amdgcn_readfirstlane(t >> 6); }
+
 // Cross-lane steps on DPP (data-parallel primitives: a VALU operand modifier
 // moving data between lanes of a 16-lane row), so that no step goes through
 // the LDS queue.  Lanes without a source read 0.
