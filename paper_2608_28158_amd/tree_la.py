@@ -112,9 +112,13 @@ class TreeLARunner:
         self._check_inputs(q, k, v, g)
         P = self.plan
         H, d = self.H, self.d
-        bank = torch.zeros((P.info["n_bank"], H, d, d), dtype=torch.float32, device=self.device)
+        # the tree-initial states lead the bank; every other slot is written by
+        # its producing round before a later round gathers it
+        bank = torch.empty((P.info["n_bank"], H, d, d), dtype=torch.float32, device=self.device)
         if S0_tree is not None:
             bank[: P.info["n_trees"]].copy_(S0_tree)
+        else:
+            bank[: P.info["n_trees"]].zero_()
         o = torch.empty_like(q) if outputs else None
         S_final = torch.empty((P.info["n_leaves"], H, d, d), dtype=torch.float32,
                               device=self.device)
@@ -150,10 +154,12 @@ class TreeLARunner:
         dg = torch.empty_like(g)
         R = P.info["R"]
         rep = torch.empty((max(R, 1), H, 2 * d + 1), dtype=torch.float32, device=self.device)
-        dS0_rounds = [None] * P.info["n_rounds"]
+        # dS0 of every sequence, in sequence (round) order; each round writes its slice
+        dS0_seq = torch.empty((P.info["n_seq"], H, d, d), dtype=torch.float32, device=self.device)
         for r in reversed(range(P.info["n_rounds"])):
             n = P.rounds[r]["n_seq"]
-            dS0 = torch.empty((n, H, d, d), dtype=torch.float32, device=self.device)
+            s0 = P.rounds[r]["seq_begin"]
+            dS0 = dS0_seq[s0:s0 + n]
             S0 = self.gather(fwd["bank"], r)
             ws = self._bytes(self.ws_bwd_saved[r])
             _lib.check(self.L.harts_la_bwd(
@@ -162,12 +168,11 @@ class TreeLARunner:
                 _ptr(dbank), _ptr(fwd["saved"][r]), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg),
                 _ptr(rep), _ptr(dS0), _ptr(ws), ws.numel(), self._stream()), "harts_la_bwd")
             self.scatter_add(dS0, dbank, r)
-            dS0_rounds[r] = dS0
         _lib.check(self.L.harts_replay_reduce(
             P.handle, _ptr(self.blob), self.code, H, d, d, _ptr(rep), _ptr(dk), _ptr(dv),
             _ptr(dg), self._stream()), "harts_replay_reduce")
         return dict(dq=dq, dk=dk, dv=dv, dg=dg, dS0_tree=dbank[: P.info["n_trees"]],
-                    dS0_seq=torch.cat(dS0_rounds, 0), dbank=dbank)
+                    dS0_seq=dS0_seq, dbank=dbank)
 
 
 class _TreeLAFn(torch.autograd.Function):
