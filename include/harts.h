@@ -192,7 +192,12 @@ int harts_plan_blob(const harts_plan_t* plan, void* host_dst, size_t bytes);
  *           S_final[final_leaf] = the state after its last token;
  *           saved (if non-NULL): what harts_la_bwd needs to skip the
  *           recompute (sized by harts_la_saved_size).
- *   S0       [n_seq_round, H, dk, dv] float32 (harts_state_gather output).
+ *   S0       [n_seq_round, H, dk, dv] float32 (harts_state_gather output),
+ *            or NULL: every sequence's initial state is then read in place
+ *            from bank (its row in the round's init index, a zero state
+ *            where that index is -1), which saves the gather's copy; bank
+ *            is then required.  Slots this round writes are never its own
+ *            initial states, so reading and writing bank in one call is safe.
  *   scale    output scale (1/sqrt(dk) is the usual choice).
  * Errors: HARTS_EINVAL (null required pointer, bad round, ws too small),
  * HARTS_EUNSUPPORTED (dtype / dims / chunk), HARTS_EHIP (launch failed).
@@ -210,6 +215,9 @@ int harts_la_fwd(const harts_plan_t* plan, int32_t round, const void* d_blob,
  * later round that consumed it has run and scattered its dS0 (harts_state_gather
  * mode 1).
  *
+ *   S0, bank  initial states as for harts_la_fwd: S0 [n_seq_round, H, dk, dv],
+ *             or S0 NULL and bank [n_bank, H, dk, dv] read through the round's
+ *             init index (bank is unused when S0 is given).
  *   dO        [C, H, dv] upstream gradient of o (own rows of the round read).
  *   dS_final  [n_leaves, H, dk, dv] upstream gradient of the final states.
  *   dbank     [n_bank, H, dk, dv] accumulated gradients of requested states.
@@ -227,10 +235,10 @@ int harts_la_fwd(const harts_plan_t* plan, int32_t round, const void* d_blob,
 int harts_la_bwd(const harts_plan_t* plan, int32_t round, const void* d_blob,
                  int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
                  const void* q, const void* k, const void* v, const float* g,
-                 const float* S0, const void* dO, const float* dS_final,
-                 const float* dbank, const void* saved, void* dq, void* dk_,
-                 void* dv_, float* dg, float* replay_grad, float* dS0,
-                 void* ws, size_t ws_bytes, void* stream);
+                 const float* S0, const float* bank, const void* dO,
+                 const float* dS_final, const float* dbank, const void* saved,
+                 void* dq, void* dk_, void* dv_, float* dg, float* replay_grad,
+                 float* dS0, void* ws, size_t ws_bytes, void* stream);
 
 /* Bytes of device scratch for a round's forward (pass 0) or backward
  * (pass 1; has_saved = 0 means the recompute path). */

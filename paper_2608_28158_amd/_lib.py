@@ -124,7 +124,7 @@ def lib():
                                vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.harts_la_bwd.restype = C.c_int
     L.harts_la_bwd.argtypes = [vp, i32, vp, i32, i32, i32, i32, f32,
-                               vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                               vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.harts_la_workspace_size.restype = C.c_int
     L.harts_la_workspace_size.argtypes = [vp, i32, i32, i32, i32, i32, i32, i32,

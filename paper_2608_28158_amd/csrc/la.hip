@@ -262,8 +262,8 @@ __device__ inline void state_to_lds(float* stg, const float* __restrict__ src, i
   }
 }
 // The whole staged load, in NPASS passes of D / NPASS stored rows each (for
-// LDS that holds only part of a state); every thread of the workgroup calls
-// it (it synchronises the workgroup).
+// LDS that holds only part of a state; src null: a zero state); every thread
+// of the workgroup calls it (it synchronises the workgroup).
 template <int D, int CPW, int NTH, int NPASS>
 __device__ inline void state_via_lds(f32x4* S, float* stg, const float* __restrict__ src,
                                      bool transpose, int w, int lane, int tid) {
@@ -276,7 +276,8 @@ __device__ inline void state_via_lds(f32x4* S, float* stg, const float* __restri
       const int e4 = tid + i * NTH;
       const int r = e4 / (D / 4), c = (e4 % (D / 4)) * 4;
       *reinterpret_cast<float4*>(stg + r * P + c) =
-          *reinterpret_cast<const float4*>(src + (static_cast<int64_t>(pass) * RP * D + e4 * 4));
+          src ? *reinterpret_cast<const float4*>(src + (static_cast<int64_t>(pass) * RP * D + e4 * 4))
+              : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     __syncthreads();
 #pragma unroll
@@ -476,6 +477,21 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   if (!side && t == 0) gam[bi] = Gs;
 }
 
+// Where the initial states of a round's sequences are: S0 [n_seq, H, d, d],
+// or (S0 null) rows of the boundary bank picked by the round's init index,
+// -1 meaning a zero state.
+struct InitSrc {
+  const float* S0;
+  const float* bank;
+  const int32_t* idx;
+};
+// Head h of sequence li's initial state, or nullptr for a zero state.
+__device__ inline const float* init_state(const InitSrc& is, int li, int H, int h, int64_t DD) {
+  if (is.S0) return is.S0 + (static_cast<int64_t>(li) * H + h) * DD;
+  const int i = is.idx[li];
+  return i >= 0 ? is.bank + (static_cast<int64_t>(i) * H + h) * DD : nullptr;
+}
+
 // ---------------------------------------------------------------------------
 // element-parallel chains over the blocks of every sequence
 // ---------------------------------------------------------------------------
@@ -487,7 +503,7 @@ constexpr int SCAN_PF = 8;
 template <int D>
 __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
-    const float* __restrict__ S0, const float* __restrict__ dSb, const float* __restrict__ gam,
+    const InitSrc is, const float* __restrict__ dSb, const float* __restrict__ gam,
     float* __restrict__ S_end, float* __restrict__ bank, float* __restrict__ S_final) {
   constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
   constexpr int NSW = static_cast<int>(SS4 / SCAN_THR);
@@ -495,7 +511,8 @@ __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
   const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + threadIdx.x;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
-  float4 s = reinterpret_cast<const float4*>(S0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4];
+  const float* s0 = init_state(is, li, H, h, SS4 * 4);
+  float4 s = s0 ? reinterpret_cast<const float4*>(s0)[e4] : make_float4(0.f, 0.f, 0.f, 0.f);
   for (int bg = b0; bg < b0 + nb; bg += SCAN_PF) {
     float4 x[SCAN_PF];
     float gm[SCAN_PF];
@@ -621,7 +638,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ S0, const float* __restrict__ S_end, T* __restrict__ o) {
+    const InitSrc is, const float* __restrict__ S_end, T* __restrict__ o) {
   using C = Cfg<T, D>;
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
@@ -646,7 +663,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   static_assert(D / 2 * (D + 4) * 4 <= static_cast<int>(sizeof(FwdSmem<T, D>) - sizeof(ChunkMeta)),
                 "half a state fits the tiles");
   state_via_lds<D, C::CPW, C::NTHR, 2>(S, reinterpret_cast<float*>(&sm.Q[0]),
-                                       bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                       bk[BLK_IDX] == 0 ? init_state(is, li, H, h, DD)
                                                         : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
                                        false, w, lane, t);
   for (int c = c0; c < c_end; ++c) {
@@ -731,7 +748,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
     const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const T* __restrict__ dO, const float* __restrict__ S0, const float* __restrict__ S_end,
+    const T* __restrict__ dO, const InitSrc is, const float* __restrict__ S_end,
     T* __restrict__ dq, float* __restrict__ rq_out) {
   using C = Cfg<T, D>;
   using RB = RegB<T>;
@@ -757,7 +774,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   // the start state, staged through the (still unused) tiles
   static_assert(D * (D + 4) * 4 <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)), "state fits the tiles");
   state_via_lds<D, C::CPW, C::NTHR, 1>(St, reinterpret_cast<float*>(&sm.dO[0]),
-                                       bk[BLK_IDX] == 0 ? S0 + (static_cast<int64_t>(li) * H + h) * DD
+                                       bk[BLK_IDX] == 0 ? init_state(is, li, H, h, DD)
                                                         : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
                                        true, w, lane, t);
   for (int c = c0; c < c_end; ++c) {
@@ -1320,12 +1337,13 @@ struct Blob {
   const int32_t* blk_tab;
   const int32_t* blk_order;
   const int32_t* replay_row;
+  const int32_t* init_idx;
 };
 
 Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   const int32_t* b = static_cast<const int32_t*>(d_blob);
   const RoundLayout& L = p->rounds[round];
-  return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_order, b + p->off_replay_row};
+  return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_order, b + p->off_replay_row, b + L.init_idx};
 }
 
 // Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b).
@@ -1344,14 +1362,14 @@ int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, 
 
 // Chain of block summaries: S_end per block, requested boundary states, final states.
 template <int D>
-int launch_fwd_scan(const harts_plan_t* p, int32_t round, const Blob& B, int H, const float* S0,
+int launch_fwd_scan(const harts_plan_t* p, int32_t round, const Blob& B, int H, const InitSrc& is,
                     const float* dSb, const float* gam, float* S_end, float* bank, float* S_final,
                     hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   constexpr int NSW = D * D / 4 / SCAN_THR;
   ProfScope ps("k_fwd_blockscan", s);
   hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
-                     B.seq_tab, B.blk_tab, H, S0, dSb, gam, S_end, bank, S_final);
+                     B.seq_tab, B.blk_tab, H, is, dSb, gam, S_end, bank, S_final);
   return hip_check("k_fwd_blockscan");
 }
 
@@ -1365,16 +1383,17 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   float* dSb = reinterpret_cast<float*>(ws);
   float* S_end = reinterpret_cast<float*>(saved);
   float* gam = reinterpret_cast<float*>(saved + z.blk_state);
+  const InitSrc is{S0, bank, B.init_idx};
   if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, nullptr, g, dSb, nullptr,
                                       gam, 0, 1, s))
     return rc;
-  if (int rc = launch_fwd_scan<D>(p, round, B, H, S0, dSb, gam, S_end, bank, S_final, s)) return rc;
+  if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam, S_end, bank, S_final, s)) return rc;
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
   {
     ProfScope ps("k_fwd_block", s);
     hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
-                       static_cast<const T*>(k), static_cast<const T*>(v), g, S0, S_end,
+                       static_cast<const T*>(k), static_cast<const T*>(v), g, is, S_end,
                        static_cast<T*>(o));
   }
   return hip_check("k_fwd_block");
@@ -1383,12 +1402,13 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
 template <typename T, int D>
 int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, float scale,
             const void* q, const void* k, const void* v, const float* g, const float* S0,
-            const void* dO, const float* dS_final, const float* dbank, const char* saved,
+            const float* bank, const void* dO, const float* dS_final, const float* dbank, const char* saved,
             char* ws, void* dq, void* dk, void* dv, float* dg, float* rep_grad, float* dS0,
             hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   const Sizes z = sizes(p, round, H, D);
   const Blob B = blob_ptrs(p, round, d_blob);
+  const InitSrc is{S0, bank, B.init_idx};
   char* w = ws;
   float* U = reinterpret_cast<float*>(w);
   w += z.blk_state;
@@ -1409,7 +1429,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     float* gam_w = reinterpret_cast<float*>(sv + z.blk_state);
     if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, dSb, U, gam_w, 0, 2, s))
       return rc;
-    if (int rc = launch_fwd_scan<D>(p, round, B, H, S0, dSb, gam_w, S_end_w, nullptr, nullptr, s))
+    if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam_w, S_end_w, nullptr, nullptr, s))
       return rc;
     saved = sv;
   } else if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, nullptr, U,
@@ -1431,7 +1451,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
-                       static_cast<const T*>(dO), S0, S_end, static_cast<T*>(dq), rq);
+                       static_cast<const T*>(dO), is, S_end, static_cast<T*>(dq), rq);
   }
   if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
@@ -1484,7 +1504,7 @@ extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_
                             const float* S0, void* o, float* S_final, float* bank, void* saved,
                             void* ws, size_t ws_bytes, void* stream) {
   if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_fwd")) return rc;
-  if (!d_blob || !q || !k || !v || !g || !S0 || !S_final || !ws || (!bank && p->n_slots > 0)) {
+  if (!d_blob || !q || !k || !v || !g || !S_final || !ws || (!bank && (p->n_slots > 0 || !S0))) {
     set_error("harts_la_fwd: NULL required pointer");
     return HARTS_EINVAL;
   }
@@ -1512,19 +1532,20 @@ extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_
 extern "C" int harts_la_bwd(const harts_plan_t* p, int32_t round, const void* d_blob,
                             int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
                             const void* q, const void* k, const void* v, const float* g,
-                            const float* S0, const void* dO, const float* dS_final,
-                            const float* dbank, const void* saved, void* dq, void* dk_, void* dv_,
-                            float* dg, float* replay_grad, float* dS0, void* ws, size_t ws_bytes,
-                            void* stream) {
+                            const float* S0, const float* bank, const void* dO,
+                            const float* dS_final, const float* dbank, const void* saved, void* dq,
+                            void* dk_, void* dv_, float* dg, float* replay_grad, float* dS0,
+                            void* ws, size_t ws_bytes, void* stream) {
   if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_bwd")) return rc;
-  if (!d_blob || !q || !k || !v || !g || !S0 || !dO || !dS_final || !dq || !dk_ || !dv_ || !dg ||
+  if (!d_blob || !q || !k || !v || !g || (!S0 && !bank) || !dO || !dS_final || !dq || !dk_ || !dv_ || !dg ||
       !dS0 || (!dbank && p->n_slots > 0) || (!replay_grad && p->R > 0) || !ws) {
     set_error("harts_la_bwd: NULL required pointer");
     return HARTS_EINVAL;
   }
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) || !aligned16(dq) ||
       !aligned16(dk_) || !aligned16(dv_) || !aligned16(saved) || !aligned16(ws) ||
-      !aligned16(dS0) || !aligned16(dS_final) || !aligned16(S0) || !aligned16(dbank)) {
+      !aligned16(dS0) || !aligned16(dS_final) || !aligned16(S0) || !aligned16(bank) ||
+      !aligned16(dbank)) {
     set_error("harts_la_bwd: pointers must be 16-byte aligned");
     return HARTS_EINVAL;
   }
@@ -1538,12 +1559,12 @@ extern "C" int harts_la_bwd(const harts_plan_t* p, int32_t round, const void* d_
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == HARTS_BF16) {
     if (dk == 128)
-      return run_bwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank,
+      return run_bwd<bf16, 128>(p, round, d_blob, H, scale, q, k, v, g, S0, bank, dO, dS_final, dbank,
                                 sv, w, dq, dk_, dv_, dg, replay_grad, dS0, s);
-    return run_bwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank, sv,
+    return run_bwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, bank, dO, dS_final, dbank, sv,
                              w, dq, dk_, dv_, dg, replay_grad, dS0, s);
   }
-  return run_bwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, dO, dS_final, dbank, sv,
+  return run_bwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, bank, dO, dS_final, dbank, sv,
                             w, dq, dk_, dv_, dg, replay_grad, dS0, s);
 }
 extern "C" int harts_state_gather(const float* src, const int32_t* idx, int32_t n,

@@ -1,9 +1,11 @@
 """Round driver and autograd wrapper for tree-packed linear attention.
 
 Each execution round is one packed call (Sec. 3.4, "Round-wise execution"):
-``harts_state_gather`` builds the round's initial states from the state bank
-(tree initial states, then the boundary states written by earlier rounds),
-``harts_la_fwd`` runs the round.  The backward walks the rounds in reverse
+``harts_la_fwd`` runs the round, reading each sequence's initial state from
+the state bank (tree initial states, then the boundary states written by
+earlier rounds) through the round's init index; with ``gather_init=True``
+the round's initial states are first gathered into a dense buffer by
+``harts_state_gather`` instead.  The backward walks the rounds in reverse
 (Sec. 3.4, "Differentiable boundary states"): ``harts_la_bwd`` per round,
 then the scatter-add adjoint of the gather into the bank gradient, and
 finally ``harts_replay_reduce``.  With ``recompute=True`` the forward keeps
@@ -38,8 +40,10 @@ def _dtype_code(dt):
 class TreeLARunner:
     """Forward / backward of one linear-attention layer over a plan."""
 
-    def __init__(self, plan: HartsPlan, H: int, d: int, dtype, device, scale=None):
+    def __init__(self, plan: HartsPlan, H: int, d: int, dtype, device, scale=None,
+                 gather_init=False):
         self.plan = plan
+        self.gather_init = gather_init
         self.H, self.d = H, d
         self.dtype = dtype
         self.code = _dtype_code(dtype)
@@ -124,7 +128,7 @@ class TreeLARunner:
                               device=self.device)
         saved = []
         for r in range(P.info["n_rounds"]):
-            S0 = self.gather(bank, r)
+            S0 = self.gather(bank, r) if self.gather_init else None
             sv = self._bytes(self.saved_bytes[r]) if keep_states else None
             ws = self._bytes(self.ws_fwd[r] if keep_states else self.ws_fwd_nosave[r])
             _lib.check(self.L.harts_la_fwd(
@@ -160,11 +164,12 @@ class TreeLARunner:
             n = P.rounds[r]["n_seq"]
             s0 = P.rounds[r]["seq_begin"]
             dS0 = dS0_seq[s0:s0 + n]
-            S0 = self.gather(fwd["bank"], r)
+            S0 = self.gather(fwd["bank"], r) if self.gather_init else None
             ws = self._bytes(self.ws_bwd_saved[r])
             _lib.check(self.L.harts_la_bwd(
                 P.handle, r, _ptr(self.blob), self.code, H, d, d, self.scale,
-                _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S0), _ptr(dO), _ptr(dS_final),
+                _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S0), _ptr(fwd["bank"]), _ptr(dO),
+                _ptr(dS_final),
                 _ptr(dbank), _ptr(fwd["saved"][r]), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg),
                 _ptr(rep), _ptr(dS0), _ptr(ws), ws.numel(), self._stream()), "harts_la_bwd")
             self.scatter_add(dS0, dbank, r)

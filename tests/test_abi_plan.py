@@ -161,7 +161,7 @@ def test_device_calls_validate_before_launch(L):
     assert rc == _lib.HARTS_EINVAL
     rc = L.harts_la_bwd(p.handle, 0, null, _lib.HARTS_BF16, 16, 128, 128, C.c_float(0.1),
                         null, null, null, null, null, null, null, null, null, null, null, null,
-                        null, null, null, null, C.c_size_t(0), null)
+                        null, null, null, null, null, C.c_size_t(0), null)
     assert rc == _lib.HARTS_EINVAL
     # state gather: bad mode / sizes rejected, an empty gather is a no-op
     g = L.harts_state_gather

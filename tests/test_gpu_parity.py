@@ -34,7 +34,7 @@ def _canon(t, phys):
     return t.float().cpu().numpy()[phys]
 
 
-def run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute=False):
+def run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute=False, gather_init=False):
     from paper_2608_28158_amd.plan import HartsPlan
     from paper_2608_28158_amd.tree_la import TreeLARunner
     plan = HartsPlan(parent, seg_len, 64)
@@ -45,7 +45,7 @@ def run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute=False):
     dO = _dev(x["dO"], phys, tdt)
     dSf = torch.from_numpy(x["dS_final"]).cuda()
     S0 = torch.from_numpy(x["S0"]).cuda()
-    runner = TreeLARunner(plan, H, d, tdt, "cuda", scale)
+    runner = TreeLARunner(plan, H, d, tdt, "cuda", scale, gather_init=gather_init)
     fwd = runner.forward(q, k, v, g, S0, keep_states=not recompute)
     bwd = runner.backward(q, k, v, g, dO, dSf, fwd=None if recompute else fwd, S0_tree=S0,
                           recompute=recompute)
@@ -94,6 +94,20 @@ def test_config0_recompute_matches_saved_bitwise():
     for name in a:
         assert np.array_equal(a[name], b[name]), name   # recompute-forward
         assert np.array_equal(a[name], c[name]), name   # run-to-run determinism
+
+
+def test_gathered_and_indexed_initial_states_agree_bitwise():
+    """Initial states read in place from the bank (S0 = NULL) and gathered
+    into a dense buffer first (harts_state_gather) give the same bits, on
+    the Figure 1 tree and on a multi-round config-1 forest."""
+    for cfg_i, dtype in ((0, "f32"), (1, "bf16")):
+        f, cfg, x = config_inputs(cfg_i, s0_scale=0.5)
+        print(f"[gpu] config{cfg_i} gathered vs indexed initial states", flush=True)
+        sc = cfg["d"] ** -0.5
+        a, _ = run_gpu(f.parent, f.seg_len, x, cfg["H"], cfg["d"], dtype, sc, True, False)
+        b, _ = run_gpu(f.parent, f.seg_len, x, cfg["H"], cfg["d"], dtype, sc, True, True)
+        for name in a:
+            assert np.array_equal(a[name], b[name]), name
 
 
 def _random_forest(r, n, max_len, p_root=0.1):
