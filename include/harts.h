@@ -189,7 +189,8 @@ int harts_plan_blob(const harts_plan_t* plan, void* host_dst, size_t bytes);
  *   writes  o for its own rows only (o may be NULL: state pass only, the
  *           recompute-forward of the backward -- states, no outputs);
  *           bank[req] = S_c for each requested chunk boundary c;
- *           S_final[final_leaf] = the state after its last token;
+ *           S_final[final_leaf] = the state after its last token (S_final
+ *           may be NULL: not written, e.g. in a recompute-forward);
  *           saved (if non-NULL): what harts_la_bwd needs to skip the
  *           recompute (sized by harts_la_saved_size).
  *   S0       [n_seq_round, H, dk, dv] float32 (harts_state_gather output),

@@ -1504,7 +1504,7 @@ extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_
                             const float* S0, void* o, float* S_final, float* bank, void* saved,
                             void* ws, size_t ws_bytes, void* stream) {
   if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_fwd")) return rc;
-  if (!d_blob || !q || !k || !v || !g || !S_final || !ws || (!bank && (p->n_slots > 0 || !S0))) {
+  if (!d_blob || !q || !k || !v || !g || !ws || (!bank && (p->n_slots > 0 || !S0))) {
     set_error("harts_la_fwd: NULL required pointer");
     return HARTS_EINVAL;
   }

@@ -124,8 +124,9 @@ class TreeLARunner:
         else:
             bank[: P.info["n_trees"]].zero_()
         o = torch.empty_like(q) if outputs else None
+        # the state-only pass (recompute-forward) writes no final states
         S_final = torch.empty((P.info["n_leaves"], H, d, d), dtype=torch.float32,
-                              device=self.device)
+                              device=self.device) if outputs else None
         saved = []
         for r in range(P.info["n_rounds"]):
             S0 = self.gather(bank, r) if self.gather_init else None
