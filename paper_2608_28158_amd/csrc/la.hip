@@ -211,22 +211,9 @@ __device__ inline void meta_publish(ChunkMeta& m, const ChunkSrc<T, D, NTH>& cs,
   GL = lane_value(x, CB - 1);
 }
 
-// A wave's part of a [D x D] state: tile j * NT + i is rows 16 i.., columns
-// 16 (CPW w + j).. of the matrix (or of its transpose).
-template <int D, int CPW>
-__device__ inline void state_load(f32x4* S, const float* src, bool transpose, int w, int lane) {
-  constexpr int NT = D / 16;
-#pragma unroll
-  for (int j = 0; j < CPW; ++j)
-#pragma unroll
-    for (int i = 0; i < NT; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
-        S[j * NT + i][r] = src ? (transpose ? src[b * D + a] : src[a * D + b]) : 0.f;
-      }
-}
-
+// A wave's part of a [D x D] state is held in the accumulator layout: tile
+// j * NT + i covers rows 16 i.., columns 16 (CPW w + j).. of the matrix (or of
+// its transpose), lane (g, c) element r at row 16 i + 4g + r, column .. + c.
 template <int D, int CPW>
 __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) {
   constexpr int NT = D / 16;
@@ -241,7 +228,7 @@ __device__ inline void state_store(float* dst, const f32x4* S, int w, int lane) 
 
 // A [D x D] float state staged through LDS: read once with 16-byte loads by
 // all NTH threads (row pitch D + 4 floats), then handed out to the waves in
-// the accumulator layout of state_load.  The pitch makes the reads of the
+// their accumulator layout (above).  The pitch makes the reads of the
 // plain layout free of bank conflicts; the transposed ones conflict up to
 // four ways, once per block.
 template <int D>
@@ -308,54 +295,11 @@ __device__ inline void state_from_lds(f32x4* S, const float* stg, bool transpose
       }
 }
 
-// Row block it (the wave index) of a masked score tile, all four column
-// tiles: P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for n <= m, 0 above the
-// diagonal.  Tiles above the diagonal are computed and discarded: the wave
-// owning the last row block has four tiles to compute in any case, and the
-// code stays free of branches.  With PT the tile is stored transposed
-// (P[n][m] holds the value of row m, column n).
-template <typename T, int D, bool PT = false>
-__device__ __forceinline__ void score_tile(T* P, const T* Lt, const T* Rt, const float* G, float f,
-                                           int it, int lane) {
-  using TA = Tile<T, CB>;
-  using TD = Tile<T, D>;
-  using F = Frag<T>;
-  f32x4 c[CB / 16];
-#pragma unroll
-  for (int jt = 0; jt < CB / 16; ++jt) c[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 1
-  for (int k = 0; k < D; k += F::KSTEP) {
-    // all five reads of the step are issued before its first product
-    const typename F::V a = F::template kc<TD>(Lt, it * 16, k, lane);
-    typename F::V b[CB / 16];
-#pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) b[jt] = F::template kc<TD>(Rt, jt * 16, k, lane);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int jt = 0; jt < CB / 16; ++jt) F::mma(c[jt], a, b[jt]);
-  }
-  const f32x4 Gm = row_vec(G, it * 16, lane);
-#pragma unroll
-  for (int jt = 0; jt < CB / 16; ++jt) {
-    const int n = jt * 16 + acc_col(lane);
-    const float Gn = G[n];
-    f32x4 v;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = it * 16 + acc_row(lane, r);
-      v[r] = n <= m ? c[jt][r] * __expf(Gm[r] - Gn) * f : 0.f;
-      if (!PT) P[TA::at(m, n)] = Elem<T>::from_f(v[r]);
-    }
-    // transposed: the lane's four rows m are contiguous in row n of P^T
-    if (PT) Vec4<T>::store(P + TA::at(n, it * 16 + acc_row(lane, 0)), v);
-  }
-}
-
 // The masked score tile in three 32 x 32 blocks, (row half, column half) =
 // (0, 0), (1, 0), (1, 1) for waves 0, 1, 2; the block above the diagonal is
 // never read by the consumers and wave 3 does nothing here.  Each block is
 // 2 x 2 tiles of 16 and reads 32 rows of each operand (the four row blocks
-// of score_tile read all of R four times).  Inside the diagonal blocks the
+// of 16 rows each would read all of R four times).  Inside the diagonal blocks the
 // tile above the diagonal is skipped and stored as zeros: the consumers'
 // 32-deep steps read it.  P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for
 // n <= m; with PT the tile is stored transposed.

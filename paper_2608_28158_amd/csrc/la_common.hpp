@@ -209,18 +209,6 @@ template <> struct Frag<float> {
   }
 };
 
-// c += A * B over K; A, B described as (tile, layout, kc/km, origin).
-template <typename T, typename LA, bool A_KM, typename LB, bool B_KM>
-__device__ inline void tile(f32x4& c, const T* A, int am, const T* B, int bn, int K, int lane) {
-  using F = Frag<T>;
-#pragma unroll
-  for (int k = 0; k < K; k += F::KSTEP) {
-    const typename F::V a = A_KM ? F::template km<LA>(A, k, am, lane) : F::template kc<LA>(A, am, k, lane);
-    const typename F::V b = B_KM ? F::template km<LB>(B, k, bn, lane) : F::template kc<LB>(B, bn, k, lane);
-    F::mma(c, a, b);
-  }
-}
-
 // c[j] += A * B_j for the NJ output tiles of one row block (origins bn + 16 j),
 // the A fragment shared; B is k-major.  k runs over [k0, K).
 // With SWAP the operands of each product trade places, which leaves the
@@ -413,28 +401,7 @@ __device__ inline void opaque_state(f32x4* S) {
   for (int i = 0; i < N; ++i) asm volatile("" : "+v"(S[i]));
 }
 
-// Reads in the accumulator layout of a 16x16 tile: lane (g, i), g = lane / 16,
-// receives rows r0 + 4g + e (e = 0..3) of column c0 + i.  For bf16 this is one
-// transpose read (lane i of group g points at row r0 + 4g + i/4, column
-// c0 + 4 (i % 4)); per-row float vectors are one 16-byte read.
-template <typename T> struct ColRead;
-template <> struct ColRead<bf16> {
-  template <typename L>
-  __device__ static inline f32x4 get(const bf16* t, int r0, int c0, int lane) {
-    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const int r = r0 + (lane >> 4) * 4 + ((lane & 15) >> 2), c = c0 + 4 * (lane & 3);
-    const bf16x4 b = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(t + L::at(r, c))));
-    return f32x4{static_cast<float>(b[0]), static_cast<float>(b[1]), static_cast<float>(b[2]),
-                 static_cast<float>(b[3])};
-  }
-};
-template <> struct ColRead<float> {
-  template <typename L>
-  __device__ static inline f32x4 get(const float* t, int r0, int c0, int lane) {
-    const int r = r0 + (lane >> 4) * 4, c = c0 + (lane & 15);
-    return f32x4{t[L::at(r, c)], t[L::at(r + 1, c)], t[L::at(r + 2, c)], t[L::at(r + 3, c)]};
-  }
-};
+// Four consecutive floats of a per-row vector at rows r0 + 4g .. + 3 (lane group g).
 __device__ inline f32x4 row_vec(const float* v, int r0, int lane) {
   return *reinterpret_cast<const f32x4*>(v + r0 + (lane >> 4) * 4);
 }
@@ -484,21 +451,9 @@ __device__ inline float dpp(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
                                                                0xF, 0xF, true));
 }
-constexpr int DPP_QUAD_XOR1 = 0xB1;      // quad_perm [1, 0, 3, 2]
-constexpr int DPP_QUAD_XOR2 = 0x4E;      // quad_perm [2, 3, 0, 1]
 constexpr int DPP_ROW_SHL = 0x100;       // + n: lane i reads lane i + n of its row
 constexpr int DPP_ROW_SHR = 0x110;       // + n: lane i reads lane i - n of its row
-constexpr int DPP_ROW_MIRROR = 0x140;    // lane i reads lane 15 - i
-constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane i reads lane 7 - i of its half row
 
-// Sum over the 16 lanes of a row (the lanes that share accumulator rows).
-__device__ inline float sum16(float x) {
-  x += dpp<DPP_QUAD_XOR1>(x);
-  x += dpp<DPP_QUAD_XOR2>(x);
-  x += dpp<DPP_ROW_HALF_MIRROR>(x);
-  x += dpp<DPP_ROW_MIRROR>(x);
-  return x;
-}
 
 // Inclusive prefix sum over the 64 lanes of a wave (lane order).
 __device__ inline float wave_prefix_sum(float x, int lane) {
