@@ -167,6 +167,16 @@ def test_config1_spine_bf16():
             label="config1")
 
 
+@pytest.mark.parametrize("min_blocks,sizes", [("1", "64"), ("12", "16 and 24"), ("16", "12")])
+def test_config1_block_sizes(min_blocks, sizes, monkeypatch):
+    """The same workload cut into blocks of other sizes (the planner's block
+    target, read when the plan is built) stays within tolerance."""
+    monkeypatch.setenv("HARTS_MIN_BLOCKS", min_blocks)
+    f, cfg, x = config_inputs(1)
+    compare(f.parent, f.seg_len, x, cfg["H"], cfg["d"], "bf16", heads=[0, 9],
+            label=f"config1 blocks of {sizes} chunks")
+
+
 def test_config2_agentic_bf16_sampled_heads():
     f, cfg, x = config_inputs(2)
     compare(f.parent, f.seg_len, x, cfg["H"], cfg["d"], "bf16", heads=[3], label="config2")
