@@ -77,43 +77,54 @@ def phys_index(seg_len, seg_row):
 
 
 def algorithmic_bytes(plan, H, d, el):
-    """Bytes each kernel must move for its job over one step, by kernel.
+    """Bytes each kernel must move for its job over one step (forward, then
+    the backward with the recompute-forward), by kernel, for the launches the
+    runner makes.
 
     Rows are packed rows (own + replay); q, o, dO and dq exist on own rows
     only.  Block-level states (summaries, chained block-end states, local
     adjoints) are float32 H*d*d each and are counted for the kernels whose
     job is to produce or consume them; per-chunk states are never
-    materialised.  Returns (bytes per step, launches per step) per kernel."""
+    materialised.  Initial states are read in place from the bank (no
+    gather).  Returns (bytes per step, launches per step) per kernel."""
     st = H * d * d * 4
     K = plan.info["n_rounds"]
-    b = dict.fromkeys(["k_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder",
-                       "k_bwd_blockscan", "k_bwd_revorder", "k_dg_carry", "k_gather",
-                       "k_scatter_add"], 0)
+    names = ["k_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan",
+             "k_bwd_revorder", "k_dg_carry", "k_scatter_add", "k_replay_reduce"]
+    b = dict.fromkeys(names, 0)
+    n = dict.fromkeys(names, 0)
+    init_bank = np.asarray(plan["seq_init_bank"])
     for r in plan.rounds:
         rows, own, rep, nseq, nblk = (r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"],
                                       r["n_blk"])
-        nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i]
-                       for i in range(r["seq_begin"], r["seq_begin"] + nseq)))
+        s0, s1 = r["seq_begin"], r["seq_begin"] + nseq
+        nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i] for i in range(s0, s1)))
+        ninit = int(np.sum(init_bank[s0:s1] >= 0))            # sequences with a non-zero start
         kv = rows * H * (2 * d * el + 4)                       # k, v, g of every packed row
         qdo = own * H * 2 * d * el + rows * H * 4                # q, dO of own rows, g
-        # side 0 (k, v) in the forward and the recompute pass, side 1 (q, dO) in backward
+        # forward chain of block-end states: summaries in, states out, the
+        # initial states in, requested states out (the final states in the
+        # forward only; the recompute pass writes none)
+        b["k_fwd_blockscan"] += (2 * nblk * st + ninit * st + nreq * st + nseq * st
+                                 + 2 * nblk * st + ninit * st + nreq * st)
+        n["k_fwd_blockscan"] += 2
+        # summaries: side 0 in the forward and the recompute pass, side 1 in backward
         b["k_blocksum"] += 2 * (kv + nblk * st) + qdo + nblk * st
-        b["k_fwd_blockscan"] += 2 * (nseq * st + 2 * nblk * st + nreq * st + nseq * st)
-        b["k_fwd_block"] += kv + own * H * 2 * d * el + nblk * st
+        n["k_blocksum"] += 3
+        b["k_fwd_block"] += kv + own * H * 2 * d * el + ninit * st + nblk * st
         b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + nblk * st
         b["k_bwd_blockscan"] += 4 * nblk * st + nseq * st + nreq * st + nseq * st
         b["k_bwd_revorder"] += (kv + own * H * (2 * d * el + 2 * d * el + 4)
                                 + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st)
         b["k_dg_carry"] += rows * H * 8
-        b["k_gather"] += 2 * 2 * nseq * st                     # forward + recompute
         b["k_scatter_add"] += 3 * nseq * st
+        for name in ("k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan", "k_bwd_revorder",
+                     "k_dg_carry", "k_scatter_add"):
+            n[name] += 1
     R = plan.info["R"]
     b["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
-    launches = {"k_blocksum": 2 * K, "k_fwd_blockscan": 2 * K, "k_fwd_block": K,
-                "k_bwd_fwdorder": K, "k_bwd_blockscan": K, "k_bwd_revorder": K,
-                "k_dg_carry": K, "k_gather": 2 * K, "k_scatter_add": K,
-                "k_replay_reduce": 1 if R else 0}
-    return b, launches
+    n["k_replay_reduce"] = 1 if R else 0
+    return b, n
 
 
 def read_traffic(kernel, workload_key):
