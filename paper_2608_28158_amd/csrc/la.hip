@@ -146,6 +146,14 @@ struct ChunkMeta {
   int rowk[CB];  // physical row * 4 + kind (replay index = replay_off + position)
 };
 
+// 1 KiB of zeros: rows that must read as zero (padding, or rows of a kind a
+// tensor does not hold) are loaded from here, so that every lane issues the
+// same unconditional load and no load sits in a divergent branch (a load in
+// one, followed by a write of its register in the other, would have to
+// complete before the branches join).
+__device__ __align__(16) uint4 kZeroRow[64] = {};  // never written
+static_assert(sizeof(kZeroRow) >= 256 * sizeof(float), "one zero row of up to 256 floats");
+
 // Where this thread's rows of one chunk live, resolved one chunk ahead: the
 // rows it stages (all threads) and, for the wave that publishes the chunk's
 // row table (mrow = its lane, -1 elsewhere), row mrow of the chunk with its g.
@@ -168,7 +176,8 @@ struct ChunkSrc {
       refs.resolve(seq, c, replay_row, t);
       if (mrow >= 0) {
         mr = pos_row(seq, c * CB + mrow, replay_row);
-        gv = mr.kind != ROW_PAD ? g[static_cast<int64_t>(mr.row) * H + h] : 0.f;
+        gv = *(mr.kind != ROW_PAD ? g + static_cast<int64_t>(mr.row) * H + h
+                                  : reinterpret_cast<const float*>(kZeroRow));
       }
     }
   }
@@ -193,9 +202,9 @@ __device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkS
   for (int i = 0; i < C::NV; ++i) {
     const int d0 = ((t + i * C::NTHR) % C::VPR) * C::VE;
     const int row = cs.refs.rk[i] >> 2;
-    dst[i].u = (cs.refs.rk[i] & 3) >= min_kind
-                   ? *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(row) * H + h) * D + d0)
-                   : make_uint4(0u, 0u, 0u, 0u);
+    const T* p = (cs.refs.rk[i] & 3) >= min_kind ? src + (static_cast<int64_t>(row) * H + h) * D + d0
+                                                 : reinterpret_cast<const T*>(kZeroRow) + d0;
+    dst[i].u = *reinterpret_cast<const uint4*>(p);
   }
 }
 
