@@ -1159,28 +1159,37 @@ __global__ void k_scatter_add(const float4* __restrict__ src, const int32_t* __r
   }
 }
 
+// One wave per (compact row, head): lane l owns elements 4l .. 4l + 3 of the
+// row's 2D gradient values (dk then dv), lane 0 also its dg; each sums the
+// row's replay instances in order and adds the sum to the own-row gradient.
+constexpr int RED_WAVES = 4;
 template <typename T, int D>
-__global__ void k_replay_reduce(const int32_t* __restrict__ red_rows,
-                                const int32_t* __restrict__ red_off,
-                                const int32_t* __restrict__ red_idx, int H,
-                                const float* __restrict__ rep_grad, T* __restrict__ dk,
-                                T* __restrict__ dv, float* __restrict__ dg) {
+__global__ __launch_bounds__(64 * RED_WAVES) void k_replay_reduce(
+    const int32_t* __restrict__ red_rows, const int32_t* __restrict__ red_off,
+    const int32_t* __restrict__ red_idx, int H, const float* __restrict__ rep_grad,
+    T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dg) {
   constexpr int RG = 2 * D + 1;
-  const int u = blockIdx.x, h = blockIdx.y;
+  static_assert(2 * D / 4 <= 64, "a wave covers the row");
+  const int u = blockIdx.x, lane = threadIdx.x & 63;
+  const int h = blockIdx.y * RED_WAVES + wave_id(threadIdx.x);
+  if (h >= H) return;
   const int64_t row = red_rows[u];
   const int b = red_off[u], e = red_off[u + 1];
-  for (int x = threadIdx.x; x < RG; x += blockDim.x) {
-    float s = 0.f;
-    for (int j = b; j < e; ++j) s += rep_grad[(static_cast<int64_t>(red_idx[j]) * H + h) * RG + x];
-    if (x < D) {
-      T* p = dk + (row * H + h) * D + x;
-      *p = Elem<T>::from_f(Elem<T>::to_f(*p) + s);
-    } else if (x < 2 * D) {
-      T* p = dv + (row * H + h) * D + (x - D);
-      *p = Elem<T>::from_f(Elem<T>::to_f(*p) + s);
-    } else {
-      dg[row * H + h] += s;
+  if (lane < 2 * D / 4) {
+    f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = b; j < e; ++j) {
+      const float* r = rep_grad + (static_cast<int64_t>(red_idx[j]) * H + h) * RG + 4 * lane;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[i] += r[i];
     }
+    const int x = 4 * lane;
+    T* p = x < D ? dk + (row * H + h) * D + x : dv + (row * H + h) * D + (x - D);
+    Vec4<T>::store(p, Vec4<T>::load(p) + s);
+  }
+  if (lane == 0) {
+    float s = 0.f;
+    for (int j = b; j < e; ++j) s += rep_grad[(static_cast<int64_t>(red_idx[j]) * H + h) * RG + 2 * D];
+    dg[row * H + h] += s;
   }
 }
 
@@ -1562,19 +1571,19 @@ extern "C" int harts_replay_reduce(const harts_plan_t* p, const void* d_blob, in
   }
   const int32_t* b = static_cast<const int32_t*>(d_blob);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const dim3 grid(static_cast<unsigned>(p->n_red), H);
+  const dim3 grid(static_cast<unsigned>(p->n_red), (H + RED_WAVES - 1) / RED_WAVES);
   ProfScope ps("k_replay_reduce", s);
   if (dtype == HARTS_BF16) {
     if (dk == 128)
-      hipLaunchKernelGGL((k_replay_reduce<bf16, 128>), grid, dim3(256), 0, s, b + p->off_red_rows,
+      hipLaunchKernelGGL((k_replay_reduce<bf16, 128>), grid, dim3(64 * RED_WAVES), 0, s, b + p->off_red_rows,
                          b + p->off_red_off, b + p->off_red_idx, H, replay_grad,
                          static_cast<bf16*>(dk_), static_cast<bf16*>(dv_), dg);
     else
-      hipLaunchKernelGGL((k_replay_reduce<bf16, 64>), grid, dim3(256), 0, s, b + p->off_red_rows,
+      hipLaunchKernelGGL((k_replay_reduce<bf16, 64>), grid, dim3(64 * RED_WAVES), 0, s, b + p->off_red_rows,
                          b + p->off_red_off, b + p->off_red_idx, H, replay_grad,
                          static_cast<bf16*>(dk_), static_cast<bf16*>(dv_), dg);
   } else {
-    hipLaunchKernelGGL((k_replay_reduce<float, 64>), grid, dim3(256), 0, s, b + p->off_red_rows,
+    hipLaunchKernelGGL((k_replay_reduce<float, 64>), grid, dim3(64 * RED_WAVES), 0, s, b + p->off_red_rows,
                        b + p->off_red_off, b + p->off_red_idx, H, replay_grad,
                        static_cast<float*>(dk_), static_cast<float*>(dv_), dg);
   }
