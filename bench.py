@@ -76,6 +76,23 @@ def phys_index(seg_len, seg_row):
     return phys
 
 
+def seq_blocks(plan, i, B, block_chunks):
+    """Blocks of sequence i as the planner cuts them: at every requested
+    boundary and after at most block_chunks chunks."""
+    tok = int(plan["seq_n_replay"][i]) + int(plan["seq_n_own"][i])
+    nc = (tok + B - 1) // B
+    reqs = [int(c) for c in plan["req_chunk"][plan["seq_req_off"][i]:plan["seq_req_off"][i + 1]]]
+    nb, c0, j = 0, 0, 0
+    while c0 < nc:
+        c1 = min(nc, c0 + block_chunks)
+        while j < len(reqs) and reqs[j] <= c0:
+            j += 1
+        if j < len(reqs) and reqs[j] <= c1:
+            c1 = reqs[j]
+        nb, c0 = nb + 1, c1
+    return nb
+
+
 def algorithmic_bytes(plan, H, d, el):
     """Bytes each kernel must move for its job over one step (forward, then
     the backward with the recompute-forward), by kernel, for the launches the
@@ -86,9 +103,13 @@ def algorithmic_bytes(plan, H, d, el):
     adjoints) are float32 H*d*d each and are counted for the kernels whose
     job is to produce or consume them; per-chunk states are never
     materialised.  Initial states are read in place from the bank (no
-    gather).  Returns (bytes per step, launches per step) per kernel."""
+    gather).  Sequences of one block have no summaries and no chains: the
+    block kernels start and end them (the forward block kernel writes their
+    final states, the forward-order backward kernel reads dS_final for the
+    boundary term, the reverse-order one starts from dS_final and writes
+    dS0).  Returns (bytes per step, launches per step) per kernel."""
     st = H * d * d * 4
-    K = plan.info["n_rounds"]
+    B = plan.info["chunk"] if "chunk" in plan.info else 64
     names = ["k_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan",
              "k_bwd_revorder", "k_dg_carry", "k_scatter_add", "k_replay_reduce"]
     b = dict.fromkeys(names, 0)
@@ -98,24 +119,35 @@ def algorithmic_bytes(plan, H, d, el):
         rows, own, rep, nseq, nblk = (r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"],
                                       r["n_blk"])
         s0, s1 = r["seq_begin"], r["seq_begin"] + nseq
+        nbs = [seq_blocks(plan, i, B, r["block_chunks"]) for i in range(s0, s1)]
+        assert sum(nbs) == nblk, "block count differs from the planner's"
+        multi = [i for i, nb in zip(range(s0, s1), nbs) if nb > 1]
+        rows_m = sum(int(plan["seq_n_replay"][i]) + int(plan["seq_n_own"][i]) for i in multi)
+        own_m = sum(int(plan["seq_n_own"][i]) for i in multi)
+        nblk_m = sum(nb for nb in nbs if nb > 1)
+        nseq_m, nseq_1 = len(multi), nseq - len(multi)
         nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i] for i in range(s0, s1)))
-        ninit = int(np.sum(init_bank[s0:s1] >= 0))            # sequences with a non-zero start
-        kv = rows * H * (2 * d * el + 4)                       # k, v, g of every packed row
-        qdo = own * H * 2 * d * el + rows * H * 4                # q, dO of own rows, g
-        # forward chain of block-end states: summaries in, states out, the
-        # initial states in, requested states out (the final states in the
-        # forward only; the recompute pass writes none)
-        b["k_fwd_blockscan"] += (2 * nblk * st + ninit * st + nreq * st + nseq * st
-                                 + 2 * nblk * st + ninit * st + nreq * st)
+        ninit = int(np.sum(init_bank[s0:s1] >= 0))             # sequences with a non-zero start
+        ninit_m = int(sum(1 for i in multi if init_bank[i] >= 0))
+        kv = rows * H * (2 * d * el + 4)                        # k, v, g of every packed row
+        kv_m = rows_m * H * (2 * d * el + 4)
+        qdo_m = own_m * H * 2 * d * el + rows_m * H * 4         # q, dO of own rows, g
+        starts = (nblk - nseq + ninit) * st                     # start state of every block
+        # forward chain of block-end states (sequences of several blocks):
+        # summaries in, states out, the initial states in, requested states
+        # out, final states out in the forward only
+        b["k_fwd_blockscan"] += (2 * nblk_m * st + ninit_m * st + nreq * st + nseq_m * st
+                                 + 2 * nblk_m * st + ninit_m * st + nreq * st)
         n["k_fwd_blockscan"] += 2
         # summaries: side 0 in the forward and the recompute pass, side 1 in backward
-        b["k_blocksum"] += 2 * (kv + nblk * st) + qdo + nblk * st
+        b["k_blocksum"] += 2 * (kv_m + nblk_m * st) + qdo_m + nblk_m * st
         n["k_blocksum"] += 3
-        b["k_fwd_block"] += kv + own * H * 2 * d * el + ninit * st + nblk * st
-        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + nblk * st
-        b["k_bwd_blockscan"] += 4 * nblk * st + nseq * st + nreq * st + nseq * st
+        b["k_fwd_block"] += kv + own * H * 2 * d * el + starts + nseq_1 * st
+        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq_1 * st
+        b["k_bwd_blockscan"] += 4 * nblk_m * st + nseq_m * st + nreq * st + nseq_m * st
         b["k_bwd_revorder"] += (kv + own * H * (2 * d * el + 2 * d * el + 4)
-                                + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st)
+                                + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st
+                                + nseq_1 * st)
         b["k_dg_carry"] += rows * H * 8
         b["k_scatter_add"] += 3 * nseq * st
         for name in ("k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan", "k_bwd_revorder",

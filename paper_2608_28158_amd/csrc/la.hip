@@ -304,6 +304,43 @@ __device__ inline void state_from_lds(f32x4* S, const float* stg, bool transpose
       }
 }
 
+// <X, S>_F of a state S held in accumulators (as state_from_lds lays it out,
+// transposed or not) with a row-major D x D state X in global memory, summed
+// over the workgroup of NTH threads and returned to every thread.  X is staged
+// through stg (D x (D + 4) floats); red holds NTH / 64 floats.  Every thread
+// calls it (it synchronises the workgroup).
+template <int D, int CPW, int NTH>
+__device__ inline float state_dot_via_lds(const f32x4* S, float* stg, const float* __restrict__ X,
+                                          bool transpose, int w, int lane, int tid, float* red) {
+  constexpr int NT = D / 16, P = StateStage<D>::PITCH, N4 = D * D / 4;
+  static_assert(N4 % NTH == 0, "state split");
+#pragma unroll
+  for (int i = 0; i < N4 / NTH; ++i) {
+    const int e4 = tid + i * NTH;
+    const int r = e4 / (D / 4), c = (e4 % (D / 4)) * 4;
+    *reinterpret_cast<float4*>(stg + r * P + c) = *reinterpret_cast<const float4*>(X + static_cast<int64_t>(e4) * 4);
+  }
+  __syncthreads();
+  float x = 0.f;
+#pragma unroll
+  for (int j = 0; j < CPW; ++j)
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
+        x += S[j * NT + i][r] * (transpose ? stg[b * P + a] : stg[a * P + b]);
+      }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  if (lane == 0) red[tid >> 6] = x;
+  __syncthreads();
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NTH / 64; ++i) sum += red[i];
+  return sum;
+}
+
 // The masked score tile in three 32 x 32 blocks, (row half, column half) =
 // (0, 0), (1, 0), (1, 1) for waves 0, 1, 2; the block above the diagonal is
 // never read by the consumers and wave 3 does nothing here.  Each block is
@@ -378,7 +415,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dO,
     const float* __restrict__ g, float* __restrict__ dSb, float* __restrict__ U,
-    float* __restrict__ gam, int side0) {
+    float* __restrict__ gam, int side0, int skip1) {
   using C = Cfg<T, D>;
   __shared__ T Xs[Tile<T, D>::SIZE];
   __shared__ T Ys[Tile<T, D>::SIZE];
@@ -387,6 +424,9 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
   const int32_t* bk = blk_tab + b * BLK_WORDS;
+  // a sequence of one block needs no summary when its consumers take the
+  // block's end state from the block kernels themselves
+  if (skip1 && seq_tab[bk[BLK_SEQ] * SEQ_WORDS + SEQ_N_BLK] == 1) return;
   const SeqInfo sq = seq_info(seq_tab + bk[BLK_SEQ] * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
   const T* X = side ? q : k;
@@ -457,13 +497,14 @@ template <int D>
 __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
     const InitSrc is, const float* __restrict__ dSb, const float* __restrict__ gam,
-    float* __restrict__ S_end, float* __restrict__ bank, float* __restrict__ S_final) {
+    float* __restrict__ S_end, float* __restrict__ bank, float* __restrict__ S_final, int skip1) {
   constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
   constexpr int NSW = static_cast<int>(SS4 / SCAN_THR);
   const int li = blockIdx.x / NSW, part = blockIdx.x % NSW, h = blockIdx.y;
   const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + threadIdx.x;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
+  if (skip1 && nb == 1) return;  // its final state comes from the block kernel
   const float* s0 = init_state(is, li, H, h, SS4 * 4);
   float4 s = s0 ? reinterpret_cast<const float4*>(s0)[e4] : make_float4(0.f, 0.f, 0.f, 0.f);
   for (int bg = b0; bg < b0 + nb; bg += SCAN_PF) {
@@ -523,6 +564,9 @@ __global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
   const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + t;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
+  // one-block sequences: the reverse-order kernel starts from dS_final and
+  // writes dS0, the forward-order kernel writes the boundary term
+  if (nb == 1) return;
   const float4* S4 = reinterpret_cast<const float4*>(S_end);
   float4 ds = reinterpret_cast<const float4*>(dS_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4];
   {
@@ -591,7 +635,7 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     const int32_t* __restrict__ blk_order,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
-    const InitSrc is, const float* __restrict__ S_end, T* __restrict__ o) {
+    const InitSrc is, const float* __restrict__ S_end, T* __restrict__ o, float* __restrict__ S_final) {
   using C = Cfg<T, D>;
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
@@ -678,6 +722,10 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, sm.K, sm.V, col0, sm.meta.x, lane);
     __syncthreads();
   }
+  // a sequence of one block: its final state is this block's end state
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  if (S_final && seq[SEQ_N_BLK] == 1)
+    state_store<D, C::CPW>(S_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * DD, S, w, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -702,7 +750,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const T* __restrict__ dO, const InitSrc is, const float* __restrict__ S_end,
-    T* __restrict__ dq, float* __restrict__ rq_out) {
+    T* __restrict__ dq, float* __restrict__ rq_out, const float* __restrict__ dS_final,
+    float* __restrict__ betap) {
   using C = Cfg<T, D>;
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
@@ -804,6 +853,16 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
       for (int i = 0; i < C::NW; ++i) s += sm.rq[i][t];
       rq_out[((static_cast<int64_t>(sq.chunk_off) + c) * CB + t) * H + h] = s;
     }
+  }
+  // A sequence of one block ends here: <dS_final, S_final> (S^T is held) is
+  // its boundary term of dg, the first of the block's NSW partial sums.
+  const int32_t* seq = seq_tab + li * SEQ_WORDS;
+  if (seq[SEQ_N_BLK] == 1) {
+    constexpr int NSW = D * D / 4 / SCAN_THR;
+    const float dot = state_dot_via_lds<D, C::CPW, C::NTHR>(
+        St, reinterpret_cast<float*>(&sm.dO[0]),
+        dS_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * DD, true, w, lane, t, sm.rq[0]);
+    if (t < NSW) betap[(static_cast<int64_t>(b) * H + h) * NSW + t] = t == 0 ? dot : 0.f;
   }
 }
 
@@ -950,7 +1009,8 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     float scale, const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
     const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
-    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb) {
+    float* __restrict__ dg, float* __restrict__ rep_grad, float* __restrict__ Rb,
+    const float* __restrict__ dS_final, float* __restrict__ dS0) {
   using C = Cfg<T, D>;
   constexpr int NTH = 2 * C::NTHR;
   using SG = Stg<T, D, NTH>;
@@ -964,6 +1024,10 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
+  // a sequence of one block starts from dS_final and ends with its dS0
+  const bool one = seq_tab[li * SEQ_WORDS + SEQ_N_BLK] == 1;
+  const float* dS_in = one ? dS_final + (static_cast<int64_t>(seq_tab[li * SEQ_WORDS + SEQ_FINAL_LEAF]) * H + h) * DD
+                           : dS_end + (static_cast<int64_t>(b) * H + h) * DD;
   static_assert(StateStage<D>::BYTES <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)),
                 "state staging fits the second tile buffer");
   float* stg = reinterpret_cast<float*>(&sm.tile[1][0][0]);
@@ -986,7 +1050,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   cs.resolve(sq, c_last, replay_row, g, H, h, tid, mrow);
   fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
   fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
-  state_to_lds<D, NTH>(stg, dS_end + (static_cast<int64_t>(b) * H + h) * DD, tid);
+  state_to_lds<D, NTH>(stg, dS_in, tid);
   put<T, D, NTH>(sm.tile[0][TQ], pa, nullptr, tid);
   put<T, D, NTH>(sm.tile[0][TK], pb, nullptr, tid);
   fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
@@ -1095,6 +1159,8 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     suffix(c0);
     if (lane == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
   }
+  // side 0 holds dS at the start of the block: a one-block sequence's dS0
+  if (one && side == 0) state_store<D, C::CPW>(dS0 + (static_cast<int64_t>(li) * H + h) * DD, dS, w, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1308,30 +1374,32 @@ Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_order, b + p->off_replay_row, b + L.init_idx};
 }
 
-// Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b).
+// Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b);
+// skip1: none for sequences of one block.
 template <typename T, int D>
 int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, float scale,
                     const void* q, const void* k, const void* v, const void* dO, const float* g,
-                    float* dSb, float* U, float* gam, int side0, int n_sides, hipStream_t s) {
+                    float* dSb, float* U, float* gam, int side0, int n_sides, int skip1, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   ProfScope ps("k_blocksum", s);
   hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk * H, 1, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
                      B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                      static_cast<const T*>(k), static_cast<const T*>(v),
-                     static_cast<const T*>(dO), g, dSb, U, gam, side0);
+                     static_cast<const T*>(dO), g, dSb, U, gam, side0, skip1);
   return hip_check("k_blocksum");
 }
 
-// Chain of block summaries: S_end per block, requested boundary states, final states.
+// Chain of block summaries: S_end per block, requested boundary states, final
+// states; skip1: not for sequences of one block.
 template <int D>
 int launch_fwd_scan(const harts_plan_t* p, int32_t round, const Blob& B, int H, const InitSrc& is,
                     const float* dSb, const float* gam, float* S_end, float* bank, float* S_final,
-                    hipStream_t s) {
+                    int skip1, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   constexpr int NSW = D * D / 4 / SCAN_THR;
   ProfScope ps("k_fwd_blockscan", s);
   hipLaunchKernelGGL((k_fwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
-                     B.seq_tab, B.blk_tab, H, is, dSb, gam, S_end, bank, S_final);
+                     B.seq_tab, B.blk_tab, H, is, dSb, gam, S_end, bank, S_final, skip1);
   return hip_check("k_fwd_blockscan");
 }
 
@@ -1346,17 +1414,22 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   float* S_end = reinterpret_cast<float*>(saved);
   float* gam = reinterpret_cast<float*>(saved + z.blk_state);
   const InitSrc is{S0, bank, B.init_idx};
+  // Sequences of one block need no summary or chain: the block kernel starts
+  // from the initial state and writes the final state itself (with outputs),
+  // and the backward kernels start and end such sequences themselves.
+  const int skip1 = o || !S_final;
   if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, nullptr, g, dSb, nullptr,
-                                      gam, 0, 1, s))
+                                      gam, 0, 1, skip1, s))
     return rc;
-  if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam, S_end, bank, S_final, s)) return rc;
+  if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam, S_end, bank, S_final, skip1, s))
+    return rc;
   if (!o) return HARTS_OK;  // state pass only (recompute-forward)
   {
     ProfScope ps("k_fwd_block", s);
     hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g, is, S_end,
-                       static_cast<T*>(o));
+                       static_cast<T*>(o), S_final);
   }
   return hip_check("k_fwd_block");
 }
@@ -1389,13 +1462,13 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     char* sv = w + z.blk_state;
     float* S_end_w = reinterpret_cast<float*>(sv);
     float* gam_w = reinterpret_cast<float*>(sv + z.blk_state);
-    if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, dSb, U, gam_w, 0, 2, s))
+    if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, dSb, U, gam_w, 0, 2, 1, s))
       return rc;
-    if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam_w, S_end_w, nullptr, nullptr, s))
+    if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam_w, S_end_w, nullptr, nullptr, 1, s))
       return rc;
     saved = sv;
   } else if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, nullptr, U,
-                                             nullptr, 1, 1, s)) {
+                                             nullptr, 1, 1, 1, s)) {
     return rc;
   }
   const float* S_end = reinterpret_cast<const float*>(saved);
@@ -1413,7 +1486,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
                        B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
-                       static_cast<const T*>(dO), is, S_end, static_cast<T*>(dq), rq);
+                       static_cast<const T*>(dO), is, S_end, static_cast<T*>(dq), rq, dS_final, betap);
   }
   if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
@@ -1422,7 +1495,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
                        B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale,
                        static_cast<const T*>(q), static_cast<const T*>(k),
                        static_cast<const T*>(v), g, static_cast<const T*>(dO), dS_end, rq,
-                       static_cast<T*>(dk), static_cast<T*>(dv), dg, rep_grad, Rb);
+                       static_cast<T*>(dk), static_cast<T*>(dv), dg, rep_grad, Rb, dS_final, dS0);
   }
   if (int rc = hip_check("k_bwd_revorder")) return rc;
   {

@@ -111,8 +111,10 @@ class TreeLARunner:
             raise ValueError(f"g must be contiguous float32 [{Cn},{self.H}]")
 
     # -- forward -------------------------------------------------------------
-    def forward(self, q, k, v, g, S0_tree=None, outputs=True, keep_states=True):
-        """Run all rounds.  Returns dict(o, S_final, bank, saved[r])."""
+    def forward(self, q, k, v, g, S0_tree=None, outputs=True, keep_states=True, final_states=None):
+        """Run all rounds.  Returns dict(o, S_final, bank, saved[r]).  The
+        final states are written when final_states is true (default: with
+        the outputs)."""
         self._check_inputs(q, k, v, g)
         P = self.plan
         H, d = self.H, self.d
@@ -125,8 +127,10 @@ class TreeLARunner:
             bank[: P.info["n_trees"]].zero_()
         o = torch.empty_like(q) if outputs else None
         # the state-only pass (recompute-forward) writes no final states
+        if final_states is None:
+            final_states = outputs
         S_final = torch.empty((P.info["n_leaves"], H, d, d), dtype=torch.float32,
-                              device=self.device) if outputs else None
+                              device=self.device) if final_states else None
         saved = []
         for r in range(P.info["n_rounds"]):
             S0 = self.gather(bank, r) if self.gather_init else None

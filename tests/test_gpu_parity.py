@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle.compact import compact_fwd_bwd
+from oracle.compact import compact_fwd, compact_fwd_bwd
 from tests.harness import TOL, config_inputs, max_rel, phys_index
 from workloads import draw_inputs
 
@@ -108,6 +108,37 @@ def test_gathered_and_indexed_initial_states_agree_bitwise():
         b, _ = run_gpu(f.parent, f.seg_len, x, cfg["H"], cfg["d"], dtype, sc, True, True)
         for name in a:
             assert np.array_equal(a[name], b[name]), name
+
+
+def test_final_states_with_and_without_outputs():
+    """Final states from a forward with outputs (the block kernel ends the
+    sequences of one block) and from a state-only forward that requests them
+    (summaries and chains for every sequence) agree with the oracle, on the
+    Figure 1 tree and on a config-1 forest (sequences of one block and of
+    several in both)."""
+    from paper_2608_28158_amd.plan import HartsPlan
+    from paper_2608_28158_amd.tree_la import TreeLARunner
+    for cfg_i, dtype in ((0, "f32"), (1, "bf16")):
+        f, cfg, x = config_inputs(cfg_i, s0_scale=0.5)
+        H, d = cfg["H"], cfg["d"]
+        print(f"[gpu] config{cfg_i} final states with and without outputs", flush=True)
+        plan = HartsPlan(f.parent, f.seg_len, 64)
+        phys = phys_index(f.seg_len, plan["seg_row"])
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        q, k, v = (_dev(x[n], phys, tdt) for n in ("q", "k", "v"))
+        g = _dev(x["g"], phys, torch.float32)
+        S0 = torch.from_numpy(x["S0"]).cuda()
+        runner = TreeLARunner(plan, H, d, tdt, "cuda", d ** -0.5)
+        a = runner.forward(q, k, v, g, S0, outputs=True)["S_final"]
+        b = runner.forward(q, k, v, g, S0, outputs=False, final_states=True)["S_final"]
+        torch.cuda.synchronize()
+        f64 = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+        ref = compact_fwd(f.parent, f.seg_len, 64, f64(x["q"]), f64(x["k"]), f64(x["v"]), f64(x["g"]),
+                          d ** -0.5, f64(x["S0"]))["S_final"].numpy()
+        for got in (a, b):
+            err = max_rel(got.cpu().numpy(), ref)
+            print(f"[gpu] config{cfg_i} S_final max-rel {err:.2e}", flush=True)
+            assert err <= TOL[dtype]
 
 
 def _random_forest(r, n, max_len, p_root=0.1):
