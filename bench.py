@@ -77,20 +77,24 @@ def phys_index(seg_len, seg_row):
 
 
 def seq_blocks(plan, i, B, block_chunks):
-    """Blocks of sequence i as the planner cuts them: at every requested
-    boundary and after at most block_chunks chunks."""
-    tok = int(plan["seq_n_replay"][i]) + int(plan["seq_n_own"][i])
+    """Blocks of sequence i as the planner cuts them (at every requested
+    boundary and after at most block_chunks chunks), as (packed rows, own
+    rows) per block."""
+    n_rep = int(plan["seq_n_replay"][i])
+    tok = n_rep + int(plan["seq_n_own"][i])
     nc = (tok + B - 1) // B
     reqs = [int(c) for c in plan["req_chunk"][plan["seq_req_off"][i]:plan["seq_req_off"][i + 1]]]
-    nb, c0, j = 0, 0, 0
+    out, c0, j = [], 0, 0
     while c0 < nc:
         c1 = min(nc, c0 + block_chunks)
         while j < len(reqs) and reqs[j] <= c0:
             j += 1
         if j < len(reqs) and reqs[j] <= c1:
             c1 = reqs[j]
-        nb, c0 = nb + 1, c1
-    return nb
+        p0, p1 = c0 * B, min(c1 * B, tok)
+        out.append((p1 - p0, max(0, p1 - max(p0, n_rep))))
+        c0 = c1
+    return out
 
 
 def algorithmic_bytes(plan, H, d, el):
@@ -103,13 +107,15 @@ def algorithmic_bytes(plan, H, d, el):
     adjoints) are float32 H*d*d each and are counted for the kernels whose
     job is to produce or consume them; per-chunk states are never
     materialised.  Initial states are read in place from the bank (no
-    gather).  Sequences of one block have no summaries and no chains: the
-    block kernels start and end them (the forward block kernel writes their
-    final states, the forward-order backward kernel reads dS_final for the
-    boundary term, the reverse-order one starts from dS_final and writes
-    dS0).  Returns (bytes per step, launches per step) per kernel."""
+    gather).  The block kernels end every sequence's forward chain and start
+    its adjoint chain: no forward summary of a last block (its g only, for
+    the total decay), no adjoint summary of a first block, no chain step for
+    either; the forward block kernel writes the final states, the
+    forward-order backward kernel reads dS_final for the boundary term, the
+    reverse-order one starts last blocks from dS_final and writes dS0.
+    Returns (bytes per step, launches per step) per kernel."""
     st = H * d * d * 4
-    B = plan.info["chunk"] if "chunk" in plan.info else 64
+    B = 64
     names = ["k_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan",
              "k_bwd_revorder", "k_dg_carry", "k_scatter_add", "k_replay_reduce"]
     b = dict.fromkeys(names, 0)
@@ -119,35 +125,41 @@ def algorithmic_bytes(plan, H, d, el):
         rows, own, rep, nseq, nblk = (r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"],
                                       r["n_blk"])
         s0, s1 = r["seq_begin"], r["seq_begin"] + nseq
-        nbs = [seq_blocks(plan, i, B, r["block_chunks"]) for i in range(s0, s1)]
-        assert sum(nbs) == nblk, "block count differs from the planner's"
-        multi = [i for i, nb in zip(range(s0, s1), nbs) if nb > 1]
-        rows_m = sum(int(plan["seq_n_replay"][i]) + int(plan["seq_n_own"][i]) for i in multi)
-        own_m = sum(int(plan["seq_n_own"][i]) for i in multi)
-        nblk_m = sum(nb for nb in nbs if nb > 1)
-        nseq_m, nseq_1 = len(multi), nseq - len(multi)
+        blks = [seq_blocks(plan, i, B, r["block_chunks"]) for i in range(s0, s1)]
+        assert sum(len(x) for x in blks) == nblk, "block count differs from the planner's"
+        multi = [i for i, x in zip(range(s0, s1), blks) if len(x) > 1]
+        nblk_m = sum(len(x) for x in blks if len(x) > 1)
+        nseq_m = len(multi)
+        rows_nl = sum(rw for x in blks for rw, _ in x[:-1])      # rows of blocks not last
+        rows_l = sum(x[-1][0] for x in blks)                      # rows of last blocks
+        rows_nf = sum(rw for x in blks for rw, _ in x[1:])       # rows of blocks not first
+        own_nf = sum(ow for x in blks for _, ow in x[1:])
         nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i] for i in range(s0, s1)))
         ninit = int(np.sum(init_bank[s0:s1] >= 0))             # sequences with a non-zero start
         ninit_m = int(sum(1 for i in multi if init_bank[i] >= 0))
         kv = rows * H * (2 * d * el + 4)                        # k, v, g of every packed row
-        kv_m = rows_m * H * (2 * d * el + 4)
-        qdo_m = own_m * H * 2 * d * el + rows_m * H * 4         # q, dO of own rows, g
+        chained = nblk_m - nseq_m                               # blocks with a chain step
         starts = (nblk - nseq + ninit) * st                     # start state of every block
-        # forward chain of block-end states (sequences of several blocks):
-        # summaries in, states out, the initial states in, requested states
-        # out, final states out in the forward only
-        b["k_fwd_blockscan"] += (2 * nblk_m * st + ninit_m * st + nreq * st + nseq_m * st
-                                 + 2 * nblk_m * st + ninit_m * st + nreq * st)
+        # forward chain (start states of blocks after the first): summaries
+        # in, states out, the initial states in, requested states out; in the
+        # forward and in the recompute pass
+        b["k_fwd_blockscan"] += 2 * (2 * chained * st + ninit_m * st + nreq * st)
         n["k_fwd_blockscan"] += 2
-        # summaries: side 0 in the forward and the recompute pass, side 1 in backward
-        b["k_blocksum"] += 2 * (kv_m + nblk_m * st) + qdo_m + nblk_m * st
+        # summaries: side 0 in the forward and the recompute pass (k, v, g of
+        # blocks not last, g of last blocks), side 1 in backward (q, dO of
+        # own rows and g of blocks not first)
+        side0 = rows_nl * H * (2 * d * el + 4) + rows_l * H * 4 + (nblk - nseq) * st
+        side1 = own_nf * H * 2 * d * el + rows_nf * H * 4 + (nblk - nseq) * st
+        b["k_blocksum"] += 2 * side0 + side1
         n["k_blocksum"] += 3
-        b["k_fwd_block"] += kv + own * H * 2 * d * el + starts + nseq_1 * st
-        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq_1 * st
-        b["k_bwd_blockscan"] += 4 * nblk_m * st + nseq_m * st + nreq * st + nseq_m * st
+        b["k_fwd_block"] += kv + own * H * 2 * d * el + starts + nseq * st
+        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq * st
+        # adjoint chain: dS_final in, local adjoints of blocks not first in,
+        # end adjoints of blocks not last out, requested injections and states in
+        b["k_bwd_blockscan"] += (nseq_m + 2 * chained + 2 * nreq) * st
         b["k_bwd_revorder"] += (kv + own * H * (2 * d * el + 2 * d * el + 4)
                                 + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st
-                                + nseq_1 * st)
+                                + nseq * st)
         b["k_dg_carry"] += rows * H * 8
         b["k_scatter_add"] += 3 * nseq * st
         for name in ("k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan", "k_bwd_revorder",

@@ -424,11 +424,26 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
   const int32_t* bk = blk_tab + b * BLK_WORDS;
-  // a sequence of one block needs no summary when its consumers take the
-  // block's end state from the block kernels themselves
-  if (skip1 && seq_tab[bk[BLK_SEQ] * SEQ_WORDS + SEQ_N_BLK] == 1) return;
+  // The block kernels end a sequence's forward chain and start its adjoint
+  // chain themselves: the first block's adjoint summary is never needed, nor
+  // the last block's forward summary, of which only Gamma_b is (for the
+  // adjoint chain).
+  if (skip1 && side && bk[BLK_IDX] == 0) return;
   const SeqInfo sq = seq_info(seq_tab + bk[BLK_SEQ] * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  const int64_t bi = static_cast<int64_t>(b) * H + h;
+  if (skip1 && !side && bk[BLK_IDX] == seq_tab[bk[BLK_SEQ] * SEQ_WORDS + SEQ_N_BLK] - 1) {
+    if (w != 0) return;
+    // Gamma_b alone, summed chunk by chunk as below; wave 0, lane = row
+    ChunkSrc<T, D> cs;
+    float Gs = 0.f;
+    for (int c = c0; c < c_end; ++c) {
+      cs.resolve(sq, c, replay_row, g, H, h, t, t);
+      Gs += lane_value(wave_prefix_sum(cs.gv, t), CB - 1);
+    }
+    if (t == 0) gam[bi] = Gs;
+    return;
+  }
   const T* X = side ? q : k;
   const T* Y = side ? dO : v;
   const int min_kind = side ? ROW_OWN : ROW_REPLAY;
@@ -465,7 +480,6 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
     Gs += GL;
     __syncthreads();
   }
-  const int64_t bi = static_cast<int64_t>(b) * H + h;
   state_store<D, C::CPW>((side ? U : dSb) + bi * D * D, S, w, lane);
   if (!side && t == 0) gam[bi] = Gs;
 }
@@ -503,8 +517,11 @@ __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
   const int li = blockIdx.x / NSW, part = blockIdx.x % NSW, h = blockIdx.y;
   const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + threadIdx.x;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
-  if (skip1 && nb == 1) return;  // its final state comes from the block kernel
+  const int b0 = seq[SEQ_BLK_OFF];
+  // skip1: the last block's end state (the final state) comes from the block
+  // kernel, and only the start states of the other blocks are chained
+  const int nb = seq[SEQ_N_BLK] - (skip1 ? 1 : 0);
+  if (nb == 0) return;
   const float* s0 = init_state(is, li, H, h, SS4 * 4);
   float4 s = s0 ? reinterpret_cast<const float4*>(s0)[e4] : make_float4(0.f, 0.f, 0.f, 0.f);
   for (int bg = b0; bg < b0 + nb; bg += SCAN_PF) {
@@ -535,7 +552,7 @@ __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
       }
     }
   }
-  if (S_final)
+  if (S_final && !skip1)
     reinterpret_cast<float4*>(S_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4] = s;
 }
 
@@ -556,7 +573,7 @@ __global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
     const float* __restrict__ dS_final, const float* __restrict__ dbank,
     const float* __restrict__ S_end, const float* __restrict__ U, const float* __restrict__ gam,
-    float* __restrict__ dS_end, float* __restrict__ dS0, float* __restrict__ betap) {
+    float* __restrict__ dS_end, float* __restrict__ betap) {
   constexpr int64_t SS4 = static_cast<int64_t>(D) * D / 4;
   constexpr int NSW = static_cast<int>(SS4 / SCAN_THR);
   __shared__ float red[SCAN_THR / 64];
@@ -564,23 +581,20 @@ __global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
   const int64_t e4 = static_cast<int64_t>(part) * SCAN_THR + t;
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
   const int b0 = seq[SEQ_BLK_OFF], nb = seq[SEQ_N_BLK];
-  // one-block sequences: the reverse-order kernel starts from dS_final and
-  // writes dS0, the forward-order kernel writes the boundary term
+  // The reverse-order kernel starts a sequence's last block from dS_final
+  // and ends its first block with dS0; the forward-order kernel adds the last
+  // block's boundary term <dS_final, S_final>.  Here: the end adjoints of
+  // the other blocks, with the injections and boundary terms of requested
+  // states at their ends.
   if (nb == 1) return;
   const float4* S4 = reinterpret_cast<const float4*>(S_end);
   float4 ds = reinterpret_cast<const float4*>(dS_final)[(static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * SS4 + e4];
-  {
-    const int bl = b0 + nb - 1;
-    const float4 s = S4[(static_cast<int64_t>(bl) * H + h) * SS4 + e4];
-    const float bsum = scan_block_sum(ds.x * s.x + ds.y * s.y + ds.z * s.z + ds.w * s.w, red, t);
-    if (t == 0) betap[(static_cast<int64_t>(bl) * H + h) * NSW + part] = bsum;
-  }
-  for (int bg = b0 + nb - 1; bg >= b0; bg -= SCAN_PF) {
+  for (int bg = b0 + nb - 1; bg > b0; bg -= SCAN_PF) {
     float4 u[SCAN_PF];
     float gm[SCAN_PF];
 #pragma unroll
     for (int i = 0; i < SCAN_PF; ++i) {
-      if (bg - i >= b0) {
+      if (bg - i > b0) {
         const int64_t bi = static_cast<int64_t>(bg - i) * H + h;
         gm[i] = gam[bi];
         u[i] = reinterpret_cast<const float4*>(U)[bi * SS4 + e4];
@@ -589,32 +603,29 @@ __global__ __launch_bounds__(SCAN_THR) void k_bwd_blockscan(
 #pragma unroll
     for (int i = 0; i < SCAN_PF; ++i) {
       const int b = bg - i;
-      if (b < b0) break;
-      const int64_t bi = static_cast<int64_t>(b) * H + h;
-      reinterpret_cast<float4*>(dS_end)[bi * SS4 + e4] = ds;
+      if (b <= b0) break;
+      // ds: the adjoint at the end of block b -> at its start = the end of b - 1
       const float dec = __expf(gm[i]);
       ds.x = dec * ds.x + u[i].x;
       ds.y = dec * ds.y + u[i].y;
       ds.z = dec * ds.z + u[i].z;
       ds.w = dec * ds.w + u[i].w;
-      if (b > b0) {
-        const int64_t pi = static_cast<int64_t>(b - 1) * H + h;
-        const int eb = blk_tab[(b - 1) * BLK_WORDS + BLK_END_BANK];
-        float bsum = 0.f;
-        if (eb >= 0) {  // uniform over the workgroup
-          const float4 inj = reinterpret_cast<const float4*>(dbank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4];
-          const float4 s = S4[pi * SS4 + e4];
-          bsum = scan_block_sum(inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w, red, t);
-          ds.x += inj.x;
-          ds.y += inj.y;
-          ds.z += inj.z;
-          ds.w += inj.w;
-        }
-        if (t == 0) betap[pi * NSW + part] = bsum;
+      const int64_t pi = static_cast<int64_t>(b - 1) * H + h;
+      const int eb = blk_tab[(b - 1) * BLK_WORDS + BLK_END_BANK];
+      float bsum = 0.f;
+      if (eb >= 0) {  // uniform over the workgroup
+        const float4 inj = reinterpret_cast<const float4*>(dbank)[(static_cast<int64_t>(eb) * H + h) * SS4 + e4];
+        const float4 s = S4[pi * SS4 + e4];
+        bsum = scan_block_sum(inj.x * s.x + inj.y * s.y + inj.z * s.z + inj.w * s.w, red, t);
+        ds.x += inj.x;
+        ds.y += inj.y;
+        ds.z += inj.z;
+        ds.w += inj.w;
       }
+      if (t == 0) betap[pi * NSW + part] = bsum;
+      reinterpret_cast<float4*>(dS_end)[pi * SS4 + e4] = ds;
     }
   }
-  reinterpret_cast<float4*>(dS0)[(static_cast<int64_t>(li) * H + h) * SS4 + e4] = ds;
 }
 
 // ---------------------------------------------------------------------------
@@ -722,9 +733,9 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, sm.K, sm.V, col0, sm.meta.x, lane);
     __syncthreads();
   }
-  // a sequence of one block: its final state is this block's end state
+  // the last block of a sequence: its end state is the final state
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  if (S_final && seq[SEQ_N_BLK] == 1)
+  if (S_final && bk[BLK_IDX] == seq[SEQ_N_BLK] - 1)
     state_store<D, C::CPW>(S_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * DD, S, w, lane);
 }
 
@@ -854,10 +865,11 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
       rq_out[((static_cast<int64_t>(sq.chunk_off) + c) * CB + t) * H + h] = s;
     }
   }
-  // A sequence of one block ends here: <dS_final, S_final> (S^T is held) is
-  // its boundary term of dg, the first of the block's NSW partial sums.
+  // The last block of a sequence ends with S_final (S^T is held):
+  // <dS_final, S_final> is its boundary term of dg, the first of the block's
+  // NSW partial sums.
   const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  if (seq[SEQ_N_BLK] == 1) {
+  if (bk[BLK_IDX] == seq[SEQ_N_BLK] - 1) {
     constexpr int NSW = D * D / 4 / SCAN_THR;
     const float dot = state_dot_via_lds<D, C::CPW, C::NTHR>(
         St, reinterpret_cast<float*>(&sm.dO[0]),
@@ -1024,10 +1036,10 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
   const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
-  // a sequence of one block starts from dS_final and ends with its dS0
-  const bool one = seq_tab[li * SEQ_WORDS + SEQ_N_BLK] == 1;
-  const float* dS_in = one ? dS_final + (static_cast<int64_t>(seq_tab[li * SEQ_WORDS + SEQ_FINAL_LEAF]) * H + h) * DD
-                           : dS_end + (static_cast<int64_t>(b) * H + h) * DD;
+  // a sequence's last block starts from dS_final, its first block ends with dS0
+  const bool last = bk[BLK_IDX] == seq_tab[li * SEQ_WORDS + SEQ_N_BLK] - 1;
+  const float* dS_in = last ? dS_final + (static_cast<int64_t>(seq_tab[li * SEQ_WORDS + SEQ_FINAL_LEAF]) * H + h) * DD
+                            : dS_end + (static_cast<int64_t>(b) * H + h) * DD;
   static_assert(StateStage<D>::BYTES <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)),
                 "state staging fits the second tile buffer");
   float* stg = reinterpret_cast<float*>(&sm.tile[1][0][0]);
@@ -1159,8 +1171,8 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     suffix(c0);
     if (lane == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
   }
-  // side 0 holds dS at the start of the block: a one-block sequence's dS0
-  if (one && side == 0) state_store<D, C::CPW>(dS0 + (static_cast<int64_t>(li) * H + h) * DD, dS, w, lane);
+  // side 0 holds dS at the start of the block: the first block's is dS0
+  if (bk[BLK_IDX] == 0 && side == 0) state_store<D, C::CPW>(dS0 + (static_cast<int64_t>(li) * H + h) * DD, dS, w, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1477,8 +1489,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     constexpr int NSW = D * D / 4 / SCAN_THR;
     ProfScope ps("k_bwd_blockscan", s);
     hipLaunchKernelGGL((k_bwd_blockscan<D>), dim3(L.n_seq * NSW, H), dim3(SCAN_THR), 0, s,
-                       B.seq_tab, B.blk_tab, H, dS_final, dbank, S_end, U, gam, dS_end, dS0,
-                       betap);
+                       B.seq_tab, B.blk_tab, H, dS_final, dbank, S_end, U, gam, dS_end, betap);
   }
   if (int rc = hip_check("k_bwd_blockscan")) return rc;
   {
