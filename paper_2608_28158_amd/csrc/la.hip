@@ -883,49 +883,118 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
 // two halves per (block, head), sharing the chunk tiles in LDS:
 //   waves 0..3 (side 0): dv = diag(exp(G_last - G)) K dS + scale A^T dO,
 //                        holding dS;
-//   waves 4..7 (side 1): dk = diag(exp(G_last - G)) V dS^T + dA^T Q, holding
-//                        dS^T, plus k.dk per row and the local suffix sums of
-//                        dg.
-// Each half runs the adjoint recurrence
+//   waves 4..7 (side 1): dk = diag(exp(G_last - G)) V dS^T + dA^T Q, plus
+//                        k.dk per row and the local suffix sums of dg.
+// The adjoint recurrence
 //   dS_c = exp(G_last) dS_{c+1} + Q^T diag(exp(G) scale) dO
-// in its own layout.
+// runs in side 0 only (bf16): after each update side 0 converts dS once to
+// bf16 MFMA operands and writes them, transposed, to LDS, from where side 1
+// reads its operands of V dS^T with the transpose read during the next
+// score phase.  In fp32 each half runs the recurrence in its own layout.
 // ---------------------------------------------------------------------------
-// The chunk tiles are double-buffered: while a chunk is computed from one
-// buffer, the next chunk's tiles are written into the other, two tiles at a
-// time, from registers loaded one phase earlier.  Two score tiles fit next to
-// that in bf16 only; in fp32 the halves take turns with one tile (score A,
-// dv rows, score dA, dk rows).
+// Chunk tiles.  bf16: Q and K are double-buffered (the next chunk's are
+// written during the score phase), V and dO single-buffered (written after
+// every wave is done with the current ones); the packed transposed adjoint
+// takes the room of the second V, dO pair, next to two score tiles.  fp32:
+// all four double-buffered, the halves taking turns with one score tile
+// (score A, dv rows, score dA, dk rows).
 enum { TQ = 0, TK = 1, TV = 2, TDO = 3 };
+
+// [D][D] bf16 tile of the adjoint's transpose (rows dv, columns dk), each
+// row padded by 16 bytes like the chunk tiles.
+template <int D>
+struct AdjT {
+  static constexpr int LD = D + 8;
+  static constexpr int SIZE = D * LD;
+  __device__ static inline int at(int r, int c) { return r * LD + c; }
+};
+
+template <typename T, int D, bool SH = (sizeof(T) == 2)>
+struct BrTiles;
+template <typename T, int D>
+struct BrTiles<T, D, false> {
+  T tile[2][4][Tile<T, D>::SIZE];
+  static constexpr int STAGE_BYTES = 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T));
+  __device__ inline T* at(int bf, int which) { return tile[bf][which]; }
+  __device__ inline float* stage() { return reinterpret_cast<float*>(&tile[1][0][0]); }
+};
+template <typename T, int D>
+struct BrTiles<T, D, true> {
+  T qk[2][2][Tile<T, D>::SIZE];
+  T dt[AdjT<D>::SIZE];  // follows qk[1]: the two form the staging area
+  T vdo[2][Tile<T, D>::SIZE];
+  static constexpr int STAGE_BYTES = (2 * Tile<T, D>::SIZE + AdjT<D>::SIZE) * static_cast<int>(sizeof(T));
+  __device__ inline T* at(int bf, int which) { return which < 2 ? qk[bf][which] : vdo[which - 2]; }
+  __device__ inline float* stage() { return reinterpret_cast<float*>(&qk[1][0][0]); }
+};
+
 template <typename T, int D>
 struct BrSmem {
   using C = Cfg<T, D>;
-  static constexpr int NP = sizeof(T) == 2 ? 2 : 1;
-  T tile[2][4][Tile<T, D>::SIZE];  // [buffer][Q (own rows), K, V, dO (own rows)]
+  static constexpr bool SH = sizeof(T) == 2;  // one adjoint, shared through LDS
+  static constexpr int NP = SH ? 2 : 1;
+  BrTiles<T, D> tl;
   T P[NP][Tile<T, CB>::SIZE];      // A = Q K^T masked; dA = scale (dO V^T) masked
   ChunkMeta meta[2];               // x = exp(G_last - G), y = exp(G) * scale
   float rk[C::NW][CB];             // partial k.dk of each row, per wave
 };
 
-// Output rows and adjoint update of one chunk (tiles of buffer bf) for one
-// half of the workgroup.  The products run with their operands swapped, so
-// that lane (g, i) of a wave holds row 16 jt + i of the output at columns
-// col0 + 16 j + 4g .. + 3: one 8-byte (bf16) or 16-byte (float) store per
-// strip, one row per lane.
+// Side 1's B operands of V dS^T from the transposed adjoint in LDS: the same
+// values as PackedState::pack of dS^T held in side 1's accumulator layout.
+template <int D, int NT, int CPW>
+__device__ inline void adj_load(PackedState<bf16, NT, CPW>& ps, const bf16* dt, int w, int lane) {
+#pragma unroll
+  for (int j = 0; j < CPW; ++j)
+#pragma unroll
+    for (int kt = 0; kt < NT; kt += 2)
+      ps.p[j][kt / 2] = Frag<bf16>::km<AdjT<D>>(dt, 16 * kt, 16 * (CPW * w + j), lane);
+}
+
+// Side 0's packed adjoint written transposed: lane (g, i) of strip j holds
+// dS[16 kt + 4g + 0..3][16 (CPW w + j) + i] (and the next 16 rows), four
+// consecutive elements of row dv = 16 (CPW w + j) + i of the transpose.
+template <int D, int NT, int CPW>
+__device__ inline void adj_store(bf16* dt, const PackedState<bf16, NT, CPW>& ps, int w, int lane) {
+  const int r = 16 * CPW * w + (lane & 15), c = 4 * (lane >> 4);
+#pragma unroll
+  for (int j = 0; j < CPW; ++j)
+#pragma unroll
+    for (int kt = 0; kt < NT; kt += 2) {
+      const bf16x8 v = ps.p[j][kt / 2];
+      bf16x4 lo, hi;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] = v[e];
+        hi[e] = v[4 + e];
+      }
+      *reinterpret_cast<bf16x4*>(dt + AdjT<D>::at(r + 16 * j, 16 * kt + c)) = lo;
+      *reinterpret_cast<bf16x4*>(dt + AdjT<D>::at(r + 16 * j, 16 * kt + 16 + c)) = hi;
+    }
+}
+
+// Output rows of one chunk (tiles of buffer bf) for one half of the
+// workgroup, from the adjoint's B operands ps.  The products run with their
+// operands swapped, so that lane (g, i) of a wave holds row 16 jt + i of the
+// output at columns col0 + 16 j + 4g .. + 3: one 8-byte (bf16) or 16-byte
+// (float) store per strip, one row per lane.  Then the adjoint update: in
+// bf16 by side 0 only, which also converts the new adjoint for the next
+// chunk (ps) and publishes it (when `more`); in fp32 by each half.
 template <typename T, int D, int SIDE>
 __device__ __forceinline__ void bwd_revorder_rows(
-    BrSmem<T, D>& sm, int bf, f32x4* dS, const ChunkRows& cur, const SeqInfo& sq, int c, int H,
-    int h, float scale, float GL, int w, int lane, T* __restrict__ dk, T* __restrict__ dv,
-    float* __restrict__ rep_grad) {
+    BrSmem<T, D>& sm, int bf, f32x4* dS, PackedState<T, Cfg<T, D>::NT, Cfg<T, D>::CPW>& ps,
+    const ChunkRows& cur, const SeqInfo& sq, int c, bool more, int H, int h, float scale, float GL,
+    int w, int lane, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ rep_grad) {
   using C = Cfg<T, D>;
+  constexpr bool SH = BrSmem<T, D>::SH;
   constexpr int NS = C::CPW * C::NT;
   constexpr int RG = 2 * D + 1;
   constexpr bool side = SIDE == 1;
   const int col0 = C::CPW * w * 16;
   const T* PT = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];  // transposed score tile
-  const T* Q = sm.tile[bf][TQ];
-  const T* K = sm.tile[bf][TK];
-  const T* V = sm.tile[bf][TV];
-  const T* dOt = sm.tile[bf][TDO];
+  const T* Q = sm.tl.at(bf, TQ);
+  const T* K = sm.tl.at(bf, TK);
+  const T* V = sm.tl.at(bf, TV);
+  const T* dOt = sm.tl.at(bf, TDO);
   const ChunkMeta& mt = sm.meta[bf];
   const int g4 = 4 * (lane >> 4);
   // the chunk's 64 rows of the output (row0 may precede the sequence's own
@@ -933,8 +1002,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
   const __amdgpu_buffer_rsrc_t out_rsrc =
       buffer_rsrc((side ? dk : dv) + static_cast<int64_t>(cur.row0) * H * D,
                   static_cast<uint32_t>(CB * H * D * sizeof(T)));
-  PackedState<T, C::NT, C::CPW> ps;
-  ps.pack(dS);
+  if constexpr (!SH) ps.pack(dS);
   // the row factors of the lane's four rows, read before the loop
   float xr[CB / 16];
 #pragma unroll
@@ -1003,8 +1071,11 @@ __device__ __forceinline__ void bwd_revorder_rows(
         for (int r = 0; r < 4; ++r) dst[16 * j + r] = acc[j][r];
     }
   }
+  if constexpr (SH) {
+    if (side) return;
+  }
   // side 0: dS   <- exp(G_last) dS   + Q^T  diag(exp(G) scale) dO
-  // side 1: dS^T <- exp(G_last) dS^T + dO^T diag(exp(G) scale) Q
+  // side 1: dS^T <- exp(G_last) dS^T + dO^T diag(exp(G) scale) Q   (fp32)
   const float dec = __expf(GL);
 #pragma unroll
   for (int i = 0; i < NS; ++i) dS[i] *= dec;
@@ -1012,6 +1083,12 @@ __device__ __forceinline__ void bwd_revorder_rows(
     state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, Q, dOt, col0, mt.y, lane);
   else
     state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, dOt, Q, col0, mt.y, lane);
+  if constexpr (SH) {
+    if (more) {
+      ps.pack(dS);
+      adj_store<D, C::NT, C::CPW>(sm.tl.dt, ps, w, lane);
+    }
+  }
 }
 
 template <typename T, int D>
@@ -1025,6 +1102,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     const float* __restrict__ dS_final, float* __restrict__ dS0) {
   using C = Cfg<T, D>;
   constexpr int NTH = 2 * C::NTHR;
+  constexpr bool SH = BrSmem<T, D>::SH;
   using SG = Stg<T, D, NTH>;
   constexpr int RG = 2 * D + 1;
   __shared__ BrSmem<T, D> sm;
@@ -1040,9 +1118,9 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   const bool last = bk[BLK_IDX] == seq_tab[li * SEQ_WORDS + SEQ_N_BLK] - 1;
   const float* dS_in = last ? dS_final + (static_cast<int64_t>(seq_tab[li * SEQ_WORDS + SEQ_FINAL_LEAF]) * H + h) * DD
                             : dS_end + (static_cast<int64_t>(b) * H + h) * DD;
-  static_assert(StateStage<D>::BYTES <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)),
-                "state staging fits the second tile buffer");
-  float* stg = reinterpret_cast<float*>(&sm.tile[1][0][0]);
+  static_assert(StateStage<D>::BYTES <= BrTiles<T, D>::STAGE_BYTES,
+                "state staging fits the tiles that are free before the loop");
+  float* stg = sm.tl.stage();
   // Side 0, wave 3 (lane = row of the chunk) publishes each chunk's row table
   // and decay factors during the score phase of the chunk before it, in which
   // it computes no score block.
@@ -1057,25 +1135,28 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   // The last chunk of the block goes into buffer 0, two tiles at a time.
   ChunkSrc<T, D, NTH> cs;
   Vec16 pa[SG::NV], pb[SG::NV];
-  // dS_end is read once into the second buffer (free until the first
-  // chunk's score), next to the first chunk's tiles
+  // dS_end is read once into the staging area (free until the first chunk's
+  // score), next to the first chunk's tiles
   cs.resolve(sq, c_last, replay_row, g, H, h, tid, mrow);
   fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
   fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
   state_to_lds<D, NTH>(stg, dS_in, tid);
-  put<T, D, NTH>(sm.tile[0][TQ], pa, nullptr, tid);
-  put<T, D, NTH>(sm.tile[0][TK], pb, nullptr, tid);
+  put<T, D, NTH>(sm.tl.at(0, TQ), pa, nullptr, tid);
+  put<T, D, NTH>(sm.tl.at(0, TK), pb, nullptr, tid);
   fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
   fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
-  put<T, D, NTH>(sm.tile[0][TV], pa, nullptr, tid);
-  put<T, D, NTH>(sm.tile[0][TDO], pb, nullptr, tid);
+  put<T, D, NTH>(sm.tl.at(0, TV), pa, nullptr, tid);
+  put<T, D, NTH>(sm.tl.at(0, TDO), pb, nullptr, tid);
   if (pw) publish(cs, 0);
   ChunkRows cur_next = cs.cr;
   __syncthreads();
   // side 0: dS   rows (dk), columns (dv) of the wave's strips
-  // side 1: dS^T rows (dv), columns (dk) of the wave's strips
+  // side 1: dS^T rows (dv), columns (dk) of the wave's strips (bf16: only
+  // to form the first chunk's operands)
   f32x4 dS[C::CPW * C::NT];
   state_from_lds<D, C::CPW>(dS, stg, side == 1, w, lane);
+  PackedState<T, C::NT, C::CPW> ps;
+  if constexpr (SH) ps.pack(dS);
   // the first two tiles of the chunk before it
   if (c_last > c0) {
     cs.resolve(sq, c_last - 1, replay_row, g, H, h, tid, mrow);
@@ -1117,10 +1198,14 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     const float GL = sm.meta[bf].G[CB - 1];
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i], in three 32 x 32 blocks per half
-    if constexpr (BrSmem<T, D>::NP == 2) {
+    if constexpr (SH) {
+      // side 1: the adjoint's operands as side 0 left them after the chunk before
+      if (side && c < c_last) {
+        if constexpr (sizeof(T) == 2) adj_load<D, C::NT, C::CPW>(ps, sm.tl.dt, w, lane);
+      }
       if (w < 3) {
-        if (side) score_block<T, D, true>(sm.P[1], sm.tile[bf][TDO], sm.tile[bf][TV], sm.meta[bf].G, scale, w, lane);
-        else score_block<T, D, true>(sm.P[0], sm.tile[bf][TQ], sm.tile[bf][TK], sm.meta[bf].G, 1.f, w, lane);
+        if (side) score_block<T, D, true>(sm.P[1], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
+        else score_block<T, D, true>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
       } else if (sw && c < c_last) {
         suffix(c + 1);
       } else if (pw && more) {
@@ -1128,32 +1213,35 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       }
     } else {
       if (pw && more) publish(cs, nb);
-      if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.tile[bf][TQ], sm.tile[bf][TK], sm.meta[bf].G, 1.f, w, lane);
+      if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
     }
     // next chunk: Q, K into the other buffer; V, dO requested
     if (more) {
-      put<T, D, NTH>(sm.tile[nb][TQ], pa, nullptr, tid);
-      put<T, D, NTH>(sm.tile[nb][TK], pb, nullptr, tid);
+      put<T, D, NTH>(sm.tl.at(nb, TQ), pa, nullptr, tid);
+      put<T, D, NTH>(sm.tl.at(nb, TK), pb, nullptr, tid);
       fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
       fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
     }
     __syncthreads();
-    if constexpr (BrSmem<T, D>::NP == 2) {
-      if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
-      else bwd_revorder_rows<T, D, 0>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+    if constexpr (SH) {
+      if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      else bwd_revorder_rows<T, D, 0>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      // every wave is done with this chunk's V and dO before the next ones
+      // replace them
+      if (more) __syncthreads();
     } else {
-      if (!side) bwd_revorder_rows<T, D, 0>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      if (!side) bwd_revorder_rows<T, D, 0>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
       __syncthreads();
-      if (side && w < 3) score_block<T, D, true>(sm.P[0], sm.tile[bf][TDO], sm.tile[bf][TV], sm.meta[bf].G, scale, w, lane);
+      if (side && w < 3) score_block<T, D, true>(sm.P[0], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
       else if (sw && c < c_last) suffix(c + 1);
       __syncthreads();
-      if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, cur, sq, c, H, h, scale, GL, w, lane, dk, dv, rep_grad);
+      if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
     }
-    // next chunk: V, dO into the other buffer; the chunk after it resolved
-    // and its Q, K requested
+    // next chunk: V, dO into their buffer; the chunk after it resolved and
+    // its Q, K requested
     if (more) {
-      put<T, D, NTH>(sm.tile[nb][TV], pa, nullptr, tid);
-      put<T, D, NTH>(sm.tile[nb][TDO], pb, nullptr, tid);
+      put<T, D, NTH>(sm.tl.at(nb, TV), pa, nullptr, tid);
+      put<T, D, NTH>(sm.tl.at(nb, TDO), pb, nullptr, tid);
       cur_next = cs.cr;
       if (c - 1 > c0) {
         cs.resolve(sq, c - 2, replay_row, g, H, h, tid, mrow);

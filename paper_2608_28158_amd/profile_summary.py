@@ -5,9 +5,16 @@ summaries kept under ``profiles/``.
     python -m paper_2608_28158_amd.profile_summary traffic <fetch.csv> <write.csv> \\
         <copy_fetch.csv> <copy_write.csv> <copy_mib> <kernel> <out.txt> <command...>
 
+    python -m paper_2608_28158_amd.profile_summary counters <out.md> <cu_count> \\
+        <pass1.csv> [<pass2.csv> ...] -- <command...>
+
 The traffic summary scales FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by
 what the same counters read for a plain device copy of known size, and
-records the hash of the kernel sources it was taken on.
+records the hash of the kernel sources it was taken on.  The counter summary
+gives every counter's mean per dispatch for each kernel, and the derived
+ratios: MFMA busy (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE times four
+SIMDs per CU), and the shares of wave cycles spent waiting or issuing LDS,
+VALU and vector-memory instructions.
 """
 from __future__ import annotations
 
@@ -82,8 +89,54 @@ def traffic(fetch, write, cfetch, cwrite, copy_mib, kernel, out, cmd):
     open(out, "w").write("\n".join(lines) + "\n")
 
 
+def counters(out, cu_count, paths, cmd):
+    vals = collections.defaultdict(dict)   # kernel -> counter -> mean per dispatch
+    for path in paths:
+        agg = collections.defaultdict(float)
+        disp = collections.defaultdict(set)
+        for r in csv.DictReader(open(path)):
+            k = short(r["Kernel_Name"])
+            agg[(k, r["Counter_Name"])] += float(r["Counter_Value"])
+            disp[(k, r["Counter_Name"])].add(r["Dispatch_Id"])
+        for (k, c), v in agg.items():
+            vals[k][c] = v / len(disp[(k, c)])
+    names = sorted({c for d in vals.values() for c in d})
+    kernels = sorted(vals, key=lambda k: -vals[k].get("SQ_WAVE_CYCLES", vals[k].get("GRBM_GUI_ACTIVE", 0)))
+    lines = ["# rocprofv3 counters per kernel (mean per dispatch)", "", "Command (one run per pass):",
+             "", "    " + " ".join(cmd), "", f"Kernel source hash: {source_sha()}", ""]
+
+    def ratio(d, a, b, f=1.0):
+        return "%.1f%%" % (100.0 * d[a] / (d[b] * f)) if a in d and d.get(b) else "-"
+
+    lines += ["| kernel | MFMA busy | MFMA bf16 Mops | wait any | wait LDS | LDS issue | "
+              "VALU issue | VMEM issue | LDS bank-conflict cycles / LDS instr |",
+              "|---|---|---|---|---|---|---|---|---|"]
+    for k in kernels:
+        d = vals[k]
+        conf = ("%.2f" % (d["SQ_LDS_BANK_CONFLICT"] / d["SQ_INSTS_LDS"])
+                if d.get("SQ_INSTS_LDS") and "SQ_LDS_BANK_CONFLICT" in d else "-")
+        mops = ("%.0f" % (d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] / 1e6)
+                if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in d else "-")
+        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s | %s |" % (
+            k, ratio(d, "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", 4.0 * cu_count), mops,
+            ratio(d, "SQ_WAIT_ANY", "SQ_WAVE_CYCLES"), ratio(d, "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES"),
+            ratio(d, "SQ_ACTIVE_INST_LDS", "SQ_WAVE_CYCLES"),
+            ratio(d, "SQ_ACTIVE_INST_VALU", "SQ_WAVE_CYCLES"),
+            ratio(d, "SQ_ACTIVE_INST_VMEM", "SQ_WAVE_CYCLES"), conf))
+    lines += ["", "Raw means per dispatch:", "", "| kernel | " + " | ".join(names) + " |",
+              "|---" * (len(names) + 1) + "|"]
+    for k in kernels:
+        lines.append("| %s | " % k + " | ".join(
+            "%.4g" % vals[k][c] if c in vals[k] else "-" for c in names) + " |")
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4:])
+    elif sys.argv[1] == "counters":
+        rest = sys.argv[4:]
+        cut = rest.index("--")
+        counters(sys.argv[2], int(sys.argv[3]), rest[:cut], rest[cut + 1:])
     else:
         traffic(*sys.argv[2:9], sys.argv[9:])
