@@ -348,11 +348,54 @@ __device__ inline float state_dot_via_lds(const f32x4* S, float* stg, const floa
 // of 16 rows each would read all of R four times).  Inside the diagonal blocks the
 // tile above the diagonal is skipped and stored as zeros: the consumers'
 // 32-deep steps read it.  P[m][n] = f * exp(G_m - G_n) * (L R^T)[m][n] for
-// n <= m; with PT the tile is stored transposed.
+// n <= m; with PT the tile is stored transposed.  The weight is one base-2
+// exponential per element of the difference of pre-scaled prefix sums (the
+// factor f folded in as log2|f| on the row side); above the diagonal of a
+// diagonal tile the exponent is -inf, so the weight is exactly zero.
+template <bool DIAG, bool NEG, typename T, int D, bool PT>
+__device__ __forceinline__ void score_epilogue(T* P, const f32x4 (&c)[2][2], const float* G, float lf,
+                                               int rb, int cb, int lane) {
+  using TA = Tile<T, CB>;
+  constexpr float L2E = 1.4426950408889634f;
+  f32x4 mb;  // exponent bias of a diagonal tile at the lane's rows 4g + r, column lane % 16
+#pragma unroll
+  for (int r = 0; r < 4; ++r) mb[r] = (lane & 15) <= acc_row(lane, r) ? 0.f : -__builtin_inff();
+#pragma unroll
+  for (int ti = 0; ti < 2; ++ti) {
+    const int m0 = rb + 16 * ti;
+    const f32x4 Gm = row_vec(G, m0, lane);
+    f32x4 Gm2;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Gm2[r] = Gm[r] * L2E + lf;
+#pragma unroll
+    for (int tj = 0; tj < 2; ++tj) {
+      const int n = cb + 16 * tj + acc_col(lane);
+      const float Gn2 = G[n] * L2E;
+      f32x4 v;
+      if (DIAG && ti == 0 && tj == 1) {
+        v = f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float a = Gm2[r] - Gn2;
+          if (DIAG && ti == tj) a += mb[r];
+          v[r] = c[ti][tj][r] * __builtin_amdgcn_exp2f(a);
+          if (NEG) v[r] = -v[r];
+        }
+      }
+      if (PT) {
+        Vec4<T>::store(P + TA::at(n, m0 + acc_row(lane, 0)), v);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) P[TA::at(m0 + acc_row(lane, r), n)] = Elem<T>::from_f(v[r]);
+      }
+    }
+  }
+}
+
 template <typename T, int D, bool PT = false>
 __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f,
                                             int w, int lane) {
-  using TA = Tile<T, CB>;
   using TD = Tile<T, D>;
   using F = Frag<T>;
   const int rb = w == 0 ? 0 : 32, cb = w == 2 ? 32 : 0;
@@ -374,24 +417,14 @@ __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, cons
     F::mma(c[1][1], a1, b1);
     if (!diag) F::mma(c[0][1], a0, b1);
   }
-#pragma unroll
-  for (int ti = 0; ti < 2; ++ti) {
-    const int m0 = rb + 16 * ti;
-    const f32x4 Gm = row_vec(G, m0, lane);
-#pragma unroll
-    for (int tj = 0; tj < 2; ++tj) {
-      const int n = cb + 16 * tj + acc_col(lane);
-      const float Gn = G[n];
-      const bool zero = diag && ti == 0 && tj == 1;
-      f32x4 v;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + acc_row(lane, r);
-        v[r] = !zero && n <= m ? c[ti][tj][r] * __expf(Gm[r] - Gn) * f : 0.f;
-        if (!PT) P[TA::at(m, n)] = Elem<T>::from_f(v[r]);
-      }
-      if (PT) Vec4<T>::store(P + TA::at(n, m0 + acc_row(lane, 0)), v);
-    }
+  // f = 1 folds away; otherwise log2|f| joins the row exponents
+  const float lf = f == 1.f ? 0.f : __builtin_amdgcn_logf(__builtin_fabsf(f));
+  if (f < 0.f) {
+    if (diag) score_epilogue<true, true, T, D, PT>(P, c, G, lf, rb, cb, lane);
+    else score_epilogue<false, true, T, D, PT>(P, c, G, lf, rb, cb, lane);
+  } else {
+    if (diag) score_epilogue<true, false, T, D, PT>(P, c, G, lf, rb, cb, lane);
+    else score_epilogue<false, false, T, D, PT>(P, c, G, lf, rb, cb, lane);
   }
 }
 
