@@ -113,13 +113,17 @@ def algorithmic_bytes(plan, H, d, el):
     either; the forward block kernel writes the final states, the
     forward-order backward kernel reads dS_final for the boundary term, the
     reverse-order one starts last blocks from dS_final and writes dS0.
-    Returns (bytes per step, launches per step) per kernel."""
+    Returns (bytes per step, launches per step) per kernel, and the bytes of
+    the separate passes: "fwd" (outputs and final states), "state" (the
+    state pass that the recompute-forward repeats) and "bwd" (the backward
+    from saved block states)."""
     st = H * d * d * 4
     B = 64
     names = ["k_blocksum", "k_fwd_blockscan", "k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan",
              "k_bwd_revorder", "k_dg_carry", "k_scatter_add", "k_replay_reduce"]
     b = dict.fromkeys(names, 0)
     n = dict.fromkeys(names, 0)
+    passes = {"fwd": 0, "state": 0, "bwd": 0}
     init_bank = np.asarray(plan["seq_init_bank"])
     for r in plan.rounds:
         rows, own, rep, nseq, nblk = (r["n_rows"], r["n_own"], r["n_replay"], r["n_seq"],
@@ -143,7 +147,8 @@ def algorithmic_bytes(plan, H, d, el):
         # forward chain (start states of blocks after the first): summaries
         # in, states out, the initial states in, requested states out; in the
         # forward and in the recompute pass
-        b["k_fwd_blockscan"] += 2 * (2 * chained * st + ninit_m * st + nreq * st)
+        scan = 2 * chained * st + ninit_m * st + nreq * st
+        b["k_fwd_blockscan"] += 2 * scan
         n["k_fwd_blockscan"] += 2
         # summaries: side 0 in the forward and the recompute pass (k, v, g of
         # blocks not last, g of last blocks), side 1 in backward (q, dO of
@@ -152,23 +157,32 @@ def algorithmic_bytes(plan, H, d, el):
         side1 = own_nf * H * 2 * d * el + rows_nf * H * 4 + (nblk - nseq) * st
         b["k_blocksum"] += 2 * side0 + side1
         n["k_blocksum"] += 3
-        b["k_fwd_block"] += kv + own * H * 2 * d * el + starts + nseq * st
-        b["k_bwd_fwdorder"] += kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq * st
+        fblock = kv + own * H * 2 * d * el + starts + nseq * st
+        b["k_fwd_block"] += fblock
+        fwdorder = kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq * st
+        b["k_bwd_fwdorder"] += fwdorder
         # adjoint chain: dS_final in, local adjoints of blocks not first in,
         # end adjoints of blocks not last out, requested injections and states in
-        b["k_bwd_blockscan"] += (nseq_m + 2 * chained + 2 * nreq) * st
-        b["k_bwd_revorder"] += (kv + own * H * (2 * d * el + 2 * d * el + 4)
-                                + rep * H * (2 * d + 1) * 4 + rows * H * 4 + nblk * st
-                                + nseq * st)
+        bscan = (nseq_m + 2 * chained + 2 * nreq) * st
+        b["k_bwd_blockscan"] += bscan
+        revorder = (kv + own * H * (2 * d * el + 2 * d * el + 4) + rep * H * (2 * d + 1) * 4
+                    + rows * H * 4 + nblk * st + nseq * st)
+        b["k_bwd_revorder"] += revorder
         b["k_dg_carry"] += rows * H * 8
         b["k_scatter_add"] += 3 * nseq * st
         for name in ("k_fwd_block", "k_bwd_fwdorder", "k_bwd_blockscan", "k_bwd_revorder",
                      "k_dg_carry", "k_scatter_add"):
             n[name] += 1
+        passes["fwd"] += side0 + scan + fblock
+        passes["state"] += side0 + scan
+        passes["bwd"] += side1 + bscan + fwdorder + revorder + rows * H * 8 + 3 * nseq * st
     R = plan.info["R"]
     b["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
     n["k_replay_reduce"] = 1 if R else 0
-    return b, n
+    passes["bwd"] += b["k_replay_reduce"]
+    assert abs(passes["fwd"] + passes["state"] + passes["bwd"] - sum(b.values())) < 1, \
+        "pass bytes add up to the step"
+    return b, n, passes
 
 
 def read_traffic(kernel, workload_key):
@@ -387,7 +401,7 @@ def main():
     el = 2 if cfg["dtype"] == "bf16" else 4
     C = plan.info["C"]
     value = C / (ms * 1e-3)
-    alg, per_step = algorithmic_bytes(plan, H, d, el)
+    alg, per_step, pass_bytes = algorithmic_bytes(plan, H, d, el)
     kstats = {}
     for name, (n, tot) in kern.items():
         steps_seen = max(1, n // max(1, per_step.get(name, 1)))
@@ -436,7 +450,22 @@ def main():
     }
     log("[bench] separate passes")
     passes = pass_times(runner, t, args.steps, args.warmup)
-    out["passes"] = {k: {"ms": v, "compact_tok_s": C / (v * 1e-3)} for k, v in passes.items()}
+    # per pass: algorithmic bytes and FLOPs (SURVEY counts per compact token:
+    # forward 98,304, backward 245,760, state pass 32,768 per head at d = 128)
+    fscale = H * (d / 128) ** 2
+    work = {"fwd": (pass_bytes["fwd"], 98304 * fscale),
+            "bwd": (pass_bytes["bwd"], 245760 * fscale),
+            "fwd_bwd": (pass_bytes["fwd"] + pass_bytes["bwd"], (98304 + 245760) * fscale),
+            "recompute_fwd_bwd": (pass_bytes["fwd"] + pass_bytes["state"] + pass_bytes["bwd"],
+                                  (98304 + 245760 + 32768) * fscale)}
+    out["passes"] = {}
+    for k, v in passes.items():
+        by, fl = work[k]
+        gbs = by / (v * 1e-3) / 1e9
+        tfs = C * fl / (v * 1e-3) / 1e12
+        out["passes"][k] = {"ms": v, "compact_tok_s": C / (v * 1e-3),
+                            "alg_GB": by / 1e9, "alg_GBs": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
+                            "TFLOPs": tfs, "mfma_frac": tfs / peak_tf}
     if not args.no_expanded:
         log("[bench] compact vs expanded (4 trees, ~32k compact tokens)")
         out["compact_vs_expanded"] = expanded_comparison(max(3, args.steps // 2), 2)

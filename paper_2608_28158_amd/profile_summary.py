@@ -5,7 +5,7 @@ summaries kept under ``profiles/``.
     python -m paper_2608_28158_amd.profile_summary traffic <fetch.csv> <write.csv> \\
         <copy_fetch.csv> <copy_write.csv> <copy_mib> <kernel> <out.txt> <command...>
 
-    python -m paper_2608_28158_amd.profile_summary counters <out.md> <cu_count> \\
+    python -m paper_2608_28158_amd.profile_summary counters <out.md> <n_cu> <n_xcd> \\
         <pass1.csv> [<pass2.csv> ...] -- <command...>
 
 The traffic summary scales FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by
@@ -89,45 +89,61 @@ def traffic(fetch, write, cfetch, cwrite, copy_mib, kernel, out, cmd):
     open(out, "w").write("\n".join(lines) + "\n")
 
 
-def counters(out, cu_count, paths, cmd):
+def counters(out, n_cu, n_xcd, paths, cmd):
+    """Per-kernel means per dispatch of every counter in the given pass
+    files, with derived ratios.  GRBM_GUI_ACTIVE reads as the sum over the
+    XCDs, so the MFMA busy share is SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE / n_xcd * n_cu * 4 SIMDs; the bf16 MFMA rate is
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 FLOP over the dispatch duration."""
     vals = collections.defaultdict(dict)   # kernel -> counter -> mean per dispatch
+    dur = collections.defaultdict(list)    # kernel -> dispatch durations (ns)
     for path in paths:
         agg = collections.defaultdict(float)
         disp = collections.defaultdict(set)
+        seen = set()
         for r in csv.DictReader(open(path)):
             k = short(r["Kernel_Name"])
             agg[(k, r["Counter_Name"])] += float(r["Counter_Value"])
             disp[(k, r["Counter_Name"])].add(r["Dispatch_Id"])
+            if (k, r["Dispatch_Id"]) not in seen:
+                seen.add((k, r["Dispatch_Id"]))
+                dur[k].append(float(r["End_Timestamp"]) - float(r["Start_Timestamp"]))
         for (k, c), v in agg.items():
             vals[k][c] = v / len(disp[(k, c)])
     names = sorted({c for d in vals.values() for c in d})
     kernels = sorted(vals, key=lambda k: -vals[k].get("SQ_WAVE_CYCLES", vals[k].get("GRBM_GUI_ACTIVE", 0)))
     lines = ["# rocprofv3 counters per kernel (mean per dispatch)", "", "Command (one run per pass):",
-             "", "    " + " ".join(cmd), "", f"Kernel source hash: {source_sha()}", ""]
+             "", "    " + " ".join(cmd), "", f"Kernel source hash: {source_sha()}", "",
+             f"MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {n_xcd} XCDs x {n_cu} CUs "
+             "x 4 SIMDs); bf16 MFMA rate = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP / dispatch "
+             "duration (peak 2500 TFLOP/s); wait, issue and LDS shares are of SQ_WAVE_CYCLES "
+             "(all in quad-cycles); LDS busy = SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE / "
+             f"{n_xcd} x {n_cu}).", ""]
 
     def ratio(d, a, b, f=1.0):
         return "%.1f%%" % (100.0 * d[a] / (d[b] * f)) if a in d and d.get(b) else "-"
 
-    lines += ["| kernel | MFMA busy | MFMA bf16 Mops | wait any | wait LDS | LDS issue | "
-              "VALU issue | VMEM issue | LDS bank-conflict cycles / LDS instr |",
-              "|---|---|---|---|---|---|---|---|---|"]
+    lines += ["| kernel | MFMA busy | bf16 MFMA TFLOP/s | LDS busy | LDS conflict share | wait any | "
+              "VALU issue | LDS issue |",
+              "|---|---|---|---|---|---|---|---|"]
     for k in kernels:
         d = vals[k]
-        conf = ("%.2f" % (d["SQ_LDS_BANK_CONFLICT"] / d["SQ_INSTS_LDS"])
-                if d.get("SQ_INSTS_LDS") and "SQ_LDS_BANK_CONFLICT" in d else "-")
-        mops = ("%.0f" % (d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] / 1e6)
-                if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in d else "-")
-        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s | %s |" % (
-            k, ratio(d, "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", 4.0 * cu_count), mops,
-            ratio(d, "SQ_WAIT_ANY", "SQ_WAVE_CYCLES"), ratio(d, "SQ_WAIT_INST_LDS", "SQ_WAVE_CYCLES"),
-            ratio(d, "SQ_ACTIVE_INST_LDS", "SQ_WAVE_CYCLES"),
+        tf = "-"
+        if d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16") and dur.get(k):
+            ns = sum(dur[k]) / len(dur[k])
+            tf = "%.0f" % (d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 / ns / 1e3)
+        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s |" % (
+            k, ratio(d, "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", 4.0 * n_cu / n_xcd), tf,
+            ratio(d, "SQ_LDS_IDX_ACTIVE", "GRBM_GUI_ACTIVE", 1.0 * n_cu / n_xcd),
+            ratio(d, "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE"),
+            ratio(d, "SQ_WAIT_ANY", "SQ_WAVE_CYCLES"),
             ratio(d, "SQ_ACTIVE_INST_VALU", "SQ_WAVE_CYCLES"),
-            ratio(d, "SQ_ACTIVE_INST_VMEM", "SQ_WAVE_CYCLES"), conf))
-    lines += ["", "Raw means per dispatch:", "", "| kernel | " + " | ".join(names) + " |",
-              "|---" * (len(names) + 1) + "|"]
-    for k in kernels:
-        lines.append("| %s | " % k + " | ".join(
-            "%.4g" % vals[k][c] if c in vals[k] else "-" for c in names) + " |")
+            ratio(d, "SQ_ACTIVE_INST_LDS", "SQ_WAVE_CYCLES")))
+    lines += ["", "Raw means per dispatch:", "", "| counter | " + " | ".join(kernels) + " |",
+              "|---" * (len(kernels) + 1) + "|"]
+    for c in names:
+        lines.append("| %s | " % c + " | ".join(
+            "%.4g" % vals[k][c] if c in vals[k] else "-" for k in kernels) + " |")
     open(out, "w").write("\n".join(lines) + "\n")
 
 
@@ -135,8 +151,8 @@ if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4:])
     elif sys.argv[1] == "counters":
-        rest = sys.argv[4:]
+        rest = sys.argv[5:]
         cut = rest.index("--")
-        counters(sys.argv[2], int(sys.argv[3]), rest[:cut], rest[cut + 1:])
+        counters(sys.argv[2], int(sys.argv[3]), int(sys.argv[4]), rest[:cut], rest[cut + 1:])
     else:
         traffic(*sys.argv[2:9], sys.argv[9:])
