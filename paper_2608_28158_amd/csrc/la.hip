@@ -46,6 +46,7 @@
 // and accumulation are float32; no floating-point atomics.
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
 #include <cstdint>
 #include <cstring>
 #include <mutex>
@@ -119,8 +120,8 @@ struct ChunkRefs {
   }
 };
 
-// dst[row][d] = src[row][d] (* scale[row] if scale != nullptr)
-template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
+// dst[row][d] = src[row][d] (* scale[row] if scale != nullptr), dst in layout L
+template <typename T, int D, int NTH = Cfg<T, D>::NTHR, typename L = Tile<T, D>>
 __device__ inline void put(T* dst, const Vec16* src, const float* scale, int t) {
   using C = Stg<T, D, NTH>;
 #pragma unroll
@@ -133,7 +134,7 @@ __device__ inline void put(T* dst, const Vec16* src, const float* scale, int t) 
 #pragma unroll
       for (int e = 0; e < C::VE; ++e) vset<T>(v, e, Elem<T>::from_f(Elem<T>::to_f(vget<T>(v, e)) * s));
     }
-    *reinterpret_cast<uint4*>(dst + C::TD::at(row, d0)) = v.u;
+    *reinterpret_cast<uint4*>(dst + L::at(row, d0)) = v.u;
   }
 }
 
@@ -393,10 +394,9 @@ __device__ __forceinline__ void score_epilogue(T* P, const f32x4 (&c)[2][2], con
   }
 }
 
-template <typename T, int D, bool PT = false>
+template <typename T, int D, bool PT = false, typename LL = Tile<T, D>, typename LR = Tile<T, D>>
 __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f,
                                             int w, int lane) {
-  using TD = Tile<T, D>;
   using F = Frag<T>;
   const int rb = w == 0 ? 0 : 32, cb = w == 2 ? 32 : 0;
   const bool diag = rb == cb;
@@ -407,10 +407,10 @@ __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, cons
     for (int j = 0; j < 2; ++j) c[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 1
   for (int k = 0; k < D; k += F::KSTEP) {
-    const typename F::V a0 = F::template kc<TD>(Lt, rb, k, lane);
-    const typename F::V a1 = F::template kc<TD>(Lt, rb + 16, k, lane);
-    const typename F::V b0 = F::template kc<TD>(Rt, cb, k, lane);
-    const typename F::V b1 = F::template kc<TD>(Rt, cb + 16, k, lane);
+    const typename F::V a0 = F::template kc<LL>(Lt, rb, k, lane);
+    const typename F::V a1 = F::template kc<LL>(Lt, rb + 16, k, lane);
+    const typename F::V b0 = F::template kc<LR>(Rt, cb, k, lane);
+    const typename F::V b1 = F::template kc<LR>(Rt, cb + 16, k, lane);
     __builtin_amdgcn_sched_barrier(0);
     F::mma(c[0][0], a0, b0);
     F::mma(c[1][0], a1, b0);
@@ -818,7 +818,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
   f32x4 St[NS];  // S^T : rows (dv), columns (dk) of the wave's strips
   // the start state, staged through the (still unused) tiles
-  static_assert(D * (D + 4) * 4 <= 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T)), "state fits the tiles");
+  using BfS = BfSmem<T, D>;
+  static_assert(D * (D + 4) * 4 <= static_cast<int>(offsetof(BfS, dA)), "state fits the tiles");
   state_via_lds<D, C::CPW, C::NTHR, 1>(St, reinterpret_cast<float*>(&sm.dO[0]),
                                        bk[BLK_IDX] == 0 ? init_state(is, li, H, h, DD)
                                                         : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
@@ -940,12 +941,19 @@ struct AdjT {
   static constexpr int LD = D + 8;
   static constexpr int SIZE = D * LD;
   __device__ static inline int at(int r, int c) { return r * LD + c; }
+  __device__ static inline int base(int r0, int c0) { return r0 * LD + c0; }
+  __device__ static inline int lane(int ri, int ci) { return ri * LD + ci; }
 };
 
+// Q and dO are read transposed (state update, the products with the score
+// tiles) and take the swizzled layout where it exists; K and V are read
+// k-contiguous only.
 template <typename T, int D, bool SH = (sizeof(T) == 2)>
 struct BrTiles;
 template <typename T, int D>
 struct BrTiles<T, D, false> {
+  using LQ = Tile<T, D>;
+  using LK = Tile<T, D>;
   T tile[2][4][Tile<T, D>::SIZE];
   static constexpr int STAGE_BYTES = 4 * Tile<T, D>::SIZE * static_cast<int>(sizeof(T));
   __device__ inline T* at(int bf, int which) { return tile[bf][which]; }
@@ -953,12 +961,20 @@ struct BrTiles<T, D, false> {
 };
 template <typename T, int D>
 struct BrTiles<T, D, true> {
-  T qk[2][2][Tile<T, D>::SIZE];
-  T dt[AdjT<D>::SIZE];  // follows qk[1]: the two form the staging area
-  T vdo[2][Tile<T, D>::SIZE];
-  static constexpr int STAGE_BYTES = (2 * Tile<T, D>::SIZE + AdjT<D>::SIZE) * static_cast<int>(sizeof(T));
-  __device__ inline T* at(int bf, int which) { return which < 2 ? qk[bf][which] : vdo[which - 2]; }
-  __device__ inline float* stage() { return reinterpret_cast<float*>(&qk[1][0][0]); }
+  using LQ = TileX<T, D>;  // Q and dO
+  using LK = Tile<T, D>;   // K and V
+  T q0[LQ::SIZE];
+  T k0[LK::SIZE];
+  T q1[LQ::SIZE];          // q1, k1 and dt form the staging area
+  T k1[LK::SIZE];
+  T dt[AdjT<D>::SIZE];
+  T v[LK::SIZE];
+  T dO[LQ::SIZE];
+  static constexpr int STAGE_BYTES = (LQ::SIZE + LK::SIZE + AdjT<D>::SIZE) * static_cast<int>(sizeof(T));
+  __device__ inline T* at(int bf, int which) {
+    return which == TQ ? (bf ? q1 : q0) : which == TK ? (bf ? k1 : k0) : which == TV ? v : dO;
+  }
+  __device__ inline float* stage() { return reinterpret_cast<float*>(q1); }
 };
 
 template <typename T, int D>
@@ -1024,6 +1040,8 @@ __device__ __forceinline__ void bwd_revorder_rows(
   constexpr bool side = SIDE == 1;
   const int col0 = C::CPW * w * 16;
   const T* PT = sm.P[BrSmem<T, D>::NP == 2 ? SIDE : 0];  // transposed score tile
+  using LQ = typename BrTiles<T, D>::LQ;  // Q and dO
+  using LK = typename BrTiles<T, D>::LK;  // K and V
   const T* Q = sm.tl.at(bf, TQ);
   const T* K = sm.tl.at(bf, TK);
   const T* V = sm.tl.at(bf, TV);
@@ -1047,7 +1065,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
     typename Vec4Raw<T>::V kraw[C::CPW];
     if (side) {
 #pragma unroll
-      for (int j = 0; j < C::CPW; ++j) kraw[j] = Vec4Raw<T>::load(K + C::TD::at(m, col0 + 16 * j + g4));
+      for (int j = 0; j < C::CPW; ++j) kraw[j] = Vec4Raw<T>::load(K + LK::at(m, col0 + 16 * j + g4));
     }
     // side 0: dv = diag(x) K dS + scale A^T dO ; side 1: dk = diag(x) V dS^T + dA^T Q
     // (A and dA vanish above the diagonal, so the transposed products start at row block jt)
@@ -1057,9 +1075,9 @@ __device__ __forceinline__ void bwd_revorder_rows(
       acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
       ad[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true, true>(acc, side ? V : K, jt * 16, ps, lane);
+    regb_rows_packed<T, LK, C::NT, C::CPW, true, true>(acc, side ? V : K, jt * 16, ps, lane);
     const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
-    tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true, true>(
+    tile_cols<T, typename C::TA, false, LQ, C::CPW, true, true>(
         ad, PT, jt * 16, side ? Q : dOt, col0, k0, CB, lane);
     float e = xr[0];
 #pragma unroll
@@ -1113,9 +1131,9 @@ __device__ __forceinline__ void bwd_revorder_rows(
 #pragma unroll
   for (int i = 0; i < NS; ++i) dS[i] *= dec;
   if (!side)
-    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, Q, dOt, col0, mt.y, lane);
+    state_update<T, LQ, LQ, C::NT, C::CPW, true>(dS, Q, dOt, col0, mt.y, lane);
   else
-    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW, true>(dS, dOt, Q, col0, mt.y, lane);
+    state_update<T, LQ, LQ, C::NT, C::CPW, true>(dS, dOt, Q, col0, mt.y, lane);
   if constexpr (SH) {
     if (more) {
       ps.pack(dS);
@@ -1137,6 +1155,8 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   constexpr int NTH = 2 * C::NTHR;
   constexpr bool SH = BrSmem<T, D>::SH;
   using SG = Stg<T, D, NTH>;
+  using LQ = typename BrTiles<T, D>::LQ;  // Q and dO
+  using LK = typename BrTiles<T, D>::LK;  // K and V
   constexpr int RG = 2 * D + 1;
   __shared__ BrSmem<T, D> sm;
   const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, tid = threadIdx.x;
@@ -1174,12 +1194,12 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
   fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
   state_to_lds<D, NTH>(stg, dS_in, tid);
-  put<T, D, NTH>(sm.tl.at(0, TQ), pa, nullptr, tid);
-  put<T, D, NTH>(sm.tl.at(0, TK), pb, nullptr, tid);
+  put<T, D, NTH, LQ>(sm.tl.at(0, TQ), pa, nullptr, tid);
+  put<T, D, NTH, LK>(sm.tl.at(0, TK), pb, nullptr, tid);
   fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
   fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
-  put<T, D, NTH>(sm.tl.at(0, TV), pa, nullptr, tid);
-  put<T, D, NTH>(sm.tl.at(0, TDO), pb, nullptr, tid);
+  put<T, D, NTH, LK>(sm.tl.at(0, TV), pa, nullptr, tid);
+  put<T, D, NTH, LQ>(sm.tl.at(0, TDO), pb, nullptr, tid);
   if (pw) publish(cs, 0);
   ChunkRows cur_next = cs.cr;
   __syncthreads();
@@ -1237,8 +1257,8 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
         if constexpr (sizeof(T) == 2) adj_load<D, C::NT, C::CPW>(ps, sm.tl.dt, w, lane);
       }
       if (w < 3) {
-        if (side) score_block<T, D, true>(sm.P[1], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
-        else score_block<T, D, true>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
+        if (side) score_block<T, D, true, LQ, LK>(sm.P[1], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
+        else score_block<T, D, true, LQ, LK>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
       } else if (sw && c < c_last) {
         suffix(c + 1);
       } else if (pw && more) {
@@ -1246,12 +1266,12 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       }
     } else {
       if (pw && more) publish(cs, nb);
-      if (!side && w < 3) score_block<T, D, true>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
+      if (!side && w < 3) score_block<T, D, true, LQ, LK>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
     }
     // next chunk: Q, K into the other buffer; V, dO requested
     if (more) {
-      put<T, D, NTH>(sm.tl.at(nb, TQ), pa, nullptr, tid);
-      put<T, D, NTH>(sm.tl.at(nb, TK), pb, nullptr, tid);
+      put<T, D, NTH, LQ>(sm.tl.at(nb, TQ), pa, nullptr, tid);
+      put<T, D, NTH, LK>(sm.tl.at(nb, TK), pb, nullptr, tid);
       fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
       fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
     }
@@ -1265,7 +1285,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     } else {
       if (!side) bwd_revorder_rows<T, D, 0>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
       __syncthreads();
-      if (side && w < 3) score_block<T, D, true>(sm.P[0], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
+      if (side && w < 3) score_block<T, D, true, LQ, LK>(sm.P[0], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
       else if (sw && c < c_last) suffix(c + 1);
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
@@ -1273,8 +1293,8 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     // next chunk: V, dO into their buffer; the chunk after it resolved and
     // its Q, K requested
     if (more) {
-      put<T, D, NTH>(sm.tl.at(nb, TV), pa, nullptr, tid);
-      put<T, D, NTH>(sm.tl.at(nb, TDO), pb, nullptr, tid);
+      put<T, D, NTH, LK>(sm.tl.at(nb, TV), pa, nullptr, tid);
+      put<T, D, NTH, LQ>(sm.tl.at(nb, TDO), pb, nullptr, tid);
       cur_next = cs.cr;
       if (c - 1 > c0) {
         cs.resolve(sq, c - 2, replay_row, g, H, h, tid, mrow);

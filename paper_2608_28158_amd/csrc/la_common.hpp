@@ -106,15 +106,34 @@ template <> struct BufVec4<float> {
 // LDS tile layout: 64 rows of COLS elements, row-major, each row padded by
 // 16 bytes.  Addresses are affine in (r, c), so every fragment read is a
 // per-lane base plus an immediate offset.  With the padding, 16-byte row
-// writes and 2-byte accumulator-layout writes are free of bank conflicts and
-// the 8-byte fragment reads below (k-contiguous and transposed) lose at most
-// a few cycles per instruction to them.
-template <typename T, int COLS>
+// writes, 2-byte accumulator-layout writes and the k-contiguous 8-byte
+// fragment reads below are free of bank conflicts; the transpose reads take
+// twice their minimum time (measured on gfx950, whose LDS serves 256 bytes a
+// clock to reads).
+//
+// XS (bf16 rows of 128 elements only): rows padded by 32 bytes, and in rows
+// 8..15 of every 16-row group the 8-byte units swap in pairs of pairs
+// (element bit 3 flipped).  Then both the k-contiguous fragment reads and
+// the transpose reads are conflict-free: a half-wave's 32 lanes hit 32
+// distinct bank pairs (the plain 32-byte pad serves the transpose reads but
+// doubles the fragment reads).  16-byte units stay contiguous.  Fragment
+// reads with origins (r0, c0) that are multiples of 16 address
+// base(r0, c0) + lane(ri, ci): an affine part plus a lane constant.
+template <typename T, int COLS, bool XS = false>
 struct Tile {
-  static constexpr int LD = COLS + 16 / static_cast<int>(sizeof(T));  // row stride (elements)
+  static_assert(!XS || (sizeof(T) == 2 && COLS == 128), "swizzled rows are bf16 x 128");
+  static constexpr int LD = COLS + (XS ? 32 : 16) / static_cast<int>(sizeof(T));  // row stride (elements)
   static constexpr int SIZE = CB * LD;
-  __device__ static inline int at(int r, int c) { return r * LD + c; }
+  __device__ static inline int swz(int r) { return XS ? ((r >> 3) & 1) << 3 : 0; }
+  __device__ static inline int at(int r, int c) { return r * LD + (c ^ swz(r)); }
+  __device__ static inline int base(int r0, int c0) { return r0 * LD + c0; }
+  __device__ static inline int lane(int ri, int ci) { return ri * LD + (ci ^ swz(ri)); }
 };
+
+// The swizzled layout where the element type and head dimension allow it,
+// else the plain one.
+template <typename T, int D>
+using TileX = Tile<T, D, sizeof(T) == 2 && D == 128>;
 
 // Launch shape for element type T and head dimension D.  Four waves per
 // workgroup; wave w owns the state columns 16 CPW w .. 16 CPW (w + 1) - 1 (CPW
@@ -131,6 +150,7 @@ struct Cfg {
   static constexpr int CPW = D / 16 / NW;              // 16-column strips per wave
   static constexpr int WPE = 2;                        // waves per SIMD
   using TD = Tile<T, D>;                               // [64][D] tiles
+  using TX = TileX<T, D>;                              // [64][D] tiles read transposed
   using TA = Tile<T, CB>;                              // [64][64] tiles
   static_assert(CPW >= 1 && NT == NW * CPW, "state split into column strips");
 };
@@ -155,18 +175,18 @@ template <> struct Frag<bf16> {
     v[4] = b[0]; v[5] = b[1]; v[6] = b[2]; v[7] = b[3];
     return v;
   }
+  // (r0, c0 multiples of 16: the lane parts stay inside one 16 x 16 block)
   template <typename L>
   __device__ static inline V kc(const bf16* t, int r0, int c0, int lane) {
-    const int r = r0 + (lane & 15), c = c0 + (lane >> 4) * 4;
-    return join(*reinterpret_cast<const bf16x4*>(t + L::at(r, c)),
-                *reinterpret_cast<const bf16x4*>(t + L::at(r, c + 16)));
+    const bf16* p = t + L::base(r0, c0) + L::lane(lane & 15, (lane >> 4) * 4);
+    return join(*reinterpret_cast<const bf16x4*>(p), *reinterpret_cast<const bf16x4*>(p + 16));
   }
   template <typename L>
   __device__ static inline V km(const bf16* t, int r0, int c0, int lane) {
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const int r = r0 + (lane >> 4) * 4 + ((lane & 15) >> 2), c = c0 + 4 * (lane & 3);
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(t + L::at(r, c)));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(t + L::at(r + 16, c)));
+    const bf16* p = t + L::base(r0, c0) + L::lane((lane >> 4) * 4 + ((lane & 15) >> 2), 4 * (lane & 3));
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * L::LD));
     return join(__builtin_bit_cast(bf16x4, lo), __builtin_bit_cast(bf16x4, hi));
   }
   // km fragment with row k of the tile (the contraction index) scaled by
