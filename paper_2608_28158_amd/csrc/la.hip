@@ -444,7 +444,7 @@ __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, cons
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksum(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ blk_order,
+    const int32_t* __restrict__ blk_launch,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dO,
     const float* __restrict__ g, float* __restrict__ dSb, float* __restrict__ U,
@@ -454,18 +454,18 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   __shared__ T Ys[Tile<T, D>::SIZE];
   __shared__ ChunkMeta meta;
   const int side = side0 + static_cast<int>(blockIdx.z);
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
+  const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
+  const int b = bl.b, h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
   // The block kernels end a sequence's forward chain and start its adjoint
   // chain themselves: the first block's adjoint summary is never needed, nor
   // the last block's forward summary, of which only Gamma_b is (for the
   // adjoint chain).
-  if (skip1 && side && bk[BLK_IDX] == 0) return;
-  const SeqInfo sq = seq_info(seq_tab + bk[BLK_SEQ] * SEQ_WORDS);
-  const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  if (skip1 && side && bl.idx == 0) return;
+  const SeqInfo sq = bl.sq;
+  const int c0 = bl.c0, c_end = c0 + bl.nc;
   const int64_t bi = static_cast<int64_t>(b) * H + h;
-  if (skip1 && !side && bk[BLK_IDX] == seq_tab[bk[BLK_SEQ] * SEQ_WORDS + SEQ_N_BLK] - 1) {
+  if (skip1 && !side && bl.idx == bl.n_blk - 1) {
     if (w != 0) return;
     // Gamma_b alone, summed chunk by chunk as below; wave 0, lane = row
     ChunkSrc<T, D> cs;
@@ -530,6 +530,11 @@ __device__ inline const float* init_state(const InitSrc& is, int li, int H, int 
   if (is.S0) return is.S0 + (static_cast<int64_t>(li) * H + h) * DD;
   const int i = is.idx[li];
   return i >= 0 ? is.bank + (static_cast<int64_t>(i) * H + h) * DD : nullptr;
+}
+// The same with the bank index already at hand (from the launch table).
+__device__ inline const float* init_state(const InitSrc& is, const BlkInfo& bl, int H, int h, int64_t DD) {
+  if (is.S0) return is.S0 + (static_cast<int64_t>(bl.li) * H + h) * DD;
+  return bl.init_bank >= 0 ? is.bank + (static_cast<int64_t>(bl.init_bank) * H + h) * DD : nullptr;
 }
 
 // ---------------------------------------------------------------------------
@@ -676,7 +681,7 @@ struct FwdSmem {
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_block(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ blk_order,
+    const int32_t* __restrict__ blk_launch,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const InitSrc is, const float* __restrict__ S_end, T* __restrict__ o, float* __restrict__ S_final) {
@@ -684,13 +689,12 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ FwdSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
+  const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
+  const int b = bl.b, h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
   const int col0 = C::CPW * w * 16;
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int li = bk[BLK_SEQ];
-  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
-  const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  const SeqInfo sq = bl.sq;
+  const int c0 = bl.c0, c_end = c0 + bl.nc;
   const int64_t DD = static_cast<int64_t>(D) * D;
   // the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
@@ -704,8 +708,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
   static_assert(D / 2 * (D + 4) * 4 <= static_cast<int>(sizeof(FwdSmem<T, D>) - sizeof(ChunkMeta)),
                 "half a state fits the tiles");
   state_via_lds<D, C::CPW, C::NTHR, 2>(S, reinterpret_cast<float*>(&sm.Q[0]),
-                                       bk[BLK_IDX] == 0 ? init_state(is, li, H, h, DD)
-                                                        : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                                       bl.idx == 0 ? init_state(is, bl, H, h, DD)
+                                                   : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
                                        false, w, lane, t);
   for (int c = c0; c < c_end; ++c) {
     if (t < CB) {
@@ -767,9 +771,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     __syncthreads();
   }
   // the last block of a sequence: its end state is the final state
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  if (S_final && bk[BLK_IDX] == seq[SEQ_N_BLK] - 1)
-    state_store<D, C::CPW>(S_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * DD, S, w, lane);
+  if (S_final && bl.idx == bl.n_blk - 1)
+    state_store<D, C::CPW>(S_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD, S, w, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -790,7 +793,7 @@ struct BfSmem {
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwdorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ blk_order,
+    const int32_t* __restrict__ blk_launch,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const T* __restrict__ dO, const InitSrc is, const float* __restrict__ S_end,
@@ -800,13 +803,12 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ BfSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
+  const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
+  const int b = bl.b, h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
   const int col0 = C::CPW * w * 16;
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int li = bk[BLK_SEQ];
-  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
-  const int c0 = bk[BLK_C0], c_end = c0 + bk[BLK_NC];
+  const SeqInfo sq = bl.sq;
+  const int c0 = bl.c0, c_end = c0 + bl.nc;
   const int64_t DD = static_cast<int64_t>(D) * D;
   // the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
@@ -821,8 +823,8 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   using BfS = BfSmem<T, D>;
   static_assert(D * (D + 4) * 4 <= static_cast<int>(offsetof(BfS, dA)), "state fits the tiles");
   state_via_lds<D, C::CPW, C::NTHR, 1>(St, reinterpret_cast<float*>(&sm.dO[0]),
-                                       bk[BLK_IDX] == 0 ? init_state(is, li, H, h, DD)
-                                                        : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                                       bl.idx == 0 ? init_state(is, bl, H, h, DD)
+                                                   : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
                                        true, w, lane, t);
   for (int c = c0; c < c_end; ++c) {
     if (t < CB) {
@@ -902,12 +904,11 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwd
   // The last block of a sequence ends with S_final (S^T is held):
   // <dS_final, S_final> is its boundary term of dg, the first of the block's
   // NSW partial sums.
-  const int32_t* seq = seq_tab + li * SEQ_WORDS;
-  if (bk[BLK_IDX] == seq[SEQ_N_BLK] - 1) {
+  if (bl.idx == bl.n_blk - 1) {
     constexpr int NSW = D * D / 4 / SCAN_THR;
     const float dot = state_dot_via_lds<D, C::CPW, C::NTHR>(
         St, reinterpret_cast<float*>(&sm.dO[0]),
-        dS_final + (static_cast<int64_t>(seq[SEQ_FINAL_LEAF]) * H + h) * DD, true, w, lane, t, sm.rq[0]);
+        dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD, true, w, lane, t, sm.rq[0]);
     if (t < NSW) betap[(static_cast<int64_t>(b) * H + h) * NSW + t] = t == 0 ? dot : 0.f;
   }
 }
@@ -1145,7 +1146,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
 template <typename T, int D>
 __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_revorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
-    const int32_t* __restrict__ blk_order, const int32_t* __restrict__ replay_row, int H,
+    const int32_t* __restrict__ blk_launch, const int32_t* __restrict__ replay_row, int H,
     float scale, const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ g, const T* __restrict__ dO, const float* __restrict__ dS_end,
     const float* __restrict__ rq, T* __restrict__ dk, T* __restrict__ dv,
@@ -1159,17 +1160,17 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   using LK = typename BrTiles<T, D>::LK;  // K and V
   constexpr int RG = 2 * D + 1;
   __shared__ BrSmem<T, D> sm;
-  const int b = blk_order[blockIdx.x / H], h = blockIdx.x % H, tid = threadIdx.x;
+  const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
+  const int b = bl.b, h = blockIdx.x % H, tid = threadIdx.x;
   const int side = tid >= C::NTHR ? 1 : 0;  // uniform over a wave
   const int t = tid - side * C::NTHR, lane = tid & 63, w = wave_id(t);
-  const int32_t* bk = blk_tab + b * BLK_WORDS;
-  const int li = bk[BLK_SEQ];
-  const SeqInfo sq = seq_info(seq_tab + li * SEQ_WORDS);
-  const int c0 = bk[BLK_C0], c_last = c0 + bk[BLK_NC] - 1;
+  const int li = bl.li;
+  const SeqInfo sq = bl.sq;
+  const int c0 = bl.c0, c_last = c0 + bl.nc - 1;
   const int64_t DD = static_cast<int64_t>(D) * D;
   // a sequence's last block starts from dS_final, its first block ends with dS0
-  const bool last = bk[BLK_IDX] == seq_tab[li * SEQ_WORDS + SEQ_N_BLK] - 1;
-  const float* dS_in = last ? dS_final + (static_cast<int64_t>(seq_tab[li * SEQ_WORDS + SEQ_FINAL_LEAF]) * H + h) * DD
+  const bool last = bl.idx == bl.n_blk - 1;
+  const float* dS_in = last ? dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD
                             : dS_end + (static_cast<int64_t>(b) * H + h) * DD;
   static_assert(StateStage<D>::BYTES <= BrTiles<T, D>::STAGE_BYTES,
                 "state staging fits the tiles that are free before the loop");
@@ -1188,18 +1189,22 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
   // The last chunk of the block goes into buffer 0, two tiles at a time.
   ChunkSrc<T, D, NTH> cs;
   Vec16 pa[SG::NV], pb[SG::NV];
-  // dS_end is read once into the staging area (free until the first chunk's
-  // score), next to the first chunk's tiles
+  // The first chunk's four tiles and dS_end (read once into the staging
+  // area, free until the first chunk's score) are requested together: one
+  // memory round trip before the loop.
   cs.resolve(sq, c_last, replay_row, g, H, h, tid, mrow);
-  fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
-  fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
-  state_to_lds<D, NTH>(stg, dS_in, tid);
-  put<T, D, NTH, LQ>(sm.tl.at(0, TQ), pa, nullptr, tid);
-  put<T, D, NTH, LK>(sm.tl.at(0, TK), pb, nullptr, tid);
-  fetch<T, D, NTH>(pa, v, cs, H, h, tid, ROW_REPLAY);
-  fetch<T, D, NTH>(pb, dO, cs, H, h, tid, ROW_OWN);
-  put<T, D, NTH, LK>(sm.tl.at(0, TV), pa, nullptr, tid);
-  put<T, D, NTH, LQ>(sm.tl.at(0, TDO), pb, nullptr, tid);
+  {
+    Vec16 pc[SG::NV], pd[SG::NV];
+    fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
+    fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
+    fetch<T, D, NTH>(pc, v, cs, H, h, tid, ROW_REPLAY);
+    fetch<T, D, NTH>(pd, dO, cs, H, h, tid, ROW_OWN);
+    state_to_lds<D, NTH>(stg, dS_in, tid);
+    put<T, D, NTH, LQ>(sm.tl.at(0, TQ), pa, nullptr, tid);
+    put<T, D, NTH, LK>(sm.tl.at(0, TK), pb, nullptr, tid);
+    put<T, D, NTH, LK>(sm.tl.at(0, TV), pc, nullptr, tid);
+    put<T, D, NTH, LQ>(sm.tl.at(0, TDO), pd, nullptr, tid);
+  }
   if (pw) publish(cs, 0);
   ChunkRows cur_next = cs.cr;
   __syncthreads();
@@ -1313,7 +1318,7 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     if (lane == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
   }
   // side 0 holds dS at the start of the block: the first block's is dS0
-  if (bk[BLK_IDX] == 0 && side == 0) state_store<D, C::CPW>(dS0 + (static_cast<int64_t>(li) * H + h) * DD, dS, w, lane);
+  if (bl.idx == 0 && side == 0) state_store<D, C::CPW>(dS0 + (static_cast<int64_t>(li) * H + h) * DD, dS, w, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1516,7 +1521,7 @@ Sizes sizes(const harts_plan_t* p, int32_t round, int32_t H, int32_t D) {
 struct Blob {
   const int32_t* seq_tab;
   const int32_t* blk_tab;
-  const int32_t* blk_order;
+  const int32_t* blk_launch;
   const int32_t* replay_row;
   const int32_t* init_idx;
 };
@@ -1524,7 +1529,7 @@ struct Blob {
 Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   const int32_t* b = static_cast<const int32_t*>(d_blob);
   const RoundLayout& L = p->rounds[round];
-  return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_order, b + p->off_replay_row, b + L.init_idx};
+  return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_launch, b + p->off_replay_row, b + L.init_idx};
 }
 
 // Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b);
@@ -1536,7 +1541,7 @@ int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, 
   const RoundLayout& L = p->rounds[round];
   ProfScope ps("k_blocksum", s);
   hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk * H, 1, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
-                     B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
+                     B.seq_tab, B.blk_tab, B.blk_launch, B.replay_row, H, scale, static_cast<const T*>(q),
                      static_cast<const T*>(k), static_cast<const T*>(v),
                      static_cast<const T*>(dO), g, dSb, U, gam, side0, skip1);
   return hip_check("k_blocksum");
@@ -1580,7 +1585,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   {
     ProfScope ps("k_fwd_block", s);
     hipLaunchKernelGGL((k_fwd_block<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
+                       B.blk_tab, B.blk_launch, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g, is, S_end,
                        static_cast<T*>(o), S_final);
   }
@@ -1636,7 +1641,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   {
     ProfScope ps("k_bwd_fwdorder", s);
     hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.blk_order, B.replay_row, H, scale, static_cast<const T*>(q),
+                       B.blk_tab, B.blk_launch, B.replay_row, H, scale, static_cast<const T*>(q),
                        static_cast<const T*>(k), static_cast<const T*>(v), g,
                        static_cast<const T*>(dO), is, S_end, static_cast<T*>(dq), rq, dS_final, betap);
   }
@@ -1644,7 +1649,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   {
     ProfScope ps("k_bwd_revorder", s);
     hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk * H), dim3(2 * Cfg<T, D>::NTHR), 0, s,
-                       B.seq_tab, B.blk_tab, B.blk_order, B.replay_row, H, scale,
+                       B.seq_tab, B.blk_tab, B.blk_launch, B.replay_row, H, scale,
                        static_cast<const T*>(q), static_cast<const T*>(k),
                        static_cast<const T*>(v), g, static_cast<const T*>(dO), dS_end, rq,
                        static_cast<T*>(dk), static_cast<T*>(dv), dg, rep_grad, Rb, dS_final, dS0);

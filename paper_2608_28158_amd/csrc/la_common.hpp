@@ -445,6 +445,32 @@ __device__ inline SeqInfo seq_info(const int32_t* seq) {
                  seq[SEQ_CHUNK_OFF]};
 }
 
+// A block kernel workgroup's unit of work: one entry of the round's launch
+// table (uniform, kept in scalar registers).
+struct BlkInfo {
+  int b;           // block id
+  int li;          // sequence (local index within the round)
+  int c0, nc;      // first chunk of the block (within the sequence), chunks
+  int idx, n_blk;  // block index within the sequence, blocks of the sequence
+  int final_leaf;  // leaf index receiving the sequence's final state
+  int init_bank;   // bank entry of the sequence's initial state, or -1
+  SeqInfo sq;
+};
+__device__ inline BlkInfo blk_info(const int32_t* launch, int j) {
+  const int32_t* e = launch + j * LCH_WORDS;
+  BlkInfo bl;
+  bl.b = e[LCH_BLK];
+  bl.li = e[LCH_SEQ];
+  bl.c0 = e[LCH_C0];
+  bl.nc = e[LCH_NC];
+  bl.idx = e[LCH_IDX];
+  bl.n_blk = e[LCH_N_BLK];
+  bl.final_leaf = e[LCH_FINAL_LEAF];
+  bl.init_bank = e[LCH_INIT_BANK];
+  bl.sq = SeqInfo{e[LCH_N_REPLAY], e[LCH_N_TOK], e[LCH_REPLAY_OFF], e[LCH_OWN_ROW], e[LCH_CHUNK_OFF]};
+  return bl;
+}
+
 // Packed position p of a sequence -> (global row, kind, replay index).
 struct RowRef {
   int row, kind, rep;

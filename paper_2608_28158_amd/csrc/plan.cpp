@@ -418,8 +418,8 @@ struct Builder {
       off = align_up(off + 2 * L.n_chunks);
       L.blk_tab = off;
       off = align_up(off + int64_t(L.n_blk) * BLK_WORDS);
-      L.blk_order = off;
-      off = align_up(off + L.n_blk);
+      L.blk_launch = off;
+      off = align_up(off + int64_t(L.n_blk) * LCH_WORDS);
     }
     p.off_replay_row = off;
     off = align_up(off + p.R);
@@ -510,7 +510,24 @@ struct Builder {
       std::stable_sort(order.begin(), order.end(), [bt](int32_t x, int32_t y) {
         return bt[x * BLK_WORDS + BLK_NC] > bt[y * BLK_WORDS + BLK_NC];
       });
-      std::copy(order.begin(), order.end(), b + L.blk_order);
+      for (int32_t j = 0; j < L.n_blk; ++j) {
+        const int32_t* bk = bt + order[j] * BLK_WORDS;
+        const int32_t* e = b + L.seq_tab + int64_t(bk[BLK_SEQ]) * SEQ_WORDS;
+        int32_t* ln = b + L.blk_launch + int64_t(j) * LCH_WORDS;
+        ln[LCH_BLK] = order[j];
+        ln[LCH_SEQ] = bk[BLK_SEQ];
+        ln[LCH_C0] = bk[BLK_C0];
+        ln[LCH_NC] = bk[BLK_NC];
+        ln[LCH_IDX] = bk[BLK_IDX];
+        ln[LCH_N_BLK] = e[SEQ_N_BLK];
+        ln[LCH_FINAL_LEAF] = e[SEQ_FINAL_LEAF];
+        ln[LCH_INIT_BANK] = e[SEQ_INIT_BANK];
+        ln[LCH_N_TOK] = e[SEQ_N_TOK];
+        ln[LCH_N_REPLAY] = e[SEQ_N_REPLAY];
+        ln[LCH_REPLAY_OFF] = e[SEQ_REPLAY_OFF];
+        ln[LCH_OWN_ROW] = e[SEQ_OWN_ROW];
+        ln[LCH_CHUNK_OFF] = e[SEQ_CHUNK_OFF];
+      }
     }
     for (int64_t j = 0; j < p.R; ++j) b[p.off_replay_row + j] = static_cast<int32_t>(p.replay_row[j]);
     for (size_t j = 0; j < p.req_chunk.size(); ++j) {

@@ -39,11 +39,32 @@ enum BlkField : int {
   BLK_WORDS = 8
 };
 
+// Fields of one entry of a round's launch table: the blocks in the order the
+// block kernels take them (longest first), each entry holding every block
+// and sequence field those kernels read, so that a workgroup finds its work
+// with one load instead of a chain of dependent ones.
+enum LaunchField : int {
+  LCH_BLK = 0,         // block id (index into the block table)
+  LCH_SEQ = 1,         // sequence (local index within the round)
+  LCH_C0 = 2,          // first chunk of the block (within the sequence)
+  LCH_NC = 3,          // chunks in the block
+  LCH_IDX = 4,         // block index within the sequence
+  LCH_N_BLK = 5,       // blocks of the sequence
+  LCH_FINAL_LEAF = 6,  // leaf index receiving the sequence's final state
+  LCH_INIT_BANK = 7,   // bank entry of the sequence's initial state, or -1
+  LCH_N_TOK = 8,       // replay + own rows of the sequence
+  LCH_N_REPLAY = 9,    // replay rows of the sequence
+  LCH_REPLAY_OFF = 10, // global replay index of its first replay row
+  LCH_OWN_ROW = 11,    // physical row of its first own row
+  LCH_CHUNK_OFF = 12,  // its first chunk within the round
+  LCH_WORDS = 16
+};
+
 struct RoundLayout {
   int32_t n_seq = 0, seq_begin = 0, max_seq_chunks = 0;
   int32_t n_blk = 0, block_chunks = 0, max_seq_blocks = 0;
   int64_t blk_tab = 0;    // int32 offset of the [n_blk][BLK_WORDS] block table
-  int64_t blk_order = 0;  // int32 offset of [n_blk] block ids, longest block first
+  int64_t blk_launch = 0; // int32 offset of the [n_blk][LCH_WORDS] launch table
   int64_t n_chunks = 0, n_rows = 0, n_own = 0, n_replay = 0, own_row_begin = 0;
   int64_t seq_tab = 0;    // int32 offset of the sequence table
   int64_t init_idx = 0;   // int32 offset of the [n_seq] init bank indices
