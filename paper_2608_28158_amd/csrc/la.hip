@@ -209,6 +209,27 @@ __device__ inline void fetch(Vec16* dst, const T* __restrict__ src, const ChunkS
   }
 }
 
+// Resolves chunk c into cs and requests two of its tiles, with the fast and
+// the slow case each in one branch.  A load of the slow case's row lookups
+// then never reaches the fast case's code, whose address arithmetic would
+// otherwise wait for every outstanding memory operation (the output stores
+// included) before reusing such a load's destination register.
+template <typename T, int D, int NTH = Cfg<T, D>::NTHR>
+__device__ inline void resolve_fetch2(ChunkSrc<T, D, NTH>& cs, const SeqInfo& sq, int c,
+                                      const int32_t* replay_row, const float* g, int H, int h,
+                                      int t, int mrow, Vec16* da, const T* __restrict__ sa,
+                                      int ka, Vec16* db, const T* __restrict__ sb, int kb) {
+  if (chunk_rows(sq, c).fast) {
+    cs.resolve(sq, c, replay_row, g, H, h, t, mrow);
+    fetch<T, D, NTH>(da, sa, cs, H, h, t, ka);
+    fetch<T, D, NTH>(db, sb, cs, H, h, t, kb);
+  } else {
+    cs.resolve(sq, c, replay_row, g, H, h, t, mrow);
+    fetch<T, D, NTH>(da, sa, cs, H, h, t, ka);
+    fetch<T, D, NTH>(db, sb, cs, H, h, t, kb);
+  }
+}
+
 // The publishing wave (lane t = row t): publishes the row table and G of the
 // chunk whose sources are in cs; returns G_t and G_last.
 template <typename T, int D, int NTH>
@@ -353,10 +374,9 @@ __device__ inline float state_dot_via_lds(const f32x4* S, float* stg, const floa
 // exponential per element of the difference of pre-scaled prefix sums (the
 // factor f folded in as log2|f| on the row side); above the diagonal of a
 // diagonal tile the exponent is -inf, so the weight is exactly zero.
-template <bool DIAG, bool NEG, typename T, int D, bool PT>
+template <bool DIAG, bool NEG, typename T, int D, bool PT, typename TA>
 __device__ __forceinline__ void score_epilogue(T* P, const f32x4 (&c)[2][2], const float* G, float lf,
                                                int rb, int cb, int lane) {
-  using TA = Tile<T, CB>;
   constexpr float L2E = 1.4426950408889634f;
   f32x4 mb;  // exponent bias of a diagonal tile at the lane's rows 4g + r, column lane % 16
 #pragma unroll
@@ -394,7 +414,8 @@ __device__ __forceinline__ void score_epilogue(T* P, const f32x4 (&c)[2][2], con
   }
 }
 
-template <typename T, int D, bool PT = false, typename LL = Tile<T, D>, typename LR = Tile<T, D>>
+template <typename T, int D, bool PT = false, typename LL = Tile<T, D>, typename LR = Tile<T, D>,
+          typename LP = Tile<T, CB>>
 __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, const float* G, float f,
                                             int w, int lane) {
   using F = Frag<T>;
@@ -420,11 +441,11 @@ __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, cons
   // f = 1 folds away; otherwise log2|f| joins the row exponents
   const float lf = f == 1.f ? 0.f : __builtin_amdgcn_logf(__builtin_fabsf(f));
   if (f < 0.f) {
-    if (diag) score_epilogue<true, true, T, D, PT>(P, c, G, lf, rb, cb, lane);
-    else score_epilogue<false, true, T, D, PT>(P, c, G, lf, rb, cb, lane);
+    if (diag) score_epilogue<true, true, T, D, PT, LP>(P, c, G, lf, rb, cb, lane);
+    else score_epilogue<false, true, T, D, PT, LP>(P, c, G, lf, rb, cb, lane);
   } else {
-    if (diag) score_epilogue<true, false, T, D, PT>(P, c, G, lf, rb, cb, lane);
-    else score_epilogue<false, false, T, D, PT>(P, c, G, lf, rb, cb, lane);
+    if (diag) score_epilogue<true, false, T, D, PT, LP>(P, c, G, lf, rb, cb, lane);
+    else score_epilogue<false, false, T, D, PT, LP>(P, c, G, lf, rb, cb, lane);
   }
 }
 
@@ -983,10 +1004,14 @@ struct BrSmem {
   using C = Cfg<T, D>;
   static constexpr bool SH = sizeof(T) == 2;  // one adjoint, shared through LDS
   static constexpr int NP = SH ? 2 : 1;
+  // score tiles: rows padded by 8 bytes in bf16 (fragment reads stay
+  // conflict-free, and the workgroup's LDS fits 160 KiB)
+  using TP = Tile<T, CB, false, SH ? 8 : 16>;
   BrTiles<T, D> tl;
-  T P[NP][Tile<T, CB>::SIZE];      // A = Q K^T masked; dA = scale (dO V^T) masked
+  T P[NP][TP::SIZE];               // A = Q K^T masked; dA = scale (dO V^T) masked
   ChunkMeta meta[2];               // x = exp(G_last - G), y = exp(G) * scale
   float rk[C::NW][CB];             // partial k.dk of each row, per wave
+  float rqb[2][CB];                // q.dq of the rows of a chunk (buffer as meta)
 };
 
 // Side 1's B operands of V dS^T from the transposed adjoint in LDS: the same
@@ -1078,7 +1103,7 @@ __device__ __forceinline__ void bwd_revorder_rows(
     }
     regb_rows_packed<T, LK, C::NT, C::CPW, true, true>(acc, side ? V : K, jt * 16, ps, lane);
     const int k0 = (jt * 16 / Frag<T>::KSTEP) * Frag<T>::KSTEP;
-    tile_cols<T, typename C::TA, false, LQ, C::CPW, true, true>(
+    tile_cols<T, typename BrSmem<T, D>::TP, false, LQ, C::CPW, true, true>(
         ad, PT, jt * 16, side ? Q : dOt, col0, k0, CB, lane);
     float e = xr[0];
 #pragma unroll
@@ -1221,23 +1246,25 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
     fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
   }
-  // Side 1, wave 3 (lane = row of the chunk) loads q.dq one chunk ahead and
-  // takes the local suffix sums of q.dq - k.dk of each chunk during the next
-  // chunk's score phase, in which it computes no score block.
+  // Side 1, wave 3 (lane = row of the chunk) takes the local suffix sums of
+  // q.dq - k.dk of each chunk during the next chunk's score phase, in which
+  // it computes no score block.  It loads q.dq one chunk ahead and keeps it
+  // in LDS (rqb, buffered as the chunk metadata): a loaded value carried in
+  // registers from one chunk to the next would make every wave wait, at the
+  // loop's back edge, for the tile loads issued after it.
   const bool sw = side == 1 && w == 3;
   const float* rq_h = rq + (static_cast<int64_t>(sq.chunk_off) * CB + lane) * H + h;
-  float rq_next = sw ? rq_h[static_cast<int64_t>(c_last) * CB * H] : 0.f;
-  float rq_prev = 0.f;  // chunk cp, the one after the current chunk
-  int rowk_prev = 0;
+  if (sw) sm.rqb[0][lane] = rq_h[static_cast<int64_t>(c_last) * CB * H];
+  int rowk_prev = 0;    // row table entry of chunk cp, the one after the current chunk
   float carry = 0.f;    // sum of (q.dq - k.dk) over the later chunks of the block
-  const auto suffix = [&](int cp) {
+  const auto suffix = [&](int cp, int buf) {
     const int kind = rowk_prev & 3;
     float x = 0.f;
     if (kind != ROW_PAD) {
       float rks = 0.f;
 #pragma unroll
       for (int i = 0; i < C::NW; ++i) rks += sm.rk[i][lane];
-      x = rq_prev - rks;
+      x = sm.rqb[buf][lane] - rks;
     }
     x = wave_suffix_sum(x, lane);
     const float val = x + carry;
@@ -1251,8 +1278,6 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     const int bf = (c_last - c) & 1, nb = bf ^ 1;
     const bool more = c > c0;
     const ChunkRows cur = cur_next;
-    const float rq_cur = rq_next;
-    if (sw && more) rq_next = rq_h[static_cast<int64_t>(c - 1) * CB * H];
     const float GL = sm.meta[bf].G[CB - 1];
     // side 0: A = (Q K^T) * M ; side 1: dA = scale (dO V^T) * M,
     // M = exp(G_i - G_j) [j <= i], in three 32 x 32 blocks per half
@@ -1262,16 +1287,21 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
         if constexpr (sizeof(T) == 2) adj_load<D, C::NT, C::CPW>(ps, sm.tl.dt, w, lane);
       }
       if (w < 3) {
-        if (side) score_block<T, D, true, LQ, LK>(sm.P[1], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
-        else score_block<T, D, true, LQ, LK>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
-      } else if (sw && c < c_last) {
-        suffix(c + 1);
+        if (side) score_block<T, D, true, LQ, LK, typename BrSmem<T, D>::TP>(sm.P[1], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
+        else score_block<T, D, true, LQ, LK, typename BrSmem<T, D>::TP>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
+      } else if (sw) {
+        // the suffix of the chunk after, then the chunk before's q.dq into
+        // the buffer it has read (loaded here, so that no other path of the
+        // loop sees the load outstanding)
+        const float rq_ld = more ? rq_h[static_cast<int64_t>(c - 1) * CB * H] : 0.f;
+        if (c < c_last) suffix(c + 1, nb);
+        if (more) sm.rqb[nb][lane] = rq_ld;
       } else if (pw && more) {
         publish(cs, nb);
       }
     } else {
       if (pw && more) publish(cs, nb);
-      if (!side && w < 3) score_block<T, D, true, LQ, LK>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
+      if (!side && w < 3) score_block<T, D, true, LQ, LK, typename BrSmem<T, D>::TP>(sm.P[0], sm.tl.at(bf, TQ), sm.tl.at(bf, TK), sm.meta[bf].G, 1.f, w, lane);
     }
     // next chunk: Q, K into the other buffer; V, dO requested
     if (more) {
@@ -1290,8 +1320,12 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
     } else {
       if (!side) bwd_revorder_rows<T, D, 0>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
       __syncthreads();
-      if (side && w < 3) score_block<T, D, true, LQ, LK>(sm.P[0], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
-      else if (sw && c < c_last) suffix(c + 1);
+      if (side && w < 3) score_block<T, D, true, LQ, LK, typename BrSmem<T, D>::TP>(sm.P[0], sm.tl.at(bf, TDO), sm.tl.at(bf, TV), sm.meta[bf].G, scale, w, lane);
+      else if (sw) {
+        const float rq_ld = more ? rq_h[static_cast<int64_t>(c - 1) * CB * H] : 0.f;
+        if (c < c_last) suffix(c + 1, nb);
+        if (more) sm.rqb[nb][lane] = rq_ld;
+      }
       __syncthreads();
       if (side) bwd_revorder_rows<T, D, 1>(sm, bf, dS, ps, cur, sq, c, more, H, h, scale, GL, w, lane, dk, dv, rep_grad);
     }
@@ -1301,20 +1335,15 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       put<T, D, NTH, LK>(sm.tl.at(nb, TV), pa, nullptr, tid);
       put<T, D, NTH, LQ>(sm.tl.at(nb, TDO), pb, nullptr, tid);
       cur_next = cs.cr;
-      if (c - 1 > c0) {
-        cs.resolve(sq, c - 2, replay_row, g, H, h, tid, mrow);
-        fetch<T, D, NTH>(pa, q, cs, H, h, tid, ROW_OWN);
-        fetch<T, D, NTH>(pb, k, cs, H, h, tid, ROW_REPLAY);
-      }
+      if (c - 1 > c0)
+        resolve_fetch2<T, D, NTH>(cs, sq, c - 2, replay_row, g, H, h, tid, mrow, pa, q, ROW_OWN, pb, k,
+                                  ROW_REPLAY);
     }
-    if (sw) {
-      rowk_prev = sm.meta[bf].rowk[lane];
-      rq_prev = rq_cur;
-    }
+    if (sw) rowk_prev = sm.meta[bf].rowk[lane];
     __syncthreads();
   }
   if (sw) {
-    suffix(c0);
+    suffix(c0, (c_last - c0) & 1);
     if (lane == 0) Rb[static_cast<int64_t>(b) * H + h] = carry;
   }
   // side 0 holds dS at the start of the block: the first block's is dS0

@@ -119,10 +119,10 @@ template <> struct BufVec4<float> {
 // doubles the fragment reads).  16-byte units stay contiguous.  Fragment
 // reads with origins (r0, c0) that are multiples of 16 address
 // base(r0, c0) + lane(ri, ci): an affine part plus a lane constant.
-template <typename T, int COLS, bool XS = false>
+template <typename T, int COLS, bool XS = false, int PADB = (XS ? 32 : 16)>
 struct Tile {
   static_assert(!XS || (sizeof(T) == 2 && COLS == 128), "swizzled rows are bf16 x 128");
-  static constexpr int LD = COLS + (XS ? 32 : 16) / static_cast<int>(sizeof(T));  // row stride (elements)
+  static constexpr int LD = COLS + PADB / static_cast<int>(sizeof(T));  // row stride (elements)
   static constexpr int SIZE = CB * LD;
   __device__ static inline int swz(int r) { return XS ? ((r >> 3) & 1) << 3 : 0; }
   __device__ static inline int at(int r, int c) { return r * LD + (c ^ swz(r)); }
