@@ -168,6 +168,23 @@ typedef struct harts_round_info {
   int64_t init_idx_off;  /* byte offset in the blob of the round's int32
                             [n_seq] initial-state bank indices (the idx
                             argument of harts_state_gather)                 */
+  /* Byte offsets in the blob of the round's tables (int32 words), for
+   * inspection; the device calls find them themselves.
+   *   sequence table [n_seq][16]: chunk offset in the round, packed rows,
+   *     replay rows, first replay index, physical row of the first own row,
+   *     initial-state bank entry, final leaf, first request, requests,
+   *     chunks, first block, blocks, 4 unused;
+   *   block table [n_blk][8]: sequence (in the round), first chunk,
+   *     chunks, index in the sequence, bank entry requested at its end or
+   *     -1, 3 unused;
+   *   launch table [n_blk][16]: the blocks in launch order (most chunks
+   *     first, ties by block id): block id, sequence, first chunk, chunks,
+   *     index in the sequence, blocks of the sequence, final leaf,
+   *     initial-state bank entry, packed rows, replay rows, first replay
+   *     index, physical row of the first own row, chunk offset, 3 unused. */
+  int64_t seq_tab_off;
+  int64_t blk_tab_off;
+  int64_t launch_off;
 } harts_round_info;
 
 int harts_plan_round_info(const harts_plan_t* plan, int32_t round,

@@ -77,7 +77,8 @@ class RoundInfo(C.Structure):
     _fields_ = [("n_seq", C.c_int32), ("seq_begin", C.c_int32), ("n_blk", C.c_int32),
                 ("block_chunks", C.c_int32)] + [
         (n, C.c_int64) for n in ("n_chunks", "n_rows", "n_own", "n_replay",
-                                 "own_row_begin", "init_idx_off")]
+                                 "own_row_begin", "init_idx_off", "seq_tab_off",
+                                 "blk_tab_off", "launch_off")]
 
 
 class KernelTime(C.Structure):

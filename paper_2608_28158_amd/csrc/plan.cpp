@@ -658,6 +658,9 @@ extern "C" int harts_plan_round_info(const harts_plan_t* p, int32_t round, harts
   info->n_replay = L.n_replay;
   info->own_row_begin = L.own_row_begin;
   info->init_idx_off = L.init_idx * static_cast<int64_t>(sizeof(int32_t));
+  info->seq_tab_off = L.seq_tab * static_cast<int64_t>(sizeof(int32_t));
+  info->blk_tab_off = L.blk_tab * static_cast<int64_t>(sizeof(int32_t));
+  info->launch_off = L.blk_launch * static_cast<int64_t>(sizeof(int32_t));
   return HARTS_OK;
 }
 

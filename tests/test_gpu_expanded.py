@@ -1,0 +1,111 @@
+"""GPU metamorphic test, independent of the oracle: the tree-packed plan
+against trajectory-wise execution (every root-to-leaf path its own
+zero-history sequence, the baseline the paper compares with), both through
+the C ABI on the same seeded inputs.
+
+Compact execution reaches the trajectory-wise result at every shared token
+(Sec. 2.2: the same chunk partition from each trajectory's start), so:
+  - the compact output of row c equals the trajectory-wise output of c in
+    every trajectory through c, and the final states agree per leaf;
+  - with the upstream gradient of row c given to one trajectory through c
+    (the lowest leaf id) and dS_final per leaf, the compact dq, dk, dv, dg
+    of c equal the sums over the trajectories through c, and the tree
+    initial-state gradient the sum over the tree's trajectories.
+Tolerances as for the oracle parity (max relative error per tensor).
+"""
+import numpy as np
+import pytest
+import torch
+
+from tests.harness import TOL, max_rel
+from tests.test_gpu_parity import run_gpu
+from workloads import draw_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2608_28158_amd import _lib
+    _lib.lib()
+
+
+def trajectories(parent, seg_len):
+    parent = np.asarray(parent)
+    seg_len = np.asarray(seg_len, np.int64)
+    n = len(parent)
+    kids = [[] for _ in range(n)]
+    for v, p in enumerate(parent.tolist()):
+        if p >= 0:
+            kids[p].append(v)
+    row0 = np.concatenate([[0], np.cumsum(seg_len)[:-1]])
+    root = np.empty(n, np.int64)
+    roots = [v for v in range(n) if parent[v] < 0]
+    for v in range(n):
+        u = v
+        while parent[u] >= 0:
+            u = parent[u]
+        root[v] = roots.index(u)
+    trajs, tree_of = [], []
+    for leaf in [v for v in range(n) if not kids[v]]:
+        path, u = [], leaf
+        while u >= 0:
+            path.append(u)
+            u = parent[u]
+        trajs.append(np.concatenate([row0[w] + np.arange(seg_len[w]) for w in reversed(path)]))
+        tree_of.append(root[leaf])
+    return trajs, np.array(tree_of)
+
+
+def check(parent, seg_len, H, d, dtype, seed, label):
+    print(f"[gpu] expanded-vs-packed {label} n_seg={len(parent)} C={int(np.sum(seg_len))} "
+          f"H={H} d={d} {dtype}", flush=True)
+    rng = np.random.default_rng(seed)
+    trajs, tree_of = trajectories(parent, seg_len)
+    n_trees = int(np.sum(np.asarray(parent) < 0))
+    C = int(np.sum(seg_len))
+    x = draw_inputs(C, len(trajs), H, d, d, rng, dtype, n_trees=n_trees, s0_scale=0.5)
+    scale = d ** -0.5
+    packed, _ = run_gpu(parent, seg_len, x, H, d, dtype, scale)
+    # trajectory-wise inputs: row c's upstream gradient on its first trajectory only
+    rows = np.concatenate(trajs)
+    first = np.full(C, -1, np.int64)
+    for t, r in enumerate(trajs):
+        new = first[r] < 0
+        first[r[new]] = t
+    owner = np.concatenate([np.full(len(r), t) for t, r in enumerate(trajs)])
+    xe = {n: x[n][rows] for n in ("q", "k", "v", "g")}
+    xe["dO"] = np.where((first[rows] == owner)[:, None, None], x["dO"][rows], 0).astype(np.float32)
+    xe["dS_final"] = x["dS_final"]
+    xe["S0"] = x["S0"][tree_of]
+    lens = np.array([len(r) for r in trajs], np.int64)
+    expd, _ = run_gpu(np.full(len(trajs), -1, np.int32), lens, xe, H, d, dtype, scale)
+    tol = TOL[dtype]
+    errs = {"o": max_rel(packed["o"][rows], expd["o"]),
+            "S_final": max_rel(packed["S_final"], expd["S_final"])}
+    for name in ("dq", "dk", "dv", "dg"):
+        acc = np.zeros_like(packed[name], dtype=np.float64)
+        np.add.at(acc, rows, expd[name])
+        errs[name] = max_rel(packed[name], acc)
+    dS0 = np.zeros_like(packed["dS0_tree"], dtype=np.float64)
+    np.add.at(dS0, tree_of, expd["dS0_tree"])
+    errs["dS0_tree"] = max_rel(packed["dS0_tree"], dS0)
+    print(f"[gpu] expanded-vs-packed {label}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()),
+          flush=True)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, f"{label}: above {tol}: {bad}"
+
+
+def test_figure1_fp32():
+    from workloads.trees import figure1_forest
+    f = figure1_forest()
+    check(f.parent, f.seg_len, 2, 64, "f32", 3, "figure 1")
+
+
+def test_random_forest_bf16():
+    rng = np.random.default_rng(11)
+    parent = np.array([-1, 0, 0, 1, 1, 2, -1, 6, 6, 8], np.int32)
+    seg_len = rng.integers(40, 1500, size=len(parent)).astype(np.int64)
+    check(parent, seg_len, 4, 128, "bf16", 12, "two trees, unaligned forks")
