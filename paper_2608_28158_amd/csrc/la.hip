@@ -19,21 +19,20 @@
 // fragments in registers, so LDS holds only unscaled chunk tiles.  Blocks of
 // one sequence are chained by element-parallel scans over block summaries:
 //
-//   forward   k_blocksum      side 0: state of each block started from zero
-//                             and its total log-decay Gamma_b;
+//   forward   k_blocksum      state of each block started from zero and
+//                             its total log-decay Gamma_b;
 //             k_fwd_blockscan S_end[b] = exp(Gamma_b) S_end[b-1] + dS_b,
 //                             which also yields every requested boundary
 //                             state and every final state;
 //             k_fwd_block     outputs of the own rows of each block.
-//   backward  k_blocksum      side 1: the block's local adjoint
-//                             U_b = sum_t exp(G_t^blk) scale q_t dO_t^T
-//                             (with side 0 as well when recomputing);
+//   backward  (k_blocksum and k_fwd_blockscan first when recomputing)
+//             k_bwd_fwdorder  dq and q.dq per row (needs S_c, so it walks
+//                             chunks forward), and the block's local adjoint
+//                             U_b = sum_t exp(G_t^blk) scale q_t dO_t^T;
 //             k_bwd_blockscan dS_end[b] by the reverse recurrence
 //                             dS_start[b] = exp(Gamma_b) dS_end[b] + U_b,
 //                             bank gradients injected at requested block
 //                             ends, dS0 per sequence, boundary terms;
-//             k_bwd_fwdorder  dq and q.dq per row (needs S_c, so it walks
-//                             chunks forward);
 //             k_bwd_revorder  dv (side 0) and dk, k.dk, local suffix sums of
 //                             dg (side 1); both need dS_{c+1} and walk
 //                             chunks backward;
@@ -281,10 +280,11 @@ __device__ inline void state_to_lds(float* stg, const float* __restrict__ src, i
 }
 // The whole staged load, in NPASS passes of D / NPASS stored rows each (for
 // LDS that holds only part of a state; src null: a zero state); every thread
-// of the workgroup calls it (it synchronises the workgroup).
+// of the workgroup calls it (it synchronises the workgroup), and the waves
+// with take set receive their strips.
 template <int D, int CPW, int NTH, int NPASS>
 __device__ inline void state_via_lds(f32x4* S, float* stg, const float* __restrict__ src,
-                                     bool transpose, int w, int lane, int tid) {
+                                     bool transpose, int w, int lane, int tid, bool take = true) {
   constexpr int NT = D / 16, P = D + 4, RP = D / NPASS, N4 = RP * D / 4;
   static_assert(N4 % NTH == 0, "state split");
 #pragma unroll
@@ -298,16 +298,18 @@ __device__ inline void state_via_lds(f32x4* S, float* stg, const float* __restri
               : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     __syncthreads();
+    if (take) {
 #pragma unroll
-    for (int j = 0; j < CPW; ++j)
+      for (int j = 0; j < CPW; ++j)
 #pragma unroll
-      for (int i = 0; i < NT; ++i)
+        for (int i = 0; i < NT; ++i)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
-          const int row = transpose ? b : a, col = transpose ? a : b;
-          if (row / RP == pass) S[j * NT + i][r] = stg[(row - pass * RP) * P + col];
-        }
+          for (int r = 0; r < 4; ++r) {
+            const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
+            const int row = transpose ? b : a, col = transpose ? a : b;
+            if (row / RP == pass) S[j * NT + i][r] = stg[(row - pass * RP) * P + col];
+          }
+    }
     __syncthreads();
   }
 }
@@ -328,12 +330,13 @@ __device__ inline void state_from_lds(f32x4* S, const float* stg, bool transpose
 
 // <X, S>_F of a state S held in accumulators (as state_from_lds lays it out,
 // transposed or not) with a row-major D x D state X in global memory, summed
-// over the workgroup of NTH threads and returned to every thread.  X is staged
-// through stg (D x (D + 4) floats); red holds NTH / 64 floats.  Every thread
-// calls it (it synchronises the workgroup).
+// over the waves with take set (of the workgroup of NTH threads) and returned
+// to every thread.  X is staged through stg (D x (D + 4) floats); red holds
+// NTH / 64 floats.  Every thread calls it (it synchronises the workgroup).
 template <int D, int CPW, int NTH>
 __device__ inline float state_dot_via_lds(const f32x4* S, float* stg, const float* __restrict__ X,
-                                          bool transpose, int w, int lane, int tid, float* red) {
+                                          bool transpose, int w, int lane, int tid, float* red,
+                                          bool take = true) {
   constexpr int NT = D / 16, P = StateStage<D>::PITCH, N4 = D * D / 4;
   static_assert(N4 % NTH == 0, "state split");
 #pragma unroll
@@ -344,15 +347,17 @@ __device__ inline float state_dot_via_lds(const f32x4* S, float* stg, const floa
   }
   __syncthreads();
   float x = 0.f;
+  if (take) {
 #pragma unroll
-  for (int j = 0; j < CPW; ++j)
+    for (int j = 0; j < CPW; ++j)
 #pragma unroll
-    for (int i = 0; i < NT; ++i)
+      for (int i = 0; i < NT; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
-        x += S[j * NT + i][r] * (transpose ? stg[b * P + a] : stg[a * P + b]);
-      }
+        for (int r = 0; r < 4; ++r) {
+          const int a = i * 16 + acc_row(lane, r), b = (CPW * w + j) * 16 + acc_col(lane);
+          x += S[j * NT + i][r] * (transpose ? stg[b * P + a] : stg[a * P + b]);
+        }
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
   if (lane == 0) red[tid >> 6] = x;
@@ -454,39 +459,32 @@ __device__ __forceinline__ void score_block(T* P, const T* Lt, const T* Rt, cons
 // worth of registers).
 
 // ---------------------------------------------------------------------------
-// block summaries: one pass over a block's chunks, state started from zero
+// forward block summaries: one pass over a block's chunks, state started from
+// zero: dS_b = sum over the block of the chunk recurrence
+// S <- exp(G_last) S + K^T diag(exp(G_last - G)) V, and Gamma_b = the total
+// log-decay of the block.  (The adjoint summaries U_b are formed by the
+// forward-order backward kernel, which holds the chunk's q and dO anyway.)
 // ---------------------------------------------------------------------------
-// side 0 (forward):  dS_b = sum over the block of the chunk recurrence
-//                    S <- exp(G_last) S + K^T diag(exp(G_last - G)) V, and
-//                    Gamma_b = total log-decay of the block;
-// side 1 (adjoint):  U_b = sum_t exp(G_t^blk) scale q_t dO_t^T, G_t^blk the
-//                    inclusive log-decay from the block start to row t.
-// blockIdx.z selects the side (side0 + z).
 template <typename T, int D>
 __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksum(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ blk_launch,
-    const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
-    const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dO,
-    const float* __restrict__ g, float* __restrict__ dSb, float* __restrict__ U,
-    float* __restrict__ gam, int side0, int skip1) {
+    const int32_t* __restrict__ replay_row, int H, const T* __restrict__ k,
+    const T* __restrict__ v, const float* __restrict__ g, float* __restrict__ dSb,
+    float* __restrict__ gam, int skip1) {
   using C = Cfg<T, D>;
   __shared__ T Xs[Tile<T, D>::SIZE];
   __shared__ T Ys[Tile<T, D>::SIZE];
   __shared__ ChunkMeta meta;
-  const int side = side0 + static_cast<int>(blockIdx.z);
   const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
   const int b = bl.b, h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
-  // The block kernels end a sequence's forward chain and start its adjoint
-  // chain themselves: the first block's adjoint summary is never needed, nor
-  // the last block's forward summary, of which only Gamma_b is (for the
-  // adjoint chain).
-  if (skip1 && side && bl.idx == 0) return;
   const SeqInfo sq = bl.sq;
   const int c0 = bl.c0, c_end = c0 + bl.nc;
   const int64_t bi = static_cast<int64_t>(b) * H + h;
-  if (skip1 && !side && bl.idx == bl.n_blk - 1) {
+  // The block kernels end a sequence's forward chain themselves: of the last
+  // block only Gamma_b is needed (for the adjoint chain).
+  if (skip1 && bl.idx == bl.n_blk - 1) {
     if (w != 0) return;
     // Gamma_b alone, summed chunk by chunk as below; wave 0, lane = row
     ChunkSrc<T, D> cs;
@@ -498,23 +496,20 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
     if (t == 0) gam[bi] = Gs;
     return;
   }
-  const T* X = side ? q : k;
-  const T* Y = side ? dO : v;
-  const int min_kind = side ? ROW_OWN : ROW_REPLAY;
   f32x4 S[C::CPW * C::NT];
 #pragma unroll
   for (int i = 0; i < C::CPW * C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   ChunkSrc<T, D> cs;
   Vec16 px[C::NV], py[C::NV];
   cs.resolve(sq, c0, replay_row, g, H, h, t, t < CB ? t : -1);
-  fetch<T, D>(px, X, cs, H, h, t, min_kind);
-  fetch<T, D>(py, Y, cs, H, h, t, min_kind);
+  fetch<T, D>(px, k, cs, H, h, t, ROW_REPLAY);
+  fetch<T, D>(py, v, cs, H, h, t, ROW_REPLAY);
   float Gs = 0.f;  // log-decay from the block start to the current chunk start
   for (int c = c0; c < c_end; ++c) {
     if (t < CB) {
       float Gt, GLw;
       meta_publish(meta, cs, t, Gt, GLw);
-      meta.x[t] = side ? __expf(Gs + Gt) * scale : __expf(GLw - Gt);
+      meta.x[t] = __expf(GLw - Gt);
     }
     put<T, D>(Xs, px, nullptr, t);
     put<T, D>(Ys, py, nullptr, t);
@@ -522,20 +517,18 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
     const float GL = meta.G[CB - 1];
     if (c + 1 < c_end) {
       cs.resolve(sq, c + 1, replay_row, g, H, h, t, t < CB ? t : -1);
-      fetch<T, D>(px, X, cs, H, h, t, min_kind);
-      fetch<T, D>(py, Y, cs, H, h, t, min_kind);
+      fetch<T, D>(px, k, cs, H, h, t, ROW_REPLAY);
+      fetch<T, D>(py, v, cs, H, h, t, ROW_REPLAY);
     }
-    if (!side) {
-      const float dec = __expf(GL);
+    const float dec = __expf(GL);
 #pragma unroll
-      for (int i = 0; i < C::CPW * C::NT; ++i) S[i] *= dec;
-    }
+    for (int i = 0; i < C::CPW * C::NT; ++i) S[i] *= dec;
     state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, Xs, Ys, C::CPW * w * 16, meta.x, lane);
     Gs += GL;
     __syncthreads();
   }
-  state_store<D, C::CPW>((side ? U : dSb) + bi * D * D, S, w, lane);
-  if (!side && t == 0) gam[bi] = Gs;
+  state_store<D, C::CPW>(dSb + bi * D * D, S, w, lane);
+  if (t == 0) gam[bi] = Gs;
 }
 
 // Where the initial states of a round's sequences are: S0 [n_seq, H, d, d],
@@ -797,139 +790,225 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
 }
 
 // ---------------------------------------------------------------------------
-// backward, forward order: dq and q.dq per row (needs S_c: chunks forward)
+// backward, forward order (needs S_c: chunks forward).  One workgroup of two
+// halves per (block, head), sharing double-buffered chunk tiles in LDS:
+//   waves 0..3 (side 0): dq = scale diag(exp(G)) dO S_c^T + dA K and q.dq
+//                        per row, holding S^T (rows dv, columns dk);
+//   waves 4..7 (side 1): every load and LDS write of the chunk tiles and of
+//                        the row table; the masked score
+//                        dA = scale (dO V^T) exp(G_i - G_j) [j <= i]
+//                        (waves 4..6; wave 7 sums the previous chunk's q.dq);
+//                        and the block's adjoint summary
+//                        U_b = sum_t exp(G_t^blk) scale q_t dO_t^T, with
+//                        G_t^blk the inclusive log-decay from the block start
+//                        to row t, which the adjoint chain over blocks needs
+//                        (never for a sequence's first block).
+// Per chunk c, between two workgroup barriers each: (1) side 0 converts
+// S_c^T once to MFMA operands and advances S^T, side 1 forms dA; (2) side 0
+// forms the dq rows from the converted S_c^T, side 1 advances U_b, writes
+// chunk c + 1 (loaded during chunk c - 1) to the other buffer and requests
+// chunk c + 2.
 // ---------------------------------------------------------------------------
+template <typename T, int D>
+struct BfMeta {
+  ChunkMeta m;              // x = exp(G_last - G), y = exp(G) * scale
+  alignas(16) float u[CB];  // exp(G_t^blk) * scale
+};
 template <typename T, int D>
 struct BfSmem {
   using C = Cfg<T, D>;
-  T dO[Tile<T, D>::SIZE];
-  T V[Tile<T, D>::SIZE];
-  T K[Tile<T, D>::SIZE];
-  T Q[Tile<T, D>::SIZE];     // own rows
+  T dO[2][Tile<T, D>::SIZE];
+  T V[2][Tile<T, D>::SIZE];
+  T K[2][Tile<T, D>::SIZE];
+  T Q[2][Tile<T, D>::SIZE];  // own rows
   T dA[Tile<T, CB>::SIZE];   // scale * (dO V^T) masked
-  ChunkMeta meta;  // x = exp(G_last - G), y = exp(G) * scale
+  BfMeta<T, D> meta[2];
   float rq[C::NW][CB];
+  float red[2 * C::NW];
 };
 
 template <typename T, int D>
-__global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwdorder(
+__global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd_fwdorder(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab,
     const int32_t* __restrict__ blk_launch,
     const int32_t* __restrict__ replay_row, int H, float scale, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const T* __restrict__ dO, const InitSrc is, const float* __restrict__ S_end,
     T* __restrict__ dq, float* __restrict__ rq_out, const float* __restrict__ dS_final,
-    float* __restrict__ betap) {
+    float* __restrict__ betap, float* __restrict__ U) {
   using C = Cfg<T, D>;
-  using RB = RegB<T>;
+  constexpr int NTH = 2 * C::NTHR;
   constexpr int NS = C::CPW * C::NT;
+  constexpr int NIT = CB / 16;
   __shared__ BfSmem<T, D> sm;
   const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
   const int b = bl.b, h = blockIdx.x % H, t = threadIdx.x, lane = t & 63;
   const int w = wave_id(t);
-  const int col0 = C::CPW * w * 16;
+  const int side = w >= C::NW;
+  const int ws = w - side * C::NW;       // wave within its half
+  const int t1 = t - side * C::NTHR;     // thread within its half
+  const int col0 = C::CPW * ws * 16;
   const SeqInfo sq = bl.sq;
   const int c0 = bl.c0, c_end = c0 + bl.nc;
   const int64_t DD = static_cast<int64_t>(D) * D;
-  // the first chunk's rows are requested before the start state
+  const bool want_u = bl.idx > 0;
+  // side 1: the first chunk's rows are requested before the start state
   ChunkSrc<T, D> cs;
   Vec16 pq[C::NV], pk[C::NV], pv[C::NV], pd[C::NV];
-  cs.resolve(sq, c0, replay_row, g, H, h, t, t < CB ? t : -1);
-  fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
-  fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
-  f32x4 St[NS];  // S^T : rows (dv), columns (dk) of the wave's strips
+  if (side) {
+    cs.resolve(sq, c0, replay_row, g, H, h, t1, t1 < CB ? t1 : -1);
+    fetch<T, D>(pq, q, cs, H, h, t1, ROW_OWN);
+    fetch<T, D>(pk, k, cs, H, h, t1, ROW_REPLAY);
+    fetch<T, D>(pv, v, cs, H, h, t1, ROW_REPLAY);
+    fetch<T, D>(pd, dO, cs, H, h, t1, ROW_OWN);
+  }
+  f32x4 S[NS];  // side 0: S^T in its column strips; side 1: U_b in its column strips
   // the start state, staged through the (still unused) tiles
   using BfS = BfSmem<T, D>;
   static_assert(D * (D + 4) * 4 <= static_cast<int>(offsetof(BfS, dA)), "state fits the tiles");
-  state_via_lds<D, C::CPW, C::NTHR, 1>(St, reinterpret_cast<float*>(&sm.dO[0]),
-                                       bl.idx == 0 ? init_state(is, bl, H, h, DD)
-                                                   : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
-                                       true, w, lane, t);
-  for (int c = c0; c < c_end; ++c) {
-    if (t < CB) {
+  float* stage = reinterpret_cast<float*>(&sm.dO[0][0]);
+  state_via_lds<D, C::CPW, NTH, 1>(S, stage,
+                                   bl.idx == 0 ? init_state(is, bl, H, h, DD)
+                                               : S_end + (static_cast<int64_t>(b - 1) * H + h) * DD,
+                                   true, ws, lane, t, !side);
+  float Gs = 0.f;  // wave 4, lane = row: log-decay from the block start to the chunk start
+  // side 1 writes a chunk (its row table and tiles) to buffer nb
+  auto put_chunk = [&](int nb) {
+    if (t1 < CB) {
       float Gt, GLw;
-      meta_publish(sm.meta, cs, t, Gt, GLw);
-      sm.meta.x[t] = __expf(GLw - Gt);
-      sm.meta.y[t] = __expf(Gt) * scale;
+      meta_publish(sm.meta[nb].m, cs, t1, Gt, GLw);
+      sm.meta[nb].m.x[t1] = __expf(GLw - Gt);
+      sm.meta[nb].m.y[t1] = __expf(Gt) * scale;
+      sm.meta[nb].u[t1] = __expf(Gs + Gt) * scale;
+      Gs += GLw;
     }
-    const ChunkRows cur = cs.cr;
-    put<T, D>(sm.dO, pd, nullptr, t);
-    put<T, D>(sm.V, pv, nullptr, t);
-    put<T, D>(sm.K, pk, nullptr, t);
-    put<T, D>(sm.Q, pq, nullptr, t);
-    __syncthreads();
-    const float GL = sm.meta.G[CB - 1];
-    // the next chunk's rows, one tile at a time between the phases
-    const bool more = c + 1 < c_end;
-    if (more) {
-      cs.resolve(sq, c + 1, replay_row, g, H, h, t, t < CB ? t : -1);
-      fetch<T, D>(pd, dO, cs, H, h, t, ROW_OWN);
-    }
-    // dA = scale * (dO V^T) * exp(G_i - G_j) [j <= i]; wave w computes row block w
-    if (w < 3) score_block<T, D>(sm.dA, sm.dO, sm.V, sm.meta.G, scale, w, lane);
-    if (more) fetch<T, D>(pv, v, cs, H, h, t, ROW_REPLAY);
-    __syncthreads();
-    // dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial q.dq.
-    // Products with swapped operands: lane (g, i) holds row 16 it + i,
-    // columns col0 + 16 j + 4g .. + 3
-#pragma unroll 1
-    for (int it = 0; it < CB / 16; ++it) {
-      if (it == 1 && more) fetch<T, D>(pk, k, cs, H, h, t, ROW_REPLAY);
-      if (it == 2 && more) fetch<T, D>(pq, q, cs, H, h, t, ROW_OWN);
-      f32x4 acc[C::CPW];
+    put<T, D>(sm.dO[nb], pd, nullptr, t1);
+    put<T, D>(sm.V[nb], pv, nullptr, t1);
+    put<T, D>(sm.K[nb], pk, nullptr, t1);
+    put<T, D>(sm.Q[nb], pq, nullptr, t1);
+  };
+  if (side) {
 #pragma unroll
-      for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      opaque_state<NS>(St);
-      regb_rows<T, typename C::TD, C::NT, C::CPW, true>(acc, sm.dO, it * 16, St, lane);
-      const int m = it * 16 + (lane & 15);
-      {
-        const float e = sm.meta.y[m];
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j) acc[j] *= e;
-      }
-      tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true>(acc, sm.dA, it * 16, sm.K, col0,
-                                                                       0, (it + 1) * 16, lane);
-      const int g4 = 4 * (lane >> 4);
-      float qd = 0.f;
-#pragma unroll
-      for (int j = 0; j < C::CPW; ++j) {
-        const f32x4 qv = Vec4<T>::load(sm.Q + C::TD::at(m, col0 + 16 * j + g4));
-#pragma unroll
-        for (int r = 0; r < 4; ++r) qd += qv[r] * acc[j][r];
-      }
-      qd = group_sum4(qd);
-      if (lane < 16) sm.rq[w][m] = qd;
-      const int rk = cur.fast ? 0 : sm.meta.rowk[m];
-      if (cur.fast || (rk & 3) == ROW_OWN) {
-        const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (rk >> 2);
-        T* dst = dq + (row * H + h) * D + col0 + g4;
-#pragma unroll
-        for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j]);
-      }
-    }
-    // S^T <- exp(G_last) S^T + V^T diag(exp(G_last - G)) K
-    const float dec = __expf(GL);
-#pragma unroll
-    for (int i = 0; i < NS; ++i) St[i] *= dec;
-    state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(St, sm.V, sm.K, col0, sm.meta.x, lane);
-    __syncthreads();
-    if (t < CB) {
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < C::NW; ++i) s += sm.rq[i][t];
-      rq_out[((static_cast<int64_t>(sq.chunk_off) + c) * CB + t) * H + h] = s;
+    for (int i = 0; i < NS; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    put_chunk(0);
+    if (c0 + 1 < c_end) {
+      cs.resolve(sq, c0 + 1, replay_row, g, H, h, t1, t1 < CB ? t1 : -1);
+      fetch<T, D>(pq, q, cs, H, h, t1, ROW_OWN);
+      fetch<T, D>(pk, k, cs, H, h, t1, ROW_REPLAY);
+      fetch<T, D>(pv, v, cs, H, h, t1, ROW_REPLAY);
+      fetch<T, D>(pd, dO, cs, H, h, t1, ROW_OWN);
     }
   }
-  // The last block of a sequence ends with S_final (S^T is held):
+  __syncthreads();
+  // The halves run loops of their own (the branch is uniform per wave), each
+  // with two workgroup barriers per chunk, so that neither half's registers
+  // are held across the other's code.  The lane index is hidden from the
+  // optimiser inside the loops: LDS addresses are formed per chunk instead
+  // of being held across the loop.
+  if (!side) {
+    for (int c = c0; c < c_end; ++c) {
+      const int bf = (c - c0) & 1;
+      const ChunkMeta& mt = sm.meta[bf].m;
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      // (1) S_c^T packed once into MFMA operands for the rows below, then
+      // S^T <- exp(G_last) S^T + V^T diag(exp(G_last - G)) K
+      PackedState<T, C::NT, C::CPW> ps;
+      ps.pack(S);
+      const float dec = __expf(mt.G[CB - 1]);
+#pragma unroll
+      for (int i = 0; i < NS; ++i) S[i] *= dec;
+      state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, sm.V[bf], sm.K[bf], col0, mt.x, ln);
+      __syncthreads();
+      // (2) dq[:, wave columns] = scale diag(exp(G)) dO S_c^T + dA K ; partial
+      // q.dq.  Products with swapped operands: lane (g, i) holds row
+      // 16 it + i, columns col0 + 16 j + 4g .. + 3
+      const ChunkRows cur = chunk_rows(sq, c);
+      const int g4 = 4 * (ln >> 4);
+#pragma unroll 1
+      for (int it = 0; it < NIT; ++it) {
+        f32x4 acc[C::CPW];
+#pragma unroll
+        for (int j = 0; j < C::CPW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        regb_rows_packed<T, typename C::TD, C::NT, C::CPW, true>(acc, sm.dO[bf], it * 16, ps, ln);
+        const int m = it * 16 + (ln & 15);
+        {
+          const float e = mt.y[m];
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j) acc[j] *= e;
+        }
+        tile_cols<T, typename C::TA, false, typename C::TD, C::CPW, true>(acc, sm.dA, it * 16, sm.K[bf],
+                                                                         col0, 0, (it + 1) * 16, ln);
+        float qd = 0.f;
+#pragma unroll
+        for (int j = 0; j < C::CPW; ++j) {
+          const f32x4 qv = Vec4<T>::load(sm.Q[bf] + C::TD::at(m, col0 + 16 * j + g4));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) qd += qv[r] * acc[j][r];
+        }
+        qd = group_sum4(qd);
+        if (ln < 16) sm.rq[ws][m] = qd;
+        const int rk = cur.fast ? 0 : mt.rowk[m];
+        if (cur.fast || (rk & 3) == ROW_OWN) {
+          const int64_t row = cur.fast ? static_cast<int64_t>(cur.row0) + m : (rk >> 2);
+          T* dst = dq + (row * H + h) * D + col0 + g4;
+#pragma unroll
+          for (int j = 0; j < C::CPW; ++j) Vec4<T>::store(dst + 16 * j, acc[j]);
+        }
+      }
+      __syncthreads();
+    }
+  } else {
+    for (int c = c0; c < c_end; ++c) {
+      const int bf = (c - c0) & 1;
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      // (1) the masked score dA (waves 4..6); wave 7: q.dq of the previous
+      // chunk's rows (lane = row)
+      if (ws < 3) {
+        score_block<T, D>(sm.dA, sm.dO[bf], sm.V[bf], sm.meta[bf].m.G, scale, ws, ln);
+      } else if (c > c0) {
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < C::NW; ++i) s += sm.rq[i][ln];
+        rq_out[((static_cast<int64_t>(sq.chunk_off) + c - 1) * CB + ln) * H + h] = s;
+      }
+      __syncthreads();
+      // (2) U_b += Q^T diag(exp(G^blk) scale) dO; then the next chunk to the
+      // other buffer, and the one after it requested
+      if (want_u)
+        state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, sm.Q[bf], sm.dO[bf], col0,
+                                                                       sm.meta[bf].u, ln);
+      if (c + 1 < c_end) {
+        put_chunk(bf ^ 1);
+        if (c + 2 < c_end) {
+          int tt = t1;
+          asm volatile("" : "+v"(tt));
+          cs.resolve(sq, c + 2, replay_row, g, H, h, tt, tt < CB ? tt : -1);
+          fetch<T, D>(pq, q, cs, H, h, tt, ROW_OWN);
+          fetch<T, D>(pk, k, cs, H, h, tt, ROW_REPLAY);
+          fetch<T, D>(pv, v, cs, H, h, tt, ROW_REPLAY);
+          fetch<T, D>(pd, dO, cs, H, h, tt, ROW_OWN);
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (w == 2 * C::NW - 1) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < C::NW; ++i) s += sm.rq[i][lane];
+    rq_out[((static_cast<int64_t>(sq.chunk_off) + c_end - 1) * CB + lane) * H + h] = s;
+  }
+  if (side && want_u) state_store<D, C::CPW>(U + (static_cast<int64_t>(b) * H + h) * DD, S, ws, lane);
+  // The last block of a sequence ends with S_final (S^T is held by side 0):
   // <dS_final, S_final> is its boundary term of dg, the first of the block's
   // NSW partial sums.
   if (bl.idx == bl.n_blk - 1) {
     constexpr int NSW = D * D / 4 / SCAN_THR;
-    const float dot = state_dot_via_lds<D, C::CPW, C::NTHR>(
-        St, reinterpret_cast<float*>(&sm.dO[0]),
-        dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD, true, w, lane, t, sm.rq[0]);
+    const float dot = state_dot_via_lds<D, C::CPW, NTH>(
+        S, stage, dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD, true, ws, lane, t,
+        sm.red, !side);
     if (t < NSW) betap[(static_cast<int64_t>(b) * H + h) * NSW + t] = t == 0 ? dot : 0.f;
   }
 }
@@ -1561,18 +1640,17 @@ Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
   return Blob{b + L.seq_tab, b + L.blk_tab, b + L.blk_launch, b + p->off_replay_row, b + L.init_idx};
 }
 
-// Block summaries of the given sides (0: forward dS_b and Gamma_b, 1: adjoint U_b);
-// skip1: none for sequences of one block.
+// Forward block summaries dS_b and Gamma_b; skip1: none for sequences of one
+// block.
 template <typename T, int D>
 int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, float scale,
-                    const void* q, const void* k, const void* v, const void* dO, const float* g,
-                    float* dSb, float* U, float* gam, int side0, int n_sides, int skip1, hipStream_t s) {
+                    const void* q, const void* k, const void* v, const float* g, float* dSb,
+                    float* gam, int skip1, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   ProfScope ps("k_blocksum", s);
-  hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk * H, 1, n_sides), dim3(Cfg<T, D>::NTHR), 0, s,
-                     B.seq_tab, B.blk_tab, B.blk_launch, B.replay_row, H, scale, static_cast<const T*>(q),
-                     static_cast<const T*>(k), static_cast<const T*>(v),
-                     static_cast<const T*>(dO), g, dSb, U, gam, side0, skip1);
+  hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
+                     B.blk_tab, B.blk_launch, B.replay_row, H, static_cast<const T*>(k),
+                     static_cast<const T*>(v), g, dSb, gam, skip1);
   return hip_check("k_blocksum");
 }
 
@@ -1605,8 +1683,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   // from the initial state and writes the final state itself (with outputs),
   // and the backward kernels start and end such sequences themselves.
   const int skip1 = o || !S_final;
-  if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, nullptr, g, dSb, nullptr,
-                                      gam, 0, 1, skip1, s))
+  if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, g, dSb, gam, skip1, s))
     return rc;
   if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam, S_end, bank, S_final, skip1, s))
     return rc;
@@ -1643,23 +1720,28 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   float* betap = reinterpret_cast<float*>(w);
   w += z.betap;
   if (!saved) {
-    // recompute-forward: forward summaries (chained from S0 below) and the
-    // adjoint summaries in one launch
+    // recompute-forward: forward summaries, chained from S0 below
     float* dSb = reinterpret_cast<float*>(w);
     char* sv = w + z.blk_state;
     float* S_end_w = reinterpret_cast<float*>(sv);
     float* gam_w = reinterpret_cast<float*>(sv + z.blk_state);
-    if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, dSb, U, gam_w, 0, 2, 1, s))
+    if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, g, dSb, gam_w, 1, s))
       return rc;
     if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam_w, S_end_w, nullptr, nullptr, 1, s))
       return rc;
     saved = sv;
-  } else if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, dO, g, nullptr, U,
-                                             nullptr, 1, 1, 1, s)) {
-    return rc;
   }
   const float* S_end = reinterpret_cast<const float*>(saved);
   const float* gam = reinterpret_cast<const float*>(saved + z.blk_state);
+  {
+    ProfScope ps("k_bwd_fwdorder", s);
+    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk * H), dim3(2 * Cfg<T, D>::NTHR), 0, s,
+                       B.seq_tab, B.blk_tab, B.blk_launch, B.replay_row, H, scale,
+                       static_cast<const T*>(q), static_cast<const T*>(k),
+                       static_cast<const T*>(v), g, static_cast<const T*>(dO), is, S_end,
+                       static_cast<T*>(dq), rq, dS_final, betap, U);
+  }
+  if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
     constexpr int NSW = D * D / 4 / SCAN_THR;
     ProfScope ps("k_bwd_blockscan", s);
@@ -1667,14 +1749,6 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
                        B.seq_tab, B.blk_tab, H, dS_final, dbank, S_end, U, gam, dS_end, betap);
   }
   if (int rc = hip_check("k_bwd_blockscan")) return rc;
-  {
-    ProfScope ps("k_bwd_fwdorder", s);
-    hipLaunchKernelGGL((k_bwd_fwdorder<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
-                       B.blk_tab, B.blk_launch, B.replay_row, H, scale, static_cast<const T*>(q),
-                       static_cast<const T*>(k), static_cast<const T*>(v), g,
-                       static_cast<const T*>(dO), is, S_end, static_cast<T*>(dq), rq, dS_final, betap);
-  }
-  if (int rc = hip_check("k_bwd_fwdorder")) return rc;
   {
     ProfScope ps("k_bwd_revorder", s);
     hipLaunchKernelGGL((k_bwd_revorder<T, D>), dim3(L.n_blk * H), dim3(2 * Cfg<T, D>::NTHR), 0, s,
