@@ -100,7 +100,8 @@ def seq_blocks(plan, i, B, block_chunks):
 def algorithmic_bytes(plan, H, d, el):
     """Bytes each kernel must move for its job over one step (forward, then
     the backward with the recompute-forward), by kernel, for the launches the
-    runner makes.
+    runner makes.  The local adjoint of a block is formed by the
+    forward-order backward kernel, which reads the block's q and dO anyway.
 
     Rows are packed rows (own + replay); q, o, dO and dq exist on own rows
     only.  Block-level states (summaries, chained block-end states, local
@@ -136,8 +137,6 @@ def algorithmic_bytes(plan, H, d, el):
         nseq_m = len(multi)
         rows_nl = sum(rw for x in blks for rw, _ in x[:-1])      # rows of blocks not last
         rows_l = sum(x[-1][0] for x in blks)                      # rows of last blocks
-        rows_nf = sum(rw for x in blks for rw, _ in x[1:])       # rows of blocks not first
-        own_nf = sum(ow for x in blks for _, ow in x[1:])
         nreq = int(sum(plan["seq_req_off"][i + 1] - plan["seq_req_off"][i] for i in range(s0, s1)))
         ninit = int(np.sum(init_bank[s0:s1] >= 0))             # sequences with a non-zero start
         ninit_m = int(sum(1 for i in multi if init_bank[i] >= 0))
@@ -150,16 +149,15 @@ def algorithmic_bytes(plan, H, d, el):
         scan = 2 * chained * st + ninit_m * st + nreq * st
         b["k_fwd_blockscan"] += 2 * scan
         n["k_fwd_blockscan"] += 2
-        # summaries: side 0 in the forward and the recompute pass (k, v, g of
-        # blocks not last, g of last blocks), side 1 in backward (q, dO of
-        # own rows and g of blocks not first)
+        # forward summaries, in the forward and the recompute pass (k, v, g
+        # of blocks not last, g of last blocks)
         side0 = rows_nl * H * (2 * d * el + 4) + rows_l * H * 4 + (nblk - nseq) * st
-        side1 = own_nf * H * 2 * d * el + rows_nf * H * 4 + (nblk - nseq) * st
-        b["k_blocksum"] += 2 * side0 + side1
-        n["k_blocksum"] += 3
+        b["k_blocksum"] += 2 * side0
+        n["k_blocksum"] += 2
         fblock = kv + own * H * 2 * d * el + starts + nseq * st
         b["k_fwd_block"] += fblock
-        fwdorder = kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq * st
+        # dq and q.dq, and the local adjoints of blocks not first (written)
+        fwdorder = kv + own * H * 3 * d * el + rows * H * 4 + starts + nseq * st + (nblk - nseq) * st
         b["k_bwd_fwdorder"] += fwdorder
         # adjoint chain: dS_final in, local adjoints of blocks not first in,
         # end adjoints of blocks not last out, requested injections and states in
@@ -175,7 +173,7 @@ def algorithmic_bytes(plan, H, d, el):
             n[name] += 1
         passes["fwd"] += side0 + scan + fblock
         passes["state"] += side0 + scan
-        passes["bwd"] += side1 + bscan + fwdorder + revorder + rows * H * 8 + 3 * nseq * st
+        passes["bwd"] += bscan + fwdorder + revorder + rows * H * 8 + 3 * nseq * st
     R = plan.info["R"]
     b["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
     n["k_replay_reduce"] = 1 if R else 0
