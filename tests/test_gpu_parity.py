@@ -192,6 +192,24 @@ def test_random_forests_bf16_d64():
         compare(parent, seg_len, x, 3, 64, "bf16", label=f"bf16-d64-{trial}")
 
 
+@pytest.mark.parametrize("dtype,H", [("f32", 2), ("bf16", 3)])
+def test_multiblock_sequences_d64(dtype, H, monkeypatch):
+    """Sequences of several blocks at d = 64 in both dtypes: block
+    summaries, the local adjoints formed by the forward-order kernel, and
+    both chains over blocks.  A 1,900-token root (30 chunks) with forks at
+    unaligned offsets, cut into 8-chunk blocks (the planner's smallest, for
+    a block target it cannot reach)."""
+    monkeypatch.setenv("HARTS_MIN_BLOCKS", "100000")
+    parent = [-1, 0, 0, 1, 1]
+    seg_len = [1900, 700, 333, 75, 610]
+    r = np.random.default_rng(2024 + H)
+    x = draw_inputs(sum(seg_len), 3, H, 64, 64, r, dtype, n_trees=1, s0_scale=0.3)
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan(parent, seg_len, 64)
+    assert plan.rounds[0]["block_chunks"] == 8 and plan.rounds[0]["n_blk"] > plan.rounds[0]["n_seq"]
+    compare(parent, seg_len, x, H, 64, dtype, label=f"multi-block {dtype}")
+
+
 def test_config1_spine_bf16():
     f, cfg, x = config_inputs(1)
     compare(f.parent, f.seg_len, x, cfg["H"], cfg["d"], "bf16", heads=[0, 5, 10, 15],
