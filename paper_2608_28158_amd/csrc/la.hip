@@ -958,6 +958,17 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       }
       __syncthreads();
     }
+    // The last block of a sequence ends with S_final (S^T is held here):
+    // <dS_final, S_final> is its boundary term of dg, the first of the
+    // block's NSW partial sums (threads t < NSW are in this half).
+    if (bl.idx == bl.n_blk - 1) {
+      constexpr int NSW = D * D / 4 / SCAN_THR;
+      static_assert(NSW <= 64 * C::NW, "partial sums written by side 0");
+      const float dot = state_dot_via_lds<D, C::CPW, NTH>(
+          S, stage, dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD, true, ws, lane, t,
+          sm.red, true);
+      if (t < NSW) betap[(static_cast<int64_t>(b) * H + h) * NSW + t] = t == 0 ? dot : 0.f;
+    }
   } else {
     for (int c = c0; c < c_end; ++c) {
       const int bf = (c - c0) & 1;
@@ -993,23 +1004,17 @@ __global__ __launch_bounds__((2 * Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_bwd
       }
       __syncthreads();
     }
-  }
-  if (w == 2 * C::NW - 1) {
-    float s = 0.f;
+    if (ws == C::NW - 1) {
+      float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < C::NW; ++i) s += sm.rq[i][lane];
-    rq_out[((static_cast<int64_t>(sq.chunk_off) + c_end - 1) * CB + lane) * H + h] = s;
-  }
-  if (side && want_u) state_store<D, C::CPW>(U + (static_cast<int64_t>(b) * H + h) * DD, S, ws, lane);
-  // The last block of a sequence ends with S_final (S^T is held by side 0):
-  // <dS_final, S_final> is its boundary term of dg, the first of the block's
-  // NSW partial sums.
-  if (bl.idx == bl.n_blk - 1) {
-    constexpr int NSW = D * D / 4 / SCAN_THR;
-    const float dot = state_dot_via_lds<D, C::CPW, NTH>(
-        S, stage, dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD, true, ws, lane, t,
-        sm.red, !side);
-    if (t < NSW) betap[(static_cast<int64_t>(b) * H + h) * NSW + t] = t == 0 ? dot : 0.f;
+      for (int i = 0; i < C::NW; ++i) s += sm.rq[i][lane];
+      rq_out[((static_cast<int64_t>(sq.chunk_off) + c_end - 1) * CB + lane) * H + h] = s;
+    }
+    if (want_u) state_store<D, C::CPW>(U + (static_cast<int64_t>(b) * H + h) * DD, S, ws, lane);
+    // (this half joins the staging and the sum of side 0's boundary term)
+    if (bl.idx == bl.n_blk - 1)
+      state_dot_via_lds<D, C::CPW, NTH>(S, stage, dS_final + (static_cast<int64_t>(bl.final_leaf) * H + h) * DD,
+                                        true, ws, lane, t, sm.red, false);
   }
 }
 
