@@ -558,6 +558,8 @@ constexpr int SCAN_THR = 256;
 // Blocks whose summaries a scan requests together: the chain is serial in
 // the blocks, its loads are not.
 constexpr int SCAN_PF = 8;
+constexpr int DG_HEADS = 16;  // heads per workgroup of k_dg_carry
+static_assert(SCAN_THR % DG_HEADS == 0, "head lanes split the workgroup");
 
 template <int D>
 __global__ __launch_bounds__(SCAN_THR) void k_fwd_blockscan(
@@ -1442,27 +1444,51 @@ __global__ __launch_bounds__(SCAN_THR) void k_dg_carry(
     const int32_t* __restrict__ seq_tab, const int32_t* __restrict__ blk_tab, int H,
     const float* __restrict__ betap, const float* __restrict__ Rb, float* __restrict__ dg,
     float* __restrict__ rep_grad) {
+  // One workgroup per (block, chunk of the block, group of DG_HEADS heads):
+  // lane hl = t % DG_HEADS is a head, part = t / DG_HEADS a slice of the
+  // terms summed into its carry; the chunk's rows are then updated for all
+  // heads of the group at once (dg rows are [rows, H], so a row's heads are
+  // contiguous).
   constexpr int NSW = D * D / 4 / SCAN_THR;
   constexpr int RG = 2 * D + 1;
-  const int b = blockIdx.x, h = blockIdx.y, t = threadIdx.x;
+  constexpr int NPART = SCAN_THR / DG_HEADS;
+  __shared__ float red[SCAN_THR];
+  __shared__ float carry_s[DG_HEADS];
+  const int b = blockIdx.x, cc = blockIdx.y, h0 = blockIdx.z * DG_HEADS, t = threadIdx.x;
+  const int hl = t % DG_HEADS, part = t / DG_HEADS, h = h0 + hl;
   const int32_t* bk = blk_tab + b * BLK_WORDS;
+  if (cc >= bk[BLK_NC]) return;  // uniform: blocks have up to block_chunks chunks
   const int32_t* seq = seq_tab + bk[BLK_SEQ] * SEQ_WORDS;
   const int b_end = seq[SEQ_BLK_OFF] + seq[SEQ_N_BLK];
   float carry = 0.f;
-  for (int bb = b; bb < b_end; ++bb) {
-    const int64_t bi = static_cast<int64_t>(bb) * H + h;
-    for (int p = 0; p < NSW; ++p) carry += betap[bi * NSW + p];
-    if (bb > b) carry += Rb[bi];
+  if (h < H) {
+    for (int bb = b; bb < b_end; ++bb) {
+      const int64_t bi = static_cast<int64_t>(bb) * H + h;
+      for (int p = part; p < NSW; p += NPART) carry += betap[bi * NSW + p];
+      if (bb > b && part == 0) carry += Rb[bi];
+    }
   }
-  const int c0 = bk[BLK_C0], nc = bk[BLK_NC];
+  red[t] = carry;
+  __syncthreads();
+  if (t < DG_HEADS) {
+    float c = 0.f;
+#pragma unroll
+    for (int k = 0; k < NPART; ++k) c += red[t + DG_HEADS * k];
+    carry_s[t] = c;
+  }
+  __syncthreads();
+  const float ch = carry_s[hl];
+  const int c = bk[BLK_C0] + cc;
   const int n_rep = seq[SEQ_N_REPLAY], n_tok = seq[SEQ_N_TOK];
-  for (int idx = t; idx < nc * CB; idx += SCAN_THR) {
-    const int p = c0 * CB + idx;
+  if (h >= H) return;
+#pragma unroll
+  for (int idx = t; idx < CB * DG_HEADS; idx += SCAN_THR) {
+    const int p = c * CB + idx / DG_HEADS;  // idx % DG_HEADS == hl
     if (p < n_rep) {
       const int j = seq[SEQ_REPLAY_OFF] + p;
-      rep_grad[(static_cast<int64_t>(j) * H + h) * RG + 2 * D] += carry;
+      rep_grad[(static_cast<int64_t>(j) * H + h) * RG + 2 * D] += ch;
     } else if (p < n_tok) {
-      dg[(static_cast<int64_t>(seq[SEQ_OWN_ROW]) + (p - n_rep)) * H + h] += carry;
+      dg[(static_cast<int64_t>(seq[SEQ_OWN_ROW]) + (p - n_rep)) * H + h] += ch;
     }
   }
 }
@@ -1765,8 +1791,8 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   if (int rc = hip_check("k_bwd_revorder")) return rc;
   {
     ProfScope ps("k_dg_carry", s);
-    hipLaunchKernelGGL((k_dg_carry<D>), dim3(L.n_blk, H), dim3(SCAN_THR), 0, s, B.seq_tab,
-                       B.blk_tab, H, betap, Rb, dg, rep_grad);
+    hipLaunchKernelGGL((k_dg_carry<D>), dim3(L.n_blk, L.block_chunks, (H + DG_HEADS - 1) / DG_HEADS),
+                       dim3(SCAN_THR), 0, s, B.seq_tab, B.blk_tab, H, betap, Rb, dg, rep_grad);
   }
   return hip_check("k_dg_carry");
 }
