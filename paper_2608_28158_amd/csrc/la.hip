@@ -1674,9 +1674,8 @@ Blob blob_ptrs(const harts_plan_t* p, int32_t round, const void* d_blob) {
 // Forward block summaries dS_b and Gamma_b; skip1: none for sequences of one
 // block.
 template <typename T, int D>
-int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, float scale,
-                    const void* q, const void* k, const void* v, const float* g, float* dSb,
-                    float* gam, int skip1, hipStream_t s) {
+int launch_blocksum(const harts_plan_t* p, int32_t round, const Blob& B, int H, const void* k,
+                    const void* v, const float* g, float* dSb, float* gam, int skip1, hipStream_t s) {
   const RoundLayout& L = p->rounds[round];
   ProfScope ps("k_blocksum", s);
   hipLaunchKernelGGL((k_blocksum<T, D>), dim3(L.n_blk * H), dim3(Cfg<T, D>::NTHR), 0, s, B.seq_tab,
@@ -1714,7 +1713,7 @@ int run_fwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
   // from the initial state and writes the final state itself (with outputs),
   // and the backward kernels start and end such sequences themselves.
   const int skip1 = o || !S_final;
-  if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, g, dSb, gam, skip1, s))
+  if (int rc = launch_blocksum<T, D>(p, round, B, H, k, v, g, dSb, gam, skip1, s))
     return rc;
   if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam, S_end, bank, S_final, skip1, s))
     return rc;
@@ -1756,7 +1755,7 @@ int run_bwd(const harts_plan_t* p, int32_t round, const void* d_blob, int H, flo
     char* sv = w + z.blk_state;
     float* S_end_w = reinterpret_cast<float*>(sv);
     float* gam_w = reinterpret_cast<float*>(sv + z.blk_state);
-    if (int rc = launch_blocksum<T, D>(p, round, B, H, scale, q, k, v, g, dSb, gam_w, 1, s))
+    if (int rc = launch_blocksum<T, D>(p, round, B, H, k, v, g, dSb, gam_w, 1, s))
       return rc;
     if (int rc = launch_fwd_scan<D>(p, round, B, H, is, dSb, gam_w, S_end_w, nullptr, nullptr, 1, s))
       return rc;
