@@ -373,11 +373,13 @@ struct Builder {
     harts_plan_s& p = *P;
     const int32_t K = p.K;
     // Target number of blocks per round (tuning knob).  Larger blocks move
-    // fewer block states through HBM, smaller ones expose more workgroups;
-    // 80 measured best on the 64k-token agentic workload at 16 heads
-    // (16-chunk blocks in its long-sequence round; 2.30 ms per step against
-    // 2.45 ms with 8-chunk and 2.56 ms with 64-chunk blocks).
-    int32_t min_blocks = 80;
+    // fewer block states through HBM and start fewer workgroups (each reads
+    // a start state before its first chunk), smaller ones expose more
+    // workgroups.  56 measured best on the 64k-token agentic workload at 16
+    // heads: 48-chunk blocks in its long-sequence round (59 blocks), 1.777 ms
+    // per step against 1.797 ms with 16-chunk blocks (target 80), in
+    // alternating runs.
+    int32_t min_blocks = 56;
     if (const char* env = std::getenv("HARTS_MIN_BLOCKS")) {
       const long x = std::strtol(env, nullptr, 10);
       if (x >= 1 && x <= (1 << 20)) min_blocks = static_cast<int32_t>(x);
