@@ -225,7 +225,7 @@ def cpu_baseline(forest, x, cfg, heads=(0, 5, 10, 15)):
 def run_step(runner, t):
     fwd = runner.forward(t["q"], t["k"], t["v"], t["g"], t["S0"], outputs=True,
                          keep_states=False)
-    runner.backward(t["q"], t["k"], t["v"], t["g"], t["dO"], t["dS_final"], fwd=None,
+    runner.backward(t["q"], t["k"], t["v"], t["g"], t["dO"], t["dS_final"], fwd=fwd,
                     S0_tree=t["S0"], recompute=True)
     return fwd
 

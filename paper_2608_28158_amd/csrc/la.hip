@@ -1623,6 +1623,12 @@ int check_shape(const harts_plan_t* p, int32_t round, int32_t dtype, int32_t H, 
   if (dtype != HARTS_F32 && dtype != HARTS_BF16) { set_error(w + ": unknown dtype"); return HARTS_EUNSUPPORTED; }
   if (dk != dv || (dk != 64 && dk != 128)) { set_error(w + ": need dk == dv in {64, 128}"); return HARTS_EUNSUPPORTED; }
   if (dtype == HARTS_F32 && dk != 64) { set_error(w + ": float32 path supports d = 64"); return HARTS_EUNSUPPORTED; }
+  // the kernels' row tables pack (physical row, kind) as row * 4 + kind in
+  // an int32, so packed rows must stay below 2^29
+  if (p->C + p->R >= (int64_t{1} << 29)) {
+    set_error(w + ": more than 2^29 packed rows (C + R) per plan");
+    return HARTS_EUNSUPPORTED;
+  }
   return HARTS_OK;
 }
 

@@ -9,8 +9,10 @@ the round's initial states are first gathered into a dense buffer by
 (Sec. 3.4, "Differentiable boundary states"): ``harts_la_bwd`` per round,
 then the scatter-add adjoint of the gather into the bank gradient, and
 finally ``harts_replay_reduce``.  With ``recompute=True`` the forward keeps
-only its inputs and the plan; the backward first re-runs the state pass of
-every round from the same plan ("Full-layer activation recomputation").
+only its inputs, the plan and the bank of boundary states the rounds hand
+over; each round's backward re-runs that round's state pass from the same
+plan inside ``harts_la_bwd`` (saved = NULL), "Full-layer activation
+recomputation" of Sec. 3.4.
 
 Python here only marshals arguments and owns torch buffers; every step runs
 in libharts.
@@ -146,12 +148,16 @@ class TreeLARunner:
     # -- backward ------------------------------------------------------------
     def backward(self, q, k, v, g, dO, dS_final, fwd=None, S0_tree=None, recompute=False):
         """Gradients of <dO, o> + <dS_final, S_final>.  ``fwd`` is the dict
-        from forward(keep_states=True); with recompute=True (or fwd None)
-        the state pass of every round is re-run from the plan first."""
+        from forward(); its bank holds the boundary states every round starts
+        from.  With recompute=True, or when the forward kept no block states
+        (keep_states=False), each round's ``harts_la_bwd`` re-runs that
+        round's state pass itself (saved = NULL); with fwd None a state-only
+        forward first rebuilds the bank."""
         P = self.plan
         H, d = self.H, self.d
-        if recompute or fwd is None:
-            fwd = self.forward(q, k, v, g, S0_tree, outputs=False, keep_states=True)
+        if fwd is None:
+            fwd = self.forward(q, k, v, g, S0_tree, outputs=False, keep_states=False)
+            recompute = True
         if dO.dtype != self.dtype or not dO.is_contiguous() or dO.shape != q.shape:
             raise ValueError("dO must match o")
         if dS_final is None:
@@ -170,12 +176,13 @@ class TreeLARunner:
             s0 = P.rounds[r]["seq_begin"]
             dS0 = dS0_seq[s0:s0 + n]
             S0 = self.gather(fwd["bank"], r) if self.gather_init else None
-            ws = self._bytes(self.ws_bwd_saved[r])
+            sv = None if recompute else fwd["saved"][r]
+            ws = self._bytes(self.ws_bwd_rec[r] if sv is None else self.ws_bwd_saved[r])
             _lib.check(self.L.harts_la_bwd(
                 P.handle, r, _ptr(self.blob), self.code, H, d, d, self.scale,
                 _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(S0), _ptr(fwd["bank"]), _ptr(dO),
                 _ptr(dS_final),
-                _ptr(dbank), _ptr(fwd["saved"][r]), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg),
+                _ptr(dbank), _ptr(sv), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg),
                 _ptr(rep), _ptr(dS0), _ptr(ws), ws.numel(), self._stream()), "harts_la_bwd")
             self.scatter_add(dS0, dbank, r)
         _lib.check(self.L.harts_replay_reduce(
@@ -191,7 +198,9 @@ class _TreeLAFn(torch.autograd.Function):
         res = runner.forward(q, k, v, g, S0_tree, outputs=True, keep_states=not recompute)
         ctx.runner = runner
         ctx.recompute = recompute
-        ctx.fwd = None if recompute else res
+        # with recompute the block states are not kept: the backward re-runs
+        # each round's state pass from the bank of boundary states
+        ctx.fwd = res
         ctx.save_for_backward(q, k, v, g, S0_tree)
         return res["o"], res["S_final"]
 

@@ -9,6 +9,14 @@ from workloads import config_inputs  # noqa: F401
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
+# (label, dtype, {tensor: max-rel error}) of every GPU comparison run in this
+# session; printed by the terminal summary hook in conftest.py.
+MARGINS = []
+
+
+def record(label, dtype, errs):
+    MARGINS.append((label, dtype, dict(errs)))
+
 
 def max_rel(x, ref):
     x = np.asarray(x, np.float64)

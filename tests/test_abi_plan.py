@@ -172,3 +172,18 @@ def test_device_calls_validate_before_launch(L):
     assert g(null, null, 0, C.c_int64(16), null, 0, null) == _lib.HARTS_OK
     p.close()
     p2.close()
+
+
+def test_device_calls_reject_plans_beyond_the_row_limit(L):
+    """Device row tables hold physical row * 4 + kind in int32: a plan of
+    2^29 or more packed rows plans on the host but every device call
+    rejects it with HARTS_EUNSUPPORTED before launching anything."""
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    sz = C.c_size_t()
+    for n_rows, rc in (((1 << 29) - 64, _lib.HARTS_OK), (1 << 29, _lib.HARTS_EUNSUPPORTED)):
+        p = HartsPlan([-1], [n_rows], 64)
+        assert p["C"] + p["R"] == n_rows
+        assert L.harts_la_workspace_size(p.handle, 0, 0, _lib.HARTS_BF16, 1, 64, 64, 0,
+                                         C.byref(sz)) == rc
+        p.close()

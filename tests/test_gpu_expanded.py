@@ -17,7 +17,7 @@ import numpy as np
 import pytest
 import torch
 
-from tests.harness import TOL, max_rel
+from tests.harness import TOL, max_rel, record
 from tests.test_gpu_parity import run_gpu
 from workloads import draw_inputs
 
@@ -94,6 +94,7 @@ def check(parent, seg_len, H, d, dtype, seed, label):
     errs["dS0_tree"] = max_rel(packed["dS0_tree"], dS0)
     print(f"[gpu] expanded-vs-packed {label}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()),
           flush=True)
+    record(f"expanded-vs-packed {label}", dtype, errs)
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, f"{label}: above {tol}: {bad}"
 
