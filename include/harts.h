@@ -25,7 +25,9 @@
  *     Round-to-round dependencies are carried by stream order.
  *   - The library never allocates device memory.  The caller owns every
  *     device buffer; scratch space is passed as (ws, ws_bytes) sized by the
- *     *_workspace_size queries.  Plans are library-owned host objects.
+ *     *_workspace_size queries.  Plans are library-owned host objects.  The
+ *     one exception is harts_la_fwd_noalloc's fixed scratch array, part of
+ *     the library's device image.
  *   - Row layout: token-major [rows, H, d] in the plan's physical row order
  *     (sequences in id order, each sequence's own segments contiguous).
  *     q, k: [C, H, dk]; v, o: [C, H, dv]; g, dg: float32 [C, H].
@@ -33,7 +35,8 @@
  *   - dtype: HARTS_F32 (q, k, v, o, dO and gradients float32) or HARTS_BF16
  *     (those tensors bfloat16; g, states and their gradients always float32).
  *   - Supported head shapes: dk = dv in {64, 128} for bf16, 64 for float32;
- *     chunk size 64.  Anything else returns HARTS_EUNSUPPORTED.
+ *     chunk size 64; fewer than 2^29 packed rows (C + R) per plan.  Anything
+ *     else returns HARTS_EUNSUPPORTED.
  */
 #ifndef HARTS_H_
 #define HARTS_H_
@@ -225,6 +228,31 @@ int harts_la_fwd(const harts_plan_t* plan, int32_t round, const void* d_blob,
                  const void* q, const void* k, const void* v, const float* g,
                  const float* S0, void* o, float* S_final, float* bank,
                  void* saved, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * harts_la_fwd_noalloc -- harts_la_fwd for callers that cannot allocate
+ * device memory or pass a workspace: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Same arguments, results
+ * and errors as harts_la_fwd with saved = NULL and no workspace: the
+ * round's scratch (block summaries, block-end states and log-decays) lives
+ * in a fixed 64 MiB array in device memory that the library holds on every
+ * GPU it runs on until the process ends.  The caller still owns and passes
+ * inputs and outputs.  Nothing is allocated: no hipMalloc, hipFree or
+ * allocating library call.  The scratch needs no clearing between calls
+ * (every byte read is written first in the same call).
+ *   Limit: rounds whose scratch (2 states of H*dk*dv*4 bytes per block,
+ *   plus the block log-decays, 256-byte aligned) exceeds 64 MiB return
+ *   HARTS_ENOMEM with the required size in the message, before anything
+ *   is enqueued.
+ *   Concurrency: all calls on one GPU share its array; two calls that may
+ *   overlap on one GPU (different streams, or host threads) race.  Calls
+ *   ordered on one stream are safe.
+ * ---------------------------------------------------------------------- */
+int harts_la_fwd_noalloc(const harts_plan_t* plan, int32_t round, const void* d_blob,
+                         int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                         const void* q, const void* k, const void* v, const float* g,
+                         const float* S0, void* o, float* S_final, float* bank,
+                         void* stream);
 
 /* ------------------------------------------------------------------------
  * harts_la_bwd -- backward of one round (Sec. 3.4 "Differentiable boundary

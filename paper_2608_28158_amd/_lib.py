@@ -21,7 +21,7 @@ HARTS_F32, HARTS_BF16 = 0, 1
 EXPORTS = (
     "harts_last_error", "harts_plan", "harts_plan_free", "harts_plan_get_info",
     "harts_plan_export", "harts_plan_round_info", "harts_plan_blob",
-    "harts_la_fwd", "harts_la_bwd", "harts_la_workspace_size",
+    "harts_la_fwd", "harts_la_fwd_noalloc", "harts_la_bwd", "harts_la_workspace_size",
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
     "harts_profile_begin", "harts_profile_end",
 )
@@ -123,6 +123,9 @@ def lib():
     L.harts_la_fwd.restype = C.c_int
     L.harts_la_fwd.argtypes = [vp, i32, vp, i32, i32, i32, i32, f32,
                                vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.harts_la_fwd_noalloc.restype = C.c_int
+    L.harts_la_fwd_noalloc.argtypes = [vp, i32, vp, i32, i32, i32, i32, f32,
+                                       vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.harts_la_bwd.restype = C.c_int
     L.harts_la_bwd.argtypes = [vp, i32, vp, i32, i32, i32, i32, f32,
                                vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,

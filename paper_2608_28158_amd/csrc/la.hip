@@ -1829,24 +1829,27 @@ extern "C" int harts_la_workspace_size(const harts_plan_t* p, int32_t round, int
   return HARTS_OK;
 }
 
-extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_blob,
-                            int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
-                            const void* q, const void* k, const void* v, const float* g,
-                            const float* S0, void* o, float* S_final, float* bank, void* saved,
-                            void* ws, size_t ws_bytes, void* stream) {
-  if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_fwd")) return rc;
+namespace harts {
+namespace {
+
+int la_fwd_impl(const harts_plan_t* p, int32_t round, const void* d_blob, int32_t dtype, int32_t H,
+                int32_t dk, int32_t dv, float scale, const void* q, const void* k, const void* v,
+                const float* g, const float* S0, void* o, float* S_final, float* bank, void* saved,
+                void* ws, size_t ws_bytes, void* stream, const char* where) {
+  const std::string w0(where);
+  if (int rc = check_shape(p, round, dtype, H, dk, dv, where)) return rc;
   if (!d_blob || !q || !k || !v || !g || !ws || (!bank && (p->n_slots > 0 || !S0))) {
-    set_error("harts_la_fwd: NULL required pointer");
+    set_error(w0 + ": NULL required pointer");
     return HARTS_EINVAL;
   }
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(S0) || !aligned16(o) ||
       !aligned16(S_final) || !aligned16(bank) || !aligned16(saved) || !aligned16(ws)) {
-    set_error("harts_la_fwd: pointers must be 16-byte aligned");
+    set_error(w0 + ": pointers must be 16-byte aligned");
     return HARTS_EINVAL;
   }
   const Sizes z = sizes(p, round, H, dk);
   if (ws_bytes < z.ws_fwd + (saved ? 0 : z.saved)) {
-    set_error("harts_la_fwd: workspace too small (see harts_la_workspace_size)");
+    set_error(w0 + ": workspace too small (see harts_la_workspace_size)");
     return HARTS_EINVAL;
   }
   char* w = static_cast<char*>(ws);
@@ -1858,6 +1861,71 @@ extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_
     return run_fwd<bf16, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, sv, w, s);
   }
   return run_fwd<float, 64>(p, round, d_blob, H, scale, q, k, v, g, S0, o, S_final, bank, sv, w, s);
+}
+
+// Scratch of harts_la_fwd_noalloc: the round's block summaries, block-end
+// states and block log-decays, in a file-scope device array that each GPU
+// holds from the library's load until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in
+// for the symbol): the device address comes from hipGetSymbolAddress, taken
+// once per device with that device current.
+constexpr size_t kScratchBytes = size_t{64} << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_ptr(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    set_error("harts_la_fwd_noalloc: no current HIP device (or device id >= 64)");
+    return HARTS_EHIP;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      set_error(std::string("harts_la_fwd_noalloc: hipGetSymbolAddress: ") + hipGetErrorString(e));
+      return HARTS_EHIP;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return HARTS_OK;
+}
+
+}  // namespace
+}  // namespace harts
+
+extern "C" int harts_la_fwd(const harts_plan_t* p, int32_t round, const void* d_blob,
+                            int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                            const void* q, const void* k, const void* v, const float* g,
+                            const float* S0, void* o, float* S_final, float* bank, void* saved,
+                            void* ws, size_t ws_bytes, void* stream) {
+  return la_fwd_impl(p, round, d_blob, dtype, H, dk, dv, scale, q, k, v, g, S0, o, S_final, bank,
+                     saved, ws, ws_bytes, stream, "harts_la_fwd");
+}
+
+extern "C" int harts_la_fwd_noalloc(const harts_plan_t* p, int32_t round, const void* d_blob,
+                                    int32_t dtype, int32_t H, int32_t dk, int32_t dv, float scale,
+                                    const void* q, const void* k, const void* v, const float* g,
+                                    const float* S0, void* o, float* S_final, float* bank,
+                                    void* stream) {
+  if (int rc = check_shape(p, round, dtype, H, dk, dv, "harts_la_fwd_noalloc")) return rc;
+  const Sizes z = sizes(p, round, H, dk);
+  const size_t need = z.ws_fwd + z.saved;
+  if (need > kScratchBytes) {
+    set_error("harts_la_fwd_noalloc: the round needs " + std::to_string(need) +
+              " bytes of scratch, above the library's fixed " + std::to_string(kScratchBytes) +
+              " (use harts_la_fwd with a workspace)");
+    return HARTS_ENOMEM;
+  }
+  void* ws = nullptr;
+  if (int rc = scratch_ptr(&ws)) return rc;
+  return la_fwd_impl(p, round, d_blob, dtype, H, dk, dv, scale, q, k, v, g, S0, o, S_final, bank,
+                     nullptr, ws, kScratchBytes, stream, "harts_la_fwd_noalloc");
 }
 
 extern "C" int harts_la_bwd(const harts_plan_t* p, int32_t round, const void* d_blob,
