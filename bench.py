@@ -97,10 +97,53 @@ def seq_blocks(plan, i, B, block_chunks):
     return out
 
 
-def algorithmic_bytes(plan, H, d, el):
-    """Bytes each kernel must move for its job over one step (forward, then
-    the backward with the recompute-forward), by kernel, for the launches the
-    runner makes.  The local adjoint of a block is formed by the
+def alg_bytes(plan, H, d, el):
+    """Algorithmic bytes of one step: what the method must move, the
+    per-token figures of the measurement plan (q, k, v, dO read once; o, dq,
+    dk, dv, g and dg once) plus the plan's replay rows and states.
+
+    Per compact (own) row, with E = d * el bytes per head vector:
+      forward          q, k, v, g read; o written           H (4E + 4)
+      backward         q, k, v, dO, g read; dq, dk, dv, dg   H (7E + 8)
+      recompute        q, k, v, g read (state pass)          H (3E + 4)
+    Per replay row: k, v, g read in every pass (H (2E + 4) each), and in the
+    backward its dk, dv, dg contributions written once, float32
+    (H (2d + 1) 4).  Per state (H d d 4 bytes): forward reads every
+    sequence's initial state and writes every requested state and every
+    final state; the backward reads initial states, dS_final and the
+    requested states' gradients and writes dS0 of every sequence; the
+    recompute reads initial states again.
+
+    Returns {"fwd", "bwd", "state"} bytes and the share of the two backward
+    kernels and of the forward block kernel (the bytes of their own outputs:
+    the inputs those outputs need, once, and the outputs).  At H = 16,
+    d = 128, bf16 the per-row figures are 16,448 / 28,800 / 12,352 bytes."""
+    E = d * el
+    st = H * d * d * 4
+    C, R = plan.info["C"], plan.info["R"]
+    n_seq, n_slots, n_leaves = plan.info["n_seq"], plan.info["n_slots"], plan.info["n_leaves"]
+    rep = H * (2 * E + 4)
+    out = {
+        "fwd": C * H * (4 * E + 4) + R * rep + (n_seq + n_slots + n_leaves) * st,
+        "bwd": C * H * (7 * E + 8) + R * (rep + H * (2 * d + 1) * 4)
+               + (2 * n_seq + n_leaves + n_slots) * st,
+        "state": C * H * (3 * E + 4) + R * rep + n_seq * st,
+    }
+    # per-kernel shares, per step (each kernel runs once per round)
+    share = {
+        "k_fwd_block": C * H * (4 * E + 4) + R * rep + (n_seq + n_leaves) * st,
+        "k_bwd_fwdorder": C * H * (5 * E + 4) + R * rep + n_seq * st,
+        "k_bwd_revorder": C * H * (6 * E + 8) + R * (rep + H * (2 * d + 1) * 4)
+                          + 2 * n_seq * st,
+    }
+    return out, share
+
+
+def design_bytes(plan, H, d, el):
+    """Design traffic: the bytes each kernel of this implementation moves
+    over one step (forward, then the backward with the recompute-forward),
+    by kernel, for the launches the runner makes -- a diagnostic of the
+    decomposition, not the method's minimum (``alg_bytes``).  The local adjoint of a block is formed by the
     forward-order backward kernel, which reads the block's q and dO anyway.
 
     Rows are packed rows (own + replay); q, o, dO and dq exist on own rows
@@ -147,7 +190,8 @@ def algorithmic_bytes(plan, H, d, el):
         # in, states out, the initial states in, requested states out; in the
         # forward and in the recompute pass
         scan = 2 * chained * st + ninit_m * st + nreq * st
-        b["k_fwd_blockscan"] += 2 * scan
+        # the recompute inside the backward writes no bank slots
+        b["k_fwd_blockscan"] += 2 * scan - nreq * st
         n["k_fwd_blockscan"] += 2
         # forward summaries, in the forward and the recompute pass (k, v, g
         # of blocks not last, g of last blocks)
@@ -172,7 +216,7 @@ def algorithmic_bytes(plan, H, d, el):
                      "k_dg_carry", "k_scatter_add"):
             n[name] += 1
         passes["fwd"] += side0 + scan + fblock
-        passes["state"] += side0 + scan
+        passes["state"] += side0 + scan - nreq * st
         passes["bwd"] += bscan + fwdorder + revorder + rows * H * 8 + 3 * nseq * st
     R = plan.info["R"]
     b["k_replay_reduce"] = R * H * (2 * d + 1) * 4 + R * H * (2 * d * el * 2 + 8)
@@ -203,23 +247,99 @@ def read_traffic(kernel, workload_key):
         return None
 
 
-def cpu_baseline(forest, x, cfg, heads=(0, 5, 10, 15)):
-    """The fp64 oracle (compact chunkwise execution + reverse-mode gradients)
-    on a bounded sample: the listed heads of the same microbatch."""
-    import torch
-    from oracle.compact import compact_fwd_bwd
-    hs = list(heads)
-    sl = lambda a: a[:, hs]
+def _cpu_item(args):
+    """One (trajectory, head) work item of the fp64 trajectory-wise
+    recurrence: the forward, or the backward (which runs the forward states
+    itself).  Runs in a worker process; returns (tokens, seconds)."""
+    from oracle.recurrent import la_bwd, la_fwd
+    q, k, v, g, dO, dSf, scale, mode = args
     t0 = time.perf_counter()
-    compact_fwd_bwd(forest.parent, forest.seg_len, 64, sl(x["q"]), sl(x["k"]), sl(x["v"]),
-                    sl(x["g"]), cfg["d"] ** -0.5, sl(x["dO"]), sl(x["dS_final"]), sl(x["S0"]))
-    dt = time.perf_counter() - t0
-    H = cfg["H"]
-    return {"value": forest.n_rows / (dt * H / len(hs)), "unit": "compact tokens/s",
-            "cores": torch.get_num_threads(), "kind": "oracle",
-            "sample": f"{len(hs)} of {H} heads of the same microbatch, forward + backward, "
-                      f"float64 compact chunkwise oracle; {dt:.1f} s, scaled by {H // len(hs)} "
-                      f"(heads are independent)"}
+    S0 = np.zeros((1, q.shape[2], v.shape[2]))
+    if mode == "fwd":
+        la_fwd(q, k, v, g, S0, scale)
+    else:
+        la_bwd(q, k, v, g, S0, scale, dO, dSf)
+    return q.shape[0], time.perf_counter() - t0
+
+
+def _trajectory_rows(forest):
+    parent = forest.parent
+    row0 = np.concatenate([[0], np.cumsum(forest.seg_len)[:-1]])
+    out = []
+    for leaf in forest.leaves():
+        path, v = [], leaf
+        while v >= 0:
+            path.append(v)
+            v = parent[v]
+        out.append(np.concatenate([row0[w] + np.arange(forest.seg_len[w]) for w in reversed(path)]))
+    return out
+
+
+def cpu_baseline(forest, x, cfg, budget_s=8.0, seed=0):
+    """The fp64 oracle's trajectory-wise recurrence (every root-to-leaf path
+    run token by token, forward and backward) on the host's cores: a
+    process pool over (trajectory, head) items on every core of
+    os.sched_getaffinity (at most 16, the box's share), and one core.  Each
+    run takes a seeded random sample of the workload's items until its work
+    reaches about budget_s seconds of pool time; the measured token-head
+    rate is scaled to the whole job (S trajectory tokens times H heads) and
+    reported as compact tokens per second, C / time."""
+    import multiprocessing as mp
+    trajs = _trajectory_rows(forest)
+    H, d = cfg["H"], cfg["d"]
+    S = sum(len(r) for r in trajs)
+    rng = np.random.default_rng(seed)
+    items = [(t, h) for t in range(len(trajs)) for h in range(H)]
+    order = rng.permutation(len(items))
+
+    def item_args(i, mode):
+        t, h = items[i]
+        r = trajs[t]
+        sl = lambda a: np.ascontiguousarray(a[r][:, h:h + 1])
+        return (sl(x["q"]), sl(x["k"]), sl(x["v"]), sl(x["g"]), sl(x["dO"]),
+                x["dS_final"][t, h:h + 1].astype(np.float64), d ** -0.5, mode)
+
+    ncore = min(len(os.sched_getaffinity(0)), 16)
+    os.environ.setdefault("OMP_NUM_THREADS", "1")
+    ctx = mp.get_context("spawn")
+    res = {}
+    for label, procs in (("all_cores", ncore), ("one_core", 1)):
+        res[label] = {"cores": procs}
+        with ctx.Pool(procs) as pool:
+            for mode in ("fwd", "fwd_bwd"):
+                # probe: one short item gives the per-token cost; then a sample
+                # sized to the budget
+                n_tok, sec = pool.apply(_cpu_item, (item_args(order[0], mode),))
+                per_tok = sec / max(n_tok, 1)
+                want = budget_s * procs / per_tok / (2 if label == "one_core" else 1)
+                pick, tok = [], 0
+                for i in order:
+                    if tok >= want:
+                        break
+                    pick.append(i)
+                    tok += len(trajs[items[i][0]])
+                t0 = time.perf_counter()
+                done = pool.map(_cpu_item, [item_args(i, mode) for i in pick], chunksize=1)
+                wall = time.perf_counter() - t0
+                tok_heads = sum(n for n, _ in done)
+                full_s = S * H / (tok_heads / wall)
+                res[label][mode] = {"compact_tok_s": forest.n_rows / full_s,
+                                    "items": len(pick), "token_heads": tok_heads,
+                                    "wall_s": wall, "job_s_est": full_s}
+    a = res["all_cores"]
+    return {"value": a["fwd_bwd"]["compact_tok_s"], "unit": "compact tokens/s",
+            "cores": a["cores"], "kind": "oracle",
+            "sample": (f"fp64 trajectory-wise recurrence (oracle), forward + backward, "
+                       f"{a['fwd_bwd']['items']} random (trajectory, head) items of the same "
+                       f"microbatch ({a['fwd_bwd']['token_heads']} token-heads of "
+                       f"{S * H}) in {a['fwd_bwd']['wall_s']:.1f} s on a pool of {a['cores']} "
+                       f"processes, scaled to the whole job (S = {S} trajectory tokens x "
+                       f"{H} heads), reported as C / time"),
+            "forward_compact_tok_s": a["fwd"]["compact_tok_s"],
+            "one_core": {"cores": 1,
+                         "fwd_bwd_compact_tok_s": res["one_core"]["fwd_bwd"]["compact_tok_s"],
+                         "fwd_compact_tok_s": res["one_core"]["fwd"]["compact_tok_s"]},
+            "detail": res}
 
 
 def run_step(runner, t):
@@ -310,7 +430,6 @@ def expanded_comparison(steps, warmup):
     forest, cfg, x, plan, t, runner, _ = setup(4)
     ms_tree, _, _ = time_steps(runner, t, steps, warmup, profile=False)
     # expanded forest: one single-segment tree per trajectory, canonical rows
-    kids = forest.children()
     parent = forest.parent
     row0 = np.concatenate([[0], np.cumsum(forest.seg_len)[:-1]])
     trajs = []
@@ -337,20 +456,51 @@ def expanded_comparison(steps, warmup):
                            device="cuda")
     erunner = TreeLARunner(eplan, cfg["H"], cfg["d"], dt, "cuda")
     ms_exp, _, _ = time_steps(erunner, te, steps, warmup, profile=False)
-    # metamorphic check: identical outputs on every trajectory row (same
-    # chunk grid, same floating-point path)
-    fo = run_step(runner, t)["o"].float().cpu().numpy()
-    eo = run_step(erunner, te)["o"].float().cpu().numpy()
+    # metamorphic check (Sec. 2.2: the same chunk grid from every
+    # trajectory's start): outputs agree on every trajectory row and final
+    # states per leaf; with row c's upstream gradient given to one
+    # trajectory through c, the compact gradients of c equal the sums over
+    # the trajectories through c
+    first = np.full(forest.n_rows, -1, np.int64)
+    for i, r in enumerate(trajs):
+        new = first[r] < 0
+        first[r[new]] = i
+    owner = np.repeat(np.arange(len(trajs)), lens)
+    dO_e = np.where((first[erows] == owner)[:, None, None], x["dO"][erows], 0).astype(np.float32)
+    te_chk = dict(te, dO=to_device(dO_e, ephys, dt))
+
+    def full(rn, tt):
+        fwd = rn.forward(tt["q"], tt["k"], tt["v"], tt["g"], tt["S0"], outputs=True,
+                         keep_states=False)
+        grads = rn.backward(tt["q"], tt["k"], tt["v"], tt["g"], tt["dO"], tt["dS_final"],
+                            fwd=fwd, S0_tree=tt["S0"], recompute=True)
+        out = {"o": fwd["o"], "S_final": fwd["S_final"]}
+        out.update({n: grads[n] for n in ("dq", "dk", "dv", "dg")})
+        return {n: v.float().cpu().numpy().astype(np.float64) for n, v in out.items()}
+
+    a = full(runner, t)
+    b = full(erunner, te_chk)
     phys = phys_index(forest.seg_len, plan["seg_row"])
-    diff = float(np.max(np.abs(fo[phys][erows] - eo[ephys])) / np.max(np.abs(eo)))
+    rel = lambda u, w: float(np.max(np.abs(u - w)) / max(np.max(np.abs(w)), 1e-30))
+    agree = {"o": rel(a["o"][phys][erows], b["o"][ephys]),
+             "S_final": rel(a["S_final"], b["S_final"])}
+    for n in ("dq", "dk", "dv", "dg"):
+        acc = np.zeros_like(a[n])
+        np.add.at(acc, erows, b[n][ephys])
+        agree[n] = rel(a[n][phys], acc)
+    tol = 2e-2 if cfg["dtype"] == "bf16" else 1e-4
+    bad = {n: e for n, e in agree.items() if not e <= tol}
+    assert not bad, f"tree-packed and expanded runs disagree: {bad}"
     C = forest.n_rows
     S = int(lens.sum())
     return {"workload": "4 agentic trees, ~32k compact tokens, H=16, d=128, bf16, fwd+bwd "
                         "with recompute",
-            "C": C, "S": S, "tree_packed_ms": ms_tree, "expanded_ms": ms_exp,
+            "C": C, "S": S, "expansion_S_over_C": S / C,
+            "tree_packed_ms": ms_tree, "expanded_ms": ms_exp,
             "tree_packed_compact_tok_s": C / (ms_tree * 1e-3),
             "expanded_compact_tok_s": C / (ms_exp * 1e-3),
-            "speedup": ms_exp / ms_tree, "outputs_max_rel_diff": diff,
+            "speedup": ms_exp / ms_tree,
+            "agreement_max_rel": agree, "agreement_tol": tol,
             "paper_context": "4.81-4.87x F/B/Grad end-to-end speedup, 8x H20-3e, BF16, "
                              "Ling-3.0-tiny (whole model, not this operator)"}
 
@@ -398,24 +548,33 @@ def main():
     H, d = cfg["H"], cfg["d"]
     el = 2 if cfg["dtype"] == "bf16" else 4
     C = plan.info["C"]
+    K = plan.info["n_rounds"]
     value = C / (ms * 1e-3)
-    alg, per_step, pass_bytes = algorithmic_bytes(plan, H, d, el)
+    pass_bytes, share = alg_bytes(plan, H, d, el)
+    step_bytes = pass_bytes["fwd"] + pass_bytes["state"] + pass_bytes["bwd"]
+    dbytes, per_step, dpass = design_bytes(plan, H, d, el)
     kstats = {}
+    ktot = sum(v[1] for v in kern.values())
     for name, (n, tot) in kern.items():
-        steps_seen = max(1, n // max(1, per_step.get(name, 1)))
-        b = alg.get(name, 0) / max(1, per_step.get(name, 1))   # per launch
         avg_ms = tot / n
-        kstats[name] = {"launches": n, "avg_ms": avg_ms,
-                        "share": tot / sum(v[1] for v in kern.values()),
-                        "alg_bytes_per_launch": b,
-                        "achieved_GBs": b / (avg_ms * 1e-3) / 1e9}
+        st = {"launches": n, "avg_ms": avg_ms, "share_of_time": tot / ktot}
+        if name in share:        # its own outputs' bytes, per launch (one launch per round)
+            b = share[name] / K
+            st.update(alg_bytes_per_launch=b, alg_GBs=b / (avg_ms * 1e-3) / 1e9,
+                      alg_frac=b / (avg_ms * 1e-3) / 1e9 / PEAK_HBM_GBS)
+        if name in dbytes and per_step.get(name):
+            b = dbytes[name] / per_step[name]
+            st.update(design_bytes_per_launch=b, design_GBs=b / (avg_ms * 1e-3) / 1e9)
+        kstats[name] = st
     dom = max(kstats, key=lambda k: kstats[k]["avg_ms"] * kstats[k]["launches"])
+    if dom not in share:
+        raise RuntimeError(f"dominant kernel {dom} has no algorithmic share")
     ds = kstats[dom]
     traffic = read_traffic(dom, WORKLOAD_KEY[args.config])
     flop_tok = H * (98304 + 245760 + 32768) * (d / 128) ** 2  # fwd + bwd + recompute state pass
     achieved_tflops = C * flop_tok / (ms * 1e-3) / 1e12
     peak_tf = PEAK_BF16_TFLOPS if el == 2 else PEAK_F32_TFLOPS
-    step_bytes = sum(alg.values())
+    step_gbs = step_bytes / (ms * 1e-3) / 1e9
     out = {
         "metric": "compact tokens/s, tree-packed linear-attn fwd+bwd; MFMA util % of peak",
         "value": value,
@@ -430,14 +589,18 @@ def main():
         "dtype": cfg["dtype"],
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "C": C, "S": plan.info["S"],
-                   "R": plan.info["R"], "rounds": plan.info["n_rounds"],
+                   "R": plan.info["R"], "rounds": K,
                    "sequences": plan.info["n_seq"], "H": H, "d": d, "chunk": 64},
         "roofline": {"bound": "hbm", "kernel": dom,
-                     "achieved": ds["achieved_GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": ds["achieved_GBs"] / PEAK_HBM_GBS,
-                     "traffic": traffic},
+                     "achieved": ds["alg_GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": ds["alg_frac"], "traffic": traffic,
+                     "alg_bytes_per_launch": ds["alg_bytes_per_launch"],
+                     "avg_launch_ms": ds["avg_ms"]},
+        "step_roofline": {"alg_GB": step_bytes / 1e9, "achieved_GBs": step_gbs,
+                          "hbm_frac": step_gbs / PEAK_HBM_GBS,
+                          "design_GB": sum(dbytes.values()) / 1e9,
+                          "design_over_alg": sum(dbytes.values()) / step_bytes},
         "mfma_util_pct": 100.0 * achieved_tflops / peak_tf,
-        "step_alg_GBs": step_bytes / (ms * 1e-3) / 1e9,
         "ms_median": float(np.median(step_ms)),
         "ms_p10": float(np.percentile(step_ms, 10)),
         "ms_p90": float(np.percentile(step_ms, 90)),
@@ -448,8 +611,8 @@ def main():
     }
     log("[bench] separate passes")
     passes = pass_times(runner, t, args.steps, args.warmup)
-    # per pass: algorithmic bytes and FLOPs (SURVEY counts per compact token:
-    # forward 98,304, backward 245,760, state pass 32,768 per head at d = 128)
+    # per pass: algorithmic bytes and FLOPs (per compact token and head at
+    # d = 128: forward 98,304, backward 245,760, state pass 32,768)
     fscale = H * (d / 128) ** 2
     work = {"fwd": (pass_bytes["fwd"], 98304 * fscale),
             "bwd": (pass_bytes["bwd"], 245760 * fscale),
@@ -468,8 +631,8 @@ def main():
         log("[bench] compact vs expanded (4 trees, ~32k compact tokens)")
         out["compact_vs_expanded"] = expanded_comparison(max(3, args.steps // 2), 2)
     if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle, four heads)")
-        out["cpu_baseline"] = cpu_baseline(forest, x, cfg)
+        log("[bench] cpu baseline (oracle, trajectory-wise recurrence)")
+        out["cpu_baseline"] = cpu_baseline(forest, x, cfg, budget_s=6.0)
     print(json.dumps(out), flush=True)
 
 

@@ -1,11 +1,11 @@
 """Turns rocprofv3 output of ``bench.py --steps-only`` into the short text
 summaries kept under ``profiles/``.
 
-    python -m paper_2608_28158_amd.profile_summary stats <kernel_stats.csv> <out.md> <command...>
-    python -m paper_2608_28158_amd.profile_summary traffic <fetch.csv> <write.csv> \\
+    python profile_summary.py stats <kernel_stats.csv> <out.md> <command...>
+    python profile_summary.py traffic <fetch.csv> <write.csv> \\
         <copy_fetch.csv> <copy_write.csv> <copy_mib> <kernel> <out.txt> <command...>
 
-    python -m paper_2608_28158_amd.profile_summary counters <out.md> <n_cu> <n_xcd> \\
+    python profile_summary.py counters <out.md> <n_cu> <n_xcd> \\
         <pass1.csv> [<pass2.csv> ...] -- <command...>
 
 The traffic summary scales FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by
@@ -24,7 +24,7 @@ import hashlib
 import os
 import sys
 
-ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+ROOT = os.path.dirname(os.path.abspath(__file__))
 
 
 def source_sha():
