@@ -1,0 +1,58 @@
+"""The host planner built with AddressSanitizer and UndefinedBehaviorSanitizer
+(host code only, g++), running the planner's own test files in a child
+process: the C ABI tests (bit-exact against the oracle planner on the
+figures, the workloads and random forests; argument validation) and the
+decoded device tables.  Any out-of-bounds access, use after free, signed
+overflow or other undefined behaviour aborts the child.
+
+The sanitized library links the planner, compiled here, with the HIP object
+the regular build left in _build (its device code is not instrumented and
+never runs here).
+"""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PKG = os.path.join(ROOT, "paper_2608_28158_amd")
+
+
+def _runtime(name):
+    out = subprocess.run(["g++", f"-print-file-name={name}"], capture_output=True, text=True)
+    path = out.stdout.strip()
+    return path if os.path.isabs(path) and os.path.exists(path) else None
+
+
+def test_planner_under_asan_and_ubsan(tmp_path):
+    hip_obj = os.path.join(PKG, "_build", "la.hip.o")
+    if shutil.which("g++") is None or not os.path.exists(hip_obj):
+        pytest.skip("needs g++ and the regular build's HIP object")
+    asan, ubsan = _runtime("libasan.so"), _runtime("libubsan.so")
+    if not asan or not ubsan:
+        pytest.skip("sanitizer runtimes not found")
+    san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
+    obj = str(tmp_path / "plan.o")
+    lib = str(tmp_path / "libharts_san.so")
+    subprocess.run(["g++", "-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "-fPIC"] + san +
+                   ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"), "-c",
+                    os.path.join(PKG, "csrc", "plan.cpp"), "-o", obj], check=True)
+    subprocess.run(["g++", "-shared"] + san + [obj, hip_obj, "-L/opt/rocm/lib", "-lamdhip64",
+                                               "-Wl,-rpath,/opt/rocm/lib", "-o", lib], check=True)
+    env = dict(os.environ, HARTS_LIB=lib, LD_PRELOAD=f"{asan}:{ubsan}",
+               ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
+               UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
+    code = ("import sys, pytest\n"
+            "from paper_2608_28158_amd import _lib\n"
+            f"assert _lib.LIB_PATH == {lib!r}\n"
+            "sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider', "
+            "'tests/test_abi_plan.py', 'tests/test_plan_tables.py']))\n")
+    res = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True,
+                         text=True, timeout=600)
+    out = res.stdout + res.stderr
+    print(out[-3000:])
+    assert res.returncode == 0, out[-3000:]
+    assert "AddressSanitizer" not in out and "runtime error" not in out
+    assert " passed" in out
