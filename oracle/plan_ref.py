@@ -1,16 +1,33 @@
-"""Reference minimum-call planner: Algorithm "minimum-call" of Sec. 3.3.
+"""Reference minimum-call planner (Sec. 3.3, Algorithm "minimum-call").
 
-Written from the paper's statement of the dynamic program (eqs. leaf-calls,
-tin, tpre with the early-start condition eq. early-start) and of the Recover
-procedure; plain recursive Python, no tricks.
+Written from the paper's definitions, in a structure of its own:
+
+* the minimum call counts of every subtree, T_pre and T_in, straight from
+  eqs. leaf-calls, tin and tpre with the early-start condition eq.
+  early-start (e_v < a_v + B), children visited in postorder;
+* recovery as a feasibility test against one deadline per tree: the tree's
+  rounds are 1 .. D with D = T_pre(root), and every segment of it must finish
+  by round D.  A segment v reached in round r continues its sequence with the
+  first child (in child order) whose own subtree still finishes by D when
+  continued in the same sequence, provided every other child, started as a
+  side branch in the earliest round its anchor state S_{b_v} allows, also
+  finishes by D.  (The printed procedure's round budgets K_round and K_side
+  are this deadline counted from r and from the side branches' start round.)
+
+A side branch starts in round r itself when v's entry anchor state was ready
+before round r and v crosses no chunk boundary (e_v < a_v + B), from v's
+sequence's own initial state; otherwise in round r + 1 from S_{b_v},
+requested from v's sequence.  The direct child inherits "ready" exactly in
+the first case: its entry state is then the same ready anchor state.
 
 Conventions where the paper leaves a choice (the library follows the same):
 
 * children are visited in ascending segment id ("a fixed child order");
-* sequences are created in Recover's order (the direct continuation is
-  recursed into before the side children are launched, side children in
-  child order), trees in ascending root id; sequence ids are assigned by a
-  stable sort of that creation order on the round number;
+* sequences are created in the order of a depth-first recovery that finishes
+  the direct continuation's subtree before launching a segment's side
+  branches, side branches in child order (each with its whole subtree), and
+  trees in ascending root id; sequence ids are a stable sort of that creation
+  order on the round number;
 * a side branch launched in the same round reuses its parent sequence's
   initial-state source; one launched in the next round consumes the boundary
   state S_{b_v} requested from the parent's sequence;
@@ -23,11 +40,15 @@ Conventions where the paper leaves a choice (the library follows the same):
 """
 from __future__ import annotations
 
-import sys
-
 import numpy as np
 
 from .forest import SegTree, anchor
+
+
+def early_start(t: SegTree, v: int, B: int) -> bool:
+    """eq. early-start: v ends before the chunk boundary after its entry
+    anchor a_v, so it produces no new boundary state (b_v = a_v)."""
+    return t.e[v] < anchor(t.s[v], B) + B
 
 
 def dp_calls(t: SegTree, B: int):
@@ -36,20 +57,15 @@ def dp_calls(t: SegTree, B: int):
     T_in = [0] * t.n
     for v in t.postorder():
         ch = t.kids[v]
-        if not ch:
+        if not ch:                                    # eq. leaf-calls
             T_pre[v] = T_in[v] = 1
             continue
-        best = None
-        for o in ch:
-            others = [T_pre[u] for u in ch if u != o]
-            h = max(others) if others else 0      # max of an empty set is 0
-            cand = max(T_in[o], 1 + h)
-            best = cand if best is None else min(best, cand)
-        T_in[v] = best
-        if t.e[v] < anchor(t.s[v], B) + B:        # early start (strict)
-            T_pre[v] = max(T_pre[u] for u in ch)
-        else:
-            T_pre[v] = T_in[v]
+        # eq. tin: the direct child o keeps the call; every other child
+        # waits one round for its anchor state (max over an empty set = 0)
+        T_in[v] = min(max(T_in[o], 1 + max([T_pre[u] for u in ch if u != o], default=0))
+                      for o in ch)
+        # eq. tpre
+        T_pre[v] = max(T_pre[u] for u in ch) if early_start(t, v, B) else T_in[v]
     return T_pre, T_in
 
 
@@ -79,47 +95,55 @@ def plan_ref(parent, seg_len, B: int):
         seqs.append(q)
         return q
 
-    def recover(v, ready, K, r, q):
-        q.chain.append(v)
-        seg_seq[v] = q
-        ch = t.kids[v]
-        if not ch:
-            return
-        same = ready and (t.e[v] < anchor(t.s[v], B) + B)
-        delta = 0 if same else 1
-        K_side = K - delta
-        need = {o: (T_pre[o] if same else T_in[o]) for o in ch}
-        f = sum(1 for u in ch if T_pre[u] > K_side)
-        o = None
-        for c in ch:
-            if need[c] <= K and f - (1 if T_pre[c] > K_side else 0) == 0:
-                o = c
+    def grow(q, first, ready, deadline, todo):
+        """Extend sequence q from segment `first` (entered with its anchor
+        state ready before q's round, or not) down its chain of direct
+        continuations; queue every side branch on `todo` so that the side
+        branches of deeper chain segments are launched first."""
+        v, r = first, q.round
+        launches = []
+        while True:
+            q.chain.append(v)
+            seg_seq[v] = q
+            ch = t.kids[v]
+            if not ch:
                 break
-        assert o is not None, "round budget infeasible"
-        recover(o, same, K, r, q)
-        b_v = anchor(t.e[v], B)
-        for u in ch:
-            if u == o:
-                continue
-            if same:
+            same_round = ready and early_start(t, v, B)
+            side_round = r if same_round else r + 1
+            # finishing by the deadline: a subtree entering round x with a
+            # count of T rounds ends in round x + T - 1
+            side_ok = [side_round + T_pre[u] - 1 <= deadline for u in ch]
+            direct = None
+            for o in ch:
+                need = T_pre[o] if same_round else T_in[o]
+                if r + need - 1 <= deadline and all(ok for u, ok in zip(ch, side_ok) if u != o):
+                    direct = o
+                    break
+            assert direct is not None, "no child meets the tree's deadline"
+            launches.append((v, same_round, side_round,
+                             [u for u in ch if u != direct]))
+            v, ready = direct, same_round
+        # deepest segment's side branches first; within a segment, child order
+        for v, same_round, side_round, sides in launches:
+            todo.extend((v, same_round, side_round, u) for u in reversed(sides))
+
+    K_tree = []
+    for ti, root in enumerate(t.roots):
+        D = T_pre[root]                  # the root's zero state is ready before round 1
+        K_tree.append(D)
+        todo = []
+        grow(new_seq(ti, 1, 0, ("tree", ti)), root, True, D, todo)
+        while todo:
+            v, same_round, side_round, u = todo.pop()
+            q = seg_seq[v]
+            b_v = anchor(t.e[v], B)
+            if same_round:               # b_v = a_v: the sequence's own initial state
                 assert b_v == q.anchor
-                qu = new_seq(q.tree, r, b_v, q.init)
+                qu = new_seq(ti, side_round, b_v, q.init)
             else:
                 requests.append((q, b_v))
-                qu = new_seq(q.tree, r + 1, b_v, ("slot", q, b_v))
-            recover(u, True, K_side, r + delta, qu)
-
-    old_limit = sys.getrecursionlimit()
-    sys.setrecursionlimit(max(old_limit, 4 * t.n + 1000))
-    try:
-        K_tree = []
-        for ti, root in enumerate(t.roots):
-            K_root = T_pre[root]
-            K_tree.append(K_root)
-            q0 = new_seq(ti, 1, 0, ("tree", ti))
-            recover(root, True, K_root, 1, q0)
-    finally:
-        sys.setrecursionlimit(old_limit)
+                qu = new_seq(ti, side_round, b_v, ("slot", q, b_v))
+            grow(qu, u, True, D, todo)
     K = max(K_tree)
 
     order = sorted(seqs, key=lambda q: (q.round, q.creation))
