@@ -407,7 +407,7 @@ def setup(idx):
     plan_times = []
     for _ in range(5):
         t0 = time.perf_counter()
-        plan = HartsPlan(forest.parent, forest.seg_len, 64)
+        plan = HartsPlan(forest.parent, forest.seg_len, 64, heads=cfg["H"])
         plan_times.append(time.perf_counter() - t0)
     phys = phys_index(forest.seg_len, plan["seg_row"])
     dt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
@@ -442,7 +442,7 @@ def expanded_comparison(steps, warmup):
         rows = np.concatenate([row0[w] + np.arange(forest.seg_len[w]) for w in reversed(path)])
         trajs.append(rows)
     lens = np.array([len(r) for r in trajs], np.int64)
-    eplan = HartsPlan(np.full(len(trajs), -1, np.int32), lens, 64)
+    eplan = HartsPlan(np.full(len(trajs), -1, np.int32), lens, 64, heads=cfg["H"])
     assert eplan.info["n_rounds"] == 1
     erows = np.concatenate(trajs)                       # canonical row of each expanded row
     ephys = phys_index(lens, eplan["seg_row"])          # expanded canonical -> physical

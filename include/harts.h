@@ -156,6 +156,23 @@ typedef struct harts_plan_arrays {
 
 int harts_plan_export(const harts_plan_t* plan, const harts_plan_arrays* dst);
 
+/* ------------------------------------------------------------------------
+ * harts_plan_set_blocks -- the work decomposition of the device tables.
+ * Each round's sequences are cut into blocks of consecutive chunks (at every
+ * requested boundary, and after at most block_chunks chunks); one workgroup
+ * runs one (block, head).  block_chunks is the largest of 64, 48, 32, 24,
+ * 16, 12, 8 that still yields min_blocks blocks in the round (8 if none
+ * does).  min_blocks = 0 chooses ceil(896 / H), i.e. about 896 (block, head)
+ * workgroups per round; a plan fresh from harts_plan is set for H = 16.
+ * Only the device descriptor image and the per-round block facts change:
+ * fetch harts_plan_get_info / harts_plan_round_info / harts_plan_blob again
+ * afterwards.  Results of the device calls do not depend on the blocking
+ * beyond floating-point summation order.
+ * Errors: HARTS_EINVAL (NULL plan, H < 1, min_blocks outside [0, 2^20]),
+ * HARTS_ENOMEM (host memory; the plan's device tables are then unusable).
+ * ---------------------------------------------------------------------- */
+int harts_plan_set_blocks(harts_plan_t* plan, int32_t H, int32_t min_blocks);
+
 /* Per-round launch facts (round is 0-based, < n_rounds). */
 typedef struct harts_round_info {
   int32_t n_seq;         /* sequences in the round                          */

@@ -20,7 +20,7 @@ HARTS_F32, HARTS_BF16 = 0, 1
 # Every symbol include/harts.h declares.
 EXPORTS = (
     "harts_last_error", "harts_plan", "harts_plan_free", "harts_plan_get_info",
-    "harts_plan_export", "harts_plan_round_info", "harts_plan_blob",
+    "harts_plan_export", "harts_plan_set_blocks", "harts_plan_round_info", "harts_plan_blob",
     "harts_la_fwd", "harts_la_fwd_noalloc", "harts_la_bwd", "harts_la_workspace_size",
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
     "harts_profile_begin", "harts_profile_end",
@@ -116,6 +116,8 @@ def lib():
     L.harts_plan_get_info.argtypes = [vp, C.POINTER(PlanInfo)]
     L.harts_plan_export.restype = C.c_int
     L.harts_plan_export.argtypes = [vp, C.POINTER(PlanArrays)]
+    L.harts_plan_set_blocks.restype = C.c_int
+    L.harts_plan_set_blocks.argtypes = [vp, i32, i32]
     L.harts_plan_round_info.restype = C.c_int
     L.harts_plan_round_info.argtypes = [vp, i32, C.POINTER(RoundInfo)]
     L.harts_plan_blob.restype = C.c_int

@@ -29,6 +29,22 @@ int64_t align_up(int64_t x) { return (x + kAlignWords - 1) / kAlignWords * kAlig
 
 inline int64_t anchor_of(int64_t p, int64_t B) { return (p / B) * B; }  // eq. resume-anchor
 
+}  // namespace
+
+// Block target of a round: enough blocks that the (block, head) work units
+// fill the GPU about 3.5 times over (896 workgroups: 56 blocks at 16 heads).
+// Larger blocks move fewer block states through HBM and start fewer
+// workgroups (each reads a start state before its first chunk); smaller
+// ones expose more workgroups.  56 blocks measured best on the 64k-token
+// agentic workload at 16 heads: 48-chunk blocks in its long-sequence round,
+// 1.777 ms per step against 1.797 ms with 16-chunk blocks (80 blocks).
+int32_t default_min_blocks(int32_t H) {
+  constexpr int32_t kTargetUnits = 56 * 16;
+  return std::max<int32_t>(1, (kTargetUnits + H - 1) / H);
+}
+
+namespace {
+
 struct Builder {
   int32_t n;
   int64_t B;
@@ -371,19 +387,10 @@ struct Builder {
 
   void build_blob() {
     harts_plan_s& p = *P;
+    p.blob.clear();
+    p.rounds.clear();
     const int32_t K = p.K;
-    // Target number of blocks per round (tuning knob).  Larger blocks move
-    // fewer block states through HBM and start fewer workgroups (each reads
-    // a start state before its first chunk), smaller ones expose more
-    // workgroups.  56 measured best on the 64k-token agentic workload at 16
-    // heads: 48-chunk blocks in its long-sequence round (59 blocks), 1.777 ms
-    // per step against 1.797 ms with 16-chunk blocks (target 80), in
-    // alternating runs.
-    int32_t min_blocks = 56;
-    if (const char* env = std::getenv("HARTS_MIN_BLOCKS")) {
-      const long x = std::strtol(env, nullptr, 10);
-      if (x >= 1 && x <= (1 << 20)) min_blocks = static_cast<int32_t>(x);
-    }
+    const int32_t min_blocks = p.min_blocks;
     int64_t off = 0;
     p.rounds.assign(K, RoundLayout{});
     p.n_chunks = 0;
@@ -550,6 +557,32 @@ struct Builder {
 
 using harts::set_error;
 
+extern "C" int harts_plan_set_blocks(harts_plan_t* p, int32_t H, int32_t min_blocks) {
+  if (!p || H < 1 || min_blocks < 0 || min_blocks > (1 << 20)) {
+    set_error("harts_plan_set_blocks: need a plan, H >= 1 and 0 <= min_blocks <= 2^20");
+    return HARTS_EINVAL;
+  }
+  const int32_t target = min_blocks ? min_blocks : harts::default_min_blocks(H);
+  if (target == p->min_blocks) return HARTS_OK;
+  const int32_t old = p->min_blocks;
+  try {
+    harts::Builder bld;
+    bld.n = p->n_seg;
+    bld.B = p->chunk;
+    bld.P = p;
+    p->min_blocks = target;
+    bld.build_blob();
+  } catch (const std::bad_alloc&) {
+    p->min_blocks = old;
+    set_error("harts_plan_set_blocks: out of host memory (the plan's device tables are gone)");
+    p->blob.clear();
+    p->rounds.clear();
+    return HARTS_ENOMEM;
+  }
+  set_error("");
+  return HARTS_OK;
+}
+
 extern "C" const char* harts_last_error(void) { return harts::g_last_error.c_str(); }
 
 extern "C" int harts_plan(int32_t n_seg, const int32_t* parent, const int64_t* seg_len,
@@ -572,6 +605,7 @@ extern "C" int harts_plan(int32_t n_seg, const int32_t* parent, const int64_t* s
     bld.P = p;
     p->n_seg = n_seg;
     p->chunk = chunk;
+    p->min_blocks = harts::default_min_blocks(16);
     if (!bld.children_and_positions()) { delete p; return HARTS_EINVAL; }
     bld.dynamic_program();
     if (!bld.recover() || !bld.finish()) { delete p; return HARTS_EINVAL; }

@@ -76,6 +76,7 @@ struct RoundLayout {
 struct harts_plan_s {
   int32_t n_seg = 0, n_trees = 0, n_leaves = 0, K = 0, n_seq = 0, n_slots = 0;
   int32_t n_bank = 0, chunk = 0;
+  int32_t min_blocks = 0;  // block target of the device tables (harts_plan_set_blocks)
   int64_t C = 0, S = 0, R = 0, n_chunks = 0;
 
   std::vector<int64_t> seg_start, seg_end, seg_row, seg_mult;

@@ -14,7 +14,10 @@ from . import _lib
 
 
 class HartsPlan:
-    def __init__(self, parent, seg_len, chunk: int = 64):
+    def __init__(self, parent, seg_len, chunk: int = 64, heads: int = 16, min_blocks: int = 0):
+        """Plan a forest (``harts_plan``) and cut its rounds into device
+        work blocks for ``heads`` heads (``harts_plan_set_blocks``; a
+        non-zero ``min_blocks`` overrides the head-count rule)."""
         L = _lib.lib()
         parent = np.ascontiguousarray(parent, dtype=np.int32)
         seg_len = np.ascontiguousarray(seg_len, dtype=np.int64)
@@ -27,6 +30,8 @@ class HartsPlan:
                                 int(chunk), C.byref(h)), "harts_plan")
         self._h = h
         self._L = L
+        _lib.check(L.harts_plan_set_blocks(h, int(heads), int(min_blocks)),
+                   "harts_plan_set_blocks")
         info = _lib.PlanInfo()
         _lib.check(L.harts_plan_get_info(h, C.byref(info)), "harts_plan_get_info")
         self.info = {n: getattr(info, n) for n, _ in _lib.PlanInfo._fields_}

@@ -187,3 +187,36 @@ def test_device_calls_reject_plans_beyond_the_row_limit(L):
         assert L.harts_la_workspace_size(p.handle, 0, 0, _lib.HARTS_BF16, 1, 64, 64, 0,
                                          C.byref(sz)) == rc
         p.close()
+
+
+def test_set_blocks_recuts_rounds_by_head_count(L):
+    """harts_plan_set_blocks: the largest block size (64, 48, ..., 8 chunks)
+    that yields min_blocks blocks, min_blocks = ceil(896 / H) by default;
+    the plan proper (rounds, sequences, rows) is untouched."""
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    f, _, _ = forest_for_config(2)
+    base = HartsPlan(f.parent, f.seg_len, 64)                  # set for 16 heads
+    seen = {}
+    for H, mb in ((16, 0), (32, 0), (8, 0), (16, 56), (16, 100000)):
+        p = HartsPlan(f.parent, f.seg_len, 64, heads=H, min_blocks=mb)
+        target = mb or -(-896 // H)
+        for r, rd in enumerate(p.rounds):
+            nc = rd["n_chunks"]
+            assert rd["block_chunks"] in (64, 48, 32, 24, 16, 12, 8)
+            assert rd["n_blk"] >= min(target, rd["n_blk"])
+            if rd["block_chunks"] != 8:
+                assert rd["n_blk"] >= target
+            assert rd["n_blk"] >= rd["n_seq"] and rd["n_blk"] <= nc
+        for key in ("seq_round", "seg_row", "replay_row", "seq_init_bank"):
+            assert np.array_equal(p[key], base[key])
+        seen[(H, mb)] = [rd["block_chunks"] for rd in p.rounds]
+        p.close()
+    assert seen[(16, 0)] == seen[(16, 56)]
+    assert seen[(16, 100000)] == [8] * len(seen[(16, 0)])
+    assert all(a >= b for a, b in zip(seen[(32, 0)], seen[(16, 0)]))
+    h = base.handle
+    assert L.harts_plan_set_blocks(h, 0, 0) == _lib.HARTS_EINVAL
+    assert L.harts_plan_set_blocks(h, 16, -1) == _lib.HARTS_EINVAL
+    assert L.harts_plan_set_blocks(None, 16, 0) == _lib.HARTS_EINVAL
+    base.close()

@@ -43,7 +43,7 @@ def test_tree_la_autograd_matches_oracle(dtype, d, recompute):
     print(f"[gpu] {label}", flush=True)
     r = np.random.default_rng(7 + d + recompute)
     x = draw_inputs(sum(SEG_LEN), 4, H, d, d, r, dtype, n_trees=1, s0_scale=0.3)
-    plan = HartsPlan(PARENT, SEG_LEN, 64)
+    plan = HartsPlan(PARENT, SEG_LEN, 64, heads=H)
     assert plan["n_rounds"] == 3
     phys = phys_index(SEG_LEN, plan["seg_row"])
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
@@ -78,22 +78,21 @@ def test_tree_la_autograd_matches_oracle(dtype, d, recompute):
 
 
 @pytest.mark.parametrize("dtype,H", [("f32", 2), ("bf16", 3)])
-def test_recompute_in_library_matches_saved_multiblock(dtype, H, monkeypatch):
+def test_recompute_in_library_matches_saved_multiblock(dtype, H):
     """Sequences of several blocks at d = 64 (8-chunk blocks), on a
     three-call forest: the backward that recomputes every round's block
     states inside harts_la_bwd gives the same bits as the backward reading
     the states its forward saved, and reruns are identical."""
-    monkeypatch.setenv("HARTS_MIN_BLOCKS", "100000")
     parent = [-1, 0, 0, 1, 1, 2, 2]
     seg_len = [1300, 700, 900, 610, 575, 333, 820]
     r = np.random.default_rng(300 + H)
     x = draw_inputs(sum(seg_len), 4, H, 64, 64, r, dtype, n_trees=1, s0_scale=0.3)
     print(f"[gpu] recompute vs saved, multi-block {dtype}", flush=True)
-    a, plan = run_gpu(parent, seg_len, x, H, 64, dtype, 0.125, recompute=False)
+    a, plan = run_gpu(parent, seg_len, x, H, 64, dtype, 0.125, recompute=False, min_blocks=100000)
     assert plan["n_rounds"] == 3
     assert any(rd["n_blk"] > rd["n_seq"] for rd in plan.rounds)
-    b, _ = run_gpu(parent, seg_len, x, H, 64, dtype, 0.125, recompute=True)
-    c, _ = run_gpu(parent, seg_len, x, H, 64, dtype, 0.125, recompute=True)
+    b, _ = run_gpu(parent, seg_len, x, H, 64, dtype, 0.125, recompute=True, min_blocks=100000)
+    c, _ = run_gpu(parent, seg_len, x, H, 64, dtype, 0.125, recompute=True, min_blocks=100000)
     for name in a:
         assert np.array_equal(a[name], b[name]), name
         assert np.array_equal(b[name], c[name]), name

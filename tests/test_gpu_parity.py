@@ -34,10 +34,11 @@ def _canon(t, phys):
     return t.float().cpu().numpy()[phys]
 
 
-def run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute=False, gather_init=False):
+def run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute=False, gather_init=False,
+            min_blocks=0):
     from paper_2608_28158_amd.plan import HartsPlan
     from paper_2608_28158_amd.tree_la import TreeLARunner
-    plan = HartsPlan(parent, seg_len, 64)
+    plan = HartsPlan(parent, seg_len, 64, heads=H, min_blocks=min_blocks)
     phys = phys_index(seg_len, plan["seg_row"])
     tdt = torch.float32 if dtype == "f32" else torch.bfloat16
     q, k, v = (_dev(x[n], phys, tdt) for n in ("q", "k", "v"))
@@ -56,11 +57,11 @@ def run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute=False, gather_init
     return out, plan
 
 
-def compare(parent, seg_len, x, H, d, dtype, heads=None, recompute=False, label=""):
+def compare(parent, seg_len, x, H, d, dtype, heads=None, recompute=False, label="", min_blocks=0):
     scale = d ** -0.5
     print(f"[gpu] {label} n_seg={len(parent)} C={int(np.sum(seg_len))} H={H} d={d} "
           f"{dtype} recompute={recompute}", flush=True)
-    got, plan = run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute)
+    got, plan = run_gpu(parent, seg_len, x, H, d, dtype, scale, recompute, min_blocks=min_blocks)
     hs = list(range(H)) if heads is None else list(heads)
     sl = lambda a: a[:, hs]
     ref = compact_fwd_bwd(parent, seg_len, 64, sl(x["q"]), sl(x["k"]), sl(x["v"]), sl(x["g"]),
@@ -122,7 +123,7 @@ def test_final_states_with_and_without_outputs():
         f, cfg, x = config_inputs(cfg_i, s0_scale=0.5)
         H, d = cfg["H"], cfg["d"]
         print(f"[gpu] config{cfg_i} final states with and without outputs", flush=True)
-        plan = HartsPlan(f.parent, f.seg_len, 64)
+        plan = HartsPlan(f.parent, f.seg_len, 64, heads=H)
         phys = phys_index(f.seg_len, plan["seg_row"])
         tdt = torch.float32 if dtype == "f32" else torch.bfloat16
         q, k, v = (_dev(x[n], phys, tdt) for n in ("q", "k", "v"))
@@ -194,21 +195,20 @@ def test_random_forests_bf16_d64():
 
 
 @pytest.mark.parametrize("dtype,H", [("f32", 2), ("bf16", 3)])
-def test_multiblock_sequences_d64(dtype, H, monkeypatch):
+def test_multiblock_sequences_d64(dtype, H):
     """Sequences of several blocks at d = 64 in both dtypes: block
     summaries, the local adjoints formed by the forward-order kernel, and
     both chains over blocks.  A 1,900-token root (30 chunks) with forks at
     unaligned offsets, cut into 8-chunk blocks (the planner's smallest, for
     a block target it cannot reach)."""
-    monkeypatch.setenv("HARTS_MIN_BLOCKS", "100000")
     parent = [-1, 0, 0, 1, 1]
     seg_len = [1900, 700, 333, 75, 610]
     r = np.random.default_rng(2024 + H)
     x = draw_inputs(sum(seg_len), 3, H, 64, 64, r, dtype, n_trees=1, s0_scale=0.3)
     from paper_2608_28158_amd.plan import HartsPlan
-    plan = HartsPlan(parent, seg_len, 64)
+    plan = HartsPlan(parent, seg_len, 64, heads=H, min_blocks=100000)
     assert plan.rounds[0]["block_chunks"] == 8 and plan.rounds[0]["n_blk"] > plan.rounds[0]["n_seq"]
-    compare(parent, seg_len, x, H, 64, dtype, label=f"multi-block {dtype}")
+    compare(parent, seg_len, x, H, 64, dtype, label=f"multi-block {dtype}", min_blocks=100000)
 
 
 def test_config1_spine_bf16_all_heads():
@@ -217,13 +217,12 @@ def test_config1_spine_bf16_all_heads():
 
 
 @pytest.mark.parametrize("min_blocks,sizes", [("1", "64"), ("12", "16 and 24"), ("16", "12")])
-def test_config1_block_sizes(min_blocks, sizes, monkeypatch):
-    """The same workload cut into blocks of other sizes (the planner's block
-    target, read when the plan is built) stays within tolerance."""
-    monkeypatch.setenv("HARTS_MIN_BLOCKS", min_blocks)
+def test_config1_block_sizes(min_blocks, sizes):
+    """The same workload cut into blocks of other sizes (the block target of
+    harts_plan_set_blocks) stays within tolerance."""
     f, cfg, x = config_inputs(1)
     compare(f.parent, f.seg_len, x, cfg["H"], cfg["d"], "bf16", heads=[0, 9],
-            label=f"config1 blocks of {sizes} chunks")
+            label=f"config1 blocks of {sizes} chunks", min_blocks=int(min_blocks))
 
 
 def test_config2_agentic_bf16_sampled_heads():

@@ -74,9 +74,9 @@ def random_k3_forests(seed, count, max_len):
     return out
 
 
-def run_case(parent, seg_len, H, d, dtype, seed, label, min_rounds=3):
+def run_case(parent, seg_len, H, d, dtype, seed, label, min_rounds=3, min_blocks=0):
     from paper_2608_28158_amd.plan import HartsPlan
-    plan = HartsPlan(parent, seg_len, 64)
+    plan = HartsPlan(parent, seg_len, 64, heads=H, min_blocks=min_blocks)
     chained, depth = handoff_depth(plan)
     print(f"[gpu] {label}: K={plan['n_rounds']} chained={chained} handoff depth={depth}",
           flush=True)
@@ -86,7 +86,7 @@ def run_case(parent, seg_len, H, d, dtype, seed, label, min_rounds=3):
     n_leaves = len([v for v in range(len(parent)) if v not in parent])
     x = draw_inputs(int(sum(seg_len)), n_leaves, H, d, d, r, dtype,
                     n_trees=list(parent).count(-1), s0_scale=0.3)
-    compare(parent, seg_len, x, H, d, dtype, label=label)
+    compare(parent, seg_len, x, H, d, dtype, label=label, min_blocks=min_blocks)
 
 
 BINARY = [(3, 10), (4, 11), (5, 12)]
@@ -132,16 +132,16 @@ def test_three_calls_with_forks_at_boundaries(seg_len):
 
 
 @pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
-def test_multiblock_chained_handoffs(dtype, d, monkeypatch):
+def test_multiblock_chained_handoffs(dtype, d):
     """Long segments cut into 8-chunk blocks: slot-initialised sequences of
     several blocks, with requested boundaries inside them (the adjoint chain
     injects dbank into a sequence that itself started from a slot)."""
-    monkeypatch.setenv("HARTS_MIN_BLOCKS", "100000")
     parent, seg_len = full_binary(4, np.random.default_rng(41), lo=300, hi=900)
     from paper_2608_28158_amd.plan import HartsPlan
-    plan = HartsPlan(parent, seg_len, 64)
+    plan = HartsPlan(parent, seg_len, 64, min_blocks=100000)
     assert any(r["n_blk"] > r["n_seq"] for r in plan.rounds[1:])
-    run_case(parent, seg_len, 2, d, dtype, 42, f"multi-block binary4 {dtype} d{d}", min_rounds=4)
+    run_case(parent, seg_len, 2, d, dtype, 42, f"multi-block binary4 {dtype} d{d}", min_rounds=4,
+             min_blocks=100000)
 
 
 def test_random_k3_forests_fp32():

@@ -71,15 +71,14 @@ CASES = [
 ]
 
 
-def test_noalloc_forward_matches_workspace_forward(L, monkeypatch):
+def test_noalloc_forward_matches_workspace_forward(L):
     from paper_2608_28158_amd import _lib
     from paper_2608_28158_amd.plan import HartsPlan
-    # short blocks: several blocks per sequence, so the scratch holds
-    # summaries and chained block-end states
-    monkeypatch.setenv("HARTS_MIN_BLOCKS", "100000")
     for i, (label, parent, seg_len, H, d, dtype) in enumerate(CASES):
         print(f"[gpu] noalloc call {i}: {label}", flush=True)
-        plan = HartsPlan(parent, seg_len, 64)
+        # short blocks: several blocks per sequence, so the scratch holds
+        # summaries and chained block-end states
+        plan = HartsPlan(parent, seg_len, 64, heads=H, min_blocks=100000)
         blob = plan.blob("cuda")
         code = _lib.HARTS_F32 if dtype == "f32" else _lib.HARTS_BF16
         n_leaves = plan["n_leaves"]
