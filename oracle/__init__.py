@@ -24,6 +24,9 @@ Contents (all float64 unless stated):
 * ``compact``     -- execution of plan_ref's rounds with the chunkwise form,
                      boundary-state handoffs (eq. chunkla-interface) and
                      gradients by reverse-mode differentiation of that program.
+* ``logprob``     -- compact-to-semantic log-probabilities and their gradient
+                     (eqs. mapped-logp, mapped-logp-grad), one log-softmax
+                     per semantic position.
 
 Recurrence reading used throughout (the paper prints only KDA's chunk update,
 eq. chunk-state): S_t = exp(g_t) S_{t-1} + k_t v_t^T and o_t = scale S_t^T q_t,
