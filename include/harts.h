@@ -346,6 +346,56 @@ int harts_replay_reduce(const harts_plan_t* plan, const void* d_blob,
                         float* dg, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Compact-to-semantic log-probabilities (Sec. 3.5, eqs. mapped-logp and
+ * mapped-logp-grad).  Vocabulary-wide work runs once per compact logit row;
+ * only scalar work runs per semantic position, and no S x V tensor exists.
+ *
+ * harts_semantic_map (host) -- the positions of the original batch and the
+ * rows that serve them.  Trajectories are taken by ascending leaf id (the
+ * order of harts_plan_arrays.leaf_seg), positions in trajectory order; the
+ * last position of every trajectory has no next token and is left out, so
+ * there are n_pos = S - n_leaves positions.
+ *   tokens   [C] token id of every compact row, physical row order.
+ *   m        [n_pos] out: physical row of position s (its logit row).
+ *   y        [n_pos] out: the token at position s + 1 of the same trajectory.
+ *   row_off  [C + 1] out, row_pos [n_pos] out: positions served by each
+ *            row, row c owning row_pos[row_off[c] .. row_off[c+1]), ordered
+ *            by (y, position).
+ * Linear in S.  Errors: HARTS_EINVAL (NULL, n_pos != S - n_leaves),
+ * HARTS_EUNSUPPORTED (C or n_pos >= 2^31), HARTS_ENOMEM.
+ *
+ * harts_logp_fwd (device) -- lse[c] = log sum_v exp z[c, v] for every row,
+ * then logp[s] = z[m[s], y[s]] - lse[m[s]] for every position.
+ *   logits   [C, V] row-major, HARTS_BF16 or HARTS_F32 (dtype), 16-byte
+ *            aligned; V a positive multiple of 8.
+ *   lse      [C] float32 out; logp [n_pos] float32 out.
+ *   An (m, y) pair outside [0, C) x [0, V) yields logp = NaN; nothing is
+ *   read out of bounds.
+ *
+ * harts_logp_bwd (device) -- for upstream gradients dlogp[s] (zero where
+ * the action mask drops a position):
+ *   row_g[c]        = sum of dlogp over the row's positions (float32 out);
+ *   dlogits[c, v]   = -row_g[c] softmax(z[c])_v
+ *                     + sum of dlogp[s] over the row's positions with y = v,
+ *   written (not added) for every row, in the logits' dtype, rounded once.
+ *   lse from harts_logp_fwd; row_off, row_pos, y from harts_semantic_map.
+ *   Deterministic: each row's sums run in its (y, position) order.
+ * Both: asynchronous on the stream; errors HARTS_EINVAL (NULL required
+ * pointer, negative sizes, misaligned logits), HARTS_EUNSUPPORTED (dtype,
+ * V), HARTS_EHIP.
+ * ---------------------------------------------------------------------- */
+int harts_semantic_map(const harts_plan_t* plan, const int32_t* tokens, int64_t n_pos,
+                       int32_t* m, int32_t* y, int64_t* row_off, int32_t* row_pos);
+
+int harts_logp_fwd(int32_t dtype, int64_t C, int64_t V, const void* logits, int64_t n_pos,
+                   const int32_t* m, const int32_t* y, float* lse, float* logp, void* stream);
+
+int harts_logp_bwd(int32_t dtype, int64_t C, int64_t V, const void* logits, const float* lse,
+                   int64_t n_pos, const int64_t* row_off, const int32_t* row_pos,
+                   const int32_t* y, const float* dlogp, float* row_g, void* dlogits,
+                   void* stream);
+
+/* ------------------------------------------------------------------------
  * Kernel timing (measurement support; not part of the method).  Between
  * harts_profile_begin and harts_profile_end every kernel the library
  * launches is bracketed by a pair of HIP events recorded on its own launch

@@ -23,6 +23,7 @@ EXPORTS = (
     "harts_plan_export", "harts_plan_set_blocks", "harts_plan_round_info", "harts_plan_blob",
     "harts_la_fwd", "harts_la_fwd_noalloc", "harts_la_bwd", "harts_la_workspace_size",
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
+    "harts_semantic_map", "harts_logp_fwd", "harts_logp_bwd",
     "harts_profile_begin", "harts_profile_end",
 )
 
@@ -142,6 +143,12 @@ def lib():
     L.harts_replay_reduce.restype = C.c_int
     L.harts_replay_reduce.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp,
                                       vp, vp]
+    L.harts_semantic_map.restype = C.c_int
+    L.harts_semantic_map.argtypes = [vp, vp, i64, vp, vp, vp, vp]
+    L.harts_logp_fwd.restype = C.c_int
+    L.harts_logp_fwd.argtypes = [i32, i64, i64, vp, i64, vp, vp, vp, vp, vp]
+    L.harts_logp_bwd.restype = C.c_int
+    L.harts_logp_bwd.argtypes = [i32, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp]
     L.harts_profile_begin.restype = C.c_int
     L.harts_profile_begin.argtypes = []
     L.harts_profile_end.restype = C.c_int

@@ -610,6 +610,7 @@ extern "C" int harts_plan(int32_t n_seg, const int32_t* parent, const int64_t* s
     bld.dynamic_program();
     if (!bld.recover() || !bld.finish()) { delete p; return HARTS_EINVAL; }
     bld.build_blob();
+    p->parent.assign(parent, parent + n_seg);
   } catch (const std::bad_alloc&) {
     delete p;
     set_error("harts_plan: out of host memory");

@@ -79,6 +79,7 @@ struct harts_plan_s {
   int32_t min_blocks = 0;  // block target of the device tables (harts_plan_set_blocks)
   int64_t C = 0, S = 0, R = 0, n_chunks = 0;
 
+  std::vector<int32_t> parent;  // the forest as given (-1 marks a root)
   std::vector<int64_t> seg_start, seg_end, seg_row, seg_mult;
   std::vector<int32_t> seg_seq, seg_tpre, seg_tin, seg_tree, leaf_seg;
   std::vector<int32_t> tree_calls, round_seq_off;

@@ -1,13 +1,14 @@
-"""The host planner built with AddressSanitizer and UndefinedBehaviorSanitizer
-(host code only, g++), running the planner's own test files in a child
-process: the C ABI tests (bit-exact against the oracle planner on the
-figures, the workloads and random forests; argument validation) and the
-decoded device tables.  Any out-of-bounds access, use after free, signed
-overflow or other undefined behaviour aborts the child.
+"""The host C++ of the library (the planner and the semantic map) built with
+AddressSanitizer and UndefinedBehaviorSanitizer (host code only, g++),
+running their test files in a child process: the C ABI tests (bit-exact
+against the oracle planner on the figures, the workloads and random forests;
+argument validation), the decoded device tables and the semantic map.  Any
+out-of-bounds access, use after free, signed overflow or other undefined
+behaviour aborts the child.
 
-The sanitized library links the planner, compiled here, with the HIP object
-the regular build left in _build (its device code is not instrumented and
-never runs here).
+The sanitized library links the host sources, compiled here, with the HIP
+objects the regular build left in _build (their device code is not
+instrumented and never runs here).
 """
 import os
 import shutil
@@ -26,21 +27,29 @@ def _runtime(name):
     return path if os.path.isabs(path) and os.path.exists(path) else None
 
 
+HOST_SOURCES = ("plan.cpp", "semantic.cpp")
+HIP_OBJECTS = ("la.hip.o", "logp.hip.o")
+
+
 def test_planner_under_asan_and_ubsan(tmp_path):
-    hip_obj = os.path.join(PKG, "_build", "la.hip.o")
-    if shutil.which("g++") is None or not os.path.exists(hip_obj):
-        pytest.skip("needs g++ and the regular build's HIP object")
+    hip_objs = [os.path.join(PKG, "_build", o) for o in HIP_OBJECTS]
+    if shutil.which("g++") is None or not all(os.path.exists(o) for o in hip_objs):
+        pytest.skip("needs g++ and the regular build's HIP objects")
     asan, ubsan = _runtime("libasan.so"), _runtime("libubsan.so")
     if not asan or not ubsan:
         pytest.skip("sanitizer runtimes not found")
     san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
-    obj = str(tmp_path / "plan.o")
+    objs = []
+    for src in HOST_SOURCES:
+        obj = str(tmp_path / (src + ".o"))
+        subprocess.run(["g++", "-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "-fPIC"] +
+                       san + ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
+                              "-c", os.path.join(PKG, "csrc", src), "-o", obj], check=True)
+        objs.append(obj)
     lib = str(tmp_path / "libharts_san.so")
-    subprocess.run(["g++", "-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "-fPIC"] + san +
-                   ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"), "-c",
-                    os.path.join(PKG, "csrc", "plan.cpp"), "-o", obj], check=True)
-    subprocess.run(["g++", "-shared"] + san + [obj, hip_obj, "-L/opt/rocm/lib", "-lamdhip64",
-                                               "-Wl,-rpath,/opt/rocm/lib", "-o", lib], check=True)
+    subprocess.run(["g++", "-shared"] + san + objs + hip_objs +
+                   ["-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib", "-o", lib],
+                   check=True)
     env = dict(os.environ, HARTS_LIB=lib, LD_PRELOAD=f"{asan}:{ubsan}",
                ASAN_OPTIONS="detect_leaks=0:abort_on_error=1",
                UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
@@ -48,7 +57,8 @@ def test_planner_under_asan_and_ubsan(tmp_path):
             "from paper_2608_28158_amd import _lib\n"
             f"assert _lib.LIB_PATH == {lib!r}\n"
             "sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider', "
-            "'tests/test_abi_plan.py', 'tests/test_plan_tables.py']))\n")
+            "'tests/test_abi_plan.py', 'tests/test_plan_tables.py', "
+            "'tests/test_semantic_map.py']))\n")
     res = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True,
                          text=True, timeout=600)
     out = res.stdout + res.stderr
