@@ -52,9 +52,10 @@ def log(*a):
 WORKLOAD_KEY = {1: "spine16k", 2: "agentic64k", 3: "agentic128k"}
 
 
-def la_source_sha():
+def la_source_sha(kernel=None):
+    names = ("logp.hip",) if kernel and kernel.startswith("k_logp") else ("la.hip", "la_common.hpp")
     h = hashlib.sha256()
-    for name in ("la.hip", "la_common.hpp"):
+    for name in names:
         with open(os.path.join(ROOT, "paper_2608_28158_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -239,7 +240,7 @@ def read_traffic(kernel, workload_key):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("source_sha") != la_source_sha():
+    if vals.get("source_sha") != la_source_sha(kernel):
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -505,6 +506,118 @@ def expanded_comparison(steps, warmup):
                              "Ling-3.0-tiny (whole model, not this operator)"}
 
 
+LOGP_V = 157184        # the paper's vocabulary (bf16 logits)
+
+
+def logp_measurement(steps, warmup, profile_only=False):
+    """Compact-to-semantic log-probabilities on the same 64k-token
+    microbatch: 68,161 compact logit rows x 157,184 bf16 logits (seeded
+    N(0, 4) on the device), every nonterminal semantic position; forward
+    (row log-sum-exp, target gather) and backward (row sums, softmax
+    gradient rows, target columns) timed separately with events on the
+    launch stream.  Algorithmic bytes: the forward reads the logits once,
+    the backward reads them once and writes dlogits once; per row and per
+    position only scalars move (counted)."""
+    import ctypes as C
+    import torch
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    from workloads import forest_for_config
+    L = _lib.lib()
+    f, _, cfg = forest_for_config(2)
+    t0 = time.perf_counter()
+    plan = HartsPlan(f.parent, f.seg_len, 64, heads=cfg["H"])
+    Cn, V = f.n_rows, LOGP_V
+    rng = np.random.default_rng(42)
+    tok = rng.integers(0, V, size=Cn).astype(np.int32)          # physical row order
+    n_pos = plan["S"] - plan["n_leaves"]
+    m = np.zeros(n_pos, np.int32)
+    y = np.zeros(n_pos, np.int32)
+    off = np.zeros(Cn + 1, np.int64)
+    pos = np.zeros(n_pos, np.int32)
+    t1 = time.perf_counter()
+    _lib.check(L.harts_semantic_map(plan.handle, tok.ctypes.data, n_pos, m.ctypes.data,
+                                    y.ctypes.data, off.ctypes.data, pos.ctypes.data),
+               "harts_semantic_map")
+    map_ms = (time.perf_counter() - t1) * 1e3
+    g = (rng.standard_normal(n_pos) * (rng.random(n_pos) < 0.7)).astype(np.float32)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    md, yd, offd, posd, gd = dev(m), dev(y), dev(off), dev(pos), dev(g)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(42)
+    z = torch.empty((Cn, V), dtype=torch.bfloat16, device="cuda")
+    for i in range(0, Cn, 4096):
+        n = min(4096, Cn - i)
+        z[i:i + n] = torch.randn((n, V), device="cuda", generator=gen).mul_(2.0)
+    dz = torch.empty_like(z)
+    lse = torch.empty(Cn, dtype=torch.float32, device="cuda")
+    logp = torch.empty(n_pos, dtype=torch.float32, device="cuda")
+    row_g = torch.empty(Cn, dtype=torch.float32, device="cuda")
+    P = lambda t: C.c_void_p(t.data_ptr())
+    stream = torch.cuda.current_stream()
+    st = C.c_void_p(stream.cuda_stream)
+    code = _lib.HARTS_BF16
+
+    def fwd():
+        _lib.check(L.harts_logp_fwd(code, Cn, V, P(z), n_pos, P(md), P(yd), P(lse), P(logp), st),
+                   "harts_logp_fwd")
+
+    def bwd():
+        _lib.check(L.harts_logp_bwd(code, Cn, V, P(z), P(lse), n_pos, P(offd), P(posd), P(yd),
+                                    P(gd), P(row_g), P(dz), st), "harts_logp_bwd")
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(steps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / steps
+
+    ms_f = timed(fwd)
+    ms_b = timed(bwd)
+    if profile_only:
+        return None
+    el = 2
+    by_f = Cn * V * el + Cn * 4 + n_pos * (4 + 4 + el + 4 + 4)
+    by_b = 2 * Cn * V * el + Cn * (8 + 4 + 4 + 4) + n_pos * (4 + 4 + 4) + n_pos * (el * 2 + 4)
+    out = {"workload": f"64k-token agentic microbatch: {Cn} compact logit rows x {V} bf16 "
+                       f"logits, {n_pos} semantic positions",
+           "C": Cn, "V": V, "positions": n_pos,
+           "fwd_ms": ms_f, "bwd_ms": ms_b,
+           "fwd": {"alg_GB": by_f / 1e9, "achieved_GBs": by_f / (ms_f * 1e-3) / 1e9,
+                   "hbm_frac": by_f / (ms_f * 1e-3) / 1e9 / PEAK_HBM_GBS},
+           "bwd": {"alg_GB": by_b / 1e9, "achieved_GBs": by_b / (ms_b * 1e-3) / 1e9,
+                   "hbm_frac": by_b / (ms_b * 1e-3) / 1e9 / PEAK_HBM_GBS},
+           "semantic_positions_per_s_fwd_bwd": n_pos / ((ms_f + ms_b) * 1e-3),
+           "traffic_k_logp_lse": read_traffic("k_logp_lse", "agentic64k_v157184"),
+           "traffic_k_logp_grad": read_traffic("k_logp_grad", "agentic64k_v157184"),
+           "map_ms": map_ms, "plan_ms": (t1 - t0) * 1e3}
+    # the oracle's one log-softmax per semantic position (fp64), timed on a
+    # sample of positions and scaled to all of them
+    from oracle.logprob import logp_bwd, logp_fwd
+    k = 1024
+    sel = rng.choice(n_pos, k, replace=False)
+    rows = z[torch.from_numpy(m[sel]).cuda().long()].float().cpu().numpy()
+    loc = np.arange(k)
+    t2 = time.perf_counter()
+    logp_fwd(rows, loc, y[sel])
+    logp_bwd(rows, loc, y[sel], g[sel].astype(np.float64))
+    cpu_s = time.perf_counter() - t2
+    out["cpu_baseline"] = {"value": k / cpu_s, "unit": "semantic positions/s", "cores": 1,
+                           "kind": "oracle",
+                           "sample": f"{k} random positions of the same microbatch, forward + "
+                                     f"backward, one fp64 log-softmax over {V} logits per "
+                                     f"position ({cpu_s:.1f} s)"}
+    del z, dz
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -513,8 +626,11 @@ def main():
     ap.add_argument("--config", type=int, default=2, choices=(1, 2, 3))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-expanded", action="store_true")
+    ap.add_argument("--no-logp", action="store_true")
     ap.add_argument("--steps-only", action="store_true",
                     help="run the timed steps only (for profiler runs)")
+    ap.add_argument("--logp-only", action="store_true",
+                    help="run the timed log-probability calls only (for profiler runs)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run a plain device copy of this many MiB (counter scale)")
     args = ap.parse_args()
@@ -533,6 +649,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         log(f"copy probe: {args.copy_probe_mib} MiB read + written, 5 launches")
+        return
+    if args.logp_only:
+        logp_measurement(args.steps, args.warmup, profile_only=True)
+        log("[bench] logp calls done")
         return
     log(f"[bench] config {args.config}: building workload")
     forest, cfg, x, plan, t, runner, plan_s = setup(args.config)
@@ -630,6 +750,9 @@ def main():
     if not args.no_expanded:
         log("[bench] compact vs expanded (4 trees, ~32k compact tokens)")
         out["compact_vs_expanded"] = expanded_comparison(max(3, args.steps // 2), 2)
+    if not args.no_logp:
+        log("[bench] compact-to-semantic log-probabilities (157,184-token vocabulary)")
+        out["logp"] = logp_measurement(args.steps, args.warmup)
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle, trajectory-wise recurrence)")
         out["cpu_baseline"] = cpu_baseline(forest, x, cfg, budget_s=6.0)

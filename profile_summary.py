@@ -27,9 +27,17 @@ import sys
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
 
-def source_sha():
+def sources_of(kernel=None):
+    """The source files a kernel is built from (the linear-attention kernels
+    by default)."""
+    if kernel and kernel.startswith("k_logp"):
+        return ("logp.hip",)
+    return ("la.hip", "la_common.hpp")
+
+
+def source_sha(kernel=None):
     h = hashlib.sha256()
-    for name in ("la.hip", "la_common.hpp"):
+    for name in sources_of(kernel):
         with open(os.path.join(ROOT, "paper_2608_28158_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -39,7 +47,8 @@ def short(name):
     n = name.split("(")[0]
     for key in ("k_bwd_revorder", "k_bwd_fwdorder", "k_blocksum", "k_fwd_blockscan",
                 "k_fwd_block", "k_bwd_blockscan", "k_dg_carry", "k_gather", "k_scatter_add",
-                "k_replay_reduce"):
+                "k_replay_reduce", "k_logp_lse", "k_logp_gather", "k_logp_rowsum",
+                "k_logp_grad", "k_logp_onehot"):
         if key in n:
             return key
     return n.replace("void ", "")[:48]
@@ -49,7 +58,8 @@ def stats(src, out, cmd):
     rows = list(csv.DictReader(open(src)))
     tot = sum(float(r["TotalDurationNs"]) for r in rows)
     lines = ["# rocprofv3 kernel statistics", "", "Command:", "", "    " + " ".join(cmd), "",
-             f"Kernel source hash: {source_sha()}", "",
+             f"Kernel source hashes: la.hip + la_common.hpp {source_sha()}, "
+             f"logp.hip {source_sha('k_logp')}", "",
              "| kernel | calls | total ms | avg us | min us | max us | share |",
              "|---|---|---|---|---|---|---|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
@@ -72,6 +82,8 @@ def per_kernel(path, counter):
 
 
 def traffic(fetch, write, cfetch, cwrite, copy_mib, kernel, out, cmd):
+    """HBM bytes per dispatch of one kernel, FETCH_SIZE and WRITE_SIZE each
+    scaled by what it reads for a plain copy of copy_mib MiB."""
     f, w = per_kernel(fetch, "FETCH_SIZE"), per_kernel(write, "WRITE_SIZE")
     cf = max(v for k, v in per_kernel(cfetch, "FETCH_SIZE").items() if "copy" in k.lower())
     cw = max(v for k, v in per_kernel(cwrite, "WRITE_SIZE").items() if "copy" in k.lower())
@@ -85,7 +97,8 @@ def traffic(fetch, write, cfetch, cwrite, copy_mib, kernel, out, cmd):
              f"fetch_kib_per_launch: {f[kernel]:.0f}",
              f"write_kib_per_launch: {w[kernel]:.0f}",
              f"hbm_bytes_per_launch: {hbm:.0f}",
-             f"source_sha: {source_sha()}"]
+             f"sources: {' + '.join(sources_of(kernel))}",
+             f"source_sha: {source_sha(kernel)}"]
     open(out, "w").write("\n".join(lines) + "\n")
 
 
