@@ -24,6 +24,10 @@ Contents (all float64 unless stated):
 * ``compact``     -- execution of plan_ref's rounds with the chunkwise form,
                      boundary-state handoffs (eq. chunkla-interface) and
                      gradients by reverse-mode differentiation of that program.
+* ``mbplan``      -- prefix-aware microbatch and data-parallel planning
+                     (Sec. 3.2): compact-trie work, natural partition, exact
+                     contiguous DP, evolution, trie-aware greedy, refinement,
+                     replica/slot assignment and the lexicographic choice.
 * ``logprob``     -- compact-to-semantic log-probabilities and their gradient
                      (eqs. mapped-logp, mapped-logp-grad), one log-softmax
                      per semantic position.
