@@ -618,6 +618,59 @@ def logp_measurement(steps, warmup, profile_only=False):
     return out
 
 
+def mbplan_measurement(D=4, T=65536):
+    """Prefix-aware microbatch/DP planning at the paper's scale: a seeded
+    batch of 215 agentic rollout trees at full length (about 1,600
+    trajectories, 45 M trajectory tokens, 8.5 M compact), capacity 65,536
+    and DP degree 4; trajectories longer than the capacity cannot be
+    scheduled and are dropped.  The oracle (plain Python) is timed on the
+    first 48 trajectories, next to the library on the same sample."""
+    import ctypes as C
+    from oracle.mbplan import plan_microbatches
+    from paper_2608_28158_amd import _lib
+    from workloads import agentic_forest, trajectory_tokens
+    L = _lib.lib()
+    f, rng = agentic_forest(11, 215, 1.0, 8_000_000, tol=0.1)
+    all_t = trajectory_tokens(f, rng)
+    trajs = [t for t in all_t if len(t) <= T]
+
+    def run(ts):
+        N = len(ts)
+        off = np.zeros(N + 1, np.int64)
+        off[1:] = np.cumsum([len(t) for t in ts])
+        tok = np.concatenate(ts).astype(np.int32)
+        outs = [np.zeros(N, np.int32) for _ in range(3)] + [np.zeros(N, np.int64)]
+        res = _lib.MbResult()
+        t0 = time.perf_counter()
+        _lib.check(L.harts_mb_plan(N, off.ctypes.data, tok.ctypes.data, D, T, 0,
+                                   *[o.ctypes.data for o in outs], C.byref(res)), "harts_mb_plan")
+        return time.perf_counter() - t0, res
+
+    times = []
+    for _ in range(3):
+        dt, res = run(trajs)
+        times.append(dt)
+    raw = sum(len(t) for t in trajs)
+    sample = [list(map(int, t)) for t in trajs[:48]]
+    dt_lib_s, res_s = run([np.asarray(t, np.int32) for t in sample])
+    t0 = time.perf_counter()
+    ref = plan_microbatches(sample, D, T)
+    dt_orc = time.perf_counter() - t0
+    assert ref["J"] == (res_s.work_total, res_s.slot_critical, res_s.replica_max)
+    return {"workload": f"{len(trajs)} trajectories of 215 agentic rollout trees "
+                        f"({len(all_t) - len(trajs)} above the capacity dropped), "
+                        f"{raw} trajectory tokens, T={T}, D={D}",
+            "plan_ms": float(np.median(times)) * 1e3, "K": res.K, "natural_K": res.natural_K,
+            "J": [res.work_total, res.slot_critical, res.replica_max],
+            "trie_work_one_microbatch": res.trie_work,
+            "raw_over_compact": raw / res.work_total,
+            "cpu_baseline": {"value": 48 / dt_orc, "unit": "trajectories planned/s", "cores": 1,
+                             "kind": "oracle",
+                             "sample": f"first 48 trajectories, {dt_orc:.2f} s; the library plans "
+                                       f"the same sample in {dt_lib_s * 1e3:.2f} ms with the "
+                                       f"same J"}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -627,6 +680,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-expanded", action="store_true")
     ap.add_argument("--no-logp", action="store_true")
+    ap.add_argument("--no-mbplan", action="store_true")
     ap.add_argument("--steps-only", action="store_true",
                     help="run the timed steps only (for profiler runs)")
     ap.add_argument("--logp-only", action="store_true",
@@ -753,6 +807,9 @@ def main():
     if not args.no_logp:
         log("[bench] compact-to-semantic log-probabilities (157,184-token vocabulary)")
         out["logp"] = logp_measurement(args.steps, args.warmup)
+    if not args.no_mbplan:
+        log("[bench] prefix-aware microbatch planning (host)")
+        out["mb_plan"] = mbplan_measurement()
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle, trajectory-wise recurrence)")
         out["cpu_baseline"] = cpu_baseline(forest, x, cfg, budget_s=6.0)

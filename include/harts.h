@@ -346,6 +346,48 @@ int harts_replay_reduce(const harts_plan_t* plan, const void* d_blob,
                         float* dg, void* stream);
 
 /* ------------------------------------------------------------------------
+ * harts_mb_plan -- prefix-aware microbatch and data-parallel planning
+ * (Sec. 3.2; eqs. prefix-plan-objective, compact-trie-cost,
+ * cut-prefix-loss, k-lower-bound, k-search-range, contiguous-dp,
+ * greedy-insertion-delta).  Host only.
+ *
+ * Groups N trajectories into K microbatches (K a multiple of D, exactly K/D
+ * per DP replica, each microbatch's compact-trie work <= T) and orders them
+ * into K/D slots, minimising J = (total compact work, sum over slots of the
+ * slot's heaviest microbatch, heaviest replica's total) lexicographically
+ * over the candidates it generates: the exact minimum-work contiguous
+ * partitions (in lexicographic order) for every K of the search range when
+ * N <= exact_max, otherwise merge/split evolutions of the natural partition
+ * at up to 32 sampled K; and the best trie-aware greedy plan; refined by
+ * boundary moves and sparse repair within 8 lexicographic positions.
+ *   n_traj     N >= D trajectories; trajectory i is
+ *              tokens[tok_off[i] .. tok_off[i+1]), 1 <= length <= T.
+ *   D, T       DP degree >= 1; microbatch capacity in compact tokens >= 1.
+ *   exact_max  exact-search threshold; 0 means the paper's 512.
+ *   group      [N] out: microbatch of every trajectory (0 .. K-1).
+ *   mb_replica, mb_slot, mb_work  [N] out (first K entries): replica, slot
+ *              and compact work of every microbatch.
+ *   result     out: K, the natural partition's size, J and the work of the
+ *              whole batch as one trie.
+ * Ties are broken by the earlier candidate, the smaller index or the
+ * smaller lexicographic rank at every step (deterministic).  Errors:
+ * HARTS_EINVAL (NULL, D < 1, T < 1, N < D, an empty trajectory or one above
+ * T, no feasible plan), HARTS_ENOMEM.
+ * ---------------------------------------------------------------------- */
+typedef struct harts_mb_result {
+  int32_t K;              /* microbatches in the plan                          */
+  int32_t natural_K;      /* microbatches of the natural partition            */
+  int64_t work_total;     /* J[0]: summed compact work                        */
+  int64_t slot_critical;  /* J[1]: sum over slots of the heaviest microbatch  */
+  int64_t replica_max;    /* J[2]: heaviest replica's summed work             */
+  int64_t trie_work;      /* G: compact work of all trajectories as one trie  */
+} harts_mb_result;
+
+int harts_mb_plan(int32_t n_traj, const int64_t* tok_off, const int32_t* tokens, int32_t D,
+                  int64_t T, int32_t exact_max, int32_t* group, int32_t* mb_replica,
+                  int32_t* mb_slot, int64_t* mb_work, harts_mb_result* result);
+
+/* ------------------------------------------------------------------------
  * Compact-to-semantic log-probabilities (Sec. 3.5, eqs. mapped-logp and
  * mapped-logp-grad).  Vocabulary-wide work runs once per compact logit row;
  * only scalar work runs per semantic position, and no S x V tensor exists.

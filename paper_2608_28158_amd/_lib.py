@@ -23,7 +23,7 @@ EXPORTS = (
     "harts_plan_export", "harts_plan_set_blocks", "harts_plan_round_info", "harts_plan_blob",
     "harts_la_fwd", "harts_la_fwd_noalloc", "harts_la_bwd", "harts_la_workspace_size",
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
-    "harts_semantic_map", "harts_logp_fwd", "harts_logp_bwd",
+    "harts_semantic_map", "harts_logp_fwd", "harts_logp_bwd", "harts_mb_plan",
     "harts_profile_begin", "harts_profile_end",
 )
 
@@ -80,6 +80,12 @@ class RoundInfo(C.Structure):
         (n, C.c_int64) for n in ("n_chunks", "n_rows", "n_own", "n_replay",
                                  "own_row_begin", "init_idx_off", "seq_tab_off",
                                  "blk_tab_off", "launch_off")]
+
+
+class MbResult(C.Structure):
+    _fields_ = [("K", C.c_int32), ("natural_K", C.c_int32), ("work_total", C.c_int64),
+                ("slot_critical", C.c_int64), ("replica_max", C.c_int64),
+                ("trie_work", C.c_int64)]
 
 
 class KernelTime(C.Structure):
@@ -149,6 +155,8 @@ def lib():
     L.harts_logp_fwd.argtypes = [i32, i64, i64, vp, i64, vp, vp, vp, vp, vp]
     L.harts_logp_bwd.restype = C.c_int
     L.harts_logp_bwd.argtypes = [i32, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp]
+    L.harts_mb_plan.restype = C.c_int
+    L.harts_mb_plan.argtypes = [i32, vp, vp, i32, i64, i32, vp, vp, vp, vp, C.POINTER(MbResult)]
     L.harts_profile_begin.restype = C.c_int
     L.harts_profile_begin.argtypes = []
     L.harts_profile_end.restype = C.c_int

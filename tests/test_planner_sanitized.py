@@ -1,4 +1,4 @@
-"""The host C++ of the library (the planner and the semantic map) built with
+"""The host C++ of the library (the planners and the semantic map) built with
 AddressSanitizer and UndefinedBehaviorSanitizer (host code only, g++),
 running their test files in a child process: the C ABI tests (bit-exact
 against the oracle planner on the figures, the workloads and random forests;
@@ -27,7 +27,7 @@ def _runtime(name):
     return path if os.path.isabs(path) and os.path.exists(path) else None
 
 
-HOST_SOURCES = ("plan.cpp", "semantic.cpp")
+HOST_SOURCES = ("plan.cpp", "semantic.cpp", "mbplan.cpp")
 HIP_OBJECTS = ("la.hip.o", "logp.hip.o")
 
 
@@ -58,7 +58,7 @@ def test_planner_under_asan_and_ubsan(tmp_path):
             f"assert _lib.LIB_PATH == {lib!r}\n"
             "sys.exit(pytest.main(['-q', '-x', '-p', 'no:cacheprovider', "
             "'tests/test_abi_plan.py', 'tests/test_plan_tables.py', "
-            "'tests/test_semantic_map.py']))\n")
+            "'tests/test_semantic_map.py', 'tests/test_abi_mbplan.py']))\n")
     res = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True,
                          text=True, timeout=600)
     out = res.stdout + res.stderr

@@ -11,5 +11,6 @@ from .trees import (  # noqa: F401
     agentic_forest,
     forest_for_config,
     CONFIGS,
+    trajectory_tokens,
 )
 from .tensors import config_inputs, draw_inputs, to_bf16_roundtrip  # noqa: F401

@@ -222,3 +222,19 @@ def forest_for_config(idx: int):
     f, rng = agentic_forest(cfg["seed"], cfg["n_trees"], cfg["lam"],
                             cfg["target"], cfg.get("depth_cap"))
     return f, rng, cfg
+
+
+def trajectory_tokens(forest: Forest, rng, vocab: int = 157184):
+    """Token sequences of every root-to-leaf trajectory (leaves by ascending
+    id): one seeded token id per compact row, read along each path, so that
+    trajectories of one tree share exactly their common prefix."""
+    tok = rng.integers(0, vocab, size=forest.n_rows).astype(np.int32)
+    row0 = np.concatenate([[0], np.cumsum(forest.seg_len)[:-1]])
+    out = []
+    for leaf in forest.leaves():
+        path, v = [], leaf
+        while v >= 0:
+            path.append(v)
+            v = int(forest.parent[v])
+        out.append(np.concatenate([tok[row0[w]:row0[w] + forest.seg_len[w]] for w in reversed(path)]))
+    return out
