@@ -28,6 +28,8 @@ Contents (all float64 unless stated):
                      (Sec. 3.2): compact-trie work, natural partition, exact
                      contiguous DP, evolution, trie-aware greedy, refinement,
                      replica/slot assignment and the lexicographic choice.
+* ``conv``        -- causal depthwise convolution along every trajectory (the
+                     true-ancestor context of Sec. 4.2) and its gradients.
 * ``logprob``     -- compact-to-semantic log-probabilities and their gradient
                      (eqs. mapped-logp, mapped-logp-grad), one log-softmax
                      per semantic position.
