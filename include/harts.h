@@ -388,6 +388,48 @@ int harts_mb_plan(int32_t n_traj, const int64_t* tok_off, const int32_t* tokens,
                   int32_t* mb_slot, int64_t* mb_work, harts_mb_result* result);
 
 /* ------------------------------------------------------------------------
+ * Causal depthwise convolution with true-ancestor context (Sec. 4.2, "KDA
+ * state reuse and causal convolution"): along every trajectory,
+ *     y_t[c] = sum_{i < w} W[c, i] x_{t-i}[c]   (zero before the start),
+ * computed once per compact row.  A row's window reaches its own ancestors
+ * only, never an adjacent packed sequence; replay rows of the linear
+ * attention read these results and never recompute them.
+ *
+ * harts_conv_context (host) -- the window of every row, from the plan.
+ *   w         width, 2..8 (the paper's KDA uses 4).
+ *   pred      [C][w-1] out: physical row of the row's i-th predecessor on
+ *             its trajectory (i = 1..w-1), -1 before the trajectory start.
+ *   succ_off  [C+1] out, succ [C*(w-1)] out: the consumers of every row,
+ *             encoded consumer_row * 8 + i, ordered by (i, consumer_row);
+ *             succ_off[C] entries in all (pass it as n_succ).
+ *   Linear in C * w.  Errors: HARTS_EINVAL (NULL), HARTS_EUNSUPPORTED
+ *   (w, C >= 2^28), HARTS_ENOMEM.
+ * harts_conv_fwd (device) -- y [C, Cch] from x [C, Cch] (dtype HARTS_BF16
+ *   or HARTS_F32, 16-byte aligned, physical row order) and float32 weights
+ *   W [Cch][w]; Cch a positive multiple of 8.
+ * harts_conv_bwd (device) -- for upstream dy [C, Cch]:
+ *   dx[r] = W[:, 0] dy[r] + sum over the consumers (s, i) of r of
+ *           W[:, i] dy[s]   (written, in x's dtype);
+ *   dW[c, i] = sum_r x[pred_i(r)][c] dy[r][c]   (float32, written),
+ *   summed in fixed orders (deterministic).  ws: float32 scratch of
+ *   harts_conv_workspace_size bytes (per-block partial sums of dW).
+ * Table entries outside [0, C) are treated as absent (zero), never read.
+ * Errors: HARTS_EINVAL (NULL / misaligned pointer, small workspace),
+ * HARTS_EUNSUPPORTED (dtype, w, Cch, C), HARTS_EHIP.  Asynchronous.
+ * ---------------------------------------------------------------------- */
+int harts_conv_context(const harts_plan_t* plan, int32_t w, int32_t* pred, int64_t* succ_off,
+                       int32_t* succ);
+
+int harts_conv_workspace_size(int64_t C, int32_t Cch, int32_t w, size_t* bytes);
+
+int harts_conv_fwd(int32_t dtype, int64_t C, int32_t Cch, int32_t w, const void* x, const float* W,
+                   const int32_t* pred, void* y, void* stream);
+
+int harts_conv_bwd(int32_t dtype, int64_t C, int32_t Cch, int32_t w, const void* x, const float* W,
+                   const int32_t* pred, const int64_t* succ_off, const int32_t* succ, int64_t n_succ,
+                   const void* dy, void* dx, float* dW, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Compact-to-semantic log-probabilities (Sec. 3.5, eqs. mapped-logp and
  * mapped-logp-grad).  Vocabulary-wide work runs once per compact logit row;
  * only scalar work runs per semantic position, and no S x V tensor exists.

@@ -24,6 +24,7 @@ EXPORTS = (
     "harts_la_fwd", "harts_la_fwd_noalloc", "harts_la_bwd", "harts_la_workspace_size",
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
     "harts_semantic_map", "harts_logp_fwd", "harts_logp_bwd", "harts_mb_plan",
+    "harts_conv_context", "harts_conv_workspace_size", "harts_conv_fwd", "harts_conv_bwd",
     "harts_profile_begin", "harts_profile_end",
 )
 
@@ -157,6 +158,14 @@ def lib():
     L.harts_logp_bwd.argtypes = [i32, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp]
     L.harts_mb_plan.restype = C.c_int
     L.harts_mb_plan.argtypes = [i32, vp, vp, i32, i64, i32, vp, vp, vp, vp, C.POINTER(MbResult)]
+    L.harts_conv_context.restype = C.c_int
+    L.harts_conv_context.argtypes = [vp, i32, vp, vp, vp]
+    L.harts_conv_workspace_size.restype = C.c_int
+    L.harts_conv_workspace_size.argtypes = [i64, i32, i32, C.POINTER(sz)]
+    L.harts_conv_fwd.restype = C.c_int
+    L.harts_conv_fwd.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
+    L.harts_conv_bwd.restype = C.c_int
+    L.harts_conv_bwd.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, sz, vp]
     L.harts_profile_begin.restype = C.c_int
     L.harts_profile_begin.argtypes = []
     L.harts_profile_end.restype = C.c_int

@@ -80,3 +80,44 @@ def test_semantic_map_validates():
     assert L.harts_semantic_map(plan.handle, p, 5, p, p, p, p) == _lib.HARTS_EINVAL
     assert L.harts_semantic_map(None, p, 955, p, p, p, p) == _lib.HARTS_EINVAL
     assert L.harts_semantic_map(plan.handle, None, 955, p, p, p, p) == _lib.HARTS_EINVAL
+
+
+@pytest.mark.parametrize("label,parent,seg_len", CASES + [
+    ("chain of one-token segments", [-1, 0, 1, 2, 3, 3, 5], [1, 1, 1, 1, 1, 4, 2])],
+    ids=[c[0] for c in CASES] + ["tiny segments"])
+@pytest.mark.parametrize("w", [2, 4, 8])
+def test_conv_context_follows_each_trajectory(label, parent, seg_len, w):
+    """harts_conv_context: a row's i-th predecessor is the row i positions
+    earlier on its own trajectory (-1 before the start), the same on every
+    trajectory through the row; the consumer lists are its transpose."""
+    from oracle.forest import SegTree
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan(parent, seg_len, 64)
+    C_ = int(np.sum(seg_len))
+    k = w - 1
+    pred = np.full(C_ * k, -7, np.int32)
+    off = np.zeros(C_ + 1, np.int64)
+    succ = np.zeros(C_ * k, np.int32)
+    L = _lib.lib()
+    _lib.check(L.harts_conv_context(plan.handle, w, pred.ctypes.data, off.ctypes.data,
+                                    succ.ctypes.data), "harts_conv_context")
+    pred = pred.reshape(C_, k)
+    phys = phys_index(seg_len, plan["seg_row"])
+    t = SegTree(parent, seg_len)
+    want = {}
+    for leaf in t.leaves:
+        rows = t.trajectory_rows(leaf)
+        for pos, row in enumerate(rows):
+            exp = [int(phys[rows[pos - i]]) if pos - i >= 0 else -1 for i in range(1, w)]
+            assert want.setdefault(int(phys[row]), exp) == exp
+    for r in range(C_):
+        assert list(pred[r]) == want[r]
+    entries = []
+    for r in range(C_):
+        lst = [(int(c) & 7, int(c) >> 3) for c in succ[off[r]:off[r + 1]]]
+        assert lst == sorted(lst)
+        entries += [(s, i, r) for i, s in lst]
+    expect = [(s, i, int(pred[s, i - 1])) for s in range(C_) for i in range(1, w)
+              if pred[s, i - 1] >= 0]
+    assert sorted(entries) == sorted(expect)
