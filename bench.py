@@ -53,7 +53,12 @@ WORKLOAD_KEY = {1: "spine16k", 2: "agentic64k", 3: "agentic128k"}
 
 
 def la_source_sha(kernel=None):
-    names = ("logp.hip",) if kernel and kernel.startswith("k_logp") else ("la.hip", "la_common.hpp")
+    if kernel and kernel.startswith("k_logp"):
+        names = ("logp.hip",)
+    elif kernel and kernel.startswith("k_conv"):
+        names = ("conv.hip",)
+    else:
+        names = ("la.hip", "la_common.hpp")
     h = hashlib.sha256()
     for name in names:
         with open(os.path.join(ROOT, "paper_2608_28158_amd", "csrc", name), "rb") as f:
@@ -618,6 +623,104 @@ def logp_measurement(steps, warmup, profile_only=False):
     return out
 
 
+CONV_CH, CONV_W = 6144, 4   # q, k, v of 16 heads x 128; the paper's KDA width
+
+
+def conv_measurement(steps, warmup, profile_only=False):
+    """Causal depthwise convolution with true-ancestor context on the
+    64k-token microbatch: 68,161 compact rows x 6,144 bf16 channels, width
+    4.  Algorithmic bytes: the forward reads x once and writes y once; the
+    backward reads dy and writes dx once, and reads x and dy once more for
+    the weight gradient (the taps of a row's window hit rows already read);
+    the row tables (12 bytes a row) are counted."""
+    import ctypes as C
+    import torch
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    from workloads import forest_for_config
+    L = _lib.lib()
+    f, _, cfg = forest_for_config(2)
+    plan = HartsPlan(f.parent, f.seg_len, 64, heads=cfg["H"])
+    Cn, Cch, w = f.n_rows, CONV_CH, CONV_W
+    k = w - 1
+    pred = np.zeros(Cn * k, np.int32)
+    off = np.zeros(Cn + 1, np.int64)
+    succ = np.zeros(Cn * k, np.int32)
+    t0 = time.perf_counter()
+    _lib.check(L.harts_conv_context(plan.handle, w, pred.ctypes.data, off.ctypes.data,
+                                    succ.ctypes.data), "harts_conv_context")
+    ctx_ms = (time.perf_counter() - t0) * 1e3
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    pd, od, sd = dev(pred), dev(off), dev(succ)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(7)
+    x = torch.randn((Cn, Cch), device="cuda", generator=gen).to(torch.bfloat16)
+    dy = torch.randn((Cn, Cch), device="cuda", generator=gen).to(torch.bfloat16)
+    Wd = (torch.randn((Cch, w), device="cuda", generator=gen) * 0.5).contiguous()
+    y, dx = torch.empty_like(x), torch.empty_like(x)
+    dW = torch.empty((Cch, w), dtype=torch.float32, device="cuda")
+    sz = C.c_size_t()
+    _lib.check(L.harts_conv_workspace_size(Cn, Cch, w, C.byref(sz)), "harts_conv_workspace_size")
+    ws = torch.empty(sz.value, dtype=torch.uint8, device="cuda")
+    P = lambda t: C.c_void_p(t.data_ptr())
+    stream = torch.cuda.current_stream()
+    st = C.c_void_p(stream.cuda_stream)
+    code = _lib.HARTS_BF16
+
+    def fwd():
+        _lib.check(L.harts_conv_fwd(code, Cn, Cch, w, P(x), P(Wd), P(pd), P(y), st), "harts_conv_fwd")
+
+    def bwd():
+        _lib.check(L.harts_conv_bwd(code, Cn, Cch, w, P(x), P(Wd), P(pd), P(od), P(sd), int(off[-1]),
+                                    P(dy), P(dx), P(dW), P(ws), ws.numel(), st), "harts_conv_bwd")
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(steps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / steps
+
+    ms_f, ms_b = timed(fwd), timed(bwd)
+    if profile_only:
+        return None
+    row = Cch * 2
+    by_f = 2 * Cn * row + Cn * 12 + Cch * w * 4
+    by_b = 3 * Cn * row + Cn * 12 + int(off[-1]) * 4 + Cn * 8 + 2 * Cch * w * 4
+    out = {"workload": f"64k-token agentic microbatch: {Cn} compact rows x {Cch} bf16 channels, "
+                       f"width {w}",
+           "fwd_ms": ms_f, "bwd_ms": ms_b,
+           "fwd": {"alg_GB": by_f / 1e9, "achieved_GBs": by_f / (ms_f * 1e-3) / 1e9,
+                   "hbm_frac": by_f / (ms_f * 1e-3) / 1e9 / PEAK_HBM_GBS},
+           "bwd": {"alg_GB": by_b / 1e9, "achieved_GBs": by_b / (ms_b * 1e-3) / 1e9,
+                   "hbm_frac": by_b / (ms_b * 1e-3) / 1e9 / PEAK_HBM_GBS},
+           "context_ms": ctx_ms,
+           "traffic_k_conv_fwd": read_traffic("k_conv_fwd", "agentic64k_c6144"),
+           "traffic_k_conv_dx": read_traffic("k_conv_dx", "agentic64k_c6144")}
+    # the oracle (fp64, trajectory by trajectory) on a sample of channels
+    from oracle.conv import conv_bwd, conv_fwd
+    chs = 8
+    phys = phys_index(f.seg_len, plan["seg_row"])
+    take = lambda t: t[:, :chs].float().cpu().numpy()[phys]
+    xs, dys, Ws = take(x), take(dy), Wd[:chs].cpu().numpy()
+    t1 = time.perf_counter()
+    conv_fwd(f.parent, f.seg_len, xs, Ws)
+    conv_bwd(f.parent, f.seg_len, xs, Ws, dys)
+    cpu_s = time.perf_counter() - t1
+    out["cpu_baseline"] = {"value": Cn * chs / Cch / cpu_s, "unit": "compact rows/s (all channels)",
+                           "cores": 1, "kind": "oracle",
+                           "sample": f"{chs} of {Cch} channels, forward + backward over every "
+                                     f"trajectory ({cpu_s:.1f} s), scaled by {Cch // chs}"}
+    del x, dy, y, dx
+    torch.cuda.empty_cache()
+    return out
+
+
 def mbplan_measurement(D=4, T=65536):
     """Prefix-aware microbatch/DP planning at the paper's scale: a seeded
     batch of 215 agentic rollout trees at full length (about 1,600
@@ -681,6 +784,9 @@ def main():
     ap.add_argument("--no-expanded", action="store_true")
     ap.add_argument("--no-logp", action="store_true")
     ap.add_argument("--no-mbplan", action="store_true")
+    ap.add_argument("--no-conv", action="store_true")
+    ap.add_argument("--conv-only", action="store_true",
+                    help="run the timed convolution calls only (for profiler runs)")
     ap.add_argument("--steps-only", action="store_true",
                     help="run the timed steps only (for profiler runs)")
     ap.add_argument("--logp-only", action="store_true",
@@ -707,6 +813,10 @@ def main():
     if args.logp_only:
         logp_measurement(args.steps, args.warmup, profile_only=True)
         log("[bench] logp calls done")
+        return
+    if args.conv_only:
+        conv_measurement(args.steps, args.warmup, profile_only=True)
+        log("[bench] conv calls done")
         return
     log(f"[bench] config {args.config}: building workload")
     forest, cfg, x, plan, t, runner, plan_s = setup(args.config)
@@ -807,6 +917,9 @@ def main():
     if not args.no_logp:
         log("[bench] compact-to-semantic log-probabilities (157,184-token vocabulary)")
         out["logp"] = logp_measurement(args.steps, args.warmup)
+    if not args.no_conv:
+        log("[bench] causal convolution with ancestor context (6,144 channels)")
+        out["conv"] = conv_measurement(args.steps, args.warmup)
     if not args.no_mbplan:
         log("[bench] prefix-aware microbatch planning (host)")
         out["mb_plan"] = mbplan_measurement()

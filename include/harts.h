@@ -405,8 +405,8 @@ int harts_mb_plan(int32_t n_traj, const int64_t* tok_off, const int32_t* tokens,
  *   Linear in C * w.  Errors: HARTS_EINVAL (NULL), HARTS_EUNSUPPORTED
  *   (w, C >= 2^28), HARTS_ENOMEM.
  * harts_conv_fwd (device) -- y [C, Cch] from x [C, Cch] (dtype HARTS_BF16
- *   or HARTS_F32, 16-byte aligned, physical row order) and float32 weights
- *   W [Cch][w]; Cch a positive multiple of 8.
+ *   or HARTS_F32, physical row order) and float32 weights W [Cch][w]; Cch
+ *   a positive multiple of 8; x, y, W (and dy, dx) 16-byte aligned.
  * harts_conv_bwd (device) -- for upstream dy [C, Cch]:
  *   dx[r] = W[:, 0] dy[r] + sum over the consumers (s, i) of r of
  *           W[:, i] dy[s]   (written, in x's dtype);

@@ -9,12 +9,11 @@
 // semantic.cpp) writes that predecessor table once per plan, and the
 // transposed table of consumers, which the backward walks to gather each
 // row's gradient.
-//   k_conv_fwd      one thread per (row, 16-byte channel vector);
-//   k_conv_dx       one thread per (row, vector): its own term plus every
-//                   consumer's, in (tap, row) order;
-//   k_conv_dw_part  per block of 512 rows and channel vector, the tap sums
-//                   x[pred_i(r)] dy[r] over the block's rows, in row order;
-//   k_conv_dw_sum   per (channel, tap), the block partials in block order.
+//   k_conv_fwd      one thread per (4 channels, run of 64 rows);
+//   k_conv_bwd      runs of 128 rows: dx of each row (its own term plus
+//                   every consumer's, in (tap, row) order) and the run's
+//                   tap sums x[pred_i(r)] dy[r], in row order;
+//   k_conv_dw_sum   per (channel, tap), the runs' partials in a fixed order.
 // Arithmetic in float32; no atomics, so reruns are bitwise identical.
 #include <hip/hip_runtime.h>
 
@@ -33,26 +32,26 @@ namespace {
 typedef __bf16 bf16;
 constexpr int CV_THR = 256;
 constexpr int CV_MAXW = 8;
-constexpr int CV_ROWS = 512;  // rows per weight-gradient block
+constexpr int CV_RUN = 32;     // rows per thread in the forward
+constexpr int CV_RUN_B = 64;   // rows per thread in the backward (one partial dW per run)
+constexpr int CV_SUCC = 2048;  // consumer entries of a backward run staged in LDS
 
 template <typename T> struct CV;
 template <> struct CV<bf16> {
-  static constexpr int N = 8;
+  static constexpr int N = 4;  // 8-byte pieces: half the registers of 16-byte ones
   __device__ static inline void load(const bf16* p, float* x) {
-    const uint4 u = *reinterpret_cast<const uint4*>(p);
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[2 * i] = __uint_as_float(w[i] << 16);
-      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    }
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    x[0] = __uint_as_float(u.x << 16);
+    x[1] = __uint_as_float(u.x & 0xffff0000u);
+    x[2] = __uint_as_float(u.y << 16);
+    x[3] = __uint_as_float(u.y & 0xffff0000u);
   }
   __device__ static inline void store(bf16* p, const float* x) {
-    typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-    bf16x8 b;
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    bf16x4 b;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) b[i] = static_cast<bf16>(x[i]);
-    *reinterpret_cast<bf16x8*>(p) = b;
+    for (int i = 0; i < 4; ++i) b[i] = static_cast<bf16>(x[i]);
+    *reinterpret_cast<bf16x4*>(p) = b;
   }
 };
 template <> struct CV<float> {
@@ -66,106 +65,231 @@ template <> struct CV<float> {
   }
 };
 
+// Threads own 4 channels each (consecutive threads,
+// consecutive vectors of the same rows: coalesced) and walk a run of rows,
+// with their W taps in registers.  Inside a segment a row's predecessors
+// are the rows just before it, so the activations of the previous rows are
+// kept in registers and reloaded only where the table points elsewhere
+// (a segment's first rows, whose window reaches into an ancestor).
+template <typename T, int W>
+__device__ inline void load_taps(const float* __restrict__ Wt, int c0, float (&wt)[W][CV<T>::N]) {
+#pragma unroll
+  for (int e = 0; e < CV<T>::N; ++e) {
+    const float4* src = reinterpret_cast<const float4*>(Wt + (c0 + e) * W);
+    if constexpr (W % 4 == 0) {
+#pragma unroll
+      for (int q = 0; q < W / 4; ++q) {
+        const float4 u = src[q];
+        wt[4 * q][e] = u.x; wt[4 * q + 1][e] = u.y; wt[4 * q + 2][e] = u.z; wt[4 * q + 3][e] = u.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < W; ++i) wt[i][e] = Wt[(c0 + e) * W + i];
+    }
+  }
+}
+
+// v <- x[pred_i(r)] (tap i >= 1): from the registers of the previous rows
+// when the predecessor is the row i above in this thread's run, else loaded
+// (zero before the trajectory start or for an invalid entry).
+// hist[j] = x[r - 1 - j].
+template <typename T, int W>
+__device__ inline void tap_value(const T* __restrict__ x, int64_t C, int Cch, int c0, int64_t r,
+                                 int64_t run0, int i, int32_t p, const float (&hist)[W - 1][CV<T>::N],
+                                 float (&v)[CV<T>::N]) {
+  if (p == r - i && r - i >= run0) {
+#pragma unroll
+    for (int e = 0; e < CV<T>::N; ++e) v[e] = hist[i - 1][e];
+  } else if (p >= 0 && p < C) {
+    CV<T>::load(x + static_cast<int64_t>(p) * Cch + c0, v);
+  } else {
+#pragma unroll
+    for (int e = 0; e < CV<T>::N; ++e) v[e] = 0.f;
+  }
+}
+
+template <typename T, int W>
+__device__ inline void shift_hist(float (&hist)[W - 1][CV<T>::N], const float (&cur)[CV<T>::N]) {
+#pragma unroll
+  for (int j = W - 2; j > 0; --j)
+#pragma unroll
+    for (int e = 0; e < CV<T>::N; ++e) hist[j][e] = hist[j - 1][e];
+#pragma unroll
+  for (int e = 0; e < CV<T>::N; ++e) hist[0][e] = cur[e];
+}
+
 template <typename T, int W>
 __global__ __launch_bounds__(CV_THR) void k_conv_fwd(int64_t C, int Cch, const T* __restrict__ x,
                                                      const float* __restrict__ Wt,
                                                      const int32_t* __restrict__ pred, T* __restrict__ y) {
   using V = CV<T>;
-  const int nvec = Cch / V::N;
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * CV_THR + threadIdx.x;
-  const int64_t row = idx / nvec;
-  if (row >= C) return;
-  const int c0 = static_cast<int>(idx % nvec) * V::N;
-  float acc[V::N], v[V::N];
-  V::load(x + row * Cch + c0, v);
-#pragma unroll
-  for (int e = 0; e < V::N; ++e) acc[e] = Wt[(c0 + e) * W] * v[e];
-#pragma unroll
-  for (int i = 1; i < W; ++i) {
-    const int32_t p = pred[row * (W - 1) + i - 1];
-    if (p < 0 || p >= C) continue;  // before the trajectory start (or invalid): zero
-    V::load(x + static_cast<int64_t>(p) * Cch + c0, v);
-#pragma unroll
-    for (int e = 0; e < V::N; ++e) acc[e] += Wt[(c0 + e) * W + i] * v[e];
-  }
-  V::store(y + row * Cch + c0, acc);
-}
-
-template <typename T, int W>
-__global__ __launch_bounds__(CV_THR) void k_conv_dx(int64_t C, int Cch, const float* __restrict__ Wt,
-                                                    const int64_t* __restrict__ succ_off,
-                                                    const int32_t* __restrict__ succ, int64_t n_succ,
-                                                    const T* __restrict__ dy, T* __restrict__ dx) {
-  using V = CV<T>;
-  const int nvec = Cch / V::N;
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * CV_THR + threadIdx.x;
-  const int64_t row = idx / nvec;
-  if (row >= C) return;
-  const int c0 = static_cast<int>(idx % nvec) * V::N;
-  float acc[V::N], v[V::N];
-  V::load(dy + row * Cch + c0, v);
-#pragma unroll
-  for (int e = 0; e < V::N; ++e) acc[e] = Wt[(c0 + e) * W] * v[e];
-  const int64_t b = succ_off[row] < 0 ? 0 : succ_off[row];
-  const int64_t end = succ_off[row + 1] > n_succ ? n_succ : succ_off[row + 1];
-  for (int64_t j = b; j < end; ++j) {
-    const int32_t code = succ[j];
-    const int32_t s = code >> 3, i = code & 7;  // consumer row, tap
-    if (s < 0 || s >= C || i < 1 || i >= W) continue;
-    V::load(dy + static_cast<int64_t>(s) * Cch + c0, v);
-#pragma unroll
-    for (int e = 0; e < V::N; ++e) acc[e] += Wt[(c0 + e) * W + i] * v[e];
-  }
-  V::store(dx + row * Cch + c0, acc);
-}
-
-// partial[blk][c][i] = sum over the block's rows r of x[pred_i(r)][c] dy[r][c]
-template <typename T, int W>
-__global__ __launch_bounds__(CV_THR) void k_conv_dw_part(int64_t C, int Cch, const T* __restrict__ x,
-                                                         const int32_t* __restrict__ pred,
-                                                         const T* __restrict__ dy,
-                                                         float* __restrict__ part) {
-  using V = CV<T>;
-  const int nvec = Cch / V::N;
-  const int vec = blockIdx.y * CV_THR + threadIdx.x;
-  if (vec >= nvec) return;
+  const int vec = blockIdx.x * CV_THR + threadIdx.x;
   const int c0 = vec * V::N;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * CV_ROWS;
-  const int64_t r1 = r0 + CV_ROWS < C ? r0 + CV_ROWS : C;
-  float acc[W][V::N];
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * CV_RUN;
+  const int64_t r1 = r0 + CV_RUN < C ? r0 + CV_RUN : C;
+  // the run's predecessor table, staged in LDS (one global round trip per
+  // workgroup instead of one per row)
+  __shared__ int32_t s_pred[CV_RUN * (W - 1)];
+  for (int j = threadIdx.x; j < (r1 - r0) * (W - 1); j += CV_THR) s_pred[j] = pred[r0 * (W - 1) + j];
+  __syncthreads();
+  if (vec >= Cch / V::N) return;
+  float wt[W][V::N], hist[W - 1][V::N];
+  load_taps<T, W>(Wt, c0, wt);
+  for (int64_t r = r0; r < r1; ++r) {
+    float cur[V::N], v[V::N], acc[V::N];
+    V::load(x + r * Cch + c0, cur);
+#pragma unroll
+    for (int e = 0; e < V::N; ++e) acc[e] = wt[0][e] * cur[e];
+#pragma unroll
+    for (int i = 1; i < W; ++i) {
+      tap_value<T, W>(x, C, Cch, c0, r, r0, i, s_pred[(r - r0) * (W - 1) + i - 1], hist, v);
+#pragma unroll
+      for (int e = 0; e < V::N; ++e) acc[e] += wt[i][e] * v[e];
+    }
+    V::store(y + r * Cch + c0, acc);
+    shift_hist<T, W>(hist, cur);
+  }
+}
+
+// dx of a run of rows, and the run's partial weight gradient:
+// part[run][c][i] = sum over the run's rows r of x[pred_i(r)][c] dy[r][c].
+// Inside a segment the consumers of row r through tap i are the rows r + i,
+// so dy of the next W - 1 rows rides along in registers (one new row
+// loaded per step) and only consumers elsewhere (the first rows of child
+// segments) are loaded through the table.
+template <typename T, int W>
+__global__ __launch_bounds__(CV_THR) void k_conv_bwd(int64_t C, int Cch, const T* __restrict__ x,
+                                                     const float* __restrict__ Wt,
+                                                     const int32_t* __restrict__ pred,
+                                                     const int64_t* __restrict__ succ_off,
+                                                     const int32_t* __restrict__ succ, int64_t n_succ,
+                                                     const T* __restrict__ dy, T* __restrict__ dx,
+                                                     float* __restrict__ part) {
+  using V = CV<T>;
+  const int vec = blockIdx.x * CV_THR + threadIdx.x;
+  const int c0 = vec * V::N;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * CV_RUN_B;
+  const int64_t r1 = r0 + CV_RUN_B < C ? r0 + CV_RUN_B : C;
+  // the run's tables, staged in LDS: predecessors, consumer offsets
+  // (relative to the run's first entry) and up to CV_SUCC consumer entries;
+  // entries beyond that (rows feeding very many children) are read from
+  // global memory
+  __shared__ int32_t s_pred[CV_RUN_B * (W - 1)];
+  __shared__ int32_t s_off[CV_RUN_B + 1];
+  __shared__ int32_t s_succ[CV_SUCC];
+  const int64_t nr = r1 - r0;
+  const int64_t b0 = succ_off[r0] < 0 ? 0 : (succ_off[r0] > n_succ ? n_succ : succ_off[r0]);
+  for (int j = threadIdx.x; j < nr * (W - 1); j += CV_THR) s_pred[j] = pred[r0 * (W - 1) + j];
+  for (int j = threadIdx.x; j <= nr; j += CV_THR) {
+    int64_t o = succ_off[r0 + j];
+    o = o < b0 ? b0 : (o > n_succ ? n_succ : o);
+    s_off[j] = static_cast<int32_t>(o - b0 < INT32_MAX ? o - b0 : INT32_MAX);
+  }
+  __syncthreads();
+  const int32_t n_run_succ = s_off[nr];
+  for (int j = threadIdx.x; j < n_run_succ && j < CV_SUCC; j += CV_THR) s_succ[j] = succ[b0 + j];
+  __syncthreads();
+  if (vec >= Cch / V::N) return;
+  float wt[W][V::N], hist[W - 1][V::N], gw[W][V::N], dwin[W][V::N];
+  load_taps<T, W>(Wt, c0, wt);
 #pragma unroll
   for (int i = 0; i < W; ++i)
 #pragma unroll
-    for (int e = 0; e < V::N; ++e) acc[i][e] = 0.f;
-  for (int64_t r = r0; r < r1; ++r) {
-    float g[V::N], v[V::N];
-    V::load(dy + r * Cch + c0, g);
-    V::load(x + r * Cch + c0, v);
+    for (int e = 0; e < V::N; ++e) gw[i][e] = 0.f;
+  // dwin[i] = dy[r + i] (zero past the last row)
 #pragma unroll
-    for (int e = 0; e < V::N; ++e) acc[0][e] += v[e] * g[e];
+  for (int i = 0; i < W; ++i) {
+    if (r0 + i < C) {
+      V::load(dy + (r0 + i) * Cch + c0, dwin[i]);
+    } else {
 #pragma unroll
-    for (int i = 1; i < W; ++i) {
-      const int32_t p = pred[r * (W - 1) + i - 1];
-      if (p < 0 || p >= C) continue;
-      V::load(x + static_cast<int64_t>(p) * Cch + c0, v);
-#pragma unroll
-      for (int e = 0; e < V::N; ++e) acc[i][e] += v[e] * g[e];
+      for (int e = 0; e < V::N; ++e) dwin[i][e] = 0.f;
     }
   }
-  float* out = part + static_cast<int64_t>(blockIdx.x) * Cch * W;
+  for (int64_t r = r0; r < r1; ++r) {
+    float cur[V::N], v[V::N], acc[V::N];
+    V::load(x + r * Cch + c0, cur);
 #pragma unroll
-  for (int e = 0; e < V::N; ++e)
+    for (int e = 0; e < V::N; ++e) {
+      acc[e] = wt[0][e] * dwin[0][e];
+      gw[0][e] += cur[e] * dwin[0][e];
+    }
 #pragma unroll
-    for (int i = 0; i < W; ++i) out[(c0 + e) * W + i] = acc[i][e];
+    for (int i = 1; i < W; ++i) {
+      tap_value<T, W>(x, C, Cch, c0, r, r0, i, s_pred[(r - r0) * (W - 1) + i - 1], hist, v);
+#pragma unroll
+      for (int e = 0; e < V::N; ++e) gw[i][e] += v[e] * dwin[0][e];
+    }
+    const int32_t jb = s_off[r - r0], je = s_off[r - r0 + 1];
+    for (int32_t j = jb; j < je; ++j) {
+      const int32_t code = j < CV_SUCC ? s_succ[j] : succ[b0 + j];
+      const int32_t sr = code >> 3, i = code & 7;  // consumer row, tap
+      if (sr < 0 || sr >= C || i < 1 || i >= W) continue;
+      if (sr == r + i) {  // the row i below: already in registers
+#pragma unroll
+        for (int k = 1; k < W; ++k)
+          if (k == i) {
+#pragma unroll
+            for (int e = 0; e < V::N; ++e) acc[e] += wt[k][e] * dwin[k][e];
+          }
+      } else {
+        V::load(dy + static_cast<int64_t>(sr) * Cch + c0, v);
+#pragma unroll
+        for (int k = 1; k < W; ++k)
+          if (k == i) {
+#pragma unroll
+            for (int e = 0; e < V::N; ++e) acc[e] += wt[k][e] * v[e];
+          }
+      }
+    }
+    V::store(dx + r * Cch + c0, acc);
+    shift_hist<T, W>(hist, cur);
+#pragma unroll
+    for (int k = 0; k + 1 < W; ++k)
+#pragma unroll
+      for (int e = 0; e < V::N; ++e) dwin[k][e] = dwin[k + 1][e];
+    if (r + W < C) {
+      V::load(dy + (r + W) * Cch + c0, dwin[W - 1]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < V::N; ++e) dwin[W - 1][e] = 0.f;
+    }
+  }
+  // partials tap-major ([run][tap][channel]): every store is a coalesced
+  // 16- or 32-byte piece of one tap's channel row
+  float* out = part + static_cast<int64_t>(blockIdx.y) * Cch * W;
+#pragma unroll
+  for (int i = 0; i < W; ++i)
+#pragma unroll
+    for (int e = 0; e < V::N; e += 4)
+      *reinterpret_cast<float4*>(out + static_cast<int64_t>(i) * Cch + c0 + e) =
+          float4{gw[i][e], gw[i][e + 1], gw[i][e + 2], gw[i][e + 3]};
 }
 
-__global__ __launch_bounds__(CV_THR) void k_conv_dw_sum(int64_t n_blk, int64_t n, const float* __restrict__ part,
+// dW[c][i] = sum over runs of part[run][i][c]: a workgroup takes 32
+// consecutive (tap, channel) entries; its 8 groups of 32 threads sum every
+// 8th run (group g takes runs g, g + 8, ...), and the 8 group sums are
+// added in group order: a fixed association, independent of scheduling.
+constexpr int DW_K = 32, DW_G = CV_THR / DW_K;
+__global__ __launch_bounds__(CV_THR) void k_conv_dw_sum(int64_t n_run, int Cch, int W,
+                                                        const float* __restrict__ part,
                                                         float* __restrict__ dW) {
-  const int64_t k = static_cast<int64_t>(blockIdx.x) * CV_THR + threadIdx.x;
-  if (k >= n) return;
+  __shared__ float red[DW_G][DW_K];
+  const int lk = threadIdx.x % DW_K, g = threadIdx.x / DW_K;
+  const int64_t n = static_cast<int64_t>(Cch) * W;
+  const int64_t k = static_cast<int64_t>(blockIdx.x) * DW_K + lk;  // i * Cch + c
   float acc = 0.f;
-  for (int64_t b = 0; b < n_blk; ++b) acc += part[b * n + k];
-  dW[k] = acc;
+  if (k < n)
+    for (int64_t b = g; b < n_run; b += DW_G) acc += part[b * n + k];
+  red[g][lk] = acc;
+  __syncthreads();
+  if (g == 0 && k < n) {
+    float sum = red[0][lk];
+#pragma unroll
+    for (int j = 1; j < DW_G; ++j) sum += red[j][lk];
+    const int64_t i = k / Cch, c = k % Cch;
+    dW[c * W + i] = sum;
+  }
 }
 
 int conv_status(const char* where) {
@@ -194,8 +318,9 @@ bool a16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 template <typename T>
 int launch_fwd(int w, int64_t C, int Cch, const void* x, const float* Wt, const int32_t* pred, void* y,
                hipStream_t s) {
-  const int64_t threads = C * (Cch / CV<T>::N);
-  const dim3 grid(static_cast<uint32_t>((threads + CV_THR - 1) / CV_THR));
+  const int nvec = Cch / CV<T>::N;
+  const dim3 grid(static_cast<uint32_t>((nvec + CV_THR - 1) / CV_THR),
+                  static_cast<uint32_t>((C + CV_RUN - 1) / CV_RUN));
   const T* xx = static_cast<const T*>(x);
   T* yy = static_cast<T*>(y);
   switch (w) {
@@ -212,30 +337,26 @@ template <typename T>
 int launch_bwd(int w, int64_t C, int Cch, const void* x, const float* Wt, const int32_t* pred,
                const int64_t* succ_off, const int32_t* succ, int64_t n_succ, const void* dy, void* dx,
                float* dW, float* part, hipStream_t s) {
-  const int64_t threads = C * (Cch / CV<T>::N);
-  const dim3 grid(static_cast<uint32_t>((threads + CV_THR - 1) / CV_THR));
-  const int64_t n_blk = (C + CV_ROWS - 1) / CV_ROWS;
   const int nvec = Cch / CV<T>::N;
-  const dim3 pgrid(static_cast<uint32_t>(n_blk), static_cast<uint32_t>((nvec + CV_THR - 1) / CV_THR));
+  const int64_t n_run = (C + CV_RUN_B - 1) / CV_RUN_B;
+  const dim3 grid(static_cast<uint32_t>((nvec + CV_THR - 1) / CV_THR), static_cast<uint32_t>(n_run));
   const T* xx = static_cast<const T*>(x);
   const T* gy = static_cast<const T*>(dy);
   T* gx = static_cast<T*>(dx);
   switch (w) {
-#define HARTS_CONV_BWD(WW)                                                                              \
-  case WW:                                                                                              \
-    hipLaunchKernelGGL((k_conv_dx<T, WW>), grid, dim3(CV_THR), 0, s, C, Cch, Wt, succ_off, succ, n_succ, \
-                       gy, gx);                                                                         \
-    if (int rc = conv_status("k_conv_dx")) return rc;                                                   \
-    hipLaunchKernelGGL((k_conv_dw_part<T, WW>), pgrid, dim3(CV_THR), 0, s, C, Cch, xx, pred, gy, part); \
+#define HARTS_CONV_BWD(WW)                                                                            \
+  case WW:                                                                                            \
+    hipLaunchKernelGGL((k_conv_bwd<T, WW>), grid, dim3(CV_THR), 0, s, C, Cch, xx, Wt, pred, succ_off, \
+                       succ, n_succ, gy, gx, part);                                                   \
     break;
     HARTS_CONV_BWD(2) HARTS_CONV_BWD(3) HARTS_CONV_BWD(4) HARTS_CONV_BWD(5)
     HARTS_CONV_BWD(6) HARTS_CONV_BWD(7) HARTS_CONV_BWD(8)
 #undef HARTS_CONV_BWD
   }
-  if (int rc = conv_status("k_conv_dw_part")) return rc;
+  if (int rc = conv_status("k_conv_bwd")) return rc;
   const int64_t n = static_cast<int64_t>(Cch) * w;
-  hipLaunchKernelGGL(k_conv_dw_sum, dim3(static_cast<uint32_t>((n + CV_THR - 1) / CV_THR)), dim3(CV_THR), 0,
-                     s, n_blk, n, part, dW);
+  hipLaunchKernelGGL(k_conv_dw_sum, dim3(static_cast<uint32_t>((n + DW_K - 1) / DW_K)), dim3(CV_THR), 0,
+                     s, n_run, Cch, w, part, dW);
   return conv_status("k_conv_dw_sum");
 }
 
@@ -247,8 +368,8 @@ using namespace harts;
 extern "C" int harts_conv_workspace_size(int64_t C, int32_t Cch, int32_t w, size_t* bytes) {
   if (int rc = check_conv(HARTS_F32, C, Cch, w, "harts_conv_workspace_size")) return rc;
   if (!bytes) { set_error("harts_conv_workspace_size: NULL bytes"); return HARTS_EINVAL; }
-  const int64_t n_blk = (C + CV_ROWS - 1) / CV_ROWS;
-  *bytes = static_cast<size_t>(std::max<int64_t>(n_blk, 1)) * Cch * w * sizeof(float);
+  const int64_t n_run = (C + CV_RUN_B - 1) / CV_RUN_B;
+  *bytes = static_cast<size_t>(std::max<int64_t>(n_run, 1)) * Cch * w * sizeof(float);
   return HARTS_OK;
 }
 
@@ -256,7 +377,7 @@ extern "C" int harts_conv_fwd(int32_t dtype, int64_t C, int32_t Cch, int32_t w, 
                               const int32_t* pred, void* y, void* stream) {
   if (int rc = check_conv(dtype, C, Cch, w, "harts_conv_fwd")) return rc;
   if (C == 0) return HARTS_OK;
-  if (!x || !Wt || !pred || !y || !a16(x) || !a16(y)) {
+  if (!x || !Wt || !pred || !y || !a16(x) || !a16(y) || !a16(Wt)) {
     set_error("harts_conv_fwd: NULL or misaligned (16 bytes) pointer");
     return HARTS_EINVAL;
   }
@@ -272,7 +393,7 @@ extern "C" int harts_conv_bwd(int32_t dtype, int64_t C, int32_t Cch, int32_t w, 
   if (int rc = check_conv(dtype, C, Cch, w, "harts_conv_bwd")) return rc;
   if (C == 0) return HARTS_OK;
   if (!x || !Wt || !pred || !succ_off || (!succ && n_succ > 0) || n_succ < 0 || !dy || !dx || !dW || !ws ||
-      !a16(x) || !a16(dy) || !a16(dx)) {
+      !a16(x) || !a16(dy) || !a16(dx) || !a16(Wt)) {
     set_error("harts_conv_bwd: NULL or misaligned (16 bytes) pointer, or n_succ < 0");
     return HARTS_EINVAL;
   }

@@ -32,6 +32,8 @@ def sources_of(kernel=None):
     by default)."""
     if kernel and kernel.startswith("k_logp"):
         return ("logp.hip",)
+    if kernel and kernel.startswith("k_conv"):
+        return ("conv.hip",)
     return ("la.hip", "la_common.hpp")
 
 
@@ -48,7 +50,8 @@ def short(name):
     for key in ("k_bwd_revorder", "k_bwd_fwdorder", "k_blocksum", "k_fwd_blockscan",
                 "k_fwd_block", "k_bwd_blockscan", "k_dg_carry", "k_gather", "k_scatter_add",
                 "k_replay_reduce", "k_logp_lse", "k_logp_gather", "k_logp_rowsum",
-                "k_logp_grad", "k_logp_onehot"):
+                "k_logp_grad", "k_logp_onehot", "k_conv_fwd", "k_conv_dx", "k_conv_dw_part",
+                "k_conv_dw_sum"):
         if key in n:
             return key
     return n.replace("void ", "")[:48]
@@ -59,7 +62,7 @@ def stats(src, out, cmd):
     tot = sum(float(r["TotalDurationNs"]) for r in rows)
     lines = ["# rocprofv3 kernel statistics", "", "Command:", "", "    " + " ".join(cmd), "",
              f"Kernel source hashes: la.hip + la_common.hpp {source_sha()}, "
-             f"logp.hip {source_sha('k_logp')}", "",
+             f"logp.hip {source_sha('k_logp')}, conv.hip {source_sha('k_conv')}", "",
              "| kernel | calls | total ms | avg us | min us | max us | share |",
              "|---|---|---|---|---|---|---|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
