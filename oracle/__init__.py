@@ -30,6 +30,9 @@ Contents (all float64 unless stated):
                      replica/slot assignment and the lexicographic choice.
 * ``conv``        -- causal depthwise convolution along every trajectory (the
                      true-ancestor context of Sec. 4.2) and its gradients.
+* ``attn``        -- causal softmax attention along every trajectory, and one
+                     branch through asymmetric Q/KV views with bottom-right
+                     alignment (Sec. 4.2).
 * ``logprob``     -- compact-to-semantic log-probabilities and their gradient
                      (eqs. mapped-logp, mapped-logp-grad), one log-softmax
                      per semantic position.
