@@ -430,6 +430,63 @@ int harts_conv_bwd(int32_t dtype, int64_t C, int32_t Cch, int32_t w, const void*
                    const void* dy, void* dx, float* dW, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Full attention through asymmetric packed Q/KV views (Sec. 4.2, eqs.
+ * asymmetric-qkv and bottom-right), bf16, d in {64, 128}.
+ *
+ * One view per input sequence of the plan: its queries are the sequence's
+ * l own rows; its key/value row holds the h ancestor positions of its
+ * trajectory followed by the same l rows; query i sees keys j <= h + i
+ * (bottom-right alignment).  Per head: o = softmax(scale Q K^T) V over the
+ * visible keys.  Each compact row is the query of exactly one view, so
+ * outputs and dq go straight to compact rows; key/value gradients of the
+ * views are summed back into the rows they were gathered from.
+ *
+ * harts_attn_layout / harts_attn_views (host) -- sizes, then tables:
+ *   views    [n_views][4]: first own row, l, offset in the view rows, h.
+ *   kv_rows  [n_kv]: compact row of every view row (views in order).
+ *   qtiles   [n_qtiles][2], kvtiles [n_kvtiles][2]: (view, first row) of
+ *            every 64-row query tile and key tile.
+ *   row_off  [C+1], row_ent [n_kv]: view rows of every compact row,
+ *            ascending (the order of the gradient sums).
+ * harts_attn_gather (device) -- dst[e] = src[kv_rows[e]], [rows, H, d] bf16
+ *   (the key and value views).
+ * harts_attn_fwd (device) -- o [C, H, d] bf16 for every query row and
+ *   lse [C, H] float32 (natural log of the softmax denominator, needed by
+ *   the backward), from q [C, H, d] and the key/value views [n_kv, H, d].
+ * harts_attn_bwd (device) -- from dO [C, H, d]: dq [C, H, d] bf16 (written),
+ *   dk_view, dv_view [n_kv, H, d] float32 (written); delta [C, H] float32 is
+ *   scratch (dO . o per row).
+ * harts_attn_scatter (device) -- dst [C, H, d] bf16 = sum over each row's
+ *   view rows of src [n_kv, H, d] float32, in row_ent order (deterministic).
+ * Pointers to row tensors 16-byte aligned.  Errors: HARTS_EINVAL (NULL,
+ * misaligned, sizes), HARTS_EUNSUPPORTED (H, d; more than 2^31 - 1 view
+ * rows), HARTS_EHIP, HARTS_ENOMEM.  Device calls are asynchronous.
+ * ---------------------------------------------------------------------- */
+typedef struct harts_attn_sizes {
+  int64_t n_views, n_kv, n_qtiles, n_kvtiles;
+} harts_attn_sizes;
+
+int harts_attn_layout(const harts_plan_t* plan, harts_attn_sizes* out);
+
+int harts_attn_views(const harts_plan_t* plan, int32_t* views, int32_t* kv_rows, int32_t* qtiles,
+                     int32_t* kvtiles, int64_t* row_off, int32_t* row_ent);
+
+int harts_attn_gather(const void* src, const int32_t* kv_rows, int64_t n_kv, int64_t C, int32_t H,
+                      int32_t d, void* dst, void* stream);
+
+int harts_attn_fwd(const int32_t* views, const int32_t* qtiles, int64_t n_qtiles, int32_t H, int32_t d,
+                   float scale, const void* q, const void* kv_k, const void* kv_v, void* o, float* lse,
+                   void* stream);
+
+int harts_attn_bwd(const int32_t* views, const int32_t* qtiles, int64_t n_qtiles, const int32_t* kvtiles,
+                   int64_t n_kvtiles, int64_t C, int32_t H, int32_t d, float scale, const void* q,
+                   const void* kv_k, const void* kv_v, const void* o, const float* lse, const void* dO,
+                   float* delta, void* dq, float* dk_view, float* dv_view, void* stream);
+
+int harts_attn_scatter(const float* src, const int64_t* row_off, const int32_t* row_ent, int64_t C,
+                       int64_t n_kv, int32_t H, int32_t d, void* dst, void* stream);
+
+/* ------------------------------------------------------------------------
  * Compact-to-semantic log-probabilities (Sec. 3.5, eqs. mapped-logp and
  * mapped-logp-grad).  Vocabulary-wide work runs once per compact logit row;
  * only scalar work runs per semantic position, and no S x V tensor exists.

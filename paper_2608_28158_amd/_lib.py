@@ -25,6 +25,8 @@ EXPORTS = (
     "harts_la_saved_size", "harts_state_gather", "harts_replay_reduce",
     "harts_semantic_map", "harts_logp_fwd", "harts_logp_bwd", "harts_mb_plan",
     "harts_conv_context", "harts_conv_workspace_size", "harts_conv_fwd", "harts_conv_bwd",
+    "harts_attn_layout", "harts_attn_views", "harts_attn_gather", "harts_attn_fwd",
+    "harts_attn_bwd", "harts_attn_scatter",
     "harts_profile_begin", "harts_profile_end",
 )
 
@@ -87,6 +89,10 @@ class MbResult(C.Structure):
     _fields_ = [("K", C.c_int32), ("natural_K", C.c_int32), ("work_total", C.c_int64),
                 ("slot_critical", C.c_int64), ("replica_max", C.c_int64),
                 ("trie_work", C.c_int64)]
+
+
+class AttnLayout(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in ("n_views", "n_kv", "n_qtiles", "n_kvtiles")]
 
 
 class KernelTime(C.Structure):
@@ -166,6 +172,19 @@ def lib():
     L.harts_conv_fwd.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp]
     L.harts_conv_bwd.restype = C.c_int
     L.harts_conv_bwd.argtypes = [i32, i64, i32, i32, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, sz, vp]
+    L.harts_attn_layout.restype = C.c_int
+    L.harts_attn_layout.argtypes = [vp, C.POINTER(AttnLayout)]
+    L.harts_attn_views.restype = C.c_int
+    L.harts_attn_views.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    L.harts_attn_gather.restype = C.c_int
+    L.harts_attn_gather.argtypes = [vp, vp, i64, i64, i32, i32, vp, vp]
+    L.harts_attn_fwd.restype = C.c_int
+    L.harts_attn_fwd.argtypes = [vp, vp, i64, i32, i32, f32, vp, vp, vp, vp, vp, vp]
+    L.harts_attn_bwd.restype = C.c_int
+    L.harts_attn_bwd.argtypes = [vp, vp, i64, vp, i64, i64, i32, i32, f32, vp, vp, vp, vp, vp, vp,
+                                 vp, vp, vp, vp, vp]
+    L.harts_attn_scatter.restype = C.c_int
+    L.harts_attn_scatter.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp]
     L.harts_profile_begin.restype = C.c_int
     L.harts_profile_begin.argtypes = []
     L.harts_profile_end.restype = C.c_int

@@ -152,3 +152,94 @@ extern "C" int harts_conv_context(const harts_plan_t* p, int32_t w, int32_t* pre
   return HARTS_OK;
 }
 
+
+// Asymmetric Q/KV views for full attention (Sec. 4.2, eqs. asymmetric-qkv
+// and bottom-right): one view per input sequence of the plan.  Its queries
+// are the sequence's own rows; its key/value row lists the physical rows of
+// the trajectory positions before its first own token (its h ancestors),
+// then its own rows.
+namespace {
+
+// Physical rows of the trajectory positions [0, upto) of segment v's path.
+void ancestor_rows(const harts_plan_t* p, int32_t v, std::vector<int32_t>& path, std::vector<int32_t>& out) {
+  path.clear();
+  for (int32_t u = p->parent[v]; u >= 0; u = p->parent[u]) path.push_back(u);
+  out.clear();
+  for (auto it = path.rbegin(); it != path.rend(); ++it) {
+    const int32_t u = *it;
+    const int64_t len = p->seg_end[u] - p->seg_start[u];
+    for (int64_t k = 0; k < len; ++k) out.push_back(static_cast<int32_t>(p->seg_row[u] + k));
+  }
+}
+
+}  // namespace
+
+extern "C" int harts_attn_layout(const harts_plan_t* p, harts_attn_sizes* out) {
+  if (!p || !out) {
+    set_error("harts_attn_layout: NULL argument");
+    return HARTS_EINVAL;
+  }
+  int64_t n_kv = 0, nq = 0, nk = 0;
+  for (int32_t i = 0; i < p->n_seq; ++i) {
+    const int32_t first = p->chain_seg[p->seq_chain_off[i]];
+    const int64_t h = p->seg_start[first], l = p->seq_n_own[i];
+    n_kv += h + l;
+    nq += (l + 63) / 64;
+    nk += (h + l + 63) / 64;
+  }
+  if (n_kv >= INT32_MAX || p->C >= INT32_MAX) {
+    set_error("harts_attn_layout: more than 2^31 - 1 view rows");
+    return HARTS_EUNSUPPORTED;
+  }
+  out->n_views = p->n_seq;
+  out->n_kv = n_kv;
+  out->n_qtiles = nq;
+  out->n_kvtiles = nk;
+  return HARTS_OK;
+}
+
+extern "C" int harts_attn_views(const harts_plan_t* p, int32_t* views, int32_t* kv_rows, int32_t* qtiles,
+                                int32_t* kvtiles, int64_t* row_off, int32_t* row_ent) {
+  harts_attn_sizes lay;
+  if (int rc = harts_attn_layout(p, &lay)) return rc;
+  if (!views || !kv_rows || !qtiles || !kvtiles || !row_off || !row_ent) {
+    set_error("harts_attn_views: NULL argument");
+    return HARTS_EINVAL;
+  }
+  try {
+    std::vector<int32_t> path, anc;
+    int64_t off = 0, nq = 0, nk = 0;
+    for (int32_t i = 0; i < p->n_seq; ++i) {
+      const int32_t first = p->chain_seg[p->seq_chain_off[i]];
+      ancestor_rows(p, first, path, anc);
+      const int64_t h = static_cast<int64_t>(anc.size()), l = p->seq_n_own[i];
+      views[4 * i + 0] = static_cast<int32_t>(p->seq_row[i]);
+      views[4 * i + 1] = static_cast<int32_t>(l);
+      views[4 * i + 2] = static_cast<int32_t>(off);
+      views[4 * i + 3] = static_cast<int32_t>(h);
+      for (int64_t k = 0; k < h; ++k) kv_rows[off + k] = anc[k];
+      for (int64_t k = 0; k < l; ++k) kv_rows[off + h + k] = static_cast<int32_t>(p->seq_row[i] + k);
+      for (int64_t t0 = 0; t0 < l; t0 += 64, ++nq) {
+        qtiles[2 * nq] = i;
+        qtiles[2 * nq + 1] = static_cast<int32_t>(t0);
+      }
+      for (int64_t k0 = 0; k0 < h + l; k0 += 64, ++nk) {
+        kvtiles[2 * nk] = i;
+        kvtiles[2 * nk + 1] = static_cast<int32_t>(k0);
+      }
+      off += h + l;
+    }
+    // view entries of every compact row, ascending
+    const int64_t C = p->C;
+    std::fill(row_off, row_off + C + 1, 0);
+    for (int64_t e = 0; e < off; ++e) ++row_off[kv_rows[e] + 1];
+    for (int64_t r = 0; r < C; ++r) row_off[r + 1] += row_off[r];
+    std::vector<int64_t> fill(row_off, row_off + C);
+    for (int64_t e = 0; e < off; ++e) row_ent[fill[kv_rows[e]]++] = static_cast<int32_t>(e);
+  } catch (const std::bad_alloc&) {
+    set_error("harts_attn_views: out of host memory");
+    return HARTS_ENOMEM;
+  }
+  set_error("");
+  return HARTS_OK;
+}

@@ -28,7 +28,7 @@ def _runtime(name):
 
 
 HOST_SOURCES = ("plan.cpp", "semantic.cpp", "mbplan.cpp")
-HIP_OBJECTS = ("la.hip.o", "logp.hip.o", "conv.hip.o")
+HIP_OBJECTS = ("la.hip.o", "logp.hip.o", "conv.hip.o", "attn.hip.o")
 
 
 def test_planner_under_asan_and_ubsan(tmp_path):

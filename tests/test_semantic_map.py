@@ -121,3 +121,92 @@ def test_conv_context_follows_each_trajectory(label, parent, seg_len, w):
     expect = [(s, i, int(pred[s, i - 1])) for s in range(C_) for i in range(1, w)
               if pred[s, i - 1] >= 0]
     assert sorted(entries) == sorted(expect)
+
+
+def lib_views(plan):
+    from paper_2608_28158_amd import _lib
+    L = _lib.lib()
+    lay = _lib.AttnLayout()
+    _lib.check(L.harts_attn_layout(plan.handle, C.byref(lay)), "harts_attn_layout")
+    views = np.zeros((lay.n_views, 4), np.int32)
+    kv_rows = np.zeros(lay.n_kv, np.int32)
+    qt = np.zeros((lay.n_qtiles, 2), np.int32)
+    kt = np.zeros((lay.n_kvtiles, 2), np.int32)
+    off = np.zeros(plan["C"] + 1, np.int64)
+    ent = np.zeros(lay.n_kv, np.int32)
+    _lib.check(L.harts_attn_views(plan.handle, views.ctypes.data, kv_rows.ctypes.data, qt.ctypes.data,
+                                  kt.ctypes.data, off.ctypes.data, ent.ctypes.data), "harts_attn_views")
+    return views, kv_rows, qt, kt, off, ent
+
+
+@pytest.mark.parametrize("label,parent,seg_len", CASES + [
+    ("deep chain", [-1, 0, 1, 2, 3, 4], [70, 1, 130, 5, 64, 9])], ids=[c[0] for c in CASES] + ["deep chain"])
+def test_attn_views_follow_each_trajectory(label, parent, seg_len):
+    """Views of Sec. 4.2 (eq. asymmetric-qkv): per plan sequence, the query
+    rows are its own rows and the key/value rows the trajectory positions
+    0 .. h-1 before its first own token, then the own rows; tiles cover
+    every query and key row once; the gradient lists invert kv_rows."""
+    from oracle.compact import sequence_rows
+    from oracle.forest import SegTree
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan(parent, seg_len, 64)
+    t = SegTree(parent, seg_len)
+    phys = phys_index(seg_len, plan["seg_row"])
+    views, kv_rows, qt, kt, off, ent = lib_views(plan)
+    C_ = int(np.sum(seg_len))
+    assert len(views) == plan["n_seq"]
+    seen_q = np.zeros(C_, np.int64)
+    want_q, want_k = [], []
+    for i in range(plan["n_seq"]):
+        _, own = sequence_rows(t, plan, i)
+        v0 = int(plan["chain_seg"][int(plan["seq_chain_off"][i])])
+        anc = [t.row_of(v0, pos) for pos in range(t.s[v0])]
+        q0, l, kvoff, h = (int(x) for x in views[i])
+        assert l == len(own) and h == len(anc)
+        assert np.array_equal(q0 + np.arange(l), phys[own])
+        assert np.array_equal(kv_rows[kvoff:kvoff + h + l], phys[anc + own])
+        seen_q[q0:q0 + l] += 1
+        want_q += [(i, s) for s in range(0, l, 64)]
+        want_k += [(i, s) for s in range(0, h + l, 64)]
+    assert np.all(seen_q == 1)
+    assert [tuple(x) for x in qt] == want_q and [tuple(x) for x in kt] == want_k
+    assert off[0] == 0 and off[-1] == len(kv_rows) and np.all(np.diff(off) >= 1)
+    for r in range(C_):
+        e = ent[off[r]:off[r + 1]]
+        assert np.all(np.diff(e) > 0) and np.all(kv_rows[e] == r)
+
+
+def test_attn_views_on_the_64k_workload():
+    from paper_2608_28158_amd.plan import HartsPlan
+    f, _, cfg = forest_for_config(2)
+    plan = HartsPlan(f.parent, f.seg_len, 64, heads=cfg["H"])
+    views, kv_rows, qt, kt, off, ent = lib_views(plan)
+    h = views[:, 3].astype(np.int64)
+    l = views[:, 1].astype(np.int64)
+    assert l.sum() == f.n_rows and len(kv_rows) == (h + l).sum()
+    assert len(qt) == ((l + 63) // 64).sum() and len(kt) == ((h + l + 63) // 64).sum()
+    assert np.array_equal(np.sort(kv_rows[ent]), np.sort(kv_rows)) and np.all(np.diff(kv_rows[ent]) >= 0)
+
+
+def test_attn_entry_points_validate_before_any_launch():
+    """Unsupported head sizes, NULL and misaligned pointers are rejected on
+    the host (no device work is started, so this runs without a GPU)."""
+    from paper_2608_28158_amd import _lib
+    L = _lib.lib()
+    buf = np.zeros(4096, np.int64)
+    p = buf.ctypes.data
+    f32 = C.c_float(0.1)
+    assert L.harts_attn_fwd(p, p, 1, 2, 96, f32, p, p, p, p, p, None) == _lib.HARTS_EUNSUPPORTED
+    assert L.harts_attn_fwd(p, p, 1, 0, 64, f32, p, p, p, p, p, None) == _lib.HARTS_EUNSUPPORTED
+    assert L.harts_attn_fwd(p, p, 1, 2, 64, f32, None, p, p, p, p, None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_fwd(p, p, 1, 2, 64, f32, p + 2, p, p, p, p, None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_fwd(p, p, -1, 2, 64, f32, p, p, p, p, p, None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_fwd(p, p, 0, 2, 64, f32, p, p, p, p, p, None) == _lib.HARTS_OK
+    assert L.harts_attn_bwd(p, p, 1, p, 1, 10, 2, 128, f32, p, p, p, p, p, p, p, None, p, p,
+                            None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_bwd(p, p, 1, p, 1, 10, 2, 32, f32, p, p, p, p, p, p, p, p, p, p,
+                            None) == _lib.HARTS_EUNSUPPORTED
+    assert L.harts_attn_gather(p, p, -1, 10, 2, 64, p, None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_gather(p, None, 4, 10, 2, 64, p, None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_scatter(p, p, p, 10, 4, 2, 64, p + 4, None) == _lib.HARTS_EINVAL
+    assert L.harts_attn_layout(None, None) == _lib.HARTS_EINVAL
