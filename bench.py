@@ -721,6 +721,139 @@ def conv_measurement(steps, warmup, profile_only=False):
     return out
 
 
+ATTN_H, ATTN_D = 16, 128
+
+
+def attn_measurement(steps, warmup, profile_only=False):
+    """Full attention through asymmetric Q/KV views on the 64k-token
+    microbatch: 68,161 compact query rows, 16 heads of 128, bf16.  One step
+    gathers the key and value views, runs the forward, the backward and the
+    two gradient scatters; the view tables are built once per plan (host).
+    Algorithmic FLOPs count visible (query, key) pairs only: 4 d per pair
+    and head forward (scores, P V), 10 d backward (scores, dP, dV, dK, dQ);
+    the kernels also recompute the scores and dP once more in the dq pass
+    and spend the masked halves of diagonal tiles."""
+    import ctypes as C
+    import torch
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    from workloads import forest_for_config
+    L = _lib.lib()
+    f, _, cfg = forest_for_config(2)
+    H, d = ATTN_H, ATTN_D
+    plan = HartsPlan(f.parent, f.seg_len, 64, heads=H)
+    Cn = f.n_rows
+    t0 = time.perf_counter()
+    lay = _lib.AttnLayout()
+    _lib.check(L.harts_attn_layout(plan.handle, C.byref(lay)), "harts_attn_layout")
+    views = np.zeros((lay.n_views, 4), np.int32)
+    kv_rows = np.zeros(lay.n_kv, np.int32)
+    qt = np.zeros((lay.n_qtiles, 2), np.int32)
+    kt = np.zeros((lay.n_kvtiles, 2), np.int32)
+    off = np.zeros(Cn + 1, np.int64)
+    ent = np.zeros(lay.n_kv, np.int32)
+    _lib.check(L.harts_attn_views(plan.handle, views.ctypes.data, kv_rows.ctypes.data, qt.ctypes.data,
+                                  kt.ctypes.data, off.ctypes.data, ent.ctypes.data), "harts_attn_views")
+    views_ms = (time.perf_counter() - t0) * 1e3
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    vd, kr, qd, kd, od, ed = (dev(a) for a in (views, kv_rows, qt, kt, off, ent))
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(11)
+    q, k, v, dO = (torch.randn((Cn, H, d), device="cuda", generator=gen).to(torch.bfloat16) for _ in range(4))
+    nkv = lay.n_kv
+    kvk = torch.empty((nkv, H, d), dtype=torch.bfloat16, device="cuda")
+    kvv = torch.empty_like(kvk)
+    o, dq, dk, dv = (torch.empty_like(q) for _ in range(4))
+    lse = torch.empty((Cn, H), dtype=torch.float32, device="cuda")
+    delta = torch.empty_like(lse)
+    dkv = torch.empty((nkv, H, d), dtype=torch.float32, device="cuda")
+    dvv = torch.empty_like(dkv)
+    P = lambda x: C.c_void_p(x.data_ptr())
+    stream = torch.cuda.current_stream()
+    st = C.c_void_p(stream.cuda_stream)
+    scale = C.c_float(d ** -0.5)
+
+    def gather():
+        _lib.check(L.harts_attn_gather(P(k), P(kr), nkv, Cn, H, d, P(kvk), st), "harts_attn_gather")
+        _lib.check(L.harts_attn_gather(P(v), P(kr), nkv, Cn, H, d, P(kvv), st), "harts_attn_gather")
+
+    def fwd():
+        _lib.check(L.harts_attn_fwd(P(vd), P(qd), lay.n_qtiles, H, d, scale, P(q), P(kvk), P(kvv), P(o),
+                                    P(lse), st), "harts_attn_fwd")
+
+    def bwd():
+        _lib.check(L.harts_attn_bwd(P(vd), P(qd), lay.n_qtiles, P(kd), lay.n_kvtiles, Cn, H, d, scale, P(q),
+                                    P(kvk), P(kvv), P(o), P(lse), P(dO), P(delta), P(dq), P(dkv), P(dvv), st),
+                   "harts_attn_bwd")
+
+    def scatter():
+        _lib.check(L.harts_attn_scatter(P(dkv), P(od), P(ed), Cn, nkv, H, d, P(dk), st), "harts_attn_scatter")
+        _lib.check(L.harts_attn_scatter(P(dvv), P(od), P(ed), Cn, nkv, H, d, P(dv), st), "harts_attn_scatter")
+
+    def step():
+        gather()
+        fwd()
+        bwd()
+        scatter()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(steps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / steps
+
+    step()
+    ms = {"step": timed(step), "gather": timed(gather), "fwd": timed(fwd), "bwd": timed(bwd),
+          "scatter": timed(scatter)}
+    if profile_only:
+        return None
+    hv = views[:, 3].astype(np.int64)
+    lv = views[:, 1].astype(np.int64)
+    pairs = int(np.sum(lv * hv + lv * (lv + 1) // 2))          # visible (query, key) pairs
+    # pairs of a plain causal pass over every expanded trajectory
+    from oracle.forest import SegTree
+    t = SegTree(f.parent, f.seg_len)
+    traj = np.array([t.s[u] + t.len[u] for u in t.leaves], np.int64)
+    pairs_expanded = int(np.sum(traj * (traj + 1) // 2))
+    fl_f, fl_b = 4 * d * pairs * H, 10 * d * pairs * H
+    tf = lambda fl, m: fl / (m * 1e-3) / 1e12
+    out = {"workload": f"64k-token agentic microbatch: {Cn} compact query rows, {lay.n_views} views, "
+                       f"{nkv} view key rows, {H} heads of {d}, bf16",
+           "ms_per_step": ms["step"], "compact_tok_s": Cn / (ms["step"] * 1e-3), "views_host_ms": views_ms,
+           "visible_pairs": pairs, "expanded_pairs": pairs_expanded,
+           "fwd": {"ms": ms["fwd"], "alg_TFLOP": fl_f / 1e12, "TFLOPs": tf(fl_f, ms["fwd"]),
+                   "mfma_frac": tf(fl_f, ms["fwd"]) / PEAK_BF16_TFLOPS},
+           "bwd": {"ms": ms["bwd"], "alg_TFLOP": fl_b / 1e12, "TFLOPs": tf(fl_b, ms["bwd"]),
+                   "mfma_frac": tf(fl_b, ms["bwd"]) / PEAK_BF16_TFLOPS},
+           "gather_ms": ms["gather"], "scatter_ms": ms["scatter"],
+           "step_TFLOPs": tf(fl_f + fl_b, ms["step"])}
+    # the oracle (fp64, every trajectory) on one tree and one head
+    from oracle.attn import forest_attention
+    tree0 = [u for u in range(t.n) if t.tree[u] == 0]
+    ix = {u: i for i, u in enumerate(tree0)}
+    par = [ix[f.parent[u]] if f.parent[u] >= 0 else -1 for u in tree0]
+    sl = [int(f.seg_len[u]) for u in tree0]
+    rows = np.concatenate([np.arange(t.row0[u], t.row0[u] + t.len[u]) for u in tree0])
+    sub = lambda x: x[:, :1].float().cpu().numpy()[phys_index(f.seg_len, plan["seg_row"])][rows]
+    t1 = time.perf_counter()
+    forest_attention(par, sl, sub(q), sub(k), sub(v), d ** -0.5, dO=sub(dO))
+    cpu_s = time.perf_counter() - t1
+    out["cpu_baseline"] = {"value": len(rows) / H / cpu_s, "unit": "compact rows/s (all heads)",
+                           "cores": torch.get_num_threads(), "kind": "oracle",
+                           "sample": f"tree 0 ({len(rows)} compact rows, {len(par)} segments), 1 of {H} "
+                                     f"heads, forward + backward over every trajectory ({cpu_s:.1f} s), "
+                                     f"scaled by {H}"}
+    del q, k, v, dO, kvk, kvv, dkv, dvv, o, dq, dk, dv
+    torch.cuda.empty_cache()
+    return out
+
+
 def mbplan_measurement(D=4, T=65536):
     """Prefix-aware microbatch/DP planning at the paper's scale: a seeded
     batch of 215 agentic rollout trees at full length (about 1,600
@@ -785,6 +918,9 @@ def main():
     ap.add_argument("--no-logp", action="store_true")
     ap.add_argument("--no-mbplan", action="store_true")
     ap.add_argument("--no-conv", action="store_true")
+    ap.add_argument("--no-attn", action="store_true")
+    ap.add_argument("--attn-only", action="store_true",
+                    help="run the timed attention calls only (for profiler runs)")
     ap.add_argument("--conv-only", action="store_true",
                     help="run the timed convolution calls only (for profiler runs)")
     ap.add_argument("--steps-only", action="store_true",
@@ -813,6 +949,10 @@ def main():
     if args.logp_only:
         logp_measurement(args.steps, args.warmup, profile_only=True)
         log("[bench] logp calls done")
+        return
+    if args.attn_only:
+        attn_measurement(args.steps, args.warmup, profile_only=True)
+        log("[bench] attention calls done")
         return
     if args.conv_only:
         conv_measurement(args.steps, args.warmup, profile_only=True)
@@ -920,6 +1060,9 @@ def main():
     if not args.no_conv:
         log("[bench] causal convolution with ancestor context (6,144 channels)")
         out["conv"] = conv_measurement(args.steps, args.warmup)
+    if not args.no_attn:
+        log("[bench] full attention through asymmetric Q/KV views (16 heads of 128)")
+        out["attn"] = attn_measurement(args.steps, args.warmup)
     if not args.no_mbplan:
         log("[bench] prefix-aware microbatch planning (host)")
         out["mb_plan"] = mbplan_measurement()

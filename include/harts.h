@@ -445,7 +445,9 @@ int harts_conv_bwd(int32_t dtype, int64_t C, int32_t Cch, int32_t w, const void*
  *   views    [n_views][4]: first own row, l, offset in the view rows, h.
  *   kv_rows  [n_kv]: compact row of every view row (views in order).
  *   qtiles   [n_qtiles][2], kvtiles [n_kvtiles][2]: (view, first row) of
- *            every 64-row query tile and key tile.
+ *            every 128-row query tile and key tile, heaviest first (query
+ *            tiles by the keys they see, key tiles by the queries that see
+ *            them; equal work keeps the view order).
  *   row_off  [C+1], row_ent [n_kv]: view rows of every compact row,
  *            ascending (the order of the gradient sums).
  * harts_attn_gather (device) -- dst[e] = src[kv_rows[e]], [rows, H, d] bf16

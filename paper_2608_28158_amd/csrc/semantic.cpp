@@ -172,6 +172,20 @@ void ancestor_rows(const harts_plan_t* p, int32_t v, std::vector<int32_t>& path,
   }
 }
 
+constexpr int64_t kAttnTile = 128;   // rows a workgroup owns
+
+void sort_tiles(int32_t* tiles, const std::vector<int64_t>& work) {
+  const size_t n = work.size();
+  std::vector<size_t> ord(n);
+  for (size_t j = 0; j < n; ++j) ord[j] = j;
+  std::stable_sort(ord.begin(), ord.end(), [&](size_t a, size_t b) { return work[a] > work[b]; });
+  std::vector<int32_t> tmp(tiles, tiles + 2 * n);
+  for (size_t j = 0; j < n; ++j) {
+    tiles[2 * j] = tmp[2 * ord[j]];
+    tiles[2 * j + 1] = tmp[2 * ord[j] + 1];
+  }
+}
+
 }  // namespace
 
 extern "C" int harts_attn_layout(const harts_plan_t* p, harts_attn_sizes* out) {
@@ -184,8 +198,8 @@ extern "C" int harts_attn_layout(const harts_plan_t* p, harts_attn_sizes* out) {
     const int32_t first = p->chain_seg[p->seq_chain_off[i]];
     const int64_t h = p->seg_start[first], l = p->seq_n_own[i];
     n_kv += h + l;
-    nq += (l + 63) / 64;
-    nk += (h + l + 63) / 64;
+    nq += (l + kAttnTile - 1) / kAttnTile;
+    nk += (h + l + kAttnTile - 1) / kAttnTile;
   }
   if (n_kv >= INT32_MAX || p->C >= INT32_MAX) {
     set_error("harts_attn_layout: more than 2^31 - 1 view rows");
@@ -208,6 +222,7 @@ extern "C" int harts_attn_views(const harts_plan_t* p, int32_t* views, int32_t* 
   }
   try {
     std::vector<int32_t> path, anc;
+    std::vector<int64_t> qwork, kwork;   // keys a query tile steps over; queries a key tile does
     int64_t off = 0, nq = 0, nk = 0;
     for (int32_t i = 0; i < p->n_seq; ++i) {
       const int32_t first = p->chain_seg[p->seq_chain_off[i]];
@@ -219,16 +234,22 @@ extern "C" int harts_attn_views(const harts_plan_t* p, int32_t* views, int32_t* 
       views[4 * i + 3] = static_cast<int32_t>(h);
       for (int64_t k = 0; k < h; ++k) kv_rows[off + k] = anc[k];
       for (int64_t k = 0; k < l; ++k) kv_rows[off + h + k] = static_cast<int32_t>(p->seq_row[i] + k);
-      for (int64_t t0 = 0; t0 < l; t0 += 64, ++nq) {
+      for (int64_t t0 = 0; t0 < l; t0 += kAttnTile, ++nq) {
         qtiles[2 * nq] = i;
         qtiles[2 * nq + 1] = static_cast<int32_t>(t0);
+        qwork.push_back(h + t0);
       }
-      for (int64_t k0 = 0; k0 < h + l; k0 += 64, ++nk) {
+      for (int64_t k0 = 0; k0 < h + l; k0 += kAttnTile, ++nk) {
         kvtiles[2 * nk] = i;
         kvtiles[2 * nk + 1] = static_cast<int32_t>(k0);
+        kwork.push_back(l - std::max<int64_t>(0, k0 - h));
       }
       off += h + l;
     }
+    // heaviest tiles first (fewer stragglers at the end of a launch); ties
+    // keep the view order
+    sort_tiles(qtiles, qwork);
+    sort_tiles(kvtiles, kwork);
     // view entries of every compact row, ascending
     const int64_t C = p->C;
     std::fill(row_off, row_off + C + 1, 0);

@@ -34,6 +34,8 @@ def sources_of(kernel=None):
         return ("logp.hip",)
     if kernel and kernel.startswith("k_conv"):
         return ("conv.hip",)
+    if kernel and kernel.startswith("k_attn"):
+        return ("attn.hip", "la_common.hpp")
     return ("la.hip", "la_common.hpp")
 
 
@@ -51,7 +53,8 @@ def short(name):
                 "k_fwd_block", "k_bwd_blockscan", "k_dg_carry", "k_gather", "k_scatter_add",
                 "k_replay_reduce", "k_logp_lse", "k_logp_gather", "k_logp_rowsum",
                 "k_logp_grad", "k_logp_onehot", "k_conv_fwd", "k_conv_dx", "k_conv_dw_part",
-                "k_conv_dw_sum"):
+                "k_conv_dw_sum", "k_attn_fwd", "k_attn_dq", "k_attn_dkdv", "k_attn_delta",
+                "k_attn_gather", "k_attn_scatter"):
         if key in n:
             return key
     return n.replace("void ", "")[:48]
@@ -62,7 +65,8 @@ def stats(src, out, cmd):
     tot = sum(float(r["TotalDurationNs"]) for r in rows)
     lines = ["# rocprofv3 kernel statistics", "", "Command:", "", "    " + " ".join(cmd), "",
              f"Kernel source hashes: la.hip + la_common.hpp {source_sha()}, "
-             f"logp.hip {source_sha('k_logp')}, conv.hip {source_sha('k_conv')}", "",
+             f"logp.hip {source_sha('k_logp')}, conv.hip {source_sha('k_conv')}, "
+             f"attn.hip + la_common.hpp {source_sha('k_attn')}", "",
              "| kernel | calls | total ms | avg us | min us | max us | share |",
              "|---|---|---|---|---|---|---|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
@@ -129,7 +133,9 @@ def counters(out, n_cu, n_xcd, paths, cmd):
     names = sorted({c for d in vals.values() for c in d})
     kernels = sorted(vals, key=lambda k: -vals[k].get("SQ_WAVE_CYCLES", vals[k].get("GRBM_GUI_ACTIVE", 0)))
     lines = ["# rocprofv3 counters per kernel (mean per dispatch)", "", "Command (one run per pass):",
-             "", "    " + " ".join(cmd), "", f"Kernel source hash: {source_sha()}", "",
+             "", "    " + " ".join(cmd), "",
+             "Kernel source hashes: " + ", ".join(sorted({" + ".join(sources_of(k)) + " " + source_sha(k)
+                                                         for k in vals if k.startswith("k_")})), "",
              f"MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {n_xcd} XCDs x {n_cu} CUs "
              "x 4 SIMDs); bf16 MFMA rate = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP / dispatch "
              "duration (peak 2500 TFLOP/s); wait, issue and LDS shares are of SQ_WAVE_CYCLES "

@@ -144,8 +144,9 @@ def lib_views(plan):
 def test_attn_views_follow_each_trajectory(label, parent, seg_len):
     """Views of Sec. 4.2 (eq. asymmetric-qkv): per plan sequence, the query
     rows are its own rows and the key/value rows the trajectory positions
-    0 .. h-1 before its first own token, then the own rows; tiles cover
-    every query and key row once; the gradient lists invert kv_rows."""
+    0 .. h-1 before its first own token, then the own rows; 128-row tiles
+    cover every query and key row once, heaviest first; the gradient lists
+    invert kv_rows."""
     from oracle.compact import sequence_rows
     from oracle.forest import SegTree
     from paper_2608_28158_amd.plan import HartsPlan
@@ -166,10 +167,12 @@ def test_attn_views_follow_each_trajectory(label, parent, seg_len):
         assert np.array_equal(q0 + np.arange(l), phys[own])
         assert np.array_equal(kv_rows[kvoff:kvoff + h + l], phys[anc + own])
         seen_q[q0:q0 + l] += 1
-        want_q += [(i, s) for s in range(0, l, 64)]
-        want_k += [(i, s) for s in range(0, h + l, 64)]
+        want_q += [(h + s, i, s) for s in range(0, l, 128)]
+        want_k += [(l - max(0, s - h), i, s) for s in range(0, h + l, 128)]
     assert np.all(seen_q == 1)
-    assert [tuple(x) for x in qt] == want_q and [tuple(x) for x in kt] == want_k
+    # heaviest first, equal work in view order
+    order = lambda tiles: [(i, s) for _, i, s in sorted(tiles, key=lambda x: (-x[0], x[1], x[2]))]
+    assert [tuple(x) for x in qt] == order(want_q) and [tuple(x) for x in kt] == order(want_k)
     assert off[0] == 0 and off[-1] == len(kv_rows) and np.all(np.diff(off) >= 1)
     for r in range(C_):
         e = ent[off[r]:off[r + 1]]
@@ -184,7 +187,7 @@ def test_attn_views_on_the_64k_workload():
     h = views[:, 3].astype(np.int64)
     l = views[:, 1].astype(np.int64)
     assert l.sum() == f.n_rows and len(kv_rows) == (h + l).sum()
-    assert len(qt) == ((l + 63) // 64).sum() and len(kt) == ((h + l + 63) // 64).sum()
+    assert len(qt) == ((l + 127) // 128).sum() and len(kt) == ((h + l + 127) // 128).sum()
     assert np.array_equal(np.sort(kv_rows[ent]), np.sort(kv_rows)) and np.all(np.diff(kv_rows[ent]) >= 0)
 
 
