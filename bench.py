@@ -57,6 +57,8 @@ def la_source_sha(kernel=None):
         names = ("logp.hip",)
     elif kernel and kernel.startswith("k_conv"):
         names = ("conv.hip",)
+    elif kernel and kernel.startswith("k_attn"):
+        names = ("attn.hip", "la_common.hpp")
     else:
         names = ("la.hip", "la_common.hpp")
     h = hashlib.sha256()
@@ -701,7 +703,7 @@ def conv_measurement(steps, warmup, profile_only=False):
                    "hbm_frac": by_b / (ms_b * 1e-3) / 1e9 / PEAK_HBM_GBS},
            "context_ms": ctx_ms,
            "traffic_k_conv_fwd": read_traffic("k_conv_fwd", "agentic64k_c6144"),
-           "traffic_k_conv_dx": read_traffic("k_conv_dx", "agentic64k_c6144")}
+           "traffic_k_conv_bwd": read_traffic("k_conv_bwd", "agentic64k_c6144")}
     # the oracle (fp64, trajectory by trajectory) on a sample of channels
     from oracle.conv import conv_bwd, conv_fwd
     chs = 8

@@ -52,10 +52,10 @@ def short(name):
     for key in ("k_bwd_revorder", "k_bwd_fwdorder", "k_blocksum", "k_fwd_blockscan",
                 "k_fwd_block", "k_bwd_blockscan", "k_dg_carry", "k_gather", "k_scatter_add",
                 "k_replay_reduce", "k_logp_lse", "k_logp_gather", "k_logp_rowsum",
-                "k_logp_grad", "k_logp_onehot", "k_conv_fwd", "k_conv_dx", "k_conv_dw_part",
+                "k_logp_grad", "k_logp_onehot", "k_conv_fwd", "k_conv_bwd",
                 "k_conv_dw_sum", "k_attn_fwd", "k_attn_dq", "k_attn_dkdv", "k_attn_delta",
                 "k_attn_gather", "k_attn_scatter"):
-        if key in n:
+        if key in name:
             return key
     return n.replace("void ", "")[:48]
 
