@@ -9,8 +9,8 @@
 // semantic.cpp) writes that predecessor table once per plan, and the
 // transposed table of consumers, which the backward walks to gather each
 // row's gradient.
-//   k_conv_fwd      one thread per (4 channels, run of 64 rows);
-//   k_conv_bwd      runs of 128 rows: dx of each row (its own term plus
+//   k_conv_fwd      one thread per (4 channels, run of 32 rows);
+//   k_conv_bwd      runs of 64 rows: dx of each row (its own term plus
 //                   every consumer's, in (tap, row) order) and the run's
 //                   tap sums x[pred_i(r)] dy[r], in row order;
 //   k_conv_dw_sum   per (channel, tap), the runs' partials in a fixed order.
