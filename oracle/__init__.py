@@ -36,8 +36,12 @@ Contents (all float64 unless stated):
 * ``logprob``     -- compact-to-semantic log-probabilities and their gradient
                      (eqs. mapped-logp, mapped-logp-grad), one log-softmax
                      per semantic position.
+* ``kda``         -- KDA, per-channel decay with the delta rule (Sec. 2.2):
+                     the token recurrence, the chunk form of eq. chunk-state,
+                     and trajectory-wise execution over a forest with
+                     gradients by reverse mode.
 
-Recurrence reading used throughout (the paper prints only KDA's chunk update,
-eq. chunk-state): S_t = exp(g_t) S_{t-1} + k_t v_t^T and o_t = scale S_t^T q_t,
+Recurrence reading used by every module but ``kda`` (the paper prints only
+KDA's chunk update, eq. chunk-state): S_t = exp(g_t) S_{t-1} + k_t v_t^T and o_t = scale S_t^T q_t,
 with per-head scalar log-decay g_t and state S of shape [d_k, d_v].
 """
