@@ -489,6 +489,80 @@ int harts_attn_scatter(const float* src, const int64_t* row_off, const int32_t* 
                        int64_t n_kv, int32_t H, int32_t d, void* dst, void* stream);
 
 /* ------------------------------------------------------------------------
+ * KDA: linear attention with per-channel decay and the delta rule (Sec. 2.2,
+ * eq. chunk-state), over the same plan: rounds, replay rows, requested
+ * boundary states and their differentiable handoffs (Sec. 3.4).  Per head,
+ * state S [dk = d][dv = d]:
+ *     S_t = Diag(e^{g_t}) S_{t-1}
+ *           + beta_t k_t (v_t - (Diag(e^{g_t}) S_{t-1})^T k_t)^T,
+ *     o_t = scale S_t^T q_t,
+ * run by chunks of 64 packed rows in the form of eq. chunk-state (the plan
+ * must have chunk 64).  q, k, v, o [C, H, d] (bf16 or float32), g [C, H, d]
+ * float32 log-decays (<= 0), beta [C, H] float32.
+ *
+ * harts_kda_layout / harts_kda_tables (host) -- sizes, then tables:
+ *   chunk_rows [n_chunks][64]: packed rows of every sequence (replay rows,
+ *              then own rows, then padding), in sequence order: physical
+ *              row * 2 + 1 for an own row, * 2 for a replay row, -1 padding.
+ *   seq_tab    [n_seq][8]: round (0-based), first chunk, chunks, initial
+ *              bank entry, first request, requests, final leaf, 0.
+ *   req_tab    [n_req][2]: (chunk c of the sequence, bank entry): the state
+ *              at the start of chunk c (c = chunks: the end state).
+ *   group_tab  [n_groups][4], group_seq [n_seq]: per round, the sequences
+ *              starting from each bank entry (round, entry, first member,
+ *              members), in sequence order -- the order of the adjoint sums.
+ *   row_off [C+1], row_pos [C+R]: packed rows (chunk * 64 + i) of every
+ *              compact row, ascending -- the order of the gradient sums.
+ * harts_kda_workspace_size -- float32 per-(chunk, head) blocks for all
+ *   chunks of the plan (the forward's are read by the backward).
+ * harts_kda_fwd (device) -- one round: chunks [c0, c0 + n_chunks), sequences
+ *   [s0, s0 + n_seq).  bank [n_bank][H][d][d] float32: read at the initial
+ *   entries, written at the requested ones; S_final [n_leaves][H][d][d]
+ *   (may be NULL); o written for own rows (o NULL: states only).
+ * harts_kda_bwd (device) -- one round, after the later rounds' backward:
+ *   dO [C, H, d]; dS_final (may be NULL); dbank [n_bank][H][d][d] holds the
+ *   later rounds' summed initial-state adjoints; writes dS0_seq
+ *   [n_seq][H][d][d] of the round's sequences and, per packed row, the
+ *   float32 gradients pdq, pdk, pdv, pdg [n_chunks * 64][H][d] and pdb
+ *   [n_chunks * 64][H] (padding rows untouched).
+ * harts_kda_bank_add (device) -- dbank[entry] += the group's dS0_seq, for
+ *   groups [g0, g0 + n_groups) (one round's), in member order.
+ * harts_kda_reduce (device) -- dst [C][width] (bf16 or float32) = sum over
+ *   each compact row's packed rows of src [n_pos][width], in row_pos order.
+ * All arithmetic is float32 and deterministic (no atomics).  Errors:
+ * HARTS_EINVAL (NULL, ranges), HARTS_EUNSUPPORTED (dtype, H, d, a plan with
+ * chunk != 64, more than 2^31 - 1 packed rows), HARTS_EHIP, HARTS_ENOMEM.
+ * ---------------------------------------------------------------------- */
+typedef struct harts_kda_sizes {
+  int64_t n_chunks, n_entries;
+  int32_t n_seq, n_rounds, n_groups, n_req;
+} harts_kda_sizes;
+
+int harts_kda_layout(const harts_plan_t* plan, harts_kda_sizes* out);
+
+int harts_kda_tables(const harts_plan_t* plan, int32_t* chunk_rows, int32_t* seq_tab, int32_t* req_tab,
+                     int32_t* group_tab, int32_t* group_seq, int64_t* row_off, int32_t* row_pos);
+
+int harts_kda_workspace_size(int64_t n_chunks, int32_t H, int32_t d, size_t* bytes);
+
+int harts_kda_fwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab, int64_t c0,
+                  int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H, int32_t d, float scale,
+                  const void* q, const void* k, const void* v, const float* g, const float* beta, float* bank,
+                  float* S_final, void* o, float* ws, void* stream);
+
+int harts_kda_bwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab, int64_t c0,
+                  int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H, int32_t d, float scale,
+                  const void* q, const void* k, const void* v, const float* g, const float* beta, const void* dO,
+                  const float* dS_final, const float* dbank, float* dS0_seq, float* ws, float* pdq, float* pdk,
+                  float* pdv, float* pdg, float* pdb, void* stream);
+
+int harts_kda_bank_add(const int32_t* group_tab, int32_t g0, int32_t n_groups, const int32_t* group_seq,
+                       int64_t elems, const float* dS0_seq, float* dbank, void* stream);
+
+int harts_kda_reduce(const float* src, const int64_t* row_off, const int32_t* row_pos, int64_t C, int64_t width,
+                     int64_t n_pos, int32_t dtype, void* dst, void* stream);
+
+/* ------------------------------------------------------------------------
  * Compact-to-semantic log-probabilities (Sec. 3.5, eqs. mapped-logp and
  * mapped-logp-grad).  Vocabulary-wide work runs once per compact logit row;
  * only scalar work runs per semantic position, and no S x V tensor exists.

@@ -27,6 +27,8 @@ EXPORTS = (
     "harts_conv_context", "harts_conv_workspace_size", "harts_conv_fwd", "harts_conv_bwd",
     "harts_attn_layout", "harts_attn_views", "harts_attn_gather", "harts_attn_fwd",
     "harts_attn_bwd", "harts_attn_scatter",
+    "harts_kda_layout", "harts_kda_tables", "harts_kda_workspace_size", "harts_kda_fwd", "harts_kda_bwd",
+    "harts_kda_bank_add", "harts_kda_reduce",
     "harts_profile_begin", "harts_profile_end",
 )
 
@@ -93,6 +95,11 @@ class MbResult(C.Structure):
 
 class AttnLayout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("n_views", "n_kv", "n_qtiles", "n_kvtiles")]
+
+
+class KdaSizes(C.Structure):
+    _fields_ = [("n_chunks", C.c_int64), ("n_entries", C.c_int64)] + \
+        [(n, C.c_int32) for n in ("n_seq", "n_rounds", "n_groups", "n_req")]
 
 
 class KernelTime(C.Structure):
@@ -185,6 +192,20 @@ def lib():
                                  vp, vp, vp, vp, vp]
     L.harts_attn_scatter.restype = C.c_int
     L.harts_attn_scatter.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp, vp]
+    L.harts_kda_layout.restype = C.c_int
+    L.harts_kda_layout.argtypes = [vp, vp]
+    L.harts_kda_tables.restype = C.c_int
+    L.harts_kda_tables.argtypes = [vp] * 8
+    L.harts_kda_workspace_size.restype = C.c_int
+    L.harts_kda_workspace_size.argtypes = [i64, i32, i32, vp]
+    L.harts_kda_fwd.restype = C.c_int
+    L.harts_kda_fwd.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i32, i32, C.c_float] + [vp] * 10
+    L.harts_kda_bwd.restype = C.c_int
+    L.harts_kda_bwd.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i32, i32, C.c_float] + [vp] * 16
+    L.harts_kda_bank_add.restype = C.c_int
+    L.harts_kda_bank_add.argtypes = [vp, i32, i32, vp, i64, vp, vp, vp]
+    L.harts_kda_reduce.restype = C.c_int
+    L.harts_kda_reduce.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp, vp]
     L.harts_profile_begin.restype = C.c_int
     L.harts_profile_begin.argtypes = []
     L.harts_profile_end.restype = C.c_int

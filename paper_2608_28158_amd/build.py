@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libharts.so")
-SOURCES = ["plan.cpp", "semantic.cpp", "mbplan.cpp", "la.hip", "logp.hip", "conv.hip", "attn.hip"]
+SOURCES = ["plan.cpp", "semantic.cpp", "mbplan.cpp", "kda_plan.cpp", "la.hip", "logp.hip", "conv.hip", "attn.hip",
+           "kda.hip"]
 
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -1,0 +1,927 @@
+// KDA over a packed rollout tree: linear attention with per-channel decay and
+// the delta rule (HARTS, Sec. 2.2, eq. chunk-state), forward and backward,
+// for gfx950.
+//
+// Per head, with state S (dk x dv) and per-channel log-decays g <= 0:
+//   S_t = Diag(e^{g_t}) S_{t-1} + beta_t k_t (v_t - (Diag(e^{g_t}) S_{t-1})^T k_t)^T,
+//   o_t = scale S_t^T q_t.
+// By chunks of 64 packed rows, with G the cumulative log-decay inside the
+// chunk and Gamma = e^G (eq. chunk-state):
+//   At[i][j] = sum_d k_i k_j e^{G_i - G_j} (j < i),  L = I + Diag(beta) At,
+//   Tm = L^{-1} Diag(beta),  W = Tm (K * Gamma),  U' = Tm V,
+//   X = U' - W S,  O = scale ((Q * Gamma) S + M X),
+//   M[i][j] = sum_d q_i k_j e^{G_i - G_j} (j <= i),
+//   S_next = Diag(e^{G_B}) S + (K * e^{G_B - G})^T X.
+// Chunk-local quantities are formed in parallel (k_kda_prep); the state
+// recurrence runs per (sequence, head, 32 state columns) over the chunks of
+// the sequence (k_kda_state); outputs again in parallel (k_kda_out).  The
+// backward mirrors it: dX and the state adjoints in reverse chunk order
+// (k_kda_bwd_state), then every chunk-local gradient in parallel
+// (k_kda_bwd_prod, k_kda_bwd_local) into per-packed-row buffers, reduced
+// into compact rows in a fixed order (k_kda_reduce).  Pairwise decays
+// e^{G_i - G_j} (i >= j) are evaluated exactly per channel, never as
+// products of e^{G_i} and e^{-G_j}, so no intermediate overflows.
+//
+// Packed row entries: physical row * 2 + 1 (own row), * 2 (replay row), -1
+// (padding: g = 0, beta = 0, k = q = v = 0, no outputs, no gradients).
+// Arithmetic in float32 throughout; no atomics.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "harts.h"
+#include "plan.hpp"
+
+namespace harts {
+namespace {
+
+typedef __bf16 bf16;
+constexpr int KT = 256;   // threads per workgroup
+constexpr int KB = 64;    // chunk rows
+constexpr int KVS = 32;   // state columns per workgroup in the state passes
+
+template <typename T> __device__ inline float ld(const T* p);
+template <> __device__ inline float ld<float>(const float* p) { return *p; }
+template <> __device__ inline float ld<bf16>(const bf16* p) { return static_cast<float>(*p); }
+template <typename T> __device__ inline void st(T* p, float x);
+template <> __device__ inline void st<float>(float* p, float x) { *p = x; }
+template <> __device__ inline void st<bf16>(bf16* p, float x) { *p = static_cast<bf16>(x); }
+
+// Per-(chunk, head) float32 blocks of the workspace (element offsets per
+// chunk-head given by D).
+template <int D>
+struct WsLay {
+  static constexpr int64_t RD = KB * D;       // 64 x D
+  static constexpr int64_t DD = D * D;
+  static constexpr int64_t BB = KB * KB;
+  // forward
+  static constexpr int64_t W = 0, UP = W + RD, KBM = UP + RD, GAM = KBM + RD, QG = GAM + D, M = QG + RD,
+                           SC = M + BB, X = SC + DD, FWD = X + RD;
+  // backward
+  static constexpr int64_t DXO = FWD, DSO = DXO + RD, DSN = DSO + DD, DX = DSN + DD, DQG = DX + RD,
+                           DW = DQG + RD, DKBM = DW + RD, DM = DKBM + RD, DUV = DM + BB, DGAM = DUV + BB,
+                           DKG = DGAM + D, P1Q = DKG + RD, P1K = P1Q + RD, P1G = P1K + RD, P2K = P1G + RD,
+                           P2G = P2K + RD, ALL = P2G + RD;
+};
+
+// Rows of one packed chunk and head into LDS as float32 [64][D + 1] (zero
+// for padding rows).
+template <typename T, int D>
+__device__ inline void load_rows(float* s, const T* __restrict__ src, const int32_t* ent, int H, int h, int t) {
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, c = idx % D;
+    const int32_t e = ent[r];
+    s[r * (D + 1) + c] = e >= 0 ? ld<T>(src + (static_cast<int64_t>(e >> 1) * H + h) * D + c) : 0.f;
+  }
+}
+
+// Cumulative log-decays of the chunk into sG [64][D + 1] (g of padding rows
+// reads as zero), and beta into sb.
+__device__ inline void load_decay(float* sG, float* sb, const float* __restrict__ g, const float* __restrict__ beta,
+                                  const int32_t* ent, int H, int h, int D, int t) {
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, c = idx % D;
+    const int32_t e = ent[r];
+    sG[r * (D + 1) + c] = e >= 0 ? g[(static_cast<int64_t>(e >> 1) * H + h) * D + c] : 0.f;
+  }
+  if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
+  __syncthreads();
+  if (t < D) {
+    float a = 0.f;
+    for (int r = 0; r < KB; ++r) {
+      a += sG[r * (D + 1) + t];
+      sG[r * (D + 1) + t] = a;
+    }
+  }
+  __syncthreads();
+}
+
+// sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and, if
+// sM, sM[i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere).
+template <int D>
+__device__ inline void pair_sums(float* sA, float* sM, const float* sK, const float* sQ, const float* sG, int t) {
+  constexpr int LD = D + 1;
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    float a = 0.f, m = 0.f;
+    if (j <= i) {
+      const float* ki = sK + i * LD;
+      const float* kj = sK + j * LD;
+      const float* qi = sQ + i * LD;
+      const float* gi = sG + i * LD;
+      const float* gj = sG + j * LD;
+      for (int d = 0; d < D; ++d) {
+        const float e = __expf(gi[d] - gj[d]);
+        a += ki[d] * kj[d] * e;
+        if (sM) m += qi[d] * kj[d] * e;
+      }
+    }
+    sA[i * (KB + 1) + j] = j < i ? a : 0.f;
+    if (sM) sM[i * (KB + 1) + j] = m;
+  }
+}
+
+// sL = (I + Diag(beta) At)^{-1}, unit lower triangular, by forward
+// substitution, one column per thread.
+__device__ inline void tri_inverse(float* sL, const float* sA, const float* sb, int t) {
+  constexpr int LD = KB + 1;
+  if (t < KB) {
+    const int c = t;
+    for (int i = 0; i < KB; ++i) sL[i * LD + c] = i == c ? 1.f : 0.f;
+    for (int i = c + 1; i < KB; ++i) {
+      float s = 0.f;
+      for (int j = c; j < i; ++j) s += sA[i * LD + j] * sL[j * LD + c];
+      sL[i * LD + c] = -sb[i] * s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// forward
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+                                                 const T* __restrict__ q, const T* __restrict__ k,
+                                                 const T* __restrict__ v, const float* __restrict__ g,
+                                                 const float* __restrict__ beta, float* __restrict__ ws) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1;
+  extern __shared__ float sm[];
+  float* sK = sm;
+  float* sQ = sK + KB * LD;
+  float* sG = sQ + KB * LD;
+  float* sA = sG + KB * LD;
+  float* sL = sA + KB * (KB + 1);
+  float* sb = sL + KB * (KB + 1);
+  const int c = static_cast<int>(blockIdx.x / H) + static_cast<int>(c0), h = blockIdx.x % H;
+  const int t = threadIdx.x;
+  const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  load_rows<T, D>(sK, k, ent, H, h, t);
+  load_rows<T, D>(sQ, q, ent, H, h, t);
+  load_decay(sG, sb, g, beta, ent, H, h, D, t);
+  // At and M (M straight to the workspace through sL, then sL is reused)
+  pair_sums<D>(sA, sL, sK, sQ, sG, t);
+  __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) w[Y::M + p] = sL[(p / KB) * (KB + 1) + p % KB];
+  __syncthreads();
+  tri_inverse(sL, sA, sb, t);
+  __syncthreads();
+  // Tm = L^{-1} Diag(beta) into sA
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    sA[i * (KB + 1) + j] = j <= i ? sL[i * (KB + 1) + j] * sb[j] : 0.f;
+  }
+  // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B}; then K -> K e^G in place
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, d = idx % D;
+    const float G = sG[r * LD + d], GB = sG[(KB - 1) * LD + d];
+    w[Y::KBM + idx] = sK[r * LD + d] * __expf(GB - G);
+    w[Y::QG + idx] = sQ[r * LD + d] * __expf(G);
+  }
+  if (t < D) w[Y::GAM + t] = __expf(sG[(KB - 1) * LD + t]);
+  __syncthreads();
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, d = idx % D;
+    sK[r * LD + d] *= __expf(sG[r * LD + d]);
+  }
+  load_rows<T, D>(sQ, v, ent, H, h, t);   // V into the Q tile
+  __syncthreads();
+  // W = Tm (K e^G), U' = Tm V
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int i = idx / D, d = idx % D;
+    float a = 0.f, u = 0.f;
+    for (int j = 0; j <= i; ++j) {
+      const float tm = sA[i * (KB + 1) + j];
+      a += tm * sK[j * LD + d];
+      u += tm * sQ[j * LD + d];
+    }
+    w[Y::W + idx] = a;
+    w[Y::UP + idx] = u;
+  }
+}
+
+// One (sequence, head, 32 state columns): the chunks of the sequence in
+// order.  S starts from the sequence's bank entry; the state at the start of
+// every requested chunk goes to its bank entry, the end state to S_final.
+template <int D>
+__global__ __launch_bounds__(KT) void k_kda_state(const int32_t* __restrict__ seq_tab, int32_t s0,
+                                                  const int32_t* __restrict__ req_tab, int H, float* __restrict__ ws,
+                                                  float* __restrict__ bank, float* __restrict__ S_final) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1, NS = D / KVS;
+  constexpr int LV = KVS + 1;
+  extern __shared__ float sm[];
+  float* sW = sm;                 // [64][D + 1]
+  float* sKB = sW + KB * LD;      // [64][D + 1]
+  float* sS = sKB + KB * LD;      // [D][KVS + 1]
+  float* sX = sS + D * LV;        // [64][KVS + 1]
+  float* sg = sX + KB * LV;       // [D]
+  const int b = blockIdx.x;
+  const int slab = b % NS, h = (b / NS) % H, seq = s0 + b / (NS * H);
+  const int t = threadIdx.x;
+  const int32_t* st_ = seq_tab + 8 * seq;
+  const int c_first = st_[1], nc = st_[2], init = st_[3], ro = st_[4], nr = st_[5], leaf = st_[6];
+  const int v0 = slab * KVS;
+  auto state_at = [&](float* base, int64_t entry) {   // [entry][H][D][D] slab pointer
+    return base + (entry * H + h) * Y::DD;
+  };
+  {
+    const float* s = state_at(bank, init);
+    for (int idx = t; idx < D * KVS; idx += KT) sS[(idx / KVS) * LV + idx % KVS] = s[(idx / KVS) * D + v0 + idx % KVS];
+  }
+  __syncthreads();
+  int rq = 0;
+  for (int cc = 0; cc <= nc; ++cc) {
+    // requested boundary states at the start of chunk cc (cc == nc: the end)
+    for (; rq < nr && req_tab[2 * (ro + rq)] <= cc; ++rq) {
+      if (req_tab[2 * (ro + rq)] != cc) continue;
+      float* d = state_at(bank, req_tab[2 * (ro + rq) + 1]);
+      for (int idx = t; idx < D * KVS; idx += KT) d[(idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+    }
+    if (cc == nc) break;
+    const int64_t ch = static_cast<int64_t>(c_first + cc) * H + h;
+    float* w = ws + ch * Y::ALL;
+    for (int idx = t; idx < KB * D; idx += KT) {
+      sW[(idx / D) * LD + idx % D] = w[Y::W + idx];
+      sKB[(idx / D) * LD + idx % D] = w[Y::KBM + idx];
+    }
+    if (t < D) sg[t] = w[Y::GAM + t];
+    for (int idx = t; idx < D * KVS; idx += KT)      // chunk start state, for the outputs and the backward
+      w[Y::SC + (idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+    __syncthreads();
+    // X = U' - W S
+    for (int idx = t; idx < KB * KVS; idx += KT) {
+      const int i = idx / KVS, vv = idx % KVS;
+      float a = w[Y::UP + i * D + v0 + vv];
+      for (int d = 0; d < D; ++d) a -= sW[i * LD + d] * sS[d * LV + vv];
+      sX[i * LV + vv] = a;
+      w[Y::X + i * D + v0 + vv] = a;
+    }
+    __syncthreads();
+    // S = Diag(gamma) S + KB^T X
+    for (int idx = t; idx < D * KVS; idx += KT) {
+      const int d = idx / KVS, vv = idx % KVS;
+      float a = sg[d] * sS[d * LV + vv];
+      for (int i = 0; i < KB; ++i) a += sKB[i * LD + d] * sX[i * LV + vv];
+      sS[d * LV + vv] = a;
+    }
+    __syncthreads();
+  }
+  if (S_final) {
+    float* d = state_at(S_final, leaf);
+    for (int idx = t; idx < D * KVS; idx += KT) d[(idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+  }
+}
+
+// Outputs of one (chunk, head, 64 state columns): O = scale (QG S + M X),
+// written for own rows only.
+template <typename T, int D>
+__global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+                                                float scale, const float* __restrict__ ws, T* __restrict__ o) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1, VH = 64, LV = VH + 1, NV = D / VH;
+  extern __shared__ float sm[];
+  float* sQG = sm;                // [64][D + 1]
+  float* sS = sQG + KB * LD;      // [D][65]
+  float* sM = sS + D * LV;        // [64][65]
+  float* sX = sM + KB * (KB + 1); // [64][65]
+  const int b = blockIdx.x;
+  const int half = b % NV, h = (b / NV) % H, c = static_cast<int>(b / (NV * H) + c0);
+  const int t = threadIdx.x, v0 = half * VH;
+  const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  const float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  for (int idx = t; idx < KB * D; idx += KT) sQG[(idx / D) * LD + idx % D] = w[Y::QG + idx];
+  for (int idx = t; idx < D * VH; idx += KT) sS[(idx / VH) * LV + idx % VH] = w[Y::SC + (idx / VH) * D + v0 + idx % VH];
+  for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * (KB + 1) + idx % KB] = w[Y::M + idx];
+  for (int idx = t; idx < KB * VH; idx += KT) sX[(idx / VH) * LV + idx % VH] = w[Y::X + (idx / VH) * D + v0 + idx % VH];
+  __syncthreads();
+  for (int idx = t; idx < KB * VH; idx += KT) {
+    const int i = idx / VH, vv = idx % VH;
+    const int32_t e = ent[i];
+    if (e < 0 || !(e & 1)) continue;
+    float a = 0.f;
+    for (int d = 0; d < D; ++d) a += sQG[i * LD + d] * sS[d * LV + vv];
+    for (int j = 0; j <= i; ++j) a += sM[i * (KB + 1) + j] * sX[j * LV + vv];
+    st<T>(o + (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vv, scale * a);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// backward
+// ---------------------------------------------------------------------------
+// dXo = scale M^T dO (64 x D), dSo = scale QG^T dO (D x D), dO of own rows.
+template <typename T, int D>
+__global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+                                                     float scale, const T* __restrict__ dO, float* __restrict__ ws) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1;
+  extern __shared__ float sm[];
+  float* sQG = sm;                 // [64][D + 1]
+  float* sD = sQG + KB * LD;       // [64][D + 1]
+  float* sM = sD + KB * LD;        // [64][65]
+  const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
+  const int t = threadIdx.x;
+  const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, d = idx % D;
+    const int32_t e = ent[r];
+    sQG[r * LD + d] = w[Y::QG + idx];
+    sD[r * LD + d] = (e >= 0 && (e & 1)) ? ld<T>(dO + (static_cast<int64_t>(e >> 1) * H + h) * D + d) : 0.f;
+  }
+  for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * (KB + 1) + idx % KB] = w[Y::M + idx];
+  __syncthreads();
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int j = idx / D, vv = idx % D;
+    float a = 0.f;
+    for (int i = j; i < KB; ++i) a += sM[i * (KB + 1) + j] * sD[i * LD + vv];
+    w[Y::DXO + idx] = scale * a;
+  }
+  for (int idx = t; idx < D * D; idx += KT) {
+    const int d = idx / D, vv = idx % D;
+    float a = 0.f;
+    for (int i = 0; i < KB; ++i) a += sQG[i * LD + d] * sD[i * LD + vv];
+    w[Y::DSO + idx] = scale * a;
+  }
+}
+
+// Reverse state pass of one (sequence, head, 32 columns): dSn of every chunk
+// (the adjoint of its end state), dX = dXo + KB dSn, and
+// dS = Diag(gamma) dSn + dSo - W^T dX, plus the later rounds' adjoints of the
+// requested states; the adjoint of the initial state goes to dS0_seq.
+template <int D>
+__global__ __launch_bounds__(KT) void k_kda_bwd_state(const int32_t* __restrict__ seq_tab, int32_t s0,
+                                                      const int32_t* __restrict__ req_tab, int H,
+                                                      float* __restrict__ ws, const float* __restrict__ dS_final,
+                                                      const float* __restrict__ dbank, float* __restrict__ dS0_seq) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1, NS = D / KVS, LV = KVS + 1;
+  extern __shared__ float sm[];
+  float* sW = sm;
+  float* sKB = sW + KB * LD;
+  float* sS = sKB + KB * LD;     // dS [D][KVS + 1]
+  float* sX = sS + D * LV;       // dX [64][KVS + 1]
+  float* sg = sX + KB * LV;
+  const int b = blockIdx.x;
+  const int slab = b % NS, h = (b / NS) % H, seq = s0 + b / (NS * H);
+  const int t = threadIdx.x;
+  const int32_t* st_ = seq_tab + 8 * seq;
+  const int c_first = st_[1], nc = st_[2], ro = st_[4], nr = st_[5], leaf = st_[6];
+  const int v0 = slab * KVS;
+  auto slab_of = [&](const float* base, int64_t entry) { return base + (entry * H + h) * Y::DD; };
+  for (int idx = t; idx < D * KVS; idx += KT) {
+    const int d = idx / KVS, vv = idx % KVS;
+    float a = dS_final ? slab_of(dS_final, leaf)[d * D + v0 + vv] : 0.f;
+    for (int r = 0; r < nr; ++r)
+      if (req_tab[2 * (ro + r)] == nc) a += slab_of(dbank, req_tab[2 * (ro + r) + 1])[d * D + v0 + vv];
+    sS[d * LV + vv] = a;
+  }
+  __syncthreads();
+  for (int cc = nc - 1; cc >= 0; --cc) {
+    const int64_t ch = static_cast<int64_t>(c_first + cc) * H + h;
+    float* w = ws + ch * Y::ALL;
+    for (int idx = t; idx < KB * D; idx += KT) {
+      sW[(idx / D) * LD + idx % D] = w[Y::W + idx];
+      sKB[(idx / D) * LD + idx % D] = w[Y::KBM + idx];
+    }
+    if (t < D) sg[t] = w[Y::GAM + t];
+    for (int idx = t; idx < D * KVS; idx += KT)
+      w[Y::DSN + (idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+    __syncthreads();
+    for (int idx = t; idx < KB * KVS; idx += KT) {
+      const int i = idx / KVS, vv = idx % KVS;
+      float a = w[Y::DXO + i * D + v0 + vv];
+      for (int d = 0; d < D; ++d) a += sKB[i * LD + d] * sS[d * LV + vv];
+      sX[i * LV + vv] = a;
+      w[Y::DX + i * D + v0 + vv] = a;
+    }
+    __syncthreads();
+    for (int idx = t; idx < D * KVS; idx += KT) {
+      const int d = idx / KVS, vv = idx % KVS;
+      float a = sg[d] * sS[d * LV + vv] + w[Y::DSO + d * D + v0 + vv];
+      for (int i = 0; i < KB; ++i) a -= sW[i * LD + d] * sX[i * LV + vv];
+      for (int r = 0; r < nr; ++r)
+        if (req_tab[2 * (ro + r)] == cc) a += slab_of(dbank, req_tab[2 * (ro + r) + 1])[d * D + v0 + vv];
+      sS[d * LV + vv] = a;
+    }
+    __syncthreads();
+  }
+  float* d0 = dS0_seq + (static_cast<int64_t>(seq) * H + h) * Y::DD;
+  for (int idx = t; idx < D * KVS; idx += KT) d0[(idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+}
+
+// Products of one (chunk, head) with its states, contracted over the value
+// index: dQG = scale dO S^T, dW = -dX S^T, dKB = X dSn^T, dgamma =
+// rowsum(dSn * S), dM = scale dO X^T (j <= i), dUV = dX V^T (j <= i).
+template <typename T, int D>
+__global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+                                                     float scale, const T* __restrict__ v, const T* __restrict__ dO,
+                                                     float* __restrict__ ws) {
+  using Y = WsLay<D>;
+  constexpr int VS = 32, LV = VS + 1;
+  extern __shared__ float sm[];
+  float* sS = sm;                 // [D][33] slab of S
+  float* sN = sS + D * LV;        // [D][33] slab of dSn
+  float* sO = sN + D * LV;        // [64][33] dO
+  float* sDX = sO + KB * LV;      // [64][33] dX
+  float* sX = sDX + KB * LV;      // [64][33] X
+  float* sV = sX + KB * LV;       // [64][33] V
+  const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
+  const int t = threadIdx.x;
+  const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  // accumulators: thread t owns rows/cols of the 64 x D outputs at idx = t + 256 n
+  constexpr int NR = KB * D / KT, NP = KB * KB / KT;
+  float aQ[NR], aW[NR], aK[NR], aM[NP], aU[NP], aG = 0.f;
+#pragma unroll
+  for (int n = 0; n < NR; ++n) aQ[n] = aW[n] = aK[n] = 0.f;
+#pragma unroll
+  for (int n = 0; n < NP; ++n) aM[n] = aU[n] = 0.f;
+  for (int v0 = 0; v0 < D; v0 += VS) {
+    __syncthreads();
+    for (int idx = t; idx < D * VS; idx += KT) {
+      const int d = idx / VS, vv = idx % VS;
+      sS[d * LV + vv] = w[Y::SC + d * D + v0 + vv];
+      sN[d * LV + vv] = w[Y::DSN + d * D + v0 + vv];
+    }
+    for (int idx = t; idx < KB * VS; idx += KT) {
+      const int i = idx / VS, vv = idx % VS;
+      const int32_t e = ent[i];
+      const int64_t row = (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vv;
+      sO[i * LV + vv] = (e >= 0 && (e & 1)) ? ld<T>(dO + row) : 0.f;
+      sV[i * LV + vv] = e >= 0 ? ld<T>(v + row) : 0.f;
+      sDX[i * LV + vv] = w[Y::DX + i * D + v0 + vv];
+      sX[i * LV + vv] = w[Y::X + i * D + v0 + vv];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int n = 0; n < NR; ++n) {
+      const int idx = t + KT * n, i = idx / D, d = idx % D;
+      float q_ = 0.f, w_ = 0.f, k_ = 0.f;
+#pragma unroll 4
+      for (int vv = 0; vv < VS; ++vv) {
+        const float s = sS[d * LV + vv];
+        q_ += sO[i * LV + vv] * s;
+        w_ += sDX[i * LV + vv] * s;
+        k_ += sX[i * LV + vv] * sN[d * LV + vv];
+      }
+      aQ[n] += q_;
+      aW[n] += w_;
+      aK[n] += k_;
+    }
+#pragma unroll
+    for (int n = 0; n < NP; ++n) {
+      const int idx = t + KT * n, i = idx / KB, j = idx % KB;
+      if (j > i) continue;
+      float m_ = 0.f, u_ = 0.f;
+#pragma unroll 4
+      for (int vv = 0; vv < VS; ++vv) {
+        m_ += sO[i * LV + vv] * sX[j * LV + vv];
+        u_ += sDX[i * LV + vv] * sV[j * LV + vv];
+      }
+      aM[n] += m_;
+      aU[n] += u_;
+    }
+    if (t < D)
+      for (int vv = 0; vv < VS; ++vv) aG += sN[t * LV + vv] * sS[t * LV + vv];
+  }
+#pragma unroll
+  for (int n = 0; n < NR; ++n) {
+    const int idx = t + KT * n;
+    w[Y::DQG + idx] = scale * aQ[n];
+    w[Y::DW + idx] = -aW[n];
+    w[Y::DKBM + idx] = aK[n];
+  }
+#pragma unroll
+  for (int n = 0; n < NP; ++n) {
+    const int idx = t + KT * n, i = idx / KB, j = idx % KB;
+    w[Y::DM + idx] = j <= i ? scale * aM[n] : 0.f;
+    w[Y::DUV + idx] = j <= i ? aU[n] : 0.f;
+  }
+  if (t < D) w[Y::DGAM + t] = aG;
+}
+
+// Chunk-local gradients of one (chunk, head): through Tm = L^{-1} Diag(beta),
+// L = I + Diag(beta) At, the pairwise decays of At and M, the decayed K, Q
+// and the cumulative sum of g.  Writes dq, dk, dv, dg [packed row][H][D] and
+// dbeta [packed row][H] for every real packed row.
+template <typename T, int D>
+__global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+                                                      const T* __restrict__ q, const T* __restrict__ k,
+                                                      const float* __restrict__ g, const float* __restrict__ beta,
+                                                      float* __restrict__ ws, float* __restrict__ pdq,
+                                                      float* __restrict__ pdk, float* __restrict__ pdv,
+                                                      float* __restrict__ pdg, float* __restrict__ pdb) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1, LB = KB + 1;
+  extern __shared__ float sm[];
+  float* sK = sm;                  // [64][D + 1] k
+  float* sQ = sK + KB * LD;        // [64][D + 1] q
+  float* sG = sQ + KB * LD;        // [64][D + 1] cumulative log-decay
+  float* sA = sG + KB * LD;        // [64][65] At, later dM
+  float* sL = sA + KB * LB;        // [64][65] L^{-1}
+  float* sT = sL + KB * LB;        // [64][65] dTm -> dLinv -> Y -> dA
+  float* sb = sT + KB * LB;        // [64] beta
+  float* sdb = sb + KB;            // [64] dbeta
+  const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
+  const int t = threadIdx.x;
+  const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  load_rows<T, D>(sK, k, ent, H, h, t);
+  load_rows<T, D>(sQ, q, ent, H, h, t);
+  load_decay(sG, sb, g, beta, ent, H, h, D, t);
+  pair_sums<D>(sA, nullptr, sK, sQ, sG, t);
+  __syncthreads();
+  tri_inverse(sL, sA, sb, t);
+  __syncthreads();
+  // dTm = dUV + dW (K e^G)^T  (j <= i)
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    float a = 0.f;
+    if (j <= i) {
+      a = w[Y::DUV + p];
+      const float* dw = w + Y::DW + static_cast<int64_t>(i) * D;
+      for (int d = 0; d < D; ++d) a += dw[d] * sK[j * LD + d] * __expf(sG[j * LD + d]);
+    }
+    sT[i * LB + j] = a;
+  }
+  __syncthreads();
+  // dV = Tm^T dX, dK e^G part = Tm^T dW (Tm[i][j] = L^{-1}[i][j] beta_j)
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int j = idx / D, d = idx % D;
+    float av = 0.f, ak = 0.f;
+    for (int i = j; i < KB; ++i) {
+      const float tm = sL[i * LB + j] * sb[j];
+      av += tm * w[Y::DX + i * D + d];
+      ak += tm * w[Y::DW + i * D + d];
+    }
+    const int32_t e = ent[j];
+    if (e >= 0) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + d] = av;
+    w[Y::DKG + idx] = ak;
+  }
+  // dbeta_j (Tm part) = sum_i dTm[i][j] L^{-1}[i][j]; dLinv = dTm Diag(beta)
+  if (t < KB) {
+    float a = 0.f;
+    for (int i = t; i < KB; ++i) a += sT[i * LB + t] * sL[i * LB + t];
+    sdb[t] = a;
+  }
+  __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) sT[(p / KB) * LB + p % KB] *= sb[p % KB];
+  __syncthreads();
+  // Y = dLinv L^{-T}: row a by thread a (Y[a][j] = sum_b dLinv[a][b] Linv[j][b], b <= min(a, j))
+  if (t < KB) {
+    float row[KB];
+    for (int bb = 0; bb < KB; ++bb) row[bb] = sT[t * LB + bb];
+    for (int j = 0; j < KB; ++j) {
+      float a = 0.f;
+      const int m = t < j ? t : j;
+      for (int bb = 0; bb <= m; ++bb) a += row[bb] * sL[j * LB + bb];
+      sT[t * LB + j] = a;
+    }
+  }
+  __syncthreads();
+  // dA = -(L^{-T} Y), strictly lower: column j by thread j (dA[i][j] = -sum_{a >= i} Linv[a][i] Y[a][j])
+  if (t < KB) {
+    float col[KB];
+    for (int a = 0; a < KB; ++a) col[a] = sT[a * LB + t];
+    for (int i = 0; i < KB; ++i) {
+      float s = 0.f;
+      for (int a = i; a < KB; ++a) s += sL[a * LB + i] * col[a];
+      sT[i * LB + t] = i > t ? -s : 0.f;
+    }
+  }
+  __syncthreads();
+  // dbeta_i += sum_j dA_ij At_ij; then dAt = Diag(beta) dA into sT, dM into sA
+  if (t < KB) {
+    float a = 0.f;
+    for (int j = 0; j < t; ++j) a += sT[t * LB + j] * sA[t * LB + j];
+    sdb[t] += a;
+  }
+  __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    sT[i * LB + j] *= sb[i];
+    sA[i * LB + j] = w[Y::DM + p];
+  }
+  __syncthreads();
+  // pairwise terms, per channel: threads 0..D-1 take row i's own terms
+  // (dq_i, dk_i, +dG_i), threads 128..128+D-1 the terms of column j (dk_j, -dG_j)
+  if (t < D) {
+    const int d = t;
+    for (int i = 0; i < KB; ++i) {
+      const float gi = sG[i * LD + d], ki = sK[i * LD + d], qi = sQ[i * LD + d];
+      float dq_ = 0.f, dk_ = 0.f, dg_ = 0.f;
+      for (int j = 0; j <= i; ++j) {
+        const float e = __expf(gi - sG[j * LD + d]);
+        const float kj = sK[j * LD + d];
+        const float ta = sT[i * LB + j] * e;     // 0 on the diagonal
+        const float tm = sA[i * LB + j] * e;
+        dk_ += ta * kj;
+        dq_ += tm * kj;
+        dg_ += (ta * ki + tm * qi) * kj;
+      }
+      w[Y::P1Q + i * D + d] = dq_;
+      w[Y::P1K + i * D + d] = dk_;
+      w[Y::P1G + i * D + d] = dg_;
+    }
+  } else if (t >= 128 && t < 128 + D) {
+    const int d = t - 128;
+    for (int j = 0; j < KB; ++j) {
+      const float gj = sG[j * LD + d], kj = sK[j * LD + d];
+      float dk_ = 0.f, dg_ = 0.f;
+      for (int i = j; i < KB; ++i) {
+        const float e = __expf(sG[i * LD + d] - gj);
+        const float x = (sT[i * LB + j] * sK[i * LD + d] + sA[i * LB + j] * sQ[i * LD + d]) * e;
+        dk_ += x;
+        dg_ += x * kj;
+      }
+      w[Y::P2K + j * D + d] = dk_;
+      w[Y::P2G + j * D + d] = dg_;
+    }
+  }
+  __syncthreads();
+  // elementwise terms and the reverse cumulative sum of dG; thread per channel
+  if (t < D) {
+    const int d = t;
+    const float GB = sG[(KB - 1) * LD + d];
+    float dGB = w[Y::DGAM + d] * __expf(GB), run = 0.f;
+    for (int i = 0; i < KB; ++i) {
+      const float kb = sK[i * LD + d] * __expf(GB - sG[i * LD + d]);
+      dGB += w[Y::DKBM + i * D + d] * kb;
+    }
+    for (int i = KB - 1; i >= 0; --i) {
+      const float G = sG[i * LD + d], eG = __expf(G), ki = sK[i * LD + d], qi = sQ[i * LD + d];
+      const float kb = ki * __expf(GB - G);
+      const float dqg = w[Y::DQG + i * D + d], dkg = w[Y::DKG + i * D + d], dkb = w[Y::DKBM + i * D + d];
+      const float dq_ = w[Y::P1Q + i * D + d] + dqg * eG;
+      const float dk_ = w[Y::P1K + i * D + d] + w[Y::P2K + i * D + d] + dkg * eG + dkb * __expf(GB - G);
+      float dG = w[Y::P1G + i * D + d] - w[Y::P2G + i * D + d] + dqg * qi * eG + dkg * ki * eG - dkb * kb;
+      if (i == KB - 1) dG += dGB;
+      run += dG;
+      const int32_t e = ent[i];
+      if (e >= 0) {
+        const int64_t o = (static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d;
+        pdq[o] = dq_;
+        pdk[o] = dk_;
+        pdg[o] = run;
+      }
+    }
+  }
+  if (t < KB && ent[t] >= 0) pdb[(static_cast<int64_t>(c) * KB + t) * H + h] = sdb[t];
+}
+
+// Compact rows <- sum of their packed rows, in ascending packed order.
+__global__ __launch_bounds__(KT) void k_kda_reduce(const float* __restrict__ src, const int64_t* __restrict__ row_off,
+                                                   const int32_t* __restrict__ row_pos, int64_t C, int64_t width,
+                                                   int64_t n_pos, void* __restrict__ dst, int to_bf16) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * KT + threadIdx.x;
+  if (idx >= C * width) return;
+  const int64_t r = idx / width, x = idx % width;
+  float a = 0.f;
+  for (int64_t j = row_off[r]; j < row_off[r + 1]; ++j) {
+    const int32_t p = row_pos[j];
+    if (p >= 0 && p < n_pos) a += src[static_cast<int64_t>(p) * width + x];
+  }
+  if (to_bf16) static_cast<bf16*>(dst)[idx] = static_cast<bf16>(a);
+  else static_cast<float*>(dst)[idx] = a;
+}
+
+// dbank[bank of group] += sum of dS0_seq over the group's sequences, in order.
+__global__ __launch_bounds__(KT) void k_kda_bank_add(const int32_t* __restrict__ group_tab, int32_t g0,
+                                                     const int32_t* __restrict__ group_seq, int64_t elems,
+                                                     const float* __restrict__ dS0_seq, float* __restrict__ dbank) {
+  const int gi = g0 + static_cast<int>(blockIdx.y);
+  const int64_t x = static_cast<int64_t>(blockIdx.x) * KT + threadIdx.x;
+  if (x >= elems) return;
+  const int32_t* gt = group_tab + 4 * gi;
+  float a = dbank[static_cast<int64_t>(gt[1]) * elems + x];
+  for (int m = 0; m < gt[3]; ++m) a += dS0_seq[static_cast<int64_t>(group_seq[gt[2] + m]) * elems + x];
+  dbank[static_cast<int64_t>(gt[1]) * elems + x] = a;
+}
+
+int kda_status(const char* where) {
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error(std::string(where) + ": " + hipGetErrorString(e));
+    return HARTS_EHIP;
+  }
+  return HARTS_OK;
+}
+
+template <int D>
+constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB) * sizeof(float); }
+template <int D>
+constexpr size_t lds_state() { return (2 * KB * (D + 1) + D * (KVS + 1) + KB * (KVS + 1) + D) * sizeof(float); }
+template <int D>
+constexpr size_t lds_out() { return (KB * (D + 1) + D * 65 + 2 * KB * (KB + 1)) * sizeof(float); }
+template <int D>
+constexpr size_t lds_bprep() { return (2 * KB * (D + 1) + KB * (KB + 1)) * sizeof(float); }
+template <int D>
+constexpr size_t lds_bprod() { return (2 * D * 33 + 4 * KB * 33) * sizeof(float); }
+template <int D>
+constexpr size_t lds_blocal() { return (3 * KB * (D + 1) + 3 * KB * (KB + 1) + 2 * KB) * sizeof(float); }
+
+struct KdaArgs {
+  const int32_t* chunk_rows;
+  const int32_t* seq_tab;
+  const int32_t* req_tab;
+  int64_t c0, n_chunks;
+  int32_t s0, n_seq;
+  int32_t H;
+  float scale;
+};
+
+template <typename T, int D>
+int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, const float* g, const float* beta,
+                 float* bank, float* S_final, void* o, float* ws, hipStream_t s) {
+  const auto* tq = static_cast<const T*>(q);
+  const auto* tk = static_cast<const T*>(k);
+  const auto* tv = static_cast<const T*>(v);
+  if (a.n_chunks > 0) {
+    hipLaunchKernelGGL((k_kda_prep<T, D>), dim3(static_cast<uint32_t>(a.n_chunks * a.H)), dim3(KT), lds_prep<D>(), s,
+                       a.chunk_rows, a.c0, a.H, tq, tk, tv, g, beta, ws);
+    if (int rc = kda_status("k_kda_prep")) return rc;
+  }
+  if (a.n_seq > 0) {
+    hipLaunchKernelGGL((k_kda_state<D>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / KVS))), dim3(KT),
+                       lds_state<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final);
+    if (int rc = kda_status("k_kda_state")) return rc;
+  }
+  if (a.n_chunks > 0 && o) {
+    hipLaunchKernelGGL((k_kda_out<T, D>), dim3(static_cast<uint32_t>(a.n_chunks * a.H * (D / 64))), dim3(KT),
+                       lds_out<D>(), s, a.chunk_rows, a.c0, a.H, a.scale, ws, static_cast<T*>(o));
+    if (int rc = kda_status("k_kda_out")) return rc;
+  }
+  return HARTS_OK;
+}
+
+template <typename T, int D>
+int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, const float* g, const float* beta,
+                 const void* dO, const float* dS_final, const float* dbank, float* dS0_seq, float* ws, float* pdq,
+                 float* pdk, float* pdv, float* pdg, float* pdb, hipStream_t s) {
+  const auto* tq = static_cast<const T*>(q);
+  const auto* tk = static_cast<const T*>(k);
+  const auto* tv = static_cast<const T*>(v);
+  const auto* td = static_cast<const T*>(dO);
+  const uint32_t gc = static_cast<uint32_t>(a.n_chunks * a.H);
+  if (a.n_chunks > 0) {
+    hipLaunchKernelGGL((k_kda_bwd_prep<T, D>), dim3(gc), dim3(KT), lds_bprep<D>(), s, a.chunk_rows, a.c0, a.H,
+                       a.scale, td, ws);
+    if (int rc = kda_status("k_kda_bwd_prep")) return rc;
+  }
+  if (a.n_seq > 0) {
+    hipLaunchKernelGGL((k_kda_bwd_state<D>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / KVS))), dim3(KT),
+                       lds_state<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, dS_final, dbank, dS0_seq);
+    if (int rc = kda_status("k_kda_bwd_state")) return rc;
+  }
+  if (a.n_chunks > 0) {
+    hipLaunchKernelGGL((k_kda_bwd_prod<T, D>), dim3(gc), dim3(KT), lds_bprod<D>(), s, a.chunk_rows, a.c0, a.H,
+                       a.scale, tv, td, ws);
+    if (int rc = kda_status("k_kda_bwd_prod")) return rc;
+    hipLaunchKernelGGL((k_kda_bwd_local<T, D>), dim3(gc), dim3(KT), lds_blocal<D>(), s, a.chunk_rows, a.c0, a.H,
+                       tq, tk, g, beta, ws, pdq, pdk, pdv, pdg, pdb);
+    if (int rc = kda_status("k_kda_bwd_local")) return rc;
+  }
+  return HARTS_OK;
+}
+
+bool kda_shape_ok(int32_t dtype, int32_t H, int32_t d, const char* where) {
+  if ((dtype != HARTS_BF16 && dtype != HARTS_F32) || H < 1 || H > 4096 || (d != 64 && d != 128)) {
+    set_error(std::string(where) + ": need dtype bf16 or f32, 1 <= H <= 4096, d in {64, 128}");
+    return false;
+  }
+  return true;
+}
+
+template <int D>
+bool kda_set_lds() {
+  // the kernels need more than the default 64 KiB of dynamic LDS
+  static bool done = false;
+  if (done) return true;
+  const void* fns[] = {reinterpret_cast<const void*>(&k_kda_prep<bf16, D>),
+                       reinterpret_cast<const void*>(&k_kda_prep<float, D>),
+                       reinterpret_cast<const void*>(&k_kda_state<D>),
+                       reinterpret_cast<const void*>(&k_kda_out<bf16, D>),
+                       reinterpret_cast<const void*>(&k_kda_out<float, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_prep<bf16, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_prep<float, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_state<D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_prod<bf16, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_prod<float, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_local<bf16, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_local<float, D>)};
+  for (const void* f : fns)
+    if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess) return false;
+  done = true;
+  return true;
+}
+
+}  // namespace
+}  // namespace harts
+
+using namespace harts;
+
+extern "C" int harts_kda_workspace_size(int64_t n_chunks, int32_t H, int32_t d, size_t* bytes) {
+  if (!bytes || n_chunks < 0 || H < 1 || (d != 64 && d != 128)) {
+    set_error("harts_kda_workspace_size: bad arguments");
+    return HARTS_EINVAL;
+  }
+  const int64_t per = d == 128 ? WsLay<128>::ALL : WsLay<64>::ALL;
+  *bytes = static_cast<size_t>(n_chunks) * H * per * sizeof(float);
+  return HARTS_OK;
+}
+
+extern "C" int harts_kda_fwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab,
+                             int64_t c0, int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H,
+                             int32_t d, float scale, const void* q, const void* k, const void* v, const float* g,
+                             const float* beta, float* bank, float* S_final, void* o, float* ws, void* stream) {
+  if (!kda_shape_ok(dtype, H, d, "harts_kda_fwd")) return HARTS_EUNSUPPORTED;
+  if (c0 < 0 || n_chunks < 0 || s0 < 0 || n_seq < 0) {
+    set_error("harts_kda_fwd: bad ranges");
+    return HARTS_EINVAL;
+  }
+  if (!chunk_rows || !seq_tab || !q || !k || !v || !g || !beta || !bank || !ws) {
+    set_error("harts_kda_fwd: NULL pointer");
+    return HARTS_EINVAL;
+  }
+  if (!(d == 128 ? kda_set_lds<128>() : kda_set_lds<64>())) {
+    set_error("harts_kda_fwd: cannot raise the LDS limit");
+    return HARTS_EHIP;
+  }
+  const KdaArgs a{chunk_rows, seq_tab, req_tab, c0, n_chunks, s0, n_seq, H, scale};
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == HARTS_BF16)
+    return d == 128 ? kda_fwd_impl<bf16, 128>(a, q, k, v, g, beta, bank, S_final, o, ws, s)
+                    : kda_fwd_impl<bf16, 64>(a, q, k, v, g, beta, bank, S_final, o, ws, s);
+  return d == 128 ? kda_fwd_impl<float, 128>(a, q, k, v, g, beta, bank, S_final, o, ws, s)
+                  : kda_fwd_impl<float, 64>(a, q, k, v, g, beta, bank, S_final, o, ws, s);
+}
+
+extern "C" int harts_kda_bwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab,
+                             int64_t c0, int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H,
+                             int32_t d, float scale, const void* q, const void* k, const void* v, const float* g,
+                             const float* beta, const void* dO, const float* dS_final, const float* dbank,
+                             float* dS0_seq, float* ws, float* pdq, float* pdk, float* pdv, float* pdg, float* pdb,
+                             void* stream) {
+  if (!kda_shape_ok(dtype, H, d, "harts_kda_bwd")) return HARTS_EUNSUPPORTED;
+  if (c0 < 0 || n_chunks < 0 || s0 < 0 || n_seq < 0) {
+    set_error("harts_kda_bwd: bad ranges");
+    return HARTS_EINVAL;
+  }
+  if (!chunk_rows || !seq_tab || !q || !k || !v || !g || !beta || !dO || !dbank || !dS0_seq || !ws || !pdq ||
+      !pdk || !pdv || !pdg || !pdb) {
+    set_error("harts_kda_bwd: NULL pointer");
+    return HARTS_EINVAL;
+  }
+  if (!(d == 128 ? kda_set_lds<128>() : kda_set_lds<64>())) {
+    set_error("harts_kda_bwd: cannot raise the LDS limit");
+    return HARTS_EHIP;
+  }
+  const KdaArgs a{chunk_rows, seq_tab, req_tab, c0, n_chunks, s0, n_seq, H, scale};
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == HARTS_BF16)
+    return d == 128 ? kda_bwd_impl<bf16, 128>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
+                                              pdg, pdb, s)
+                    : kda_bwd_impl<bf16, 64>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
+                                             pdg, pdb, s);
+  return d == 128 ? kda_bwd_impl<float, 128>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
+                                             pdg, pdb, s)
+                  : kda_bwd_impl<float, 64>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
+                                            pdg, pdb, s);
+}
+
+extern "C" int harts_kda_reduce(const float* src, const int64_t* row_off, const int32_t* row_pos, int64_t C,
+                                int64_t width, int64_t n_pos, int32_t dtype, void* dst, void* stream) {
+  if ((dtype != HARTS_BF16 && dtype != HARTS_F32) || C < 0 || width < 1 || n_pos < 0) {
+    set_error("harts_kda_reduce: bad arguments");
+    return HARTS_EINVAL;
+  }
+  if (C == 0) return HARTS_OK;
+  if (!src || !row_off || !row_pos || !dst) {
+    set_error("harts_kda_reduce: NULL pointer");
+    return HARTS_EINVAL;
+  }
+  const int64_t n = C * width;
+  hipLaunchKernelGGL(k_kda_reduce, dim3(static_cast<uint32_t>((n + KT - 1) / KT)), dim3(KT), 0,
+                     static_cast<hipStream_t>(stream), src, row_off, row_pos, C, width, n_pos, dst,
+                     dtype == HARTS_BF16 ? 1 : 0);
+  return kda_status("k_kda_reduce");
+}
+
+extern "C" int harts_kda_bank_add(const int32_t* group_tab, int32_t g0, int32_t n_groups, const int32_t* group_seq,
+                                  int64_t elems, const float* dS0_seq, float* dbank, void* stream) {
+  if (g0 < 0 || n_groups < 0 || elems < 1 || n_groups > 65535) {
+    set_error("harts_kda_bank_add: bad arguments");
+    return HARTS_EINVAL;
+  }
+  if (n_groups == 0) return HARTS_OK;
+  if (!group_tab || !group_seq || !dS0_seq || !dbank) {
+    set_error("harts_kda_bank_add: NULL pointer");
+    return HARTS_EINVAL;
+  }
+  hipLaunchKernelGGL(k_kda_bank_add, dim3(static_cast<uint32_t>((elems + KT - 1) / KT), static_cast<uint32_t>(n_groups)),
+                     dim3(KT), 0, static_cast<hipStream_t>(stream), group_tab, g0, group_seq, elems, dS0_seq, dbank);
+  return kda_status("k_kda_bank_add");
+}

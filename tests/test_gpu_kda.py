@@ -1,0 +1,151 @@
+"""GPU parity of KDA over packed rollout trees (Sec. 2.2, eq. chunk-state;
+handoffs of Sec. 3.4) against the fp64 trajectory-wise oracle, through the
+C ABI: o, S_final, dq, dk, dv, dg, dbeta and dS0_tree on small forests and
+plans of three and four rounds (every element); on the 64k-token agentic
+microbatch at 16 heads of 128 (the benchmark's launch configuration), two
+heads: o and dq of sampled rows from their trajectory prefixes, S_final of
+sampled leaves, and dk, dv, dg, dbeta of rows near the end of leaf segments
+(only the rest of their own trajectory depends on them) by reverse mode over
+that suffix.  Tolerances: max relative error per tensor, 1e-4 for float32,
+2e-2 for bf16 (q, k, v, dO rounded to bf16; g, beta float32)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.forest import SegTree
+from oracle.kda import kda_forest, kda_recurrent
+from tests.harness import TOL, max_rel, phys_index, record
+from tests.test_kda_tables import CASES
+from workloads.tensors import to_bf16_roundtrip
+from workloads.trees import forest_for_config
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2608_28158_amd import _lib
+    _lib.lib()
+
+
+def draw(Cn, H, d, n_trees, n_leaves, seed, bf16):
+    r = np.random.default_rng(seed)
+    f32 = lambda a: a.astype(np.float32)
+    q = f32(r.standard_normal((Cn, H, d)))
+    k = r.standard_normal((Cn, H, d))
+    k = f32(k / np.linalg.norm(k, axis=-1, keepdims=True))
+    v = f32(r.standard_normal((Cn, H, d)))
+    g = f32(r.uniform(-0.3, 0.0, (Cn, H, d)))
+    beta = f32(r.uniform(0.05, 1.0, (Cn, H)))
+    dO = f32(r.standard_normal((Cn, H, d)))
+    S0 = f32(r.standard_normal((n_trees, H, d, d)) * 0.5)
+    dSf = f32(r.standard_normal((n_leaves, H, d, d)) * 0.1)
+    if bf16:
+        q, k, v, dO = (to_bf16_roundtrip(a) for a in (q, k, v, dO))
+    return q, k, v, g, beta, dO, S0, dSf
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+@pytest.mark.parametrize("label,parent,seg_len", CASES, ids=[c[0] for c in CASES])
+def test_kda_matches_oracle(label, parent, seg_len, dtype, d):
+    from paper_2608_28158_amd.kda import KdaRunner
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan(parent, seg_len, 64)
+    H, Cn = 2, int(np.sum(seg_len))
+    print(f"[gpu] kda {label} K={plan['n_rounds']} {dtype} d={d}", flush=True)
+    q, k, v, g, beta, dO, S0, dSf = draw(Cn, H, d, plan["n_trees"], plan["n_leaves"], Cn + d, dtype == "bf16")
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    phys = phys_index(seg_len, plan["seg_row"])
+
+    def dev(a, dt):
+        out = np.empty_like(a)
+        out[phys] = a
+        return torch.from_numpy(out).to("cuda", dt).contiguous()
+
+    run = KdaRunner(plan, H, d, tdt)
+    scale = d ** -0.5
+    o, Sf = run.forward(dev(q, tdt), dev(k, tdt), dev(v, tdt), dev(g, torch.float32), dev(beta, torch.float32),
+                        torch.from_numpy(S0).cuda(), scale)
+    grads = run.backward(dev(dO, tdt), torch.from_numpy(dSf).cuda())
+    torch.cuda.synchronize()
+    ref = kda_forest(parent, seg_len, q, k, v, g, beta, scale, S0, dO=dO, dS_final=dSf)
+    host = lambda x: x.float().cpu().numpy()
+    errs = {"o": max_rel(host(o)[phys], ref["o"]), "S_final": max_rel(host(Sf), ref["S_final"])}
+    for n in ("dq", "dk", "dv", "dg", "dbeta"):
+        errs[n] = max_rel(host(grads[n])[phys], ref[n])
+    errs["dS0_tree"] = max_rel(host(grads["dS0_tree"]), ref["dS0_tree"])
+    print(f"[gpu] kda {label} {dtype} d={d}: " + ", ".join(f"{a}={b:.2e}" for a, b in errs.items()), flush=True)
+    record(f"kda {label} K={plan['n_rounds']} d={d}", dtype, errs)
+    assert all(e <= TOL[dtype] for e in errs.values()), errs
+
+
+def test_kda_64k_workload_sampled():
+    from paper_2608_28158_amd.kda import KdaRunner
+    from paper_2608_28158_amd.plan import HartsPlan
+    f, _, cfg = forest_for_config(2)
+    H, d = cfg["H"], cfg["d"]
+    plan = HartsPlan(f.parent, f.seg_len, 64, heads=H)
+    Cn = f.n_rows
+    print(f"[gpu] kda 64k workload C={Cn} H={H} d={d} K={plan['n_rounds']}", flush=True)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(13)
+    rnd = lambda *s: torch.randn(s, device="cuda", generator=gen)
+    q = rnd(Cn, H, d).to(torch.bfloat16)
+    k = rnd(Cn, H, d)
+    k = (k / k.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+    v = rnd(Cn, H, d).to(torch.bfloat16)
+    g = -0.3 * torch.rand((Cn, H, d), device="cuda", generator=gen)
+    beta = 0.05 + 0.95 * torch.rand((Cn, H), device="cuda", generator=gen)
+    dO = rnd(Cn, H, d).to(torch.bfloat16)
+    S0 = 0.5 * rnd(plan["n_trees"], H, d, d)
+    dSf = 0.1 * rnd(plan["n_leaves"], H, d, d)
+    run = KdaRunner(plan, H, d, torch.bfloat16)
+    scale = d ** -0.5
+    o, Sf = run.forward(q, k, v, g, beta, S0, scale)
+    grads = run.backward(dO, dSf)
+    torch.cuda.synchronize()
+    r = np.random.default_rng(13)
+    hs = torch.tensor(np.sort(r.choice(H, 2, replace=False))).cuda()
+    phys = phys_index(f.seg_len, plan["seg_row"])
+    host = lambda x: torch.from_numpy(x.index_select(1, hs).float().cpu().numpy()[phys]).double()
+    Q, K, V, Gd, Bt, DO = (host(x) for x in (q, k, v, g, beta, dO))
+    got = {n: host(grads[n]) for n in ("dq", "dk", "dv", "dg", "dbeta")}
+    got["o"] = host(o)
+    S0h = S0.index_select(1, hs).double().cpu()
+    Sfh = Sf.index_select(1, hs).double().cpu()
+    dSfh = dSf.index_select(1, hs).double().cpu()
+    t = SegTree(f.parent, f.seg_len)
+    ref, val = {n: [] for n in ("o", "dq", "dk", "dv", "dg", "dbeta", "S_final")}, None
+    val = {n: [] for n in ref}
+    leaves = [(li, u) for li, u in enumerate(t.leaves) if t.len[u] >= 8]
+    for li, u in (leaves[int(i)] for i in r.choice(len(leaves), 5, replace=False)):
+        rows = t.trajectory_rows(u)
+        n = len(rows)
+        cut = n - int(r.integers(2, min(48, t.len[u])))         # suffix inside the leaf segment
+        with torch.no_grad():
+            S = S0h[t.tree[u]]
+            picks = set(int(x) for x in r.choice(cut, 4, replace=False))
+            for j in range(cut):
+                ot, S = kda_recurrent(Q[[rows[j]]], K[[rows[j]]], V[[rows[j]]], Gd[[rows[j]]], Bt[[rows[j]]],
+                                      scale, S)
+                if j in picks:                                   # o and dq from the prefix state
+                    c = rows[j]
+                    ref["o"].append(ot[0])
+                    ref["dq"].append(scale * torch.einsum("hkv,hv->hk", S, DO[c]))
+                    val["o"].append(got["o"][c])
+                    val["dq"].append(got["dq"][c])
+        suf = rows[cut:]
+        xs = [x[suf].clone().requires_grad_(True) for x in (K, V, Gd, Bt)]
+        os_, Sn = kda_recurrent(Q[suf], xs[0], xs[1], xs[2], xs[3], scale, S)
+        ((os_ * DO[suf]).sum() + (Sn * dSfh[li]).sum()).backward()
+        ref["S_final"].append(Sn.detach())
+        val["S_final"].append(Sfh[li])
+        for name, x in zip(("dk", "dv", "dg", "dbeta"), xs):
+            ref[name].append(x.grad[0])
+            val[name].append(got[name][suf[0]])
+    errs = {n: max_rel(torch.stack(val[n]).numpy(), torch.stack(ref[n]).numpy()) for n in ref}
+    print("[gpu] kda 64k workload: " + ", ".join(f"{a}={b:.2e}" for a, b in errs.items()), flush=True)
+    record("kda 68k x 16 heads of 128 (sampled)", "bf16", errs)
+    assert all(e <= TOL["bf16"] for e in errs.values()), errs

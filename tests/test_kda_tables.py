@@ -1,0 +1,143 @@
+"""The KDA host tables on the CPU (Sec. 2.2 with the handoffs of Sec. 3.4):
+their structure against the plan, and their meaning: executing them in
+float64 (per sequence, replay rows then own rows from the sequence's bank
+entry, requested chunk-start states written to the bank, outputs of own rows
+kept) with the oracle's token recurrence reproduces the trajectory-wise
+oracle, on plans of one to four rounds."""
+import ctypes as C
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.kda import kda_forest, kda_recurrent
+from oracle.plan_ref import plan_ref
+from tests.harness import phys_index
+from workloads.trees import figure1_forest
+
+CASES = [
+    ("figure 1", figure1_forest().parent, figure1_forest().seg_len),
+    ("binary 3 levels", [-1, 0, 0, 1, 1, 2, 2], [150, 100, 90, 130, 70, 80, 60]),
+    ("two trees K3 + K1", [-1, 0, 0, 1, 1, 2, 2, -1, 7], [150, 100, 90, 130, 70, 80, 60, 40, 300]),
+    ("binary 4 levels", [-1, 0, 0, 1, 1, 2, 2, 3, 3, 4, 4, 5, 5, 6, 6],
+     [120, 70, 66, 90, 100, 65, 130, 80, 75, 90, 68, 77, 101, 66, 140]),
+]
+
+
+def tables(plan):
+    from paper_2608_28158_amd import _lib
+    L = _lib.lib()
+    sz = _lib.KdaSizes()
+    _lib.check(L.harts_kda_layout(plan.handle, C.byref(sz)), "harts_kda_layout")
+    t = dict(rows=np.zeros(sz.n_chunks * 64, np.int32), seq=np.zeros((sz.n_seq, 8), np.int32),
+             req=np.zeros((max(sz.n_req, 1), 2), np.int32), grp=np.zeros((sz.n_groups, 4), np.int32),
+             gseq=np.zeros(sz.n_seq, np.int32), off=np.zeros(plan["C"] + 1, np.int64),
+             pos=np.zeros(sz.n_entries, np.int32))
+    _lib.check(L.harts_kda_tables(plan.handle, *(t[k].ctypes.data for k in
+                                                 ("rows", "seq", "req", "grp", "gseq", "off", "pos"))),
+               "harts_kda_tables")
+    return sz, t
+
+
+@pytest.mark.parametrize("label,parent,seg_len", CASES, ids=[c[0] for c in CASES])
+def test_tables_follow_the_plan(label, parent, seg_len):
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan(parent, seg_len, 64)
+    sz, t = tables(plan)
+    assert sz.n_entries == plan["C"] + plan["R"] and sz.n_rounds == plan["n_rounds"]
+    c = 0
+    for i in range(plan["n_seq"]):
+        rnd, c0, nc, init, ro, nr, leaf, _ = (int(x) for x in t["seq"][i])
+        assert rnd == plan["seq_round"][i] - 1 and c0 == c and init == plan["seq_init_bank"][i]
+        assert leaf == plan["seq_final_leaf"][i]
+        a, b = plan["seq_replay_off"][i], plan["seq_replay_off"][i + 1]
+        own = plan["seq_row"][i] + np.arange(plan["seq_n_own"][i])
+        want = np.concatenate([plan["replay_row"][a:b] * 2, own * 2 + 1])
+        assert nc == -(-len(want) // 64)
+        got = t["rows"][c0 * 64:(c0 + nc) * 64]
+        assert np.array_equal(got[:len(want)], want) and np.all(got[len(want):] == -1)
+        assert ro == plan["seq_req_off"][i] and nr == plan["seq_req_off"][i + 1] - ro
+        for j in range(ro, ro + nr):
+            assert t["req"][j, 0] == plan["req_chunk"][j] and t["req"][j, 1] == plan["req_bank"][j]
+            assert 0 <= t["req"][j, 0] <= nc
+        c += nc
+    assert c == sz.n_chunks
+    # groups: every round's sequences once, by initial bank entry, in order
+    seen = []
+    for rnd, bank, first, n in t["grp"]:
+        members = t["gseq"][first:first + n]
+        assert np.all(plan["seq_init_bank"][members] == bank) and np.all(t["seq"][members, 0] == rnd)
+        assert np.all(np.diff(members) > 0)
+        seen += list(members)
+    assert sorted(seen) == list(range(plan["n_seq"]))
+    # gradient lists: every real packed row once, grouped by compact row, ascending
+    real = np.nonzero(t["rows"] >= 0)[0]
+    assert np.array_equal(np.sort(t["pos"]), real)
+    for r in range(plan["C"]):
+        p = t["pos"][t["off"][r]:t["off"][r + 1]]
+        assert np.all(np.diff(p) > 0) and np.all(t["rows"][p] // 2 == r)
+        assert np.sum(t["rows"][p] & 1) == 1          # one own position per compact row
+
+
+def execute_tables(plan, t, q, k, v, g, beta, S0_tree, scale):
+    """The tables run in float64 with the oracle's token recurrence."""
+    bank = [None] * plan["n_bank"]
+    for i in range(plan["n_trees"]):
+        bank[i] = S0_tree[i]
+    o = torch.zeros_like(v)
+    finals = [None] * plan["n_leaves"]
+    for rnd in range(plan["n_rounds"]):
+        for i in np.nonzero(t["seq"][:, 0] == rnd)[0]:
+            _, c0, nc, init, ro, nr, leaf, _ = (int(x) for x in t["seq"][i])
+            reqs = [tuple(int(x) for x in t["req"][j]) for j in range(ro, ro + nr)]
+            S = bank[init]
+            for cc in range(nc + 1):
+                for rc, b in reqs:
+                    if rc == cc:
+                        bank[b] = S.clone()
+                if cc == nc:
+                    break
+                for e in t["rows"][(c0 + cc) * 64:(c0 + cc + 1) * 64]:
+                    if e < 0:
+                        continue
+                    r = int(e) // 2
+                    ot, S = kda_recurrent(q[[r]], k[[r]], v[[r]], g[[r]], beta[[r]], scale, S)
+                    if e & 1:
+                        o[r] = ot[0]
+            finals[leaf] = S
+    return o, torch.stack(finals)
+
+
+@pytest.mark.parametrize("label,parent,seg_len", CASES, ids=[c[0] for c in CASES])
+def test_executing_the_tables_reproduces_every_trajectory(label, parent, seg_len):
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan(parent, seg_len, 64)
+    assert plan["n_rounds"] == plan_ref(parent, seg_len, 64)["K"]
+    _, t = tables(plan)
+    Cn, H, d = int(np.sum(seg_len)), 2, 3
+    r = np.random.default_rng(len(parent))
+    q, k, v = (r.standard_normal((Cn, H, d)) for _ in range(3))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    g = r.uniform(-0.2, 0.0, (Cn, H, d))
+    beta = r.uniform(0.1, 1.0, (Cn, H))
+    S0 = r.standard_normal((plan["n_trees"], H, d, d))
+    ref = kda_forest(parent, seg_len, q, k, v, g, beta, 0.5, S0)
+    phys = phys_index(seg_len, plan["seg_row"])
+    T = lambda a: torch.as_tensor(a, dtype=torch.float64)
+
+    def to_phys(a):
+        out = np.empty_like(a)
+        out[phys] = a
+        return T(out)
+
+    o, Sf = execute_tables(plan, t, *(to_phys(a) for a in (q, k, v, g, beta)), T(S0), 0.5)
+    assert np.allclose(o.numpy()[phys], ref["o"], rtol=0, atol=1e-12)
+    assert np.allclose(Sf.numpy(), ref["S_final"], rtol=0, atol=1e-12)
+
+
+def test_tables_reject_plans_of_another_chunk():
+    from paper_2608_28158_amd import _lib
+    from paper_2608_28158_amd.plan import HartsPlan
+    plan = HartsPlan([-1, 0], [40, 20], 32)
+    sz = _lib.KdaSizes()
+    assert _lib.lib().harts_kda_layout(plan.handle, C.byref(sz)) == _lib.HARTS_EUNSUPPORTED

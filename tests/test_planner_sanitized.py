@@ -27,8 +27,8 @@ def _runtime(name):
     return path if os.path.isabs(path) and os.path.exists(path) else None
 
 
-HOST_SOURCES = ("plan.cpp", "semantic.cpp", "mbplan.cpp")
-HIP_OBJECTS = ("la.hip.o", "logp.hip.o", "conv.hip.o", "attn.hip.o")
+HOST_SOURCES = ("plan.cpp", "semantic.cpp", "mbplan.cpp", "kda_plan.cpp")
+HIP_OBJECTS = ("la.hip.o", "logp.hip.o", "conv.hip.o", "attn.hip.o", "kda.hip.o")
 
 
 def test_planner_under_asan_and_ubsan(tmp_path):
