@@ -856,6 +856,101 @@ def attn_measurement(steps, warmup, profile_only=False):
     return out
 
 
+def kda_measurement(steps, warmup, profile_only=False):
+    """KDA (per-channel decay with the delta rule) over the plan of the
+    64k-token microbatch: 68,161 compact rows, 16 heads of 128, bf16 q, k,
+    v, float32 g and beta.  One step is the forward of every round and the
+    backward of every round in reverse order, with the handoffs and the
+    gradient reductions.  Algorithmic FLOPs per (64-row chunk, head) of the
+    chunk form (eq. chunk-state): forward 5 B^2 d (At, M, W, U', M X) +
+    6 B d^2 (W S, Q S, K^T X), backward twice that."""
+    import torch
+    from paper_2608_28158_amd.kda import KdaRunner
+    from paper_2608_28158_amd.plan import HartsPlan
+    from workloads import forest_for_config
+    f, _, cfg = forest_for_config(2)
+    H, d = cfg["H"], cfg["d"]
+    plan = HartsPlan(f.parent, f.seg_len, 64, heads=H)
+    Cn = f.n_rows
+    t0 = time.perf_counter()
+    run = KdaRunner(plan, H, d, torch.bfloat16)
+    tables_ms = (time.perf_counter() - t0) * 1e3
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(13)
+    rnd = lambda *sh: torch.randn(sh, device="cuda", generator=gen)
+    q = rnd(Cn, H, d).to(torch.bfloat16)
+    k = rnd(Cn, H, d)
+    k = (k / k.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+    v = rnd(Cn, H, d).to(torch.bfloat16)
+    g = -0.3 * torch.rand((Cn, H, d), device="cuda", generator=gen)
+    beta = 0.05 + 0.95 * torch.rand((Cn, H), device="cuda", generator=gen)
+    dO = rnd(Cn, H, d).to(torch.bfloat16)
+    S0 = 0.5 * rnd(plan["n_trees"], H, d, d)
+    dSf = 0.1 * rnd(plan["n_leaves"], H, d, d)
+    scale = d ** -0.5
+    stream = torch.cuda.current_stream()
+
+    def fwd():
+        run.forward(q, k, v, g, beta, S0, scale)
+
+    def step():
+        run.forward(q, k, v, g, beta, S0, scale)
+        run.backward(dO, dSf)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record(stream)
+        for _ in range(steps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / steps
+
+    ms_f, ms = timed(fwd), timed(step)
+    if profile_only:
+        return None
+    nch = run.sizes.n_chunks
+    B = 64
+    fl_f = nch * H * (5 * B * B * d + 6 * B * d * d)
+    fl = 3 * fl_f
+    tf = lambda x, m: x / (m * 1e-3) / 1e12
+    out = {"workload": f"64k-token agentic microbatch: {Cn} compact rows, {plan['R']} replay rows, "
+                       f"{nch} packed 64-row chunks, K={plan['n_rounds']}, {H} heads of {d}, bf16 q/k/v, "
+                       f"float32 g/beta/states",
+           "ms_per_step": ms, "compact_tok_s": Cn / (ms * 1e-3), "fwd_ms": ms_f, "tables_host_ms": tables_ms,
+           "alg_TFLOP_step": fl / 1e12, "TFLOPs": tf(fl, ms), "fwd_TFLOPs": tf(fl_f, ms_f),
+           "fp32_vector_frac": tf(fl, ms) / PEAK_F32_TFLOPS}
+    # the oracle: the trajectory-wise fp64 recurrence, forward and backward by
+    # reverse mode, on the first 512 tokens of one trajectory and one head
+    from oracle.kda import kda_recurrent
+    from oracle.forest import SegTree
+    t = SegTree(f.parent, f.seg_len)
+    rows = t.trajectory_rows(t.leaves[0])[:512]
+    phys = phys_index(f.seg_len, plan["seg_row"])
+    pick = torch.from_numpy(phys[rows]).cuda()
+    h1 = lambda x: x[pick][:, :1].double().cpu()
+    xs = [h1(x).requires_grad_(True) for x in (q, k, v, g)] + [h1(beta).requires_grad_(True)]
+    S0h = S0[0, :1].double().cpu().requires_grad_(True)
+    dOh = h1(dO)
+    t1 = time.perf_counter()
+    o_, S_ = kda_recurrent(*xs, scale, S0h)
+    (o_ * dOh).sum().backward()
+    cpu_s = time.perf_counter() - t1
+    rate = len(rows) / cpu_s                              # token-heads per second
+    job_s = plan["S"] * H / rate
+    out["cpu_baseline"] = {"value": Cn / job_s, "unit": "compact tokens/s", "cores": torch.get_num_threads(),
+                           "kind": "oracle",
+                           "sample": f"fp64 trajectory-wise recurrence, forward + backward by reverse mode, "
+                                     f"{len(rows)} tokens of one trajectory and one head ({cpu_s:.1f} s), scaled "
+                                     f"to S = {plan['S']} trajectory tokens x {H} heads"}
+    del run
+    torch.cuda.empty_cache()
+    return out
+
+
 def mbplan_measurement(D=4, T=65536):
     """Prefix-aware microbatch/DP planning at the paper's scale: a seeded
     batch of 215 agentic rollout trees at full length (about 1,600
@@ -921,6 +1016,9 @@ def main():
     ap.add_argument("--no-mbplan", action="store_true")
     ap.add_argument("--no-conv", action="store_true")
     ap.add_argument("--no-attn", action="store_true")
+    ap.add_argument("--no-kda", action="store_true")
+    ap.add_argument("--kda-only", action="store_true",
+                    help="run the timed KDA steps only (for profiler runs)")
     ap.add_argument("--attn-only", action="store_true",
                     help="run the timed attention calls only (for profiler runs)")
     ap.add_argument("--conv-only", action="store_true",
@@ -951,6 +1049,10 @@ def main():
     if args.logp_only:
         logp_measurement(args.steps, args.warmup, profile_only=True)
         log("[bench] logp calls done")
+        return
+    if args.kda_only:
+        kda_measurement(args.steps, args.warmup, profile_only=True)
+        log("[bench] kda steps done")
         return
     if args.attn_only:
         attn_measurement(args.steps, args.warmup, profile_only=True)
@@ -1065,6 +1167,9 @@ def main():
     if not args.no_attn:
         log("[bench] full attention through asymmetric Q/KV views (16 heads of 128)")
         out["attn"] = attn_measurement(args.steps, args.warmup)
+    if not args.no_kda:
+        log("[bench] KDA over the same plan (16 heads of 128)")
+        out["kda"] = kda_measurement(max(2, args.steps // 4), 1)
     if not args.no_mbplan:
         log("[bench] prefix-aware microbatch planning (host)")
         out["mb_plan"] = mbplan_measurement()
