@@ -17,7 +17,7 @@
 // the sequence (k_kda_state); outputs again in parallel (k_kda_out).  The
 // backward mirrors it: dX and the state adjoints in reverse chunk order
 // (k_kda_bwd_state), then every chunk-local gradient in parallel
-// (k_kda_bwd_prod, k_kda_bwd_local) into per-packed-row buffers, reduced
+// (k_kda_bwd_prod, k_kda_bwd_tm, k_kda_bwd_local) into per-packed-row buffers, reduced
 // into compact rows in a fixed order (k_kda_reduce).  Pairwise decays
 // e^{G_i - G_j} (i >= j) are evaluated exactly per channel, never as
 // products of e^{G_i} and e^{-G_j}, so no intermediate overflows.
@@ -37,7 +37,7 @@ namespace harts {
 namespace {
 
 typedef __bf16 bf16;
-constexpr int KT = 256;   // threads per workgroup
+constexpr int KT = 512;   // threads per workgroup (8 waves: two per SIMD)
 constexpr int KB = 64;    // chunk rows
 constexpr int KVS = 32;   // state columns per workgroup in the state passes
 
@@ -57,7 +57,7 @@ struct WsLay {
   static constexpr int64_t BB = KB * KB;
   // forward
   static constexpr int64_t W = 0, UP = W + RD, KBM = UP + RD, GAM = KBM + RD, QG = GAM + D, M = QG + RD,
-                           SC = M + BB, X = SC + DD, FWD = X + RD;
+                           AT = M + BB, LINV = AT + BB, SC = LINV + BB, X = SC + DD, FWD = X + RD;
   // backward
   static constexpr int64_t DXO = FWD, DSO = DXO + RD, DSN = DSO + DD, DX = DSN + DD, DQG = DX + RD,
                            DW = DQG + RD, DKBM = DW + RD, DM = DKBM + RD, DUV = DM + BB, DGAM = DUV + BB,
@@ -166,8 +166,10 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   __syncthreads();
   for (int p = t; p < KB * KB; p += KT) w[Y::M + p] = sL[(p / KB) * (KB + 1) + p % KB];
   __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * (KB + 1) + p % KB];
   tri_inverse(sL, sA, sb, t);
   __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) w[Y::LINV + p] = sL[(p / KB) * (KB + 1) + p % KB];
   // Tm = L^{-1} Diag(beta) into sA
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
@@ -503,121 +505,160 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
   if (t < D) w[Y::DGAM + t] = aG;
 }
 
-// Chunk-local gradients of one (chunk, head): through Tm = L^{-1} Diag(beta),
-// L = I + Diag(beta) At, the pairwise decays of At and M, the decayed K, Q
-// and the cumulative sum of g.  Writes dq, dk, dv, dg [packed row][H][D] and
-// dbeta [packed row][H] for every real packed row.
+// Products with Tm = L^{-1} Diag(beta) of one (chunk, head), operands staged
+// in LDS: dTm = dUV + dW (K e^G)^T (j <= i, over dUV in the workspace),
+// dV = Tm^T dX (to pdv), d(K e^G) = Tm^T dW (to the workspace).
+template <typename T, int D>
+__global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+                                                   const T* __restrict__ k, const float* __restrict__ g,
+                                                   const float* __restrict__ beta, float* __restrict__ ws,
+                                                   float* __restrict__ pdv) {
+  using Y = WsLay<D>;
+  constexpr int LD = D + 1, LB = KB + 1;
+  extern __shared__ float sm[];
+  float* sKG = sm;                 // [64][D + 1] K e^G (G first)
+  float* sDW = sKG + KB * LD;      // [64][D + 1] dW
+  float* sDX = sDW + KB * LD;      // [64][D + 1] dX
+  float* sTm = sDX + KB * LD;      // [64][65]
+  float* sb = sTm + KB * LB;       // [64]
+  float* sG = sb + KB;             // unused tail
+  (void)sG;
+  const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
+  const int t = threadIdx.x;
+  const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  load_decay(sKG, sb, g, beta, ent, H, h, D, t);           // sKG holds G now
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, d = idx % D;
+    const int32_t e = ent[r];
+    const float kv = e >= 0 ? ld<T>(k + (static_cast<int64_t>(e >> 1) * H + h) * D + d) : 0.f;
+    sKG[r * LD + d] = kv * __expf(sKG[r * LD + d]);
+    sDW[r * LD + d] = w[Y::DW + idx];
+    sDX[r * LD + d] = w[Y::DX + idx];
+  }
+  for (int p = t; p < KB * KB; p += KT) sTm[(p / KB) * LB + p % KB] = w[Y::LINV + p] * sb[p % KB];
+  __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    if (j > i) continue;
+    float a = w[Y::DUV + p];
+    for (int d = 0; d < D; ++d) a += sDW[i * LD + d] * sKG[j * LD + d];
+    w[Y::DUV + p] = a;                                       // dTm
+  }
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int j = idx / D, d = idx % D;
+    float av = 0.f, ak = 0.f;
+    for (int i = j; i < KB; ++i) {
+      const float tm = sTm[i * LB + j];
+      av += tm * sDX[i * LD + d];
+      ak += tm * sDW[i * LD + d];
+    }
+    if (ent[j] >= 0) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + d] = av;
+    w[Y::DKG + idx] = ak;
+  }
+}
+
+// Chunk-local gradients of one (chunk, head) past the products: through
+// Tm = L^{-1} Diag(beta) and L = I + Diag(beta) At (dL = -L^{-T} dL^{-1}
+// L^{-T}), the pairwise decays of At and M, the decayed K and Q, and the
+// cumulative sum of g.  Writes dq, dk, dg [packed row][H][D] and dbeta
+// [packed row][H] for every real packed row.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                       const T* __restrict__ q, const T* __restrict__ k,
                                                       const float* __restrict__ g, const float* __restrict__ beta,
                                                       float* __restrict__ ws, float* __restrict__ pdq,
-                                                      float* __restrict__ pdk, float* __restrict__ pdv,
-                                                      float* __restrict__ pdg, float* __restrict__ pdb) {
+                                                      float* __restrict__ pdk, float* __restrict__ pdg,
+                                                      float* __restrict__ pdb) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 1, LB = KB + 1;
+  constexpr int LB = KB + 1;
   extern __shared__ float sm[];
-  float* sK = sm;                  // [64][D + 1] k
-  float* sQ = sK + KB * LD;        // [64][D + 1] q
-  float* sG = sQ + KB * LD;        // [64][D + 1] cumulative log-decay
-  float* sA = sG + KB * LD;        // [64][65] At, later dM
-  float* sL = sA + KB * LB;        // [64][65] L^{-1}
-  float* sT = sL + KB * LB;        // [64][65] dTm -> dLinv -> Y -> dA
-  float* sb = sT + KB * LB;        // [64] beta
+  float* sK = sm;                  // [64][D] k (read by channel: no padding needed)
+  float* sQ = sK + KB * D;         // [64][D] q, later dG
+  float* sG = sQ + KB * D;         // [64][D] cumulative log-decay
+  float* sL = sG + KB * D;         // [64][65] L^{-1}, later dM
+  float* sT = sL + KB * LB;        // [64][65] dTm -> dLinv -> dA -> dAt
+  float* sY = sT + KB * LB;        // [64][65] Y
+  float* sb = sY + KB * LB;        // [64] beta
   float* sdb = sb + KB;            // [64] dbeta
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  load_rows<T, D>(sK, k, ent, H, h, t);
-  load_rows<T, D>(sQ, q, ent, H, h, t);
-  load_decay(sG, sb, g, beta, ent, H, h, D, t);
-  pair_sums<D>(sA, nullptr, sK, sQ, sG, t);
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, d = idx % D;
+    const int32_t e = ent[r];
+    const int64_t o = (static_cast<int64_t>(e >> 1) * H + h) * D + d;
+    sK[idx] = e >= 0 ? ld<T>(k + o) : 0.f;
+    sQ[idx] = e >= 0 ? ld<T>(q + o) : 0.f;
+    sG[idx] = e >= 0 ? g[o] : 0.f;
+  }
+  if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
+  for (int p = t; p < KB * KB; p += KT) {
+    sL[(p / KB) * LB + p % KB] = w[Y::LINV + p];
+    sT[(p / KB) * LB + p % KB] = w[Y::DUV + p];          // dTm
+  }
   __syncthreads();
-  tri_inverse(sL, sA, sb, t);
+  if (t < D) {                                             // cumulative sums of g per channel
+    float a = 0.f;
+    for (int r = 0; r < KB; ++r) {
+      a += sG[r * D + t];
+      sG[r * D + t] = a;
+    }
+  }
+  // dbeta_j from Tm = L^{-1} Diag(beta): sum_i dTm[i][j] L^{-1}[i][j]
+  if (t >= KT - KB) {
+    const int j = t - (KT - KB);
+    float a = 0.f;
+    for (int i = j; i < KB; ++i) a += sT[i * LB + j] * sL[i * LB + j];
+    sdb[j] = a;
+  }
   __syncthreads();
-  // dTm = dUV + dW (K e^G)^T  (j <= i)
+  for (int p = t; p < KB * KB; p += KT) sT[(p / KB) * LB + p % KB] *= sb[p % KB];   // dLinv
+  __syncthreads();
+  // Y[a][j] = sum_{b <= min(a, j)} dLinv[a][b] L^{-1}[j][b]
+  for (int p = t; p < KB * KB; p += KT) {
+    const int a = p / KB, j = p % KB, m = a < j ? a : j;
+    float y = 0.f;
+    for (int bb = 0; bb <= m; ++bb) y += sT[a * LB + bb] * sL[j * LB + bb];
+    sY[a * LB + j] = y;
+  }
+  __syncthreads();
+  // dA[i][j] = -sum_{a >= i} L^{-1}[a][i] Y[a][j] (i > j); dbeta_i += sum_j dA_ij At_ij; dAt = beta_i dA
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
-    float a = 0.f;
-    if (j <= i) {
-      a = w[Y::DUV + p];
-      const float* dw = w + Y::DW + static_cast<int64_t>(i) * D;
-      for (int d = 0; d < D; ++d) a += dw[d] * sK[j * LD + d] * __expf(sG[j * LD + d]);
+    float x = 0.f;
+    if (i > j) {
+      for (int a = i; a < KB; ++a) x += sL[a * LB + i] * sY[a * LB + j];
+      x = -x;
     }
-    sT[i * LB + j] = a;
+    sT[i * LB + j] = x;
   }
   __syncthreads();
-  // dV = Tm^T dX, dK e^G part = Tm^T dW (Tm[i][j] = L^{-1}[i][j] beta_j)
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int j = idx / D, d = idx % D;
-    float av = 0.f, ak = 0.f;
-    for (int i = j; i < KB; ++i) {
-      const float tm = sL[i * LB + j] * sb[j];
-      av += tm * w[Y::DX + i * D + d];
-      ak += tm * w[Y::DW + i * D + d];
-    }
-    const int32_t e = ent[j];
-    if (e >= 0) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + d] = av;
-    w[Y::DKG + idx] = ak;
-  }
-  // dbeta_j (Tm part) = sum_i dTm[i][j] L^{-1}[i][j]; dLinv = dTm Diag(beta)
   if (t < KB) {
     float a = 0.f;
-    for (int i = t; i < KB; ++i) a += sT[i * LB + t] * sL[i * LB + t];
-    sdb[t] = a;
-  }
-  __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) sT[(p / KB) * LB + p % KB] *= sb[p % KB];
-  __syncthreads();
-  // Y = dLinv L^{-T}: row a by thread a (Y[a][j] = sum_b dLinv[a][b] Linv[j][b], b <= min(a, j))
-  if (t < KB) {
-    float row[KB];
-    for (int bb = 0; bb < KB; ++bb) row[bb] = sT[t * LB + bb];
-    for (int j = 0; j < KB; ++j) {
-      float a = 0.f;
-      const int m = t < j ? t : j;
-      for (int bb = 0; bb <= m; ++bb) a += row[bb] * sL[j * LB + bb];
-      sT[t * LB + j] = a;
-    }
-  }
-  __syncthreads();
-  // dA = -(L^{-T} Y), strictly lower: column j by thread j (dA[i][j] = -sum_{a >= i} Linv[a][i] Y[a][j])
-  if (t < KB) {
-    float col[KB];
-    for (int a = 0; a < KB; ++a) col[a] = sT[a * LB + t];
-    for (int i = 0; i < KB; ++i) {
-      float s = 0.f;
-      for (int a = i; a < KB; ++a) s += sL[a * LB + i] * col[a];
-      sT[i * LB + t] = i > t ? -s : 0.f;
-    }
-  }
-  __syncthreads();
-  // dbeta_i += sum_j dA_ij At_ij; then dAt = Diag(beta) dA into sT, dM into sA
-  if (t < KB) {
-    float a = 0.f;
-    for (int j = 0; j < t; ++j) a += sT[t * LB + j] * sA[t * LB + j];
+    for (int j = 0; j < t; ++j) a += sT[t * LB + j] * w[Y::AT + t * KB + j];
     sdb[t] += a;
   }
   __syncthreads();
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
-    sT[i * LB + j] *= sb[i];
-    sA[i * LB + j] = w[Y::DM + p];
+    sT[i * LB + j] *= sb[i];                                // dAt
+    sL[i * LB + j] = w[Y::DM + p];                          // dM
   }
   __syncthreads();
   // pairwise terms, per channel: threads 0..D-1 take row i's own terms
-  // (dq_i, dk_i, +dG_i), threads 128..128+D-1 the terms of column j (dk_j, -dG_j)
+  // (dq_i, dk_i, +dG_i), threads KT/2..KT/2+D-1 the terms of column j (dk_j, -dG_j)
   if (t < D) {
     const int d = t;
     for (int i = 0; i < KB; ++i) {
-      const float gi = sG[i * LD + d], ki = sK[i * LD + d], qi = sQ[i * LD + d];
+      const float gi = sG[i * D + d], ki = sK[i * D + d], qi = sQ[i * D + d];
       float dq_ = 0.f, dk_ = 0.f, dg_ = 0.f;
       for (int j = 0; j <= i; ++j) {
-        const float e = __expf(gi - sG[j * LD + d]);
-        const float kj = sK[j * LD + d];
+        const float e = __expf(gi - sG[j * D + d]);
+        const float kj = sK[j * D + d];
         const float ta = sT[i * LB + j] * e;     // 0 on the diagonal
-        const float tm = sA[i * LB + j] * e;
+        const float tm = sL[i * LB + j] * e;
         dk_ += ta * kj;
         dq_ += tm * kj;
         dg_ += (ta * ki + tm * qi) * kj;
@@ -626,14 +667,14 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
       w[Y::P1K + i * D + d] = dk_;
       w[Y::P1G + i * D + d] = dg_;
     }
-  } else if (t >= 128 && t < 128 + D) {
-    const int d = t - 128;
+  } else if (t >= KT / 2 && t < KT / 2 + D) {
+    const int d = t - KT / 2;
     for (int j = 0; j < KB; ++j) {
-      const float gj = sG[j * LD + d], kj = sK[j * LD + d];
+      const float gj = sG[j * D + d], kj = sK[j * D + d];
       float dk_ = 0.f, dg_ = 0.f;
       for (int i = j; i < KB; ++i) {
-        const float e = __expf(sG[i * LD + d] - gj);
-        const float x = (sT[i * LB + j] * sK[i * LD + d] + sA[i * LB + j] * sQ[i * LD + d]) * e;
+        const float e = __expf(sG[i * D + d] - gj);
+        const float x = (sT[i * LB + j] * sK[i * D + d] + sL[i * LB + j] * sQ[i * D + d]) * e;
         dk_ += x;
         dg_ += x * kj;
       }
@@ -642,31 +683,34 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     }
   }
   __syncthreads();
-  // elementwise terms and the reverse cumulative sum of dG; thread per channel
+  // elementwise terms, in parallel; dG of each element into sQ
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int i = idx / D, d = idx % D;
+    const float G = sG[idx], GB = sG[(KB - 1) * D + d], eG = __expf(G), eB = __expf(GB - G);
+    const float ki = sK[idx], qi = sQ[idx];
+    const float dqg = w[Y::DQG + idx], dkg = w[Y::DKG + idx], dkb = w[Y::DKBM + idx];
+    const float dq_ = w[Y::P1Q + idx] + dqg * eG;
+    const float dk_ = w[Y::P1K + idx] + w[Y::P2K + idx] + dkg * eG + dkb * eB;
+    sQ[idx] = w[Y::P1G + idx] - w[Y::P2G + idx] + dqg * qi * eG + dkg * ki * eG - dkb * ki * eB;
+    const int32_t e = ent[i];
+    if (e >= 0) {
+      const int64_t o = (static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d;
+      pdq[o] = dq_;
+      pdk[o] = dk_;
+    }
+  }
+  __syncthreads();
+  // dG_B (gamma and the KB terms) and the reverse cumulative sum of dG, per channel
   if (t < D) {
     const int d = t;
-    const float GB = sG[(KB - 1) * LD + d];
-    float dGB = w[Y::DGAM + d] * __expf(GB), run = 0.f;
-    for (int i = 0; i < KB; ++i) {
-      const float kb = sK[i * LD + d] * __expf(GB - sG[i * LD + d]);
-      dGB += w[Y::DKBM + i * D + d] * kb;
-    }
+    const float GB = sG[(KB - 1) * D + d];
+    float dGB = w[Y::DGAM + d] * __expf(GB);
+    for (int i = 0; i < KB; ++i) dGB += w[Y::DKBM + i * D + d] * sK[i * D + d] * __expf(GB - sG[i * D + d]);
+    float run = dGB;
     for (int i = KB - 1; i >= 0; --i) {
-      const float G = sG[i * LD + d], eG = __expf(G), ki = sK[i * LD + d], qi = sQ[i * LD + d];
-      const float kb = ki * __expf(GB - G);
-      const float dqg = w[Y::DQG + i * D + d], dkg = w[Y::DKG + i * D + d], dkb = w[Y::DKBM + i * D + d];
-      const float dq_ = w[Y::P1Q + i * D + d] + dqg * eG;
-      const float dk_ = w[Y::P1K + i * D + d] + w[Y::P2K + i * D + d] + dkg * eG + dkb * __expf(GB - G);
-      float dG = w[Y::P1G + i * D + d] - w[Y::P2G + i * D + d] + dqg * qi * eG + dkg * ki * eG - dkb * kb;
-      if (i == KB - 1) dG += dGB;
-      run += dG;
+      run += sQ[i * D + d];
       const int32_t e = ent[i];
-      if (e >= 0) {
-        const int64_t o = (static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d;
-        pdq[o] = dq_;
-        pdk[o] = dk_;
-        pdg[o] = run;
-      }
+      if (e >= 0) pdg[(static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d] = run;
     }
   }
   if (t < KB && ent[t] >= 0) pdb[(static_cast<int64_t>(c) * KB + t) * H + h] = sdb[t];
@@ -721,7 +765,9 @@ constexpr size_t lds_bprep() { return (2 * KB * (D + 1) + KB * (KB + 1)) * sizeo
 template <int D>
 constexpr size_t lds_bprod() { return (2 * D * 33 + 4 * KB * 33) * sizeof(float); }
 template <int D>
-constexpr size_t lds_blocal() { return (3 * KB * (D + 1) + 3 * KB * (KB + 1) + 2 * KB) * sizeof(float); }
+constexpr size_t lds_btm() { return (3 * KB * (D + 1) + KB * (KB + 1) + 2 * KB) * sizeof(float); }
+template <int D>
+constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 1) + 2 * KB) * sizeof(float); }
 
 struct KdaArgs {
   const int32_t* chunk_rows;
@@ -780,8 +826,11 @@ int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     hipLaunchKernelGGL((k_kda_bwd_prod<T, D>), dim3(gc), dim3(KT), lds_bprod<D>(), s, a.chunk_rows, a.c0, a.H,
                        a.scale, tv, td, ws);
     if (int rc = kda_status("k_kda_bwd_prod")) return rc;
+    hipLaunchKernelGGL((k_kda_bwd_tm<T, D>), dim3(gc), dim3(KT), lds_btm<D>(), s, a.chunk_rows, a.c0, a.H, tk, g,
+                       beta, ws, pdv);
+    if (int rc = kda_status("k_kda_bwd_tm")) return rc;
     hipLaunchKernelGGL((k_kda_bwd_local<T, D>), dim3(gc), dim3(KT), lds_blocal<D>(), s, a.chunk_rows, a.c0, a.H,
-                       tq, tk, g, beta, ws, pdq, pdk, pdv, pdg, pdb);
+                       tq, tk, g, beta, ws, pdq, pdk, pdg, pdb);
     if (int rc = kda_status("k_kda_bwd_local")) return rc;
   }
   return HARTS_OK;
@@ -810,6 +859,8 @@ bool kda_set_lds() {
                        reinterpret_cast<const void*>(&k_kda_bwd_state<D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prod<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prod<float, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_tm<bf16, D>),
+                       reinterpret_cast<const void*>(&k_kda_bwd_tm<float, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_local<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_local<float, D>)};
   for (const void* f : fns)
