@@ -13,10 +13,10 @@
 //   M[i][j] = sum_d q_i k_j e^{G_i - G_j} (j <= i),
 //   S_next = Diag(e^{G_B}) S + (K * e^{G_B - G})^T X.
 // Chunk-local quantities are formed in parallel (k_kda_prep); the state
-// recurrence runs per (sequence, head, 32 state columns) over the chunks of
-// the sequence (k_kda_state); outputs again in parallel (k_kda_out).  The
+// recurrence runs per (sequence, head, 64 state columns) over the chunks of
+// the sequence (k_kda_seq); outputs again in parallel (k_kda_out).  The
 // backward mirrors it: dX and the state adjoints in reverse chunk order
-// (k_kda_bwd_state), then every chunk-local gradient in parallel
+// (k_kda_seq, reverse), then every chunk-local gradient in parallel
 // (k_kda_bwd_prod, k_kda_bwd_tm, k_kda_bwd_local) into per-packed-row buffers, reduced
 // into compact rows in a fixed order (k_kda_reduce).  Pairwise decays
 // e^{G_i - G_j} (i >= j) are evaluated exactly per channel, never as
@@ -39,7 +39,6 @@ namespace {
 typedef __bf16 bf16;
 constexpr int KT = 512;   // threads per workgroup (8 waves: two per SIMD)
 constexpr int KB = 64;    // chunk rows
-constexpr int KVS = 32;   // state columns per workgroup in the state passes
 
 template <typename T> __device__ inline float ld(const T* p);
 template <> __device__ inline float ld<float>(const float* p) { return *p; }
@@ -99,26 +98,73 @@ __device__ inline void load_decay(float* sG, float* sb, const float* __restrict_
 
 // sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and, if
 // sM, sM[i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere).
+// Work item = (4 x 4 block of pairs on or below the diagonal, quarter of the
+// channels): 136 blocks x 4 quarters; the quarters of a block are adjacent
+// lanes and are summed with two lane exchanges.  Every exponent is
+// G_i - G_j <= 0 (clamped to 0 above the diagonal, where the term is masked).
 template <int D>
 __device__ inline void pair_sums(float* sA, float* sM, const float* sK, const float* sQ, const float* sG, int t) {
-  constexpr int LD = D + 1;
-  for (int p = t; p < KB * KB; p += KT) {
-    const int i = p / KB, j = p % KB;
-    float a = 0.f, m = 0.f;
-    if (j <= i) {
-      const float* ki = sK + i * LD;
-      const float* kj = sK + j * LD;
-      const float* qi = sQ + i * LD;
-      const float* gi = sG + i * LD;
-      const float* gj = sG + j * LD;
-      for (int d = 0; d < D; ++d) {
-        const float e = __expf(gi[d] - gj[d]);
-        a += ki[d] * kj[d] * e;
-        if (sM) m += qi[d] * kj[d] * e;
+  constexpr int LD = D + 1, DQ = D / 4, NBLK = 136, NIT = NBLK * 4;
+  for (int p = t; p < KB * KB; p += KT) {         // the upper part stays zero
+    sA[(p / KB) * (KB + 1) + p % KB] = 0.f;
+    if (sM) sM[(p / KB) * (KB + 1) + p % KB] = 0.f;
+  }
+  __syncthreads();
+  for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {   // whole waves take part in the exchanges
+    const bool live = it < NIT;
+    const int b = live ? it >> 2 : 0, qd = it & 3;
+    int bi = 0;
+    while ((bi + 1) * (bi + 2) / 2 <= b) ++bi;
+    const int bj = b - bi * (bi + 1) / 2;
+    const int i0 = 4 * bi, j0 = 4 * bj;
+    float a[4][4], m[4][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
+    if (live) {
+      for (int d = qd * DQ; d < (qd + 1) * DQ; ++d) {
+        float ki[4], qi[4], gi[4], kj[4], gj[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          ki[r] = sK[(i0 + r) * LD + d];
+          qi[r] = sM ? sQ[(i0 + r) * LD + d] : 0.f;
+          gi[r] = sG[(i0 + r) * LD + d];
+          kj[r] = sK[(j0 + r) * LD + d];
+          gj[r] = sG[(j0 + r) * LD + d];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const float e = __expf(fminf(gi[r] - gj[cc], 0.f));
+            const float ke = kj[cc] * e;
+            a[r][cc] += ki[r] * ke;
+            m[r][cc] += qi[r] * ke;
+          }
       }
     }
-    sA[i * (KB + 1) + j] = j < i ? a : 0.f;
-    if (sM) sM[i * (KB + 1) + j] = m;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        a[r][cc] += __shfl_xor(a[r][cc], 1);
+        a[r][cc] += __shfl_xor(a[r][cc], 2);
+        if (sM) {
+          m[r][cc] += __shfl_xor(m[r][cc], 1);
+          m[r][cc] += __shfl_xor(m[r][cc], 2);
+        }
+      }
+    if (live && qd == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          const int i = i0 + r, j = j0 + cc;
+          if (j < i) sA[i * (KB + 1) + j] = a[r][cc];
+          if (sM && j <= i) sM[i * (KB + 1) + j] = m[r][cc];
+        }
+    }
   }
 }
 
@@ -190,91 +236,208 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   }
   load_rows<T, D>(sQ, v, ent, H, h, t);   // V into the Q tile
   __syncthreads();
-  // W = Tm (K e^G), U' = Tm V
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int i = idx / D, d = idx % D;
-    float a = 0.f, u = 0.f;
-    for (int j = 0; j <= i; ++j) {
-      const float tm = sA[i * (KB + 1) + j];
-      a += tm * sK[j * LD + d];
-      u += tm * sQ[j * LD + d];
+  // W = Tm (K e^G), U' = Tm V: 4 x 4 output tiles per thread
+  for (int tile = t; tile < KB * D / 16; tile += KT) {
+    const int i0 = (tile / (D / 4)) * 4, d0 = (tile % (D / 4)) * 4;
+    float a[4][4], u[4][4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) a[r][cc] = u[r][cc] = 0.f;
+    for (int j = 0; j <= i0 + 3; ++j) {
+      float tm[4], kg[4], vv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        tm[r] = sA[(i0 + r) * (KB + 1) + j];        // 0 above the diagonal
+        kg[r] = sK[j * LD + d0 + r];
+        vv[r] = sQ[j * LD + d0 + r];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          a[r][cc] += tm[r] * kg[cc];
+          u[r][cc] += tm[r] * vv[cc];
+        }
     }
-    w[Y::W + idx] = a;
-    w[Y::UP + idx] = u;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        w[Y::W + (i0 + r) * D + d0 + cc] = a[r][cc];
+        w[Y::UP + (i0 + r) * D + d0 + cc] = u[r][cc];
+      }
   }
 }
 
-// One (sequence, head, 32 state columns): the chunks of the sequence in
-// order.  S starts from the sequence's bank entry; the state at the start of
-// every requested chunk goes to its bank entry, the end state to S_final.
-template <int D>
-__global__ __launch_bounds__(KT) void k_kda_state(const int32_t* __restrict__ seq_tab, int32_t s0,
-                                                  const int32_t* __restrict__ req_tab, int H, float* __restrict__ ws,
-                                                  float* __restrict__ bank, float* __restrict__ S_final) {
+// The state recurrence of one (sequence, head, 64 state columns), chunk by
+// chunk, forward and reverse in one template.  With Sc the running state
+// (forward: S; reverse: the adjoint dS of the chunk's end state):
+//   forward  X = U' - W S,       S  = Diag(gamma) S + KB^T X
+//   reverse  dX = dXo + KB dS,   dS = Diag(gamma) dS + dSo - W^T dX
+// i.e. Xc = P + s1 A1 Sc and Sc = Diag(gamma) Sc + P2 + s2 A2^T Xc.  The
+// running state is stored per chunk before its update (S_c, or dSn_c), and
+// Xc too.  Thread tiles: 2 x 4 of Xc (64 x 64), TR x 4 of Sc (D x 64); the
+// next chunk's A1, A2, P, P2 and gamma are loaded into registers while the
+// current one is computed.  Forward: S starts from the bank entry, the
+// states at requested chunk starts go to the bank, the end state to
+// S_final.  Reverse: dS starts from dS_final (plus the bank adjoints of
+// requests at the end), the bank adjoints of requested chunk starts are
+// added as the pass reaches them, and the initial state's adjoint goes to
+// dS0_seq.
+constexpr int SQV = 64;                  // state columns per workgroup
+constexpr int SQL = SQV + 4;             // LDS row stride of Sc and Xc (16-byte rows)
+
+template <int D, bool REV>
+__global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_tab, int32_t s0,
+                                                const int32_t* __restrict__ req_tab, int H, float* __restrict__ ws,
+                                                float* __restrict__ bank, float* __restrict__ S_final,
+                                                const float* __restrict__ dbank, float* __restrict__ dS0_seq) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 1, NS = D / KVS;
-  constexpr int LV = KVS + 1;
+  constexpr int LA = D + 4, NV = D / SQV, TR = D * SQV / (KT * 4);   // TR: Sc rows per thread tile
+  constexpr int NA = KB * D / 4 / KT;                                   // float4 of one A tile per thread
+  constexpr int64_t OA1 = REV ? Y::KBM : Y::W, OA2 = REV ? Y::W : Y::KBM, OP = REV ? Y::DXO : Y::UP;
+  constexpr int64_t OSC = REV ? Y::DSN : Y::SC, OX = REV ? Y::DX : Y::X;
+  constexpr float S1 = REV ? 1.f : -1.f, S2 = REV ? -1.f : 1.f;
   extern __shared__ float sm[];
-  float* sW = sm;                 // [64][D + 1]
-  float* sKB = sW + KB * LD;      // [64][D + 1]
-  float* sS = sKB + KB * LD;      // [D][KVS + 1]
-  float* sX = sS + D * LV;        // [64][KVS + 1]
-  float* sg = sX + KB * LV;       // [D]
+  float* sA1 = sm;                 // [64][D + 4]
+  float* sA2 = sA1 + KB * LA;      // [64][D + 4]
+  float* sS = sA2 + KB * LA;       // [D][68]
+  float* sX = sS + D * SQL;        // [64][68]
+  float* sg = sX + KB * SQL;       // [D]
   const int b = blockIdx.x;
-  const int slab = b % NS, h = (b / NS) % H, seq = s0 + b / (NS * H);
-  const int t = threadIdx.x;
+  const int slab = b % NV, h = (b / NV) % H, seq = s0 + b / (NV * H);
+  const int t = threadIdx.x, v0 = slab * SQV;
   const int32_t* st_ = seq_tab + 8 * seq;
   const int c_first = st_[1], nc = st_[2], init = st_[3], ro = st_[4], nr = st_[5], leaf = st_[6];
-  const int v0 = slab * KVS;
-  auto state_at = [&](float* base, int64_t entry) {   // [entry][H][D][D] slab pointer
-    return base + (entry * H + h) * Y::DD;
-  };
-  {
-    const float* s = state_at(bank, init);
-    for (int idx = t; idx < D * KVS; idx += KT) sS[(idx / KVS) * LV + idx % KVS] = s[(idx / KVS) * D + v0 + idx % KVS];
+  const int xr = (t / 16) * 2, xc = (t % 16) * 4;      // Xc tile: rows xr..xr+1, columns xc..xc+3
+  const int sr = (t / 16) * TR, sc = (t % 16) * 4;     // Sc tile: rows sr..sr+TR-1, columns sc..sc+3
+  auto slab_of = [&](const float* base, int64_t entry) { return base + (entry * H + h) * Y::DD + v0; };
+  // running state
+  if (!REV) {
+    const float* src = slab_of(bank, init);
+    for (int idx = t; idx < D * SQV; idx += KT) sS[(idx / SQV) * SQL + idx % SQV] = src[(idx / SQV) * D + idx % SQV];
+  } else {
+    for (int idx = t; idx < D * SQV; idx += KT) {
+      const int r = idx / SQV, cc = idx % SQV;
+      float a = S_final ? slab_of(S_final, leaf)[r * D + cc] : 0.f;
+      for (int q = 0; q < nr; ++q)
+        if (req_tab[2 * (ro + q)] == nc) a += slab_of(dbank, req_tab[2 * (ro + q) + 1])[r * D + cc];
+      sS[r * SQL + cc] = a;
+    }
   }
+  // register prefetch of one chunk
+  float4 pA1[NA], pA2[NA], pP[2], pP2[TR], pg = {0.f, 0.f, 0.f, 0.f};
+  auto fetch = [&](int cc) {
+    const float* w = ws + (static_cast<int64_t>(c_first + cc) * H + h) * Y::ALL;
+#pragma unroll
+    for (int n = 0; n < NA; ++n) {
+      pA1[n] = *reinterpret_cast<const float4*>(w + OA1 + 4 * (t + KT * n));
+      pA2[n] = *reinterpret_cast<const float4*>(w + OA2 + 4 * (t + KT * n));
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) pP[r] = *reinterpret_cast<const float4*>(w + OP + (xr + r) * D + v0 + xc);
+#pragma unroll
+    for (int r = 0; r < TR; ++r)
+      pP2[r] = REV ? *reinterpret_cast<const float4*>(w + Y::DSO + (sr + r) * D + v0 + sc) : float4{0.f, 0.f, 0.f, 0.f};
+    if (t < D / 4) pg = *reinterpret_cast<const float4*>(w + Y::GAM + 4 * t);
+  };
+  if (nc > 0) fetch(REV ? nc - 1 : 0);
   __syncthreads();
   int rq = 0;
-  for (int cc = 0; cc <= nc; ++cc) {
-    // requested boundary states at the start of chunk cc (cc == nc: the end)
-    for (; rq < nr && req_tab[2 * (ro + rq)] <= cc; ++rq) {
-      if (req_tab[2 * (ro + rq)] != cc) continue;
-      float* d = state_at(bank, req_tab[2 * (ro + rq) + 1]);
-      for (int idx = t; idx < D * KVS; idx += KT) d[(idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+  for (int step = 0; step <= nc; ++step) {
+    const int cc = REV ? nc - 1 - step : step;
+    if (!REV) {      // requested states at the start of chunk cc (cc == nc: the end)
+      for (; rq < nr && req_tab[2 * (ro + rq)] <= cc; ++rq) {
+        if (req_tab[2 * (ro + rq)] != cc) continue;
+        float* dst = bank + (static_cast<int64_t>(req_tab[2 * (ro + rq) + 1]) * H + h) * Y::DD + v0;
+        for (int idx = t; idx < D * SQV; idx += KT) dst[(idx / SQV) * D + idx % SQV] = sS[(idx / SQV) * SQL + idx % SQV];
+      }
     }
-    if (cc == nc) break;
-    const int64_t ch = static_cast<int64_t>(c_first + cc) * H + h;
-    float* w = ws + ch * Y::ALL;
-    for (int idx = t; idx < KB * D; idx += KT) {
-      sW[(idx / D) * LD + idx % D] = w[Y::W + idx];
-      sKB[(idx / D) * LD + idx % D] = w[Y::KBM + idx];
+    if (step == nc) break;
+    float* w = ws + (static_cast<int64_t>(c_first + cc) * H + h) * Y::ALL;
+    // this chunk's operands into LDS, the running state to the workspace
+#pragma unroll
+    for (int n = 0; n < NA; ++n) {
+      const int e = 4 * (t + KT * n), r = e / D, c = e % D;
+      *reinterpret_cast<float4*>(sA1 + r * LA + c) = pA1[n];
+      *reinterpret_cast<float4*>(sA2 + r * LA + c) = pA2[n];
     }
-    if (t < D) sg[t] = w[Y::GAM + t];
-    for (int idx = t; idx < D * KVS; idx += KT)      // chunk start state, for the outputs and the backward
-      w[Y::SC + (idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
+    if (t < D / 4) *reinterpret_cast<float4*>(sg + 4 * t) = pg;
+    float4 cP[2], cP2[TR];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) cP[r] = pP[r];
+#pragma unroll
+    for (int r = 0; r < TR; ++r) cP2[r] = pP2[r];
+    for (int idx = t; idx < D * SQV / 4; idx += KT) {
+      const int r = (4 * idx) / SQV, c = (4 * idx) % SQV;
+      *reinterpret_cast<float4*>(w + OSC + r * D + v0 + c) = *reinterpret_cast<const float4*>(sS + r * SQL + c);
+    }
     __syncthreads();
-    // X = U' - W S
-    for (int idx = t; idx < KB * KVS; idx += KT) {
-      const int i = idx / KVS, vv = idx % KVS;
-      float a = w[Y::UP + i * D + v0 + vv];
-      for (int d = 0; d < D; ++d) a -= sW[i * LD + d] * sS[d * LV + vv];
-      sX[i * LV + vv] = a;
-      w[Y::X + i * D + v0 + vv] = a;
+    const int nxt = REV ? cc - 1 : cc + 1;
+    if (nxt >= 0 && nxt < nc) fetch(nxt);
+    // Xc = P + s1 A1 Sc
+    {
+      float x[2][4];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        x[r][0] = cP[r].x; x[r][1] = cP[r].y; x[r][2] = cP[r].z; x[r][3] = cP[r].w;
+      }
+      float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+      for (int d = 0; d < D; ++d) {
+        const float a0 = sA1[xr * LA + d], a1 = sA1[(xr + 1) * LA + d];
+        const float4 sv = *reinterpret_cast<const float4*>(sS + d * SQL + xc);
+        acc[0][0] += a0 * sv.x; acc[0][1] += a0 * sv.y; acc[0][2] += a0 * sv.z; acc[0][3] += a0 * sv.w;
+        acc[1][0] += a1 * sv.x; acc[1][1] += a1 * sv.y; acc[1][2] += a1 * sv.z; acc[1][3] += a1 * sv.w;
+      }
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const float4 o = {x[r][0] + S1 * acc[r][0], x[r][1] + S1 * acc[r][1], x[r][2] + S1 * acc[r][2],
+                          x[r][3] + S1 * acc[r][3]};
+        *reinterpret_cast<float4*>(sX + (xr + r) * SQL + xc) = o;
+        *reinterpret_cast<float4*>(w + OX + (xr + r) * D + v0 + xc) = o;
+      }
     }
     __syncthreads();
-    // S = Diag(gamma) S + KB^T X
-    for (int idx = t; idx < D * KVS; idx += KT) {
-      const int d = idx / KVS, vv = idx % KVS;
-      float a = sg[d] * sS[d * LV + vv];
-      for (int i = 0; i < KB; ++i) a += sKB[i * LD + d] * sX[i * LV + vv];
-      sS[d * LV + vv] = a;
+    // Sc = Diag(gamma) Sc + P2 + s2 A2^T Xc
+    {
+      float acc[TR][4];
+#pragma unroll
+      for (int r = 0; r < TR; ++r) acc[r][0] = acc[r][1] = acc[r][2] = acc[r][3] = 0.f;
+      for (int i = 0; i < KB; ++i) {
+        const float4 xv = *reinterpret_cast<const float4*>(sX + i * SQL + sc);
+        float av[TR];
+#pragma unroll
+        for (int r = 0; r < TR; ++r) av[r] = sA2[i * LA + sr + r];
+#pragma unroll
+        for (int r = 0; r < TR; ++r) {
+          acc[r][0] += av[r] * xv.x; acc[r][1] += av[r] * xv.y; acc[r][2] += av[r] * xv.z; acc[r][3] += av[r] * xv.w;
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < TR; ++r) {
+        const float gm = sg[sr + r];
+        float4 cur = *reinterpret_cast<const float4*>(sS + (sr + r) * SQL + sc);
+        cur.x = gm * cur.x + cP2[r].x + S2 * acc[r][0];
+        cur.y = gm * cur.y + cP2[r].y + S2 * acc[r][1];
+        cur.z = gm * cur.z + cP2[r].z + S2 * acc[r][2];
+        cur.w = gm * cur.w + cP2[r].w + S2 * acc[r][3];
+        if (REV)       // adjoints of the requested state at the start of chunk cc
+          for (int q = 0; q < nr; ++q)
+            if (req_tab[2 * (ro + q)] == cc) {
+              const float4 db = *reinterpret_cast<const float4*>(
+                  slab_of(dbank, req_tab[2 * (ro + q) + 1]) + (sr + r) * D + sc);
+              cur.x += db.x; cur.y += db.y; cur.z += db.z; cur.w += db.w;
+            }
+        *reinterpret_cast<float4*>(sS + (sr + r) * SQL + sc) = cur;
+      }
     }
     __syncthreads();
   }
-  if (S_final) {
-    float* d = state_at(S_final, leaf);
-    for (int idx = t; idx < D * KVS; idx += KT) d[(idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
-  }
+  float* dst = REV ? dS0_seq + (static_cast<int64_t>(seq) * H + h) * Y::DD + v0
+                   : (S_final ? S_final + (static_cast<int64_t>(leaf) * H + h) * Y::DD + v0 : nullptr);
+  if (dst)
+    for (int idx = t; idx < D * SQV; idx += KT) dst[(idx / SQV) * D + idx % SQV] = sS[(idx / SQV) * SQL + idx % SQV];
 }
 
 // Outputs of one (chunk, head, 64 state columns): O = scale (QG S + M X),
@@ -347,71 +510,6 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
     for (int i = 0; i < KB; ++i) a += sQG[i * LD + d] * sD[i * LD + vv];
     w[Y::DSO + idx] = scale * a;
   }
-}
-
-// Reverse state pass of one (sequence, head, 32 columns): dSn of every chunk
-// (the adjoint of its end state), dX = dXo + KB dSn, and
-// dS = Diag(gamma) dSn + dSo - W^T dX, plus the later rounds' adjoints of the
-// requested states; the adjoint of the initial state goes to dS0_seq.
-template <int D>
-__global__ __launch_bounds__(KT) void k_kda_bwd_state(const int32_t* __restrict__ seq_tab, int32_t s0,
-                                                      const int32_t* __restrict__ req_tab, int H,
-                                                      float* __restrict__ ws, const float* __restrict__ dS_final,
-                                                      const float* __restrict__ dbank, float* __restrict__ dS0_seq) {
-  using Y = WsLay<D>;
-  constexpr int LD = D + 1, NS = D / KVS, LV = KVS + 1;
-  extern __shared__ float sm[];
-  float* sW = sm;
-  float* sKB = sW + KB * LD;
-  float* sS = sKB + KB * LD;     // dS [D][KVS + 1]
-  float* sX = sS + D * LV;       // dX [64][KVS + 1]
-  float* sg = sX + KB * LV;
-  const int b = blockIdx.x;
-  const int slab = b % NS, h = (b / NS) % H, seq = s0 + b / (NS * H);
-  const int t = threadIdx.x;
-  const int32_t* st_ = seq_tab + 8 * seq;
-  const int c_first = st_[1], nc = st_[2], ro = st_[4], nr = st_[5], leaf = st_[6];
-  const int v0 = slab * KVS;
-  auto slab_of = [&](const float* base, int64_t entry) { return base + (entry * H + h) * Y::DD; };
-  for (int idx = t; idx < D * KVS; idx += KT) {
-    const int d = idx / KVS, vv = idx % KVS;
-    float a = dS_final ? slab_of(dS_final, leaf)[d * D + v0 + vv] : 0.f;
-    for (int r = 0; r < nr; ++r)
-      if (req_tab[2 * (ro + r)] == nc) a += slab_of(dbank, req_tab[2 * (ro + r) + 1])[d * D + v0 + vv];
-    sS[d * LV + vv] = a;
-  }
-  __syncthreads();
-  for (int cc = nc - 1; cc >= 0; --cc) {
-    const int64_t ch = static_cast<int64_t>(c_first + cc) * H + h;
-    float* w = ws + ch * Y::ALL;
-    for (int idx = t; idx < KB * D; idx += KT) {
-      sW[(idx / D) * LD + idx % D] = w[Y::W + idx];
-      sKB[(idx / D) * LD + idx % D] = w[Y::KBM + idx];
-    }
-    if (t < D) sg[t] = w[Y::GAM + t];
-    for (int idx = t; idx < D * KVS; idx += KT)
-      w[Y::DSN + (idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
-    __syncthreads();
-    for (int idx = t; idx < KB * KVS; idx += KT) {
-      const int i = idx / KVS, vv = idx % KVS;
-      float a = w[Y::DXO + i * D + v0 + vv];
-      for (int d = 0; d < D; ++d) a += sKB[i * LD + d] * sS[d * LV + vv];
-      sX[i * LV + vv] = a;
-      w[Y::DX + i * D + v0 + vv] = a;
-    }
-    __syncthreads();
-    for (int idx = t; idx < D * KVS; idx += KT) {
-      const int d = idx / KVS, vv = idx % KVS;
-      float a = sg[d] * sS[d * LV + vv] + w[Y::DSO + d * D + v0 + vv];
-      for (int i = 0; i < KB; ++i) a -= sW[i * LD + d] * sX[i * LV + vv];
-      for (int r = 0; r < nr; ++r)
-        if (req_tab[2 * (ro + r)] == cc) a += slab_of(dbank, req_tab[2 * (ro + r) + 1])[d * D + v0 + vv];
-      sS[d * LV + vv] = a;
-    }
-    __syncthreads();
-  }
-  float* d0 = dS0_seq + (static_cast<int64_t>(seq) * H + h) * Y::DD;
-  for (int idx = t; idx < D * KVS; idx += KT) d0[(idx / KVS) * D + v0 + idx % KVS] = sS[(idx / KVS) * LV + idx % KVS];
 }
 
 // Products of one (chunk, head) with its states, contracted over the value
@@ -757,7 +855,7 @@ int kda_status(const char* where) {
 template <int D>
 constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB) * sizeof(float); }
 template <int D>
-constexpr size_t lds_state() { return (2 * KB * (D + 1) + D * (KVS + 1) + KB * (KVS + 1) + D) * sizeof(float); }
+constexpr size_t lds_seq() { return (2 * KB * (D + 4) + D * SQL + KB * SQL + D) * sizeof(float); }
 template <int D>
 constexpr size_t lds_out() { return (KB * (D + 1) + D * 65 + 2 * KB * (KB + 1)) * sizeof(float); }
 template <int D>
@@ -791,9 +889,9 @@ int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     if (int rc = kda_status("k_kda_prep")) return rc;
   }
   if (a.n_seq > 0) {
-    hipLaunchKernelGGL((k_kda_state<D>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / KVS))), dim3(KT),
-                       lds_state<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final);
-    if (int rc = kda_status("k_kda_state")) return rc;
+    hipLaunchKernelGGL((k_kda_seq<D, false>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / SQV))), dim3(KT),
+                       lds_seq<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
+    if (int rc = kda_status("k_kda_seq")) return rc;
   }
   if (a.n_chunks > 0 && o) {
     hipLaunchKernelGGL((k_kda_out<T, D>), dim3(static_cast<uint32_t>(a.n_chunks * a.H * (D / 64))), dim3(KT),
@@ -818,9 +916,10 @@ int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     if (int rc = kda_status("k_kda_bwd_prep")) return rc;
   }
   if (a.n_seq > 0) {
-    hipLaunchKernelGGL((k_kda_bwd_state<D>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / KVS))), dim3(KT),
-                       lds_state<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, dS_final, dbank, dS0_seq);
-    if (int rc = kda_status("k_kda_bwd_state")) return rc;
+    hipLaunchKernelGGL((k_kda_seq<D, true>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / SQV))), dim3(KT),
+                       lds_seq<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, nullptr, const_cast<float*>(dS_final),
+                       dbank, dS0_seq);
+    if (int rc = kda_status("k_kda_seq (reverse)")) return rc;
   }
   if (a.n_chunks > 0) {
     hipLaunchKernelGGL((k_kda_bwd_prod<T, D>), dim3(gc), dim3(KT), lds_bprod<D>(), s, a.chunk_rows, a.c0, a.H,
@@ -851,12 +950,12 @@ bool kda_set_lds() {
   if (done) return true;
   const void* fns[] = {reinterpret_cast<const void*>(&k_kda_prep<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_prep<float, D>),
-                       reinterpret_cast<const void*>(&k_kda_state<D>),
+                       reinterpret_cast<const void*>(&k_kda_seq<D, false>),
+                       reinterpret_cast<const void*>(&k_kda_seq<D, true>),
                        reinterpret_cast<const void*>(&k_kda_out<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_out<float, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prep<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prep<float, D>),
-                       reinterpret_cast<const void*>(&k_kda_bwd_state<D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prod<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prod<float, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_tm<bf16, D>),
