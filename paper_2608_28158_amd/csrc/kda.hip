@@ -168,18 +168,41 @@ __device__ inline void pair_sums(float* sA, float* sM, const float* sK, const fl
   }
 }
 
-// sL = (I + Diag(beta) At)^{-1}, unit lower triangular, by forward
-// substitution, one column per thread.
-__device__ inline void tri_inverse(float* sL, const float* sA, const float* sb, int t) {
-  constexpr int LD = KB + 1;
-  if (t < KB) {
-    const int c = t;
-    for (int i = 0; i < KB; ++i) sL[i * LD + c] = i == c ? 1.f : 0.f;
-    for (int i = c + 1; i < KB; ++i) {
+// sL = (I + Diag(beta) At)^{-1}, unit lower triangular, in 16 x 16 blocks:
+// the four diagonal blocks by forward substitution (one column per thread),
+// then block row by block row, L^{-1}_{IJ} = -L^{-1}_{II} sum_{J <= K < I}
+// N_{IK} L^{-1}_{KJ} with N = Diag(beta) At.  sW is a 64 x 65 scratch tile.
+__device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const float* sb, int t) {
+  constexpr int LD = KB + 1, BS = 16;
+  for (int p = t; p < KB * KB; p += KT) sL[(p / KB) * LD + p % KB] = (p / KB == p % KB) ? 1.f : 0.f;
+  __syncthreads();
+  if (t < KB) {                                   // diagonal blocks
+    const int c = t, r0 = (c / BS) * BS;
+    for (int i = c + 1; i < r0 + BS; ++i) {
       float s = 0.f;
       for (int j = c; j < i; ++j) s += sA[i * LD + j] * sL[j * LD + c];
       sL[i * LD + c] = -sb[i] * s;
     }
+  }
+  __syncthreads();
+  for (int I = 1; I < KB / BS; ++I) {
+    // sW[I rows][J cols] = sum_{J <= K < I} N_IK L^{-1}_KJ, for every J < I
+    for (int p = t; p < BS * I * BS; p += KT) {
+      const int i = I * BS + p / (I * BS), j = p % (I * BS);
+      const int k0 = (j / BS) * BS;
+      float s = 0.f;
+      for (int k = k0; k < I * BS; ++k) s += sA[i * LD + k] * sL[k * LD + j];
+      sW[i * LD + j] = sb[i] * s;
+    }
+    __syncthreads();
+    // L^{-1}_{IJ} = -L^{-1}_{II} sW_{IJ}
+    for (int p = t; p < BS * I * BS; p += KT) {
+      const int i = I * BS + p / (I * BS), j = p % (I * BS);
+      float s = 0.f;
+      for (int k = I * BS; k <= i; ++k) s += sL[i * LD + k] * sW[k * LD + j];
+      sL[i * LD + j] = -s;
+    }
+    __syncthreads();
   }
 }
 
@@ -210,18 +233,11 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   // At and M (M straight to the workspace through sL, then sL is reused)
   pair_sums<D>(sA, sL, sK, sQ, sG, t);
   __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) w[Y::M + p] = sL[(p / KB) * (KB + 1) + p % KB];
-  __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * (KB + 1) + p % KB];
-  tri_inverse(sL, sA, sb, t);
-  __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) w[Y::LINV + p] = sL[(p / KB) * (KB + 1) + p % KB];
-  // Tm = L^{-1} Diag(beta) into sA
   for (int p = t; p < KB * KB; p += KT) {
-    const int i = p / KB, j = p % KB;
-    sA[i * (KB + 1) + j] = j <= i ? sL[i * (KB + 1) + j] * sb[j] : 0.f;
+    w[Y::M + p] = sL[(p / KB) * (KB + 1) + p % KB];
+    w[Y::AT + p] = sA[(p / KB) * (KB + 1) + p % KB];
   }
-  // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B}; then K -> K e^G in place
+  // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B}
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
     const float G = sG[r * LD + d], GB = sG[(KB - 1) * LD + d];
@@ -230,10 +246,18 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   }
   if (t < D) w[Y::GAM + t] = __expf(sG[(KB - 1) * LD + t]);
   __syncthreads();
+  tri_inverse(sL, sQ, sA, sb, t);          // the Q tile is free now: scratch
+  for (int p = t; p < KB * KB; p += KT) w[Y::LINV + p] = sL[(p / KB) * (KB + 1) + p % KB];
+  // Tm = L^{-1} Diag(beta) into sA; K -> K e^G in place
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    sA[i * (KB + 1) + j] = j <= i ? sL[i * (KB + 1) + j] * sb[j] : 0.f;
+  }
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
     sK[r * LD + d] *= __expf(sG[r * LD + d]);
   }
+  __syncthreads();
   load_rows<T, D>(sQ, v, ent, H, h, t);   // V into the Q tile
   __syncthreads();
   // W = Tm (K e^G), U' = Tm V: 4 x 4 output tiles per thread
@@ -441,51 +465,77 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
 }
 
 // Outputs of one (chunk, head, 64 state columns): O = scale (QG S + M X),
-// written for own rows only.
+// written for own rows only; 2 x 4 output tiles per thread.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                 float scale, const float* __restrict__ ws, T* __restrict__ o) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 1, VH = 64, LV = VH + 1, NV = D / VH;
+  constexpr int LD = D + 4, VH = 64, NV = D / VH;
   extern __shared__ float sm[];
-  float* sQG = sm;                // [64][D + 1]
-  float* sS = sQG + KB * LD;      // [D][65]
-  float* sM = sS + D * LV;        // [64][65]
-  float* sX = sM + KB * (KB + 1); // [64][65]
+  float* sQG = sm;                // [64][D + 4]
+  float* sS = sQG + KB * LD;      // [D][68]
+  float* sM = sS + D * SQL;       // [64][68]
+  float* sX = sM + KB * SQL;      // [64][68]
   const int b = blockIdx.x;
   const int half = b % NV, h = (b / NV) % H, c = static_cast<int>(b / (NV * H) + c0);
   const int t = threadIdx.x, v0 = half * VH;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   const float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  for (int idx = t; idx < KB * D; idx += KT) sQG[(idx / D) * LD + idx % D] = w[Y::QG + idx];
-  for (int idx = t; idx < D * VH; idx += KT) sS[(idx / VH) * LV + idx % VH] = w[Y::SC + (idx / VH) * D + v0 + idx % VH];
-  for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * (KB + 1) + idx % KB] = w[Y::M + idx];
-  for (int idx = t; idx < KB * VH; idx += KT) sX[(idx / VH) * LV + idx % VH] = w[Y::X + (idx / VH) * D + v0 + idx % VH];
+  for (int idx = t; idx < KB * D / 4; idx += KT) {
+    const int e = 4 * idx;
+    *reinterpret_cast<float4*>(sQG + (e / D) * LD + e % D) = *reinterpret_cast<const float4*>(w + Y::QG + e);
+  }
+  for (int idx = t; idx < D * VH / 4; idx += KT) {
+    const int e = 4 * idx, r = e / VH, cc = e % VH;
+    *reinterpret_cast<float4*>(sS + r * SQL + cc) = *reinterpret_cast<const float4*>(w + Y::SC + r * D + v0 + cc);
+  }
+  for (int idx = t; idx < KB * KB / 4; idx += KT) {
+    const int e = 4 * idx;
+    *reinterpret_cast<float4*>(sM + (e / KB) * SQL + e % KB) = *reinterpret_cast<const float4*>(w + Y::M + e);
+  }
+  for (int idx = t; idx < KB * VH / 4; idx += KT) {
+    const int e = 4 * idx, r = e / VH, cc = e % VH;
+    *reinterpret_cast<float4*>(sX + r * SQL + cc) = *reinterpret_cast<const float4*>(w + Y::X + r * D + v0 + cc);
+  }
   __syncthreads();
-  for (int idx = t; idx < KB * VH; idx += KT) {
-    const int i = idx / VH, vv = idx % VH;
-    const int32_t e = ent[i];
+  const int i0 = (t / 16) * 2, vc = (t % 16) * 4;
+  float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  for (int d = 0; d < D; ++d) {
+    const float a0 = sQG[i0 * LD + d], a1 = sQG[(i0 + 1) * LD + d];
+    const float4 sv = *reinterpret_cast<const float4*>(sS + d * SQL + vc);
+    acc[0][0] += a0 * sv.x; acc[0][1] += a0 * sv.y; acc[0][2] += a0 * sv.z; acc[0][3] += a0 * sv.w;
+    acc[1][0] += a1 * sv.x; acc[1][1] += a1 * sv.y; acc[1][2] += a1 * sv.z; acc[1][3] += a1 * sv.w;
+  }
+  for (int j = 0; j <= i0 + 1; ++j) {
+    const float m0 = j <= i0 ? sM[i0 * SQL + j] : 0.f, m1 = sM[(i0 + 1) * SQL + j];
+    const float4 xv = *reinterpret_cast<const float4*>(sX + j * SQL + vc);
+    acc[0][0] += m0 * xv.x; acc[0][1] += m0 * xv.y; acc[0][2] += m0 * xv.z; acc[0][3] += m0 * xv.w;
+    acc[1][0] += m1 * xv.x; acc[1][1] += m1 * xv.y; acc[1][2] += m1 * xv.z; acc[1][3] += m1 * xv.w;
+  }
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int32_t e = ent[i0 + r];
     if (e < 0 || !(e & 1)) continue;
-    float a = 0.f;
-    for (int d = 0; d < D; ++d) a += sQG[i * LD + d] * sS[d * LV + vv];
-    for (int j = 0; j <= i; ++j) a += sM[i * (KB + 1) + j] * sX[j * LV + vv];
-    st<T>(o + (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vv, scale * a);
+    T* dst = o + (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vc;
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) st<T>(dst + cc, scale * acc[r][cc]);
   }
 }
 
 // ---------------------------------------------------------------------------
 // backward
 // ---------------------------------------------------------------------------
-// dXo = scale M^T dO (64 x D), dSo = scale QG^T dO (D x D), dO of own rows.
+// dXo = scale M^T dO (64 x D), dSo = scale QG^T dO (D x D), dO of own rows;
+// 4 x 4 and 4 x 8 output tiles per thread.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                      float scale, const T* __restrict__ dO, float* __restrict__ ws) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 1;
+  constexpr int LD = D + 4;
   extern __shared__ float sm[];
-  float* sQG = sm;                 // [64][D + 1]
-  float* sD = sQG + KB * LD;       // [64][D + 1]
-  float* sM = sD + KB * LD;        // [64][65]
+  float* sQG = sm;                 // [64][D + 4]
+  float* sD = sQG + KB * LD;       // [64][D + 4]
+  float* sM = sD + KB * LD;        // [64][68]
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -496,19 +546,56 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
     sQG[r * LD + d] = w[Y::QG + idx];
     sD[r * LD + d] = (e >= 0 && (e & 1)) ? ld<T>(dO + (static_cast<int64_t>(e >> 1) * H + h) * D + d) : 0.f;
   }
-  for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * (KB + 1) + idx % KB] = w[Y::M + idx];
+  for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * SQL + idx % KB] = w[Y::M + idx];
   __syncthreads();
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int j = idx / D, vv = idx % D;
-    float a = 0.f;
-    for (int i = j; i < KB; ++i) a += sM[i * (KB + 1) + j] * sD[i * LD + vv];
-    w[Y::DXO + idx] = scale * a;
+  {   // dXo: rows j0..j0+3, columns v0..v0+TD-1
+    constexpr int TD = D / 32;
+    const int j0 = (t / 32) * 4, v0 = (t % 32) * TD;
+    float acc[4][TD];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < TD; ++cc) acc[r][cc] = 0.f;
+    for (int i = j0; i < KB; ++i) {
+      float m_[4], d_[TD];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m_[r] = j0 + r <= i ? sM[i * SQL + j0 + r] : 0.f;
+#pragma unroll
+      for (int cc = 0; cc < TD; ++cc) d_[cc] = sD[i * LD + v0 + cc];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < TD; ++cc) acc[r][cc] += m_[r] * d_[cc];
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < TD; ++cc) w[Y::DXO + (j0 + r) * D + v0 + cc] = scale * acc[r][cc];
   }
-  for (int idx = t; idx < D * D; idx += KT) {
-    const int d = idx / D, vv = idx % D;
-    float a = 0.f;
-    for (int i = 0; i < KB; ++i) a += sQG[i * LD + d] * sD[i * LD + vv];
-    w[Y::DSO + idx] = scale * a;
+  {   // dSo: rows d0..d0+3, columns v0..v0+TV-1
+    constexpr int TV = D * D / (KT * 4);
+    constexpr int NCT = D / TV;               // column tiles
+    const int d0 = (t / NCT) * 4, v0 = (t % NCT) * TV;
+    float acc[4][TV];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < TV; ++cc) acc[r][cc] = 0.f;
+    for (int i = 0; i < KB; ++i) {
+      float q_[4], d_[TV];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) q_[r] = sQG[i * LD + d0 + r];
+#pragma unroll
+      for (int cc = 0; cc < TV; ++cc) d_[cc] = sD[i * LD + v0 + cc];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < TV; ++cc) acc[r][cc] += q_[r] * d_[cc];
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < TV; ++cc) w[Y::DSO + (d0 + r) * D + v0 + cc] = scale * acc[r][cc];
   }
 }
 
@@ -532,13 +619,20 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  // accumulators: thread t owns rows/cols of the 64 x D outputs at idx = t + 256 n
-  constexpr int NR = KB * D / KT, NP = KB * KB / KT;
-  float aQ[NR], aW[NR], aK[NR], aM[NP], aU[NP], aG = 0.f;
+  // register tiles: 4 rows x TD columns of the three 64 x D products, 2 x 4
+  // of the two 64 x 64 ones
+  constexpr int TD = D / 32;
+  const int i0 = (t / 32) * 4, d0 = (t % 32) * TD;
+  const int pi0 = (t / 16) * 2, pj0 = (t % 16) * 4;
+  float aQ[4][TD], aW[4][TD], aK[4][TD], aM[2][4], aU[2][4], aG = 0.f;
 #pragma unroll
-  for (int n = 0; n < NR; ++n) aQ[n] = aW[n] = aK[n] = 0.f;
+  for (int r = 0; r < 4; ++r)
 #pragma unroll
-  for (int n = 0; n < NP; ++n) aM[n] = aU[n] = 0.f;
+    for (int cc = 0; cc < TD; ++cc) aQ[r][cc] = aW[r][cc] = aK[r][cc] = 0.f;
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) aM[r][cc] = aU[r][cc] = 0.f;
   for (int v0 = 0; v0 < D; v0 += VS) {
     __syncthreads();
     for (int idx = t; idx < D * VS; idx += KT) {
@@ -556,50 +650,67 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
       sX[i * LV + vv] = w[Y::X + i * D + v0 + vv];
     }
     __syncthreads();
+#pragma unroll 2
+    for (int vv = 0; vv < VS; ++vv) {
+      float o_[4], dx_[4], x_[4], s_[TD], n_[TD];
 #pragma unroll
-    for (int n = 0; n < NR; ++n) {
-      const int idx = t + KT * n, i = idx / D, d = idx % D;
-      float q_ = 0.f, w_ = 0.f, k_ = 0.f;
-#pragma unroll 4
-      for (int vv = 0; vv < VS; ++vv) {
-        const float s = sS[d * LV + vv];
-        q_ += sO[i * LV + vv] * s;
-        w_ += sDX[i * LV + vv] * s;
-        k_ += sX[i * LV + vv] * sN[d * LV + vv];
+      for (int r = 0; r < 4; ++r) {
+        o_[r] = sO[(i0 + r) * LV + vv];
+        dx_[r] = sDX[(i0 + r) * LV + vv];
+        x_[r] = sX[(i0 + r) * LV + vv];
       }
-      aQ[n] += q_;
-      aW[n] += w_;
-      aK[n] += k_;
-    }
 #pragma unroll
-    for (int n = 0; n < NP; ++n) {
-      const int idx = t + KT * n, i = idx / KB, j = idx % KB;
-      if (j > i) continue;
-      float m_ = 0.f, u_ = 0.f;
-#pragma unroll 4
-      for (int vv = 0; vv < VS; ++vv) {
-        m_ += sO[i * LV + vv] * sX[j * LV + vv];
-        u_ += sDX[i * LV + vv] * sV[j * LV + vv];
+      for (int cc = 0; cc < TD; ++cc) {
+        s_[cc] = sS[(d0 + cc) * LV + vv];
+        n_[cc] = sN[(d0 + cc) * LV + vv];
       }
-      aM[n] += m_;
-      aU[n] += u_;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < TD; ++cc) {
+          aQ[r][cc] += o_[r] * s_[cc];
+          aW[r][cc] += dx_[r] * s_[cc];
+          aK[r][cc] += x_[r] * n_[cc];
+        }
+      float po[2], pdx[2], px[4], pv[4];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        po[r] = sO[(pi0 + r) * LV + vv];
+        pdx[r] = sDX[(pi0 + r) * LV + vv];
+      }
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        px[cc] = sX[(pj0 + cc) * LV + vv];
+        pv[cc] = sV[(pj0 + cc) * LV + vv];
+      }
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          aM[r][cc] += po[r] * px[cc];
+          aU[r][cc] += pdx[r] * pv[cc];
+        }
     }
     if (t < D)
       for (int vv = 0; vv < VS; ++vv) aG += sN[t * LV + vv] * sS[t * LV + vv];
   }
 #pragma unroll
-  for (int n = 0; n < NR; ++n) {
-    const int idx = t + KT * n;
-    w[Y::DQG + idx] = scale * aQ[n];
-    w[Y::DW + idx] = -aW[n];
-    w[Y::DKBM + idx] = aK[n];
-  }
+  for (int r = 0; r < 4; ++r)
 #pragma unroll
-  for (int n = 0; n < NP; ++n) {
-    const int idx = t + KT * n, i = idx / KB, j = idx % KB;
-    w[Y::DM + idx] = j <= i ? scale * aM[n] : 0.f;
-    w[Y::DUV + idx] = j <= i ? aU[n] : 0.f;
-  }
+    for (int cc = 0; cc < TD; ++cc) {
+      const int idx = (i0 + r) * D + d0 + cc;
+      w[Y::DQG + idx] = scale * aQ[r][cc];
+      w[Y::DW + idx] = -aW[r][cc];
+      w[Y::DKBM + idx] = aK[r][cc];
+    }
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int cc = 0; cc < 4; ++cc) {
+      const int i = pi0 + r, j = pj0 + cc;
+      w[Y::DM + i * KB + j] = j <= i ? scale * aM[r][cc] : 0.f;
+      w[Y::DUV + i * KB + j] = j <= i ? aU[r][cc] : 0.f;
+    }
   if (t < D) w[Y::DGAM + t] = aG;
 }
 
@@ -745,11 +856,14 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     sL[i * LB + j] = w[Y::DM + p];                          // dM
   }
   __syncthreads();
-  // pairwise terms, per channel: threads 0..D-1 take row i's own terms
-  // (dq_i, dk_i, +dG_i), threads KT/2..KT/2+D-1 the terms of column j (dk_j, -dG_j)
-  if (t < D) {
-    const int d = t;
-    for (int i = 0; i < KB; ++i) {
+  // pairwise terms per channel d: thread (d, group) takes the rows and then
+  // the columns whose index is congruent to the group modulo KT / D (the
+  // triangle's work is then even across groups): row i's own terms (dq_i,
+  // dk_i, +dG_i), then column j's terms (dk_j, -dG_j)
+  {
+    constexpr int NG = KT / D;
+    const int d = t % D, grp = t / D;
+    for (int i = grp; i < KB; i += NG) {
       const float gi = sG[i * D + d], ki = sK[i * D + d], qi = sQ[i * D + d];
       float dq_ = 0.f, dk_ = 0.f, dg_ = 0.f;
       for (int j = 0; j <= i; ++j) {
@@ -765,9 +879,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
       w[Y::P1K + i * D + d] = dk_;
       w[Y::P1G + i * D + d] = dg_;
     }
-  } else if (t >= KT / 2 && t < KT / 2 + D) {
-    const int d = t - KT / 2;
-    for (int j = 0; j < KB; ++j) {
+    for (int j = grp; j < KB; j += NG) {
       const float gj = sG[j * D + d], kj = sK[j * D + d];
       float dk_ = 0.f, dg_ = 0.f;
       for (int i = j; i < KB; ++i) {
@@ -857,9 +969,9 @@ constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB)
 template <int D>
 constexpr size_t lds_seq() { return (2 * KB * (D + 4) + D * SQL + KB * SQL + D) * sizeof(float); }
 template <int D>
-constexpr size_t lds_out() { return (KB * (D + 1) + D * 65 + 2 * KB * (KB + 1)) * sizeof(float); }
+constexpr size_t lds_out() { return (KB * (D + 4) + D * SQL + 2 * KB * SQL) * sizeof(float); }
 template <int D>
-constexpr size_t lds_bprep() { return (2 * KB * (D + 1) + KB * (KB + 1)) * sizeof(float); }
+constexpr size_t lds_bprep() { return (2 * KB * (D + 4) + KB * SQL) * sizeof(float); }
 template <int D>
 constexpr size_t lds_bprod() { return (2 * D * 33 + 4 * KB * 33) * sizeof(float); }
 template <int D>
