@@ -64,14 +64,42 @@ struct WsLay {
                            P2G = P2K + RD, ALL = P2G + RD;
 };
 
-// Rows of one packed chunk and head into LDS as float32 [64][D + 1] (zero
-// for padding rows).
-template <typename T, int D>
+// Rows of one packed chunk and head into LDS as float32 [64][LDS] (zero for
+// padding rows), 16-byte loads.
+template <typename T> struct RowVec;
+template <> struct RowVec<bf16> {
+  static constexpr int N = 8;
+  __device__ static inline void get(const bf16* p, float* x) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+    }
+  }
+};
+template <> struct RowVec<float> {
+  static constexpr int N = 4;
+  __device__ static inline void get(const float* p, float* x) {
+    const float4 u = *reinterpret_cast<const float4*>(p);
+    x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
+  }
+};
+
+template <typename T, int D, int LDS = D + 1>
 __device__ inline void load_rows(float* s, const T* __restrict__ src, const int32_t* ent, int H, int h, int t) {
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int r = idx / D, c = idx % D;
+  constexpr int N = RowVec<T>::N, VR = D / N;
+  for (int idx = t; idx < KB * VR; idx += KT) {
+    const int r = idx / VR, c = (idx % VR) * N;
     const int32_t e = ent[r];
-    s[r * (D + 1) + c] = e >= 0 ? ld<T>(src + (static_cast<int64_t>(e >> 1) * H + h) * D + c) : 0.f;
+    float x[N];
+    if (e >= 0) RowVec<T>::get(src + (static_cast<int64_t>(e >> 1) * H + h) * D + c, x);
+    else
+#pragma unroll
+      for (int n = 0; n < N; ++n) x[n] = 0.f;
+#pragma unroll
+    for (int n = 0; n < N; ++n) s[r * LDS + c + n] = x[n];
   }
 }
 
@@ -79,10 +107,15 @@ __device__ inline void load_rows(float* s, const T* __restrict__ src, const int3
 // reads as zero), and beta into sb.
 __device__ inline void load_decay(float* sG, float* sb, const float* __restrict__ g, const float* __restrict__ beta,
                                   const int32_t* ent, int H, int h, int D, int t) {
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int r = idx / D, c = idx % D;
+  for (int idx = t; idx < KB * D / 4; idx += KT) {
+    const int r = (4 * idx) / D, c = (4 * idx) % D;
     const int32_t e = ent[r];
-    sG[r * (D + 1) + c] = e >= 0 ? g[(static_cast<int64_t>(e >> 1) * H + h) * D + c] : 0.f;
+    float4 x = {0.f, 0.f, 0.f, 0.f};
+    if (e >= 0) x = *reinterpret_cast<const float4*>(g + (static_cast<int64_t>(e >> 1) * H + h) * D + c);
+    sG[r * (D + 1) + c] = x.x;
+    sG[r * (D + 1) + c + 1] = x.y;
+    sG[r * (D + 1) + c + 2] = x.z;
+    sG[r * (D + 1) + c + 3] = x.w;
   }
   if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
   __syncthreads();
@@ -747,23 +780,65 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
   }
   for (int p = t; p < KB * KB; p += KT) sTm[(p / KB) * LB + p % KB] = w[Y::LINV + p] * sb[p % KB];
   __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) {
-    const int i = p / KB, j = p % KB;
-    if (j > i) continue;
-    float a = w[Y::DUV + p];
-    for (int d = 0; d < D; ++d) a += sDW[i * LD + d] * sKG[j * LD + d];
-    w[Y::DUV + p] = a;                                       // dTm
-  }
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int j = idx / D, d = idx % D;
-    float av = 0.f, ak = 0.f;
-    for (int i = j; i < KB; ++i) {
-      const float tm = sTm[i * LB + j];
-      av += tm * sDX[i * LD + d];
-      ak += tm * sDW[i * LD + d];
+  {   // dTm = dUV + dW (K e^G)^T, 2 x 4 tiles (tiles wholly above the diagonal skipped)
+    const int i0 = (t / 16) * 2, j0 = (t % 16) * 4;
+    if (j0 <= i0 + 1) {
+      float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+      for (int d = 0; d < D; ++d) {
+        const float a0 = sDW[i0 * LD + d], a1 = sDW[(i0 + 1) * LD + d];
+        float kg[4];
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) kg[cc] = sKG[(j0 + cc) * LD + d];
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          acc[0][cc] += a0 * kg[cc];
+          acc[1][cc] += a1 * kg[cc];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          const int i = i0 + r, j = j0 + cc;
+          if (j <= i) w[Y::DUV + i * KB + j] += acc[r][cc];
+        }
     }
-    if (ent[j] >= 0) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + d] = av;
-    w[Y::DKG + idx] = ak;
+  }
+  {   // dV = Tm^T dX, d(K e^G) = Tm^T dW: 4 x TD tiles
+    constexpr int TD = D / 32;
+    const int j0 = (t / 32) * 4, v0 = (t % 32) * TD;
+    float av[4][TD], ak[4][TD];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int cc = 0; cc < TD; ++cc) av[r][cc] = ak[r][cc] = 0.f;
+    for (int i = j0; i < KB; ++i) {
+      float tm[4], dx[TD], dw[TD];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) tm[r] = j0 + r <= i ? sTm[i * LB + j0 + r] : 0.f;
+#pragma unroll
+      for (int cc = 0; cc < TD; ++cc) {
+        dx[cc] = sDX[i * LD + v0 + cc];
+        dw[cc] = sDW[i * LD + v0 + cc];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < TD; ++cc) {
+          av[r][cc] += tm[r] * dx[cc];
+          ak[r][cc] += tm[r] * dw[cc];
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = j0 + r;
+      const bool real = ent[j] >= 0;
+#pragma unroll
+      for (int cc = 0; cc < TD; ++cc) {
+        if (real) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + v0 + cc] = av[r][cc];
+        w[Y::DKG + j * D + v0 + cc] = ak[r][cc];
+      }
+    }
   }
 }
 
@@ -794,14 +869,9 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int r = idx / D, d = idx % D;
-    const int32_t e = ent[r];
-    const int64_t o = (static_cast<int64_t>(e >> 1) * H + h) * D + d;
-    sK[idx] = e >= 0 ? ld<T>(k + o) : 0.f;
-    sQ[idx] = e >= 0 ? ld<T>(q + o) : 0.f;
-    sG[idx] = e >= 0 ? g[o] : 0.f;
-  }
+  load_rows<T, D, D>(sK, k, ent, H, h, t);
+  load_rows<T, D, D>(sQ, q, ent, H, h, t);
+  load_rows<float, D, D>(sG, g, ent, H, h, t);
   if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
   for (int p = t; p < KB * KB; p += KT) {
     sL[(p / KB) * LB + p % KB] = w[Y::LINV + p];
