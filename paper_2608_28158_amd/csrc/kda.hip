@@ -573,11 +573,22 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int r = idx / D, d = idx % D;
-    const int32_t e = ent[r];
-    sQG[r * LD + d] = w[Y::QG + idx];
-    sD[r * LD + d] = (e >= 0 && (e & 1)) ? ld<T>(dO + (static_cast<int64_t>(e >> 1) * H + h) * D + d) : 0.f;
+  for (int idx = t; idx < KB * D / 4; idx += KT) {
+    const int e4 = 4 * idx;
+    *reinterpret_cast<float4*>(sQG + (e4 / D) * LD + e4 % D) = *reinterpret_cast<const float4*>(w + Y::QG + e4);
+  }
+  {
+    constexpr int N = RowVec<T>::N, VR = D / N;
+    for (int idx = t; idx < KB * VR; idx += KT) {
+      const int r = idx / VR, cc = (idx % VR) * N;
+      const int32_t e = ent[r];
+      float x[N];
+#pragma unroll
+      for (int n = 0; n < N; ++n) x[n] = 0.f;
+      if (e >= 0 && (e & 1)) RowVec<T>::get(dO + (static_cast<int64_t>(e >> 1) * H + h) * D + cc, x);
+#pragma unroll
+      for (int n = 0; n < N; ++n) sD[r * LD + cc + n] = x[n];
+    }
   }
   for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * SQL + idx % KB] = w[Y::M + idx];
   __syncthreads();
@@ -668,19 +679,43 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
     for (int cc = 0; cc < 4; ++cc) aM[r][cc] = aU[r][cc] = 0.f;
   for (int v0 = 0; v0 < D; v0 += VS) {
     __syncthreads();
-    for (int idx = t; idx < D * VS; idx += KT) {
-      const int d = idx / VS, vv = idx % VS;
-      sS[d * LV + vv] = w[Y::SC + d * D + v0 + vv];
-      sN[d * LV + vv] = w[Y::DSN + d * D + v0 + vv];
+    for (int idx = t; idx < D * VS / 4; idx += KT) {
+      const int d = (4 * idx) / VS, vv = (4 * idx) % VS;
+      const float4 a = *reinterpret_cast<const float4*>(w + Y::SC + d * D + v0 + vv);
+      const float4 n = *reinterpret_cast<const float4*>(w + Y::DSN + d * D + v0 + vv);
+      float* ps = sS + d * LV + vv;
+      float* pn = sN + d * LV + vv;
+      ps[0] = a.x; ps[1] = a.y; ps[2] = a.z; ps[3] = a.w;
+      pn[0] = n.x; pn[1] = n.y; pn[2] = n.z; pn[3] = n.w;
     }
-    for (int idx = t; idx < KB * VS; idx += KT) {
-      const int i = idx / VS, vv = idx % VS;
-      const int32_t e = ent[i];
-      const int64_t row = (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vv;
-      sO[i * LV + vv] = (e >= 0 && (e & 1)) ? ld<T>(dO + row) : 0.f;
-      sV[i * LV + vv] = e >= 0 ? ld<T>(v + row) : 0.f;
-      sDX[i * LV + vv] = w[Y::DX + i * D + v0 + vv];
-      sX[i * LV + vv] = w[Y::X + i * D + v0 + vv];
+    for (int idx = t; idx < KB * VS / 4; idx += KT) {
+      const int i = (4 * idx) / VS, vv = (4 * idx) % VS;
+      const float4 a = *reinterpret_cast<const float4*>(w + Y::DX + i * D + v0 + vv);
+      const float4 x = *reinterpret_cast<const float4*>(w + Y::X + i * D + v0 + vv);
+      float* pa = sDX + i * LV + vv;
+      float* px = sX + i * LV + vv;
+      pa[0] = a.x; pa[1] = a.y; pa[2] = a.z; pa[3] = a.w;
+      px[0] = x.x; px[1] = x.y; px[2] = x.z; px[3] = x.w;
+    }
+    {   // dO (own rows) and V slabs, 16-byte loads
+      constexpr int N = RowVec<T>::N, VR = VS / N;
+      for (int idx = t; idx < KB * VR; idx += KT) {
+        const int i = idx / VR, vv = (idx % VR) * N;
+        const int32_t e = ent[i];
+        float xo[N], xv[N];
+#pragma unroll
+        for (int n = 0; n < N; ++n) xo[n] = xv[n] = 0.f;
+        if (e >= 0) {
+          const int64_t row = (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vv;
+          RowVec<T>::get(v + row, xv);
+          if (e & 1) RowVec<T>::get(dO + row, xo);
+        }
+#pragma unroll
+        for (int n = 0; n < N; ++n) {
+          sO[i * LV + vv + n] = xo[n];
+          sV[i * LV + vv + n] = xv[n];
+        }
+      }
     }
     __syncthreads();
 #pragma unroll 2
@@ -770,13 +805,21 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
   load_decay(sKG, sb, g, beta, ent, H, h, D, t);           // sKG holds G now
+  load_rows<T, D>(sDX, k, ent, H, h, t);                  // k through the dX tile
+  __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
-    const int32_t e = ent[r];
-    const float kv = e >= 0 ? ld<T>(k + (static_cast<int64_t>(e >> 1) * H + h) * D + d) : 0.f;
-    sKG[r * LD + d] = kv * __expf(sKG[r * LD + d]);
-    sDW[r * LD + d] = w[Y::DW + idx];
-    sDX[r * LD + d] = w[Y::DX + idx];
+    sKG[r * LD + d] = sDX[r * LD + d] * __expf(sKG[r * LD + d]);
+  }
+  __syncthreads();
+  for (int idx = t; idx < KB * D / 4; idx += KT) {
+    const int e4 = 4 * idx, r = e4 / D, d = e4 % D;
+    const float4 a = *reinterpret_cast<const float4*>(w + Y::DW + e4);
+    const float4 x = *reinterpret_cast<const float4*>(w + Y::DX + e4);
+    float* pa = sDW + r * LD + d;
+    float* px = sDX + r * LD + d;
+    pa[0] = a.x; pa[1] = a.y; pa[2] = a.z; pa[3] = a.w;
+    px[0] = x.x; px[1] = x.y; px[2] = x.z; px[3] = x.w;
   }
   for (int p = t; p < KB * KB; p += KT) sTm[(p / KB) * LB + p % KB] = w[Y::LINV + p] * sb[p % KB];
   __syncthreads();
