@@ -1039,11 +1039,32 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   if (t < KB && ent[t] >= 0) pdb[(static_cast<int64_t>(c) * KB + t) * H + h] = sdb[t];
 }
 
-// Compact rows <- sum of their packed rows, in ascending packed order.
+// Compact rows <- sum of their packed rows, in ascending packed order; four
+// consecutive elements per thread when the row width allows it.
 __global__ __launch_bounds__(KT) void k_kda_reduce(const float* __restrict__ src, const int64_t* __restrict__ row_off,
                                                    const int32_t* __restrict__ row_pos, int64_t C, int64_t width,
-                                                   int64_t n_pos, void* __restrict__ dst, int to_bf16) {
+                                                   int64_t n_pos, void* __restrict__ dst, int to_bf16, int vec) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * KT + threadIdx.x;
+  if (vec) {
+    const int64_t w4 = width / 4;
+    if (idx >= C * w4) return;
+    const int64_t r = idx / w4, x = (idx % w4) * 4;
+    float4 a = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t j = row_off[r]; j < row_off[r + 1]; ++j) {
+      const int32_t p = row_pos[j];
+      if (p < 0 || p >= n_pos) continue;
+      const float4 v = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(p) * width + x);
+      a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
+    }
+    if (to_bf16) {
+      bf16* o = static_cast<bf16*>(dst) + r * width + x;
+      o[0] = static_cast<bf16>(a.x); o[1] = static_cast<bf16>(a.y);
+      o[2] = static_cast<bf16>(a.z); o[3] = static_cast<bf16>(a.w);
+    } else {
+      *reinterpret_cast<float4*>(static_cast<float*>(dst) + r * width + x) = a;
+    }
+    return;
+  }
   if (idx >= C * width) return;
   const int64_t r = idx / width, x = idx % width;
   float a = 0.f;
@@ -1278,10 +1299,13 @@ extern "C" int harts_kda_reduce(const float* src, const int64_t* row_off, const 
     set_error("harts_kda_reduce: NULL pointer");
     return HARTS_EINVAL;
   }
-  const int64_t n = C * width;
+  // four elements a thread where the width and both pointers allow 16-byte source loads
+  const bool vec = (width & 3) == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(dst) & (dtype == HARTS_BF16 ? 1 : 15)) == 0;
+  const int64_t n = vec ? C * width / 4 : C * width;
   hipLaunchKernelGGL(k_kda_reduce, dim3(static_cast<uint32_t>((n + KT - 1) / KT)), dim3(KT), 0,
                      static_cast<hipStream_t>(stream), src, row_off, row_pos, C, width, n_pos, dst,
-                     dtype == HARTS_BF16 ? 1 : 0);
+                     dtype == HARTS_BF16 ? 1 : 0, vec ? 1 : 0);
   return kda_status("k_kda_reduce");
 }
 
