@@ -36,6 +36,8 @@ def sources_of(kernel=None):
         return ("conv.hip",)
     if kernel and kernel.startswith("k_attn"):
         return ("attn.hip", "la_common.hpp")
+    if kernel and kernel.startswith("k_kda"):
+        return ("kda.hip",)
     return ("la.hip", "la_common.hpp")
 
 
@@ -54,7 +56,9 @@ def short(name):
                 "k_replay_reduce", "k_logp_lse", "k_logp_gather", "k_logp_rowsum",
                 "k_logp_grad", "k_logp_onehot", "k_conv_fwd", "k_conv_bwd",
                 "k_conv_dw_sum", "k_attn_fwd", "k_attn_dq", "k_attn_dkdv", "k_attn_delta",
-                "k_attn_gather", "k_attn_scatter"):
+                "k_attn_gather", "k_attn_scatter", "k_kda_prep", "k_kda_seq", "k_kda_out",
+                "k_kda_bwd_prep", "k_kda_bwd_prod", "k_kda_bwd_tm", "k_kda_bwd_local", "k_kda_reduce",
+                "k_kda_bank_add"):
         if key in name:
             return key
     return n.replace("void ", "")[:48]
@@ -66,7 +70,7 @@ def stats(src, out, cmd):
     lines = ["# rocprofv3 kernel statistics", "", "Command:", "", "    " + " ".join(cmd), "",
              f"Kernel source hashes: la.hip + la_common.hpp {source_sha()}, "
              f"logp.hip {source_sha('k_logp')}, conv.hip {source_sha('k_conv')}, "
-             f"attn.hip + la_common.hpp {source_sha('k_attn')}", "",
+             f"attn.hip + la_common.hpp {source_sha('k_attn')}, kda.hip {source_sha('k_kda')}", "",
              "| kernel | calls | total ms | avg us | min us | max us | share |",
              "|---|---|---|---|---|---|---|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
