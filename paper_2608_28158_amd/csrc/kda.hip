@@ -602,8 +602,8 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
       for (int cc = 0; cc < TD; ++cc) acc[r][cc] = 0.f;
     for (int i = j0; i < KB; ++i) {
       float m_[4], d_[TD];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) m_[r] = j0 + r <= i ? sM[i * SQL + j0 + r] : 0.f;
+      const float4 m4 = *reinterpret_cast<const float4*>(sM + i * SQL + j0);   // 0 above the diagonal
+      m_[0] = m4.x; m_[1] = m4.y; m_[2] = m4.z; m_[3] = m4.w;
 #pragma unroll
       for (int cc = 0; cc < TD; ++cc) d_[cc] = sD[i * LD + v0 + cc];
 #pragma unroll
@@ -627,8 +627,8 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
       for (int cc = 0; cc < TV; ++cc) acc[r][cc] = 0.f;
     for (int i = 0; i < KB; ++i) {
       float q_[4], d_[TV];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) q_[r] = sQG[i * LD + d0 + r];
+      const float4 q4 = *reinterpret_cast<const float4*>(sQG + i * LD + d0);
+      q_[0] = q4.x; q_[1] = q4.y; q_[2] = q4.z; q_[3] = q4.w;
 #pragma unroll
       for (int cc = 0; cc < TV; ++cc) d_[cc] = sD[i * LD + v0 + cc];
 #pragma unroll
@@ -651,14 +651,15 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
                                                      float scale, const T* __restrict__ v, const T* __restrict__ dO,
                                                      float* __restrict__ ws) {
   using Y = WsLay<D>;
-  constexpr int VS = 32, LV = VS + 1;
+  constexpr int VS = 32, LSD = D + 4, LSR = KB + 4;
   extern __shared__ float sm[];
-  float* sS = sm;                 // [D][33] slab of S
-  float* sN = sS + D * LV;        // [D][33] slab of dSn
-  float* sO = sN + D * LV;        // [64][33] dO
-  float* sDX = sO + KB * LV;      // [64][33] dX
-  float* sX = sDX + KB * LV;      // [64][33] X
-  float* sV = sX + KB * LV;       // [64][33] V
+  // slabs of 32 value columns, stored transposed: row = value index
+  float* sS = sm;                  // [32][D + 4]  S^T
+  float* sN = sS + VS * LSD;       // [32][D + 4]  dSn^T
+  float* sO = sN + VS * LSD;       // [32][68]     dO^T
+  float* sDX = sO + VS * LSR;      // [32][68]     dX^T
+  float* sX = sDX + VS * LSR;      // [32][68]     X^T
+  float* sV = sX + VS * LSR;       // [32][68]     V^T
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -679,28 +680,24 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
     for (int cc = 0; cc < 4; ++cc) aM[r][cc] = aU[r][cc] = 0.f;
   for (int v0 = 0; v0 < D; v0 += VS) {
     __syncthreads();
-    for (int idx = t; idx < D * VS / 4; idx += KT) {
-      const int d = (4 * idx) / VS, vv = (4 * idx) % VS;
-      const float4 a = *reinterpret_cast<const float4*>(w + Y::SC + d * D + v0 + vv);
-      const float4 n = *reinterpret_cast<const float4*>(w + Y::DSN + d * D + v0 + vv);
-      float* ps = sS + d * LV + vv;
-      float* pn = sN + d * LV + vv;
-      ps[0] = a.x; ps[1] = a.y; ps[2] = a.z; ps[3] = a.w;
-      pn[0] = n.x; pn[1] = n.y; pn[2] = n.z; pn[3] = n.w;
+    for (int idx = t; idx < D * VS / 4; idx += KT) {       // consecutive lanes: consecutive rows d
+      const int d = idx % D, vq = (idx / D) * 4;
+      const float4 a = *reinterpret_cast<const float4*>(w + Y::SC + d * D + v0 + vq);
+      const float4 n = *reinterpret_cast<const float4*>(w + Y::DSN + d * D + v0 + vq);
+      sS[(vq + 0) * LSD + d] = a.x; sS[(vq + 1) * LSD + d] = a.y; sS[(vq + 2) * LSD + d] = a.z; sS[(vq + 3) * LSD + d] = a.w;
+      sN[(vq + 0) * LSD + d] = n.x; sN[(vq + 1) * LSD + d] = n.y; sN[(vq + 2) * LSD + d] = n.z; sN[(vq + 3) * LSD + d] = n.w;
     }
     for (int idx = t; idx < KB * VS / 4; idx += KT) {
-      const int i = (4 * idx) / VS, vv = (4 * idx) % VS;
-      const float4 a = *reinterpret_cast<const float4*>(w + Y::DX + i * D + v0 + vv);
-      const float4 x = *reinterpret_cast<const float4*>(w + Y::X + i * D + v0 + vv);
-      float* pa = sDX + i * LV + vv;
-      float* px = sX + i * LV + vv;
-      pa[0] = a.x; pa[1] = a.y; pa[2] = a.z; pa[3] = a.w;
-      px[0] = x.x; px[1] = x.y; px[2] = x.z; px[3] = x.w;
+      const int i = idx % KB, vq = (idx / KB) * 4;
+      const float4 a = *reinterpret_cast<const float4*>(w + Y::DX + i * D + v0 + vq);
+      const float4 x = *reinterpret_cast<const float4*>(w + Y::X + i * D + v0 + vq);
+      sDX[(vq + 0) * LSR + i] = a.x; sDX[(vq + 1) * LSR + i] = a.y; sDX[(vq + 2) * LSR + i] = a.z; sDX[(vq + 3) * LSR + i] = a.w;
+      sX[(vq + 0) * LSR + i] = x.x; sX[(vq + 1) * LSR + i] = x.y; sX[(vq + 2) * LSR + i] = x.z; sX[(vq + 3) * LSR + i] = x.w;
     }
-    {   // dO (own rows) and V slabs, 16-byte loads
+    {   // dO (own rows) and V, 16-byte loads
       constexpr int N = RowVec<T>::N, VR = VS / N;
       for (int idx = t; idx < KB * VR; idx += KT) {
-        const int i = idx / VR, vv = (idx % VR) * N;
+        const int i = idx % KB, vv = (idx / KB) * N;
         const int32_t e = ent[i];
         float xo[N], xv[N];
 #pragma unroll
@@ -712,25 +709,24 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
         }
 #pragma unroll
         for (int n = 0; n < N; ++n) {
-          sO[i * LV + vv + n] = xo[n];
-          sV[i * LV + vv + n] = xv[n];
+          sO[(vv + n) * LSR + i] = xo[n];
+          sV[(vv + n) * LSR + i] = xv[n];
         }
       }
     }
     __syncthreads();
 #pragma unroll 2
     for (int vv = 0; vv < VS; ++vv) {
-      float o_[4], dx_[4], x_[4], s_[TD], n_[TD];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        o_[r] = sO[(i0 + r) * LV + vv];
-        dx_[r] = sDX[(i0 + r) * LV + vv];
-        x_[r] = sX[(i0 + r) * LV + vv];
-      }
+      const float4 o4 = *reinterpret_cast<const float4*>(sO + vv * LSR + i0);
+      const float4 dx4 = *reinterpret_cast<const float4*>(sDX + vv * LSR + i0);
+      const float4 x4 = *reinterpret_cast<const float4*>(sX + vv * LSR + i0);
+      const float o_[4] = {o4.x, o4.y, o4.z, o4.w}, dx_[4] = {dx4.x, dx4.y, dx4.z, dx4.w},
+                  x_[4] = {x4.x, x4.y, x4.z, x4.w};
+      float s_[TD], n_[TD];
 #pragma unroll
       for (int cc = 0; cc < TD; ++cc) {
-        s_[cc] = sS[(d0 + cc) * LV + vv];
-        n_[cc] = sN[(d0 + cc) * LV + vv];
+        s_[cc] = sS[vv * LSD + d0 + cc];
+        n_[cc] = sN[vv * LSD + d0 + cc];
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r)
@@ -740,17 +736,11 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
           aW[r][cc] += dx_[r] * s_[cc];
           aK[r][cc] += x_[r] * n_[cc];
         }
-      float po[2], pdx[2], px[4], pv[4];
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        po[r] = sO[(pi0 + r) * LV + vv];
-        pdx[r] = sDX[(pi0 + r) * LV + vv];
-      }
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        px[cc] = sX[(pj0 + cc) * LV + vv];
-        pv[cc] = sV[(pj0 + cc) * LV + vv];
-      }
+      const float po[2] = {sO[vv * LSR + pi0], sO[vv * LSR + pi0 + 1]};
+      const float pdx[2] = {sDX[vv * LSR + pi0], sDX[vv * LSR + pi0 + 1]};
+      const float4 px4 = *reinterpret_cast<const float4*>(sX + vv * LSR + pj0);
+      const float4 pv4 = *reinterpret_cast<const float4*>(sV + vv * LSR + pj0);
+      const float px[4] = {px4.x, px4.y, px4.z, px4.w}, pv[4] = {pv4.x, pv4.y, pv4.z, pv4.w};
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
@@ -760,7 +750,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
         }
     }
     if (t < D)
-      for (int vv = 0; vv < VS; ++vv) aG += sN[t * LV + vv] * sS[t * LV + vv];
+      for (int vv = 0; vv < VS; ++vv) aG += sN[vv * LSD + t] * sS[vv * LSD + t];
   }
 #pragma unroll
   for (int r = 0; r < 4; ++r)
@@ -1107,7 +1097,7 @@ constexpr size_t lds_out() { return (KB * (D + 4) + D * SQL + 2 * KB * SQL) * si
 template <int D>
 constexpr size_t lds_bprep() { return (2 * KB * (D + 4) + KB * SQL) * sizeof(float); }
 template <int D>
-constexpr size_t lds_bprod() { return (2 * D * 33 + 4 * KB * 33) * sizeof(float); }
+constexpr size_t lds_bprod() { return (2 * 32 * (D + 4) + 4 * 32 * (KB + 4)) * sizeof(float); }
 template <int D>
 constexpr size_t lds_btm() { return (3 * KB * (D + 1) + KB * (KB + 1) + 2 * KB) * sizeof(float); }
 template <int D>
