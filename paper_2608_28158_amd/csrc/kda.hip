@@ -947,9 +947,11 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     sT[i * LB + j] = x;
   }
   __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) sY[(p / KB) * LB + p % KB] = w[Y::AT + p];   // Y is done: At into its tile
+  __syncthreads();
   if (t < KB) {
     float a = 0.f;
-    for (int j = 0; j < t; ++j) a += sT[t * LB + j] * w[Y::AT + t * KB + j];
+    for (int j = 0; j < t; ++j) a += sT[t * LB + j] * sY[t * LB + j];
     sdb[t] += a;
   }
   __syncthreads();
