@@ -499,33 +499,75 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_blocksu
   f32x4 S[C::CPW * C::NT];
 #pragma unroll
   for (int i = 0; i < C::CPW * C::NT; ++i) S[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  ChunkSrc<T, D> cs;
-  Vec16 px[C::NV], py[C::NV];
-  cs.resolve(sq, c0, replay_row, g, H, h, t, t < CB ? t : -1);
-  fetch<T, D>(px, k, cs, H, h, t, ROW_REPLAY);
-  fetch<T, D>(py, v, cs, H, h, t, ROW_REPLAY);
   float Gs = 0.f;  // log-decay from the block start to the current chunk start
-  for (int c = c0; c < c_end; ++c) {
+  // One chunk: its row table and decay factors published (wave 0, lane =
+  // row, from that row's g), its tiles stored, then (after the next loads
+  // are issued by `next`) added to the state.
+  const auto sum_chunk = [&](const Vec16* px, const Vec16* py, float gv, auto&& next) {
     if (t < CB) {
-      float Gt, GLw;
-      meta_publish(meta, cs, t, Gt, GLw);
-      meta.x[t] = __expf(GLw - Gt);
+      const float x = wave_prefix_sum(gv, t);
+      meta.G[t] = x;
+      meta.x[t] = __expf(lane_value(x, CB - 1) - x);
     }
     put<T, D>(Xs, px, nullptr, t);
     put<T, D>(Ys, py, nullptr, t);
     __syncthreads();
+    next();
     const float GL = meta.G[CB - 1];
-    if (c + 1 < c_end) {
-      cs.resolve(sq, c + 1, replay_row, g, H, h, t, t < CB ? t : -1);
-      fetch<T, D>(px, k, cs, H, h, t, ROW_REPLAY);
-      fetch<T, D>(py, v, cs, H, h, t, ROW_REPLAY);
-    }
     const float dec = __expf(GL);
 #pragma unroll
     for (int i = 0; i < C::CPW * C::NT; ++i) S[i] *= dec;
     state_update<T, typename C::TD, typename C::TD, C::NT, C::CPW>(S, Xs, Ys, C::CPW * w * 16, meta.x, lane);
     Gs += GL;
     __syncthreads();
+  };
+  // A sequence's first chunk holds its replay rows (looked up one by one):
+  // it is summed on its own before the others.
+  int cf = c0;
+  if (c0 == 0 && sq.n_rep > 0) {
+    ChunkSrc<T, D> cs;
+    Vec16 px[C::NV], py[C::NV];
+    cs.resolve(sq, 0, replay_row, g, H, h, t, t < CB ? t : -1);
+    fetch<T, D>(px, k, cs, H, h, t, ROW_REPLAY);
+    fetch<T, D>(py, v, cs, H, h, t, ROW_REPLAY);
+    sum_chunk(px, py, cs.gv, [] {});
+    cf = 1;
+  }
+  // The other chunks hold own rows and padding only, whose addresses need no
+  // lookup: every load is issued unconditionally (padding reads the zero
+  // row; past the block's end its last chunk is requested again), so the
+  // count of outstanding loads is the same on every path and the wait before
+  // a chunk's tiles are stored leaves the next chunk's loads in flight.  Two
+  // chunks are in flight while one is summed.
+  if (cf < c_end) {
+    using SG = Stg<T, D, C::NTHR>;
+    const auto fetch_own = [&](Vec16* px, Vec16* py, float& gv, int c) {
+      c = min(c, c_end - 1);
+#pragma unroll
+      for (int i = 0; i < C::NV; ++i) {
+        const int idx = t + i * C::NTHR;
+        const int pos = c * CB + idx / SG::VPR, d0 = (idx % SG::VPR) * SG::VE;
+        const int64_t off = (static_cast<int64_t>(sq.own_row + pos - sq.n_rep) * H + h) * D + d0;
+        const bool in = pos < sq.n_tok;
+        px[i].u = *reinterpret_cast<const uint4*>(in ? k + off : reinterpret_cast<const T*>(kZeroRow) + d0);
+        py[i].u = *reinterpret_cast<const uint4*>(in ? v + off : reinterpret_cast<const T*>(kZeroRow) + d0);
+      }
+      const int pos = c * CB + lane;
+      gv = *(pos < sq.n_tok ? g + static_cast<int64_t>(sq.own_row + pos - sq.n_rep) * H + h
+                            : reinterpret_cast<const float*>(kZeroRow));
+    };
+    Vec16 pxa[C::NV], pya[C::NV], pxb[C::NV], pyb[C::NV];
+    float ga, gb;
+    fetch_own(pxa, pya, ga, cf);
+    fetch_own(pxb, pyb, gb, cf + 1);
+    // pairs of chunks, both halves unconditional (the same loads outstanding
+    // at the loop's back edge as at its entry); an odd last chunk after
+    int c = cf;
+    for (; c + 1 < c_end; c += 2) {
+      sum_chunk(pxa, pya, ga, [&] { fetch_own(pxa, pya, ga, c + 2); });
+      sum_chunk(pxb, pyb, gb, [&] { fetch_own(pxb, pyb, gb, c + 3); });
+    }
+    if (c < c_end) sum_chunk(pxa, pya, ga, [] {});
   }
   state_store<D, C::CPW>(dSb + bi * D * D, S, w, lane);
   if (t == 0) gam[bi] = Gs;
