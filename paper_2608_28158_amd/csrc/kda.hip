@@ -19,8 +19,10 @@
 // (k_kda_seq, reverse), then every chunk-local gradient in parallel
 // (k_kda_bwd_prod, k_kda_bwd_tm, k_kda_bwd_local) into per-packed-row buffers, reduced
 // into compact rows in a fixed order (k_kda_reduce).  Pairwise decays
-// e^{G_i - G_j} (i >= j) are evaluated exactly per channel, never as
-// products of e^{G_i} and e^{-G_j}, so no intermediate overflows.
+// e^{G_i - G_j} (i >= j) are never products of e^{G_i} and e^{-G_j}: inside a
+// 16-row block they are evaluated exactly per channel, across blocks as a
+// product of three exponentials of non-positive exponents (through the
+// blocks' first rows), so no intermediate overflows.
 //
 // Packed row entries: physical row * 2 + 1 (own row), * 2 (replay row), -1
 // (padding: g = 0, beta = 0, k = q = v = 0, no outputs, no gradients).
@@ -60,8 +62,7 @@ struct WsLay {
   // backward
   static constexpr int64_t DXO = FWD, DSO = DXO + RD, DSN = DSO + DD, DX = DSN + DD, DQG = DX + RD,
                            DW = DQG + RD, DKBM = DW + RD, DM = DKBM + RD, DUV = DM + BB, DGAM = DUV + BB,
-                           DKG = DGAM + D, P1Q = DKG + RD, P1K = P1Q + RD, P1G = P1K + RD, P2K = P1G + RD,
-                           P2G = P2K + RD, ALL = P2G + RD;
+                           DKG = DGAM + D, ALL = DKG + RD;
 };
 
 // Rows of one packed chunk and head into LDS as float32 [64][LDS] (zero for
@@ -129,74 +130,177 @@ __device__ inline void load_decay(float* sG, float* sb, const float* __restrict_
   __syncthreads();
 }
 
-// sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and, if
-// sM, sM[i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere).
-// Work item = (4 x 4 block of pairs on or below the diagonal, quarter of the
-// channels): 136 blocks x 4 quarters; the quarters of a block are adjacent
-// lanes and are summed with two lane exchanges.  Every exponent is
-// G_i - G_j <= 0 (clamped to 0 above the diagonal, where the term is masked).
+// The chunk's rows in four blocks of 16.  A pairwise decay between rows i
+// of block I and j of an earlier block J factors into three exponentials of
+// non-positive exponents, through the first rows r_I = 16 I and r_{J+1}:
+//   e^{G_i - G_j} = e^{G_i - G_{r_I}} e^{G_{r_I} - G_{r_{J+1}}} e^{G_{r_{J+1}} - G_j},
+// each at most 1 (G does not increase along the chunk), so a product that
+// underflows stands for a term below the float range anyway.  Pairs inside
+// a block take the exact e^{G_i - G_j} per channel.  The factors of the
+// blocks: Kf_J = K_J e^{G_{r_{J+1}} - G_J} (J < 3), Kd_I = K_I e^{G_I - G_{r_I}}
+// and Qd_I = Q_I e^{G_I - G_{r_I}} (I > 0), and per channel the middle factors
+// of the pairs that are not adjacent, mid(2, 0) = e^{G_32 - G_16},
+// mid(3, 0) = e^{G_48 - G_16}, mid(3, 1) = e^{G_48 - G_32}.
+constexpr int PB = 16;   // rows per block of the pairwise factorization
+
+// Middle factor index of block pair (I, J), I > J: -1 for adjacent blocks.
+__device__ inline int mid_index(int I, int J) { return I == J + 1 ? -1 : (I == 2 ? 0 : (J == 0 ? 1 : 2)); }
+
+// sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and gM (the
+// workspace) [i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere).
+// sK and sQ ([64][D + 1]) are overwritten with the block factors (Kf_0..2 in
+// sK rows 0..47 and Kd_3 in rows 48..63; Kd_1 in sQ rows 0..15, Qd_1..3 in
+// its rows 16..63; Kd_2 in sX, 16 rows of D + 1); sMid holds 3 x D middle
+// factors.  Work items: 4 x 4 tiles of pairs with the channels split over
+// adjacent lanes (summed by lane exchanges): inside the blocks 40 tiles by
+// eighths of the channels, across blocks 96 tiles by quarters.
 template <int D>
-__device__ inline void pair_sums(float* sA, float* sM, const float* sK, const float* sQ, const float* sG, int t) {
-  constexpr int LD = D + 1, DQ = D / 4, NBLK = 136, NIT = NBLK * 4;
-  for (int p = t; p < KB * KB; p += KT) {         // the upper part stays zero
-    sA[(p / KB) * (KB + 1) + p % KB] = 0.f;
-    if (sM) sM[(p / KB) * (KB + 1) + p % KB] = 0.f;
+__device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, float* sQ, const float* sG, float* sX,
+                                 float* sMid, int t) {
+  constexpr int LD = D + 1;
+  for (int p = t; p < KB * KB; p += KT) {
+    const int i = p / KB, j = p % KB;
+    sA[i * (KB + 1) + j] = 0.f;
+    if (j > i) gM[p] = 0.f;
   }
   __syncthreads();
-  for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {   // whole waves take part in the exchanges
-    const bool live = it < NIT;
-    const int b = live ? it >> 2 : 0, qd = it & 3;
-    int bi = 0;
-    while ((bi + 1) * (bi + 2) / 2 <= b) ++bi;
-    const int bj = b - bi * (bi + 1) / 2;
-    const int i0 = 4 * bi, j0 = 4 * bj;
-    float a[4][4], m[4][4];
+  // pairs inside the blocks, exact: tile (block, ti >= tj), eighth of the channels
+  {
+    constexpr int DE = D / 8, NIT = 4 * 10 * 8;
+    for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {
+      const bool live = it < NIT;
+      const int tile = live ? it >> 3 : 0, de = it & 7;
+      const int blk = tile / 10, tt = tile % 10;
+      int ti = 0;
+      while ((ti + 1) * (ti + 2) / 2 <= tt) ++ti;
+      const int tj = tt - ti * (ti + 1) / 2;
+      const int i0 = PB * blk + 4 * ti, j0 = PB * blk + 4 * tj;
+      float a[4][4], m[4][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+      for (int r = 0; r < 4; ++r)
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
-    if (live) {
-      for (int d = qd * DQ; d < (qd + 1) * DQ; ++d) {
-        float ki[4], qi[4], gi[4], kj[4], gj[4];
+        for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
+      if (live) {
+#pragma unroll 2
+        for (int d = de * DE; d < (de + 1) * DE; ++d) {
+          float ki[4], qi[4], gi[4], kj[4], gj[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          ki[r] = sK[(i0 + r) * LD + d];
-          qi[r] = sM ? sQ[(i0 + r) * LD + d] : 0.f;
-          gi[r] = sG[(i0 + r) * LD + d];
-          kj[r] = sK[(j0 + r) * LD + d];
-          gj[r] = sG[(j0 + r) * LD + d];
+          for (int r = 0; r < 4; ++r) {
+            ki[r] = sK[(i0 + r) * LD + d];
+            qi[r] = sQ[(i0 + r) * LD + d];
+            gi[r] = sG[(i0 + r) * LD + d];
+            kj[r] = sK[(j0 + r) * LD + d];
+            gj[r] = sG[(j0 + r) * LD + d];
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+              const float ke = kj[cc] * __expf(fminf(gi[r] - gj[cc], 0.f));   // masked above the diagonal
+              a[r][cc] += ki[r] * ke;
+              m[r][cc] += qi[r] * ke;
+            }
         }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+          for (int x = 1; x < 8; x <<= 1) {
+            a[r][cc] += __shfl_xor(a[r][cc], x);
+            m[r][cc] += __shfl_xor(m[r][cc], x);
+          }
+      if (live && de == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
-            const float e = __expf(fminf(gi[r] - gj[cc], 0.f));
-            const float ke = kj[cc] * e;
-            a[r][cc] += ki[r] * ke;
-            m[r][cc] += qi[r] * ke;
+            const int i = i0 + r, j = j0 + cc;
+            if (j < i) sA[i * (KB + 1) + j] = a[r][cc];
+            if (j <= i) gM[i * KB + j] = m[r][cc];
           }
       }
     }
+  }
+  __syncthreads();
+  // the block factors, in place (each element read and written by one thread)
+  for (int idx = t; idx < KB * D; idx += KT) {
+    const int r = idx / D, d = idx % D, blk = r / PB;
+    const float G = sG[r * LD + d], k = sK[r * LD + d];
+    if (blk < 3) sK[r * LD + d] = k * __expf(sG[PB * (blk + 1) * LD + d] - G);   // Kf
+    if (blk > 0) {
+      const float e = __expf(G - sG[PB * blk * LD + d]);
+      const float kd = k * e;
+      if (blk == 1) sQ[(r - PB) * LD + d] = kd;
+      else if (blk == 2) sX[(r - 2 * PB) * LD + d] = kd;
+      else sK[r * LD + d] = kd;
+      sQ[r * LD + d] *= e;                                                         // Qd
+    }
+  }
+  if (t < 3 * D) {
+    const int x = t / D, d = t % D;
+    const int ri = x == 0 ? 2 * PB : 3 * PB, rj = x == 2 ? 2 * PB : PB;
+    sMid[t] = __expf(sG[ri * LD + d] - sG[rj * LD + d]);
+  }
+  __syncthreads();
+  // pairs across blocks: tile (block pair, 4 x 4), quarter of the channels
+  {
+    constexpr int DQ = D / 4, NIT = 6 * 16 * 4;
+    for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {
+      const bool live = it < NIT;
+      const int tile = live ? it >> 2 : 0, qd = it & 3;
+      const int bp = tile / 16, tt = tile % 16;
+      const int I = bp == 0 ? 1 : (bp < 3 ? 2 : 3), J = bp - (I * (I - 1)) / 2;
+      const int i0 = 4 * (tt / 4), j0 = 4 * (tt % 4);   // within the blocks
+      const float* kd = I == 1 ? sQ : (I == 2 ? sX : sK + 3 * PB * LD);
+      const float* qd_ = sQ + PB * I * LD;
+      const float* kf = sK + PB * J * LD;
+      const int mi = mid_index(I, J);
+      float a[4][4], m[4][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+      for (int r = 0; r < 4; ++r)
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        a[r][cc] += __shfl_xor(a[r][cc], 1);
-        a[r][cc] += __shfl_xor(a[r][cc], 2);
-        if (sM) {
-          m[r][cc] += __shfl_xor(m[r][cc], 1);
-          m[r][cc] += __shfl_xor(m[r][cc], 2);
+        for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
+      if (live) {
+#pragma unroll 2
+        for (int d = qd * DQ; d < (qd + 1) * DQ; ++d) {
+          const float md = mi >= 0 ? sMid[mi * D + d] : 1.f;
+          float ki[4], qi[4], kj[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            ki[r] = kd[(i0 + r) * LD + d];
+            qi[r] = qd_[(i0 + r) * LD + d];
+            kj[r] = kf[(j0 + r) * LD + d] * md;
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+              a[r][cc] += ki[r] * kj[cc];
+              m[r][cc] += qi[r] * kj[cc];
+            }
         }
       }
-    if (live && qd == 0) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc) {
-          const int i = i0 + r, j = j0 + cc;
-          if (j < i) sA[i * (KB + 1) + j] = a[r][cc];
-          if (sM && j <= i) sM[i * (KB + 1) + j] = m[r][cc];
+          a[r][cc] += __shfl_xor(a[r][cc], 1);
+          a[r][cc] += __shfl_xor(a[r][cc], 2);
+          m[r][cc] += __shfl_xor(m[r][cc], 1);
+          m[r][cc] += __shfl_xor(m[r][cc], 2);
         }
+      if (live && qd == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const int i = PB * I + i0 + r, j = PB * J + j0 + cc;
+            sA[i * (KB + 1) + j] = a[r][cc];
+            gM[i * KB + j] = m[r][cc];
+          }
+      }
     }
   }
 }
@@ -256,6 +360,7 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   float* sA = sG + KB * LD;
   float* sL = sA + KB * (KB + 1);
   float* sb = sL + KB * (KB + 1);
+  float* sMid = sb + KB;          // [3][D]
   const int c = static_cast<int>(blockIdx.x / H) + static_cast<int>(c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -263,14 +368,8 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   load_rows<T, D>(sK, k, ent, H, h, t);
   load_rows<T, D>(sQ, q, ent, H, h, t);
   load_decay(sG, sb, g, beta, ent, H, h, D, t);
-  // At and M (M straight to the workspace through sL, then sL is reused)
-  pair_sums<D>(sA, sL, sK, sQ, sG, t);
-  __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) {
-    w[Y::M + p] = sL[(p / KB) * (KB + 1) + p % KB];
-    w[Y::AT + p] = sA[(p / KB) * (KB + 1) + p % KB];
-  }
-  // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B}
+  // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B} (before the pairwise
+  // sums overwrite K and Q with their block factors)
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
     const float G = sG[r * LD + d], GB = sG[(KB - 1) * LD + d];
@@ -278,20 +377,24 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
     w[Y::QG + idx] = sQ[r * LD + d] * __expf(G);
   }
   if (t < D) w[Y::GAM + t] = __expf(sG[(KB - 1) * LD + t]);
+  // At into sA and the workspace, M into the workspace
+  pair_sums<D>(sA, w + Y::M, sK, sQ, sG, sL, sMid, t);
   __syncthreads();
+  for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * (KB + 1) + p % KB];
   tri_inverse(sL, sQ, sA, sb, t);          // the Q tile is free now: scratch
   for (int p = t; p < KB * KB; p += KT) w[Y::LINV + p] = sL[(p / KB) * (KB + 1) + p % KB];
-  // Tm = L^{-1} Diag(beta) into sA; K -> K e^G in place
+  // Tm = L^{-1} Diag(beta) into sA; K e^G and V into the K and Q tiles
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
     sA[i * (KB + 1) + j] = j <= i ? sL[i * (KB + 1) + j] * sb[j] : 0.f;
   }
+  load_rows<T, D>(sK, k, ent, H, h, t);
+  load_rows<T, D>(sQ, v, ent, H, h, t);
+  __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
     sK[r * LD + d] *= __expf(sG[r * LD + d]);
   }
-  __syncthreads();
-  load_rows<T, D>(sQ, v, ent, H, h, t);   // V into the Q tile
   __syncthreads();
   // W = Tm (K e^G), U' = Tm V: 4 x 4 output tiles per thread
   for (int tile = t; tile < KB * D / 16; tile += KT) {
@@ -890,14 +993,15 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   using Y = WsLay<D>;
   constexpr int LB = KB + 1;
   extern __shared__ float sm[];
-  float* sK = sm;                  // [64][D] k (read by channel: no padding needed)
-  float* sQ = sK + KB * D;         // [64][D] q, later dG
+  float* sK = sm;                  // [64][D] k, later its block factors, then dG
+  float* sQ = sK + KB * D;         // [64][D] q, later block factors, then the dG_B terms
   float* sG = sQ + KB * D;         // [64][D] cumulative log-decay
   float* sL = sG + KB * D;         // [64][65] L^{-1}, later dM
   float* sT = sL + KB * LB;        // [64][65] dTm -> dLinv -> dA -> dAt
   float* sY = sT + KB * LB;        // [64][65] Y
   float* sb = sY + KB * LB;        // [64] beta
   float* sdb = sb + KB;            // [64] dbeta
+  float* sMid = sdb + KB;          // [3][D] middle factors
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -961,69 +1065,174 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     sL[i * LB + j] = w[Y::DM + p];                          // dM
   }
   __syncthreads();
-  // pairwise terms per channel d: thread (d, group) takes the rows and then
-  // the columns whose index is congruent to the group modulo KT / D (the
-  // triangle's work is then even across groups): row i's own terms (dq_i,
-  // dk_i, +dG_i), then column j's terms (dk_j, -dG_j)
+  // Pairwise terms, one tile of TRW rows x 4 channels per thread.  With
+  // e_ij = e^{G_i - G_j} per channel:
+  //   row terms     R1_i = sum_{j <= i} dM_ij e_ij k_j      (dq),
+  //                 R2_i = sum_{j < i} dAt_ij e_ij k_j      (dk),
+  //   column terms  C1_j = sum_{i >= j} e_ij (dAt_ij k_i + dM_ij q_i)   (dk),
+  // and dG_i gets k_i R2_i + q_i R1_i - k_i C1_i.  Pairs inside a 16-row block
+  // take e_ij exactly; pairs across blocks go through the block factors
+  // (Kf, Kd, Qd and the middle factors, as in the preparation), which turns
+  // them into plain products whose row (column) factor e^{G_i - G_{r_I}}
+  // (e^{G_{r_{J+1}} - G_j}) is applied once at the end.
   {
-    constexpr int NG = KT / D;
-    const int d = t % D, grp = t / D;
-    for (int i = grp; i < KB; i += NG) {
-      const float gi = sG[i * D + d], ki = sK[i * D + d], qi = sQ[i * D + d];
-      float dq_ = 0.f, dk_ = 0.f, dg_ = 0.f;
-      for (int j = 0; j <= i; ++j) {
-        const float e = __expf(gi - sG[j * D + d]);
-        const float kj = sK[j * D + d];
-        const float ta = sT[i * LB + j] * e;     // 0 on the diagonal
-        const float tm = sL[i * LB + j] * e;
-        dk_ += ta * kj;
-        dq_ += tm * kj;
-        dg_ += (ta * ki + tm * qi) * kj;
-      }
-      w[Y::P1Q + i * D + d] = dq_;
-      w[Y::P1K + i * D + d] = dk_;
-      w[Y::P1G + i * D + d] = dg_;
+    constexpr int TRW = KB * (D / 4) / KT;   // rows per thread tile
+    constexpr int NCT = D / 4;               // channel tiles
+    static_assert(TRW >= 1 && (KB / TRW) * NCT == KT && PB % TRW == 0, "one tile per thread");
+    const int i0 = (t / NCT) * TRW, d0 = (t % NCT) * 4, I = i0 / PB;
+    float kr[TRW][4], qr[TRW][4], gr[TRW][4];
+    float rd1[TRW][4], rd2[TRW][4], cd[TRW][4], z1[TRW][4], z2[TRW][4], zc[TRW][4];
+    const auto f4 = [](const float* p, float* x) {
+      const float4 u = *reinterpret_cast<const float4*>(p);
+      x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
+    };
+#pragma unroll
+    for (int r = 0; r < TRW; ++r) {
+      f4(sK + (i0 + r) * D + d0, kr[r]);
+      f4(sQ + (i0 + r) * D + d0, qr[r]);
+      f4(sG + (i0 + r) * D + d0, gr[r]);
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) rd1[r][cc] = rd2[r][cc] = cd[r][cc] = z1[r][cc] = z2[r][cc] = zc[r][cc] = 0.f;
     }
-    for (int j = grp; j < KB; j += NG) {
-      const float gj = sG[j * D + d], kj = sK[j * D + d];
-      float dk_ = 0.f, dg_ = 0.f;
-      for (int i = j; i < KB; ++i) {
-        const float e = __expf(sG[i * D + d] - gj);
-        const float x = (sT[i * LB + j] * sK[i * D + d] + sL[i * LB + j] * sQ[i * D + d]) * e;
-        dk_ += x;
-        dg_ += x * kj;
+    // inside the block, exact: rows i0.. with columns j <= i, then the own
+    // rows as columns j with rows i >= j
+    for (int j = PB * I; j < i0 + TRW; ++j) {
+      float kj[4], gj[4];
+      f4(sK + j * D + d0, kj);
+      f4(sG + j * D + d0, gj);
+#pragma unroll
+      for (int r = 0; r < TRW; ++r) {
+        const bool on = j <= i0 + r;
+        const float m = on ? sL[(i0 + r) * LB + j] : 0.f, a = on ? sT[(i0 + r) * LB + j] : 0.f;
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          const float e = __expf(fminf(gr[r][cc] - gj[cc], 0.f)) * kj[cc];
+          rd1[r][cc] += m * e;
+          rd2[r][cc] += a * e;
+        }
       }
-      w[Y::P2K + j * D + d] = dk_;
-      w[Y::P2G + j * D + d] = dg_;
     }
-  }
-  __syncthreads();
-  // elementwise terms, in parallel; dG of each element into sQ
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int i = idx / D, d = idx % D;
-    const float G = sG[idx], GB = sG[(KB - 1) * D + d], eG = __expf(G), eB = __expf(GB - G);
-    const float ki = sK[idx], qi = sQ[idx];
-    const float dqg = w[Y::DQG + idx], dkg = w[Y::DKG + idx], dkb = w[Y::DKBM + idx];
-    const float dq_ = w[Y::P1Q + idx] + dqg * eG;
-    const float dk_ = w[Y::P1K + idx] + w[Y::P2K + idx] + dkg * eG + dkb * eB;
-    sQ[idx] = w[Y::P1G + idx] - w[Y::P2G + idx] + dqg * qi * eG + dkg * ki * eG - dkb * ki * eB;
-    const int32_t e = ent[i];
-    if (e >= 0) {
-      const int64_t o = (static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d;
-      pdq[o] = dq_;
-      pdk[o] = dk_;
+    for (int ip = i0; ip < PB * (I + 1); ++ip) {
+      float ki[4], qi[4], gi[4];
+      f4(sK + ip * D + d0, ki);
+      f4(sQ + ip * D + d0, qi);
+      f4(sG + ip * D + d0, gi);
+#pragma unroll
+      for (int r = 0; r < TRW; ++r) {
+        const bool on = ip >= i0 + r;
+        const float a = on ? sT[ip * LB + i0 + r] : 0.f, m = on ? sL[ip * LB + i0 + r] : 0.f;
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) cd[r][cc] += __expf(fminf(gi[cc] - gr[r][cc], 0.f)) * (a * ki[cc] + m * qi[cc]);
+      }
+    }
+    __syncthreads();
+    // the block factors in place: Kf_0..2 and Kd_3 in sK, Kd_1 in sQ rows
+    // 0..15 (its raw rows are no longer read), Qd_1..3 in sQ, Kd_2 in sY
+    for (int idx = t; idx < KB * D; idx += KT) {
+      const int r = idx / D, d = idx % D, blk = r / PB;
+      const float G = sG[idx], k_ = sK[idx];
+      if (blk < 3) sK[idx] = k_ * __expf(sG[PB * (blk + 1) * D + d] - G);
+      if (blk > 0) {
+        const float e = __expf(G - sG[PB * blk * D + d]);
+        if (blk == 1) sQ[idx - PB * D] = k_ * e;
+        else if (blk == 2) sY[idx - 2 * PB * D] = k_ * e;
+        else sK[idx] = k_ * e;
+        sQ[idx] *= e;
+      }
+    }
+    if (t < 3 * D) {
+      const int x = t / D, d = t % D;
+      const int ri = x == 0 ? 2 * PB : 3 * PB, rj = x == 2 ? 2 * PB : PB;
+      sMid[t] = __expf(sG[ri * D + d] - sG[rj * D + d]);
+    }
+    __syncthreads();
+    // across blocks: earlier blocks J as columns of the own rows ...
+    for (int J = 0; J < I; ++J) {
+      const int mi = mid_index(I, J);
+      float md[4] = {1.f, 1.f, 1.f, 1.f};
+      if (mi >= 0) f4(sMid + mi * D + d0, md);
+      for (int j = PB * J; j < PB * (J + 1); ++j) {
+        float kf[4];
+        f4(sK + j * D + d0, kf);
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) kf[cc] *= md[cc];
+#pragma unroll
+        for (int r = 0; r < TRW; ++r) {
+          const float m = sL[(i0 + r) * LB + j], a = sT[(i0 + r) * LB + j];
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            z1[r][cc] += m * kf[cc];
+            z2[r][cc] += a * kf[cc];
+          }
+        }
+      }
+    }
+    // ... and later blocks I' as rows of the own columns
+    for (int Ip = I + 1; Ip < 4; ++Ip) {
+      const int mi = mid_index(Ip, I);
+      float md[4] = {1.f, 1.f, 1.f, 1.f};
+      if (mi >= 0) f4(sMid + mi * D + d0, md);
+      const float* kd = Ip == 1 ? sQ : (Ip == 2 ? sY : sK + 3 * PB * D);
+      const float* qd = sQ + PB * Ip * D;
+      for (int x = 0; x < PB; ++x) {
+        const int ip = PB * Ip + x;
+        float kv[4], qv[4];
+        f4(kd + x * D + d0, kv);
+        f4(qd + x * D + d0, qv);
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          kv[cc] *= md[cc];
+          qv[cc] *= md[cc];
+        }
+#pragma unroll
+        for (int r = 0; r < TRW; ++r) {
+          const float a = sT[ip * LB + i0 + r], m = sL[ip * LB + i0 + r];
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) zc[r][cc] += a * kv[cc] + m * qv[cc];
+        }
+      }
+    }
+    // row and column factors, then the elementwise terms of the own tile
+    float gb[4], gI[4] = {0.f, 0.f, 0.f, 0.f}, gJ[4] = {0.f, 0.f, 0.f, 0.f};
+    f4(sG + (KB - 1) * D + d0, gb);
+    if (I > 0) f4(sG + PB * I * D + d0, gI);
+    if (I < 3) f4(sG + PB * (I + 1) * D + d0, gJ);
+    __syncthreads();     // sK and sQ are read no more: dG and the dG_B terms go there
+#pragma unroll
+    for (int r = 0; r < TRW; ++r) {
+      const int i = i0 + r;
+      float dqg[4], dkg[4], dkb[4], dq[4], dk[4];
+      f4(w + Y::DQG + i * D + d0, dqg);
+      f4(w + Y::DKG + i * D + d0, dkg);
+      f4(w + Y::DKBM + i * D + d0, dkb);
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        const float G = gr[r][cc];
+        const float E = I > 0 ? __expf(G - gI[cc]) : 0.f, F = I < 3 ? __expf(gJ[cc] - G) : 0.f;
+        const float r1 = rd1[r][cc] + E * z1[r][cc], r2 = rd2[r][cc] + E * z2[r][cc];
+        const float c1 = cd[r][cc] + F * zc[r][cc];
+        const float eG = __expf(G), eB = __expf(gb[cc] - G), k_ = kr[r][cc], q_ = qr[r][cc];
+        dq[cc] = r1 + dqg[cc] * eG;
+        dk[cc] = r2 + c1 + dkg[cc] * eG + dkb[cc] * eB;
+        sK[i * D + d0 + cc] = k_ * (r2 - c1) + q_ * r1 + (dqg[cc] * q_ + dkg[cc] * k_) * eG - dkb[cc] * k_ * eB;
+        sQ[i * D + d0 + cc] = dkb[cc] * k_ * eB;
+      }
+      if (ent[i] >= 0) {
+        const int64_t o = (static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d0;
+        *reinterpret_cast<float4*>(pdq + o) = make_float4(dq[0], dq[1], dq[2], dq[3]);
+        *reinterpret_cast<float4*>(pdk + o) = make_float4(dk[0], dk[1], dk[2], dk[3]);
+      }
     }
   }
   __syncthreads();
   // dG_B (gamma and the KB terms) and the reverse cumulative sum of dG, per channel
   if (t < D) {
     const int d = t;
-    const float GB = sG[(KB - 1) * D + d];
-    float dGB = w[Y::DGAM + d] * __expf(GB);
-    for (int i = 0; i < KB; ++i) dGB += w[Y::DKBM + i * D + d] * sK[i * D + d] * __expf(GB - sG[i * D + d]);
+    float dGB = w[Y::DGAM + d] * __expf(sG[(KB - 1) * D + d]);
+    for (int i = 0; i < KB; ++i) dGB += sQ[i * D + d];
     float run = dGB;
     for (int i = KB - 1; i >= 0; --i) {
-      run += sQ[i * D + d];
+      run += sK[i * D + d];
       const int32_t e = ent[i];
       if (e >= 0) pdg[(static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d] = run;
     }
@@ -1091,7 +1300,7 @@ int kda_status(const char* where) {
 }
 
 template <int D>
-constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB) * sizeof(float); }
+constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB + 3 * D) * sizeof(float); }
 template <int D>
 constexpr size_t lds_seq() { return (2 * KB * (D + 4) + D * SQL + KB * SQL + D) * sizeof(float); }
 template <int D>
@@ -1103,7 +1312,7 @@ constexpr size_t lds_bprod() { return (2 * 32 * (D + 4) + 4 * 32 * (KB + 4)) * s
 template <int D>
 constexpr size_t lds_btm() { return (3 * KB * (D + 1) + KB * (KB + 1) + 2 * KB) * sizeof(float); }
 template <int D>
-constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 1) + 2 * KB) * sizeof(float); }
+constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 1) + 2 * KB + 3 * D) * sizeof(float); }
 
 struct KdaArgs {
   const int32_t* chunk_rows;
