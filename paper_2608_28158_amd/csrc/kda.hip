@@ -430,80 +430,112 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   }
 }
 
-// The state recurrence of one (sequence, head, 64 state columns), chunk by
+// The state recurrence of one (sequence, head, SV state columns), chunk by
 // chunk, forward and reverse in one template.  With Sc the running state
 // (forward: S; reverse: the adjoint dS of the chunk's end state):
 //   forward  X = U' - W S,       S  = Diag(gamma) S + KB^T X
 //   reverse  dX = dXo + KB dS,   dS = Diag(gamma) dS + dSo - W^T dX
 // i.e. Xc = P + s1 A1 Sc and Sc = Diag(gamma) Sc + P2 + s2 A2^T Xc.  The
 // running state is stored per chunk before its update (S_c, or dSn_c), and
-// Xc too.  Thread tiles: 2 x 4 of Xc (64 x 64), TR x 4 of Sc (D x 64); the
-// next chunk's A1, A2, P, P2 and gamma are loaded into registers while the
-// current one is computed.  Forward: S starts from the bank entry, the
-// states at requested chunk starts go to the bank, the end state to
-// S_final.  Reverse: dS starts from dS_final (plus the bank adjoints of
-// requests at the end), the bank adjoints of requested chunk starts are
-// added as the pass reaches them, and the initial state's adjoint goes to
-// dS0_seq.
-constexpr int SQV = 64;                  // state columns per workgroup
-constexpr int SQL = SQV + 4;             // LDS row stride of Sc and Xc (16-byte rows)
+// Xc too.  Both products run on float32 MFMA (16 x 16 x 4): Sc lives in the
+// waves' accumulators (ST tiles of 16 x 16 per wave) and is mirrored in LDS
+// for the next chunk's Xc; the next chunk's A1, A2, P, P2 and gamma are
+// loaded into registers while the current one is computed.  Forward: S
+// starts from the bank entry, the states at requested chunk starts go to
+// the bank, the end state to S_final.  Reverse: dS starts from dS_final
+// (plus the bank adjoints of requests at the end), the bank adjoints of
+// requested chunk starts are added as the pass reaches them, and the
+// initial state's adjoint goes to dS0_seq.
+constexpr int SQV = 64;                  // state columns per workgroup of the output kernels
+constexpr int SQL = SQV + 4;             // LDS row stride of Sc and Xc there (16-byte rows)
 
-template <int D, bool REV>
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+// C += A B for one 16 x 16 x 4 step: lane (k = lane / 16, i = lane % 16)
+// gives A[i][k] and B[k][i]; C's lane holds rows 4 (lane / 16) + r, column
+// lane % 16.
+__device__ inline f32x4 mfma4(float a, float b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
+
+// LDS row strides of the state pass: an operand read with its row index
+// along the lane's m (n) coordinate wants a stride of 4 (mod 64 banks), one
+// read with its row index along k a stride of 16, so that the 64 lanes of a
+// fragment read hit 64 different banks.
+template <int D, int SV>
+struct SeqLds {
+  static constexpr int LA1 = D + 4, LA2 = D + 16, LS = SV + 16, LX = SV + 16;
+  static constexpr int A1 = 0, A2 = A1 + KB * LA1, S = A2 + KB * LA2, X = S + D * LS, G = X + KB * LX, ALL = G + D;
+};
+
+template <int D, bool REV, int SV>
 __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_tab, int32_t s0,
                                                 const int32_t* __restrict__ req_tab, int H, float* __restrict__ ws,
                                                 float* __restrict__ bank, float* __restrict__ S_final,
                                                 const float* __restrict__ dbank, float* __restrict__ dS0_seq) {
   using Y = WsLay<D>;
-  constexpr int LA = D + 4, NV = D / SQV, TR = D * SQV / (KT * 4);   // TR: Sc rows per thread tile
-  constexpr int NA = KB * D / 4 / KT;                                   // float4 of one A tile per thread
+  using L = SeqLds<D, SV>;
+  constexpr int NV = D / SV, NW = KT / 64, TVN = SV / 16;
+  constexpr int XT = 4 * TVN / NW, ST = (D / 16) * TVN / NW;   // X and Sc tiles per wave
+  static_assert(XT >= 1 && ST >= 1 && TVN % XT == 0 && TVN % ST == 0, "tiles of a wave share their row block");
+  constexpr int NA = KB * D / 4 / KT;                          // float4 of one A tile per thread
   constexpr int64_t OA1 = REV ? Y::KBM : Y::W, OA2 = REV ? Y::W : Y::KBM, OP = REV ? Y::DXO : Y::UP;
   constexpr int64_t OSC = REV ? Y::DSN : Y::SC, OX = REV ? Y::DX : Y::X;
   constexpr float S1 = REV ? 1.f : -1.f, S2 = REV ? -1.f : 1.f;
   extern __shared__ float sm[];
-  float* sA1 = sm;                 // [64][D + 4]
-  float* sA2 = sA1 + KB * LA;      // [64][D + 4]
-  float* sS = sA2 + KB * LA;       // [D][68]
-  float* sX = sS + D * SQL;        // [64][68]
-  float* sg = sX + KB * SQL;       // [D]
+  float* sA1 = sm + L::A1;
+  float* sA2 = sm + L::A2;
+  float* sS = sm + L::S;
+  float* sX = sm + L::X;
+  float* sg = sm + L::G;
   const int b = blockIdx.x;
   const int slab = b % NV, h = (b / NV) % H, seq = s0 + b / (NV * H);
-  const int t = threadIdx.x, v0 = slab * SQV;
+  const int t = threadIdx.x, v0 = slab * SV, lane = t & 63, wv = t >> 6;
+  const int li = lane & 15, lk = lane >> 4;     // fragment coordinates
   const int32_t* st_ = seq_tab + 8 * seq;
   const int c_first = st_[1], nc = st_[2], init = st_[3], ro = st_[4], nr = st_[5], leaf = st_[6];
-  const int xr = (t / 16) * 2, xc = (t % 16) * 4;      // Xc tile: rows xr..xr+1, columns xc..xc+3
-  const int sr = (t / 16) * TR, sc = (t % 16) * 4;     // Sc tile: rows sr..sr+TR-1, columns sc..sc+3
+  // this wave's tiles: Xc rows 16 xti.., columns 16 (xtv + x)..; Sc rows
+  // 16 sti.., columns 16 (stv + x)..
+  const int xti = (wv * XT) / TVN, xtv = (wv * XT) % TVN, sti = (wv * ST) / TVN, stv = (wv * ST) % TVN;
   auto slab_of = [&](const float* base, int64_t entry) { return base + (entry * H + h) * Y::DD + v0; };
-  // running state
+  // running state into LDS, then into the accumulators
   if (!REV) {
     const float* src = slab_of(bank, init);
-    for (int idx = t; idx < D * SQV; idx += KT) sS[(idx / SQV) * SQL + idx % SQV] = src[(idx / SQV) * D + idx % SQV];
+    for (int idx = t; idx < D * SV; idx += KT) sS[(idx / SV) * L::LS + idx % SV] = src[(idx / SV) * D + idx % SV];
   } else {
-    for (int idx = t; idx < D * SQV; idx += KT) {
-      const int r = idx / SQV, cc = idx % SQV;
+    for (int idx = t; idx < D * SV; idx += KT) {
+      const int r = idx / SV, cc = idx % SV;
       float a = S_final ? slab_of(S_final, leaf)[r * D + cc] : 0.f;
       for (int q = 0; q < nr; ++q)
         if (req_tab[2 * (ro + q)] == nc) a += slab_of(dbank, req_tab[2 * (ro + q) + 1])[r * D + cc];
-      sS[r * SQL + cc] = a;
+      sS[r * L::LS + cc] = a;
     }
   }
-  // register prefetch of one chunk
-  float4 pA1[NA], pA2[NA], pP[2], pP2[TR], pg = {0.f, 0.f, 0.f, 0.f};
-  auto fetch = [&](int cc) {
+  __syncthreads();
+  f32x4 Sa[ST];
+#pragma unroll
+  for (int x = 0; x < ST; ++x)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Sa[x][r] = sS[(16 * sti + 4 * lk + r) * L::LS + 16 * (stv + x) + li];
+  // register prefetch of one chunk (P and P2 in the accumulator layout)
+  f32x4 pA1[NA], pA2[NA], pg = {0.f, 0.f, 0.f, 0.f};
+  float pP[XT][4], pP2[ST][4];
+  auto fetch = [&](int cc) __attribute__((always_inline)) {
     const float* w = ws + (static_cast<int64_t>(c_first + cc) * H + h) * Y::ALL;
 #pragma unroll
     for (int n = 0; n < NA; ++n) {
-      pA1[n] = *reinterpret_cast<const float4*>(w + OA1 + 4 * (t + KT * n));
-      pA2[n] = *reinterpret_cast<const float4*>(w + OA2 + 4 * (t + KT * n));
+      pA1[n] = *reinterpret_cast<const f32x4*>(w + OA1 + 4 * (t + KT * n));
+      pA2[n] = *reinterpret_cast<const f32x4*>(w + OA2 + 4 * (t + KT * n));
     }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) pP[r] = *reinterpret_cast<const float4*>(w + OP + (xr + r) * D + v0 + xc);
+    for (int x = 0; x < XT; ++x)
 #pragma unroll
-    for (int r = 0; r < TR; ++r)
-      pP2[r] = REV ? *reinterpret_cast<const float4*>(w + Y::DSO + (sr + r) * D + v0 + sc) : float4{0.f, 0.f, 0.f, 0.f};
-    if (t < D / 4) pg = *reinterpret_cast<const float4*>(w + Y::GAM + 4 * t);
+      for (int r = 0; r < 4; ++r) pP[x][r] = w[OP + (16 * xti + 4 * lk + r) * D + v0 + 16 * (xtv + x) + li];
+#pragma unroll
+    for (int x = 0; x < ST; ++x)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        pP2[x][r] = REV ? w[Y::DSO + (16 * sti + 4 * lk + r) * D + v0 + 16 * (stv + x) + li] : 0.f;
+    if (t < D / 4) pg = *reinterpret_cast<const f32x4*>(w + Y::GAM + 4 * t);
   };
   if (nc > 0) fetch(REV ? nc - 1 : 0);
-  __syncthreads();
   int rq = 0;
   for (int step = 0; step <= nc; ++step) {
     const int cc = REV ? nc - 1 - step : step;
@@ -511,7 +543,7 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
       for (; rq < nr && req_tab[2 * (ro + rq)] <= cc; ++rq) {
         if (req_tab[2 * (ro + rq)] != cc) continue;
         float* dst = bank + (static_cast<int64_t>(req_tab[2 * (ro + rq) + 1]) * H + h) * Y::DD + v0;
-        for (int idx = t; idx < D * SQV; idx += KT) dst[(idx / SQV) * D + idx % SQV] = sS[(idx / SQV) * SQL + idx % SQV];
+        for (int idx = t; idx < D * SV; idx += KT) dst[(idx / SV) * D + idx % SV] = sS[(idx / SV) * L::LS + idx % SV];
       }
     }
     if (step == nc) break;
@@ -520,84 +552,70 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
 #pragma unroll
     for (int n = 0; n < NA; ++n) {
       const int e = 4 * (t + KT * n), r = e / D, c = e % D;
-      *reinterpret_cast<float4*>(sA1 + r * LA + c) = pA1[n];
-      *reinterpret_cast<float4*>(sA2 + r * LA + c) = pA2[n];
+      *reinterpret_cast<f32x4*>(sA1 + r * L::LA1 + c) = pA1[n];
+      *reinterpret_cast<f32x4*>(sA2 + r * L::LA2 + c) = pA2[n];
     }
-    if (t < D / 4) *reinterpret_cast<float4*>(sg + 4 * t) = pg;
-    float4 cP[2], cP2[TR];
+    if (t < D / 4) *reinterpret_cast<f32x4*>(sg + 4 * t) = pg;
+    f32x4 acc[XT], sacc[ST];
 #pragma unroll
-    for (int r = 0; r < 2; ++r) cP[r] = pP[r];
+    for (int x = 0; x < XT; ++x) acc[x] = f32x4{pP[x][0], pP[x][1], pP[x][2], pP[x][3]};
 #pragma unroll
-    for (int r = 0; r < TR; ++r) cP2[r] = pP2[r];
-    for (int idx = t; idx < D * SQV / 4; idx += KT) {
-      const int r = (4 * idx) / SQV, c = (4 * idx) % SQV;
-      *reinterpret_cast<float4*>(w + OSC + r * D + v0 + c) = *reinterpret_cast<const float4*>(sS + r * SQL + c);
+    for (int x = 0; x < ST; ++x) sacc[x] = f32x4{pP2[x][0], pP2[x][1], pP2[x][2], pP2[x][3]};
+    for (int idx = t; idx < D * SV / 4; idx += KT) {
+      const int r = (4 * idx) / SV, c = (4 * idx) % SV;
+      *reinterpret_cast<float4*>(w + OSC + r * D + v0 + c) = *reinterpret_cast<const float4*>(sS + r * L::LS + c);
     }
     __syncthreads();
     const int nxt = REV ? cc - 1 : cc + 1;
     if (nxt >= 0 && nxt < nc) fetch(nxt);
     // Xc = P + s1 A1 Sc
-    {
-      float x[2][4];
+#pragma unroll 4
+    for (int s = 0; s < D / 4; ++s) {
+      const float a = S1 * sA1[(16 * xti + li) * L::LA1 + 4 * s + lk];
 #pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        x[r][0] = cP[r].x; x[r][1] = cP[r].y; x[r][2] = cP[r].z; x[r][3] = cP[r].w;
-      }
-      float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-      for (int d = 0; d < D; ++d) {
-        const float a0 = sA1[xr * LA + d], a1 = sA1[(xr + 1) * LA + d];
-        const float4 sv = *reinterpret_cast<const float4*>(sS + d * SQL + xc);
-        acc[0][0] += a0 * sv.x; acc[0][1] += a0 * sv.y; acc[0][2] += a0 * sv.z; acc[0][3] += a0 * sv.w;
-        acc[1][0] += a1 * sv.x; acc[1][1] += a1 * sv.y; acc[1][2] += a1 * sv.z; acc[1][3] += a1 * sv.w;
-      }
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const float4 o = {x[r][0] + S1 * acc[r][0], x[r][1] + S1 * acc[r][1], x[r][2] + S1 * acc[r][2],
-                          x[r][3] + S1 * acc[r][3]};
-        *reinterpret_cast<float4*>(sX + (xr + r) * SQL + xc) = o;
-        *reinterpret_cast<float4*>(w + OX + (xr + r) * D + v0 + xc) = o;
-      }
+      for (int x = 0; x < XT; ++x) acc[x] = mfma4(a, sS[(4 * s + lk) * L::LS + 16 * (xtv + x) + li], acc[x]);
     }
+#pragma unroll
+    for (int x = 0; x < XT; ++x)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * xti + 4 * lk + r, col = 16 * (xtv + x) + li;
+        sX[row * L::LX + col] = acc[x][r];
+        w[OX + row * D + v0 + col] = acc[x][r];
+      }
     __syncthreads();
     // Sc = Diag(gamma) Sc + P2 + s2 A2^T Xc
-    {
-      float acc[TR][4];
 #pragma unroll
-      for (int r = 0; r < TR; ++r) acc[r][0] = acc[r][1] = acc[r][2] = acc[r][3] = 0.f;
-      for (int i = 0; i < KB; ++i) {
-        const float4 xv = *reinterpret_cast<const float4*>(sX + i * SQL + sc);
-        float av[TR];
+    for (int x = 0; x < ST; ++x)
 #pragma unroll
-        for (int r = 0; r < TR; ++r) av[r] = sA2[i * LA + sr + r];
+      for (int r = 0; r < 4; ++r) sacc[x][r] += sg[16 * sti + 4 * lk + r] * Sa[x][r];
+#pragma unroll 4
+    for (int s = 0; s < KB / 4; ++s) {
+      const float a = S2 * sA2[(4 * s + lk) * L::LA2 + 16 * sti + li];
 #pragma unroll
-        for (int r = 0; r < TR; ++r) {
-          acc[r][0] += av[r] * xv.x; acc[r][1] += av[r] * xv.y; acc[r][2] += av[r] * xv.z; acc[r][3] += av[r] * xv.w;
+      for (int x = 0; x < ST; ++x) sacc[x] = mfma4(a, sX[(4 * s + lk) * L::LX + 16 * (stv + x) + li], sacc[x]);
+    }
+    if (REV)       // adjoints of the requested states at the start of chunk cc
+      for (int q = 0; q < nr; ++q)
+        if (req_tab[2 * (ro + q)] == cc) {
+          const float* db = slab_of(dbank, req_tab[2 * (ro + q) + 1]);
+#pragma unroll
+          for (int x = 0; x < ST; ++x)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sacc[x][r] += db[(16 * sti + 4 * lk + r) * D + 16 * (stv + x) + li];
         }
-      }
 #pragma unroll
-      for (int r = 0; r < TR; ++r) {
-        const float gm = sg[sr + r];
-        float4 cur = *reinterpret_cast<const float4*>(sS + (sr + r) * SQL + sc);
-        cur.x = gm * cur.x + cP2[r].x + S2 * acc[r][0];
-        cur.y = gm * cur.y + cP2[r].y + S2 * acc[r][1];
-        cur.z = gm * cur.z + cP2[r].z + S2 * acc[r][2];
-        cur.w = gm * cur.w + cP2[r].w + S2 * acc[r][3];
-        if (REV)       // adjoints of the requested state at the start of chunk cc
-          for (int q = 0; q < nr; ++q)
-            if (req_tab[2 * (ro + q)] == cc) {
-              const float4 db = *reinterpret_cast<const float4*>(
-                  slab_of(dbank, req_tab[2 * (ro + q) + 1]) + (sr + r) * D + sc);
-              cur.x += db.x; cur.y += db.y; cur.z += db.z; cur.w += db.w;
-            }
-        *reinterpret_cast<float4*>(sS + (sr + r) * SQL + sc) = cur;
-      }
+    for (int x = 0; x < ST; ++x) {
+      Sa[x] = sacc[x];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sS[(16 * sti + 4 * lk + r) * L::LS + 16 * (stv + x) + li] = sacc[x][r];
     }
     __syncthreads();
   }
   float* dst = REV ? dS0_seq + (static_cast<int64_t>(seq) * H + h) * Y::DD + v0
                    : (S_final ? S_final + (static_cast<int64_t>(leaf) * H + h) * Y::DD + v0 : nullptr);
   if (dst)
-    for (int idx = t; idx < D * SQV; idx += KT) dst[(idx / SQV) * D + idx % SQV] = sS[(idx / SQV) * SQL + idx % SQV];
+    for (int idx = t; idx < D * SV; idx += KT) dst[(idx / SV) * D + idx % SV] = sS[(idx / SV) * L::LS + idx % SV];
 }
 
 // Outputs of one (chunk, head, 64 state columns): O = scale (QG S + M X),
@@ -1301,8 +1319,8 @@ int kda_status(const char* where) {
 
 template <int D>
 constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB + 3 * D) * sizeof(float); }
-template <int D>
-constexpr size_t lds_seq() { return (2 * KB * (D + 4) + D * SQL + KB * SQL + D) * sizeof(float); }
+template <int D, int SV>
+constexpr size_t lds_seq() { return SeqLds<D, SV>::ALL * sizeof(float); }
 template <int D>
 constexpr size_t lds_out() { return (KB * (D + 4) + D * SQL + 2 * KB * SQL) * sizeof(float); }
 template <int D>
@@ -1324,6 +1342,15 @@ struct KdaArgs {
   float scale;
 };
 
+// The state pass is a chain over each sequence's chunks: with few
+// (sequence, head) chains, slabs of 32 state columns double the workgroups
+// (and halve each chain's work per chunk); with many, 64-column slabs read
+// each chunk's operands half as often.
+template <int D>
+bool seq_narrow(const KdaArgs& a) {
+  return static_cast<int64_t>(a.n_seq) * a.H * (D / 64) < 512;
+}
+
 template <typename T, int D>
 int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, const float* g, const float* beta,
                  float* bank, float* S_final, void* o, float* ws, hipStream_t s) {
@@ -1336,8 +1363,12 @@ int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     if (int rc = kda_status("k_kda_prep")) return rc;
   }
   if (a.n_seq > 0) {
-    hipLaunchKernelGGL((k_kda_seq<D, false>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / SQV))), dim3(KT),
-                       lds_seq<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
+    if (seq_narrow<D>(a))
+      hipLaunchKernelGGL((k_kda_seq<D, false, 32>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 32))), dim3(KT),
+                         (lds_seq<D, 32>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
+    else
+      hipLaunchKernelGGL((k_kda_seq<D, false, 64>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 64))), dim3(KT),
+                         (lds_seq<D, 64>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
     if (int rc = kda_status("k_kda_seq")) return rc;
   }
   if (a.n_chunks > 0 && o) {
@@ -1363,9 +1394,14 @@ int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     if (int rc = kda_status("k_kda_bwd_prep")) return rc;
   }
   if (a.n_seq > 0) {
-    hipLaunchKernelGGL((k_kda_seq<D, true>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / SQV))), dim3(KT),
-                       lds_seq<D>(), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, nullptr, const_cast<float*>(dS_final),
-                       dbank, dS0_seq);
+    if (seq_narrow<D>(a))
+      hipLaunchKernelGGL((k_kda_seq<D, true, 32>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 32))), dim3(KT),
+                         (lds_seq<D, 32>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, nullptr,
+                         const_cast<float*>(dS_final), dbank, dS0_seq);
+    else
+      hipLaunchKernelGGL((k_kda_seq<D, true, 64>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 64))), dim3(KT),
+                         (lds_seq<D, 64>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, nullptr,
+                         const_cast<float*>(dS_final), dbank, dS0_seq);
     if (int rc = kda_status("k_kda_seq (reverse)")) return rc;
   }
   if (a.n_chunks > 0) {
@@ -1397,8 +1433,10 @@ bool kda_set_lds() {
   if (done) return true;
   const void* fns[] = {reinterpret_cast<const void*>(&k_kda_prep<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_prep<float, D>),
-                       reinterpret_cast<const void*>(&k_kda_seq<D, false>),
-                       reinterpret_cast<const void*>(&k_kda_seq<D, true>),
+                       reinterpret_cast<const void*>(&k_kda_seq<D, false, 32>),
+                       reinterpret_cast<const void*>(&k_kda_seq<D, true, 32>),
+                       reinterpret_cast<const void*>(&k_kda_seq<D, false, 64>),
+                       reinterpret_cast<const void*>(&k_kda_seq<D, true, 64>),
                        reinterpret_cast<const void*>(&k_kda_out<bf16, D>),
                        reinterpret_cast<const void*>(&k_kda_out<float, D>),
                        reinterpret_cast<const void*>(&k_kda_bwd_prep<bf16, D>),
