@@ -766,57 +766,71 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
 
 // Products of one (chunk, head) with its states, contracted over the value
 // index: dQG = scale dO S^T, dW = -dX S^T, dKB = X dSn^T, dgamma =
-// rowsum(dSn * S), dM = scale dO X^T (j <= i), dUV = dX V^T (j <= i).
+// rowsum(dSn * S), dM = scale dO X^T (j <= i), dUV = dX V^T (j <= i).  On
+// float32 MFMA over slabs of PVS value columns staged in LDS: operands whose
+// rows run along the fragment's m coordinate (dO, dX, X) as [64][PVS + 4],
+// those whose rows run along k (S^T, dSn^T, X^T, V^T) transposed with
+// strides of 16 (mod 64 banks): every fragment read is conflict-free.  Wave
+// w owns row block w / 2 of the three 64 x D products (D / 32 column blocks
+// each) and the lower-triangle blocks of dM and dUV in that row block whose
+// column block has the parity of w.
+constexpr int PVS = 16;   // value columns per slab
+template <int D>
+struct ProdLds {
+  static constexpr int LA = PVS + 4, LS = D + 16, LJ = KB + 16;
+  static constexpr int O = 0, DX = O + KB * LA, XA = DX + KB * LA, S = XA + KB * LA, N = S + PVS * LS,
+                       XB = N + PVS * LS, V = XB + PVS * LJ, ALL = V + PVS * LJ;
+};
+
 template <typename T, int D>
-__global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
+__global__ __launch_bounds__(KT, 4) void k_kda_bwd_prod(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                      float scale, const T* __restrict__ v, const T* __restrict__ dO,
                                                      float* __restrict__ ws) {
   using Y = WsLay<D>;
-  constexpr int VS = 32, LSD = D + 4, LSR = KB + 4;
+  using L = ProdLds<D>;
+  constexpr int TDW = D / 32;
   extern __shared__ float sm[];
-  // slabs of 32 value columns, stored transposed: row = value index
-  float* sS = sm;                  // [32][D + 4]  S^T
-  float* sN = sS + VS * LSD;       // [32][D + 4]  dSn^T
-  float* sO = sN + VS * LSD;       // [32][68]     dO^T
-  float* sDX = sO + VS * LSR;      // [32][68]     dX^T
-  float* sX = sDX + VS * LSR;      // [32][68]     X^T
-  float* sV = sX + VS * LSR;       // [32][68]     V^T
+  float* sO = sm + L::O;      // dO   [64][LA]
+  float* sDX = sm + L::DX;    // dX   [64][LA]
+  float* sXa = sm + L::XA;    // X    [64][LA]
+  float* sS = sm + L::S;      // S^T  [PVS][LS]
+  float* sN = sm + L::N;      // dSn^T
+  float* sXb = sm + L::XB;    // X^T  [PVS][LJ]
+  float* sV = sm + L::V;      // V^T
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  // register tiles: 4 rows x TD columns of the three 64 x D products, 2 x 4
-  // of the two 64 x 64 ones
-  constexpr int TD = D / 32;
-  const int i0 = (t / 32) * 4, d0 = (t % 32) * TD;
-  const int pi0 = (t / 16) * 2, pj0 = (t % 16) * 4;
-  float aQ[4][TD], aW[4][TD], aK[4][TD], aM[2][4], aU[2][4], aG = 0.f;
+  const int ti = wv >> 1, td0 = (wv & 1) * TDW;
+  f32x4 aQ[TDW], aW[TDW], aK[TDW], aM[2], aU[2];
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int x = 0; x < TDW; ++x) aQ[x] = aW[x] = aK[x] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int cc = 0; cc < TD; ++cc) aQ[r][cc] = aW[r][cc] = aK[r][cc] = 0.f;
-#pragma unroll
-  for (int r = 0; r < 2; ++r)
-#pragma unroll
-    for (int cc = 0; cc < 4; ++cc) aM[r][cc] = aU[r][cc] = 0.f;
-  for (int v0 = 0; v0 < D; v0 += VS) {
+  for (int x = 0; x < 2; ++x) aM[x] = aU[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float aG = 0.f;
+  for (int v0 = 0; v0 < D; v0 += PVS) {
     __syncthreads();
-    for (int idx = t; idx < D * VS / 4; idx += KT) {       // consecutive lanes: consecutive rows d
+    for (int idx = t; idx < D * PVS / 4; idx += KT) {       // consecutive lanes: consecutive rows d
       const int d = idx % D, vq = (idx / D) * 4;
-      const float4 a = *reinterpret_cast<const float4*>(w + Y::SC + d * D + v0 + vq);
-      const float4 n = *reinterpret_cast<const float4*>(w + Y::DSN + d * D + v0 + vq);
-      sS[(vq + 0) * LSD + d] = a.x; sS[(vq + 1) * LSD + d] = a.y; sS[(vq + 2) * LSD + d] = a.z; sS[(vq + 3) * LSD + d] = a.w;
-      sN[(vq + 0) * LSD + d] = n.x; sN[(vq + 1) * LSD + d] = n.y; sN[(vq + 2) * LSD + d] = n.z; sN[(vq + 3) * LSD + d] = n.w;
+      const f32x4 a = *reinterpret_cast<const f32x4*>(w + Y::SC + d * D + v0 + vq);
+      const f32x4 n = *reinterpret_cast<const f32x4*>(w + Y::DSN + d * D + v0 + vq);
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        sS[(vq + x) * L::LS + d] = a[x];
+        sN[(vq + x) * L::LS + d] = n[x];
+      }
     }
-    for (int idx = t; idx < KB * VS / 4; idx += KT) {
+    for (int idx = t; idx < KB * PVS / 4; idx += KT) {
       const int i = idx % KB, vq = (idx / KB) * 4;
-      const float4 a = *reinterpret_cast<const float4*>(w + Y::DX + i * D + v0 + vq);
-      const float4 x = *reinterpret_cast<const float4*>(w + Y::X + i * D + v0 + vq);
-      sDX[(vq + 0) * LSR + i] = a.x; sDX[(vq + 1) * LSR + i] = a.y; sDX[(vq + 2) * LSR + i] = a.z; sDX[(vq + 3) * LSR + i] = a.w;
-      sX[(vq + 0) * LSR + i] = x.x; sX[(vq + 1) * LSR + i] = x.y; sX[(vq + 2) * LSR + i] = x.z; sX[(vq + 3) * LSR + i] = x.w;
+      const f32x4 a = *reinterpret_cast<const f32x4*>(w + Y::DX + i * D + v0 + vq);
+      const f32x4 x = *reinterpret_cast<const f32x4*>(w + Y::X + i * D + v0 + vq);
+      *reinterpret_cast<f32x4*>(sDX + i * L::LA + vq) = a;
+      *reinterpret_cast<f32x4*>(sXa + i * L::LA + vq) = x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sXb[(vq + e) * L::LJ + i] = x[e];
     }
     {   // dO (own rows) and V, 16-byte loads
-      constexpr int N = RowVec<T>::N, VR = VS / N;
+      constexpr int N = RowVec<T>::N, VR = PVS / N;
       for (int idx = t; idx < KB * VR; idx += KT) {
         const int i = idx % KB, vv = (idx / KB) * N;
         const int32_t e = ent[i];
@@ -830,66 +844,58 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prod(const int32_t* __restrict__
         }
 #pragma unroll
         for (int n = 0; n < N; ++n) {
-          sO[(vv + n) * LSR + i] = xo[n];
-          sV[(vv + n) * LSR + i] = xv[n];
+          sO[i * L::LA + vv + n] = xo[n];
+          sV[(vv + n) * L::LJ + i] = xv[n];
         }
       }
     }
     __syncthreads();
-#pragma unroll 2
-    for (int vv = 0; vv < VS; ++vv) {
-      const float4 o4 = *reinterpret_cast<const float4*>(sO + vv * LSR + i0);
-      const float4 dx4 = *reinterpret_cast<const float4*>(sDX + vv * LSR + i0);
-      const float4 x4 = *reinterpret_cast<const float4*>(sX + vv * LSR + i0);
-      const float o_[4] = {o4.x, o4.y, o4.z, o4.w}, dx_[4] = {dx4.x, dx4.y, dx4.z, dx4.w},
-                  x_[4] = {x4.x, x4.y, x4.z, x4.w};
-      float s_[TD], n_[TD];
+    if (t < D)
+#pragma unroll 4
+      for (int vv = 0; vv < PVS; ++vv) aG += sN[vv * L::LS + t] * sS[vv * L::LS + t];
 #pragma unroll
-      for (int cc = 0; cc < TD; ++cc) {
-        s_[cc] = sS[vv * LSD + d0 + cc];
-        n_[cc] = sN[vv * LSD + d0 + cc];
+    for (int s4 = 0; s4 < PVS / 4; ++s4) {
+      const int k = 4 * s4 + lk;
+      const float ao = sO[(16 * ti + li) * L::LA + k], adx = sDX[(16 * ti + li) * L::LA + k];
+      const float ax = sXa[(16 * ti + li) * L::LA + k];
+#pragma unroll
+      for (int x = 0; x < TDW; ++x) {
+        const float bs = sS[k * L::LS + 16 * (td0 + x) + li], bn = sN[k * L::LS + 16 * (td0 + x) + li];
+        aQ[x] = mfma4(ao, bs, aQ[x]);
+        aW[x] = mfma4(adx, bs, aW[x]);
+        aK[x] = mfma4(ax, bn, aK[x]);
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < TD; ++cc) {
-          aQ[r][cc] += o_[r] * s_[cc];
-          aW[r][cc] += dx_[r] * s_[cc];
-          aK[r][cc] += x_[r] * n_[cc];
+      for (int x = 0; x < 2; ++x) {
+        const int tj = (wv & 1) + 2 * x;
+        if (tj <= ti) {
+          aM[x] = mfma4(ao, sXb[k * L::LJ + 16 * tj + li], aM[x]);
+          aU[x] = mfma4(adx, sV[k * L::LJ + 16 * tj + li], aU[x]);
         }
-      const float po[2] = {sO[vv * LSR + pi0], sO[vv * LSR + pi0 + 1]};
-      const float pdx[2] = {sDX[vv * LSR + pi0], sDX[vv * LSR + pi0 + 1]};
-      const float4 px4 = *reinterpret_cast<const float4*>(sX + vv * LSR + pj0);
-      const float4 pv4 = *reinterpret_cast<const float4*>(sV + vv * LSR + pj0);
-      const float px[4] = {px4.x, px4.y, px4.z, px4.w}, pv[4] = {pv4.x, pv4.y, pv4.z, pv4.w};
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          aM[r][cc] += po[r] * px[cc];
-          aU[r][cc] += pdx[r] * pv[cc];
-        }
+      }
     }
-    if (t < D)
-      for (int vv = 0; vv < VS; ++vv) aG += sN[vv * LSD + t] * sS[vv * LSD + t];
   }
 #pragma unroll
-  for (int r = 0; r < 4; ++r)
+  for (int x = 0; x < TDW; ++x)
 #pragma unroll
-    for (int cc = 0; cc < TD; ++cc) {
-      const int idx = (i0 + r) * D + d0 + cc;
-      w[Y::DQG + idx] = scale * aQ[r][cc];
-      w[Y::DW + idx] = -aW[r][cc];
-      w[Y::DKBM + idx] = aK[r][cc];
+    for (int r = 0; r < 4; ++r) {
+      const int idx = (16 * ti + 4 * lk + r) * D + 16 * (td0 + x) + li;
+      w[Y::DQG + idx] = scale * aQ[x][r];
+      w[Y::DW + idx] = -aW[x][r];
+      w[Y::DKBM + idx] = aK[x][r];
     }
+  // dM and dUV: every tile of the row block is written (zeros above the diagonal)
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
+  for (int x = 0; x < 2; ++x) {
+    const int tj = (wv & 1) + 2 * x;
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) {
-      const int i = pi0 + r, j = pj0 + cc;
-      w[Y::DM + i * KB + j] = j <= i ? scale * aM[r][cc] : 0.f;
-      w[Y::DUV + i * KB + j] = j <= i ? aU[r][cc] : 0.f;
+    for (int r = 0; r < 4; ++r) {
+      const int i = 16 * ti + 4 * lk + r, j = 16 * tj + li;
+      const bool on = tj <= ti && j <= i;
+      w[Y::DM + i * KB + j] = on ? scale * aM[x][r] : 0.f;
+      w[Y::DUV + i * KB + j] = on ? aU[x][r] : 0.f;
     }
+  }
   if (t < D) w[Y::DGAM + t] = aG;
 }
 
@@ -1326,7 +1332,7 @@ constexpr size_t lds_out() { return (KB * (D + 4) + D * SQL + 2 * KB * SQL) * si
 template <int D>
 constexpr size_t lds_bprep() { return (2 * KB * (D + 4) + KB * SQL) * sizeof(float); }
 template <int D>
-constexpr size_t lds_bprod() { return (2 * 32 * (D + 4) + 4 * 32 * (KB + 4)) * sizeof(float); }
+constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
 constexpr size_t lds_btm() { return (3 * KB * (D + 1) + KB * (KB + 1) + 2 * KB) * sizeof(float); }
 template <int D>
