@@ -619,85 +619,87 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
 }
 
 // Outputs of one (chunk, head, 64 state columns): O = scale (QG S + M X),
-// written for own rows only; 2 x 4 output tiles per thread.
+// written for own rows only.  Float32 MFMA with the S and X slabs staged in
+// LDS (row stride 68) and the A operands (rows of QG and M) read from the
+// workspace as 16-byte pieces along k, each piece feeding four steps whose
+// k order is permuted alike on both sides (k = 16 s + 4 (lane / 16) + x);
+// the stride makes those B reads conflict-free.  Wave w owns row block
+// w / 2 and column blocks 2 (w % 2) and 2 (w % 2) + 1.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                 float scale, const float* __restrict__ ws, T* __restrict__ o) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 4, VH = 64, NV = D / VH;
+  constexpr int VH = 64, NV = D / VH, LB = VH + 4;
   extern __shared__ float sm[];
-  float* sQG = sm;                // [64][D + 4]
-  float* sS = sQG + KB * LD;      // [D][68]
-  float* sM = sS + D * SQL;       // [64][68]
-  float* sX = sM + KB * SQL;      // [64][68]
+  float* sS = sm;                 // [D][68]
+  float* sX = sS + D * LB;        // [64][68]
   const int b = blockIdx.x;
   const int half = b % NV, h = (b / NV) % H, c = static_cast<int>(b / (NV * H) + c0);
-  const int t = threadIdx.x, v0 = half * VH;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4, v0 = half * VH;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   const float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  for (int idx = t; idx < KB * D / 4; idx += KT) {
-    const int e = 4 * idx;
-    *reinterpret_cast<float4*>(sQG + (e / D) * LD + e % D) = *reinterpret_cast<const float4*>(w + Y::QG + e);
-  }
   for (int idx = t; idx < D * VH / 4; idx += KT) {
     const int e = 4 * idx, r = e / VH, cc = e % VH;
-    *reinterpret_cast<float4*>(sS + r * SQL + cc) = *reinterpret_cast<const float4*>(w + Y::SC + r * D + v0 + cc);
-  }
-  for (int idx = t; idx < KB * KB / 4; idx += KT) {
-    const int e = 4 * idx;
-    *reinterpret_cast<float4*>(sM + (e / KB) * SQL + e % KB) = *reinterpret_cast<const float4*>(w + Y::M + e);
+    *reinterpret_cast<f32x4*>(sS + r * LB + cc) = *reinterpret_cast<const f32x4*>(w + Y::SC + r * D + v0 + cc);
   }
   for (int idx = t; idx < KB * VH / 4; idx += KT) {
     const int e = 4 * idx, r = e / VH, cc = e % VH;
-    *reinterpret_cast<float4*>(sX + r * SQL + cc) = *reinterpret_cast<const float4*>(w + Y::X + r * D + v0 + cc);
+    *reinterpret_cast<f32x4*>(sX + r * LB + cc) = *reinterpret_cast<const f32x4*>(w + Y::X + r * D + v0 + cc);
   }
   __syncthreads();
-  const int i0 = (t / 16) * 2, vc = (t % 16) * 4;
-  float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-  for (int d = 0; d < D; ++d) {
-    const float a0 = sQG[i0 * LD + d], a1 = sQG[(i0 + 1) * LD + d];
-    const float4 sv = *reinterpret_cast<const float4*>(sS + d * SQL + vc);
-    acc[0][0] += a0 * sv.x; acc[0][1] += a0 * sv.y; acc[0][2] += a0 * sv.z; acc[0][3] += a0 * sv.w;
-    acc[1][0] += a1 * sv.x; acc[1][1] += a1 * sv.y; acc[1][2] += a1 * sv.z; acc[1][3] += a1 * sv.w;
+  const int ti = wv >> 1, tv0 = 2 * (wv & 1);
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const float* qg = w + Y::QG + (16 * ti + li) * D + 4 * lk;
+#pragma unroll 4
+  for (int s4 = 0; s4 < D / 16; ++s4) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(qg + 16 * s4);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int k = 16 * s4 + 4 * lk + x;
+      acc[0] = mfma4(a[x], sS[k * LB + 16 * tv0 + li], acc[0]);
+      acc[1] = mfma4(a[x], sS[k * LB + 16 * (tv0 + 1) + li], acc[1]);
+    }
   }
-  for (int j = 0; j <= i0 + 1; ++j) {
-    const float m0 = j <= i0 ? sM[i0 * SQL + j] : 0.f, m1 = sM[(i0 + 1) * SQL + j];
-    const float4 xv = *reinterpret_cast<const float4*>(sX + j * SQL + vc);
-    acc[0][0] += m0 * xv.x; acc[0][1] += m0 * xv.y; acc[0][2] += m0 * xv.z; acc[0][3] += m0 * xv.w;
-    acc[1][0] += m1 * xv.x; acc[1][1] += m1 * xv.y; acc[1][2] += m1 * xv.z; acc[1][3] += m1 * xv.w;
+  const float* mr = w + Y::M + (16 * ti + li) * KB + 4 * lk;
+  for (int s4 = 0; s4 <= ti; ++s4) {   // M is zero above the diagonal
+    const f32x4 a = *reinterpret_cast<const f32x4*>(mr + 16 * s4);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int k = 16 * s4 + 4 * lk + x;
+      acc[0] = mfma4(a[x], sX[k * LB + 16 * tv0 + li], acc[0]);
+      acc[1] = mfma4(a[x], sX[k * LB + 16 * (tv0 + 1) + li], acc[1]);
+    }
   }
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int32_t e = ent[i0 + r];
+  for (int r = 0; r < 4; ++r) {
+    const int32_t e = ent[16 * ti + 4 * lk + r];
     if (e < 0 || !(e & 1)) continue;
-    T* dst = o + (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + vc;
+    T* dst = o + (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + li;
 #pragma unroll
-    for (int cc = 0; cc < 4; ++cc) st<T>(dst + cc, scale * acc[r][cc]);
+    for (int x = 0; x < 2; ++x) st<T>(dst + 16 * (tv0 + x), scale * acc[x][r]);
   }
 }
 
 // ---------------------------------------------------------------------------
 // backward
 // ---------------------------------------------------------------------------
-// dXo = scale M^T dO (64 x D), dSo = scale QG^T dO (D x D), dO of own rows;
-// 4 x 4 and 4 x 8 output tiles per thread.
+// dXo = scale M^T dO (64 x D), dSo = scale QG^T dO (D x D), dO of own rows.
+// Float32 MFMA with dO staged in LDS ([64][D + 16], rows along k) and the A
+// operands (columns of M and QG) read from the workspace.  Wave w owns the
+// flat tiles w * TS.. of dSo and w * TX.. of dXo (each run inside one row
+// block, sharing its A operand); rows of M^T's block tj see only i >= 16 tj.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                      float scale, const T* __restrict__ dO, float* __restrict__ ws) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 4;
+  constexpr int LD = D + 16, NT = D / 16, TS = NT * NT / (KT / 64), TX = 4 * NT / (KT / 64);
+  static_assert(TS >= 1 && TX >= 1 && NT % TS == 0 && NT % TX == 0, "tiles of a wave share a row block");
   extern __shared__ float sm[];
-  float* sQG = sm;                 // [64][D + 4]
-  float* sD = sQG + KB * LD;       // [64][D + 4]
-  float* sM = sD + KB * LD;        // [64][68]
+  float* sD = sm;                  // [64][D + 16]
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  for (int idx = t; idx < KB * D / 4; idx += KT) {
-    const int e4 = 4 * idx;
-    *reinterpret_cast<float4*>(sQG + (e4 / D) * LD + e4 % D) = *reinterpret_cast<const float4*>(w + Y::QG + e4);
-  }
   {
     constexpr int N = RowVec<T>::N, VR = D / N;
     for (int idx = t; idx < KB * VR; idx += KT) {
@@ -711,56 +713,31 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
       for (int n = 0; n < N; ++n) sD[r * LD + cc + n] = x[n];
     }
   }
-  for (int idx = t; idx < KB * KB; idx += KT) sM[(idx / KB) * SQL + idx % KB] = w[Y::M + idx];
   __syncthreads();
-  {   // dXo: rows j0..j0+3, columns v0..v0+TD-1
-    constexpr int TD = D / 32;
-    const int j0 = (t / 32) * 4, v0 = (t % 32) * TD;
-    float acc[4][TD];
+  const int fs = wv * TS, td = fs / NT, tvs = fs % NT;
+  const int fx = wv * TX, tj = fx / NT, tvx = fx % NT;
+  f32x4 aS[TS], aX[TX];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+  for (int x = 0; x < TS; ++x) aS[x] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int cc = 0; cc < TD; ++cc) acc[r][cc] = 0.f;
-    for (int i = j0; i < KB; ++i) {
-      float m_[4], d_[TD];
-      const float4 m4 = *reinterpret_cast<const float4*>(sM + i * SQL + j0);   // 0 above the diagonal
-      m_[0] = m4.x; m_[1] = m4.y; m_[2] = m4.z; m_[3] = m4.w;
+  for (int x = 0; x < TX; ++x) aX[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int s4 = 0; s4 < KB / 4; ++s4) {
+    const int k = 4 * s4 + lk;
+    const float aq = w[Y::QG + k * D + 16 * td + li];
+    const float am = s4 >= 4 * tj ? w[Y::M + k * KB + 16 * tj + li] : 0.f;
 #pragma unroll
-      for (int cc = 0; cc < TD; ++cc) d_[cc] = sD[i * LD + v0 + cc];
+    for (int x = 0; x < TS; ++x) aS[x] = mfma4(aq, sD[k * LD + 16 * (tvs + x) + li], aS[x]);
+    if (s4 >= 4 * tj)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < TD; ++cc) acc[r][cc] += m_[r] * d_[cc];
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int cc = 0; cc < TD; ++cc) w[Y::DXO + (j0 + r) * D + v0 + cc] = scale * acc[r][cc];
+      for (int x = 0; x < TX; ++x) aX[x] = mfma4(am, sD[k * LD + 16 * (tvx + x) + li], aX[x]);
   }
-  {   // dSo: rows d0..d0+3, columns v0..v0+TV-1
-    constexpr int TV = D * D / (KT * 4);
-    constexpr int NCT = D / TV;               // column tiles
-    const int d0 = (t / NCT) * 4, v0 = (t % NCT) * TV;
-    float acc[4][TV];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+  for (int r = 0; r < 4; ++r) {
 #pragma unroll
-      for (int cc = 0; cc < TV; ++cc) acc[r][cc] = 0.f;
-    for (int i = 0; i < KB; ++i) {
-      float q_[4], d_[TV];
-      const float4 q4 = *reinterpret_cast<const float4*>(sQG + i * LD + d0);
-      q_[0] = q4.x; q_[1] = q4.y; q_[2] = q4.z; q_[3] = q4.w;
+    for (int x = 0; x < TS; ++x) w[Y::DSO + (16 * td + 4 * lk + r) * D + 16 * (tvs + x) + li] = scale * aS[x][r];
 #pragma unroll
-      for (int cc = 0; cc < TV; ++cc) d_[cc] = sD[i * LD + v0 + cc];
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < TV; ++cc) acc[r][cc] += q_[r] * d_[cc];
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int cc = 0; cc < TV; ++cc) w[Y::DSO + (d0 + r) * D + v0 + cc] = scale * acc[r][cc];
+    for (int x = 0; x < TX; ++x) w[Y::DXO + (16 * tj + 4 * lk + r) * D + 16 * (tvx + x) + li] = scale * aX[x][r];
   }
 }
 
@@ -1328,9 +1305,9 @@ constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB 
 template <int D, int SV>
 constexpr size_t lds_seq() { return SeqLds<D, SV>::ALL * sizeof(float); }
 template <int D>
-constexpr size_t lds_out() { return (KB * (D + 4) + D * SQL + 2 * KB * SQL) * sizeof(float); }
+constexpr size_t lds_out() { return (D + KB) * 68 * sizeof(float); }
 template <int D>
-constexpr size_t lds_bprep() { return (2 * KB * (D + 4) + KB * SQL) * sizeof(float); }
+constexpr size_t lds_bprep() { return KB * (D + 16) * sizeof(float); }
 template <int D>
 constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
