@@ -876,105 +876,85 @@ __global__ __launch_bounds__(KT, 4) void k_kda_bwd_prod(const int32_t* __restric
   if (t < D) w[Y::DGAM + t] = aG;
 }
 
-// Products with Tm = L^{-1} Diag(beta) of one (chunk, head), operands staged
-// in LDS: dTm = dUV + dW (K e^G)^T (j <= i, over dUV in the workspace),
-// dV = Tm^T dX (to pdv), d(K e^G) = Tm^T dW (to the workspace).
+// Products with Tm = L^{-1} Diag(beta) of one (chunk, head): dTm = dUV +
+// dW (K e^G)^T (j <= i, into dUV in the workspace), dV = Tm^T dX (to pdv),
+// d(K e^G) = Tm^T dW (to the workspace).  Float32 MFMA with K e^G staged in
+// LDS ([64][D + 4], read along the fragment's n coordinate: conflict-free)
+// and every other operand read from the workspace.  Wave w owns row block
+// w / 2 of dV and d(K e^G) (column blocks (D / 32)(w % 2)..) and the
+// lower-triangle blocks of dTm in row block w / 2 whose column block has the
+// parity of w.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                    const T* __restrict__ k, const float* __restrict__ g,
                                                    const float* __restrict__ beta, float* __restrict__ ws,
                                                    float* __restrict__ pdv) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 1, LB = KB + 1;
+  constexpr int LG = D + 1, LK = D + 4, TDW = D / 32;
   extern __shared__ float sm[];
-  float* sKG = sm;                 // [64][D + 1] K e^G (G first)
-  float* sDW = sKG + KB * LD;      // [64][D + 1] dW
-  float* sDX = sDW + KB * LD;      // [64][D + 1] dX
-  float* sTm = sDX + KB * LD;      // [64][65]
-  float* sb = sTm + KB * LB;       // [64]
-  float* sG = sb + KB;             // unused tail
-  (void)sG;
+  float* sG = sm;                  // [64][D + 1] cumulative log-decay
+  float* sKG = sG + KB * LG;       // [64][D + 4] K e^G
+  float* sb = sKG + KB * LK;       // [64] beta
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  load_decay(sKG, sb, g, beta, ent, H, h, D, t);           // sKG holds G now
-  load_rows<T, D>(sDX, k, ent, H, h, t);                  // k through the dX tile
+  load_decay(sG, sb, g, beta, ent, H, h, D, t);
+  load_rows<T, D, LK>(sKG, k, ent, H, h, t);
   __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
-    sKG[r * LD + d] = sDX[r * LD + d] * __expf(sKG[r * LD + d]);
+    sKG[r * LK + d] *= __expf(sG[r * LG + d]);
   }
   __syncthreads();
-  for (int idx = t; idx < KB * D / 4; idx += KT) {
-    const int e4 = 4 * idx, r = e4 / D, d = e4 % D;
-    const float4 a = *reinterpret_cast<const float4*>(w + Y::DW + e4);
-    const float4 x = *reinterpret_cast<const float4*>(w + Y::DX + e4);
-    float* pa = sDW + r * LD + d;
-    float* px = sDX + r * LD + d;
-    pa[0] = a.x; pa[1] = a.y; pa[2] = a.z; pa[3] = a.w;
-    px[0] = x.x; px[1] = x.y; px[2] = x.z; px[3] = x.w;
-  }
-  for (int p = t; p < KB * KB; p += KT) sTm[(p / KB) * LB + p % KB] = w[Y::LINV + p] * sb[p % KB];
-  __syncthreads();
-  {   // dTm = dUV + dW (K e^G)^T, 2 x 4 tiles (tiles wholly above the diagonal skipped)
-    const int i0 = (t / 16) * 2, j0 = (t % 16) * 4;
-    if (j0 <= i0 + 1) {
-      float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-      for (int d = 0; d < D; ++d) {
-        const float a0 = sDW[i0 * LD + d], a1 = sDW[(i0 + 1) * LD + d];
-        float kg[4];
+  const int wi = wv >> 1, td0 = (wv & 1) * TDW;
+  // dTm blocks (wi, tj): A = dW rows, B = (K e^G)^T
+  f32x4 aT[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const float* dwr = w + Y::DW + (16 * wi + li) * D + lk;
+#pragma unroll 4
+  for (int s4 = 0; s4 < D / 4; ++s4) {
+    const float a = dwr[4 * s4];
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc) kg[cc] = sKG[(j0 + cc) * LD + d];
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          acc[0][cc] += a0 * kg[cc];
-          acc[1][cc] += a1 * kg[cc];
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 2; ++r)
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          const int i = i0 + r, j = j0 + cc;
-          if (j <= i) w[Y::DUV + i * KB + j] += acc[r][cc];
-        }
+    for (int x = 0; x < 2; ++x) {
+      const int tj = (wv & 1) + 2 * x;
+      if (tj <= wi) aT[x] = mfma4(a, sKG[(16 * tj + li) * LK + 4 * s4 + lk], aT[x]);
     }
   }
-  {   // dV = Tm^T dX, d(K e^G) = Tm^T dW: 4 x TD tiles
-    constexpr int TD = D / 32;
-    const int j0 = (t / 32) * 4, v0 = (t % 32) * TD;
-    float av[4][TD], ak[4][TD];
+  // dV and d(K e^G) of row block wi: A = Tm^T (Tm[i][j] = L^{-1}[i][j] beta_j, zero for i < j)
+  const float bj = sb[16 * wi + li];
+  f32x4 aV[TDW], aK[TDW];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+  for (int x = 0; x < TDW; ++x) aV[x] = aK[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+  for (int s4 = 4 * wi; s4 < KB / 4; ++s4) {
+    const int i = 4 * s4 + lk;
+    const float a = w[Y::LINV + i * KB + 16 * wi + li] * bj;
 #pragma unroll
-      for (int cc = 0; cc < TD; ++cc) av[r][cc] = ak[r][cc] = 0.f;
-    for (int i = j0; i < KB; ++i) {
-      float tm[4], dx[TD], dw[TD];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) tm[r] = j0 + r <= i ? sTm[i * LB + j0 + r] : 0.f;
-#pragma unroll
-      for (int cc = 0; cc < TD; ++cc) {
-        dx[cc] = sDX[i * LD + v0 + cc];
-        dw[cc] = sDW[i * LD + v0 + cc];
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < TD; ++cc) {
-          av[r][cc] += tm[r] * dx[cc];
-          ak[r][cc] += tm[r] * dw[cc];
-        }
+    for (int x = 0; x < TDW; ++x) {
+      const int col = 16 * (td0 + x) + li;
+      aV[x] = mfma4(a, w[Y::DX + i * D + col], aV[x]);
+      aK[x] = mfma4(a, w[Y::DW + i * D + col], aK[x]);
     }
+  }
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    const int tj = (wv & 1) + 2 * x;
+    if (tj > wi) continue;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int j = j0 + r;
-      const bool real = ent[j] >= 0;
+      const int i = 16 * wi + 4 * lk + r, j = 16 * tj + li;
+      if (j <= i) w[Y::DUV + i * KB + j] += aT[x][r];
+    }
+  }
 #pragma unroll
-      for (int cc = 0; cc < TD; ++cc) {
-        if (real) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + v0 + cc] = av[r][cc];
-        w[Y::DKG + j * D + v0 + cc] = ak[r][cc];
-      }
+  for (int r = 0; r < 4; ++r) {
+    const int j = 16 * wi + 4 * lk + r;
+    const bool real = ent[j] >= 0;
+#pragma unroll
+    for (int x = 0; x < TDW; ++x) {
+      const int col = 16 * (td0 + x) + li;
+      if (real) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + col] = aV[x][r];
+      w[Y::DKG + j * D + col] = aK[x][r];
     }
   }
 }
@@ -1311,7 +1291,7 @@ constexpr size_t lds_bprep() { return KB * (D + 16) * sizeof(float); }
 template <int D>
 constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
-constexpr size_t lds_btm() { return (3 * KB * (D + 1) + KB * (KB + 1) + 2 * KB) * sizeof(float); }
+constexpr size_t lds_btm() { return (KB * (D + 1) + KB * (D + 4) + KB) * sizeof(float); }
 template <int D>
 constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 1) + 2 * KB + 3 * D) * sizeof(float); }
 
