@@ -972,7 +972,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
                                                       float* __restrict__ pdk, float* __restrict__ pdg,
                                                       float* __restrict__ pdb) {
   using Y = WsLay<D>;
-  constexpr int LB = KB + 1;
+  constexpr int LB = KB + 4;       // 64 x 64 tiles: a stride of 4 (mod 64 banks) for the MFMA fragment reads
   extern __shared__ float sm[];
   float* sK = sm;                  // [64][D] k, later its block factors, then dG
   float* sQ = sK + KB * D;         // [64][D] q, later block factors, then the dG_B terms
@@ -1013,23 +1013,44 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   __syncthreads();
   for (int p = t; p < KB * KB; p += KT) sT[(p / KB) * LB + p % KB] *= sb[p % KB];   // dLinv
   __syncthreads();
-  // Y[a][j] = sum_{b <= min(a, j)} dLinv[a][b] L^{-1}[j][b]
-  for (int p = t; p < KB * KB; p += KT) {
-    const int a = p / KB, j = p % KB, m = a < j ? a : j;
-    float y = 0.f;
-    for (int bb = 0; bb <= m; ++bb) y += sT[a * LB + bb] * sL[j * LB + bb];
-    sY[a * LB + j] = y;
+  // Y = dLinv L^{-T} (both factors lower triangular: Y[a][j] sums over
+  // b <= min(a, j)), on float32 MFMA, stored transposed (sY[j][a] = Y[a][j]).
+  // Wave w: row block w / 2, column blocks 2 (w % 2) and + 1.
+  {
+    const int lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4, ta = wv >> 1;
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      const int tj = 2 * (wv & 1) + x, ns = 4 * ((ta < tj ? ta : tj) + 1);
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int s4 = 0; s4 < ns; ++s4)
+        acc = mfma4(sT[(16 * ta + li) * LB + 4 * s4 + lk], sL[(16 * tj + li) * LB + 4 * s4 + lk], acc);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sY[(16 * tj + li) * LB + 16 * ta + 4 * lk + r] = acc[r];
+    }
   }
   __syncthreads();
-  // dA[i][j] = -sum_{a >= i} L^{-1}[a][i] Y[a][j] (i > j); dbeta_i += sum_j dA_ij At_ij; dAt = beta_i dA
-  for (int p = t; p < KB * KB; p += KT) {
-    const int i = p / KB, j = p % KB;
-    float x = 0.f;
-    if (i > j) {
-      for (int a = i; a < KB; ++a) x += sL[a * LB + i] * sY[a * LB + j];
-      x = -x;
+  // dA = -(L^{-T} Y) below the diagonal (0 elsewhere): dA[i][j] = -sum_{a >= i}
+  // L^{-1}[a][i] Y[a][j], the ten blocks on or below the diagonal; dbeta_i +=
+  // sum_j dA_ij At_ij; dAt = beta_i dA
+  {
+    const int lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
+    for (int tb = wv; tb < 10; tb += KT / 64) {
+      int ti = 0;
+      while ((ti + 1) * (ti + 2) / 2 <= tb) ++ti;
+      const int tj = tb - ti * (ti + 1) / 2;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int s4 = 4 * ti; s4 < KB / 4; ++s4)
+        acc = mfma4(sL[(4 * s4 + lk) * LB + 16 * ti + li], sY[(16 * tj + li) * LB + 4 * s4 + lk], acc);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = 16 * ti + 4 * lk + r, j = 16 * tj + li;
+        sT[i * LB + j] = i > j ? -acc[r] : 0.f;
+      }
     }
-    sT[i * LB + j] = x;
+    for (int p = t; p < KB * KB; p += KT) {        // the blocks above the diagonal
+      const int i = p / KB, j = p % KB;
+      if (j / 16 > i / 16) sT[i * LB + j] = 0.f;
+    }
   }
   __syncthreads();
   for (int p = t; p < KB * KB; p += KT) sY[(p / KB) * LB + p % KB] = w[Y::AT + p];   // Y is done: At into its tile
@@ -1293,7 +1314,7 @@ constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
 constexpr size_t lds_btm() { return (KB * (D + 1) + KB * (D + 4) + KB) * sizeof(float); }
 template <int D>
-constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 1) + 2 * KB + 3 * D) * sizeof(float); }
+constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D) * sizeof(float); }
 
 struct KdaArgs {
   const int32_t* chunk_rows;
