@@ -104,31 +104,56 @@ __device__ inline void load_rows(float* s, const T* __restrict__ src, const int3
   }
 }
 
-// Cumulative log-decays of the chunk into sG [64][D + 1] (g of padding rows
+// Cumulative sums along the 64 rows of every channel of s [64][LG], in
+// place: KT / D parts of KB / (KT / D) consecutive rows per channel, each
+// summed in registers, then offset by the totals of the parts before it
+// (sTot: KT floats).  Every thread calls it (it synchronises the workgroup).
+template <int D, int LG>
+__device__ inline void cumsum_rows(float* s, float* sTot, int t) {
+  constexpr int NP = KT / D, RP = KB / NP;
+  static_assert(NP * D == KT && NP * RP == KB, "parts of the rows");
+  const int d = t % D, part = t / D;
+  float v[RP];
+  float a = 0.f;
+#pragma unroll
+  for (int r = 0; r < RP; ++r) {
+    a += s[(part * RP + r) * LG + d];
+    v[r] = a;
+  }
+  sTot[part * D + d] = a;
+  __syncthreads();
+  float off = 0.f;
+  for (int p = 0; p < part; ++p) off += sTot[p * D + d];
+#pragma unroll
+  for (int r = 0; r < RP; ++r) s[(part * RP + r) * LG + d] = v[r] + off;
+  __syncthreads();
+}
+
+// Cumulative log-decays of the chunk into sG [64][LG] (g of padding rows
 // reads as zero), and beta into sb.
-__device__ inline void load_decay(float* sG, float* sb, const float* __restrict__ g, const float* __restrict__ beta,
-                                  const int32_t* ent, int H, int h, int D, int t) {
+template <int D, int LG>
+__device__ inline void load_decay(float* sG, float* sb, float* sTot, const float* __restrict__ g,
+                                  const float* __restrict__ beta, const int32_t* ent, int H, int h, int t) {
   for (int idx = t; idx < KB * D / 4; idx += KT) {
     const int r = (4 * idx) / D, c = (4 * idx) % D;
     const int32_t e = ent[r];
     float4 x = {0.f, 0.f, 0.f, 0.f};
     if (e >= 0) x = *reinterpret_cast<const float4*>(g + (static_cast<int64_t>(e >> 1) * H + h) * D + c);
-    sG[r * (D + 1) + c] = x.x;
-    sG[r * (D + 1) + c + 1] = x.y;
-    sG[r * (D + 1) + c + 2] = x.z;
-    sG[r * (D + 1) + c + 3] = x.w;
+    sG[r * LG + c] = x.x;
+    sG[r * LG + c + 1] = x.y;
+    sG[r * LG + c + 2] = x.z;
+    sG[r * LG + c + 3] = x.w;
   }
   if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
   __syncthreads();
-  if (t < D) {
-    float a = 0.f;
-    for (int r = 0; r < KB; ++r) {
-      a += sG[r * (D + 1) + t];
-      sG[r * (D + 1) + t] = a;
-    }
-  }
-  __syncthreads();
+  cumsum_rows<D, LG>(sG, sTot, t);
 }
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+// C += A B for one 16 x 16 x 4 step: lane (k = lane / 16, i = lane % 16)
+// gives A[i][k] and B[k][i]; C's lane holds rows 4 (lane / 16) + r, column
+// lane % 16.
+__device__ inline f32x4 mfma4(float a, float b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
 
 // The chunk's rows in four blocks of 16.  A pairwise decay between rows i
 // of block I and j of an earlier block J factors into three exponentials of
@@ -147,20 +172,20 @@ constexpr int PB = 16;   // rows per block of the pairwise factorization
 __device__ inline int mid_index(int I, int J) { return I == J + 1 ? -1 : (I == 2 ? 0 : (J == 0 ? 1 : 2)); }
 
 // sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and gM (the
-// workspace) [i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere).
-// sK and sQ ([64][D + 1]) are overwritten with the block factors (Kf_0..2 in
-// sK rows 0..47 and Kd_3 in rows 48..63; Kd_1 in sQ rows 0..15, Qd_1..3 in
-// its rows 16..63; Kd_2 in sX, 16 rows of D + 1); sMid holds 3 x D middle
-// factors.  Work items: 4 x 4 tiles of pairs with the channels split over
-// adjacent lanes (summed by lane exchanges): inside the blocks 40 tiles by
-// eighths of the channels, across blocks 96 tiles by quarters.
-template <int D>
+// workspace) [i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere);
+// sK, sQ and sG have row stride LD, sA LT.  sK and sQ are overwritten with
+// the block factors (Kf_0..2 in sK rows 0..47 and Kd_3 in rows 48..63; Kd_1
+// in sQ rows 0..15, Qd_1..3 in its rows 16..63; Kd_2 in sX, 16 rows of
+// stride LD); sMid holds 3 x D middle factors.  Pairs inside the blocks:
+// 4 x 4 tiles with the channels split in eighths over adjacent lanes (summed
+// by lane exchanges).  Pairs across blocks: one 16 x 16 block of At or M per
+// wave on float32 MFMA (k = channel).
+template <int D, int LD, int LT>
 __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, float* sQ, const float* sG, float* sX,
                                  float* sMid, int t) {
-  constexpr int LD = D + 1;
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
-    sA[i * (KB + 1) + j] = 0.f;
+    sA[i * LT + j] = 0.f;
     if (j > i) gM[p] = 0.f;
   }
   __syncthreads();
@@ -217,7 +242,7 @@ __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, f
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
             const int i = i0 + r, j = j0 + cc;
-            if (j < i) sA[i * (KB + 1) + j] = a[r][cc];
+            if (j < i) sA[i * LT + j] = a[r][cc];
             if (j <= i) gM[i * KB + j] = m[r][cc];
           }
       }
@@ -244,104 +269,90 @@ __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, f
     sMid[t] = __expf(sG[ri * LD + d] - sG[rj * LD + d]);
   }
   __syncthreads();
-  // pairs across blocks: tile (block pair, 4 x 4), quarter of the channels
+  // pairs across blocks: output o = (block pair o / 2, At or M), one per wave
   {
-    constexpr int DQ = D / 4, NIT = 6 * 16 * 4;
-    for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {
-      const bool live = it < NIT;
-      const int tile = live ? it >> 2 : 0, qd = it & 3;
-      const int bp = tile / 16, tt = tile % 16;
+    const int lane = t & 63, li = lane & 15, lk = lane >> 4;
+    for (int o = t >> 6; o < 12; o += KT / 64) {
+      const int bp = o >> 1, isM = o & 1;
       const int I = bp == 0 ? 1 : (bp < 3 ? 2 : 3), J = bp - (I * (I - 1)) / 2;
-      const int i0 = 4 * (tt / 4), j0 = 4 * (tt % 4);   // within the blocks
-      const float* kd = I == 1 ? sQ : (I == 2 ? sX : sK + 3 * PB * LD);
-      const float* qd_ = sQ + PB * I * LD;
-      const float* kf = sK + PB * J * LD;
+      const float* ar = isM ? sQ + PB * I * LD : (I == 1 ? sQ : (I == 2 ? sX : sK + 3 * PB * LD));
+      const float* br = sK + PB * J * LD;
       const int mi = mid_index(I, J);
-      float a[4][4], m[4][4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
-      if (live) {
-#pragma unroll 2
-        for (int d = qd * DQ; d < (qd + 1) * DQ; ++d) {
-          const float md = mi >= 0 ? sMid[mi * D + d] : 1.f;
-          float ki[4], qi[4], kj[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            ki[r] = kd[(i0 + r) * LD + d];
-            qi[r] = qd_[(i0 + r) * LD + d];
-            kj[r] = kf[(j0 + r) * LD + d] * md;
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-#pragma unroll
-            for (int cc = 0; cc < 4; ++cc) {
-              a[r][cc] += ki[r] * kj[cc];
-              m[r][cc] += qi[r] * kj[cc];
-            }
-        }
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+      for (int s4 = 0; s4 < D / 4; ++s4) {
+        const int k = 4 * s4 + lk;
+        const float md = mi >= 0 ? sMid[mi * D + k] : 1.f;
+        acc = mfma4(ar[li * LD + k], br[li * LD + k] * md, acc);
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          a[r][cc] += __shfl_xor(a[r][cc], 1);
-          a[r][cc] += __shfl_xor(a[r][cc], 2);
-          m[r][cc] += __shfl_xor(m[r][cc], 1);
-          m[r][cc] += __shfl_xor(m[r][cc], 2);
-        }
-      if (live && qd == 0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int cc = 0; cc < 4; ++cc) {
-            const int i = PB * I + i0 + r, j = PB * J + j0 + cc;
-            sA[i * (KB + 1) + j] = a[r][cc];
-            gM[i * KB + j] = m[r][cc];
-          }
+      for (int r = 0; r < 4; ++r) {
+        const int i = PB * I + 4 * lk + r, j = PB * J + li;
+        if (isM) gM[i * KB + j] = acc[r];
+        else sA[i * LT + j] = acc[r];
       }
     }
   }
 }
 
-// sL = (I + Diag(beta) At)^{-1}, unit lower triangular, in 16 x 16 blocks:
-// the four diagonal blocks by forward substitution (one column per thread),
-// then block row by block row, L^{-1}_{IJ} = -L^{-1}_{II} sum_{J <= K < I}
-// N_{IK} L^{-1}_{KJ} with N = Diag(beta) At.  sW is a 64 x 65 scratch tile.
+// sL = (I + Diag(beta) At)^{-1}, unit lower triangular, in 16 x 16 blocks
+// (row stride LT of sL, sW and sA): the four diagonal blocks by forward
+// substitution (one column per thread), then block row by block row on
+// float32 MFMA, one wave per block column J < I:
+//   sW_IJ = sum_{J <= K < I} N_IK L^{-1}_KJ with N = Diag(beta) At,
+//   L^{-1}_IJ = -L^{-1}_II sW_IJ.
+template <int LT>
 __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const float* sb, int t) {
-  constexpr int LD = KB + 1, BS = 16;
-  for (int p = t; p < KB * KB; p += KT) sL[(p / KB) * LD + p % KB] = (p / KB == p % KB) ? 1.f : 0.f;
+  constexpr int BS = 16;
+  for (int p = t; p < KB * KB; p += KT) sL[(p / KB) * LT + p % KB] = (p / KB == p % KB) ? 1.f : 0.f;
   __syncthreads();
   if (t < KB) {                                   // diagonal blocks
     const int c = t, r0 = (c / BS) * BS;
     for (int i = c + 1; i < r0 + BS; ++i) {
       float s = 0.f;
-      for (int j = c; j < i; ++j) s += sA[i * LD + j] * sL[j * LD + c];
-      sL[i * LD + c] = -sb[i] * s;
+      for (int j = c; j < i; ++j) s += sA[i * LT + j] * sL[j * LT + c];
+      sL[i * LT + c] = -sb[i] * s;
     }
   }
   __syncthreads();
+  const int lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   for (int I = 1; I < KB / BS; ++I) {
-    // sW[I rows][J cols] = sum_{J <= K < I} N_IK L^{-1}_KJ, for every J < I
-    for (int p = t; p < BS * I * BS; p += KT) {
-      const int i = I * BS + p / (I * BS), j = p % (I * BS);
-      const int k0 = (j / BS) * BS;
-      float s = 0.f;
-      for (int k = k0; k < I * BS; ++k) s += sA[i * LD + k] * sL[k * LD + j];
-      sW[i * LD + j] = sb[i] * s;
+    if (wv < I) {
+      const int J = wv;
+      const float bi = sb[BS * I + li];
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int s4 = 4 * J; s4 < 4 * I; ++s4) {
+        const int k = 4 * s4 + lk;
+        acc = mfma4(bi * sA[(BS * I + li) * LT + k], sL[k * LT + BS * J + li], acc);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sW[(BS * I + 4 * lk + r) * LT + BS * J + li] = acc[r];
     }
     __syncthreads();
-    // L^{-1}_{IJ} = -L^{-1}_{II} sW_{IJ}
-    for (int p = t; p < BS * I * BS; p += KT) {
-      const int i = I * BS + p / (I * BS), j = p % (I * BS);
-      float s = 0.f;
-      for (int k = I * BS; k <= i; ++k) s += sL[i * LD + k] * sW[k * LD + j];
-      sL[i * LD + j] = -s;
+    if (wv < I) {
+      const int J = wv;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s4 = 4 * I; s4 < 4 * I + 4; ++s4) {
+        const int k = 4 * s4 + lk;
+        acc = mfma4(sL[(BS * I + li) * LT + k], sW[k * LT + BS * J + li], acc);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sL[(BS * I + 4 * lk + r) * LT + BS * J + li] = -acc[r];
     }
     __syncthreads();
   }
 }
+
+// LDS of the chunk preparation (floats): K and Q (row stride LD in the
+// pairwise sums, LW for the products with Tm, whose B operands run along k),
+// G, At (then Tm) and L^{-1} (stride LT), beta, middle factors, scan totals.
+template <int D>
+struct PrepLds {
+  static constexpr int LD = D + 4, LW = D + 16, LT = KB + 4;
+  static constexpr int K = 0, Q = K + KB * LW, G = Q + KB * LW, A = G + KB * LD, L = A + KB * LT, B = L + KB * LT,
+                       MID = B + KB, TOT = MID + 3 * D, ALL = TOT + KT;
+};
 
 // ---------------------------------------------------------------------------
 // forward
@@ -352,22 +363,24 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
                                                  const T* __restrict__ v, const float* __restrict__ g,
                                                  const float* __restrict__ beta, float* __restrict__ ws) {
   using Y = WsLay<D>;
-  constexpr int LD = D + 1;
+  using P = PrepLds<D>;
+  constexpr int LD = P::LD, LW = P::LW, LT = P::LT, TDW = D / 32;
   extern __shared__ float sm[];
-  float* sK = sm;
-  float* sQ = sK + KB * LD;
-  float* sG = sQ + KB * LD;
-  float* sA = sG + KB * LD;
-  float* sL = sA + KB * (KB + 1);
-  float* sb = sL + KB * (KB + 1);
-  float* sMid = sb + KB;          // [3][D]
+  float* sK = sm + P::K;
+  float* sQ = sm + P::Q;
+  float* sG = sm + P::G;
+  float* sA = sm + P::A;
+  float* sL = sm + P::L;
+  float* sb = sm + P::B;
+  float* sMid = sm + P::MID;
+  float* sTot = sm + P::TOT;
   const int c = static_cast<int>(blockIdx.x / H) + static_cast<int>(c0), h = blockIdx.x % H;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  load_rows<T, D>(sK, k, ent, H, h, t);
-  load_rows<T, D>(sQ, q, ent, H, h, t);
-  load_decay(sG, sb, g, beta, ent, H, h, D, t);
+  load_rows<T, D, LD>(sK, k, ent, H, h, t);
+  load_rows<T, D, LD>(sQ, q, ent, H, h, t);
+  load_decay<D, LD>(sG, sb, sTot, g, beta, ent, H, h, t);
   // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B} (before the pairwise
   // sums overwrite K and Q with their block factors)
   for (int idx = t; idx < KB * D; idx += KT) {
@@ -378,56 +391,47 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   }
   if (t < D) w[Y::GAM + t] = __expf(sG[(KB - 1) * LD + t]);
   // At into sA and the workspace, M into the workspace
-  pair_sums<D>(sA, w + Y::M, sK, sQ, sG, sL, sMid, t);
+  pair_sums<D, LD, LT>(sA, w + Y::M, sK, sQ, sG, sL, sMid, t);
   __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * (KB + 1) + p % KB];
-  tri_inverse(sL, sQ, sA, sb, t);          // the Q tile is free now: scratch
-  for (int p = t; p < KB * KB; p += KT) w[Y::LINV + p] = sL[(p / KB) * (KB + 1) + p % KB];
-  // Tm = L^{-1} Diag(beta) into sA; K e^G and V into the K and Q tiles
+  for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * LT + p % KB];
+  tri_inverse<LT>(sL, sQ, sA, sb, t);          // the Q tile is free now: scratch
+  for (int p = t; p < KB * KB; p += KT) w[Y::LINV + p] = sL[(p / KB) * LT + p % KB];
+  // Tm = L^{-1} Diag(beta) into sA; K e^G and V into the K and Q tiles (stride LW)
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
-    sA[i * (KB + 1) + j] = j <= i ? sL[i * (KB + 1) + j] * sb[j] : 0.f;
+    sA[i * LT + j] = j <= i ? sL[i * LT + j] * sb[j] : 0.f;
   }
-  load_rows<T, D>(sK, k, ent, H, h, t);
-  load_rows<T, D>(sQ, v, ent, H, h, t);
+  load_rows<T, D, LW>(sK, k, ent, H, h, t);
+  load_rows<T, D, LW>(sQ, v, ent, H, h, t);
   __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
-    sK[r * LD + d] *= __expf(sG[r * LD + d]);
+    sK[r * LW + d] *= __expf(sG[r * LD + d]);
   }
   __syncthreads();
-  // W = Tm (K e^G), U' = Tm V: 4 x 4 output tiles per thread
-  for (int tile = t; tile < KB * D / 16; tile += KT) {
-    const int i0 = (tile / (D / 4)) * 4, d0 = (tile % (D / 4)) * 4;
-    float a[4][4], u[4][4];
+  // W = Tm (K e^G), U' = Tm V on float32 MFMA: wave w owns row block w / 2
+  // and column blocks (D / 32)(w % 2)..; Tm is zero above the diagonal
+  const int ti = wv >> 1, td0 = (wv & 1) * TDW;
+  f32x4 aW[TDW], aU[TDW];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+  for (int x = 0; x < TDW; ++x) aW[x] = aU[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int s4 = 0; s4 < 4 * (ti + 1); ++s4) {
+    const int kk = 4 * s4 + lk;
+    const float a = sA[(16 * ti + li) * LT + kk];
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) a[r][cc] = u[r][cc] = 0.f;
-    for (int j = 0; j <= i0 + 3; ++j) {
-      float tm[4], kg[4], vv[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        tm[r] = sA[(i0 + r) * (KB + 1) + j];        // 0 above the diagonal
-        kg[r] = sK[j * LD + d0 + r];
-        vv[r] = sQ[j * LD + d0 + r];
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          a[r][cc] += tm[r] * kg[cc];
-          u[r][cc] += tm[r] * vv[cc];
-        }
+    for (int x = 0; x < TDW; ++x) {
+      aW[x] = mfma4(a, sK[kk * LW + 16 * (td0 + x) + li], aW[x]);
+      aU[x] = mfma4(a, sQ[kk * LW + 16 * (td0 + x) + li], aU[x]);
     }
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int cc = 0; cc < 4; ++cc) {
-        w[Y::W + (i0 + r) * D + d0 + cc] = a[r][cc];
-        w[Y::UP + (i0 + r) * D + d0 + cc] = u[r][cc];
-      }
   }
+#pragma unroll
+  for (int x = 0; x < TDW; ++x)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int idx = (16 * ti + 4 * lk + r) * D + 16 * (td0 + x) + li;
+      w[Y::W + idx] = aW[x][r];
+      w[Y::UP + idx] = aU[x][r];
+    }
 }
 
 // The state recurrence of one (sequence, head, SV state columns), chunk by
@@ -448,12 +452,6 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
 // initial state's adjoint goes to dS0_seq.
 constexpr int SQV = 64;                  // state columns per workgroup of the output kernels
 constexpr int SQL = SQV + 4;             // LDS row stride of Sc and Xc there (16-byte rows)
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-// C += A B for one 16 x 16 x 4 step: lane (k = lane / 16, i = lane % 16)
-// gives A[i][k] and B[k][i]; C's lane holds rows 4 (lane / 16) + r, column
-// lane % 16.
-__device__ inline f32x4 mfma4(float a, float b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
 
 // LDS row strides of the state pass: an operand read with its row index
 // along the lane's m (n) coordinate wants a stride of 4 (mod 64 banks), one
@@ -895,11 +893,12 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
   float* sG = sm;                  // [64][D + 1] cumulative log-decay
   float* sKG = sG + KB * LG;       // [64][D + 4] K e^G
   float* sb = sKG + KB * LK;       // [64] beta
+  float* sTot = sb + KB;           // [KT] scan totals
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  load_decay(sG, sb, g, beta, ent, H, h, D, t);
+  load_decay<D, LG>(sG, sb, sTot, g, beta, ent, H, h, t);
   load_rows<T, D, LK>(sKG, k, ent, H, h, t);
   __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
@@ -983,6 +982,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   float* sb = sY + KB * LB;        // [64] beta
   float* sdb = sb + KB;            // [64] dbeta
   float* sMid = sdb + KB;          // [3][D] middle factors
+  float* sTot = sMid + 3 * D;      // [2][KT] scan totals
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -996,16 +996,10 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     sT[(p / KB) * LB + p % KB] = w[Y::DUV + p];          // dTm
   }
   __syncthreads();
-  if (t < D) {                                             // cumulative sums of g per channel
-    float a = 0.f;
-    for (int r = 0; r < KB; ++r) {
-      a += sG[r * D + t];
-      sG[r * D + t] = a;
-    }
-  }
+  cumsum_rows<D, D>(sG, sTot, t);                          // cumulative sums of g per channel
   // dbeta_j from Tm = L^{-1} Diag(beta): sum_i dTm[i][j] L^{-1}[i][j]
-  if (t >= KT - KB) {
-    const int j = t - (KT - KB);
+  if (t < KB) {
+    const int j = t;
     float a = 0.f;
     for (int i = j; i < KB; ++i) a += sT[i * LB + j] * sL[i * LB + j];
     sdb[j] = a;
@@ -1227,16 +1221,29 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     }
   }
   __syncthreads();
-  // dG_B (gamma and the KB terms) and the reverse cumulative sum of dG, per channel
-  if (t < D) {
-    const int d = t;
-    float dGB = w[Y::DGAM + d] * __expf(sG[(KB - 1) * D + d]);
-    for (int i = 0; i < KB; ++i) dGB += sQ[i * D + d];
-    float run = dGB;
-    for (int i = KB - 1; i >= 0; --i) {
-      run += sK[i * D + d];
-      const int32_t e = ent[i];
-      if (e >= 0) pdg[(static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d] = run;
+  // dG_B (gamma and the KB terms) and the reverse cumulative sum of dG, per
+  // channel: KT / D parts of consecutive rows, summed in registers, then
+  // offset by dG_B and the totals of the later parts
+  {
+    constexpr int NP = KT / D, RP = KB / NP;
+    const int d = t % D, part = t / D;
+    float suf[RP];
+    float a = 0.f, xs = 0.f;
+#pragma unroll
+    for (int r = RP - 1; r >= 0; --r) {
+      a += sK[(part * RP + r) * D + d];
+      suf[r] = a;
+      xs += sQ[(part * RP + r) * D + d];
+    }
+    sTot[part * D + d] = a;
+    sTot[KT + part * D + d] = xs;
+    __syncthreads();
+    float off = w[Y::DGAM + d] * __expf(sG[(KB - 1) * D + d]);
+    for (int p = 0; p < NP; ++p) off += sTot[KT + p * D + d] + (p > part ? sTot[p * D + d] : 0.f);
+#pragma unroll
+    for (int r = 0; r < RP; ++r) {
+      const int i = part * RP + r;
+      if (ent[i] >= 0) pdg[(static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d] = suf[r] + off;
     }
   }
   if (t < KB && ent[t] >= 0) pdb[(static_cast<int64_t>(c) * KB + t) * H + h] = sdb[t];
@@ -1302,7 +1309,7 @@ int kda_status(const char* where) {
 }
 
 template <int D>
-constexpr size_t lds_prep() { return (3 * KB * (D + 1) + 2 * KB * (KB + 1) + KB + 3 * D) * sizeof(float); }
+constexpr size_t lds_prep() { return PrepLds<D>::ALL * sizeof(float); }
 template <int D, int SV>
 constexpr size_t lds_seq() { return SeqLds<D, SV>::ALL * sizeof(float); }
 template <int D>
@@ -1312,9 +1319,9 @@ constexpr size_t lds_bprep() { return KB * (D + 16) * sizeof(float); }
 template <int D>
 constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
-constexpr size_t lds_btm() { return (KB * (D + 1) + KB * (D + 4) + KB) * sizeof(float); }
+constexpr size_t lds_btm() { return (KB * (D + 1) + KB * (D + 4) + KB + KT) * sizeof(float); }
 template <int D>
-constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D) * sizeof(float); }
+constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D + 2 * KT) * sizeof(float); }
 
 struct KdaArgs {
   const int32_t* chunk_rows;
