@@ -177,8 +177,8 @@ __device__ inline int mid_index(int I, int J) { return I == J + 1 ? -1 : (I == 2
 // the block factors (Kf_0..2 in sK rows 0..47 and Kd_3 in rows 48..63; Kd_1
 // in sQ rows 0..15, Qd_1..3 in its rows 16..63; Kd_2 in sX, 16 rows of
 // stride LD); sMid holds 3 x D middle factors.  Pairs inside the blocks:
-// 4 x 4 tiles with the channels split in eighths over adjacent lanes (summed
-// by lane exchanges).  Pairs across blocks: one 16 x 16 block of At or M per
+// 4 x 4 tiles with the channels dealt over 16 adjacent lanes (summed by lane
+// exchanges).  Pairs across blocks: one 16 x 16 block of At or M per
 // wave on float32 MFMA (k = channel).
 template <int D, int LD, int LT>
 __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, float* sQ, const float* sG, float* sX,
@@ -189,12 +189,15 @@ __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, f
     if (j > i) gM[p] = 0.f;
   }
   __syncthreads();
-  // pairs inside the blocks, exact: tile (block, ti >= tj), eighth of the channels
+  // pairs inside the blocks, exact: tile (block, ti >= tj), channels
+  // de, de + 16, .. (adjacent lanes read adjacent channels: with the row
+  // stride of 4 (mod 64 banks) the four row tiles of a wave fall in
+  // different banks)
   {
-    constexpr int DE = D / 8, NIT = 4 * 10 * 8;
+    constexpr int NE = 16, DE = D / NE, NIT = 4 * 10 * NE;
     for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {
       const bool live = it < NIT;
-      const int tile = live ? it >> 3 : 0, de = it & 7;
+      const int tile = live ? it / NE : 0, de = it % NE;
       const int blk = tile / 10, tt = tile % 10;
       int ti = 0;
       while ((ti + 1) * (ti + 2) / 2 <= tt) ++ti;
@@ -207,7 +210,8 @@ __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, f
         for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
       if (live) {
 #pragma unroll 2
-        for (int d = de * DE; d < (de + 1) * DE; ++d) {
+        for (int dd = 0; dd < DE; ++dd) {
+          const int d = dd * NE + de;
           float ki[4], qi[4], gi[4], kj[4], gj[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -232,7 +236,7 @@ __device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, f
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc)
 #pragma unroll
-          for (int x = 1; x < 8; x <<= 1) {
+          for (int x = 1; x < NE; x <<= 1) {
             a[r][cc] += __shfl_xor(a[r][cc], x);
             m[r][cc] += __shfl_xor(m[r][cc], x);
           }
