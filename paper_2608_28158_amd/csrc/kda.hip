@@ -468,7 +468,7 @@ struct SeqLds {
 };
 
 template <int D, bool REV, int SV>
-__global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_tab, int32_t s0,
+__global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_tab, int32_t s0, int n_chain,
                                                 const int32_t* __restrict__ req_tab, int H, float* __restrict__ ws,
                                                 float* __restrict__ bank, float* __restrict__ S_final,
                                                 const float* __restrict__ dbank, float* __restrict__ dS0_seq) {
@@ -487,8 +487,13 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
   float* sS = sm + L::S;
   float* sX = sm + L::X;
   float* sg = sm + L::G;
+  // Workgroup ids are dealt to the 8 XCDs in turn: the slabs of one chain
+  // (sequence, head) take ids 8 apart, so that they share one L2 for the
+  // chunk operands they all read.  Ids past the last chain exit.
   const int b = blockIdx.x;
-  const int slab = b % NV, h = (b / NV) % H, seq = s0 + b / (NV * H);
+  const int chain = (b / (8 * NV)) * 8 + b % 8, slab = (b / 8) % NV;
+  if (chain >= n_chain) return;
+  const int h = chain % H, seq = s0 + chain / H;
   const int t = threadIdx.x, v0 = slab * SV, lane = t & 63, wv = t >> 6;
   const int li = lane & 15, lk = lane >> 4;     // fragment coordinates
   const int32_t* st_ = seq_tab + 8 * seq;
@@ -1345,6 +1350,9 @@ template <int D>
 bool seq_narrow(const KdaArgs& a) {
   return static_cast<int64_t>(a.n_seq) * a.H * (D / 64) < 512;
 }
+// Workgroups of the state pass: the chains rounded up to a multiple of 8,
+// times the slabs (see the id mapping in k_kda_seq).
+inline uint32_t seq_grid(int n_chain, int n_slab) { return static_cast<uint32_t>((n_chain + 7) / 8 * 8 * n_slab); }
 
 template <typename T, int D>
 int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, const float* g, const float* beta,
@@ -1358,12 +1366,13 @@ int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     if (int rc = kda_status("k_kda_prep")) return rc;
   }
   if (a.n_seq > 0) {
+    const int n_chain = a.n_seq * a.H;
     if (seq_narrow<D>(a))
-      hipLaunchKernelGGL((k_kda_seq<D, false, 32>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 32))), dim3(KT),
-                         (lds_seq<D, 32>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
+      hipLaunchKernelGGL((k_kda_seq<D, false, 32>), dim3(seq_grid(n_chain, D / 32)), dim3(KT), (lds_seq<D, 32>()), s,
+                         a.seq_tab, a.s0, n_chain, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
     else
-      hipLaunchKernelGGL((k_kda_seq<D, false, 64>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 64))), dim3(KT),
-                         (lds_seq<D, 64>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
+      hipLaunchKernelGGL((k_kda_seq<D, false, 64>), dim3(seq_grid(n_chain, D / 64)), dim3(KT), (lds_seq<D, 64>()), s,
+                         a.seq_tab, a.s0, n_chain, a.req_tab, a.H, ws, bank, S_final, nullptr, nullptr);
     if (int rc = kda_status("k_kda_seq")) return rc;
   }
   if (a.n_chunks > 0 && o) {
@@ -1389,14 +1398,15 @@ int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
     if (int rc = kda_status("k_kda_bwd_prep")) return rc;
   }
   if (a.n_seq > 0) {
+    const int n_chain = a.n_seq * a.H;
     if (seq_narrow<D>(a))
-      hipLaunchKernelGGL((k_kda_seq<D, true, 32>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 32))), dim3(KT),
-                         (lds_seq<D, 32>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, nullptr,
-                         const_cast<float*>(dS_final), dbank, dS0_seq);
+      hipLaunchKernelGGL((k_kda_seq<D, true, 32>), dim3(seq_grid(n_chain, D / 32)), dim3(KT), (lds_seq<D, 32>()), s,
+                         a.seq_tab, a.s0, n_chain, a.req_tab, a.H, ws, nullptr, const_cast<float*>(dS_final), dbank,
+                         dS0_seq);
     else
-      hipLaunchKernelGGL((k_kda_seq<D, true, 64>), dim3(static_cast<uint32_t>(a.n_seq * a.H * (D / 64))), dim3(KT),
-                         (lds_seq<D, 64>()), s, a.seq_tab, a.s0, a.req_tab, a.H, ws, nullptr,
-                         const_cast<float*>(dS_final), dbank, dS0_seq);
+      hipLaunchKernelGGL((k_kda_seq<D, true, 64>), dim3(seq_grid(n_chain, D / 64)), dim3(KT), (lds_seq<D, 64>()), s,
+                         a.seq_tab, a.s0, n_chain, a.req_tab, a.H, ws, nullptr, const_cast<float*>(dS_final), dbank,
+                         dS0_seq);
     if (int rc = kda_status("k_kda_seq (reverse)")) return rc;
   }
   if (a.n_chunks > 0) {
