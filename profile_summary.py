@@ -117,8 +117,8 @@ def counters(out, n_cu, n_xcd, paths, cmd):
     """Per-kernel means per dispatch of every counter in the given pass
     files, with derived ratios.  GRBM_GUI_ACTIVE reads as the sum over the
     XCDs, so the MFMA busy share is SQ_VALU_MFMA_BUSY_CYCLES over
-    GRBM_GUI_ACTIVE / n_xcd * n_cu * 4 SIMDs; the bf16 MFMA rate is
-    SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 FLOP over the dispatch duration."""
+    GRBM_GUI_ACTIVE / n_xcd * n_cu * 4 SIMDs; the bf16 (fp32) MFMA rate is
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 (_F32) * 512 FLOP over the dispatch duration."""
     vals = collections.defaultdict(dict)   # kernel -> counter -> mean per dispatch
     dur = collections.defaultdict(list)    # kernel -> dispatch durations (ns)
     for path in paths:
@@ -141,25 +141,29 @@ def counters(out, n_cu, n_xcd, paths, cmd):
              "Kernel source hashes: " + ", ".join(sorted({" + ".join(sources_of(k)) + " " + source_sha(k)
                                                          for k in vals if k.startswith("k_")})), "",
              f"MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {n_xcd} XCDs x {n_cu} CUs "
-             "x 4 SIMDs); bf16 MFMA rate = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 FLOP / dispatch "
-             "duration (peak 2500 TFLOP/s); wait, issue and LDS shares are of SQ_WAVE_CYCLES "
+             "x 4 SIMDs); MFMA rates = SQ_INSTS_VALU_MFMA_MOPS_BF16 (_F32) x 512 FLOP / dispatch "
+             "duration (peaks 2500 and 157.3 TFLOP/s); wait, issue and LDS shares are of SQ_WAVE_CYCLES "
              "(all in quad-cycles); LDS busy = SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE / "
              f"{n_xcd} x {n_cu}).", ""]
 
     def ratio(d, a, b, f=1.0):
         return "%.1f%%" % (100.0 * d[a] / (d[b] * f)) if a in d and d.get(b) else "-"
 
-    lines += ["| kernel | MFMA busy | bf16 MFMA TFLOP/s | LDS busy | LDS conflict share | wait any | "
-              "VALU issue | LDS issue |",
-              "|---|---|---|---|---|---|---|---|"]
+    lines += ["| kernel | MFMA busy | bf16 MFMA TFLOP/s | fp32 MFMA TFLOP/s | LDS busy | LDS conflict share | "
+              "wait any | VALU issue | LDS issue |",
+              "|---|---|---|---|---|---|---|---|---|"]
+
+    def rate(d, k, counter):
+        if not d.get(counter) or not dur.get(k):
+            return "-"
+        ns = sum(dur[k]) / len(dur[k])
+        return "%.1f" % (d[counter] * 512 / ns / 1e3)
+
     for k in kernels:
         d = vals[k]
-        tf = "-"
-        if d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16") and dur.get(k):
-            ns = sum(dur[k]) / len(dur[k])
-            tf = "%.0f" % (d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512 / ns / 1e3)
-        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s |" % (
-            k, ratio(d, "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", 4.0 * n_cu / n_xcd), tf,
+        lines.append("| %s | %s | %s | %s | %s | %s | %s | %s | %s |" % (
+            k, ratio(d, "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", 4.0 * n_cu / n_xcd),
+            rate(d, k, "SQ_INSTS_VALU_MFMA_MOPS_BF16"), rate(d, k, "SQ_INSTS_VALU_MFMA_MOPS_F32"),
             ratio(d, "SQ_LDS_IDX_ACTIVE", "GRBM_GUI_ACTIVE", 1.0 * n_cu / n_xcd),
             ratio(d, "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE"),
             ratio(d, "SQ_WAIT_ANY", "SQ_WAVE_CYCLES"),
