@@ -922,7 +922,7 @@ def kda_measurement(steps, warmup, profile_only=False):
                        f"float32 g/beta/states",
            "ms_per_step": ms, "compact_tok_s": Cn / (ms * 1e-3), "fwd_ms": ms_f, "tables_host_ms": tables_ms,
            "alg_TFLOP_step": fl / 1e12, "TFLOPs": tf(fl, ms), "fwd_TFLOPs": tf(fl_f, ms_f),
-           "fp32_vector_frac": tf(fl, ms) / PEAK_F32_TFLOPS}
+           "fp32_peak_frac": tf(fl, ms) / PEAK_F32_TFLOPS}
     # the oracle: the trajectory-wise fp64 recurrence, forward and backward by
     # reverse mode, on the first 512 tokens of one trajectory and one head
     from oracle.kda import kda_recurrent
