@@ -88,6 +88,44 @@ template <> struct RowVec<float> {
   }
 };
 
+// This thread's 16-byte pieces of the rows of one packed chunk and head
+// (zero for padding rows), held in registers from an early load to a later
+// store into LDS as float32 [64][LDS].
+template <typename T, int D>
+struct RowPre {
+  static constexpr int N = RowVec<T>::N, VR = D / N, NL = KB * VR / KT;
+  static_assert(NL >= 1 && NL * KT == KB * VR, "pieces per thread");
+  uint4 u[NL];
+  __device__ inline void load(const T* __restrict__ src, const int32_t* ent, int H, int h, int t) {
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int idx = t + i * KT, r = idx / VR, c = (idx % VR) * N;
+      const int32_t e = ent[r];
+      u[i] = e >= 0 ? *reinterpret_cast<const uint4*>(src + (static_cast<int64_t>(e >> 1) * H + h) * D + c)
+                    : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+  template <int LDS>
+  __device__ inline void store(float* s, int t) const {
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int idx = t + i * KT, r = idx / VR, c = (idx % VR) * N;
+      const uint32_t w[4] = {u[i].x, u[i].y, u[i].z, u[i].w};
+      float* d = s + r * LDS + c;
+      if (N == 8) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          d[2 * e] = __uint_as_float(w[e] << 16);
+          d[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) d[e] = __uint_as_float(w[e]);
+      }
+    }
+  }
+};
+
 template <typename T, int D, int LDS = D + 1>
 __device__ inline void load_rows(float* s, const T* __restrict__ src, const int32_t* ent, int H, int h, int t) {
   constexpr int N = RowVec<T>::N, VR = D / N;
@@ -382,8 +420,14 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  load_rows<T, D, LD>(sK, k, ent, H, h, t);
-  load_rows<T, D, LD>(sQ, q, ent, H, h, t);
+  // k, q and v requested together at the start (k is stored twice, at
+  // both strides; v waits in registers until the products with Tm)
+  RowPre<T, D> pk, pq, pv;
+  pk.load(k, ent, H, h, t);
+  pq.load(q, ent, H, h, t);
+  pv.load(v, ent, H, h, t);
+  pk.template store<LD>(sK, t);
+  pq.template store<LD>(sQ, t);
   load_decay<D, LD>(sG, sb, sTot, g, beta, ent, H, h, t);
   // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B} (before the pairwise
   // sums overwrite K and Q with their block factors)
@@ -405,8 +449,8 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
     const int i = p / KB, j = p % KB;
     sA[i * LT + j] = j <= i ? sL[i * LT + j] * sb[j] : 0.f;
   }
-  load_rows<T, D, LW>(sK, k, ent, H, h, t);
-  load_rows<T, D, LW>(sQ, v, ent, H, h, t);
+  pk.template store<LW>(sK, t);
+  pv.template store<LW>(sQ, t);
   __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
