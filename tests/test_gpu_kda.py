@@ -50,11 +50,34 @@ def draw(Cn, H, d, n_trees, n_leaves, seed, bf16):
 @pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
 @pytest.mark.parametrize("label,parent,seg_len", CASES, ids=[c[0] for c in CASES])
 def test_kda_matches_oracle(label, parent, seg_len, dtype, d):
+    check_forest(label, parent, seg_len, dtype, d, 2)
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 128), ("bf16", 64)])
+def test_kda_other_dtype_and_width(dtype, d):
+    label, parent, seg_len = CASES[2]
+    check_forest(label, parent, seg_len, dtype, d, 2)
+
+
+# A root of 70 rows with 18 leaves of 3..63 rows at 32 heads: the round of
+# the leaves runs 17 state chains per head, 544 in all, enough for the state
+# pass's 64-column slabs (the small forests above take its 32-column slabs).
+STAR = ("star of 18 leaves", [-1] + [0] * 18, [70] + [3 + (9 * i + 5) % 61 for i in range(18)])
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_kda_wide_state_slabs(dtype, d):
+    run = check_forest(*STAR, dtype, d, 32)
+    assert max(s1 - s0 for s0, s1, *_ in run.rounds) * 32 * (d // 64) >= 512
+
+
+def check_forest(label, parent, seg_len, dtype, d, H):
+    """Every element of o, S_final and the gradients against the oracle."""
     from paper_2608_28158_amd.kda import KdaRunner
     from paper_2608_28158_amd.plan import HartsPlan
-    plan = HartsPlan(parent, seg_len, 64)
-    H, Cn = 2, int(np.sum(seg_len))
-    print(f"[gpu] kda {label} K={plan['n_rounds']} {dtype} d={d}", flush=True)
+    plan = HartsPlan(parent, seg_len, 64, heads=H)
+    Cn = int(np.sum(seg_len))
+    print(f"[gpu] kda {label} K={plan['n_rounds']} {dtype} d={d} H={H}", flush=True)
     q, k, v, g, beta, dO, S0, dSf = draw(Cn, H, d, plan["n_trees"], plan["n_leaves"], Cn + d, dtype == "bf16")
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     phys = phys_index(seg_len, plan["seg_row"])
@@ -77,8 +100,9 @@ def test_kda_matches_oracle(label, parent, seg_len, dtype, d):
         errs[n] = max_rel(host(grads[n])[phys], ref[n])
     errs["dS0_tree"] = max_rel(host(grads["dS0_tree"]), ref["dS0_tree"])
     print(f"[gpu] kda {label} {dtype} d={d}: " + ", ".join(f"{a}={b:.2e}" for a, b in errs.items()), flush=True)
-    record(f"kda {label} K={plan['n_rounds']} d={d}", dtype, errs)
+    record(f"kda {label} K={plan['n_rounds']} d={d} H={H}", dtype, errs)
     assert all(e <= TOL[dtype] for e in errs.values()), errs
+    return run
 
 
 def test_kda_64k_workload_sampled():
