@@ -511,8 +511,12 @@ int harts_attn_scatter(const float* src, const int64_t* row_off, const int32_t* 
  *   group_tab  [n_groups][4], group_seq [n_seq]: per round, the sequences
  *              starting from each bank entry (round, entry, first member,
  *              members), in sequence order -- the order of the adjoint sums.
- *   row_off [C+1], row_pos [C+R]: packed rows (chunk * 64 + i) of every
- *              compact row, ascending -- the order of the gradient sums.
+ *   pos_slot   [n_chunks * 64]: per packed row (chunk * 64 + i), -1 when
+ *              its compact row has no other packed row (its gradients go
+ *              straight to the outputs), else its slot: the n_multi compact
+ *              rows with replay copies, ascending, hold slots
+ *              [multi_off[m], multi_off[m + 1]) in ascending packed order.
+ *   multi_row  [n_multi], multi_off [n_multi + 1] (n_slots in all).
  * harts_kda_workspace_size -- float32 per-(chunk, head) blocks for all
  *   chunks of the plan (the forward's are read by the backward).
  * harts_kda_fwd (device) -- one round: chunks [c0, c0 + n_chunks), sequences
@@ -522,26 +526,32 @@ int harts_attn_scatter(const float* src, const int64_t* row_off, const int32_t* 
  * harts_kda_bwd (device) -- one round, after the later rounds' backward:
  *   dO [C, H, d]; dS_final (may be NULL); dbank [n_bank][H][d][d] holds the
  *   later rounds' summed initial-state adjoints; writes dS0_seq
- *   [n_seq][H][d][d] of the round's sequences and, per packed row, the
- *   float32 gradients pdq, pdk, pdv, pdg [n_chunks * 64][H][d] and pdb
- *   [n_chunks * 64][H] (padding rows untouched).
+ *   [n_seq][H][d][d] of the round's sequences.  Gradients of the round's
+ *   packed rows: for a compact row with one packed row, straight into
+ *   dq, dk, dv [C, H, d] (dtype), dg [C, H, d] and dbeta [C, H] (float32);
+ *   otherwise float32 partials into its slot of sdq, sdk, sdv, sdg
+ *   [n_slots][H][d] and sdb [n_slots][H] (NULL allowed when n_slots = 0).
+ *   dq, dk, sdq and sdk must be 16-byte aligned (four-element stores).
  * harts_kda_bank_add (device) -- dbank[entry] += the group's dS0_seq, for
  *   groups [g0, g0 + n_groups) (one round's), in member order.
- * harts_kda_reduce (device) -- dst [C][width] (bf16 or float32) = sum over
- *   each compact row's packed rows of src [n_pos][width], in row_pos order.
+ * harts_kda_reduce (device) -- after every round's backward: for the
+ *   n_multi compact rows with several packed rows, dst [C][width] (bf16 or
+ *   float32) row multi_row[m] = the sum of src [n_slots][width] over slots
+ *   [multi_off[m], multi_off[m + 1]), in slot order.
  * All arithmetic is float32 and deterministic (no atomics).  Errors:
  * HARTS_EINVAL (NULL, ranges), HARTS_EUNSUPPORTED (dtype, H, d, a plan with
  * chunk != 64, more than 2^31 - 1 packed rows), HARTS_EHIP, HARTS_ENOMEM.
  * ---------------------------------------------------------------------- */
 typedef struct harts_kda_sizes {
-  int64_t n_chunks, n_entries;
-  int32_t n_seq, n_rounds, n_groups, n_req;
+  int64_t n_chunks, n_slots;
+  int32_t n_seq, n_rounds, n_groups, n_req, n_multi, pad;
 } harts_kda_sizes;
 
 int harts_kda_layout(const harts_plan_t* plan, harts_kda_sizes* out);
 
 int harts_kda_tables(const harts_plan_t* plan, int32_t* chunk_rows, int32_t* seq_tab, int32_t* req_tab,
-                     int32_t* group_tab, int32_t* group_seq, int64_t* row_off, int32_t* row_pos);
+                     int32_t* group_tab, int32_t* group_seq, int32_t* pos_slot, int32_t* multi_row,
+                     int64_t* multi_off);
 
 int harts_kda_workspace_size(int64_t n_chunks, int32_t H, int32_t d, size_t* bytes);
 
@@ -550,17 +560,18 @@ int harts_kda_fwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32
                   const void* q, const void* k, const void* v, const float* g, const float* beta, float* bank,
                   float* S_final, void* o, float* ws, void* stream);
 
-int harts_kda_bwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab, int64_t c0,
-                  int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H, int32_t d, float scale,
-                  const void* q, const void* k, const void* v, const float* g, const float* beta, const void* dO,
-                  const float* dS_final, const float* dbank, float* dS0_seq, float* ws, float* pdq, float* pdk,
-                  float* pdv, float* pdg, float* pdb, void* stream);
+int harts_kda_bwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab, const int32_t* pos_slot,
+                  int64_t c0, int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H, int32_t d,
+                  float scale, const void* q, const void* k, const void* v, const float* g, const float* beta,
+                  const void* dO, const float* dS_final, const float* dbank, float* dS0_seq, float* ws, void* dq,
+                  void* dk, void* dv, float* dg, float* dbeta, float* sdq, float* sdk, float* sdv, float* sdg,
+                  float* sdb, void* stream);
 
 int harts_kda_bank_add(const int32_t* group_tab, int32_t g0, int32_t n_groups, const int32_t* group_seq,
                        int64_t elems, const float* dS0_seq, float* dbank, void* stream);
 
-int harts_kda_reduce(const float* src, const int64_t* row_off, const int32_t* row_pos, int64_t C, int64_t width,
-                     int64_t n_pos, int32_t dtype, void* dst, void* stream);
+int harts_kda_reduce(const float* src, const int32_t* multi_row, const int64_t* multi_off, int64_t n_multi,
+                     int64_t width, int32_t dtype, void* dst, void* stream);
 
 /* ------------------------------------------------------------------------
  * Compact-to-semantic log-probabilities (Sec. 3.5, eqs. mapped-logp and

@@ -98,8 +98,8 @@ class AttnLayout(C.Structure):
 
 
 class KdaSizes(C.Structure):
-    _fields_ = [("n_chunks", C.c_int64), ("n_entries", C.c_int64)] + \
-        [(n, C.c_int32) for n in ("n_seq", "n_rounds", "n_groups", "n_req")]
+    _fields_ = [("n_chunks", C.c_int64), ("n_slots", C.c_int64)] + \
+        [(n, C.c_int32) for n in ("n_seq", "n_rounds", "n_groups", "n_req", "n_multi", "pad")]
 
 
 class KernelTime(C.Structure):
@@ -195,17 +195,17 @@ def lib():
     L.harts_kda_layout.restype = C.c_int
     L.harts_kda_layout.argtypes = [vp, vp]
     L.harts_kda_tables.restype = C.c_int
-    L.harts_kda_tables.argtypes = [vp] * 8
+    L.harts_kda_tables.argtypes = [vp] * 9
     L.harts_kda_workspace_size.restype = C.c_int
     L.harts_kda_workspace_size.argtypes = [i64, i32, i32, vp]
     L.harts_kda_fwd.restype = C.c_int
     L.harts_kda_fwd.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i32, i32, C.c_float] + [vp] * 10
     L.harts_kda_bwd.restype = C.c_int
-    L.harts_kda_bwd.argtypes = [vp, vp, vp, i64, i64, i32, i32, i32, i32, i32, C.c_float] + [vp] * 16
+    L.harts_kda_bwd.argtypes = [vp, vp, vp, vp, i64, i64, i32, i32, i32, i32, i32, C.c_float] + [vp] * 21
     L.harts_kda_bank_add.restype = C.c_int
     L.harts_kda_bank_add.argtypes = [vp, i32, i32, vp, i64, vp, vp, vp]
     L.harts_kda_reduce.restype = C.c_int
-    L.harts_kda_reduce.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp, vp]
+    L.harts_kda_reduce.argtypes = [vp, vp, vp, i64, i64, i32, vp, vp]
     L.harts_profile_begin.restype = C.c_int
     L.harts_profile_begin.argtypes = []
     L.harts_profile_end.restype = C.c_int

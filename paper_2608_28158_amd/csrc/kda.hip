@@ -48,6 +48,26 @@ template <> __device__ inline float ld<bf16>(const bf16* p) { return static_cast
 template <typename T> __device__ inline void st(T* p, float x);
 template <> __device__ inline void st<float>(float* p, float x) { *p = x; }
 template <> __device__ inline void st<bf16>(bf16* p, float x) { *p = static_cast<bf16>(x); }
+// four consecutive elements
+template <typename T> __device__ inline void st4(T* p, const float* x);
+template <> __device__ inline void st4<float>(float* p, const float* x) {
+  *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+}
+template <> __device__ inline void st4<bf16>(bf16* p, const float* x) {
+  bf16 b[4] = {static_cast<bf16>(x[0]), static_cast<bf16>(x[1]), static_cast<bf16>(x[2]), static_cast<bf16>(x[3])};
+  *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(b);
+}
+
+// Where the backward's per-row gradients go: a packed row whose compact row
+// has no other packed row (slot -1) writes the compact row's gradients
+// directly; the others write float32 partials into their slot, summed by
+// k_kda_reduce after the last round.
+struct KdaGrads {
+  const int32_t* slot;                 // [n_chunks * 64]
+  void* dq; void* dk; void* dv;        // [C][H][d], the input dtype
+  float* dg; float* dbeta;             // [C][H][d], [C][H]
+  float* sdq; float* sdk; float* sdv; float* sdg; float* sdb;   // [n_slots][H][d], [n_slots][H]
+};
 
 // Per-(chunk, head) float32 blocks of the workspace (element offsets per
 // chunk-head given by D).
@@ -939,7 +959,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                    const T* __restrict__ k, const float* __restrict__ g,
                                                    const float* __restrict__ beta, float* __restrict__ ws,
-                                                   float* __restrict__ pdv) {
+                                                   const KdaGrads go) {
   using Y = WsLay<D>;
   constexpr int LG = D + 1, LK = D + 4, TDW = D / 32;
   extern __shared__ float sm[];
@@ -1001,11 +1021,15 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int j = 16 * wi + 4 * lk + r;
-    const bool real = ent[j] >= 0;
+    const int32_t e = ent[j];
+    const int32_t sl = e >= 0 ? go.slot[static_cast<int64_t>(c) * KB + j] : -1;
 #pragma unroll
     for (int x = 0; x < TDW; ++x) {
       const int col = 16 * (td0 + x) + li;
-      if (real) pdv[(static_cast<int64_t>(c) * KB + j) * H * D + static_cast<int64_t>(h) * D + col] = aV[x][r];
+      if (e >= 0) {
+        if (sl < 0) st<T>(static_cast<T*>(go.dv) + (static_cast<int64_t>(e >> 1) * H + h) * D + col, aV[x][r]);
+        else go.sdv[(static_cast<int64_t>(sl) * H + h) * D + col] = aV[x][r];
+      }
       w[Y::DKG + j * D + col] = aK[x][r];
     }
   }
@@ -1020,9 +1044,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                       const T* __restrict__ q, const T* __restrict__ k,
                                                       const float* __restrict__ g, const float* __restrict__ beta,
-                                                      float* __restrict__ ws, float* __restrict__ pdq,
-                                                      float* __restrict__ pdk, float* __restrict__ pdg,
-                                                      float* __restrict__ pdb) {
+                                                      float* __restrict__ ws, const KdaGrads go) {
   using Y = WsLay<D>;
   constexpr int LB = KB + 4;       // 64 x 64 tiles: a stride of 4 (mod 64 banks) for the MFMA fragment reads
   extern __shared__ float sm[];
@@ -1266,10 +1288,18 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
         sK[i * D + d0 + cc] = k_ * (r2 - c1) + q_ * r1 + (dqg[cc] * q_ + dkg[cc] * k_) * eG - dkb[cc] * k_ * eB;
         sQ[i * D + d0 + cc] = dkb[cc] * k_ * eB;
       }
-      if (ent[i] >= 0) {
-        const int64_t o = (static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d0;
-        *reinterpret_cast<float4*>(pdq + o) = make_float4(dq[0], dq[1], dq[2], dq[3]);
-        *reinterpret_cast<float4*>(pdk + o) = make_float4(dk[0], dk[1], dk[2], dk[3]);
+      const int32_t e = ent[i];
+      if (e >= 0) {
+        const int32_t sl = go.slot[static_cast<int64_t>(c) * KB + i];
+        if (sl < 0) {
+          const int64_t o = (static_cast<int64_t>(e >> 1) * H + h) * D + d0;
+          st4<T>(static_cast<T*>(go.dq) + o, dq);
+          st4<T>(static_cast<T*>(go.dk) + o, dk);
+        } else {
+          const int64_t o = (static_cast<int64_t>(sl) * H + h) * D + d0;
+          st4<float>(go.sdq + o, dq);
+          st4<float>(go.sdk + o, dk);
+        }
       }
     }
   }
@@ -1296,47 +1326,50 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
 #pragma unroll
     for (int r = 0; r < RP; ++r) {
       const int i = part * RP + r;
-      if (ent[i] >= 0) pdg[(static_cast<int64_t>(c) * KB + i) * H * D + static_cast<int64_t>(h) * D + d] = suf[r] + off;
+      const int32_t e = ent[i];
+      if (e < 0) continue;
+      const int32_t sl = go.slot[static_cast<int64_t>(c) * KB + i];
+      float* dst = sl < 0 ? go.dg + (static_cast<int64_t>(e >> 1) * H + h) * D
+                          : go.sdg + (static_cast<int64_t>(sl) * H + h) * D;
+      dst[d] = suf[r] + off;
     }
   }
-  if (t < KB && ent[t] >= 0) pdb[(static_cast<int64_t>(c) * KB + t) * H + h] = sdb[t];
+  if (t < KB && ent[t] >= 0) {
+    const int32_t sl = go.slot[static_cast<int64_t>(c) * KB + t];
+    if (sl < 0) go.dbeta[static_cast<int64_t>(ent[t] >> 1) * H + h] = sdb[t];
+    else go.sdb[static_cast<int64_t>(sl) * H + h] = sdb[t];
+  }
 }
 
-// Compact rows <- sum of their packed rows, in ascending packed order; four
-// consecutive elements per thread when the row width allows it.
-__global__ __launch_bounds__(KT) void k_kda_reduce(const float* __restrict__ src, const int64_t* __restrict__ row_off,
-                                                   const int32_t* __restrict__ row_pos, int64_t C, int64_t width,
-                                                   int64_t n_pos, void* __restrict__ dst, int to_bf16, int vec) {
+// The compact rows with several packed rows <- the sum of their slots, in
+// slot order; four consecutive elements per thread when the row width
+// allows it.
+__global__ __launch_bounds__(KT) void k_kda_reduce(const float* __restrict__ src,
+                                                   const int32_t* __restrict__ multi_row,
+                                                   const int64_t* __restrict__ multi_off, int64_t n_multi,
+                                                   int64_t width, void* __restrict__ dst, int to_bf16, int vec) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * KT + threadIdx.x;
   if (vec) {
     const int64_t w4 = width / 4;
-    if (idx >= C * w4) return;
-    const int64_t r = idx / w4, x = (idx % w4) * 4;
-    float4 a = {0.f, 0.f, 0.f, 0.f};
-    for (int64_t j = row_off[r]; j < row_off[r + 1]; ++j) {
-      const int32_t p = row_pos[j];
-      if (p < 0 || p >= n_pos) continue;
-      const float4 v = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(p) * width + x);
-      a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
+    if (idx >= n_multi * w4) return;
+    const int64_t m = idx / w4, x = (idx % w4) * 4;
+    float a[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t s = multi_off[m]; s < multi_off[m + 1]; ++s) {
+      const float4 v = *reinterpret_cast<const float4*>(src + s * width + x);
+      a[0] += v.x; a[1] += v.y; a[2] += v.z; a[3] += v.w;
     }
-    if (to_bf16) {
-      bf16* o = static_cast<bf16*>(dst) + r * width + x;
-      o[0] = static_cast<bf16>(a.x); o[1] = static_cast<bf16>(a.y);
-      o[2] = static_cast<bf16>(a.z); o[3] = static_cast<bf16>(a.w);
-    } else {
-      *reinterpret_cast<float4*>(static_cast<float*>(dst) + r * width + x) = a;
-    }
+    const int64_t o = static_cast<int64_t>(multi_row[m]) * width + x;
+    if (to_bf16) st4<bf16>(static_cast<bf16*>(dst) + o, a);
+    else st4<float>(static_cast<float*>(dst) + o, a);
     return;
   }
-  if (idx >= C * width) return;
-  const int64_t r = idx / width, x = idx % width;
+  if (idx >= n_multi * width) return;
+  const int64_t m = idx / width, x = idx % width;
   float a = 0.f;
-  for (int64_t j = row_off[r]; j < row_off[r + 1]; ++j) {
-    const int32_t p = row_pos[j];
-    if (p >= 0 && p < n_pos) a += src[static_cast<int64_t>(p) * width + x];
-  }
-  if (to_bf16) static_cast<bf16*>(dst)[idx] = static_cast<bf16>(a);
-  else static_cast<float*>(dst)[idx] = a;
+  for (int64_t s = multi_off[m]; s < multi_off[m + 1]; ++s) a += src[s * width + x];
+  const int64_t o = static_cast<int64_t>(multi_row[m]) * width + x;
+  if (to_bf16) static_cast<bf16*>(dst)[o] = static_cast<bf16>(a);
+  else static_cast<float*>(dst)[o] = a;
 }
 
 // dbank[bank of group] += sum of dS0_seq over the group's sequences, in order.
@@ -1429,8 +1462,8 @@ int kda_fwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
 
 template <typename T, int D>
 int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, const float* g, const float* beta,
-                 const void* dO, const float* dS_final, const float* dbank, float* dS0_seq, float* ws, float* pdq,
-                 float* pdk, float* pdv, float* pdg, float* pdb, hipStream_t s) {
+                 const void* dO, const float* dS_final, const float* dbank, float* dS0_seq, float* ws,
+                 const KdaGrads& go, hipStream_t s) {
   const auto* tq = static_cast<const T*>(q);
   const auto* tk = static_cast<const T*>(k);
   const auto* tv = static_cast<const T*>(v);
@@ -1458,10 +1491,10 @@ int kda_bwd_impl(const KdaArgs& a, const void* q, const void* k, const void* v, 
                        a.scale, tv, td, ws);
     if (int rc = kda_status("k_kda_bwd_prod")) return rc;
     hipLaunchKernelGGL((k_kda_bwd_tm<T, D>), dim3(gc), dim3(KT), lds_btm<D>(), s, a.chunk_rows, a.c0, a.H, tk, g,
-                       beta, ws, pdv);
+                       beta, ws, go);
     if (int rc = kda_status("k_kda_bwd_tm")) return rc;
     hipLaunchKernelGGL((k_kda_bwd_local<T, D>), dim3(gc), dim3(KT), lds_blocal<D>(), s, a.chunk_rows, a.c0, a.H,
-                       tq, tk, g, beta, ws, pdq, pdk, pdg, pdb);
+                       tq, tk, g, beta, ws, go);
     if (int rc = kda_status("k_kda_bwd_local")) return rc;
   }
   return HARTS_OK;
@@ -1544,19 +1577,25 @@ extern "C" int harts_kda_fwd(const int32_t* chunk_rows, const int32_t* seq_tab, 
 }
 
 extern "C" int harts_kda_bwd(const int32_t* chunk_rows, const int32_t* seq_tab, const int32_t* req_tab,
-                             int64_t c0, int64_t n_chunks, int32_t s0, int32_t n_seq, int32_t dtype, int32_t H,
-                             int32_t d, float scale, const void* q, const void* k, const void* v, const float* g,
-                             const float* beta, const void* dO, const float* dS_final, const float* dbank,
-                             float* dS0_seq, float* ws, float* pdq, float* pdk, float* pdv, float* pdg, float* pdb,
-                             void* stream) {
+                             const int32_t* pos_slot, int64_t c0, int64_t n_chunks, int32_t s0, int32_t n_seq,
+                             int32_t dtype, int32_t H, int32_t d, float scale, const void* q, const void* k,
+                             const void* v, const float* g, const float* beta, const void* dO, const float* dS_final,
+                             const float* dbank, float* dS0_seq, float* ws, void* dq, void* dk, void* dv, float* dg,
+                             float* dbeta, float* sdq, float* sdk, float* sdv, float* sdg, float* sdb, void* stream) {
   if (!kda_shape_ok(dtype, H, d, "harts_kda_bwd")) return HARTS_EUNSUPPORTED;
   if (c0 < 0 || n_chunks < 0 || s0 < 0 || n_seq < 0) {
     set_error("harts_kda_bwd: bad ranges");
     return HARTS_EINVAL;
   }
-  if (!chunk_rows || !seq_tab || !q || !k || !v || !g || !beta || !dO || !dbank || !dS0_seq || !ws || !pdq ||
-      !pdk || !pdv || !pdg || !pdb) {
+  if (!chunk_rows || !seq_tab || !pos_slot || !q || !k || !v || !g || !beta || !dO || !dbank || !dS0_seq || !ws ||
+      !dq || !dk || !dv || !dg || !dbeta) {
     set_error("harts_kda_bwd: NULL pointer");
+    return HARTS_EINVAL;
+  }
+  // four-element stores of dq, dk and their slot partials
+  const auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  if (!al(dq) || !al(dk) || (sdq && !al(sdq)) || (sdk && !al(sdk))) {
+    set_error("harts_kda_bwd: dq, dk, sdq and sdk must be 16-byte aligned");
     return HARTS_EINVAL;
   }
   if (!(d == 128 ? kda_set_lds<128>() : kda_set_lds<64>())) {
@@ -1564,35 +1603,32 @@ extern "C" int harts_kda_bwd(const int32_t* chunk_rows, const int32_t* seq_tab, 
     return HARTS_EHIP;
   }
   const KdaArgs a{chunk_rows, seq_tab, req_tab, c0, n_chunks, s0, n_seq, H, scale};
+  const KdaGrads go{pos_slot, dq, dk, dv, dg, dbeta, sdq, sdk, sdv, sdg, sdb};
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == HARTS_BF16)
-    return d == 128 ? kda_bwd_impl<bf16, 128>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
-                                              pdg, pdb, s)
-                    : kda_bwd_impl<bf16, 64>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
-                                             pdg, pdb, s);
-  return d == 128 ? kda_bwd_impl<float, 128>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
-                                             pdg, pdb, s)
-                  : kda_bwd_impl<float, 64>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, pdq, pdk, pdv,
-                                            pdg, pdb, s);
+    return d == 128 ? kda_bwd_impl<bf16, 128>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, go, s)
+                    : kda_bwd_impl<bf16, 64>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, go, s);
+  return d == 128 ? kda_bwd_impl<float, 128>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, go, s)
+                  : kda_bwd_impl<float, 64>(a, q, k, v, g, beta, dO, dS_final, dbank, dS0_seq, ws, go, s);
 }
 
-extern "C" int harts_kda_reduce(const float* src, const int64_t* row_off, const int32_t* row_pos, int64_t C,
-                                int64_t width, int64_t n_pos, int32_t dtype, void* dst, void* stream) {
-  if ((dtype != HARTS_BF16 && dtype != HARTS_F32) || C < 0 || width < 1 || n_pos < 0) {
+extern "C" int harts_kda_reduce(const float* src, const int32_t* multi_row, const int64_t* multi_off,
+                                int64_t n_multi, int64_t width, int32_t dtype, void* dst, void* stream) {
+  if ((dtype != HARTS_BF16 && dtype != HARTS_F32) || n_multi < 0 || width < 1) {
     set_error("harts_kda_reduce: bad arguments");
     return HARTS_EINVAL;
   }
-  if (C == 0) return HARTS_OK;
-  if (!src || !row_off || !row_pos || !dst) {
+  if (n_multi == 0) return HARTS_OK;
+  if (!src || !multi_row || !multi_off || !dst) {
     set_error("harts_kda_reduce: NULL pointer");
     return HARTS_EINVAL;
   }
-  // four elements a thread where the width and both pointers allow 16-byte source loads
+  // four elements a thread where the width and both pointers allow 16-byte loads and 8- or 16-byte stores
   const bool vec = (width & 3) == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
-                   (reinterpret_cast<uintptr_t>(dst) & (dtype == HARTS_BF16 ? 1 : 15)) == 0;
-  const int64_t n = vec ? C * width / 4 : C * width;
+                   (reinterpret_cast<uintptr_t>(dst) & (dtype == HARTS_BF16 ? 7 : 15)) == 0;
+  const int64_t n = vec ? n_multi * width / 4 : n_multi * width;
   hipLaunchKernelGGL(k_kda_reduce, dim3(static_cast<uint32_t>((n + KT - 1) / KT)), dim3(KT), 0,
-                     static_cast<hipStream_t>(stream), src, row_off, row_pos, C, width, n_pos, dst,
+                     static_cast<hipStream_t>(stream), src, multi_row, multi_off, n_multi, width, dst,
                      dtype == HARTS_BF16 ? 1 : 0, vec ? 1 : 0);
   return kda_status("k_kda_reduce");
 }

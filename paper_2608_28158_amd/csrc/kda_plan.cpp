@@ -48,21 +48,37 @@ extern "C" int harts_kda_layout(const harts_plan_t* p, harts_kda_sizes* out) {
     set_error("harts_kda_layout: more than 2^31 - 1 packed rows");
     return HARTS_EUNSUPPORTED;
   }
+  // compact rows with replay copies hold several packed rows: one slot each
+  int64_t n_multi = 0, n_slots = 0;
+  try {
+    std::vector<int32_t> copies(static_cast<size_t>(p->C), 0);
+    for (int64_t j = 0; j < p->R; ++j) ++copies[p->replay_row[j]];
+    for (int64_t r = 0; r < p->C; ++r)
+      if (copies[r] > 0) {
+        ++n_multi;
+        n_slots += 1 + copies[r];
+      }
+  } catch (const std::bad_alloc&) {
+    set_error("harts_kda_layout: out of host memory");
+    return HARTS_ENOMEM;
+  }
   out->n_chunks = nc;
-  out->n_entries = p->C + p->R;
+  out->n_slots = n_slots;
   out->n_seq = p->n_seq;
   out->n_rounds = p->K;
   out->n_groups = groups;
   out->n_req = static_cast<int32_t>(p->req_chunk.size());
+  out->n_multi = static_cast<int32_t>(n_multi);
   return HARTS_OK;
 }
 
 extern "C" int harts_kda_tables(const harts_plan_t* p, int32_t* chunk_rows, int32_t* seq_tab, int32_t* req_tab,
-                                int32_t* group_tab, int32_t* group_seq, int64_t* row_off, int32_t* row_pos) {
+                                int32_t* group_tab, int32_t* group_seq, int32_t* pos_slot, int32_t* multi_row,
+                                int64_t* multi_off) {
   harts_kda_sizes sz;
   if (int rc = harts_kda_layout(p, &sz)) return rc;
-  if (!chunk_rows || !seq_tab || (sz.n_req > 0 && !req_tab) || !group_tab || !group_seq || !row_off ||
-      !row_pos) {
+  if (!chunk_rows || !seq_tab || (sz.n_req > 0 && !req_tab) || !group_tab || !group_seq || !pos_slot ||
+      (sz.n_multi > 0 && !multi_row) || !multi_off) {
     set_error("harts_kda_tables: NULL argument");
     return HARTS_EINVAL;
   }
@@ -114,15 +130,25 @@ extern "C" int harts_kda_tables(const harts_plan_t* p, int32_t* chunk_rows, int3
       req_tab[2 * j] = p->req_chunk[j];
       req_tab[2 * j + 1] = p->req_bank[j];
     }
-    // packed positions of every compact row, ascending
+    // packed positions of every compact row; the rows with several of them
+    // (ascending row order) get consecutive slots in ascending position order
     const int64_t C = p->C, npk = sz.n_chunks * kKdaChunk;
-    std::fill(row_off, row_off + C + 1, 0);
+    std::vector<int32_t> count(static_cast<size_t>(C), 0), first(static_cast<size_t>(C), -1);
     for (int64_t e = 0; e < npk; ++e)
-      if (chunk_rows[e] >= 0) ++row_off[chunk_rows[e] / 2 + 1];
-    for (int64_t r = 0; r < C; ++r) row_off[r + 1] += row_off[r];
-    std::vector<int64_t> fill(row_off, row_off + C);
-    for (int64_t e = 0; e < npk; ++e)
-      if (chunk_rows[e] >= 0) row_pos[fill[chunk_rows[e] / 2]++] = static_cast<int32_t>(e);
+      if (chunk_rows[e] >= 0) ++count[chunk_rows[e] / 2];
+    int32_t m = 0;
+    multi_off[0] = 0;
+    for (int64_t r = 0; r < C; ++r)
+      if (count[r] > 1) {
+        multi_row[m] = static_cast<int32_t>(r);
+        first[r] = static_cast<int32_t>(multi_off[m]);
+        multi_off[m + 1] = multi_off[m] + count[r];
+        ++m;
+      }
+    for (int64_t e = 0; e < npk; ++e) {
+      const int32_t r = chunk_rows[e] >= 0 ? chunk_rows[e] / 2 : -1;
+      pos_slot[e] = r >= 0 && first[r] >= 0 ? first[r]++ : -1;
+    }
   } catch (const std::bad_alloc&) {
     set_error("harts_kda_tables: out of host memory");
     return HARTS_ENOMEM;

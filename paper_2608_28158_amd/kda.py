@@ -34,22 +34,22 @@ class KdaRunner:
         sz = _lib.KdaSizes()
         _lib.check(L.harts_kda_layout(plan.handle, C.byref(sz)), "harts_kda_layout")
         self.sizes = sz
-        Cn = plan["C"]
         self.chunk_rows = np.zeros(max(sz.n_chunks, 1) * 64, np.int32)
         self.seq_tab = np.zeros((sz.n_seq, 8), np.int32)
         self.req_tab = np.zeros((max(sz.n_req, 1), 2), np.int32)
         self.group_tab = np.zeros((max(sz.n_groups, 1), 4), np.int32)
         self.group_seq = np.zeros(max(sz.n_seq, 1), np.int32)
-        self.row_off = np.zeros(Cn + 1, np.int64)
-        self.row_pos = np.zeros(max(sz.n_entries, 1), np.int32)
+        self.pos_slot = np.zeros(max(sz.n_chunks, 1) * 64, np.int32)
+        self.multi_row = np.zeros(max(sz.n_multi, 1), np.int32)
+        self.multi_off = np.zeros(sz.n_multi + 1, np.int64)
         _lib.check(L.harts_kda_tables(plan.handle, self.chunk_rows.ctypes.data, self.seq_tab.ctypes.data,
                                       self.req_tab.ctypes.data, self.group_tab.ctypes.data,
-                                      self.group_seq.ctypes.data, self.row_off.ctypes.data,
-                                      self.row_pos.ctypes.data), "harts_kda_tables")
+                                      self.group_seq.ctypes.data, self.pos_slot.ctypes.data,
+                                      self.multi_row.ctypes.data, self.multi_off.ctypes.data), "harts_kda_tables")
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
         self.d_rows, self.d_seq, self.d_req = dev(self.chunk_rows), dev(self.seq_tab), dev(self.req_tab)
         self.d_group, self.d_gseq = dev(self.group_tab), dev(self.group_seq)
-        self.d_off, self.d_pos = dev(self.row_off), dev(self.row_pos)
+        self.d_slot, self.d_mrow, self.d_moff = dev(self.pos_slot), dev(self.multi_row), dev(self.multi_off)
         # per round: sequences [s0, s1), chunks [c0, c1), groups [g0, g1)
         self.rounds = []
         for r in range(sz.n_rounds):
@@ -92,30 +92,28 @@ class KdaRunner:
         H, d, sz = self.H, self.d, self.sizes
         dbank = torch.zeros((self.n_bank, H, d, d), dtype=torch.float32, device=self.device)
         dS0_seq = torch.empty((sz.n_seq, H, d, d), dtype=torch.float32, device=self.device)
-        npk = max(sz.n_chunks, 1) * 64
-        pd = [torch.empty((npk, H, d), dtype=torch.float32, device=self.device) for _ in range(4)]
-        pb = torch.empty((npk, H), dtype=torch.float32, device=self.device)
+        Cn = self.plan["C"]
+        out = {n: torch.empty((Cn, H, d), dtype=self.dtype, device=self.device) for n in ("dq", "dk", "dv")}
+        out["dg"] = torch.empty((Cn, H, d), dtype=torch.float32, device=self.device)
+        out["dbeta"] = torch.empty((Cn, H), dtype=torch.float32, device=self.device)
+        # float32 partials of the compact rows that are also replayed: one slot per packed row
+        ns = max(sz.n_slots, 1)
+        slots = {n: torch.empty((ns, H, d), dtype=torch.float32, device=self.device) for n in ("dq", "dk", "dv", "dg")}
+        slots["dbeta"] = torch.empty((ns, H), dtype=torch.float32, device=self.device)
+        names = ("dq", "dk", "dv", "dg", "dbeta")
         st = self._stream()
         for s0, s1, c0, c1, g0, g1 in reversed(self.rounds):
-            _lib.check(self.L.harts_kda_bwd(_p(self.d_rows), _p(self.d_seq), _p(self.d_req), c0, c1 - c0, s0,
-                                            s1 - s0, self.code, H, d, C.c_float(scale), _p(q), _p(k), _p(v),
-                                            _p(g), _p(beta), _p(dO), _p(dS_final), _p(dbank), _p(dS0_seq),
-                                            _p(self.ws), _p(pd[0]), _p(pd[1]), _p(pd[2]), _p(pd[3]), _p(pb), st),
-                       "harts_kda_bwd")
+            _lib.check(self.L.harts_kda_bwd(_p(self.d_rows), _p(self.d_seq), _p(self.d_req), _p(self.d_slot), c0,
+                                            c1 - c0, s0, s1 - s0, self.code, H, d, C.c_float(scale), _p(q), _p(k),
+                                            _p(v), _p(g), _p(beta), _p(dO), _p(dS_final), _p(dbank), _p(dS0_seq),
+                                            _p(self.ws), *(_p(out[n]) for n in names),
+                                            *(_p(slots[n]) for n in names), st), "harts_kda_bwd")
             _lib.check(self.L.harts_kda_bank_add(_p(self.d_group), g0, g1 - g0, _p(self.d_gseq), H * d * d,
                                                  _p(dS0_seq), _p(dbank), st), "harts_kda_bank_add")
-        Cn = self.plan["C"]
-        out = {}
-        for name, src, dt in (("dq", pd[0], self.dtype), ("dk", pd[1], self.dtype), ("dv", pd[2], self.dtype),
-                              ("dg", pd[3], torch.float32)):
-            dst = torch.empty((Cn, H, d), dtype=dt, device=self.device)
-            code = _lib.HARTS_BF16 if dt == torch.bfloat16 else _lib.HARTS_F32
-            _lib.check(self.L.harts_kda_reduce(_p(src), _p(self.d_off), _p(self.d_pos), Cn, H * d, npk, code,
-                                               _p(dst), st), "harts_kda_reduce")
-            out[name] = dst
-        db = torch.empty((Cn, H), dtype=torch.float32, device=self.device)
-        _lib.check(self.L.harts_kda_reduce(_p(pb), _p(self.d_off), _p(self.d_pos), Cn, H, npk, _lib.HARTS_F32,
-                                           _p(db), st), "harts_kda_reduce")
-        out["dbeta"] = db
+        for n in names:
+            width = H if n == "dbeta" else H * d
+            code = _lib.HARTS_BF16 if out[n].dtype == torch.bfloat16 else _lib.HARTS_F32
+            _lib.check(self.L.harts_kda_reduce(_p(slots[n]), _p(self.d_mrow), _p(self.d_moff), sz.n_multi, width,
+                                               code, _p(out[n]), st), "harts_kda_reduce")
         out["dS0_tree"] = dbank[:self.n_trees]
         return out

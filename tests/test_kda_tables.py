@@ -31,10 +31,10 @@ def tables(plan):
     _lib.check(L.harts_kda_layout(plan.handle, C.byref(sz)), "harts_kda_layout")
     t = dict(rows=np.zeros(sz.n_chunks * 64, np.int32), seq=np.zeros((sz.n_seq, 8), np.int32),
              req=np.zeros((max(sz.n_req, 1), 2), np.int32), grp=np.zeros((sz.n_groups, 4), np.int32),
-             gseq=np.zeros(sz.n_seq, np.int32), off=np.zeros(plan["C"] + 1, np.int64),
-             pos=np.zeros(sz.n_entries, np.int32))
+             gseq=np.zeros(sz.n_seq, np.int32), slot=np.zeros(sz.n_chunks * 64, np.int32),
+             mrow=np.zeros(max(sz.n_multi, 1), np.int32), moff=np.zeros(sz.n_multi + 1, np.int64))
     _lib.check(L.harts_kda_tables(plan.handle, *(t[k].ctypes.data for k in
-                                                 ("rows", "seq", "req", "grp", "gseq", "off", "pos"))),
+                                                 ("rows", "seq", "req", "grp", "gseq", "slot", "mrow", "moff"))),
                "harts_kda_tables")
     return sz, t
 
@@ -44,7 +44,7 @@ def test_tables_follow_the_plan(label, parent, seg_len):
     from paper_2608_28158_amd.plan import HartsPlan
     plan = HartsPlan(parent, seg_len, 64)
     sz, t = tables(plan)
-    assert sz.n_entries == plan["C"] + plan["R"] and sz.n_rounds == plan["n_rounds"]
+    assert sz.n_rounds == plan["n_rounds"]
     c = 0
     for i in range(plan["n_seq"]):
         rnd, c0, nc, init, ro, nr, leaf, _ = (int(x) for x in t["seq"][i])
@@ -70,13 +70,22 @@ def test_tables_follow_the_plan(label, parent, seg_len):
         assert np.all(np.diff(members) > 0)
         seen += list(members)
     assert sorted(seen) == list(range(plan["n_seq"]))
-    # gradient lists: every real packed row once, grouped by compact row, ascending
+    # gradient slots: every real packed row of a compact row with no other
+    # packed row writes directly (-1); the compact rows with replay copies,
+    # ascending, hold consecutive slots in ascending packed order
     real = np.nonzero(t["rows"] >= 0)[0]
-    assert np.array_equal(np.sort(t["pos"]), real)
-    for r in range(plan["C"]):
-        p = t["pos"][t["off"][r]:t["off"][r + 1]]
-        assert np.all(np.diff(p) > 0) and np.all(t["rows"][p] // 2 == r)
-        assert np.sum(t["rows"][p] & 1) == 1          # one own position per compact row
+    owner = t["rows"][real] // 2
+    count = np.bincount(owner, minlength=plan["C"])
+    assert np.all(count >= 1)
+    assert np.all(np.bincount(owner[(t["rows"][real] & 1) == 1], minlength=plan["C"]) == 1)   # one own row each
+    multi = np.nonzero(count > 1)[0]
+    assert sz.n_multi == len(multi) == len(np.unique(plan["replay_row"]))
+    assert np.array_equal(t["mrow"][:sz.n_multi], multi)
+    assert t["moff"][0] == 0 and np.array_equal(np.diff(t["moff"]), count[multi]) and t["moff"][-1] == sz.n_slots
+    assert np.all(t["slot"][real][count[owner] == 1] == -1)
+    for m, r in enumerate(multi):
+        p = real[owner == r]                              # ascending packed positions
+        assert np.array_equal(t["slot"][p], np.arange(t["moff"][m], t["moff"][m + 1]))
 
 
 def execute_tables(plan, t, q, k, v, g, beta, S0_tree, scale):
