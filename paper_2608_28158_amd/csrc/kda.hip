@@ -971,8 +971,10 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  RowPre<T, D> pk;                 // k requested together with g
+  pk.load(k, ent, H, h, t);
   load_decay<D, LG>(sG, sb, sTot, g, beta, ent, H, h, t);
-  load_rows<T, D, LK>(sKG, k, ent, H, h, t);
+  pk.template store<LK>(sKG, t);
   __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
@@ -1062,14 +1064,36 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  load_rows<T, D, D>(sK, k, ent, H, h, t);
-  load_rows<T, D, D>(sQ, q, ent, H, h, t);
-  load_rows<float, D, D>(sG, g, ent, H, h, t);
-  if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
-  for (int p = t; p < KB * KB; p += KT) {
-    sL[(p / KB) * LB + p % KB] = w[Y::LINV + p];
-    sT[(p / KB) * LB + p % KB] = w[Y::DUV + p];          // dTm
+  // every input tile requested at once: k, q, g, L^{-1} and dTm for now, At
+  // and dM (held in registers) for the later phases
+  constexpr int NP = KB * KB / 4 / KT;                     // float4 of a 64 x 64 tile per thread
+  RowPre<T, D> pk, pq;
+  RowPre<float, D> pg;
+  f32x4 pL[NP], pT[NP], pA[NP], pM[NP];
+  pk.load(k, ent, H, h, t);
+  pq.load(q, ent, H, h, t);
+  pg.load(g, ent, H, h, t);
+#pragma unroll
+  for (int n = 0; n < NP; ++n) {
+    const int e = 4 * (t + KT * n);
+    pL[n] = *reinterpret_cast<const f32x4*>(w + Y::LINV + e);
+    pT[n] = *reinterpret_cast<const f32x4*>(w + Y::DUV + e);
+    pA[n] = *reinterpret_cast<const f32x4*>(w + Y::AT + e);
+    pM[n] = *reinterpret_cast<const f32x4*>(w + Y::DM + e);
   }
+  const auto put64 = [&](float* dst, const f32x4* src) {
+#pragma unroll
+    for (int n = 0; n < NP; ++n) {
+      const int e = 4 * (t + KT * n);
+      *reinterpret_cast<f32x4*>(dst + (e / KB) * LB + e % KB) = src[n];
+    }
+  };
+  if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
+  pk.template store<D>(sK, t);
+  pq.template store<D>(sQ, t);
+  pg.template store<D>(sG, t);
+  put64(sL, pL);
+  put64(sT, pT);                                           // dTm
   __syncthreads();
   cumsum_rows<D, D>(sG, sTot, t);                          // cumulative sums of g per channel
   // dbeta_j from Tm = L^{-1} Diag(beta): sum_i dTm[i][j] L^{-1}[i][j]
@@ -1122,7 +1146,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     }
   }
   __syncthreads();
-  for (int p = t; p < KB * KB; p += KT) sY[(p / KB) * LB + p % KB] = w[Y::AT + p];   // Y is done: At into its tile
+  put64(sY, pA);                                           // Y is done: At into its tile
   __syncthreads();
   if (t < KB) {
     float a = 0.f;
@@ -1133,8 +1157,8 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
     sT[i * LB + j] *= sb[i];                                // dAt
-    sL[i * LB + j] = w[Y::DM + p];                          // dM
   }
+  put64(sL, pM);                                           // dM
   __syncthreads();
   // Pairwise terms, one tile of TRW rows x 4 channels per thread.  With
   // e_ij = e^{G_i - G_j} per channel:
