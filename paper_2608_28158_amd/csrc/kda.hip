@@ -239,7 +239,7 @@ __device__ inline int mid_index(int I, int J) { return I == J + 1 ? -1 : (I == 2
 // exchanges).  Pairs across blocks: one 16 x 16 block of At or M per
 // wave on float32 MFMA (k = channel).
 template <int D, int LD, int LT>
-__device__ inline void pair_sums(float* sA, float* __restrict__ gM, float* sK, float* sQ, const float* sG, float* sX,
+__device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, float* sK, float* sQ, const float* sG, float* sX,
                                  float* sMid, int t) {
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
