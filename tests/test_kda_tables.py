@@ -150,3 +150,32 @@ def test_tables_reject_plans_of_another_chunk():
     plan = HartsPlan([-1, 0], [40, 20], 32)
     sz = _lib.KdaSizes()
     assert _lib.lib().harts_kda_layout(plan.handle, C.byref(sz)) == _lib.HARTS_EUNSUPPORTED
+
+
+def test_kda_entry_points_reject_bad_arguments():
+    """Argument checks of the device entry points, which return before any
+    GPU call: unsupported dtype or width, missing tables, misaligned gradient
+    outputs, bad reduction arguments; empty work returns HARTS_OK."""
+    from paper_2608_28158_amd import _lib
+    L = _lib.lib()
+    buf = np.zeros(4096, np.float32)
+    p = buf.ctypes.data + (16 - buf.ctypes.data % 16) % 16         # 16-byte aligned host address
+    tabs = np.zeros(64, np.int32).ctypes.data
+
+    def bwd(dtype=_lib.HARTS_BF16, d=128, slot=tabs, dq=p):
+        ptrs = [p] * 10
+        return L.harts_kda_bwd(tabs, tabs, tabs, slot, 0, 1, 0, 1, dtype, 2, d, C.c_float(1.0),
+                               p, p, p, p, p, p, p, p, p, p, dq, p, p, p, p, *ptrs[:5], None)
+
+    assert bwd(dtype=7) == _lib.HARTS_EUNSUPPORTED
+    assert bwd(d=96) == _lib.HARTS_EUNSUPPORTED
+    assert bwd(slot=None) == _lib.HARTS_EINVAL
+    assert bwd(dq=p + 4) == _lib.HARTS_EINVAL
+    assert b"16-byte aligned" in L.harts_last_error()
+    red = lambda n, w, dt=_lib.HARTS_F32, src=p: L.harts_kda_reduce(src, tabs, tabs, n, w, dt, p, None)
+    assert red(0, 8) == _lib.HARTS_OK                              # nothing to sum: no launch
+    assert red(3, 0) == _lib.HARTS_EINVAL
+    assert red(3, 8, dt=5) == _lib.HARTS_EINVAL
+    assert red(3, 8, src=None) == _lib.HARTS_EINVAL
+    assert L.harts_kda_bank_add(tabs, 0, 0, tabs, 16, p, p, None) == _lib.HARTS_OK
+    assert L.harts_kda_bank_add(tabs, 0, -1, tabs, 16, p, p, None) == _lib.HARTS_EINVAL
