@@ -30,6 +30,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 #include <string>
 
 #include "harts.h"
@@ -585,60 +586,68 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
   for (int x = 0; x < ST; ++x)
 #pragma unroll
     for (int r = 0; r < 4; ++r) Sa[x][r] = sS[(16 * sti + 4 * lk + r) * L::LS + 16 * (stv + x) + li];
-  // register prefetch of one chunk (P and P2 in the accumulator layout)
-  f32x4 pA1[NA], pA2[NA], pg = {0.f, 0.f, 0.f, 0.f};
-  float pP[XT][4], pP2[ST][4];
-  auto fetch = [&](int cc) __attribute__((always_inline)) {
+  // Register prefetch two chunks ahead in two sets (P and P2 in the
+  // accumulator layout).  Every load is unconditional (past the sequence's
+  // end its last chunk is requested again), so the count of outstanding
+  // loads is the same on every path and the wait before a set is staged
+  // leaves the other set's loads in flight.
+  f32x4 pA1[2][NA], pA2[2][NA], pg[2];
+  float pP[2][XT][4], pP2[2][ST][4];
+  const auto chunk_of = [&](int step) { return REV ? nc - 1 - step : step; };
+  const auto fetch = [&](auto set, int step) __attribute__((always_inline)) {
+    constexpr int Z = decltype(set)::value;
+    const int cc = chunk_of(step < nc ? step : nc - 1);
     const float* w = ws + (static_cast<int64_t>(c_first + cc) * H + h) * Y::ALL;
 #pragma unroll
     for (int n = 0; n < NA; ++n) {
-      pA1[n] = *reinterpret_cast<const f32x4*>(w + OA1 + 4 * (t + KT * n));
-      pA2[n] = *reinterpret_cast<const f32x4*>(w + OA2 + 4 * (t + KT * n));
+      pA1[Z][n] = *reinterpret_cast<const f32x4*>(w + OA1 + 4 * (t + KT * n));
+      pA2[Z][n] = *reinterpret_cast<const f32x4*>(w + OA2 + 4 * (t + KT * n));
     }
 #pragma unroll
     for (int x = 0; x < XT; ++x)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) pP[x][r] = w[OP + (16 * xti + 4 * lk + r) * D + v0 + 16 * (xtv + x) + li];
+      for (int r = 0; r < 4; ++r) pP[Z][x][r] = w[OP + (16 * xti + 4 * lk + r) * D + v0 + 16 * (xtv + x) + li];
 #pragma unroll
     for (int x = 0; x < ST; ++x)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        pP2[x][r] = REV ? w[Y::DSO + (16 * sti + 4 * lk + r) * D + v0 + 16 * (stv + x) + li] : 0.f;
-    if (t < D / 4) pg = *reinterpret_cast<const f32x4*>(w + Y::GAM + 4 * t);
+        pP2[Z][x][r] = REV ? w[Y::DSO + (16 * sti + 4 * lk + r) * D + v0 + 16 * (stv + x) + li] : 0.f;
+    pg[Z] = *reinterpret_cast<const f32x4*>(w + Y::GAM + 4 * (t % (D / 4)));
   };
-  if (nc > 0) fetch(REV ? nc - 1 : 0);
   int rq = 0;
-  for (int step = 0; step <= nc; ++step) {
-    const int cc = REV ? nc - 1 - step : step;
-    if (!REV) {      // requested states at the start of chunk cc (cc == nc: the end)
-      for (; rq < nr && req_tab[2 * (ro + rq)] <= cc; ++rq) {
-        if (req_tab[2 * (ro + rq)] != cc) continue;
-        float* dst = bank + (static_cast<int64_t>(req_tab[2 * (ro + rq) + 1]) * H + h) * Y::DD + v0;
-        for (int idx = t; idx < D * SV; idx += KT) dst[(idx / SV) * D + idx % SV] = sS[(idx / SV) * L::LS + idx % SV];
-      }
+  // forward: the states requested at the start of chunk cc (cc == nc: the end)
+  const auto requests = [&](int cc) {
+    if (REV) return;
+    for (; rq < nr && req_tab[2 * (ro + rq)] <= cc; ++rq) {
+      if (req_tab[2 * (ro + rq)] != cc) continue;
+      float* dst = bank + (static_cast<int64_t>(req_tab[2 * (ro + rq) + 1]) * H + h) * Y::DD + v0;
+      for (int idx = t; idx < D * SV; idx += KT) dst[(idx / SV) * D + idx % SV] = sS[(idx / SV) * L::LS + idx % SV];
     }
-    if (step == nc) break;
+  };
+  const auto chunk = [&](auto set, int step) __attribute__((always_inline)) {
+    constexpr int Z = decltype(set)::value;
+    const int cc = chunk_of(step);
+    requests(cc);
     float* w = ws + (static_cast<int64_t>(c_first + cc) * H + h) * Y::ALL;
     // this chunk's operands into LDS, the running state to the workspace
 #pragma unroll
     for (int n = 0; n < NA; ++n) {
       const int e = 4 * (t + KT * n), r = e / D, c = e % D;
-      *reinterpret_cast<f32x4*>(sA1 + r * L::LA1 + c) = pA1[n];
-      *reinterpret_cast<f32x4*>(sA2 + r * L::LA2 + c) = pA2[n];
+      *reinterpret_cast<f32x4*>(sA1 + r * L::LA1 + c) = pA1[Z][n];
+      *reinterpret_cast<f32x4*>(sA2 + r * L::LA2 + c) = pA2[Z][n];
     }
-    if (t < D / 4) *reinterpret_cast<f32x4*>(sg + 4 * t) = pg;
+    if (t < D / 4) *reinterpret_cast<f32x4*>(sg + 4 * t) = pg[Z];
     f32x4 acc[XT], sacc[ST];
 #pragma unroll
-    for (int x = 0; x < XT; ++x) acc[x] = f32x4{pP[x][0], pP[x][1], pP[x][2], pP[x][3]};
+    for (int x = 0; x < XT; ++x) acc[x] = f32x4{pP[Z][x][0], pP[Z][x][1], pP[Z][x][2], pP[Z][x][3]};
 #pragma unroll
-    for (int x = 0; x < ST; ++x) sacc[x] = f32x4{pP2[x][0], pP2[x][1], pP2[x][2], pP2[x][3]};
+    for (int x = 0; x < ST; ++x) sacc[x] = f32x4{pP2[Z][x][0], pP2[Z][x][1], pP2[Z][x][2], pP2[Z][x][3]};
     for (int idx = t; idx < D * SV / 4; idx += KT) {
       const int r = (4 * idx) / SV, c = (4 * idx) % SV;
       *reinterpret_cast<float4*>(w + OSC + r * D + v0 + c) = *reinterpret_cast<const float4*>(sS + r * L::LS + c);
     }
     __syncthreads();
-    const int nxt = REV ? cc - 1 : cc + 1;
-    if (nxt >= 0 && nxt < nc) fetch(nxt);
+    fetch(set, step + 2);
     // Xc = P + s1 A1 Sc
 #pragma unroll 4
     for (int s = 0; s < D / 4; ++s) {
@@ -682,7 +691,20 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
       for (int r = 0; r < 4; ++r) sS[(16 * sti + 4 * lk + r) * L::LS + 16 * (stv + x) + li] = sacc[x][r];
     }
     __syncthreads();
+  };
+  using Z0 = std::integral_constant<int, 0>;
+  using Z1 = std::integral_constant<int, 1>;
+  if (nc > 0) {
+    fetch(Z0{}, 0);
+    fetch(Z1{}, 1);
+    int step = 0;
+    for (; step + 1 < nc; step += 2) {     // pairs of chunks: both sets in every iteration
+      chunk(Z0{}, step);
+      chunk(Z1{}, step + 1);
+    }
+    if (step < nc) chunk(Z0{}, step);
   }
+  requests(nc);
   float* dst = REV ? dS0_seq + (static_cast<int64_t>(seq) * H + h) * Y::DD + v0
                    : (S_final ? S_final + (static_cast<int64_t>(leaf) * H + h) * Y::DD + v0 : nullptr);
   if (dst)
