@@ -220,7 +220,8 @@ __device__ inline f32x4 mfma4(float a, float b, f32x4 c) { return __builtin_amdg
 //   e^{G_i - G_j} = e^{G_i - G_{r_I}} e^{G_{r_I} - G_{r_{J+1}}} e^{G_{r_{J+1}} - G_j},
 // each at most 1 (G does not increase along the chunk), so a product that
 // underflows stands for a term below the float range anyway.  Pairs inside
-// a block take the exact e^{G_i - G_j} per channel.  The factors of the
+// a block factor through r_I alone where that is safe (KF_RANGE below) and
+// take the exact e^{G_i - G_j} per channel elsewhere.  The factors of the
 // blocks: Kf_J = K_J e^{G_{r_{J+1}} - G_J} (J < 3), Kd_I = K_I e^{G_I - G_{r_I}}
 // and Qd_I = Q_I e^{G_I - G_{r_I}} (I > 0), and per channel the middle factors
 // of the pairs that are not adjacent, mid(2, 0) = e^{G_32 - G_16},
@@ -230,29 +231,73 @@ constexpr int PB = 16;   // rows per block of the pairwise factorization
 // Middle factor index of block pair (I, J), I > J: -1 for adjacent blocks.
 __device__ inline int mid_index(int I, int J) { return I == J + 1 ? -1 : (I == 2 ? 0 : (J == 0 ? 1 : 2)); }
 
+// Pairs inside a block factor through its first row as well,
+//   e^{G_i - G_j} = e^{G_i - G_{r_I}} e^{G_{r_I} - G_j}   (i, j in block I),
+// a factor at most 1 times one at least 1, wherever the channel's decay over
+// the block's 16 rows, G_{r_I} - G_{r_I + 15}, is at most KF_RANGE: then
+// neither factor leaves the normal float range (e^{-60} > 2^{-87}) and the
+// in-block pairs become plain products on MFMA.  A (block, channel) with a
+// larger range is "wide": its in-block pairs are left out of the products
+// and summed with the exact per-pair exponential instead.
+constexpr float KF_RANGE = 60.f;
+
+// Wide flags of the four blocks: bit d of word (I D + d) / 32 for channel d
+// of block I, from the cumulative log-decays sG (row stride LD).  Every
+// thread calls it; it returns whether any (block, channel) of the chunk is
+// wide (the call synchronises the workgroup).
+template <int D, int LD>
+__device__ inline bool wide_flags(uint32_t* sWide, const float* sG, int t) {
+  static_assert(4 * D <= KT && (4 * D) % 64 == 0 && (4 * D / 32) % 4 == 0, "one (block, channel) per thread, whole waves");
+  if (t < 4 * D) {
+    const int I = t / D, d = t % D;
+    const uint64_t m = __ballot(sG[PB * I * LD + d] - sG[(PB * I + PB - 1) * LD + d] > KF_RANGE);
+    if ((t & 63) == 0) {
+      sWide[t / 32] = static_cast<uint32_t>(m);
+      sWide[t / 32 + 1] = static_cast<uint32_t>(m >> 32);
+    }
+  }
+  __syncthreads();
+  uint32_t any = 0;
+#pragma unroll
+  for (int x = 0; x < 4 * D / 32; x += 4) {
+    const uint4 u = *reinterpret_cast<const uint4*>(sWide + x);
+    any |= u.x | u.y | u.z | u.w;
+  }
+  return any != 0;
+}
+template <int D>
+__device__ inline bool is_wide(const uint32_t* sWide, int I, int d) {
+  const int b = I * D + d;
+  return (sWide[b >> 5] >> (b & 31)) & 1u;
+}
+
 // sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and gM (the
 // workspace) [i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere);
-// sK, sQ and sG have row stride LD, sA LT.  sK and sQ are overwritten with
-// the block factors (Kf_0..2 in sK rows 0..47 and Kd_3 in rows 48..63; Kd_1
-// in sQ rows 0..15, Qd_1..3 in its rows 16..63; Kd_2 in sX, 16 rows of
-// stride LD); sMid holds 3 x D middle factors.  Pairs inside the blocks:
-// 4 x 4 tiles with the channels dealt over 16 adjacent lanes (summed by lane
-// exchanges).  Pairs across blocks: one 16 x 16 block of At or M per
-// wave on float32 MFMA (k = channel).
+// sK, sQ and sG have row stride LD, sA and sX LT; sX (64 x 64) is scratch,
+// sMid holds 3 x D middle factors, sWide the wide flags.  K, Q and G are
+// left as they are.  All block pairs run on float32 MFMA (k = channel), the
+// operands' exponential factors formed as they are read: one (block pair,
+// At and M) per wave.  The in-block pairs of wide channels are summed
+// exactly first (4 x 4 tiles with the channels dealt over 16 adjacent lanes,
+// summed by lane exchanges) and added to the products.
 template <int D, int LD, int LT>
-__device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, float* sK, float* sQ, const float* sG, float* sX,
-                                 float* sMid, int t) {
+__device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, const float* sK, const float* sQ,
+                                          const float* sG, float* sX, float* sMid, uint32_t* sWide, int t) {
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
     sA[i * LT + j] = 0.f;
+    sX[i * LT + j] = 0.f;
     if (j > i) gM[p] = 0.f;
   }
-  __syncthreads();
-  // pairs inside the blocks, exact: tile (block, ti >= tj), channels
-  // de, de + 16, .. (adjacent lanes read adjacent channels: with the row
-  // stride of 4 (mod 64 banks) the four row tiles of a wave fall in
-  // different banks)
-  {
+  if (t < 3 * D) {
+    const int x = t / D, d = t % D;
+    const int ri = x == 0 ? 2 * PB : 3 * PB, rj = x == 2 ? 2 * PB : PB;
+    sMid[t] = __expf(sG[ri * LD + d] - sG[rj * LD + d]);
+  }
+  const bool any_wide = wide_flags<D, LD>(sWide, sG, t);
+  if (any_wide) {
+    // the wide channels' in-block pairs, exact: tile (block, ti >= tj),
+    // channels de, de + 16, .. (At into sA, M into sX)
     constexpr int NE = 16, DE = D / NE, NIT = 4 * 10 * NE;
     for (int it = t; it < ((NIT + 63) / 64) * 64; it += KT) {
       const bool live = it < NIT;
@@ -268,9 +313,9 @@ __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, flo
 #pragma unroll
         for (int cc = 0; cc < 4; ++cc) a[r][cc] = m[r][cc] = 0.f;
       if (live) {
-#pragma unroll 2
         for (int dd = 0; dd < DE; ++dd) {
           const int d = dd * NE + de;
+          if (!is_wide<D>(sWide, blk, d)) continue;
           float ki[4], qi[4], gi[4], kj[4], gj[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -306,53 +351,52 @@ __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, flo
           for (int cc = 0; cc < 4; ++cc) {
             const int i = i0 + r, j = j0 + cc;
             if (j < i) sA[i * LT + j] = a[r][cc];
-            if (j <= i) gM[i * KB + j] = m[r][cc];
+            if (j <= i) sX[i * LT + j] = m[r][cc];
           }
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
-  // the block factors, in place (each element read and written by one thread)
-  for (int idx = t; idx < KB * D; idx += KT) {
-    const int r = idx / D, d = idx % D, blk = r / PB;
-    const float G = sG[r * LD + d], k = sK[r * LD + d];
-    if (blk < 3) sK[r * LD + d] = k * __expf(sG[PB * (blk + 1) * LD + d] - G);   // Kf
-    if (blk > 0) {
-      const float e = __expf(G - sG[PB * blk * LD + d]);
-      const float kd = k * e;
-      if (blk == 1) sQ[(r - PB) * LD + d] = kd;
-      else if (blk == 2) sX[(r - 2 * PB) * LD + d] = kd;
-      else sK[r * LD + d] = kd;
-      sQ[r * LD + d] *= e;                                                         // Qd
-    }
-  }
-  if (t < 3 * D) {
-    const int x = t / D, d = t % D;
-    const int ri = x == 0 ? 2 * PB : 3 * PB, rj = x == 2 ? 2 * PB : PB;
-    sMid[t] = __expf(sG[ri * LD + d] - sG[rj * LD + d]);
-  }
-  __syncthreads();
-  // pairs across blocks: output o = (block pair o / 2, At or M), one per wave
+  // Block pair o (I >= J): o < 4 in-block (I = J = o), else the six pairs
+  // across blocks.  At and M of a pair share their B operand:
+  //   in-block  A = K_I e^{G_I - G_{r_I}} (Q_I ..),  B = K_I e^{G_{r_I} - G_I} (0 where wide)
+  //   across    A = K_I e^{G_I - G_{r_I}} (Q_I ..),  B = K_J e^{G_{r_{J+1}} - G_J} mid(I, J)
   {
     const int lane = t & 63, li = lane & 15, lk = lane >> 4;
-    for (int o = t >> 6; o < 12; o += KT / 64) {
-      const int bp = o >> 1, isM = o & 1;
-      const int I = bp == 0 ? 1 : (bp < 3 ? 2 : 3), J = bp - (I * (I - 1)) / 2;
-      const float* ar = isM ? sQ + PB * I * LD : (I == 1 ? sQ : (I == 2 ? sX : sK + 3 * PB * LD));
-      const float* br = sK + PB * J * LD;
-      const int mi = mid_index(I, J);
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int o = t >> 6; o < 10; o += KT / 64) {
+      int I, J;
+      if (o < 4) I = J = o;
+      else {
+        const int bp = o - 4;
+        I = bp == 0 ? 1 : (bp < 3 ? 2 : 3);
+        J = bp - (I * (I - 1)) / 2;
+      }
+      const bool in = I == J;
+      const int mi = in ? -1 : mid_index(I, J);
+      const int ri = PB * I + li, rj = PB * J + li, rb = in ? PB * I : PB * (J + 1);
+      f32x4 accA = {0.f, 0.f, 0.f, 0.f}, accM = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
       for (int s4 = 0; s4 < D / 4; ++s4) {
         const int k = 4 * s4 + lk;
-        const float md = mi >= 0 ? sMid[mi * D + k] : 1.f;
-        acc = mfma4(ar[li * LD + k], br[li * LD + k] * md, acc);
+        const float gI = sG[PB * I * LD + k];
+        const float x = __expf(sG[ri * LD + k] - gI);
+        float bf = __expf(sG[rb * LD + k] - sG[rj * LD + k]);
+        if (in) bf = is_wide<D>(sWide, I, k) ? 0.f : bf;
+        else if (mi >= 0) bf *= sMid[mi * D + k];
+        const float b = sK[rj * LD + k] * bf;
+        accA = mfma4(sK[ri * LD + k] * x, b, accA);
+        accM = mfma4(sQ[ri * LD + k] * x, b, accM);
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = PB * I + 4 * lk + r, j = PB * J + li;
-        if (isM) gM[i * KB + j] = acc[r];
-        else sA[i * LT + j] = acc[r];
+        if (in) {
+          if (j < i) sA[i * LT + j] += accA[r];
+          if (j <= i) gM[i * KB + j] = accM[r] + sX[i * LT + j];
+        } else {
+          sA[i * LT + j] = accA[r];
+          gM[i * KB + j] = accM[r];
+        }
       }
     }
   }
@@ -414,7 +458,7 @@ template <int D>
 struct PrepLds {
   static constexpr int LD = D + 4, LW = D + 16, LT = KB + 4;
   static constexpr int K = 0, Q = K + KB * LW, G = Q + KB * LW, A = G + KB * LD, L = A + KB * LT, B = L + KB * LT,
-                       MID = B + KB, TOT = MID + 3 * D, ALL = TOT + KT;
+                       MID = B + KB, TOT = MID + 3 * D, WIDE = TOT + KT, ALL = WIDE + 4 * D / 32;
 };
 
 // ---------------------------------------------------------------------------
@@ -437,6 +481,7 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   float* sb = sm + P::B;
   float* sMid = sm + P::MID;
   float* sTot = sm + P::TOT;
+  uint32_t* sWide = reinterpret_cast<uint32_t*>(sm + P::WIDE);
   const int c = static_cast<int>(blockIdx.x / H) + static_cast<int>(c0), h = blockIdx.x % H;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -460,7 +505,7 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   }
   if (t < D) w[Y::GAM + t] = __expf(sG[(KB - 1) * LD + t]);
   // At into sA and the workspace, M into the workspace
-  pair_sums<D, LD, LT>(sA, w + Y::M, sK, sQ, sG, sL, sMid, t);
+  pair_sums<D, LD, LT>(sA, w + Y::M, sK, sQ, sG, sL, sMid, sWide, t);
   __syncthreads();
   for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * LT + p % KB];
   tri_inverse<LT>(sL, sQ, sA, sb, t);          // the Q tile is free now: scratch
@@ -1082,6 +1127,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   float* sdb = sb + KB;            // [64] dbeta
   float* sMid = sdb + KB;          // [3][D] middle factors
   float* sTot = sMid + 3 * D;      // [2][KT] scan totals
+  uint32_t* sWide = reinterpret_cast<uint32_t*>(sTot + 2 * KT);   // [4 D / 32] wide flags
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
@@ -1182,23 +1228,28 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   }
   put64(sL, pM);                                           // dM
   __syncthreads();
-  // Pairwise terms, one tile of TRW rows x 4 channels per thread.  With
-  // e_ij = e^{G_i - G_j} per channel:
+  // Pairwise terms.  With e_ij = e^{G_i - G_j} per channel:
   //   row terms     R1_i = sum_{j <= i} dM_ij e_ij k_j      (dq),
   //                 R2_i = sum_{j < i} dAt_ij e_ij k_j      (dk),
   //   column terms  C1_j = sum_{i >= j} e_ij (dAt_ij k_i + dM_ij q_i)   (dk),
-  // and dG_i gets k_i R2_i + q_i R1_i - k_i C1_i.  Pairs inside a 16-row block
-  // take e_ij exactly; pairs across blocks go through the block factors
-  // (Kf, Kd, Qd and the middle factors, as in the preparation), which turns
-  // them into plain products whose row (column) factor e^{G_i - G_{r_I}}
-  // (e^{G_{r_{J+1}} - G_j}) is applied once at the end.
+  // and dG_i gets k_i R2_i + q_i R1_i - k_i C1_i.  They run on float32 MFMA
+  // (k = the summed row) with the factorization of the preparation, the
+  // operands' factors formed as they are read:
+  //   R of block I = e^{G_i - G_{r_I}} x (dM, dAt)_{I,J} B_J, with
+  //     B_J = K_J e^{G_{r_{J+1}} - G_J} mid(I, J) (J < I), K_I e^{G_{r_I} - G_I} (J = I, 0 where wide);
+  //   C of block J = e^{G_{r_J} - G_j} (0 where wide) x the in-block products
+  //     + e^{G_{r_{J+1}} - G_j} x those across blocks, with the transposed
+  //     (dAt, dM) blocks and B = (K_I, Q_I) e^{G_I - G_{r_I}} mid(I, J).
+  // Wave w owns 16 channels (both kinds at d = 128, one at d = 64).  The
+  // in-block pairs of wide channels are summed exactly first, one tile of
+  // TRW rows x 4 channels per thread, which then takes the elementwise terms.
   {
     constexpr int TRW = KB * (D / 4) / KT;   // rows per thread tile
     constexpr int NCT = D / 4;               // channel tiles
     static_assert(TRW >= 1 && (KB / TRW) * NCT == KT && PB % TRW == 0, "one tile per thread");
     const int i0 = (t / NCT) * TRW, d0 = (t % NCT) * 4, I = i0 / PB;
-    float kr[TRW][4], qr[TRW][4], gr[TRW][4];
-    float rd1[TRW][4], rd2[TRW][4], cd[TRW][4], z1[TRW][4], z2[TRW][4], zc[TRW][4];
+    float kr[TRW][4], qr[TRW][4];
+    float rd1[TRW][4], rd2[TRW][4], cd[TRW][4];
     const auto f4 = [](const float* p, float* x) {
       const float4 u = *reinterpret_cast<const float4*>(p);
       x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
@@ -1207,127 +1258,171 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     for (int r = 0; r < TRW; ++r) {
       f4(sK + (i0 + r) * D + d0, kr[r]);
       f4(sQ + (i0 + r) * D + d0, qr[r]);
-      f4(sG + (i0 + r) * D + d0, gr[r]);
 #pragma unroll
-      for (int cc = 0; cc < 4; ++cc) rd1[r][cc] = rd2[r][cc] = cd[r][cc] = z1[r][cc] = z2[r][cc] = zc[r][cc] = 0.f;
-    }
-    // inside the block, exact: rows i0.. with columns j <= i, then the own
-    // rows as columns j with rows i >= j
-    for (int j = PB * I; j < i0 + TRW; ++j) {
-      float kj[4], gj[4];
-      f4(sK + j * D + d0, kj);
-      f4(sG + j * D + d0, gj);
-#pragma unroll
-      for (int r = 0; r < TRW; ++r) {
-        const bool on = j <= i0 + r;
-        const float m = on ? sL[(i0 + r) * LB + j] : 0.f, a = on ? sT[(i0 + r) * LB + j] : 0.f;
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          const float e = __expf(fminf(gr[r][cc] - gj[cc], 0.f)) * kj[cc];
-          rd1[r][cc] += m * e;
-          rd2[r][cc] += a * e;
-        }
-      }
-    }
-    for (int ip = i0; ip < PB * (I + 1); ++ip) {
-      float ki[4], qi[4], gi[4];
-      f4(sK + ip * D + d0, ki);
-      f4(sQ + ip * D + d0, qi);
-      f4(sG + ip * D + d0, gi);
-#pragma unroll
-      for (int r = 0; r < TRW; ++r) {
-        const bool on = ip >= i0 + r;
-        const float a = on ? sT[ip * LB + i0 + r] : 0.f, m = on ? sL[ip * LB + i0 + r] : 0.f;
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) cd[r][cc] += __expf(fminf(gi[cc] - gr[r][cc], 0.f)) * (a * ki[cc] + m * qi[cc]);
-      }
-    }
-    __syncthreads();
-    // the block factors in place: Kf_0..2 and Kd_3 in sK, Kd_1 in sQ rows
-    // 0..15 (its raw rows are no longer read), Qd_1..3 in sQ, Kd_2 in sY
-    for (int idx = t; idx < KB * D; idx += KT) {
-      const int r = idx / D, d = idx % D, blk = r / PB;
-      const float G = sG[idx], k_ = sK[idx];
-      if (blk < 3) sK[idx] = k_ * __expf(sG[PB * (blk + 1) * D + d] - G);
-      if (blk > 0) {
-        const float e = __expf(G - sG[PB * blk * D + d]);
-        if (blk == 1) sQ[idx - PB * D] = k_ * e;
-        else if (blk == 2) sY[idx - 2 * PB * D] = k_ * e;
-        else sK[idx] = k_ * e;
-        sQ[idx] *= e;
-      }
+      for (int cc = 0; cc < 4; ++cc) rd1[r][cc] = rd2[r][cc] = cd[r][cc] = 0.f;
     }
     if (t < 3 * D) {
       const int x = t / D, d = t % D;
       const int ri = x == 0 ? 2 * PB : 3 * PB, rj = x == 2 ? 2 * PB : PB;
       sMid[t] = __expf(sG[ri * D + d] - sG[rj * D + d]);
     }
-    __syncthreads();
-    // across blocks: earlier blocks J as columns of the own rows ...
-    for (int J = 0; J < I; ++J) {
-      const int mi = mid_index(I, J);
-      float md[4] = {1.f, 1.f, 1.f, 1.f};
-      if (mi >= 0) f4(sMid + mi * D + d0, md);
-      for (int j = PB * J; j < PB * (J + 1); ++j) {
-        float kf[4];
-        f4(sK + j * D + d0, kf);
+    if (wide_flags<D, D>(sWide, sG, t)) {
+      // inside the block, exact for the wide channels: rows i0.. with
+      // columns j <= i, then the own rows as columns j with rows i >= j
+      float wm[4];
 #pragma unroll
-        for (int cc = 0; cc < 4; ++cc) kf[cc] *= md[cc];
+      for (int cc = 0; cc < 4; ++cc) wm[cc] = is_wide<D>(sWide, I, d0 + cc) ? 1.f : 0.f;
+      float gr[TRW][4];
+#pragma unroll
+      for (int r = 0; r < TRW; ++r) f4(sG + (i0 + r) * D + d0, gr[r]);
+      for (int j = PB * I; j < i0 + TRW; ++j) {
+        float kj[4], gj[4];
+        f4(sK + j * D + d0, kj);
+        f4(sG + j * D + d0, gj);
 #pragma unroll
         for (int r = 0; r < TRW; ++r) {
-          const float m = sL[(i0 + r) * LB + j], a = sT[(i0 + r) * LB + j];
+          const bool on = j <= i0 + r;
+          const float m = on ? sL[(i0 + r) * LB + j] : 0.f, a = on ? sT[(i0 + r) * LB + j] : 0.f;
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
-            z1[r][cc] += m * kf[cc];
-            z2[r][cc] += a * kf[cc];
+            const float e = wm[cc] * __expf(fminf(gr[r][cc] - gj[cc], 0.f)) * kj[cc];
+            rd1[r][cc] += m * e;
+            rd2[r][cc] += a * e;
           }
         }
       }
-    }
-    // ... and later blocks I' as rows of the own columns
-    for (int Ip = I + 1; Ip < 4; ++Ip) {
-      const int mi = mid_index(Ip, I);
-      float md[4] = {1.f, 1.f, 1.f, 1.f};
-      if (mi >= 0) f4(sMid + mi * D + d0, md);
-      const float* kd = Ip == 1 ? sQ : (Ip == 2 ? sY : sK + 3 * PB * D);
-      const float* qd = sQ + PB * Ip * D;
-      for (int x = 0; x < PB; ++x) {
-        const int ip = PB * Ip + x;
-        float kv[4], qv[4];
-        f4(kd + x * D + d0, kv);
-        f4(qd + x * D + d0, qv);
-#pragma unroll
-        for (int cc = 0; cc < 4; ++cc) {
-          kv[cc] *= md[cc];
-          qv[cc] *= md[cc];
-        }
+      for (int ip = i0; ip < PB * (I + 1); ++ip) {
+        float ki[4], qi[4], gi[4];
+        f4(sK + ip * D + d0, ki);
+        f4(sQ + ip * D + d0, qi);
+        f4(sG + ip * D + d0, gi);
 #pragma unroll
         for (int r = 0; r < TRW; ++r) {
-          const float a = sT[ip * LB + i0 + r], m = sL[ip * LB + i0 + r];
+          const bool on = ip >= i0 + r;
+          const float a = on ? sT[ip * LB + i0 + r] : 0.f, m = on ? sL[ip * LB + i0 + r] : 0.f;
 #pragma unroll
-          for (int cc = 0; cc < 4; ++cc) zc[r][cc] += a * kv[cc] + m * qv[cc];
+          for (int cc = 0; cc < 4; ++cc)
+            cd[r][cc] += wm[cc] * __expf(fminf(gi[cc] - gr[r][cc], 0.f)) * (a * ki[cc] + m * qi[cc]);
         }
       }
     }
-    // row and column factors, then the elementwise terms of the own tile
-    float gb[4], gI[4] = {0.f, 0.f, 0.f, 0.f}, gJ[4] = {0.f, 0.f, 0.f, 0.f};
+    const int lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
+    constexpr int NT16 = D / 16;
+    static_assert(NT16 == KT / 64 || 2 * NT16 == KT / 64, "one or both kinds of terms per wave");
+    const bool doR = NT16 == KT / 64 || wv < NT16, doC = NT16 == KT / 64 || wv >= NT16;
+    const int d = 16 * (wv % NT16) + li;
+    f32x4 r1v[4], r2v[4], cv[4];
+    if (doR) {
+#pragma unroll
+      for (int Ib = 0; Ib < 4; ++Ib) {
+        f32x4 a1 = {0.f, 0.f, 0.f, 0.f}, a2 = {0.f, 0.f, 0.f, 0.f};
+        const float gRI = sG[PB * Ib * D + d];
+        const int ri = PB * Ib + li;
+        const bool wz = is_wide<D>(sWide, Ib, d);
+#pragma unroll
+        for (int J = 0; J <= Ib; ++J) {
+          const bool in = J == Ib;
+          const int mi = in ? -1 : mid_index(Ib, J);
+          const float md = mi >= 0 ? sMid[mi * D + d] : 1.f;
+          const float gref = in ? gRI : sG[PB * (J + 1) * D + d];
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4) {
+            const int j = PB * J + 4 * s4 + lk;
+            float bf = __expf(gref - sG[j * D + d]) * md;
+            if (in && wz) bf = 0.f;
+            const float bv = sK[j * D + d] * bf;
+            float am = sL[ri * LB + j];
+            if (in && j > ri) am = 0.f;
+            a1 = mfma4(am, bv, a1);
+            a2 = mfma4(sT[ri * LB + j], bv, a2);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float x = __expf(sG[(PB * Ib + 4 * lk + r) * D + d] - gRI);
+          r1v[Ib][r] = x * a1[r];
+          r2v[Ib][r] = x * a2[r];
+        }
+      }
+    }
+    if (doC) {
+#pragma unroll
+      for (int Jb = 0; Jb < 4; ++Jb) {
+        f32x4 ain = {0.f, 0.f, 0.f, 0.f}, ax = {0.f, 0.f, 0.f, 0.f};
+        const int rj = PB * Jb + li;
+#pragma unroll
+        for (int Ib = Jb; Ib < 4; ++Ib) {
+          const bool in = Ib == Jb;
+          const int mi = in ? -1 : mid_index(Ib, Jb);
+          const float md = mi >= 0 ? sMid[mi * D + d] : 1.f;
+          const float gRI = sG[PB * Ib * D + d];
+#pragma unroll
+          for (int s4 = 0; s4 < 4; ++s4) {
+            const int i = PB * Ib + 4 * s4 + lk;
+            const float x = __expf(sG[i * D + d] - gRI) * md;
+            const float bk = sK[i * D + d] * x, bq = sQ[i * D + d] * x;
+            const float at = sT[i * LB + rj];
+            float am = sL[i * LB + rj];
+            if (in && i < rj) am = 0.f;
+            if (in) {
+              ain = mfma4(at, bk, ain);
+              ain = mfma4(am, bq, ain);
+            } else {
+              ax = mfma4(at, bk, ax);
+              ax = mfma4(am, bq, ax);
+            }
+          }
+        }
+        const float gRJ = sG[PB * Jb * D + d];
+        const float gRN = Jb < 3 ? sG[PB * (Jb + 1) * D + d] : 0.f;
+        const bool wz = is_wide<D>(sWide, Jb, d);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gj = sG[(PB * Jb + 4 * lk + r) * D + d];
+          float u = __expf(gRJ - gj);
+          if (wz) u = 0.f;
+          const float y = Jb < 3 ? __expf(gRN - gj) : 0.f;
+          cv[Jb][r] = u * ain[r] + y * ax[r];
+        }
+      }
+    }
+    float gb[4];
     f4(sG + (KB - 1) * D + d0, gb);
-    if (I > 0) f4(sG + PB * I * D + d0, gI);
-    if (I < 3) f4(sG + PB * (I + 1) * D + d0, gJ);
-    __syncthreads();     // sK and sQ are read no more: dG and the dG_B terms go there
+    __syncthreads();     // K, Q, dM and dAt are read no more: R1 into sK, R2 into sQ, C1 over the dM tiles
+    float* sC = sL;      // [64][D] over sL, sT and sY
+    if (doR) {
+#pragma unroll
+      for (int Ib = 0; Ib < 4; ++Ib)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = PB * Ib + 4 * lk + r;
+          sK[i * D + d] = r1v[Ib][r];
+          sQ[i * D + d] = r2v[Ib][r];
+        }
+    }
+    if (doC) {
+#pragma unroll
+      for (int Jb = 0; Jb < 4; ++Jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sC[(PB * Jb + 4 * lk + r) * D + d] = cv[Jb][r];
+    }
+    __syncthreads();
+    // the elementwise terms of the own tile (dG into sK, the dG_B terms into sQ)
 #pragma unroll
     for (int r = 0; r < TRW; ++r) {
       const int i = i0 + r;
-      float dqg[4], dkg[4], dkb[4], dq[4], dk[4];
+      float dqg[4], dkg[4], dkb[4], dq[4], dk[4], R1[4], R2[4], C1[4], gi[4];
       f4(w + Y::DQG + i * D + d0, dqg);
       f4(w + Y::DKG + i * D + d0, dkg);
       f4(w + Y::DKBM + i * D + d0, dkb);
+      f4(sK + i * D + d0, R1);
+      f4(sQ + i * D + d0, R2);
+      f4(sC + i * D + d0, C1);
+      f4(sG + i * D + d0, gi);
 #pragma unroll
       for (int cc = 0; cc < 4; ++cc) {
-        const float G = gr[r][cc];
-        const float E = I > 0 ? __expf(G - gI[cc]) : 0.f, F = I < 3 ? __expf(gJ[cc] - G) : 0.f;
-        const float r1 = rd1[r][cc] + E * z1[r][cc], r2 = rd2[r][cc] + E * z2[r][cc];
-        const float c1 = cd[r][cc] + F * zc[r][cc];
+        const float G = gi[cc];
+        const float r1 = rd1[r][cc] + R1[cc], r2 = rd2[r][cc] + R2[cc], c1 = cd[r][cc] + C1[cc];
         const float eG = __expf(G), eB = __expf(gb[cc] - G), k_ = kr[r][cc], q_ = qr[r][cc];
         dq[cc] = r1 + dqg[cc] * eG;
         dk[cc] = r2 + c1 + dkg[cc] * eG + dkb[cc] * eB;
@@ -1453,7 +1548,7 @@ constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
 constexpr size_t lds_btm() { return (KB * (D + 1) + KB * (D + 4) + KB + KT) * sizeof(float); }
 template <int D>
-constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D + 2 * KT) * sizeof(float); }
+constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D + 2 * KT + 4 * D / 32) * sizeof(float); }
 
 struct KdaArgs {
   const int32_t* chunk_rows;

@@ -30,7 +30,7 @@ def _need_gpu():
     _lib.lib()
 
 
-def draw(Cn, H, d, n_trees, n_leaves, seed, bf16):
+def draw(Cn, H, d, n_trees, n_leaves, seed, bf16, strong=False):
     r = np.random.default_rng(seed)
     f32 = lambda a: a.astype(np.float32)
     q = f32(r.standard_normal((Cn, H, d)))
@@ -38,6 +38,11 @@ def draw(Cn, H, d, n_trees, n_leaves, seed, bf16):
     k = f32(k / np.linalg.norm(k, axis=-1, keepdims=True))
     v = f32(r.standard_normal((Cn, H, d)))
     g = f32(r.uniform(-0.3, 0.0, (Cn, H, d)))
+    if strong:
+        # every fifth channel decays by up to 12 per row (about 96 over 16
+        # rows), the next by up to 7.5 (about 56 +- 8 over 16 rows)
+        g[:, :, 0::5] = r.uniform(-12.0, 0.0, g[:, :, 0::5].shape)
+        g[:, :, 1::5] = r.uniform(-7.5, 0.0, g[:, :, 1::5].shape)
     beta = f32(r.uniform(0.05, 1.0, (Cn, H)))
     dO = f32(r.standard_normal((Cn, H, d)))
     S0 = f32(r.standard_normal((n_trees, H, d, d)) * 0.5)
@@ -71,14 +76,25 @@ def test_kda_wide_state_slabs(dtype, d):
     assert max(s1 - s0 for s0, s1, *_ in run.rounds) * 32 * (d // 64) >= 512
 
 
-def check_forest(label, parent, seg_len, dtype, d, H):
+# Channels whose log-decay falls by more than 60 over a 16-row block take the
+# exact per-pair exponentials inside the block; the others factor through
+# the block's first row.  Strong decays put both kinds, and channels close
+# to the boundary, into every chunk.
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("f32", 128), ("bf16", 128)])
+def test_kda_strong_decays(dtype, d):
+    label, parent, seg_len = CASES[2]
+    check_forest(label + " strong decays", parent, seg_len, dtype, d, 2, strong=True)
+
+
+def check_forest(label, parent, seg_len, dtype, d, H, strong=False):
     """Every element of o, S_final and the gradients against the oracle."""
     from paper_2608_28158_amd.kda import KdaRunner
     from paper_2608_28158_amd.plan import HartsPlan
     plan = HartsPlan(parent, seg_len, 64, heads=H)
     Cn = int(np.sum(seg_len))
     print(f"[gpu] kda {label} K={plan['n_rounds']} {dtype} d={d} H={H}", flush=True)
-    q, k, v, g, beta, dO, S0, dSf = draw(Cn, H, d, plan["n_trees"], plan["n_leaves"], Cn + d, dtype == "bf16")
+    q, k, v, g, beta, dO, S0, dSf = draw(Cn, H, d, plan["n_trees"], plan["n_leaves"], Cn + d, dtype == "bf16",
+                                         strong)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     phys = phys_index(seg_len, plan["seg_row"])
 
