@@ -244,13 +244,16 @@ constexpr float KF_RANGE = 60.f;
 // Wide flags of the four blocks: bit d of word (I D + d) / 32 for channel d
 // of block I, from the cumulative log-decays sG (row stride LD).  Every
 // thread calls it; it returns whether any (block, channel) of the chunk is
-// wide (the call synchronises the workgroup).
+// wide (the call synchronises the workgroup).  With sKeep, also 0 (wide) or
+// 1 per (block, channel) there.
 template <int D, int LD>
-__device__ inline bool wide_flags(uint32_t* sWide, const float* sG, int t) {
+__device__ inline bool wide_flags(uint32_t* sWide, const float* sG, int t, float* sKeep = nullptr) {
   static_assert(4 * D <= KT && (4 * D) % 64 == 0 && (4 * D / 32) % 4 == 0, "one (block, channel) per thread, whole waves");
   if (t < 4 * D) {
     const int I = t / D, d = t % D;
-    const uint64_t m = __ballot(sG[PB * I * LD + d] - sG[(PB * I + PB - 1) * LD + d] > KF_RANGE);
+    const bool wide = sG[PB * I * LD + d] - sG[(PB * I + PB - 1) * LD + d] > KF_RANGE;
+    if (sKeep) sKeep[t] = wide ? 0.f : 1.f;
+    const uint64_t m = __ballot(wide);
     if ((t & 63) == 0) {
       sWide[t / 32] = static_cast<uint32_t>(m);
       sWide[t / 32 + 1] = static_cast<uint32_t>(m >> 32);
@@ -273,16 +276,19 @@ __device__ inline bool is_wide(const uint32_t* sWide, int I, int d) {
 
 // sA[i][j] = sum_d k_i k_j e^{G_i - G_j} for j < i (0 elsewhere) and gM (the
 // workspace) [i][j] = sum_d q_i k_j e^{G_i - G_j} for j <= i (0 elsewhere);
-// sK, sQ and sG have row stride LD, sA and sX LT; sX (64 x 64) is scratch,
-// sMid holds 3 x D middle factors, sWide the wide flags.  K, Q and G are
-// left as they are.  All block pairs run on float32 MFMA (k = channel), the
-// operands' exponential factors formed as they are read: one (block pair,
-// At and M) per wave.  The in-block pairs of wide channels are summed
-// exactly first (4 x 4 tiles with the channels dealt over 16 adjacent lanes,
-// summed by lane exchanges) and added to the products.
+// sK, sQ and sG have row stride LD, sA and sX LT; sX (64 x 64) is scratch.
+// sF [8][D] receives per-channel factors of the B operands: rows 0..3 keep
+// (1) or drop (0, wide) block I's in-block pairs, rows 4..6 the middle
+// factors, row 7 ones.  K, Q and G are left as they are.  All block pairs
+// run on float32 MFMA (k = channel), the operands' exponential factors
+// formed as they are read, one (block pair, At and M) per wave; each lane
+// reads 16-byte runs of 4 channels (the channel order permuted alike in both
+// operands).  The in-block pairs of wide channels are summed exactly first
+// (4 x 4 tiles with the channels dealt over 16 adjacent lanes, summed by
+// lane exchanges) and added to the products.
 template <int D, int LD, int LT>
 __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, const float* sK, const float* sQ,
-                                          const float* sG, float* sX, float* sMid, uint32_t* sWide, int t) {
+                                          const float* sG, float* sX, float* sF, uint32_t* sWide, int t) {
   for (int p = t; p < KB * KB; p += KT) {
     const int i = p / KB, j = p % KB;
     sA[i * LT + j] = 0.f;
@@ -292,9 +298,11 @@ __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, con
   if (t < 3 * D) {
     const int x = t / D, d = t % D;
     const int ri = x == 0 ? 2 * PB : 3 * PB, rj = x == 2 ? 2 * PB : PB;
-    sMid[t] = __expf(sG[ri * LD + d] - sG[rj * LD + d]);
+    sF[4 * D + t] = __expf(sG[ri * LD + d] - sG[rj * LD + d]);
+  } else if (t < 4 * D) {
+    sF[4 * D + t] = 1.f;
   }
-  const bool any_wide = wide_flags<D, LD>(sWide, sG, t);
+  const bool any_wide = wide_flags<D, LD>(sWide, sG, t, sF);
   if (any_wide) {
     // the wide channels' in-block pairs, exact: tile (block, ti >= tj),
     // channels de, de + 16, .. (At into sA, M into sX)
@@ -361,6 +369,8 @@ __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, con
   // across blocks.  At and M of a pair share their B operand:
   //   in-block  A = K_I e^{G_I - G_{r_I}} (Q_I ..),  B = K_I e^{G_{r_I} - G_I} (0 where wide)
   //   across    A = K_I e^{G_I - G_{r_I}} (Q_I ..),  B = K_J e^{G_{r_{J+1}} - G_J} mid(I, J)
+  // An exponential that overflows (a wide channel's in-block B) is clamped
+  // to a finite value before its factor 0 applies.
   {
     const int lane = t & 63, li = lane & 15, lk = lane >> 4;
     for (int o = t >> 6; o < 10; o += KT / 64) {
@@ -373,19 +383,32 @@ __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, con
       }
       const bool in = I == J;
       const int mi = in ? -1 : mid_index(I, J);
-      const int ri = PB * I + li, rj = PB * J + li, rb = in ? PB * I : PB * (J + 1);
+      const float* gIr = sG + PB * I * LD + 4 * lk;                       // G_{r_I}
+      const float* ga = sG + (PB * I + li) * LD + 4 * lk;                 // A rows
+      const float* ka = sK + (PB * I + li) * LD + 4 * lk;
+      const float* qa = sQ + (PB * I + li) * LD + 4 * lk;
+      const float* gbr = sG + (in ? PB * I : PB * (J + 1)) * LD + 4 * lk; // B's reference row
+      const float* gb = sG + (PB * J + li) * LD + 4 * lk;                 // B rows
+      const float* kb = sK + (PB * J + li) * LD + 4 * lk;
+      const float* fb = sF + (in ? I : (mi >= 0 ? 4 + mi : 7)) * D + 4 * lk;
       f32x4 accA = {0.f, 0.f, 0.f, 0.f}, accM = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-      for (int s4 = 0; s4 < D / 4; ++s4) {
-        const int k = 4 * s4 + lk;
-        const float gI = sG[PB * I * LD + k];
-        const float x = __expf(sG[ri * LD + k] - gI);
-        float bf = __expf(sG[rb * LD + k] - sG[rj * LD + k]);
-        if (in) bf = is_wide<D>(sWide, I, k) ? 0.f : bf;
-        else if (mi >= 0) bf *= sMid[mi * D + k];
-        const float b = sK[rj * LD + k] * bf;
-        accA = mfma4(sK[ri * LD + k] * x, b, accA);
-        accM = mfma4(sQ[ri * LD + k] * x, b, accM);
+#pragma unroll 2
+      for (int c16 = 0; c16 < D; c16 += 16) {
+        const f32x4 gI4 = *reinterpret_cast<const f32x4*>(gIr + c16);
+        const f32x4 ga4 = *reinterpret_cast<const f32x4*>(ga + c16);
+        const f32x4 ka4 = *reinterpret_cast<const f32x4*>(ka + c16);
+        const f32x4 qa4 = *reinterpret_cast<const f32x4*>(qa + c16);
+        const f32x4 gr4 = *reinterpret_cast<const f32x4*>(gbr + c16);
+        const f32x4 gb4 = *reinterpret_cast<const f32x4*>(gb + c16);
+        const f32x4 kb4 = *reinterpret_cast<const f32x4*>(kb + c16);
+        const f32x4 f4 = *reinterpret_cast<const f32x4*>(fb + c16);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x = __expf(ga4[e] - gI4[e]);
+          const float b = kb4[e] * (fminf(__expf(gr4[e] - gb4[e]), 3.0e38f) * f4[e]);
+          accA = mfma4(ka4[e] * x, b, accA);
+          accM = mfma4(qa4[e] * x, b, accM);
+        }
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -453,12 +476,12 @@ __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const 
 
 // LDS of the chunk preparation (floats): K and Q (row stride LD in the
 // pairwise sums, LW for the products with Tm, whose B operands run along k),
-// G, At (then Tm) and L^{-1} (stride LT), beta, middle factors, scan totals.
+// G, At (then Tm) and L^{-1} (stride LT), beta, channel factors of the block pairs, scan totals, wide flags.
 template <int D>
 struct PrepLds {
   static constexpr int LD = D + 4, LW = D + 16, LT = KB + 4;
   static constexpr int K = 0, Q = K + KB * LW, G = Q + KB * LW, A = G + KB * LD, L = A + KB * LT, B = L + KB * LT,
-                       MID = B + KB, TOT = MID + 3 * D, WIDE = TOT + KT, ALL = WIDE + 4 * D / 32;
+                       FAC = B + KB, TOT = FAC + 8 * D, WIDE = TOT + KT, ALL = WIDE + 4 * D / 32;
 };
 
 // ---------------------------------------------------------------------------
@@ -479,7 +502,7 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   float* sA = sm + P::A;
   float* sL = sm + P::L;
   float* sb = sm + P::B;
-  float* sMid = sm + P::MID;
+  float* sFac = sm + P::FAC;
   float* sTot = sm + P::TOT;
   uint32_t* sWide = reinterpret_cast<uint32_t*>(sm + P::WIDE);
   const int c = static_cast<int>(blockIdx.x / H) + static_cast<int>(c0), h = blockIdx.x % H;
@@ -505,7 +528,7 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   }
   if (t < D) w[Y::GAM + t] = __expf(sG[(KB - 1) * LD + t]);
   // At into sA and the workspace, M into the workspace
-  pair_sums<D, LD, LT>(sA, w + Y::M, sK, sQ, sG, sL, sMid, sWide, t);
+  pair_sums<D, LD, LT>(sA, w + Y::M, sK, sQ, sG, sL, sFac, sWide, t);
   __syncthreads();
   for (int p = t; p < KB * KB; p += KT) w[Y::AT + p] = sA[(p / KB) * LT + p % KB];
   tri_inverse<LT>(sL, sQ, sA, sb, t);          // the Q tile is free now: scratch
