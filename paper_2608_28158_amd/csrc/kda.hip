@@ -436,13 +436,22 @@ __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const 
   constexpr int BS = 16;
   for (int p = t; p < KB * KB; p += KT) sL[(p / KB) * LT + p % KB] = (p / KB == p % KB) ? 1.f : 0.f;
   __syncthreads();
-  if (t < KB) {                                   // diagonal blocks
-    const int c = t, r0 = (c / BS) * BS;
-    for (int i = c + 1; i < r0 + BS; ++i) {
+  if (t < KB) {                                   // diagonal blocks, the column in registers
+    const int c = t, cb = c % BS, r0 = c - cb;
+    float col[BS];
+#pragma unroll
+    for (int x = 0; x < BS; ++x) col[x] = x == cb ? 1.f : 0.f;
+#pragma unroll
+    for (int x = 1; x < BS; ++x) {
+      // rows above the diagonal of column c hold 0, so the sum starts at row c
+      const float* ar = sA + (r0 + x) * LT + r0;
       float s = 0.f;
-      for (int j = c; j < i; ++j) s += sA[i * LT + j] * sL[j * LT + c];
-      sL[i * LT + c] = -sb[i] * s;
+#pragma unroll
+      for (int y = 0; y < x; ++y) s += ar[y] * col[y];
+      if (x > cb) col[x] = -sb[r0 + x] * s;
     }
+#pragma unroll
+    for (int x = 1; x < BS; ++x) sL[(r0 + x) * LT + c] = col[x];
   }
   __syncthreads();
   const int lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
@@ -509,15 +518,20 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  // k, q and v requested together at the start (k is stored twice, at
+  // k, q, g and v requested together at the start (k is stored twice, at
   // both strides; v waits in registers until the products with Tm)
   RowPre<T, D> pk, pq, pv;
+  RowPre<float, D> pg;
   pk.load(k, ent, H, h, t);
   pq.load(q, ent, H, h, t);
+  pg.load(g, ent, H, h, t);
   pv.load(v, ent, H, h, t);
+  if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
   pk.template store<LD>(sK, t);
   pq.template store<LD>(sQ, t);
-  load_decay<D, LD>(sG, sb, sTot, g, beta, ent, H, h, t);
+  pg.template store<LD>(sG, t);
+  __syncthreads();
+  cumsum_rows<D, LD>(sG, sTot, t);
   // KB = K e^{G_B - G}, QG = Q e^G, gamma = e^{G_B} (before the pairwise
   // sums overwrite K and Q with their block factors)
   for (int idx = t; idx < KB * D; idx += KT) {
