@@ -1193,6 +1193,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
       *reinterpret_cast<f32x4*>(dst + (e / KB) * LB + e % KB) = src[n];
     }
   };
+  const float dgam = w[Y::DGAM + t % D];                 // for the reverse sum of dG at the end
   if (t < KB) sb[t] = ent[t] >= 0 ? beta[static_cast<int64_t>(ent[t] >> 1) * H + h] : 0.f;
   pk.template store<D>(sK, t);
   pq.template store<D>(sQ, t);
@@ -1499,7 +1500,7 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
     sTot[part * D + d] = a;
     sTot[KT + part * D + d] = xs;
     __syncthreads();
-    float off = w[Y::DGAM + d] * __expf(sG[(KB - 1) * D + d]);
+    float off = dgam * __expf(sG[(KB - 1) * D + d]);
     for (int p = 0; p < NP; ++p) off += sTot[KT + p * D + d] + (p > part ? sTot[p * D + d] : 0.f);
 #pragma unroll
     for (int r = 0; r < RP; ++r) {
