@@ -1052,91 +1052,126 @@ __global__ __launch_bounds__(KT, 4) void k_kda_bwd_prod(const int32_t* __restric
 }
 
 // Products with Tm = L^{-1} Diag(beta) of one (chunk, head): dTm = dUV +
-// dW (K e^G)^T (j <= i, into dUV in the workspace), dV = Tm^T dX (to pdv),
-// d(K e^G) = Tm^T dW (to the workspace).  Float32 MFMA with K e^G staged in
-// LDS ([64][D + 4], read along the fragment's n coordinate: conflict-free)
-// and every other operand read from the workspace.  Wave w owns row block
-// w / 2 of dV and d(K e^G) (column blocks (D / 32)(w % 2)..) and the
-// lower-triangle blocks of dTm in row block w / 2 whose column block has the
-// parity of w.
+// dW (K e^G)^T (j <= i, into dUV in the workspace), dV = Tm^T dX (to the
+// gradient outputs), d(K e^G) = Tm^T dW (to the workspace).  Float32 MFMA.
+// K e^G stays in LDS ([64][D + 4], read along the fragment's n coordinate);
+// dW and dX pass through LDS in slabs of BTM_SW columns (once K e^G is
+// formed, in the space of G), dW twice: rows along m for dTm ([64][SW + 4])
+// and along k for d(K e^G) ([64][SW + 16]), every fragment read
+// conflict-free; the next slab waits in registers meanwhile.  Each wave's
+// Tm^T fragments are requested at the start and held in registers.  Wave w
+// owns row block w / 2: the lower-triangle blocks of dTm whose column block
+// has the parity of w, and per slab the column block of parity w of dV and
+// d(K e^G).
+constexpr int BTM_SW = 32;
+template <int D>
+struct BtmLds {
+  static constexpr int LG = D + 4, LK = D + 4, SW = BTM_SW, LA = SW + 4, LB = SW + 16;
+  static constexpr int STG = KB * (LA + 2 * LB), GS = KB * LG > STG ? KB * LG : STG;
+  static constexpr int G = 0, WA = 0, WB = WA + KB * LA, XB = WB + KB * LB, KG = GS, B = KG + KB * LK, TOT = B + KB,
+                       ALL = TOT + KT;
+};
+
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                    const T* __restrict__ k, const float* __restrict__ g,
                                                    const float* __restrict__ beta, float* __restrict__ ws,
                                                    const KdaGrads go) {
   using Y = WsLay<D>;
-  constexpr int LG = D + 1, LK = D + 4, TDW = D / 32;
+  using L = BtmLds<D>;
+  constexpr int SW = L::SW, NS = D / SW;
+  static_assert(SW * KB / 4 == KT && (SW / 16) * 4 == KT / 64, "one float4 of a slab per thread; 2 column blocks x 4 row blocks per slab");
   extern __shared__ float sm[];
-  float* sG = sm;                  // [64][D + 1] cumulative log-decay
-  float* sKG = sG + KB * LG;       // [64][D + 4] K e^G
-  float* sb = sKG + KB * LK;       // [64] beta
-  float* sTot = sb + KB;           // [KT] scan totals
+  float* sG = sm + L::G;           // [64][LG] cumulative log-decay, then the slabs:
+  float* sWa = sm + L::WA;         //   dW [64][LA]
+  float* sWb = sm + L::WB;         //   dW [64][LB]
+  float* sXb = sm + L::XB;         //   dX [64][LB]
+  float* sKG = sm + L::KG;         // [64][LK] K e^G
+  float* sb = sm + L::B;           // [64] beta
+  float* sTot = sm + L::TOT;       // [KT] scan totals
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
-  RowPre<T, D> pk;                 // k requested together with g
+  const int wi = wv >> 1, par = wv & 1;
+  // requested at the start: k, the first slab of dW and dX, the Tm^T
+  // fragments (rows i = 4 s4 + lk, s4 = 4 wi ..; past the last row block
+  // the last rows are requested again and not used)
+  RowPre<T, D> pk;
   pk.load(k, ent, H, h, t);
-  load_decay<D, LG>(sG, sb, sTot, g, beta, ent, H, h, t);
-  pk.template store<LK>(sKG, t);
+  const int sr = t / (SW / 4), sc = 4 * (t % (SW / 4));
+  f32x4 nW = *reinterpret_cast<const f32x4*>(w + Y::DW + sr * D + sc);
+  f32x4 nX = *reinterpret_cast<const f32x4*>(w + Y::DX + sr * D + sc);
+  float pl[KB / 4];
+#pragma unroll
+  for (int n = 0; n < KB / 4; ++n) {
+    const int s4 = 4 * wi + n < KB / 4 ? 4 * wi + n : KB / 4 - 1;
+    pl[n] = w[Y::LINV + (4 * s4 + lk) * KB + 16 * wi + li];
+  }
+  load_decay<D, L::LG>(sG, sb, sTot, g, beta, ent, H, h, t);
+  pk.template store<L::LK>(sKG, t);
   __syncthreads();
   for (int idx = t; idx < KB * D; idx += KT) {
     const int r = idx / D, d = idx % D;
-    sKG[r * LK + d] *= __expf(sG[r * LG + d]);
+    sKG[r * L::LK + d] *= __expf(sG[r * L::LG + d]);
   }
-  __syncthreads();
-  const int wi = wv >> 1, td0 = (wv & 1) * TDW;
-  // dTm blocks (wi, tj): A = dW rows, B = (K e^G)^T
-  f32x4 aT[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-  const float* dwr = w + Y::DW + (16 * wi + li) * D + lk;
-#pragma unroll 4
-  for (int s4 = 0; s4 < D / 4; ++s4) {
-    const float a = dwr[4 * s4];
-#pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      const int tj = (wv & 1) + 2 * x;
-      if (tj <= wi) aT[x] = mfma4(a, sKG[(16 * tj + li) * LK + 4 * s4 + lk], aT[x]);
-    }
-  }
-  // dV and d(K e^G) of row block wi: A = Tm^T (Tm[i][j] = L^{-1}[i][j] beta_j, zero for i < j)
   const float bj = sb[16 * wi + li];
-  f32x4 aV[TDW], aK[TDW];
+  const int ns = KB / 4 - 4 * wi;                          // k steps of Tm^T products
+  f32x4 aT[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  for (int sl = 0; sl < NS; ++sl) {
+    __syncthreads();                                       // G (first slab) or the last slab is read no more
+    *reinterpret_cast<f32x4*>(sWa + sr * L::LA + sc) = nW;
+    *reinterpret_cast<f32x4*>(sWb + sr * L::LB + sc) = nW;
+    *reinterpret_cast<f32x4*>(sXb + sr * L::LB + sc) = nX;
+    __syncthreads();
+    {
+      const int nx = sl + 1 < NS ? sl + 1 : sl;            // the next slab (the last one again at the end)
+      nW = *reinterpret_cast<const f32x4*>(w + Y::DW + sr * D + SW * nx + sc);
+      nX = *reinterpret_cast<const f32x4*>(w + Y::DX + sr * D + SW * nx + sc);
+    }
+    // dTm blocks (wi, tj): A = dW rows, B = (K e^G)^T, over the slab's channels
 #pragma unroll
-  for (int x = 0; x < TDW; ++x) aV[x] = aK[x] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-  for (int s4 = 4 * wi; s4 < KB / 4; ++s4) {
-    const int i = 4 * s4 + lk;
-    const float a = w[Y::LINV + i * KB + 16 * wi + li] * bj;
+    for (int s4 = 0; s4 < SW / 4; ++s4) {
+      const float a = sWa[(16 * wi + li) * L::LA + 4 * s4 + lk];
 #pragma unroll
-    for (int x = 0; x < TDW; ++x) {
-      const int col = 16 * (td0 + x) + li;
-      aV[x] = mfma4(a, w[Y::DX + i * D + col], aV[x]);
-      aK[x] = mfma4(a, w[Y::DW + i * D + col], aK[x]);
+      for (int x = 0; x < 2; ++x) {
+        const int tj = par + 2 * x;
+        if (tj <= wi) aT[x] = mfma4(a, sKG[(16 * tj + li) * L::LK + SW * sl + 4 * s4 + lk], aT[x]);
+      }
+    }
+    // dV and d(K e^G) of row block wi, column block par of the slab: A = Tm^T
+    // (Tm[i][j] = L^{-1}[i][j] beta_j, zero for i < j)
+    f32x4 aV = {0.f, 0.f, 0.f, 0.f}, aK = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int n = 0; n < KB / 4; ++n) {
+      if (n < ns) {
+        const int i = 4 * (4 * wi + n) + lk;
+        const float a = pl[n] * bj;
+        aV = mfma4(a, sXb[i * L::LB + 16 * par + li], aV);
+        aK = mfma4(a, sWb[i * L::LB + 16 * par + li], aK);
+      }
+    }
+    const int col = SW * sl + 16 * par + li;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = 16 * wi + 4 * lk + r;
+      const int32_t e = ent[j];
+      if (e >= 0) {
+        const int32_t slt = go.slot[static_cast<int64_t>(c) * KB + j];
+        if (slt < 0) st<T>(static_cast<T*>(go.dv) + (static_cast<int64_t>(e >> 1) * H + h) * D + col, aV[r]);
+        else go.sdv[(static_cast<int64_t>(slt) * H + h) * D + col] = aV[r];
+      }
+      w[Y::DKG + j * D + col] = aK[r];
     }
   }
 #pragma unroll
   for (int x = 0; x < 2; ++x) {
-    const int tj = (wv & 1) + 2 * x;
+    const int tj = par + 2 * x;
     if (tj > wi) continue;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int i = 16 * wi + 4 * lk + r, j = 16 * tj + li;
       if (j <= i) w[Y::DUV + i * KB + j] += aT[x][r];
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int j = 16 * wi + 4 * lk + r;
-    const int32_t e = ent[j];
-    const int32_t sl = e >= 0 ? go.slot[static_cast<int64_t>(c) * KB + j] : -1;
-#pragma unroll
-    for (int x = 0; x < TDW; ++x) {
-      const int col = 16 * (td0 + x) + li;
-      if (e >= 0) {
-        if (sl < 0) st<T>(static_cast<T*>(go.dv) + (static_cast<int64_t>(e >> 1) * H + h) * D + col, aV[x][r]);
-        else go.sdv[(static_cast<int64_t>(sl) * H + h) * D + col] = aV[x][r];
-      }
-      w[Y::DKG + j * D + col] = aK[x][r];
     }
   }
 }
@@ -1584,7 +1619,7 @@ constexpr size_t lds_bprep() { return KB * (D + 16) * sizeof(float); }
 template <int D>
 constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
-constexpr size_t lds_btm() { return (KB * (D + 1) + KB * (D + 4) + KB + KT) * sizeof(float); }
+constexpr size_t lds_btm() { return BtmLds<D>::ALL * sizeof(float); }
 template <int D>
 constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D + 2 * KT + 4 * D / 32) * sizeof(float); }
 
