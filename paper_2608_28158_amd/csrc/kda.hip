@@ -860,7 +860,8 @@ __global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chun
 // ---------------------------------------------------------------------------
 // dXo = scale M^T dO (64 x D), dSo = scale QG^T dO (D x D), dO of own rows.
 // Float32 MFMA with dO staged in LDS ([64][D + 16], rows along k) and the A
-// operands (columns of M and QG) read from the workspace.  Wave w owns the
+// operands (columns of M and QG) requested from the workspace into registers
+// before the staging.  Wave w owns the
 // flat tiles w * TS.. of dSo and w * TX.. of dXo (each run inside one row
 // block, sharing its A operand); rows of M^T's block tj see only i >= 16 tj.
 template <typename T, int D>
@@ -875,6 +876,17 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  const int fs = wv * TS, td = fs / NT, tvs = fs % NT;
+  const int fx = wv * TX, tj = fx / NT, tvx = fx % NT;
+  // the A operands requested first: column 16 td + li of QG and column
+  // 16 tj + li of M at the lane's rows (above the diagonal M holds zeros)
+  float paq[KB / 4], pam[KB / 4];
+#pragma unroll
+  for (int s4 = 0; s4 < KB / 4; ++s4) {
+    const int k = 4 * s4 + lk;
+    paq[s4] = w[Y::QG + k * D + 16 * td + li];
+    pam[s4] = w[Y::M + k * KB + 16 * tj + li];
+  }
   {
     constexpr int N = RowVec<T>::N, VR = D / N;
     for (int idx = t; idx < KB * VR; idx += KT) {
@@ -889,23 +901,19 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_prep(const int32_t* __restrict__
     }
   }
   __syncthreads();
-  const int fs = wv * TS, td = fs / NT, tvs = fs % NT;
-  const int fx = wv * TX, tj = fx / NT, tvx = fx % NT;
   f32x4 aS[TS], aX[TX];
 #pragma unroll
   for (int x = 0; x < TS; ++x) aS[x] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int x = 0; x < TX; ++x) aX[x] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
+#pragma unroll
   for (int s4 = 0; s4 < KB / 4; ++s4) {
     const int k = 4 * s4 + lk;
-    const float aq = w[Y::QG + k * D + 16 * td + li];
-    const float am = s4 >= 4 * tj ? w[Y::M + k * KB + 16 * tj + li] : 0.f;
 #pragma unroll
-    for (int x = 0; x < TS; ++x) aS[x] = mfma4(aq, sD[k * LD + 16 * (tvs + x) + li], aS[x]);
+    for (int x = 0; x < TS; ++x) aS[x] = mfma4(paq[s4], sD[k * LD + 16 * (tvs + x) + li], aS[x]);
     if (s4 >= 4 * tj)
 #pragma unroll
-      for (int x = 0; x < TX; ++x) aX[x] = mfma4(am, sD[k * LD + 16 * (tvx + x) + li], aX[x]);
+      for (int x = 0; x < TX; ++x) aX[x] = mfma4(pam[s4], sD[k * LD + 16 * (tvx + x) + li], aX[x]);
   }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
