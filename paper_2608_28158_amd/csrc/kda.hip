@@ -610,7 +610,7 @@ constexpr int SQL = SQV + 4;             // LDS row stride of Sc and Xc there (1
 // fragment read hit 64 different banks.
 template <int D, int SV>
 struct SeqLds {
-  static constexpr int LA1 = D + 4, LA2 = D + 16, LS = SV + 16, LX = SV + 16;
+  static constexpr int LA1 = D + 4, LA2 = D + 16, LS = SV + 4, LX = SV + 16;
   static constexpr int A1 = 0, A2 = A1 + KB * LA1, S = A2 + KB * LA2, X = S + D * LS, G = X + KB * LX, ALL = G + D;
 };
 
@@ -730,12 +730,30 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
     }
     __syncthreads();
     fetch(set, step + 2);
-    // Xc = P + s1 A1 Sc
-#pragma unroll 4
-    for (int s = 0; s < D / 4; ++s) {
-      const float a = S1 * sA1[(16 * xti + li) * L::LA1 + 4 * s + lk];
+    // Xc = P + s1 A1 Sc: the lane reads 16-byte runs of its A1 row, k
+    // permuted alike on both operands (k = 16 g + 4 (lane / 16) + e); with
+    // one tile per wave the steps alternate between two accumulators; the
+    // product loops are unrolled fully where the registers allow it
+    // (32-column slabs)
+    {
+      f32x4 acc2[XT];
 #pragma unroll
-      for (int x = 0; x < XT; ++x) acc[x] = mfma4(a, sS[(4 * s + lk) * L::LS + 16 * (xtv + x) + li], acc[x]);
+      for (int x = 0; x < XT; ++x) acc2[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll (SV == 32 ? D / 16 : 2)
+      for (int g = 0; g < D / 16; ++g) {
+        const f32x4 a4 = *reinterpret_cast<const f32x4*>(sA1 + (16 * xti + li) * L::LA1 + 16 * g + 4 * lk);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int k = 16 * g + 4 * lk + e;
+#pragma unroll
+          for (int x = 0; x < XT; ++x) {
+            const float bv = sS[k * L::LS + 16 * (xtv + x) + li];
+            if (XT == 1 && (e & 1)) acc2[x] = mfma4(S1 * a4[e], bv, acc2[x]);
+            else acc[x] = mfma4(S1 * a4[e], bv, acc[x]);
+          }
+        }
+      }
+      if constexpr (XT == 1) acc[0] += acc2[0];
     }
 #pragma unroll
     for (int x = 0; x < XT; ++x)
@@ -751,7 +769,7 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
     for (int x = 0; x < ST; ++x)
 #pragma unroll
       for (int r = 0; r < 4; ++r) sacc[x][r] += sg[16 * sti + 4 * lk + r] * Sa[x][r];
-#pragma unroll 4
+#pragma unroll (SV == 32 ? KB / 4 : 4)
     for (int s = 0; s < KB / 4; ++s) {
       const float a = S2 * sA2[(4 * s + lk) * L::LA2 + 16 * sti + li];
 #pragma unroll
