@@ -427,15 +427,17 @@ __device__ __forceinline__ void pair_sums(float* sA, float* __restrict__ gM, con
 
 // sL = (I + Diag(beta) At)^{-1}, unit lower triangular, in 16 x 16 blocks
 // (row stride LT of sL, sW and sA): the four diagonal blocks by forward
-// substitution (one column per thread), then block row by block row on
-// float32 MFMA, one wave per block column J < I:
+// substitution (one column per thread of wave 0, held in registers) while
+// the other waves zero the blocks above the diagonal; then each block
+// column J < 3 by one wave, down its block rows I > J on float32 MFMA:
 //   sW_IJ = sum_{J <= K < I} N_IK L^{-1}_KJ with N = Diag(beta) At,
 //   L^{-1}_IJ = -L^{-1}_II sW_IJ.
+// A block column needs only its own blocks and the diagonal ones, so the
+// waves proceed independently (their LDS writes and reads stay in program
+// order within the wave).
 template <int LT>
 __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const float* sb, int t) {
   constexpr int BS = 16;
-  for (int p = t; p < KB * KB; p += KT) sL[(p / KB) * LT + p % KB] = (p / KB == p % KB) ? 1.f : 0.f;
-  __syncthreads();
   if (t < KB) {                                   // diagonal blocks, the column in registers
     const int c = t, cb = c % BS, r0 = c - cb;
     float col[BS];
@@ -451,13 +453,18 @@ __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const 
       if (x > cb) col[x] = -sb[r0 + x] * s;
     }
 #pragma unroll
-    for (int x = 1; x < BS; ++x) sL[(r0 + x) * LT + c] = col[x];
+    for (int x = 0; x < BS; ++x) sL[(r0 + x) * LT + c] = col[x];
+  } else {
+    for (int p = t - KB; p < KB * KB; p += KT - KB) {
+      const int i = p / KB, j = p % KB;
+      if (j / BS > i / BS) sL[i * LT + j] = 0.f;
+    }
   }
   __syncthreads();
   const int lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
-  for (int I = 1; I < KB / BS; ++I) {
-    if (wv < I) {
-      const int J = wv;
+  if (wv < KB / BS - 1) {
+    const int J = wv;
+    for (int I = J + 1; I < KB / BS; ++I) {
       const float bi = sb[BS * I + li];
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
       for (int s4 = 4 * J; s4 < 4 * I; ++s4) {
@@ -466,11 +473,8 @@ __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const 
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) sW[(BS * I + 4 * lk + r) * LT + BS * J + li] = acc[r];
-    }
-    __syncthreads();
-    if (wv < I) {
-      const int J = wv;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s4 = 4 * I; s4 < 4 * I + 4; ++s4) {
         const int k = 4 * s4 + lk;
@@ -478,9 +482,10 @@ __device__ inline void tri_inverse(float* sL, float* sW, const float* sA, const 
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) sL[(BS * I + 4 * lk + r) * LT + BS * J + li] = -acc[r];
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
-    __syncthreads();
   }
+  __syncthreads();
 }
 
 // LDS of the chunk preparation (floats): K and Q (row stride LD in the
