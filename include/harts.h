@@ -507,7 +507,8 @@ int harts_attn_scatter(const float* src, const int64_t* row_off, const int32_t* 
  *   seq_tab    [n_seq][8]: round (0-based), first chunk, chunks, initial
  *              bank entry, first request, requests, final leaf, 0.
  *   req_tab    [n_req][2]: (chunk c of the sequence, bank entry): the state
- *              at the start of chunk c (c = chunks: the end state).
+ *              at the start of chunk c (c = chunks: the end state), each
+ *              sequence's requests in ascending chunk order.
  *   group_tab  [n_groups][4], group_seq [n_seq]: per round, the sequences
  *              starting from each bank entry (round, entry, first member,
  *              members), in sequence order -- the order of the adjoint sums.

@@ -702,6 +702,11 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
     pg[Z] = *reinterpret_cast<const f32x4*>(w + Y::GAM + 4 * (t % (D / 4)));
   };
   int rq = 0;
+  // reverse: the requests (in ascending chunk order) walked from the end,
+  // those at the end (cc == nc) already added to the initial adjoint
+  int rr = nr - 1;
+  if (REV)
+    while (rr >= 0 && req_tab[2 * (ro + rr)] >= nc) --rr;
   // forward: the states requested at the start of chunk cc (cc == nc: the end)
   const auto requests = [&](int cc) {
     if (REV) return;
@@ -781,9 +786,9 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
       for (int x = 0; x < ST; ++x) sacc[x] = mfma4(a, sX[(4 * s + lk) * L::LX + 16 * (stv + x) + li], sacc[x]);
     }
     if (REV)       // adjoints of the requested states at the start of chunk cc
-      for (int q = 0; q < nr; ++q)
-        if (req_tab[2 * (ro + q)] == cc) {
-          const float* db = slab_of(dbank, req_tab[2 * (ro + q) + 1]);
+      for (; rr >= 0 && req_tab[2 * (ro + rr)] >= cc; --rr)
+        if (req_tab[2 * (ro + rr)] == cc) {
+          const float* db = slab_of(dbank, req_tab[2 * (ro + rr) + 1]);
 #pragma unroll
           for (int x = 0; x < ST; ++x)
 #pragma unroll
