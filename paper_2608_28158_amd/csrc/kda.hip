@@ -1495,6 +1495,14 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
         }
       }
     }
+    // the workspace terms of the elementwise phase, requested before the terms go through LDS
+    f32x4 wq[TRW], wk[TRW], wb[TRW];
+#pragma unroll
+    for (int r = 0; r < TRW; ++r) {
+      wq[r] = *reinterpret_cast<const f32x4*>(w + Y::DQG + (i0 + r) * D + d0);
+      wk[r] = *reinterpret_cast<const f32x4*>(w + Y::DKG + (i0 + r) * D + d0);
+      wb[r] = *reinterpret_cast<const f32x4*>(w + Y::DKBM + (i0 + r) * D + d0);
+    }
     float gb[4];
     f4(sG + (KB - 1) * D + d0, gb);
     __syncthreads();     // K, Q, dM and dAt are read no more: R1 into sK, R2 into sQ, C1 over the dM tiles
@@ -1520,10 +1528,10 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
 #pragma unroll
     for (int r = 0; r < TRW; ++r) {
       const int i = i0 + r;
-      float dqg[4], dkg[4], dkb[4], dq[4], dk[4], R1[4], R2[4], C1[4], gi[4];
-      f4(w + Y::DQG + i * D + d0, dqg);
-      f4(w + Y::DKG + i * D + d0, dkg);
-      f4(w + Y::DKBM + i * D + d0, dkb);
+      float dq[4], dk[4], R1[4], R2[4], C1[4], gi[4];
+      const float dqg[4] = {wq[r][0], wq[r][1], wq[r][2], wq[r][3]};
+      const float dkg[4] = {wk[r][0], wk[r][1], wk[r][2], wk[r][3]};
+      const float dkb[4] = {wb[r][0], wb[r][1], wb[r][2], wb[r][3]};
       f4(sK + i * D + d0, R1);
       f4(sQ + i * D + d0, R2);
       f4(sC + i * D + d0, C1);
