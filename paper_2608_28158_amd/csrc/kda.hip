@@ -1105,7 +1105,7 @@ struct BtmLds {
   static constexpr int LG = D + 4, LK = D + 4, SW = BTM_SW, LA = SW + 4, LB = SW + 16;
   static constexpr int STG = KB * (LA + 2 * LB), GS = KB * LG > STG ? KB * LG : STG;
   static constexpr int G = 0, WA = 0, WB = WA + KB * LA, XB = WB + KB * LB, KG = GS, B = KG + KB * LK, TOT = B + KB,
-                       ALL = TOT + KT;
+                       ENT = TOT + KT, SLOT = ENT + KB, ALL = SLOT + KB;
 };
 
 template <typename T, int D>
@@ -1125,11 +1125,18 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
   float* sKG = sm + L::KG;         // [64][LK] K e^G
   float* sb = sm + L::B;           // [64] beta
   float* sTot = sm + L::TOT;       // [KT] scan totals
+  int32_t* sEnt = reinterpret_cast<int32_t*>(sm + L::ENT);    // [64] row table entries
+  int32_t* sSlot = reinterpret_cast<int32_t*>(sm + L::SLOT);  // [64] gradient slots
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
   const int wi = wv >> 1, par = wv & 1;
+  if (t < KB) {                    // where each row's dv goes, read once
+    const int32_t e = ent[t];
+    sEnt[t] = e;
+    sSlot[t] = e >= 0 ? go.slot[static_cast<int64_t>(c) * KB + t] : -1;
+  }
   // requested at the start: k, the first slab of dW and dX, the Tm^T
   // fragments (rows i = 4 s4 + lk, s4 = 4 wi ..; past the last row block
   // the last rows are requested again and not used)
@@ -1191,9 +1198,9 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int j = 16 * wi + 4 * lk + r;
-      const int32_t e = ent[j];
+      const int32_t e = sEnt[j];
       if (e >= 0) {
-        const int32_t slt = go.slot[static_cast<int64_t>(c) * KB + j];
+        const int32_t slt = sSlot[j];
         if (slt < 0) st<T>(static_cast<T*>(go.dv) + (static_cast<int64_t>(e >> 1) * H + h) * D + col, aV[r]);
         else go.sdv[(static_cast<int64_t>(slt) * H + h) * D + col] = aV[r];
       }
@@ -1236,9 +1243,16 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
   float* sMid = sdb + KB;          // [3][D] middle factors
   float* sTot = sMid + 3 * D;      // [2][KT] scan totals
   uint32_t* sWide = reinterpret_cast<uint32_t*>(sTot + 2 * KT);   // [4 D / 32] wide flags
+  int32_t* sEnt = reinterpret_cast<int32_t*>(sWide + 4 * D / 32);  // [64] row table entries
+  int32_t* sSlot = sEnt + KB;                                        // [64] gradient slots
   const int c = static_cast<int>(blockIdx.x / H + c0), h = blockIdx.x % H;
   const int t = threadIdx.x;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
+  if (t < KB) {                    // where each row's gradients go, read once
+    const int32_t e = ent[t];
+    sEnt[t] = e;
+    sSlot[t] = e >= 0 ? go.slot[static_cast<int64_t>(c) * KB + t] : -1;
+  }
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
   // every input tile requested at once: k, q, g, L^{-1} and dTm for now, At
   // and dM (held in registers) for the later phases
@@ -1546,9 +1560,9 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
         sK[i * D + d0 + cc] = k_ * (r2 - c1) + q_ * r1 + (dqg[cc] * q_ + dkg[cc] * k_) * eG - dkb[cc] * k_ * eB;
         sQ[i * D + d0 + cc] = dkb[cc] * k_ * eB;
       }
-      const int32_t e = ent[i];
+      const int32_t e = sEnt[i];
       if (e >= 0) {
-        const int32_t sl = go.slot[static_cast<int64_t>(c) * KB + i];
+        const int32_t sl = sSlot[i];
         if (sl < 0) {
           const int64_t o = (static_cast<int64_t>(e >> 1) * H + h) * D + d0;
           st4<T>(static_cast<T*>(go.dq) + o, dq);
@@ -1584,17 +1598,17 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict_
 #pragma unroll
     for (int r = 0; r < RP; ++r) {
       const int i = part * RP + r;
-      const int32_t e = ent[i];
+      const int32_t e = sEnt[i];
       if (e < 0) continue;
-      const int32_t sl = go.slot[static_cast<int64_t>(c) * KB + i];
+      const int32_t sl = sSlot[i];
       float* dst = sl < 0 ? go.dg + (static_cast<int64_t>(e >> 1) * H + h) * D
                           : go.sdg + (static_cast<int64_t>(sl) * H + h) * D;
       dst[d] = suf[r] + off;
     }
   }
-  if (t < KB && ent[t] >= 0) {
-    const int32_t sl = go.slot[static_cast<int64_t>(c) * KB + t];
-    if (sl < 0) go.dbeta[static_cast<int64_t>(ent[t] >> 1) * H + h] = sdb[t];
+  if (t < KB && sEnt[t] >= 0) {
+    const int32_t sl = sSlot[t];
+    if (sl < 0) go.dbeta[static_cast<int64_t>(sEnt[t] >> 1) * H + h] = sdb[t];
     else go.sdb[static_cast<int64_t>(sl) * H + h] = sdb[t];
   }
 }
@@ -1665,7 +1679,7 @@ constexpr size_t lds_bprod() { return ProdLds<D>::ALL * sizeof(float); }
 template <int D>
 constexpr size_t lds_btm() { return BtmLds<D>::ALL * sizeof(float); }
 template <int D>
-constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D + 2 * KT + 4 * D / 32) * sizeof(float); }
+constexpr size_t lds_blocal() { return (3 * KB * D + 3 * KB * (KB + 4) + 2 * KB + 3 * D + 2 * KT + 4 * D / 32 + 2 * KB) * sizeof(float); }
 
 struct KdaArgs {
   const int32_t* chunk_rows;
