@@ -841,6 +841,10 @@ __global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chun
   const int t = threadIdx.x, lane = t & 63, wv = t >> 6, li = lane & 15, lk = lane >> 4, v0 = half * VH;
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   const float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
+  const int ti = wv >> 1, tv0 = 2 * (wv & 1);
+  int32_t pe[4];                  // the lane's four output rows
+#pragma unroll
+  for (int r = 0; r < 4; ++r) pe[r] = ent[16 * ti + 4 * lk + r];
   for (int idx = t; idx < D * VH / 4; idx += KT) {
     const int e = 4 * idx, r = e / VH, cc = e % VH;
     *reinterpret_cast<f32x4*>(sS + r * LB + cc) = *reinterpret_cast<const f32x4*>(w + Y::SC + r * D + v0 + cc);
@@ -850,7 +854,6 @@ __global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chun
     *reinterpret_cast<f32x4*>(sX + r * LB + cc) = *reinterpret_cast<const f32x4*>(w + Y::X + r * D + v0 + cc);
   }
   __syncthreads();
-  const int ti = wv >> 1, tv0 = 2 * (wv & 1);
   f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
   const float* qg = w + Y::QG + (16 * ti + li) * D + 4 * lk;
 #pragma unroll 4
@@ -875,7 +878,7 @@ __global__ __launch_bounds__(KT) void k_kda_out(const int32_t* __restrict__ chun
   }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const int32_t e = ent[16 * ti + 4 * lk + r];
+    const int32_t e = pe[r];
     if (e < 0 || !(e & 1)) continue;
     T* dst = o + (static_cast<int64_t>(e >> 1) * H + h) * D + v0 + li;
 #pragma unroll
@@ -990,6 +993,7 @@ __global__ __launch_bounds__(KT, 4) void k_kda_bwd_prod(const int32_t* __restric
   const int32_t* ent = chunk_rows + static_cast<int64_t>(c) * KB;
   float* w = ws + (static_cast<int64_t>(c) * H + h) * Y::ALL;
   const int ti = wv >> 1, td0 = (wv & 1) * TDW;
+  const int32_t my_ent = ent[t % KB];     // the row this thread stages from dO and V
   f32x4 aQ[TDW], aW[TDW], aK[TDW], aM[2], aU[2];
 #pragma unroll
   for (int x = 0; x < TDW; ++x) aQ[x] = aW[x] = aK[x] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1017,11 +1021,12 @@ __global__ __launch_bounds__(KT, 4) void k_kda_bwd_prod(const int32_t* __restric
 #pragma unroll
       for (int e = 0; e < 4; ++e) sXb[(vq + e) * L::LJ + i] = x[e];
     }
-    {   // dO (own rows) and V, 16-byte loads
+    {   // dO (own rows) and V, 16-byte loads (row i = t % 64 of every slab)
       constexpr int N = RowVec<T>::N, VR = PVS / N;
-      for (int idx = t; idx < KB * VR; idx += KT) {
-        const int i = idx % KB, vv = (idx / KB) * N;
-        const int32_t e = ent[i];
+      static_assert(KB * VR <= KT, "one piece per thread");
+      if (t < KB * VR) {
+        const int i = t % KB, vv = (t / KB) * N;
+        const int32_t e = my_ent;
         float xo[N], xv[N];
 #pragma unroll
         for (int n = 0; n < N; ++n) xo[n] = xv[n] = 0.f;
