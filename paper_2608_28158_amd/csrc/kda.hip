@@ -13,16 +13,20 @@
 //   M[i][j] = sum_d q_i k_j e^{G_i - G_j} (j <= i),
 //   S_next = Diag(e^{G_B}) S + (K * e^{G_B - G})^T X.
 // Chunk-local quantities are formed in parallel (k_kda_prep); the state
-// recurrence runs per (sequence, head, 64 state columns) over the chunks of
-// the sequence (k_kda_seq); outputs again in parallel (k_kda_out).  The
-// backward mirrors it: dX and the state adjoints in reverse chunk order
-// (k_kda_seq, reverse), then every chunk-local gradient in parallel
-// (k_kda_bwd_prod, k_kda_bwd_tm, k_kda_bwd_local) into per-packed-row buffers, reduced
-// into compact rows in a fixed order (k_kda_reduce).  Pairwise decays
-// e^{G_i - G_j} (i >= j) are never products of e^{G_i} and e^{-G_j}: inside a
-// 16-row block they are evaluated exactly per channel, across blocks as a
-// product of three exponentials of non-positive exponents (through the
-// blocks' first rows), so no intermediate overflows.
+// recurrence runs per (sequence, head, slab of 32 or 64 state columns) over
+// the chunks of the sequence (k_kda_seq); outputs again in parallel
+// (k_kda_out).  The backward mirrors it: dX and the state adjoints in
+// reverse chunk order (k_kda_seq, reverse), then every chunk-local gradient
+// in parallel (k_kda_bwd_prep, k_kda_bwd_prod, k_kda_bwd_tm,
+// k_kda_bwd_local).  A compact row with one packed row gets its gradients
+// written directly; the rows replayed into other sequences write float32
+// partials into slots, summed in slot order afterwards (k_kda_reduce).
+// Pairwise decays e^{G_i - G_j} (i >= j) are never products of e^{G_i} and
+// e^{-G_j}: across 16-row blocks they are a product of three exponentials
+// of non-positive exponents (through the blocks' first rows); inside a
+// block, of e^{G_i - G_{r_I}} and e^{G_{r_I} - G_j} where the block's decay
+// range keeps both in the normal float range, else exact per channel.  No
+// intermediate overflows.
 //
 // Packed row entries: physical row * 2 + 1 (own row), * 2 (replay row), -1
 // (padding: g = 0, beta = 0, k = q = v = 0, no outputs, no gradients).
