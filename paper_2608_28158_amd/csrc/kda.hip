@@ -1231,8 +1231,9 @@ __global__ __launch_bounds__(KT) void k_kda_bwd_tm(const int32_t* __restrict__ c
 // Chunk-local gradients of one (chunk, head) past the products: through
 // Tm = L^{-1} Diag(beta) and L = I + Diag(beta) At (dL = -L^{-T} dL^{-1}
 // L^{-T}), the pairwise decays of At and M, the decayed K and Q, and the
-// cumulative sum of g.  Writes dq, dk, dg [packed row][H][D] and dbeta
-// [packed row][H] for every real packed row.
+// cumulative sum of g.  Writes dq, dk, dg ([row][H][D]) and dbeta ([row][H])
+// of every real packed row: into the compact row's gradients when it is the
+// compact row's only packed row, else into its slot.
 template <typename T, int D>
 __global__ __launch_bounds__(KT) void k_kda_bwd_local(const int32_t* __restrict__ chunk_rows, int64_t c0, int H,
                                                       const T* __restrict__ q, const T* __restrict__ k,
