@@ -1,7 +1,8 @@
 """GPU parity of KDA over packed rollout trees (Sec. 2.2, eq. chunk-state;
 handoffs of Sec. 3.4) against the fp64 trajectory-wise oracle, through the
-C ABI: o, S_final, dq, dk, dv, dg, dbeta and dS0_tree on small forests and
-plans of three and four rounds (every element); on the 64k-token agentic
+C ABI: o, S_final, dq, dk, dv, dg, dbeta and dS0_tree on small forests,
+the edge-case forests of the linear-attention tests, seeded random forests
+and plans of three and four rounds, and strong decays (every element); on the 64k-token agentic
 microbatch at 16 heads of 128 (the benchmark's launch configuration), two
 heads: o and dq of sampled rows from their trajectory prefixes, S_final of
 sampled leaves, and dk, dv, dg, dbeta of rows near the end of leaf segments
@@ -74,6 +75,27 @@ STAR = ("star of 18 leaves", [-1] + [0] * 18, [70] + [3 + (9 * i + 5) % 61 for i
 def test_kda_wide_state_slabs(dtype, d):
     run = check_forest(*STAR, dtype, d, 32)
     assert max(s1 - s0 for s0, s1, *_ in run.rounds) * 32 * (d // 64) >= 512
+
+
+# The edge-case forests of the linear-attention parity tests (forks on,
+# before and after chunk boundaries, replay across several ancestors, chains
+# of one-row segments, a star, two trees, exact chunk multiples).
+from tests.test_gpu_parity import EDGE_FORESTS  # noqa: E402
+from tests.test_gpu_rounds import random_k3_forests  # noqa: E402
+
+
+@pytest.mark.parametrize("label,parent,seg_len", EDGE_FORESTS, ids=[e[0] for e in EDGE_FORESTS])
+def test_kda_edge_forests(label, parent, seg_len):
+    check_forest(label, parent, seg_len, "f32", 64, 2)
+
+
+# Seeded random forests whose plans have three or more rounds: sequences
+# that start from a requested state and request states themselves.
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_kda_random_k3_forests(dtype, d):
+    for i, (parent, seg_len) in enumerate(random_k3_forests(31 + d, 3, 150)):
+        run = check_forest(f"random K>=3 #{i}", parent, seg_len, dtype, d, 2)
+        assert len(run.rounds) >= 3
 
 
 # Channels whose log-decay falls by more than 60 over a 16-row block take the
