@@ -505,7 +505,10 @@ int harts_attn_scatter(const float* src, const int64_t* row_off, const int32_t* 
  *              then own rows, then padding), in sequence order: physical
  *              row * 2 + 1 for an own row, * 2 for a replay row, -1 padding.
  *   seq_tab    [n_seq][8]: round (0-based), first chunk, chunks, initial
- *              bank entry, first request, requests, final leaf, 0.
+ *              bank entry, first request, requests, final leaf, and in the
+ *              last column the order in which the state passes take the
+ *              round's sequences: row s0 + j holds the sequence taken j-th,
+ *              longest first (ties by id).
  *   req_tab    [n_req][2]: (chunk c of the sequence, bank entry): the state
  *              at the start of chunk c (c = chunks: the end state), each
  *              sequence's requests in ascending chunk order.

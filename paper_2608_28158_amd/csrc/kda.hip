@@ -649,7 +649,7 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
   const int b = blockIdx.x;
   const int chain = (b / (8 * NV)) * 8 + b % 8, slab = (b / 8) % NV;
   if (chain >= n_chain) return;
-  const int h = chain % H, seq = s0 + chain / H;
+  const int h = chain % H, seq = seq_tab[8 * (s0 + chain / H) + 7];   // longest sequences first
   const int t = threadIdx.x, v0 = slab * SV, lane = t & 63, wv = t >> 6;
   const int li = lane & 15, lk = lane >> 4;     // fragment coordinates
   const int32_t* st_ = seq_tab + 8 * seq;

@@ -115,7 +115,6 @@ extern "C" int harts_kda_tables(const harts_plan_t* p, int32_t* chunk_rows, int3
         s[4] = p->seq_req_off[i];
         s[5] = p->seq_req_off[i + 1] - p->seq_req_off[i];
         s[6] = p->seq_final_leaf[i];
-        s[7] = 0;
         int32_t* rows = chunk_rows + c0 * kKdaChunk;
         int64_t k = 0;
         // packed row entry: physical row * 2 + 1 for an own row, * 2 for a replay row; -1 padding
@@ -125,6 +124,14 @@ extern "C" int harts_kda_tables(const harts_plan_t* p, int32_t* chunk_rows, int3
         for (; k < nc * kKdaChunk; ++k) rows[k] = -1;
         c0 += nc;
       }
+      // the order in which the state pass takes the round's sequences:
+      // longest first (ties by id), so that the long chains start in the
+      // first wave of workgroups and the short ones fill in behind them
+      std::vector<int32_t> order;
+      for (int32_t i = p->round_seq_off[r]; i < p->round_seq_off[r + 1]; ++i) order.push_back(i);
+      std::stable_sort(order.begin(), order.end(),
+                       [&](int32_t a, int32_t b) { return seq_tab[8 * a + 2] > seq_tab[8 * b + 2]; });
+      for (size_t j = 0; j < order.size(); ++j) seq_tab[8 * (p->round_seq_off[r] + j) + 7] = order[j];
     }
     for (size_t j = 0; j < p->req_chunk.size(); ++j) {
       req_tab[2 * j] = p->req_chunk[j];

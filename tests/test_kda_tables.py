@@ -62,6 +62,13 @@ def test_tables_follow_the_plan(label, parent, seg_len):
             assert 0 <= t["req"][j, 0] <= nc
         c += nc
     assert c == sz.n_chunks
+    # the state passes' order (last column): each round's sequences once,
+    # by descending chunk count, ties by id
+    for rnd in range(sz.n_rounds):
+        ids = np.nonzero(t["seq"][:, 0] == rnd)[0]
+        order = t["seq"][ids, 7]
+        assert sorted(order) == list(ids)
+        assert order.tolist() == sorted(ids, key=lambda i: (-t["seq"][i, 2], i))
     # groups: every round's sequences once, by initial bank entry, in order
     seen = []
     for rnd, bank, first, n in t["grp"]:
