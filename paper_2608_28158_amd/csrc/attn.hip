@@ -621,22 +621,34 @@ __global__ __launch_bounds__(AT_THR, NH == 2 ? 1 : 2) void k_attn_dkdv(
   }
 }
 
-// view rows <- compact rows (bf16, 16-byte pieces)
+// view rows <- compact rows (bf16, 16-byte pieces): a thread moves the same
+// piece of AT_GR consecutive view rows, their loads in flight together
+constexpr int AT_GR = 4;
 __global__ __launch_bounds__(AT_THR) void k_attn_gather(const bf16* __restrict__ src,
                                                         const int32_t* __restrict__ rows, int64_t n_kv,
                                                         int64_t C, int row_elems, bf16* __restrict__ dst) {
   const int vpr = row_elems / 8;
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * AT_THR + threadIdx.x;
-  const int64_t e = idx / vpr;
-  if (e >= n_kv) return;
+  const int64_t e0 = (idx / vpr) * AT_GR;
+  if (e0 >= n_kv) return;
   const int c = static_cast<int>(idx % vpr) * 8;
-  const int32_t r = rows[e];
-  uint4 v = {0u, 0u, 0u, 0u};
-  if (r >= 0 && r < C) v = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r) * row_elems + c);
-  *reinterpret_cast<uint4*>(dst + e * row_elems + c) = v;
+  int32_t r[AT_GR];
+#pragma unroll
+  for (int q = 0; q < AT_GR; ++q) r[q] = e0 + q < n_kv ? rows[e0 + q] : -1;
+  uint4 v[AT_GR];
+#pragma unroll
+  for (int q = 0; q < AT_GR; ++q) {
+    v[q] = uint4{0u, 0u, 0u, 0u};
+    if (r[q] >= 0 && r[q] < C) v[q] = *reinterpret_cast<const uint4*>(src + static_cast<int64_t>(r[q]) * row_elems + c);
+  }
+#pragma unroll
+  for (int q = 0; q < AT_GR; ++q)
+    if (e0 + q < n_kv) *reinterpret_cast<uint4*>(dst + (e0 + q) * row_elems + c) = v[q];
 }
 
-// compact rows <- sum of their view rows, in the row's (fixed) entry order
+// compact rows <- sum of their view rows, in the row's (fixed) entry order;
+// the entries are taken AT_GR at a time, their indices and then their rows
+// requested together (an entry past the row's last, or invalid, adds zero)
 __global__ __launch_bounds__(AT_THR) void k_attn_scatter(const float* __restrict__ src,
                                                          const int64_t* __restrict__ row_off,
                                                          const int32_t* __restrict__ ent, int64_t C,
@@ -649,10 +661,22 @@ __global__ __launch_bounds__(AT_THR) void k_attn_scatter(const float* __restrict
   const int64_t b = row_off[r] < 0 ? 0 : row_off[r];
   const int64_t e_end = row_off[r + 1] > n_kv ? n_kv : row_off[r + 1];
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int64_t j = b; j < e_end; ++j) {
-    const int32_t e = ent[j];
-    if (e < 0 || e >= n_kv) continue;
-    acc += *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(e) * row_elems + c);
+  for (int64_t j = b; j < e_end; j += AT_GR) {
+    int32_t e[AT_GR];
+#pragma unroll
+    for (int q = 0; q < AT_GR; ++q) {
+      e[q] = j + q < e_end ? ent[j + q] : -1;
+      if (e[q] >= n_kv) e[q] = -1;
+    }
+    f32x4 v[AT_GR];
+#pragma unroll
+    for (int q = 0; q < AT_GR; ++q) {
+      v[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (e[q] >= 0) v[q] = *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(e[q]) * row_elems + c);
+    }
+#pragma unroll
+    for (int q = 0; q < AT_GR; ++q)
+      if (e[q] >= 0) acc += v[q];
   }
   Vec4<bf16>::store(dst + r * row_elems + c, acc);
 }
@@ -767,7 +791,7 @@ extern "C" int harts_attn_gather(const void* src, const int32_t* kv_rows, int64_
     return HARTS_EINVAL;
   }
   const int row_elems = H * d;
-  const int64_t threads = n_kv * (row_elems / 8);
+  const int64_t threads = (n_kv + AT_GR - 1) / AT_GR * (row_elems / 8);
   hipLaunchKernelGGL(k_attn_gather, dim3(static_cast<uint32_t>((threads + AT_THR - 1) / AT_THR)), dim3(AT_THR),
                      0, static_cast<hipStream_t>(stream), static_cast<const bf16*>(src), kv_rows, n_kv, C,
                      row_elems, static_cast<bf16*>(dst));
