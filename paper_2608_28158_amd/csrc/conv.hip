@@ -39,13 +39,15 @@ constexpr int CV_SUCC = 2048;  // consumer entries of a backward run staged in L
 template <typename T> struct CV;
 template <> struct CV<bf16> {
   static constexpr int N = 4;  // 8-byte pieces: half the registers of 16-byte ones
-  __device__ static inline void load(const bf16* p, float* x) {
-    const uint2 u = *reinterpret_cast<const uint2*>(p);
+  using Raw = uint2;           // a piece as loaded, widened where it is used
+  __device__ static inline Raw raw(const bf16* p) { return *reinterpret_cast<const uint2*>(p); }
+  __device__ static inline void cvt(const Raw u, float* x) {
     x[0] = __uint_as_float(u.x << 16);
     x[1] = __uint_as_float(u.x & 0xffff0000u);
     x[2] = __uint_as_float(u.y << 16);
     x[3] = __uint_as_float(u.y & 0xffff0000u);
   }
+  __device__ static inline void load(const bf16* p, float* x) { cvt(raw(p), x); }
   __device__ static inline void store(bf16* p, const float* x) {
     typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
     bf16x4 b;
@@ -56,10 +58,12 @@ template <> struct CV<bf16> {
 };
 template <> struct CV<float> {
   static constexpr int N = 4;
-  __device__ static inline void load(const float* p, float* x) {
-    const float4 u = *reinterpret_cast<const float4*>(p);
+  using Raw = float4;
+  __device__ static inline Raw raw(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  __device__ static inline void cvt(const Raw u, float* x) {
     x[0] = u.x; x[1] = u.y; x[2] = u.z; x[3] = u.w;
   }
+  __device__ static inline void load(const float* p, float* x) { cvt(raw(p), x); }
   __device__ static inline void store(float* p, const float* x) {
     *reinterpret_cast<float4*>(p) = float4{x[0], x[1], x[2], x[3]};
   }
@@ -190,25 +194,28 @@ __global__ __launch_bounds__(CV_THR) void k_conv_bwd(int64_t C, int Cch, const T
   for (int j = threadIdx.x; j < n_run_succ && j < CV_SUCC; j += CV_THR) s_succ[j] = succ[b0 + j];
   __syncthreads();
   if (vec >= Cch / V::N) return;
-  float wt[W][V::N], hist[W - 1][V::N], gw[W][V::N], dwin[W][V::N];
+  float wt[W][V::N], hist[W - 1][V::N], gw[W][V::N];
   load_taps<T, W>(Wt, c0, wt);
 #pragma unroll
   for (int i = 0; i < W; ++i)
 #pragma unroll
     for (int e = 0; e < V::N; ++e) gw[i][e] = 0.f;
-  // dwin[i] = dy[r + i] (zero past the last row)
+  // dr[i] = dy[r + i] as loaded, one row beyond the window, so that the
+  // window's rows are widened at the top of a row while only the row beyond
+  // it and the next row's x are in flight.  Every load is unconditional:
+  // past the last row the last row is requested again, an entry never used
+  // (the consumers of a row are rows of the table).
+  using Raw = typename V::Raw;
+  Raw dr[W + 1];
 #pragma unroll
-  for (int i = 0; i < W; ++i) {
-    if (r0 + i < C) {
-      V::load(dy + (r0 + i) * Cch + c0, dwin[i]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < V::N; ++e) dwin[i][e] = 0.f;
-    }
-  }
+  for (int i = 0; i <= W; ++i) dr[i] = V::raw(dy + (r0 + i < C ? r0 + i : C - 1) * Cch + c0);
+  Raw xr = V::raw(x + r0 * Cch + c0);   // x of the row, requested a row ahead
   for (int64_t r = r0; r < r1; ++r) {
-    float cur[V::N], v[V::N], acc[V::N];
-    V::load(x + r * Cch + c0, cur);
+    float cur[V::N], dwin[W][V::N], v[V::N], acc[V::N];
+    V::cvt(xr, cur);
+#pragma unroll
+    for (int k = 0; k < W; ++k) V::cvt(dr[k], dwin[k]);
+    xr = V::raw(x + (r + 1 < C ? r + 1 : C - 1) * Cch + c0);
 #pragma unroll
     for (int e = 0; e < V::N; ++e) {
       acc[e] = wt[0][e] * dwin[0][e];
@@ -220,11 +227,12 @@ __global__ __launch_bounds__(CV_THR) void k_conv_bwd(int64_t C, int Cch, const T
 #pragma unroll
       for (int e = 0; e < V::N; ++e) gw[i][e] += v[e] * dwin[0][e];
     }
-    const int32_t jb = s_off[r - r0], je = s_off[r - r0 + 1];
-    for (int32_t j = jb; j < je; ++j) {
-      const int32_t code = j < CV_SUCC ? s_succ[j] : succ[b0 + j];
+    // consumers in table order: the staged entries from LDS, any beyond
+    // them from global memory (two loops, so that neither read goes through
+    // a flat address that would wait for every outstanding load)
+    const auto consume = [&](int32_t code) __attribute__((always_inline)) {
       const int32_t sr = code >> 3, i = code & 7;  // consumer row, tap
-      if (sr < 0 || sr >= C || i < 1 || i >= W) continue;
+      if (sr < 0 || sr >= C || i < 1 || i >= W) return;
       if (sr == r + i) {  // the row i below: already in registers
 #pragma unroll
         for (int k = 1; k < W; ++k)
@@ -241,19 +249,16 @@ __global__ __launch_bounds__(CV_THR) void k_conv_bwd(int64_t C, int Cch, const T
             for (int e = 0; e < V::N; ++e) acc[e] += wt[k][e] * v[e];
           }
       }
-    }
+    };
+    const int32_t jb = s_off[r - r0], je = s_off[r - r0 + 1];
+    const int32_t jl = je < CV_SUCC ? je : CV_SUCC;
+    for (int32_t j = jb; j < jl; ++j) consume(s_succ[j]);
+    for (int32_t j = jb > CV_SUCC ? jb : CV_SUCC; j < je; ++j) consume(succ[b0 + j]);
     V::store(dx + r * Cch + c0, acc);
     shift_hist<T, W>(hist, cur);
 #pragma unroll
-    for (int k = 0; k + 1 < W; ++k)
-#pragma unroll
-      for (int e = 0; e < V::N; ++e) dwin[k][e] = dwin[k + 1][e];
-    if (r + W < C) {
-      V::load(dy + (r + W) * Cch + c0, dwin[W - 1]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < V::N; ++e) dwin[W - 1][e] = 0.f;
-    }
+    for (int k = 0; k < W; ++k) dr[k] = dr[k + 1];
+    dr[W] = V::raw(dy + (r + W + 1 < C ? r + W + 1 : C - 1) * Cch + c0);
   }
   // partials tap-major ([run][tap][channel]): every store is a coalesced
   // 16- or 32-byte piece of one tap's channel row
