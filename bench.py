@@ -874,7 +874,7 @@ def kda_measurement(steps, warmup, profile_only=False):
     Cn = f.n_rows
     t0 = time.perf_counter()
     run = KdaRunner(plan, H, d, torch.bfloat16)
-    tables_ms = (time.perf_counter() - t0) * 1e3
+    setup_ms = (time.perf_counter() - t0) * 1e3   # tables, their device copies and the workspace
     gen = torch.Generator(device="cuda")
     gen.manual_seed(13)
     rnd = lambda *sh: torch.randn(sh, device="cuda", generator=gen)
@@ -920,7 +920,8 @@ def kda_measurement(steps, warmup, profile_only=False):
     out = {"workload": f"64k-token agentic microbatch: {Cn} compact rows, {plan['R']} replay rows, "
                        f"{nch} packed 64-row chunks, K={plan['n_rounds']}, {H} heads of {d}, bf16 q/k/v, "
                        f"float32 g/beta/states",
-           "ms_per_step": ms, "compact_tok_s": Cn / (ms * 1e-3), "fwd_ms": ms_f, "tables_host_ms": tables_ms,
+           "ms_per_step": ms, "compact_tok_s": Cn / (ms * 1e-3), "fwd_ms": ms_f, "tables_host_ms": run.tables_ms,
+           "runner_setup_ms": setup_ms,
            "alg_TFLOP_step": fl / 1e12, "TFLOPs": tf(fl, ms), "fwd_TFLOPs": tf(fl_f, ms_f),
            "fp32_peak_frac": tf(fl, ms) / PEAK_F32_TFLOPS}
     # the oracle: the trajectory-wise fp64 recurrence, forward and backward by

@@ -15,6 +15,7 @@ g: [C, H, d] float32 log-decays; beta: [C, H] float32; S0_tree:
 from __future__ import annotations
 
 import ctypes as C
+import time
 
 import numpy as np
 import torch
@@ -42,10 +43,12 @@ class KdaRunner:
         self.pos_slot = np.zeros(max(sz.n_chunks, 1) * 64, np.int32)
         self.multi_row = np.zeros(max(sz.n_multi, 1), np.int32)
         self.multi_off = np.zeros(sz.n_multi + 1, np.int64)
+        t0 = time.perf_counter()
         _lib.check(L.harts_kda_tables(plan.handle, self.chunk_rows.ctypes.data, self.seq_tab.ctypes.data,
                                       self.req_tab.ctypes.data, self.group_tab.ctypes.data,
                                       self.group_seq.ctypes.data, self.pos_slot.ctypes.data,
                                       self.multi_row.ctypes.data, self.multi_off.ctypes.data), "harts_kda_tables")
+        self.tables_ms = (time.perf_counter() - t0) * 1e3   # host tables alone
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
         self.d_rows, self.d_seq, self.d_req = dev(self.chunk_rows), dev(self.seq_tab), dev(self.req_tab)
         self.d_group, self.d_gseq = dev(self.group_tab), dev(self.group_seq)
