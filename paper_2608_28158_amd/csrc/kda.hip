@@ -47,9 +47,6 @@ typedef __bf16 bf16;
 constexpr int KT = 512;   // threads per workgroup (8 waves: two per SIMD)
 constexpr int KB = 64;    // chunk rows
 
-template <typename T> __device__ inline float ld(const T* p);
-template <> __device__ inline float ld<float>(const float* p) { return *p; }
-template <> __device__ inline float ld<bf16>(const bf16* p) { return static_cast<float>(*p); }
 template <typename T> __device__ inline void st(T* p, float x);
 template <> __device__ inline void st<float>(float* p, float x) { *p = x; }
 template <> __device__ inline void st<bf16>(bf16* p, float x) { *p = static_cast<bf16>(x); }
@@ -610,8 +607,6 @@ __global__ __launch_bounds__(KT) void k_kda_prep(const int32_t* __restrict__ chu
 // (plus the bank adjoints of requests at the end), the bank adjoints of
 // requested chunk starts are added as the pass reaches them, and the
 // initial state's adjoint goes to dS0_seq.
-constexpr int SQV = 64;                  // state columns per workgroup of the output kernels
-constexpr int SQL = SQV + 4;             // LDS row stride of Sc and Xc there (16-byte rows)
 
 // LDS row strides of the state pass: an operand read with its row index
 // along the lane's m (n) coordinate wants a stride of 4 (mod 64 banks), one
@@ -621,6 +616,13 @@ template <int D, int SV>
 struct SeqLds {
   static constexpr int LA1 = D + 4, LA2 = D + 16, LS = SV + 4, LX = SV + 16;
   static constexpr int A1 = 0, A2 = A1 + KB * LA1, S = A2 + KB * LA2, X = S + D * LS, G = X + KB * LX, ALL = G + D;
+};
+
+// Unroll counts of the state pass's two product loops: whole loops with
+// 32-column slabs, partial ones where the registers would not hold them.
+template <int D, int SV>
+struct SeqUnroll {
+  static constexpr int X = SV == 32 ? D / 16 : 2, S = SV == 32 ? KB / 4 : 4;
 };
 
 template <int D, bool REV, int SV>
@@ -753,7 +755,7 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
       f32x4 acc2[XT];
 #pragma unroll
       for (int x = 0; x < XT; ++x) acc2[x] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll (SV == 32 ? D / 16 : 2)
+#pragma unroll SeqUnroll<D, SV>::X
       for (int g = 0; g < D / 16; ++g) {
         const f32x4 a4 = *reinterpret_cast<const f32x4*>(sA1 + (16 * xti + li) * L::LA1 + 16 * g + 4 * lk);
 #pragma unroll
@@ -783,7 +785,7 @@ __global__ __launch_bounds__(KT) void k_kda_seq(const int32_t* __restrict__ seq_
     for (int x = 0; x < ST; ++x)
 #pragma unroll
       for (int r = 0; r < 4; ++r) sacc[x][r] += sg[16 * sti + 4 * lk + r] * Sa[x][r];
-#pragma unroll (SV == 32 ? KB / 4 : 4)
+#pragma unroll SeqUnroll<D, SV>::S
     for (int s = 0; s < KB / 4; ++s) {
       const float a = S2 * sA2[(4 * s + lk) * L::LA2 + 16 * sti + li];
 #pragma unroll

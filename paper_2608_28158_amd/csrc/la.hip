@@ -744,7 +744,6 @@ __global__ __launch_bounds__((Cfg<T, D>::NTHR), (Cfg<T, D>::WPE)) void k_fwd_blo
     const T* __restrict__ k, const T* __restrict__ v, const float* __restrict__ g,
     const InitSrc is, const float* __restrict__ S_end, T* __restrict__ o, float* __restrict__ S_final) {
   using C = Cfg<T, D>;
-  using RB = RegB<T>;
   constexpr int NS = C::CPW * C::NT;
   __shared__ FwdSmem<T, D> sm;
   const BlkInfo bl = blk_info(blk_launch, blockIdx.x / H);
