@@ -48,7 +48,7 @@ constexpr int AT_THR = 256;          // 4 waves
 constexpr int AT_T = 64;             // rows of an LDS tile (keys per step, queries per step in dk/dv)
 constexpr int AT_WT = 128;           // rows of a table tile (queries in fwd/dq, keys in dk/dv)
 // 16-row halves a wave owns, per kernel (measured choices)
-constexpr int AT_FWD_NH = 2, AT_DQ_NH = 1, AT_DKDV_NH = 1;
+constexpr int AT_FWD_NH = 2, AT_DQ_NH = 2, AT_DKDV_NH = 1;
 constexpr float AT_LOG2E = 1.4426950408889634f;
 constexpr float AT_NEG = -1.0e30f;   // masked score (finite: no inf - inf)
 // The forward keeps a row's reference maximum until a score exceeds it by
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(AT_THR) void k_attn_delta(int64_t n, const bf16* __
 // them; per 64-key step S and dP from the K and V tiles (each fragment
 // feeding all halves), dS = P (dP - delta), dQ += dS K.
 template <int D, int NH>
-__global__ __launch_bounds__(AT_THR, NH == 2 ? 1 : 2) void k_attn_dq(
+__global__ __launch_bounds__(AT_THR, 2) void k_attn_dq(
     const int32_t* __restrict__ views, const int32_t* __restrict__ qtiles, int H, float scale,
     const bf16* __restrict__ q, const bf16* __restrict__ kv_k, const bf16* __restrict__ kv_v,
     const bf16* __restrict__ dO, const float* __restrict__ lse, const float* __restrict__ delta,
@@ -388,35 +388,34 @@ __global__ __launch_bounds__(AT_THR, NH == 2 ? 1 : 2) void k_attn_dq(
       pv.load(kv_v, kvoff + k0 + AT_T, min(AT_T, kv_end - k0 - AT_T), H, h, t);
     }
     if (!wave_live || k0 >= wave_end) continue;
-    f32x4 sc[NH][4], dp[NH][4];
+    // per 16-key group j: S and dP over d, then dS = P (dP - delta) with
+    // P = exp(scale s - lse), so that dP lives for one group only
+    f32x4 sc[NH][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) {
+      f32x4 dp[NH];
 #pragma unroll
       for (int a = 0; a < NH; ++a) {
         sc[a][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        dp[a][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dp[a] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int s = 0; s < NS; ++s) {
         const typename F::V kf = F::kc<L>(sK, 16 * j, 32 * s, lane);
 #pragma unroll
         for (int a = 0; a < NH; ++a) F::mma(sc[a][j], kf, qf[a][s]);
         const typename F::V vf = F::kc<L>(sV, 16 * j, 32 * s, lane);
 #pragma unroll
-        for (int a = 0; a < NH; ++a) F::mma(dp[a][j], vf, df[a][s]);
+        for (int a = 0; a < NH; ++a) F::mma(dp[a], vf, df[a][s]);
       }
-    // dS = P (dP - delta), P = exp(scale s - lse)
 #pragma unroll
-    for (int a = 0; a < NH; ++a)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int a = 0; a < NH; ++a)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float p = at_exp2(fmaf(sc[a][j][r], c2, -l2[a]));
-          sc[a][j][r] = p * (dp[a][j][r] - dl[a]);
+          sc[a][j][r] = p * (dp[a][r] - dl[a]);
         }
+    }
     // steps that cross the diagonal, or hold rows past the view: zero what
     // the row cannot see
     if (k0 + AT_T > hh + wq0 + 1 || R::WR * (w + 1) > nq) {
@@ -536,66 +535,72 @@ __global__ __launch_bounds__(AT_THR, NH == 2 ? 1 : 2) void k_attn_dkdv(
     }
     // no query of the step sees the wave's first key: skip (wave-uniform)
     if (!wave_live || wk0 > hh + t0 + nq - 1) continue;
-    // lane (g, i) of half b gets S[q = t0 + 16 j + 4 g + r][key = wk0 + 16 b + i]
-    f32x4 sc[NH][4], dp[NH][4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int b = 0; b < NH; ++b) {
-        sc[b][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-        dp[b][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const typename F::V qa = F::kc<L>(sQ, 16 * j, 32 * s, lane);
-#pragma unroll
-        for (int b = 0; b < NH; ++b) F::mma(sc[b][j], qa, kf[b][s]);
-        const typename F::V da = F::kc<L>(sD, 16 * j, 32 * s, lane);
-#pragma unroll
-        for (int b = 0; b < NH; ++b) F::mma(dp[b][j], da, vf[b][s]);
-      }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 lq = *reinterpret_cast<const f32x4*>(sL + 16 * j + 4 * g);
-      const f32x4 dq4 = *reinterpret_cast<const f32x4*>(sDl + 16 * j + 4 * g);
-#pragma unroll
-      for (int b = 0; b < NH; ++b)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float p = at_exp2(fmaf(sc[b][j][r], c2, -lq[r]));
-          sc[b][j][r] = p;                             // P
-          dp[b][j][r] = p * (dp[b][j][r] - dq4[r]);    // dS
-        }
-    }
-    // steps where some query does not see some key of the wave (the
-    // diagonal, rows past the view, keys past the view row): zero those
-    if (!(wk0 + R::WR - 1 <= hh + t0 && nq == AT_T && R::WR * (w + 1) <= nk)) {
-#pragma unroll
-      for (int b = 0; b < NH; ++b) {
-        const int key = wk0 + 16 * b + i;
-        const int kl = key < hh + l ? key - hh - t0 : INT32_MAX;   // visible iff kl <= query row
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int qr = 16 * j + 4 * g + r;          // query row within the step
-            if (qr >= nq || kl > qr) {
-              sc[b][j][r] = 0.f;
-              dp[b][j][r] = 0.f;
-            }
-          }
-      }
-    }
-    // dV^T += dO^T P, dK^T += Q^T dS: lane (g, i) of half b gets [key][d = 16 jn + 4 g + r]
+    // the step's scores go by 32-query halves s2 (16-query groups j = 2 s2,
+    // 2 s2 + 1), each half's P and dS consumed by its dV, dK products before
+    // the next half is formed
+    const bool full = wk0 + R::WR - 1 <= hh + t0 && nq == AT_T && R::WR * (w + 1) <= nk;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
+      // lane (g, i) of half b gets S[q = t0 + 16 j + 4 g + r][key = wk0 + 16 b + i]
+      f32x4 sc[NH][2], dp[NH][2];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int b = 0; b < NH; ++b) {
+          sc[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+          dp[b][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int j = 2 * s2 + jj;
+          const typename F::V qa = F::kc<L>(sQ, 16 * j, 32 * s, lane);
+#pragma unroll
+          for (int b = 0; b < NH; ++b) F::mma(sc[b][jj], qa, kf[b][s]);
+          const typename F::V da = F::kc<L>(sD, 16 * j, 32 * s, lane);
+#pragma unroll
+          for (int b = 0; b < NH; ++b) F::mma(dp[b][jj], da, vf[b][s]);
+        }
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * s2 + jj;
+        const f32x4 lq = *reinterpret_cast<const f32x4*>(sL + 16 * j + 4 * g);
+        const f32x4 dq4 = *reinterpret_cast<const f32x4*>(sDl + 16 * j + 4 * g);
+#pragma unroll
+        for (int b = 0; b < NH; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float p = at_exp2(fmaf(sc[b][jj][r], c2, -lq[r]));
+            sc[b][jj][r] = p;                             // P
+            dp[b][jj][r] = p * (dp[b][jj][r] - dq4[r]);   // dS
+          }
+      }
+      // steps where some query does not see some key of the wave (the
+      // diagonal, rows past the view, keys past the view row): zero those
+      if (!full) {
+#pragma unroll
+        for (int b = 0; b < NH; ++b) {
+          const int key = wk0 + 16 * b + i;
+          const int kl = key < hh + l ? key - hh - t0 : INT32_MAX;   // visible iff kl <= query row
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int qr = 16 * (2 * s2 + jj) + 4 * g + r;   // query row within the step
+              if (qr >= nq || kl > qr) {
+                sc[b][jj][r] = 0.f;
+                dp[b][jj][r] = 0.f;
+              }
+            }
+        }
+      }
+      // dV^T += dO^T P, dK^T += Q^T dS: lane (g, i) of half b gets [key][d = 16 jn + 4 g + r]
       bf16x8 pf[NH], sf[NH];
 #pragma unroll
       for (int b = 0; b < NH; ++b) {
-        pf[b] = RegB<bf16>::pack(sc[b] + 2 * s2);
-        sf[b] = RegB<bf16>::pack(dp[b] + 2 * s2);
+        pf[b] = RegB<bf16>::pack(sc[b]);
+        sf[b] = RegB<bf16>::pack(dp[b]);
       }
 #pragma unroll
       for (int jn = 0; jn < NJ; ++jn) {
