@@ -221,6 +221,10 @@ __global__ __launch_bounds__(AT_THR, 2) void k_attn_fwd(const int32_t* __restric
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int a = 0; a < NH; ++a) sc[a][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // the product blocks run at raised wave priority, so that the other
+    // wave of the SIMD issues its softmax work while this one feeds the
+    // matrix core
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
@@ -229,6 +233,7 @@ __global__ __launch_bounds__(AT_THR, 2) void k_attn_fwd(const int32_t* __restric
 #pragma unroll
         for (int a = 0; a < NH; ++a) F::mma(sc[a][j], kf, qf[a][s]);
       }
+    __builtin_amdgcn_s_setprio(0);
     // steps that cross the diagonal: keys past a query's last visible key
     if (k0 + AT_T > hh + wq0 + 1) {
 #pragma unroll
@@ -285,12 +290,14 @@ __global__ __launch_bounds__(AT_THR, 2) void k_attn_fwd(const int32_t* __restric
       bf16x8 pf[NH];
 #pragma unroll
       for (int a = 0; a < NH; ++a) pf[a] = RegB<bf16>::pack(sc[a] + 2 * s2);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int jn = 0; jn < NJ; ++jn) {
         const typename F::V vf = F::km<L>(sV, 32 * s2, 16 * jn, lane);
 #pragma unroll
         for (int a = 0; a < NH; ++a) F::mma(acc[a][jn], vf, pf[a]);
       }
+      __builtin_amdgcn_s_setprio(0);
     }
   }
 #pragma unroll
